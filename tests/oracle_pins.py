@@ -1,0 +1,393 @@
+"""Pins of the fp64 oracle against facts fixed outside the oracle itself.
+
+Each ``pin_*`` function raises AssertionError when the oracle disagrees with
+the paper or with mathematics: library special cases (torch float64 SDPA,
+rms_norm, silu; numpy/torch fp16/bf16 conversion), closed forms (rotary at
+p=0, norm preservation, relative-position property, complex-number form,
+single-key attention), brute force on tiny inputs (per-element INT4 decode
+with a hand-written fp16 decoder, golden layout fixture) and the paper's
+exactness claims (mask rewind equals a physical trim; the beam_idx Gather
+with identity equals no gather; a permuted beam_idx equals a physically
+permuted cache; micro-batched requests are isolated).
+
+``test_oracle_pins.py`` runs them; ``test_oracle_mutations.py`` plants
+plausible mistakes in the oracle and checks that some pin catches each one.
+"""
+from __future__ import annotations
+
+import json
+import math
+import os
+
+import numpy as np
+import torch
+import torch.nn.functional as F
+
+import oracle
+import synth
+from oracle_cases import f64, logical_positions, oracle_stage, oracle_state
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+TINY = synth.TINY
+TINY2 = synth.with_layers(synth.TINY, 2)
+
+
+# ------------------------------------------------------------------ rounding
+
+def pin_round_fp16_matches_numpy():
+    r = np.random.default_rng(1)
+    x = np.concatenate([
+        r.standard_normal(20000).astype(np.float32),
+        (r.standard_normal(5000) * 1e-6).astype(np.float32),       # fp16 subnormals
+        np.clip(r.standard_normal(5000) * 1e4, -65000, 65000).astype(np.float32),
+        np.float32([0.0, -0.0, 1 + 2 ** -11, 1 + 3 * 2 ** -11, 2 ** -25, 3 * 2 ** -25, 65504.0]),
+    ]).astype(np.float64)
+    ref = x.astype(np.float16).astype(np.float64)
+    got = oracle.to_fp16(x)
+    assert np.array_equal(got, ref), np.flatnonzero(got != ref)[:10]
+
+
+def pin_round_bf16_matches_torch():
+    r = np.random.default_rng(2)
+    x = np.concatenate([
+        r.standard_normal(20000).astype(np.float32),
+        (r.standard_normal(2000) * 1e-39).astype(np.float32),      # bf16 subnormals
+        np.float32([1 + 2 ** -8, 1 + 3 * 2 ** -8, -(1 + 2 ** -8), 0.0]),
+    ])
+    ref = torch.from_numpy(x).to(torch.bfloat16).double().numpy()
+    got = oracle.to_bf16(x.astype(np.float64))
+    assert np.array_equal(got, ref), np.flatnonzero(got != ref)[:10]
+
+
+# ------------------------------------------------------------------ INT4
+
+def _fp16_by_hand(bits: int) -> float:
+    s = -1.0 if bits >> 15 else 1.0
+    e = (bits >> 10) & 0x1F
+    m = bits & 0x3FF
+    if e == 0:
+        return s * m * 2.0 ** -24
+    assert e != 31
+    return s * (1.0 + m / 1024.0) * 2.0 ** (e - 15)
+
+
+def pin_int4_golden_layout():
+    with open(os.path.join(GOLDEN, "int4_layout.json")) as f:
+        g = json.load(f)
+    packed = np.array(g["packed"], dtype=np.uint8)
+    scales = np.array(g["scale_bits"], dtype=np.uint16)
+    codes = oracle.unpack_int4(packed, g["k"])
+    assert codes.tolist() == g["codes"], codes
+    w = oracle.dequant(packed, scales, g["k"], g["group"])
+    assert w.tolist() == g["weights"], w
+
+
+def pin_int4_bruteforce():
+    """Per-element pure-Python decode (I4) on a ragged-K matrix whose scales
+    include fp16 subnormals, zero and large values."""
+    r = np.random.default_rng(3)
+    n, k, grp = 5, 688, 128
+    m = synth.make_quant_matrix(n, k, grp, r)
+    bits = m.scales.view(np.uint16).copy()
+    bits[0, 0] = 0x0001          # smallest subnormal
+    bits[1, 5] = 0x03FF          # largest subnormal (ragged last group)
+    bits[2, 2] = 0x0000
+    bits[3, 3] = 0x7BFF          # 65504
+    bits[4, 1] = 0x8001          # negative subnormal
+    scales = bits.view(np.float16)
+    got = oracle.dequant(m.q, scales, k, grp)
+    assert got.shape == (n, k)
+    for row in range(n):
+        for col in range(k):
+            byte = int(m.q[row, col // 2])
+            nib = (byte >> 4) if (col % 2) else (byte & 0xF)
+            want = (nib - 8) * _fp16_by_hand(int(bits[row, col // grp]))
+            assert got[row, col] == want, (row, col, got[row, col], want)
+
+
+# ------------------------------------------------------------------ layer pieces vs torch float64
+
+def pin_rmsnorm_matches_torch():
+    r = np.random.default_rng(4)
+    x = r.standard_normal((3, 256)) * 3
+    gam = r.uniform(0.8, 1.2, 256)
+    ref = F.rms_norm(torch.from_numpy(x), (256,), weight=torch.from_numpy(gam), eps=1e-5).numpy()
+    got = oracle.rmsnorm(x, gam, 1e-5)
+    assert np.max(np.abs(got - ref)) <= 1e-12 * np.max(np.abs(ref))
+
+
+def pin_silu_matches_torch():
+    z = np.linspace(-30, 30, 1001)
+    ref = F.silu(torch.from_numpy(z)).numpy()
+    assert np.max(np.abs(oracle.silu(z) - ref)) <= 1e-14
+
+
+def _sdpa_reference(q, kc, vc, allowed):
+    """torch float64 SDPA with kv heads expanded by repeat_interleave.
+    q [n, Hq, D], kc/vc [Hkv, T, D], allowed bool [n, T]."""
+    hq, hkv = q.shape[1], kc.shape[0]
+    kq = torch.from_numpy(kc).repeat_interleave(hq // hkv, dim=0)      # [Hq, T, D]
+    vq = torch.from_numpy(vc).repeat_interleave(hq // hkv, dim=0)
+    qt = torch.from_numpy(q).transpose(0, 1)                            # [Hq, n, D]
+    m = torch.from_numpy(allowed)[None].expand(hq, -1, -1)
+    o = F.scaled_dot_product_attention(qt[None], kq[None], vq[None], attn_mask=m[None])
+    return o[0].transpose(0, 1).numpy()
+
+
+def pin_attention_matches_torch_sdpa():
+    r = np.random.default_rng(5)
+    hq, hkv, d, past = 4, 2, 64, 40
+    for n, holes in ((1, False), (5, False), (5, True)):
+        kc = r.standard_normal((hkv, past + n, d))
+        vc = r.standard_normal((hkv, past + n, d))
+        q = r.standard_normal((n, hq, d))
+        mask = np.ones(past + n, dtype=np.uint8)
+        if holes:
+            mask[r.choice(past, 12, replace=False)] = 0
+            mask[past + 2] = 0
+        allowed = np.zeros((n, past + n), dtype=bool)
+        for i in range(n):
+            allowed[i, : past + i + 1] = mask[: past + i + 1] != 0
+        got = oracle.attention_slot(q, kc, vc, past, mask)
+        ref = _sdpa_reference(q, kc, vc, allowed)
+        assert np.max(np.abs(got - ref)) <= 1e-12, (n, holes)
+
+
+# ------------------------------------------------------------------ rotary closed forms
+
+def pin_rope_closed_forms():
+    r = np.random.default_rng(6)
+    d, theta = 64, 500000.0
+    x = r.standard_normal((7, d))
+    assert np.array_equal(oracle.apply_rope(x, np.zeros(7), theta), x)          # p = 0 is the identity
+    p = r.integers(0, 8000, 7)
+    y = oracle.apply_rope(x, p, theta)
+    assert np.allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-13)
+    # complex form: (x_i + j x_{i+D/2}) * exp(j p theta^(-2i/D))
+    i = np.arange(d // 2)
+    z = (x[:, : d // 2] + 1j * x[:, d // 2:]) * np.exp(1j * p[:, None] * theta ** (-2.0 * i / d))
+    assert np.max(np.abs(y - np.concatenate([z.real, z.imag], axis=-1))) <= 1e-9
+    inv = oracle.rope_inv_freq(d, theta)
+    assert inv[0] == 1.0 and abs(inv[-1] - theta ** (-(d - 2) / d)) <= 1e-18
+
+
+def pin_rope_relative_position():
+    """<R(p) q, R(p') k> depends only on p - p'."""
+    r = np.random.default_rng(7)
+    d, theta = 128, 500000.0
+    q, k = r.standard_normal(d), r.standard_normal(d)
+    base = np.dot(oracle.apply_rope(q, 100, theta), oracle.apply_rope(k, 37, theta))
+    for c in (1, 250, 4000):
+        s = np.dot(oracle.apply_rope(q, 100 + c, theta), oracle.apply_rope(k, 37 + c, theta))
+        assert abs(s - base) <= 1e-9 * (1 + abs(base))
+
+
+# ------------------------------------------------------------------ attention closed forms
+
+def pin_single_key_and_own_value():
+    r = np.random.default_rng(8)
+    hkv, d, past = 2, 64, 10
+    kc = r.standard_normal((hkv, past + 1, d))
+    vc = r.standard_normal((hkv, past + 1, d))
+    q = r.standard_normal((1, 4, d))
+    mask = np.zeros(past + 1, dtype=np.uint8)
+    mask[3] = 1
+    o = oracle.attention_slot(q, kc, vc, past, mask)
+    for h in range(4):
+        assert np.array_equal(o[0, h], vc[h // 2, 3])
+    mask0 = np.ones(1, dtype=np.uint8)                 # P = 0: a token sees only itself
+    o0 = oracle.attention_slot(q, kc[:, :1], vc[:, :1], 0, mask0)
+    for h in range(4):
+        assert np.array_equal(o0[0, h], vc[h // 2, 0])
+
+
+def pin_zero_weights_identity():
+    layers = synth.make_weights(TINY2, 11)
+    for lay in layers:
+        for name in synth.MATRICES:
+            lay.mats[name] = synth.zero_quant_like(lay.mats[name])
+    st, _ = oracle_stage(TINY2, layers=layers)
+    state = oracle_state(TINY2, 1, 30, 64, 11)
+    x = f64(synth.make_hidden(TINY2, 3, 11))
+    out = oracle.forward(st, state, x, np.array([[30, 31, 32]]))
+    assert np.array_equal(out, x)
+
+
+def pin_fully_masked_row_rejected():
+    st, _ = oracle_stage(TINY)
+    state = oracle_state(TINY, 1, 4, 16)
+    mask = np.array([[0, 0, 0, 0, 0]], dtype=np.uint8)
+    try:
+        oracle.forward(st, state, f64(synth.make_hidden(TINY, 1)), np.array([[4]]), None, mask)
+    except ValueError:
+        return
+    raise AssertionError("a query row with no visible key was accepted")
+
+
+# ------------------------------------------------------------------ paper invariants (bitwise)
+
+def pin_mask_equals_trim():
+    """Mask-based rewind == physical trim (paper, "Mask-Based Rewind"), bitwise,
+    for the masked verify itself and for the following decode."""
+    shape = TINY2
+    st, _ = oracle_stage(shape, 21)
+    past, n = 72, 5
+    r = np.random.default_rng(21)
+    holes = np.ones(past, dtype=np.uint8)
+    holes[r.choice(past, 9, replace=False)] = 0
+    holed = oracle_state(shape, 1, past, 128, 21)
+    twin = oracle.trimmed_twin(holed, 0, holes)
+
+    x = f64(synth.make_hidden(shape, n, 21, 1))
+    mask = np.concatenate([holes, np.array([1, 1, 1, 0, 0], dtype=np.uint8)])[None]
+    pos = logical_positions(holes, n)
+    out_m = oracle.forward(st, holed, x, pos, None, mask)
+    out_t = oracle.forward(st, twin, x[:3], pos[:, :3], None, None)
+    assert np.array_equal(out_m[:3], out_t), np.max(np.abs(out_m[:3] - out_t))
+
+    # next decode: the holed state keeps the two rejected drafts, masked
+    mask2 = np.concatenate([mask[0], np.array([1], dtype=np.uint8)])[None]
+    pos2 = logical_positions(mask[0], 1)
+    x2 = f64(synth.make_hidden(shape, 1, 21, 2))
+    out_m2 = oracle.forward(st, holed, x2, pos2, None, mask2)
+    out_t2 = oracle.forward(st, twin, x2, pos2, None, None)
+    assert np.array_equal(out_m2, out_t2)
+
+
+def pin_identity_beam_is_no_gather():
+    shape = TINY2
+    st, _ = oracle_stage(shape, 31)
+    a = oracle_state(shape, 3, 20, 40, 31)
+    b = a.copy()
+    x = f64(synth.make_hidden(shape, 6, 31))
+    pos = np.array([[20, 21]] * 3)
+    oa = oracle.forward(st, a, x, pos, np.arange(3), None)
+    ob = oracle.forward(st, b, x, pos, None, None)
+    assert np.array_equal(oa, ob)
+
+
+def pin_permuted_beam_is_permuted_cache():
+    """beam_idx = perm on state A == identity on a state B whose slot rows were
+    physically permuted; also for the following forward (the reorder persists)."""
+    shape = TINY2
+    st, _ = oracle_stage(shape, 41)
+    a = oracle_state(shape, 3, 20, 40, 41)
+    perm = np.array([2, 0, 2])                      # duplicates allowed, as in a Gather
+    b = oracle.OracleState(shape, 3, 40)
+    for l in range(shape.n_layers):
+        for s in range(3):
+            b.K[l][s] = a.K[l][perm[s]]
+            b.V[l][s] = a.V[l][perm[s]]
+    b.P = a.P
+    x = f64(synth.make_hidden(shape, 3, 41))
+    pos = np.array([[20], [20], [20]])
+    assert np.array_equal(oracle.forward(st, a, x, pos, perm, None), oracle.forward(st, b, x, pos, None, None))
+    x2 = f64(synth.make_hidden(shape, 3, 41, 1))
+    pos2 = pos + 1
+    assert np.array_equal(oracle.forward(st, a, x2, pos2, None, None), oracle.forward(st, b, x2, pos2, None, None))
+
+
+def pin_verify_is_sequential_decodes():
+    shape = TINY2
+    st, _ = oracle_stage(shape, 51)
+    a = oracle_state(shape, 1, 30, 64, 51)
+    b = a.copy()
+    x = f64(synth.make_hidden(shape, 4, 51))
+    pos = np.arange(30, 34)[None]
+    out_v = oracle.forward(st, a, x, pos)
+    outs = [oracle.forward(st, b, x[i:i + 1], pos[:, i:i + 1]) for i in range(4)]
+    assert np.array_equal(out_v, np.concatenate(outs, axis=0))
+
+
+def pin_masked_rows_content_independent():
+    shape = TINY2
+    st, _ = oracle_stage(shape, 61)
+    a = oracle_state(shape, 1, 50, 64, 61)
+    holes = np.ones(50, dtype=np.uint8)
+    holes[[0, 7, 8, 30, 49]] = 0
+    b = a.copy()
+    for l in range(shape.n_layers):
+        idx = np.flatnonzero(holes == 0)
+        b.K[l][0][:, idx] = 1e4 * np.sign(np.random.default_rng(l).standard_normal(b.K[l][0][:, idx].shape))
+        b.V[l][0][:, idx] = -1e4
+    mask = np.concatenate([holes, [1, 1]])[None]
+    x = f64(synth.make_hidden(shape, 2, 61))
+    pos = logical_positions(holes, 2)
+    assert np.array_equal(oracle.forward(st, a, x, pos, None, mask), oracle.forward(st, b, x, pos, None, mask))
+
+
+def _batch_reqs(shape, seed, pasts, ns):
+    reqs = []
+    for r_i, (past, n) in enumerate(zip(pasts, ns)):
+        state = oracle_state(shape, 1, past, past + 8, seed, stream=r_i)
+        holes = synth.hole_mask(past, 0.1, seed, r_i)
+        holes[-1] = 1
+        mask = np.concatenate([holes, np.ones(n, dtype=np.uint8)])[None]
+        reqs.append(dict(state=state, positions=logical_positions(holes, n), beam_idx=None, mask=mask))
+    return reqs
+
+
+def _clone(reqs):
+    return [dict(r, state=r["state"].copy()) for r in reqs]
+
+
+def pin_batch_isolation():
+    """A request's rows are the same alone or micro-batched, do not move when a
+    batch-mate's input changes, and do move when its own input changes."""
+    shape = TINY2
+    st, _ = oracle_stage(shape, 71)
+    reqs = _batch_reqs(shape, 71, [17, 40, 9], [1, 5, 2])
+    rows = sum(np.asarray(r["positions"]).size for r in reqs)
+    x = f64(synth.make_hidden(shape, rows, 71))
+    full = oracle.forward_batch(st, _clone(reqs), x)
+    alone = oracle.forward_batch(st, _clone(reqs[1:2]), x[1:6])
+    assert np.array_equal(full[1:6], alone)
+    x_mate = x.copy()
+    x_mate[0] += 3.0
+    x_mate[6:] *= -1
+    assert np.array_equal(oracle.forward_batch(st, _clone(reqs), x_mate)[1:6], full[1:6])
+    x_own = x.copy()
+    x_own[3] += 1.0
+    assert np.max(np.abs(oracle.forward_batch(st, _clone(reqs), x_own)[1:6] - full[1:6])) > 1e-3
+
+
+def pin_request_permutation():
+    shape = TINY2
+    st, _ = oracle_stage(shape, 81)
+    reqs = _batch_reqs(shape, 81, [12, 25], [2, 3])
+    x = f64(synth.make_hidden(shape, 5, 81))
+    full = oracle.forward_batch(st, _clone(reqs), x)
+    swapped = oracle.forward_batch(st, _clone(reqs[::-1]), np.concatenate([x[2:], x[:2]]))
+    assert np.array_equal(swapped, np.concatenate([full[2:], full[:2]]))
+
+
+def pin_gqa_is_repeated_mha():
+    """Hkv < Hq equals an MHA stage whose k/v projections and cache rows are
+    repeated per q head (head h reads kv head h // (Hq/Hkv))."""
+    shape = TINY
+    mha = synth.StageShape(**{**shape.__dict__, "name": "tiny-mha", "n_kv_heads": shape.n_q_heads})
+    layers = synth.make_weights(shape, 91)
+    rep = shape.n_q_heads // shape.n_kv_heads
+    d = shape.head_dim
+    mha_layers = []
+    for lay in layers:
+        new = synth.LayerData(attn_norm=lay.attn_norm, ffn_norm=lay.ffn_norm, mats=dict(lay.mats))
+        for name in ("wk", "wv"):
+            m = lay.mats[name]
+            rows = np.concatenate([np.arange(g * d, (g + 1) * d) for g in range(shape.n_kv_heads) for _ in range(rep)])
+            new.mats[name] = synth.QuantMatrixData(q=m.q[rows].copy(), scales=m.scales[rows].copy(), n=m.n * rep, k=m.k)
+        mha_layers.append(new)
+    st_g, _ = oracle_stage(shape, layers=layers)
+    st_m, _ = oracle_stage(mha, layers=mha_layers)
+    g_state = oracle_state(shape, 1, 25, 40, 91)
+    m_state = oracle.OracleState(mha, 1, 40)
+    for l in range(shape.n_layers):
+        m_state.K[l] = np.repeat(g_state.K[l], rep, axis=1)
+        m_state.V[l] = np.repeat(g_state.V[l], rep, axis=1)
+    m_state.P = g_state.P
+    x = f64(synth.make_hidden(shape, 3, 91))
+    pos = np.array([[25, 26, 27]])
+    assert np.array_equal(oracle.forward(st_g, g_state, x, pos), oracle.forward(st_m, m_state, x, pos))
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
