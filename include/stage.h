@@ -1,0 +1,196 @@
+/*
+ * stage.h - C ABI of libstage: one pipeline stage's stateful decode/verify
+ * forward on an AMD Instinct MI355X (gfx950).
+ *
+ * A stage is a contiguous block of Llama-style decoder layers (paper,
+ * "Per-Stage Export Pipeline": each shard covers a contiguous layer range)
+ * with symmetric INT4 group-quantized weights (Step 4 of that pipeline),
+ * RMSNorm, rotary embeddings from a precomputed cos/sin table indexed by
+ * caller position ids (Step 2 and "Stateful KV-Cached Inference"), and
+ * scaled-dot-product attention over a per-request stateful KV cache.
+ *
+ * Two properties of the paper's shards are reproduced exactly:
+ *  - the cache is reordered along the slot axis through beam_idx, as the
+ *    Gather(ReadValue, beam_idx, axis=0) the shards insert ("Reaching
+ *    Monolithic Parity: the beam_idx Gather Injection"); here the reorder is
+ *    applied to a per-state index table and cache rows are read through it,
+ *    never copied;
+ *  - rejected speculative positions stay in the cache and are hidden by a 0
+ *    in attention_mask ("Mask-Based Rewind"); new rows are appended at the
+ *    next physical index and rotary uses the caller's (logical) position ids.
+ *
+ * Conventions
+ *  - Every call returns STAGE_OK (0) or a negative STAGE_E_* code;
+ *    stage_last_error() returns a thread-local message for the last failure.
+ *  - Validation is synchronous and all-or-nothing: on any error nothing has
+ *    been enqueued and no state (length, table, contents) has changed.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Device work is stream-ordered and asynchronous; host metadata arrays are
+ *    copied before the call returns and may be reused immediately.
+ *  - Calls on one Stage (and on the KV states it allocated) must be
+ *    serialized by the caller.  Overlapping calls on one stage race.
+ *  - Dtype codes: STAGE_DTYPE_F16 = IEEE half, STAGE_DTYPE_BF16 = bfloat16.
+ */
+#ifndef PAPER_2608_19147_STAGE_H
+#define PAPER_2608_19147_STAGE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define STAGE_OK                0
+#define STAGE_E_INVALID        -1   /* bad argument value (NULL, range, fully masked query row) */
+#define STAGE_E_SHAPE          -2   /* shape mismatch (mask length, matrix dims) */
+#define STAGE_E_CAPACITY       -3   /* KV capacity, row count or position table exceeded */
+#define STAGE_E_OOM            -4   /* device or pinned allocation failed */
+#define STAGE_E_HIP            -5   /* a HIP runtime call failed (message has the HIP error) */
+#define STAGE_E_STATE_MISMATCH -6   /* KV state belongs to another stage, or used twice in one call */
+#define STAGE_E_UNSUPPORTED    -7   /* configuration outside what the kernels implement */
+
+#define STAGE_DTYPE_F16  1
+#define STAGE_DTYPE_BF16 2
+
+/* Most activation rows (sum over requests of slots x tokens) per forward. */
+#define STAGE_MAX_ROWS 64
+
+/* Model dimensions of the stage.  Requirements: head_dim in {64, 128};
+ * n_q_heads a multiple of n_kv_heads; hidden, ffn and n_q_heads*head_dim
+ * even; group_size a multiple of 32 (the paper's shards use 128). */
+typedef struct StageConfig {
+    int32_t n_layers;
+    int32_t hidden;          /* H */
+    int32_t n_q_heads;       /* Hq */
+    int32_t n_kv_heads;      /* Hkv; q head h reads kv head h / (Hq/Hkv) */
+    int32_t head_dim;        /* D */
+    int32_t ffn;             /* F (SwiGLU inner size) */
+    int32_t group_size;      /* G: INT4 quantization group along K */
+    float   rms_eps;
+    int32_t act_dtype;       /* dtype of hidden_in / hidden_out / norm weights */
+    int32_t kv_dtype;        /* dtype of cached K/V rows */
+    double  rope_theta;      /* cos/sin(p * theta^(-2i/D)), rotate-half pairing (i, i+D/2) */
+    int32_t max_positions;   /* size of the rotary table; positions must be < this */
+    /* Optional host table [max_positions][D/2][2] fp32 (cos, sin); NULL =>
+     * computed in fp64 from rope_theta and stored as fp32. */
+    const float* rope_cos_sin;
+} StageConfig;
+
+/* One INT4 matrix W [n, k] (out = x W^T) in the canonical layout:
+ *   q      : uint8 [n][ceil(k/2)], offset-binary nibbles u = code + 8
+ *            (code in [-8, 7]); the low nibble holds the even k.
+ *   scales : fp16 bits [n][ceil(k/G)]; W[r][c] = code * scale[r][c / G]
+ *            (symmetric, no zero point; the last group of a ragged k has its
+ *            own scale; fp16 subnormal scales are honoured exactly).
+ * Host or device pointers, per the weights_on_device flag of stage_create. */
+typedef struct QuantMatrix {
+    const uint8_t*  q;
+    const uint16_t* scales;
+    int32_t n;
+    int32_t k;
+} QuantMatrix;
+
+/* One decoder layer: pre-norm attention then pre-norm SwiGLU FFN.
+ * wq [Hq*D, H], wk/wv [Hkv*D, H], wo [H, Hq*D], wg/wu [F, H], wd [H, F].
+ * attn_norm / ffn_norm: [H] in act_dtype. */
+typedef struct LayerWeights {
+    const uint16_t* attn_norm;
+    const uint16_t* ffn_norm;
+    QuantMatrix wq, wk, wv, wo, wg, wu, wd;
+} LayerWeights;
+
+typedef struct Stage Stage;
+typedef struct KVState KVState;
+
+/* Create a stage.  Copies and repacks every weight into library-owned device
+ * memory (the caller may free its copies when the call returns), builds the
+ * rotary table and sizes the workspace for STAGE_MAX_ROWS rows.
+ * layers: host array of cfg->n_layers entries; weight pointers are host
+ * pointers if weights_on_device == 0, device pointers otherwise.
+ * Errors: INVALID/SHAPE/UNSUPPORTED for a bad config or matrix dims, OOM, HIP. */
+int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights_on_device,
+                 void* stream, Stage** out);
+int stage_destroy(Stage* stage);
+
+/* Allocate a KV state of n_slots slots x capacity rows for every layer and
+ * kv head (the paper's per-request ReadValue/Assign state, "Stateful
+ * KV-Cached Inference"; one per micro-batched request, "Multi-User
+ * Throughput via Micro-Batching").  Starts with physical length P = 0 and
+ * the identity beam table.  The state is bound to `stage`. */
+int kv_state_alloc(Stage* stage, int n_slots, int capacity, KVState** out);
+int kv_state_free(KVState* state);
+/* P = 0 (contents are left in place and overwritten by later appends). */
+int kv_state_reset(KVState* state);
+
+/* Append n_tokens already-stored rows (K after rotary, V raw) for every
+ * layer, slot and kv head at physical rows P..P+n-1 of each slot, then
+ * P += n.  k, v: [L][S][Hkv][n][D] in kv_dtype; host pointers if on_device == 0
+ * (copied before return), device pointers otherwise.
+ * Errors: CAPACITY if P + n > capacity; INVALID for n < 1 or NULL. */
+int kv_append(KVState* state, const void* k, const void* v, int n_tokens, int on_device, void* stream);
+
+int kv_length(const KVState* state, int* length_out);
+
+/* Copy rows [start, start+count) of one layer and slot as the slot sees them
+ * (resolved through the beam table) to k_out, v_out: [Hkv][count][D] in
+ * kv_dtype; host pointers if out_on_device == 0 (the call then synchronizes
+ * the stream), device pointers otherwise.
+ * Errors: INVALID if the range exceeds P or layer/slot is out of range. */
+int kv_read(KVState* state, int layer, int slot, int start, int count,
+            void* k_out, void* v_out, int out_on_device, void* stream);
+
+/* Drop trailing rows: P = new_len (metadata only; 0 <= new_len <= P).  This is
+ * the physical trim the paper replaces by masking ("The Trim Problem"); it is
+ * provided for twins in tests and for fixed-length benchmarking. */
+int kv_truncate(KVState* state, int new_len);
+
+/* One request of a forward: `state` with S slots and physical length P,
+ * each slot carrying n_tokens new tokens (1 = decode, K+1 = verify).
+ *   positions      : host int32 [S * n_tokens], rotary position of each new
+ *                    token; callers keep them at the logical length (number
+ *                    of unmasked rows before it) so that masking equals trimming.
+ *   beam_idx       : host int32 [S] or NULL.  Before this forward, slot b takes
+ *                    the rows of slot beam_idx[b] (duplicates allowed); the
+ *                    reorder persists in the state.  NULL or the identity
+ *                    leaves the state as is.
+ *   attention_mask : host uint8 [S * mask_len], mask_len must equal P + n_tokens;
+ *                    0 hides that key column from every query of the slot;
+ *                    query i also never sees physical rows after P + i.
+ * Every query row must see at least one key (else STAGE_E_INVALID; a fully
+ * masked softmax row has no value). */
+typedef struct StageRequest {
+    KVState*       state;
+    int32_t        n_tokens;
+    const int32_t* positions;
+    const int32_t* beam_idx;
+    const uint8_t* attention_mask;
+    int32_t        mask_len;
+} StageRequest;
+
+/* The forward of the stage over n_req independent requests in one pass
+ * (micro-batching).  hidden_in / hidden_out: device [M][H] in act_dtype with
+ * M = sum over requests of S * n_tokens, rows request-major, then slot, then
+ * token.  They must not overlap.  Appends each request's new K/V rows and
+ * advances its P by n_tokens once the work is enqueued.
+ * Errors: INVALID (NULL, bad n, beam_idx out of range, fully masked row,
+ * state repeated), SHAPE (mask_len != P + n), CAPACITY (P + n > capacity,
+ * M > STAGE_MAX_ROWS, position >= max_positions), STATE_MISMATCH, HIP. */
+int stage_forward(Stage* stage, const StageRequest* reqs, int n_req,
+                  const void* hidden_in, void* hidden_out, void* stream);
+
+/* Test support: the dequantized weight matrix as the kernels decode it,
+ * W[r][c] = code * scale exactly, written to out_host fp32 [n][k].
+ * which: 0..6 = wq, wk, wv, wo, wg, wu, wd.  Synchronizes the device. */
+int stage_debug_dequant(Stage* stage, int layer, int which, float* out_host);
+
+/* Bytes of device memory the stage holds for weights (packed codes + scales +
+ * norm weights), as stored. */
+int64_t stage_weight_bytes(const Stage* stage);
+
+const char* stage_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PAPER_2608_19147_STAGE_H */

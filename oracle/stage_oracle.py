@@ -89,21 +89,27 @@ def fp16_bits_to_f64(scales: np.ndarray) -> np.ndarray:
 # one scale per group, no zero point.  Stored codes are offset-binary.
 
 def unpack_int4(packed: np.ndarray, k: int) -> np.ndarray:
-    """uint8 [N, ceil(K/2)] -> signed codes q in [-8, 7] as int64 [N, K]."""
+    """uint8 [N, ceil(K/2)] -> signed codes q in [-8, 7] as int8 [N, K]."""
     packed = np.asarray(packed, dtype=np.uint8)
     n, kb = packed.shape
-    u = np.empty((n, 2 * kb), dtype=np.int64)
+    u = np.empty((n, 2 * kb), dtype=np.int8)
     u[:, 0::2] = packed & 0x0F      # even k in the low nibble
     u[:, 1::2] = packed >> 4
-    return u[:, :k] - 8
+    return u[:, :k] - np.int8(8)
 
 
 def dequant(q: np.ndarray, scales: np.ndarray, k: int, group: int) -> np.ndarray:
     """W[n, k] = q[n, k] * s[n, k // G] in fp64 (exact)."""
     codes = unpack_int4(q, k)
     s = fp16_bits_to_f64(scales)
-    assert s.shape[1] == (k + group - 1) // group
-    return codes * np.repeat(s, group, axis=1)[:, :k]
+    n = codes.shape[0]
+    ng = (k + group - 1) // group
+    assert s.shape == (n, ng)
+    w = np.zeros((n, ng * group), dtype=np.float64)
+    w[:, :k] = codes
+    w = w.reshape(n, ng, group)
+    w *= s[:, :, None]
+    return w.reshape(n, ng * group)[:, :k]
 
 
 # ------------------------------------------------------------------ layer pieces
@@ -176,6 +182,13 @@ def attention_slot(q: np.ndarray, kc: np.ndarray, vc: np.ndarray, past: int,
 
 # ------------------------------------------------------------------ stage and state
 
+def _as_f64(a) -> np.ndarray:
+    """Exact fp64 copy of an fp16/bf16/fp32 array (numpy or torch tensor)."""
+    if hasattr(a, "double") and not isinstance(a, np.ndarray):
+        return a.double().cpu().numpy()
+    return np.asarray(a, dtype=np.float64)
+
+
 class OracleStage:
     """Stage weights in fp64.  ``layers[l]`` has ``attn_norm`` / ``ffn_norm``
     (values in the activation dtype, any array-like) and ``mats[name]`` with
@@ -197,8 +210,8 @@ class OracleStage:
             return self._cache[l]
         lay = self.layers[l]
         w = {name: dequant(m.q, m.scales, m.k, self.shape.group_size) for name, m in lay.mats.items()}
-        w["attn_norm"] = np.asarray(lay.attn_norm, dtype=np.float64)
-        w["ffn_norm"] = np.asarray(lay.ffn_norm, dtype=np.float64)
+        w["attn_norm"] = _as_f64(lay.attn_norm)
+        w["ffn_norm"] = _as_f64(lay.ffn_norm)
         if self.cache_weights:
             self._cache[l] = w
         return w

@@ -1,0 +1,98 @@
+"""ctypes declarations of libstage.so (include/stage.h).  Marshalling only."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libstage.so")
+
+STAGE_OK = 0
+ERRORS = {
+    -1: "STAGE_E_INVALID", -2: "STAGE_E_SHAPE", -3: "STAGE_E_CAPACITY", -4: "STAGE_E_OOM",
+    -5: "STAGE_E_HIP", -6: "STAGE_E_STATE_MISMATCH", -7: "STAGE_E_UNSUPPORTED",
+}
+DTYPE_F16 = 1
+DTYPE_BF16 = 2
+MAX_ROWS = 64
+
+# Every function that include/stage.h declares.
+EXPORTS = (
+    "stage_create", "stage_destroy", "kv_state_alloc", "kv_state_free", "kv_state_reset",
+    "kv_append", "kv_length", "kv_read", "kv_truncate", "stage_forward",
+    "stage_debug_dequant", "stage_weight_bytes", "stage_last_error",
+)
+
+
+class StageConfig(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32), ("hidden", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32),
+        ("group_size", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("act_dtype", ctypes.c_int32),
+        ("kv_dtype", ctypes.c_int32), ("rope_theta", ctypes.c_double), ("max_positions", ctypes.c_int32),
+        ("rope_cos_sin", ctypes.POINTER(ctypes.c_float)),
+    ]
+
+
+class QuantMatrix(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("scales", ctypes.c_void_p), ("n", ctypes.c_int32), ("k", ctypes.c_int32)]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [("attn_norm", ctypes.c_void_p), ("ffn_norm", ctypes.c_void_p)] + [
+        (name, QuantMatrix) for name in ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
+    ]
+
+
+class StageRequest(ctypes.Structure):
+    _fields_ = [
+        ("state", ctypes.c_void_p), ("n_tokens", ctypes.c_int32), ("positions", ctypes.c_void_p),
+        ("beam_idx", ctypes.c_void_p), ("attention_mask", ctypes.c_void_p), ("mask_len", ctypes.c_int32),
+    ]
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libstage.so; raises if it has not been built (no fallback path exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                          "(python -m paper_2608_19147_amd.build)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I, V = ctypes.POINTER, ctypes.c_int, ctypes.c_void_p
+    sig = {
+        "stage_create": (I, [P(StageConfig), P(LayerWeights), I, V, P(V)]),
+        "stage_destroy": (I, [V]),
+        "kv_state_alloc": (I, [V, I, I, P(V)]),
+        "kv_state_free": (I, [V]),
+        "kv_state_reset": (I, [V]),
+        "kv_append": (I, [V, V, V, I, I, V]),
+        "kv_length": (I, [V, P(I)]),
+        "kv_read": (I, [V, I, I, I, I, V, V, I, V]),
+        "kv_truncate": (I, [V, I]),
+        "stage_forward": (I, [V, P(StageRequest), I, V, V, V]),
+        "stage_debug_dequant": (I, [V, I, I, V]),
+        "stage_weight_bytes": (ctypes.c_int64, [V]),
+        "stage_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+class StageError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+def check(code: int) -> None:
+    if code != STAGE_OK:
+        raise StageError(code, load().stage_last_error().decode(errors="replace"))

@@ -1,0 +1,694 @@
+// gfx950 kernels of the stage forward.
+//
+// gemv_kernel  : W4A16 matrix-vector product for up to 8 activation rows.  One
+//                wave lane owns one weight row of a 64-row tile and streams
+//                16-byte chunks (32 INT4 codes) with non-temporal loads; the
+//                activation slice sits in LDS as fp16 pairs and is broadcast to
+//                all lanes; codes become fp16 with the 0x6400 mask-and-or trick
+//                and are consumed by v_dot2_f32_f16 (fp32 accumulation); the
+//                group scale multiplies each chunk's partial dot product, so the
+//                dequantized weight is exact.  Prologue: RMSNorm of the input
+//                row.  Epilogue: plain store, residual add, or SwiGLU.  K is split
+//                over workgroups; the last workgroup of a tile (atomic ticket)
+//                sums the partials in a fixed order, so results are deterministic.
+// attn_kernel  : split-KV decode/verify attention.  Grid = (slot, kv head,
+//                split); 16 lanes read one 256-byte cache row, 16 rows per step
+//                per workgroup.  Rows j < P are read through the beam table;
+//                rows j >= P are this forward's new k/v, rotated and rounded here
+//                and written to the cache by their owner.  Mask and causality
+//                decide visibility inside an online softmax (exp2 domain);
+//                partials are merged by the last split's workgroup.
+#include "common.h"
+
+namespace stg {
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+// ------------------------------------------------------------------ conversions
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
+    u += 0x7fffu + ((u >> 16) & 1u);                                           // ties to even
+    return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float f16_to_f32(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
+__device__ __forceinline__ uint16_t f32_to_f16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+
+__device__ __forceinline__ float load_val(const void* p, int dt, size_t i) {
+    if (dt == DT_F32) return ((const float*)p)[i];
+    const uint16_t b = ((const uint16_t*)p)[i];
+    return dt == DT_BF16 ? bf16_to_f32(b) : f16_to_f32(b);
+}
+
+__device__ __forceinline__ uint16_t to_half_bits(float f, int dt) { return dt == DT_BF16 ? f32_to_bf16(f) : f32_to_f16(f); }
+__device__ __forceinline__ float half_bits_to_f32(uint16_t b, int dt) { return dt == DT_BF16 ? bf16_to_f32(b) : f16_to_f32(b); }
+
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+    return (uint32_t)f32_to_f16(lo) | ((uint32_t)f32_to_f16(hi) << 16);
+}
+
+// 16-byte chunk (32 codes) -> 16 fp16 pairs of consecutive k holding q = u - 8 exactly.
+__device__ __forceinline__ void unpack_chunk(const u32x4 w, half2_t* out) {
+    const half2_t sub = {(_Float16)1032.0f, (_Float16)1032.0f};
+    const half2_t s16 = {(_Float16)0.0625f, (_Float16)0.0625f};
+    const half2_t m72 = {(_Float16)-72.0f, (_Float16)-72.0f};
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        const uint32_t x = w[d];
+        const uint32_t y = x >> 8;
+        const uint32_t p0 = (x & 0x000F000Fu) | 0x64006400u;   // 1024 + u      (k, k+1)
+        const uint32_t p1 = (x & 0x00F000F0u) | 0x64006400u;   // 1024 + 16 u   (k+2, k+3)
+        const uint32_t p2 = (y & 0x000F000Fu) | 0x64006400u;   //               (k+4, k+5)
+        const uint32_t p3 = (y & 0x00F000F0u) | 0x64006400u;   //               (k+6, k+7)
+        out[4 * d + 0] = __builtin_bit_cast(half2_t, p0) - sub;
+        out[4 * d + 1] = __builtin_elementwise_fma(__builtin_bit_cast(half2_t, p1), s16, m72);
+        out[4 * d + 2] = __builtin_bit_cast(half2_t, p2) - sub;
+        out[4 * d + 3] = __builtin_elementwise_fma(__builtin_bit_cast(half2_t, p3), s16, m72);
+    }
+}
+
+__device__ __forceinline__ int dest_row(int r, int row_off, int row_map) {
+    if (row_map == 0) return row_off + r;
+    return 64 * (r >> 5) + (r & 31) + (row_map == 2 ? 32 : 0);   // gate | up interleave
+}
+
+// ------------------------------------------------------------------ repack
+
+__global__ void repack_codes_kernel(const uint8_t* __restrict__ q, int n, int k, uint8_t* __restrict__ w_out,
+                                    int nchunk, int row_off, int row_map) {
+    const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+    if (idx >= (size_t)n * nchunk) return;
+    const int r = (int)(idx / nchunk), c = (int)(idx % nchunk);
+    const int kb = (k + 1) / 2;
+    const int dr = dest_row(r, row_off, row_map);
+    const int t = dr >> 6, lane = dr & 63;
+    u32x4 o;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        uint32_t wd = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int kk = c * 32 + d * 8 + e;
+            uint32_t nib = 8;
+            if (kk < k) {
+                const uint8_t byte = q[(size_t)r * kb + (kk >> 1)];
+                nib = (kk & 1) ? (byte >> 4) : (byte & 15);
+            }
+            const int sh = (e & 1) ? (16 + 4 * (e >> 1)) : 4 * (e >> 1);
+            wd |= nib << sh;
+        }
+        o[d] = wd;
+    }
+    *(u32x4*)(w_out + (((size_t)t * nchunk + c) * 64 + lane) * 16) = o;
+}
+
+__global__ void repack_scales_kernel(const uint16_t* __restrict__ s, int n, int ng, uint16_t* __restrict__ s_out,
+                                     int ngroups, int row_off, int row_map) {
+    const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+    if (idx >= (size_t)n * ng) return;
+    const int r = (int)(idx / ng), g = (int)(idx % ng);
+    const int dr = dest_row(r, row_off, row_map);
+    const int t = dr >> 6, lane = dr & 63;
+    s_out[((size_t)t * ngroups + g) * 64 + lane] = s[idx];
+}
+
+hipError_t launch_repack(const uint8_t* q, const uint16_t* s, int n, int k, int g, uint8_t* w_out, uint16_t* s_out,
+                         int ntiles, int nchunk, int ngroups, int row_off, int row_map, hipStream_t st) {
+    (void)ntiles;
+    const size_t nc = (size_t)n * nchunk;
+    repack_codes_kernel<<<dim3((unsigned)((nc + 255) / 256)), dim3(256), 0, st>>>(q, n, k, w_out, nchunk, row_off, row_map);
+    const int ng = (k + g - 1) / g;
+    const size_t ns = (size_t)n * ng;
+    repack_scales_kernel<<<dim3((unsigned)((ns + 255) / 256)), dim3(256), 0, st>>>(s, n, ng, s_out, ngroups, row_off, row_map);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ debug dequant
+
+__global__ void dequant_kernel(PackedMat m, int row_off, int row_map, int n_rows, float* __restrict__ out) {
+    const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+    if (idx >= (size_t)n_rows * m.nchunk) return;
+    const int r = (int)(idx / m.nchunk), c = (int)(idx % m.nchunk);
+    const int dr = dest_row(r, row_off, row_map);
+    const int t = dr >> 6, lane = dr & 63;
+    const u32x4 w = *(const u32x4*)(m.w + (((size_t)t * m.nchunk + c) * 64 + lane) * 16);
+    half2_t h[16];
+    unpack_chunk(w, h);
+    const float sc = f16_to_f32(m.s[((size_t)t * m.ngroups + c / m.gchunks) * 64 + lane]);
+#pragma unroll
+    for (int p = 0; p < 16; ++p) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int kk = c * 32 + 2 * p + e;
+            if (kk < m.k) out[(size_t)r * m.k + kk] = (float)h[p][e] * sc;
+        }
+    }
+}
+
+hipError_t launch_dequant(const PackedMat& m, int row_off, int row_map, int n_rows, float* out, hipStream_t st) {
+    const size_t nc = (size_t)n_rows * m.nchunk;
+    dequant_kernel<<<dim3((unsigned)((nc + 255) / 256)), dim3(256), 0, st>>>(m, row_off, row_map, n_rows, out);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ reductions
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the 16 lanes of a DPP row; every lane receives the identical value.
+__device__ __forceinline__ float sum16(float v) {
+    v += dpp_f<0xB1>(v);    // quad_perm [1,0,3,2]
+    v += dpp_f<0x4E>(v);    // quad_perm [2,3,0,1]
+    v += dpp_f<0x141>(v);   // row_half_mirror
+    v += dpp_f<0x140>(v);   // row_mirror
+    return v;
+}
+
+// Deterministic block sum (256 threads): fixed-order tree in LDS.
+__device__ __forceinline__ float block_sum256(float v, float* buf) {
+    const int tid = threadIdx.x;
+    buf[tid] = v;
+    __syncthreads();
+#pragma unroll
+    for (int w = 128; w > 0; w >>= 1) {
+        if (tid < w) buf[tid] += buf[tid + w];
+        __syncthreads();
+    }
+    const float r = buf[0];
+    __syncthreads();
+    return r;
+}
+
+// ------------------------------------------------------------------ GEMV
+
+template <int MT>
+__global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
+    __shared__ __attribute__((aligned(16))) uint32_t xs[MT][GEMV_MAX_CPS * 16];
+    __shared__ float red[4][MT][64];
+    __shared__ float rs_s[MT];
+    __shared__ float bsum[256];
+    __shared__ int last_s;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int t = blockIdx.x, s = blockIdx.y;
+    const PackedMat W = a.W;
+    const int M = a.M;
+    const int c0 = s * a.cps;
+    const int c1 = min(W.nchunk, c0 + a.cps);
+    const int npair = (c1 - c0) * 16;
+
+    // ---- prologue: inverse RMS of each input row
+    if (a.rms == RMS_FULLROW) {
+        for (int m = 0; m < M; ++m) {
+            float ss = 0.f;
+            for (int kk = tid; kk < W.k; kk += 256) {
+                const float v = load_val(a.in, a.in_dt, (size_t)m * a.in_ld + kk);
+                ss += v * v;
+            }
+            ss = block_sum256(ss, bsum);
+            if (tid == 0) rs_s[m] = rsqrtf(ss / (float)W.k + a.eps);
+        }
+    } else if (a.rms == RMS_PARTIALS) {
+        if (tid < M) {
+            float ss = 0.f;
+            for (int tt = 0; tt < a.ssq_tiles; ++tt) ss += a.ssq_in[(size_t)tid * a.ssq_tiles + tt];
+            rs_s[tid] = rsqrtf(ss / (float)W.k + a.eps);
+        }
+    }
+    __syncthreads();
+
+    // ---- stage the activation slice as fp16 pairs
+    for (int idx = tid; idx < M * npair; idx += 256) {
+        const int m = idx / npair, p = idx - m * npair;
+        const int kk = c0 * 32 + 2 * p;
+        float v0 = 0.f, v1 = 0.f;
+        if (kk < W.k) v0 = load_val(a.in, a.in_dt, (size_t)m * a.in_ld + kk);
+        if (kk + 1 < W.k) v1 = load_val(a.in, a.in_dt, (size_t)m * a.in_ld + kk + 1);
+        if (a.rms != RMS_NONE) {
+            const float rs = rs_s[m];
+            if (kk < W.k) v0 = (v0 * rs) * half_bits_to_f32(a.gamma[kk], a.gamma_dt);
+            if (kk + 1 < W.k) v1 = (v1 * rs) * half_bits_to_f32(a.gamma[kk + 1], a.gamma_dt);
+        }
+        xs[m][p] = pack_f16x2(v0, v1);
+    }
+    __syncthreads();
+
+    // ---- stream the tile
+    float acc[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m] = 0.f;
+    const u32x4* wbase = (const u32x4*)W.w + (size_t)t * W.nchunk * 64 + lane;
+    const uint16_t* sbase = W.s + (size_t)t * W.ngroups * 64 + lane;
+    constexpr int U = 4;
+    for (int cb = c0 + wave; cb < c1; cb += 4 * U) {
+        u32x4 wv[U];
+        float sc[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = cb + 4 * u;
+            if (c < c1) {
+                wv[u] = __builtin_nontemporal_load(wbase + (size_t)c * 64);
+                sc[u] = f16_to_f32(sbase[(size_t)(c / W.gchunks) * 64]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = cb + 4 * u;
+            if (c < c1) {
+                half2_t wq[16];
+                unpack_chunk(wv[u], wq);
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    if (m < M) {
+                        const u32x4* xv = (const u32x4*)&xs[m][(c - c0) * 16];
+                        float d = 0.f;
+#pragma unroll
+                        for (int q4 = 0; q4 < 4; ++q4) {
+                            const u32x4 x4 = xv[q4];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                // copy the element out first: a bit_cast of a vector-element
+                                // lvalue reads element 0 of the vector
+                                const uint32_t xe = x4[e];
+                                d = __builtin_amdgcn_fdot2(wq[4 * q4 + e], __builtin_bit_cast(half2_t, xe), d, false);
+                            }
+                        }
+                        acc[m] += sc[u] * d;
+                    }
+                }
+            }
+        }
+    }
+
+    // ---- reduce the four waves (fixed order)
+#pragma unroll
+    for (int m = 0; m < MT; ++m) red[wave][m][lane] = acc[m];
+    __syncthreads();
+
+    const int ldp = W.ntiles * 64;
+    float vals[(MT * 64 + 255) / 256];
+#pragma unroll
+    for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
+        const int idx = tid + 256 * q;
+        vals[q] = 0.f;
+        if (idx < M * 64) {
+            const int m = idx >> 6, r = idx & 63;
+            vals[q] = ((red[0][m][r] + red[1][m][r]) + red[2][m][r]) + red[3][m][r];
+        }
+    }
+
+    if (a.ksplit > 1) {
+#pragma unroll
+        for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
+            const int idx = tid + 256 * q;
+            if (idx < M * 64) {
+                const int m = idx >> 6, r = idx & 63;
+                a.partial[((size_t)s * M + m) * ldp + t * 64 + r] = vals[q];
+            }
+        }
+        __threadfence();
+        __syncthreads();
+        if (tid == 0) {
+            const unsigned prev = atomicAdd(&a.counters[t], 1u);
+            last_s = (prev == (unsigned)(a.ksplit - 1));
+        }
+        __syncthreads();
+        if (!last_s) return;
+        __threadfence();
+        if (tid == 0) a.counters[t] = 0u;
+#pragma unroll
+        for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
+            const int idx = tid + 256 * q;
+            if (idx < M * 64) {
+                const int m = idx >> 6, r = idx & 63;
+                float v = 0.f;
+                for (int ss = 0; ss < a.ksplit; ++ss) v += a.partial[((size_t)ss * M + m) * ldp + t * 64 + r];
+                vals[q] = v;
+            }
+        }
+    }
+
+    // ---- epilogue
+    if (a.epi == EPI_STORE) {
+#pragma unroll
+        for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
+            const int idx = tid + 256 * q;
+            if (idx < M * 64) {
+                const int m = idx >> 6, r = idx & 63;
+                const int n = t * 64 + r;
+                if (n < W.n) a.out[(size_t)m * a.out_ld + n] = vals[q];
+            }
+        }
+    } else if (a.epi == EPI_RESID) {
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
+            const int idx = tid + 256 * q;
+            if (idx < M * 64) {
+                const int m = idx >> 6, r = idx & 63;
+                const int n = t * 64 + r;
+                float xn = 0.f;
+                if (n < W.n) {
+                    xn = load_val(a.resid, a.resid_dt, (size_t)m * a.resid_ld + n) + vals[q];
+                    a.out[(size_t)m * a.out_ld + n] = xn;
+                    if (a.out_act) ((uint16_t*)a.out_act)[(size_t)m * a.out_act_ld + n] = to_half_bits(xn, a.out_act_dt);
+                }
+                red[0][m][r] = xn * xn;
+            }
+        }
+        __syncthreads();
+        if (a.ssq_out && tid < M) {
+            float ss = 0.f;
+            for (int r = 0; r < 64; ++r) ss += red[0][tid][r];
+            a.ssq_out[(size_t)tid * W.ntiles + t] = ss;
+        }
+    } else {  // EPI_SWIGLU: rows 0..31 of the tile are gate rows, 32..63 the matching up rows
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
+            const int idx = tid + 256 * q;
+            if (idx < M * 64) red[0][idx >> 6][idx & 63] = vals[q];
+        }
+        __syncthreads();
+        for (int idx = tid; idx < M * 32; idx += 256) {
+            const int m = idx >> 5, r = idx & 31;
+            const int f = t * 32 + r;
+            if (f < a.n_valid) {
+                const float gt = red[0][m][r], up = red[0][m][r + 32];
+                a.out[(size_t)m * a.out_ld + f] = (gt / (1.0f + expf(-gt))) * up;
+            }
+        }
+    }
+}
+
+hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
+    const dim3 grid(a.W.ntiles, a.ksplit), block(256);
+    switch (a.M) {
+        case 1: gemv_kernel<1><<<grid, block, 0, st>>>(a); break;
+        case 2: gemv_kernel<2><<<grid, block, 0, st>>>(a); break;
+        case 3: gemv_kernel<3><<<grid, block, 0, st>>>(a); break;
+        case 4: gemv_kernel<4><<<grid, block, 0, st>>>(a); break;
+        case 5: gemv_kernel<5><<<grid, block, 0, st>>>(a); break;
+        case 6: gemv_kernel<6><<<grid, block, 0, st>>>(a); break;
+        case 7: gemv_kernel<7><<<grid, block, 0, st>>>(a); break;
+        case 8: gemv_kernel<8><<<grid, block, 0, st>>>(a); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ attention
+
+template <int D, int RC>
+__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+    constexpr int EPL = D / 16;
+    __shared__ float lo[KGROUPS][RC][D];
+    __shared__ float lm[KGROUPS][RC], ll[KGROUPS][RC];
+    __shared__ int last_s;
+
+    const int item = blockIdx.x, g = blockIdx.y, split = blockIdx.z;
+    const ItemDev it = a.meta.items[item];
+    const ReqDev rq = a.meta.reqs[it.req];
+    const int b = it.slot;
+    const int P = rq.P, n = rq.n;
+    const int L = P + n;
+    int split_len = max(ATTN_MIN_SPLIT, (L + a.nsplit_max - 1) / a.nsplit_max);
+    split_len = (split_len + KGROUPS - 1) / KGROUPS * KGROUPS;
+    const int nsplit = (L + split_len - 1) / split_len;
+    if (split >= nsplit) return;
+    const int j0 = split * split_len, j1 = min(L, j0 + split_len);
+
+    const int tid = threadIdx.x, kg = tid >> 4, li = tid & 15;
+    const int Hq = a.Hq, Hkv = a.Hkv;
+    const int gs = Hq / Hkv;
+    const int R = gs * n;
+    const size_t lstride = (size_t)rq.S * Hkv * rq.cap * D;
+    uint16_t* kl = rq.kc + (size_t)a.layer * lstride;
+    uint16_t* vl = rq.vc + (size_t)a.layer * lstride;
+    const uint8_t* mask = a.meta.masks + rq.mask_off + (size_t)b * rq.mask_len;
+    const int16_t* tab = rq.table + (size_t)b * rq.cap;
+    const int rowbase = rq.row0 + b * n;
+    const int d0 = li * EPL;
+    constexpr int HALF = D / 2;
+
+    for (int r0 = 0; r0 < R; r0 += RC) {
+        float q[RC][EPL];
+        int qi[RC];
+#pragma unroll
+        for (int rr = 0; rr < RC; ++rr) {
+            const int r = r0 + rr;
+            qi[rr] = -1;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) q[rr][e] = 0.f;
+            if (r < R) {
+                const int i = r / gs, h = g * gs + (r % gs);
+                const int m = rowbase + i;
+                const int pos = a.meta.positions[m];
+                const float* qrow = a.qkv + (size_t)m * a.qkv_ld + (size_t)h * D;
+                qi[rr] = i;
+#pragma unroll
+                for (int e = 0; e < EPL; ++e) {
+                    const int d = d0 + e;
+                    const bool lo_half = d < HALF;
+                    const float x = qrow[d];
+                    const float xp = lo_half ? qrow[d + HALF] : qrow[d - HALF];
+                    const float2 cs = a.rope[(size_t)pos * HALF + (lo_half ? d : d - HALF)];
+                    const float y = lo_half ? (x * cs.x - xp * cs.y) : (x * cs.x + xp * cs.y);
+                    q[rr][e] = y * a.qscale;
+                }
+            }
+        }
+        float mx[RC], sl[RC], o[RC][EPL];
+#pragma unroll
+        for (int rr = 0; rr < RC; ++rr) {
+            mx[rr] = -INFINITY;
+            sl[rr] = 0.f;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) o[rr][e] = 0.f;
+        }
+
+        for (int j = j0 + kg; j < j1; j += KGROUPS) {
+            if (mask[j] == 0) continue;                       // hidden from every query of the slot
+            float kf[EPL], vf[EPL];
+            if (j < P) {
+                const int ps = tab[j];
+                const size_t off = (((size_t)ps * Hkv + g) * rq.cap + j) * D + d0;
+                uint16_t kb[EPL], vb[EPL];
+                if constexpr (EPL == 8) {
+                    *(u32x4*)kb = *(const u32x4*)(kl + off);
+                    *(u32x4*)vb = *(const u32x4*)(vl + off);
+                } else {
+                    *(u32x2*)kb = *(const u32x2*)(kl + off);
+                    *(u32x2*)vb = *(const u32x2*)(vl + off);
+                }
+#pragma unroll
+                for (int e = 0; e < EPL; ++e) {
+                    kf[e] = half_bits_to_f32(kb[e], a.kv_dt);
+                    vf[e] = half_bits_to_f32(vb[e], a.kv_dt);
+                }
+            } else {
+                const int i = j - P;
+                const int m = rowbase + i;
+                const int pos = a.meta.positions[m];
+                const float* krow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + g) * D;
+                const float* vrow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + Hkv + g) * D;
+                uint16_t kb[EPL], vb[EPL];
+#pragma unroll
+                for (int e = 0; e < EPL; ++e) {
+                    const int d = d0 + e;
+                    const bool lo_half = d < HALF;
+                    const float x = krow[d];
+                    const float xp = lo_half ? krow[d + HALF] : krow[d - HALF];
+                    const float2 cs = a.rope[(size_t)pos * HALF + (lo_half ? d : d - HALF)];
+                    const float y = lo_half ? (x * cs.x - xp * cs.y) : (x * cs.x + xp * cs.y);
+                    kb[e] = to_half_bits(y, a.kv_dt);
+                    vb[e] = to_half_bits(vrow[d], a.kv_dt);
+                    kf[e] = half_bits_to_f32(kb[e], a.kv_dt);
+                    vf[e] = half_bits_to_f32(vb[e], a.kv_dt);
+                }
+                if (r0 == 0) {                                 // append: owner of row j writes it
+                    const size_t off = (((size_t)b * Hkv + g) * rq.cap + j) * D + d0;
+#pragma unroll
+                    for (int e = 0; e < EPL; ++e) {
+                        kl[off + e] = kb[e];
+                        vl[off + e] = vb[e];
+                    }
+                    if (a.layer == 0 && g == 0 && li == 0) rq.table[(size_t)b * rq.cap + j] = (int16_t)b;
+                }
+            }
+#pragma unroll
+            for (int rr = 0; rr < RC; ++rr) {
+                if (qi[rr] < 0) continue;
+                float sd = 0.f;
+#pragma unroll
+                for (int e = 0; e < EPL; ++e) sd += q[rr][e] * kf[e];
+                sd = sum16(sd);
+                if (j > P + qi[rr]) continue;                 // causal over the physical index
+                const float mn = fmaxf(mx[rr], sd);
+                const float corr = exp2f(mx[rr] - mn);
+                const float p = exp2f(sd - mn);
+                sl[rr] = sl[rr] * corr + p;
+#pragma unroll
+                for (int e = 0; e < EPL; ++e) o[rr][e] = o[rr][e] * corr + p * vf[e];
+                mx[rr] = mn;
+            }
+        }
+
+        // ---- merge the 16 key groups (fixed order)
+#pragma unroll
+        for (int rr = 0; rr < RC; ++rr) {
+            if (li == 0) {
+                lm[kg][rr] = mx[rr];
+                ll[kg][rr] = sl[rr];
+            }
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) lo[kg][rr][d0 + e] = o[rr][e];
+        }
+        __syncthreads();
+        for (int idx = tid; idx < RC * D; idx += 256) {
+            const int rr = idx / D, d = idx % D;
+            const int r = r0 + rr;
+            if (r >= R) continue;
+            float M = -INFINITY;
+            for (int k2 = 0; k2 < KGROUPS; ++k2) M = fmaxf(M, lm[k2][rr]);
+            float O = 0.f, S = 0.f;
+            for (int k2 = 0; k2 < KGROUPS; ++k2) {
+                const float mk = lm[k2][rr];
+                const float w = (mk == -INFINITY) ? 0.f : exp2f(mk - M);
+                O += lo[k2][rr][d] * w;
+                S += ll[k2][rr] * w;
+            }
+            const int i = r / gs, h = g * gs + (r % gs);
+            const int m = rowbase + i;
+            float* pp = a.part + (((size_t)m * Hq + h) * a.nsplit_max + split) * (D + 2);
+            pp[2 + d] = O;
+            if (d == 0) {
+                pp[0] = M;
+                pp[1] = S;
+            }
+        }
+        __syncthreads();
+    }
+
+    // ---- last split of this (slot, kv head) merges all splits (fixed order)
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) {
+        const unsigned prev = atomicAdd(&a.counters[item * Hkv + g], 1u);
+        last_s = (prev == (unsigned)(nsplit - 1));
+    }
+    __syncthreads();
+    if (!last_s) return;
+    __threadfence();
+    if (tid == 0) a.counters[item * Hkv + g] = 0u;
+    for (int idx = tid; idx < R * D; idx += 256) {
+        const int r = idx / D, d = idx % D;
+        const int i = r / gs, h = g * gs + (r % gs);
+        const int m = rowbase + i;
+        const float* pp = a.part + ((size_t)m * Hq + h) * a.nsplit_max * (D + 2);
+        float M = -INFINITY;
+        for (int s2 = 0; s2 < nsplit; ++s2) M = fmaxf(M, pp[(size_t)s2 * (D + 2)]);
+        float O = 0.f, S = 0.f;
+        for (int s2 = 0; s2 < nsplit; ++s2) {
+            const float ms = pp[(size_t)s2 * (D + 2)];
+            const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - M);
+            O += pp[(size_t)s2 * (D + 2) + 2 + d] * w;
+            S += pp[(size_t)s2 * (D + 2) + 1] * w;
+        }
+        a.out[(size_t)m * a.out_ld + (size_t)h * D + d] = O / S;
+    }
+}
+
+hipError_t launch_attention(const AttnArgs& a, int head_dim, int rows_per_item_max, hipStream_t st) {
+    const dim3 grid(a.meta.n_items, a.Hkv, a.nsplit_max), block(256);
+    const bool wide = rows_per_item_max > 4;
+    if (head_dim == 128) {
+        if (wide) attn_kernel<128, 8><<<grid, block, 0, st>>>(a);
+        else attn_kernel<128, 4><<<grid, block, 0, st>>>(a);
+    } else if (head_dim == 64) {
+        if (wide) attn_kernel<64, 8><<<grid, block, 0, st>>>(a);
+        else attn_kernel<64, 4><<<grid, block, 0, st>>>(a);
+    } else {
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ KV state kernels
+
+__global__ void table_gather_kernel(const int16_t* __restrict__ src, int16_t* __restrict__ dst, const int* __restrict__ beam,
+                                    int S, int cap, int P) {
+    const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+    if (idx >= (size_t)S * P) return;
+    const int b = (int)(idx / P), j = (int)(idx % P);
+    dst[(size_t)b * cap + j] = src[(size_t)beam[b] * cap + j];
+}
+
+hipError_t launch_table_gather(const int16_t* src, int16_t* dst, const int* beam, int S, int cap, int P, hipStream_t st) {
+    const size_t n = (size_t)S * P;
+    if (n == 0) return hipSuccess;
+    table_gather_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st>>>(src, dst, beam, S, cap, P);
+    return hipGetLastError();
+}
+
+__global__ void kv_append_kernel(uint16_t* __restrict__ kc, uint16_t* __restrict__ vc, int16_t* __restrict__ table,
+                                 const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+                                 int L, int S, int Hkv, int cap, int D, int P, int n) {
+    const size_t total = (size_t)L * S * Hkv * n * D;
+    const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+    if (idx >= total) return;
+    size_t rem = idx;
+    const int d = (int)(rem % D); rem /= D;
+    const int i = (int)(rem % n); rem /= n;
+    const int g = (int)(rem % Hkv); rem /= Hkv;
+    const int b = (int)(rem % S); rem /= S;
+    const int l = (int)rem;
+    const size_t dst = ((((size_t)l * S + b) * Hkv + g) * cap + (P + i)) * D + d;
+    kc[dst] = k[idx];
+    vc[dst] = v[idx];
+    if (l == 0 && g == 0 && d == 0) table[(size_t)b * cap + P + i] = (int16_t)b;
+}
+
+hipError_t launch_kv_append(uint16_t* kc, uint16_t* vc, int16_t* table, const uint16_t* k, const uint16_t* v,
+                            int L, int S, int Hkv, int cap, int D, int P, int n, hipStream_t st) {
+    const size_t total = (size_t)L * S * Hkv * n * D;
+    kv_append_kernel<<<dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st>>>(kc, vc, table, k, v, L, S, Hkv, cap, D, P, n);
+    return hipGetLastError();
+}
+
+__global__ void kv_read_kernel(const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc, const int16_t* __restrict__ table,
+                               int layer, int slot, int start, int count, int S, int Hkv, int cap, int D,
+                               uint16_t* __restrict__ k_out, uint16_t* __restrict__ v_out) {
+    const size_t total = (size_t)Hkv * count * D;
+    const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+    if (idx >= total) return;
+    const int d = (int)(idx % D);
+    const int c = (int)((idx / D) % count);
+    const int g = (int)(idx / ((size_t)D * count));
+    const int j = start + c;
+    const int ps = table[(size_t)slot * cap + j];
+    const size_t src = ((((size_t)layer * S + ps) * Hkv + g) * cap + j) * D + d;
+    k_out[idx] = kc[src];
+    v_out[idx] = vc[src];
+}
+
+hipError_t launch_kv_read(const uint16_t* kc, const uint16_t* vc, const int16_t* table, int layer, int slot,
+                          int start, int count, int S, int Hkv, int cap, int D, uint16_t* k_out, uint16_t* v_out,
+                          hipStream_t st) {
+    const size_t total = (size_t)Hkv * count * D;
+    if (total == 0) return hipSuccess;
+    kv_read_kernel<<<dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st>>>(kc, vc, table, layer, slot, start, count,
+                                                                                  S, Hkv, cap, D, k_out, v_out);
+    return hipGetLastError();
+}
+
+}  // namespace stg

@@ -1,0 +1,783 @@
+// Host runtime of libstage: validation, weight repack, workspace, KV states,
+// metadata staging and the per-layer launch sequence of stage_forward.
+#include "stage.h"
+#include "common.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+using namespace stg;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+    g_err = msg;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                          \
+    do {                                                                                       \
+        hipError_t e_ = (expr);                                                                \
+        if (e_ != hipSuccess) return fail(STAGE_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+constexpr int META_RING = 4;
+
+struct DevMat {
+    PackedMat pm;
+    int ksplit = 1, cps = 1;
+};
+
+struct LayerDev {
+    DevMat qkv, o, gu, d;
+    uint16_t* attn_norm = nullptr;
+    uint16_t* ffn_norm = nullptr;
+};
+
+int dt_code(int stage_dt) { return stage_dt == STAGE_DTYPE_BF16 ? DT_BF16 : DT_F16; }
+
+size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
+
+}  // namespace
+
+struct Stage {
+    StageConfig cfg{};
+    int device = 0;
+    std::vector<LayerDev> layers;
+    std::vector<void*> allocs;
+    float2* rope = nullptr;
+    float *x = nullptr, *qkv = nullptr, *attn = nullptr, *act = nullptr, *gpart = nullptr, *apart = nullptr, *ssq = nullptr;
+    unsigned *gcnt = nullptr, *acnt = nullptr;
+    int ntiles_h = 0;
+    uint8_t* meta_dev = nullptr;
+    size_t meta_cap = 0;
+    uint8_t* meta_host[META_RING] = {};
+    hipEvent_t meta_ev[META_RING] = {};
+    bool meta_ev_used[META_RING] = {};
+    int ring_i = 0;
+    int64_t weight_bytes = 0;
+
+    ~Stage() {
+        (void)hipSetDevice(device);
+        (void)hipDeviceSynchronize();
+        for (void* p : allocs) (void)hipFree(p);
+        if (meta_dev) (void)hipFree(meta_dev);
+        for (int i = 0; i < META_RING; ++i) {
+            if (meta_host[i]) (void)hipHostFree(meta_host[i]);
+            if (meta_ev[i]) (void)hipEventDestroy(meta_ev[i]);
+        }
+    }
+
+    template <class T>
+    int alloc(T** p, size_t n_elems) {
+        void* q = nullptr;
+        if (n_elems == 0) n_elems = 1;
+        if (hipMalloc(&q, n_elems * sizeof(T)) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(STAGE_E_OOM, "device allocation of " + std::to_string(n_elems * sizeof(T)) + " bytes failed");
+        }
+        allocs.push_back(q);
+        *p = (T*)q;
+        return STAGE_OK;
+    }
+};
+
+struct KVState {
+    Stage* stage = nullptr;
+    int S = 0, cap = 0, P = 0;
+    uint16_t* kc = nullptr;
+    uint16_t* vc = nullptr;
+    int16_t* table[2] = {nullptr, nullptr};
+    int cur = 0;
+};
+
+namespace {
+
+void plan_split(DevMat& m) {
+    int target = 1024;
+    if (const char* e = std::getenv("STAGE_GEMV_WG_TARGET")) target = std::max(1, atoi(e));
+    const int nch = m.pm.nchunk;
+    int ks = std::max(1, std::min(nch, (target + m.pm.ntiles - 1) / m.pm.ntiles));
+    int cps = (nch + ks - 1) / ks;
+    cps = std::min(cps, GEMV_MAX_CPS);
+    ks = (nch + cps - 1) / cps;
+    m.ksplit = ks;
+    m.cps = cps;
+}
+
+int make_mat(Stage* st, DevMat& m, int n_rows_padded_tiles, int k, int g) {
+    m.pm.k = k;
+    m.pm.ntiles = n_rows_padded_tiles;
+    m.pm.nchunk = (k + CHUNK_K - 1) / CHUNK_K;
+    m.pm.gchunks = g / CHUNK_K;
+    m.pm.ngroups = (m.pm.nchunk + m.pm.gchunks - 1) / m.pm.gchunks;
+    uint8_t* w;
+    uint16_t* s;
+    const size_t wbytes = (size_t)m.pm.ntiles * m.pm.nchunk * 64 * 16;
+    const size_t selems = (size_t)m.pm.ntiles * m.pm.ngroups * 64;
+    int rc = st->alloc(&w, wbytes);
+    if (rc) return rc;
+    rc = st->alloc(&s, selems);
+    if (rc) return rc;
+    HIP_TRY(hipMemset(w, 0x88, wbytes));
+    HIP_TRY(hipMemset(s, 0, selems * sizeof(uint16_t)));
+    m.pm.w = w;
+    m.pm.s = s;
+    st->weight_bytes += (int64_t)wbytes + (int64_t)selems * 2;
+    plan_split(m);
+    return STAGE_OK;
+}
+
+// Copy one canonical matrix into the tiled layout of `m` (rows placed per row_off / row_map).
+int upload_mat(Stage* st, DevMat& m, const QuantMatrix& q, int on_device, int row_off, int row_map,
+               uint8_t* tmp_q, uint16_t* tmp_s, hipStream_t stream) {
+    const int g = st->cfg.group_size;
+    const size_t qbytes = (size_t)q.n * ((q.k + 1) / 2);
+    const size_t sbytes = (size_t)q.n * ((q.k + g - 1) / g) * 2;
+    const uint8_t* qsrc = q.q;
+    const uint16_t* ssrc = q.scales;
+    if (!on_device) {
+        HIP_TRY(hipMemcpyAsync(tmp_q, q.q, qbytes, hipMemcpyHostToDevice, stream));
+        HIP_TRY(hipMemcpyAsync(tmp_s, q.scales, sbytes, hipMemcpyHostToDevice, stream));
+        qsrc = tmp_q;
+        ssrc = tmp_s;
+    }
+    HIP_TRY(launch_repack(qsrc, ssrc, q.n, q.k, g, (uint8_t*)m.pm.w, (uint16_t*)m.pm.s, m.pm.ntiles, m.pm.nchunk,
+                          m.pm.ngroups, row_off, row_map, stream));
+    if (!on_device) HIP_TRY(hipStreamSynchronize(stream));   // tmp buffers are reused by the next matrix
+    return STAGE_OK;
+}
+
+int check_mat(const QuantMatrix& m, int n, int k, const char* name, int layer) {
+    if (!m.q || !m.scales) return fail(STAGE_E_INVALID, std::string(name) + " of layer " + std::to_string(layer) + " is NULL");
+    if (m.n != n || m.k != k)
+        return fail(STAGE_E_SHAPE, std::string(name) + " of layer " + std::to_string(layer) + " is [" + std::to_string(m.n) +
+                                       ", " + std::to_string(m.k) + "], expected [" + std::to_string(n) + ", " +
+                                       std::to_string(k) + "]");
+    return STAGE_OK;
+}
+
+int check_config(const StageConfig* c) {
+    if (!c) return fail(STAGE_E_INVALID, "config is NULL");
+    if (c->n_layers < 1 || c->hidden < 2 || c->n_q_heads < 1 || c->n_kv_heads < 1 || c->ffn < 2 || c->max_positions < 1)
+        return fail(STAGE_E_INVALID, "non-positive dimension in config");
+    if (c->hidden % 2 || c->ffn % 2) return fail(STAGE_E_UNSUPPORTED, "hidden and ffn must be even");
+    if (c->head_dim != 64 && c->head_dim != 128) return fail(STAGE_E_UNSUPPORTED, "head_dim must be 64 or 128");
+    if (c->n_q_heads % c->n_kv_heads) return fail(STAGE_E_INVALID, "n_q_heads must be a multiple of n_kv_heads");
+    if (c->group_size < 32 || c->group_size % 32) return fail(STAGE_E_UNSUPPORTED, "group_size must be a multiple of 32");
+    if ((c->act_dtype != STAGE_DTYPE_F16 && c->act_dtype != STAGE_DTYPE_BF16) ||
+        (c->kv_dtype != STAGE_DTYPE_F16 && c->kv_dtype != STAGE_DTYPE_BF16))
+        return fail(STAGE_E_INVALID, "act_dtype and kv_dtype must be STAGE_DTYPE_F16 or STAGE_DTYPE_BF16");
+    if (!(c->rms_eps > 0.f)) return fail(STAGE_E_INVALID, "rms_eps must be positive");
+    if (!c->rope_cos_sin && !(c->rope_theta > 0.0)) return fail(STAGE_E_INVALID, "rope_theta must be positive");
+    return STAGE_OK;
+}
+
+int ensure_meta(Stage* st, size_t bytes) {
+    if (bytes <= st->meta_cap) return STAGE_OK;
+    size_t cap = std::max<size_t>(bytes, 2 * st->meta_cap);
+    cap = std::max<size_t>(cap, 1 << 16);
+    HIP_TRY(hipDeviceSynchronize());   // old buffers may still be read by queued work
+    if (st->meta_dev) HIP_TRY(hipFree(st->meta_dev));
+    st->meta_dev = nullptr;
+    for (int i = 0; i < META_RING; ++i) {
+        if (st->meta_host[i]) HIP_TRY(hipHostFree(st->meta_host[i]));
+        st->meta_host[i] = nullptr;
+        st->meta_ev_used[i] = false;
+    }
+    if (hipMalloc(&st->meta_dev, cap) != hipSuccess) {
+        (void)hipGetLastError();
+        st->meta_cap = 0;
+        return fail(STAGE_E_OOM, "metadata allocation failed");
+    }
+    for (int i = 0; i < META_RING; ++i) {
+        if (hipHostMalloc(&st->meta_host[i], cap, hipHostMallocDefault) != hipSuccess) {
+            (void)hipGetLastError();
+            st->meta_cap = 0;
+            return fail(STAGE_E_OOM, "pinned metadata allocation failed");
+        }
+    }
+    st->meta_cap = cap;
+    return STAGE_OK;
+}
+
+}  // namespace
+
+// ====================================================================== C ABI
+
+extern "C" {
+
+const char* stage_last_error(void) { return g_err.c_str(); }
+
+int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights_on_device, void* stream, Stage** out) {
+    if (!out) return fail(STAGE_E_INVALID, "out is NULL");
+    *out = nullptr;
+    int rc = check_config(cfg);
+    if (rc) return rc;
+    if (!layers) return fail(STAGE_E_INVALID, "layers is NULL");
+    const StageConfig& c = *cfg;
+    const int H = c.hidden, D = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
+    const int QD = Hq * D, KVD = Hkv * D;
+    for (int l = 0; l < c.n_layers; ++l) {
+        const LayerWeights& w = layers[l];
+        if (!w.attn_norm || !w.ffn_norm) return fail(STAGE_E_INVALID, "norm weight of layer " + std::to_string(l) + " is NULL");
+        if ((rc = check_mat(w.wq, QD, H, "wq", l)) || (rc = check_mat(w.wk, KVD, H, "wk", l)) ||
+            (rc = check_mat(w.wv, KVD, H, "wv", l)) || (rc = check_mat(w.wo, H, QD, "wo", l)) ||
+            (rc = check_mat(w.wg, F, H, "wg", l)) || (rc = check_mat(w.wu, F, H, "wu", l)) ||
+            (rc = check_mat(w.wd, H, F, "wd", l)))
+            return rc;
+    }
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    hipStream_t s = (hipStream_t)stream;
+
+    Stage* st = new Stage();
+    st->cfg = c;
+    st->cfg.rope_cos_sin = nullptr;
+    st->device = dev;
+    st->layers.resize(c.n_layers);
+
+    auto cleanup = [&](int code) {
+        delete st;
+        return code;
+    };
+
+    const int nqkv = QD + 2 * KVD;
+    const int g = c.group_size;
+    size_t max_q = 0, max_s = 0;
+    auto upd = [&](int n, int k) {
+        max_q = std::max(max_q, (size_t)n * ((k + 1) / 2));
+        max_s = std::max(max_s, (size_t)n * ((k + g - 1) / g));
+    };
+    upd(QD, H); upd(KVD, H); upd(H, QD); upd(F, H); upd(H, F);
+    uint8_t* tmp_q = nullptr;
+    uint16_t* tmp_s = nullptr;
+    if (!weights_on_device) {
+        if (hipMalloc(&tmp_q, max_q) != hipSuccess || hipMalloc(&tmp_s, max_s * 2) != hipSuccess) {
+            (void)hipGetLastError();
+            if (tmp_q) (void)hipFree(tmp_q);
+            return cleanup(fail(STAGE_E_OOM, "staging allocation failed"));
+        }
+    }
+    auto free_tmp = [&]() {
+        if (tmp_q) (void)hipFree(tmp_q);
+        if (tmp_s) (void)hipFree(tmp_s);
+    };
+
+    for (int l = 0; l < c.n_layers; ++l) {
+        LayerDev& L = st->layers[l];
+        const LayerWeights& w = layers[l];
+        if ((rc = make_mat(st, L.qkv, (nqkv + 63) / 64, H, g)) || (rc = make_mat(st, L.o, (H + 63) / 64, QD, g)) ||
+            (rc = make_mat(st, L.gu, (F + 31) / 32, H, g)) || (rc = make_mat(st, L.d, (H + 63) / 64, F, g))) {
+            free_tmp();
+            return cleanup(rc);
+        }
+        L.qkv.pm.n = nqkv;
+        L.o.pm.n = H;
+        L.gu.pm.n = 2 * F;
+        L.d.pm.n = H;
+        if ((rc = upload_mat(st, L.qkv, w.wq, weights_on_device, 0, 0, tmp_q, tmp_s, s)) ||
+            (rc = upload_mat(st, L.qkv, w.wk, weights_on_device, QD, 0, tmp_q, tmp_s, s)) ||
+            (rc = upload_mat(st, L.qkv, w.wv, weights_on_device, QD + KVD, 0, tmp_q, tmp_s, s)) ||
+            (rc = upload_mat(st, L.o, w.wo, weights_on_device, 0, 0, tmp_q, tmp_s, s)) ||
+            (rc = upload_mat(st, L.gu, w.wg, weights_on_device, 0, 1, tmp_q, tmp_s, s)) ||
+            (rc = upload_mat(st, L.gu, w.wu, weights_on_device, 0, 2, tmp_q, tmp_s, s)) ||
+            (rc = upload_mat(st, L.d, w.wd, weights_on_device, 0, 0, tmp_q, tmp_s, s))) {
+            free_tmp();
+            return cleanup(rc);
+        }
+        if ((rc = st->alloc(&L.attn_norm, H)) || (rc = st->alloc(&L.ffn_norm, H))) {
+            free_tmp();
+            return cleanup(rc);
+        }
+        const hipMemcpyKind kind = weights_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+        if (hipMemcpyAsync(L.attn_norm, w.attn_norm, (size_t)H * 2, kind, s) != hipSuccess ||
+            hipMemcpyAsync(L.ffn_norm, w.ffn_norm, (size_t)H * 2, kind, s) != hipSuccess) {
+            free_tmp();
+            return cleanup(fail(STAGE_E_HIP, "norm weight copy failed"));
+        }
+        st->weight_bytes += 4 * (int64_t)H;
+    }
+    if (hipStreamSynchronize(s) != hipSuccess) {
+        free_tmp();
+        return cleanup(fail(STAGE_E_HIP, std::string("weight upload: ") + hipGetErrorString(hipGetLastError())));
+    }
+    free_tmp();
+
+    // rotary table: cos/sin(p * theta^(-2i/D)) in fp64, stored fp32
+    const size_t nrope = (size_t)c.max_positions * (D / 2);
+    std::vector<float2> rope(nrope);
+    if (cfg->rope_cos_sin) {
+        for (size_t i = 0; i < nrope; ++i) rope[i] = make_float2(cfg->rope_cos_sin[2 * i], cfg->rope_cos_sin[2 * i + 1]);
+    } else {
+        for (int p = 0; p < c.max_positions; ++p)
+            for (int i = 0; i < D / 2; ++i) {
+                const double inv = std::pow(c.rope_theta, -(2.0 * i) / D);
+                const double phi = (double)p * inv;
+                rope[(size_t)p * (D / 2) + i] = make_float2((float)std::cos(phi), (float)std::sin(phi));
+            }
+    }
+    if ((rc = st->alloc(&st->rope, nrope))) return cleanup(rc);
+    if (hipMemcpy(st->rope, rope.data(), nrope * sizeof(float2), hipMemcpyHostToDevice) != hipSuccess)
+        return cleanup(fail(STAGE_E_HIP, "rope upload failed"));
+
+    // workspace
+    st->ntiles_h = (H + 63) / 64;
+    size_t gpart = 0;
+    unsigned max_tiles = 0;
+    for (auto& L : st->layers)
+        for (DevMat* m : {&L.qkv, &L.o, &L.gu, &L.d}) {
+            gpart = std::max(gpart, (size_t)m->ksplit * GEMV_MAX_M * m->pm.ntiles * 64);
+            max_tiles = std::max<unsigned>(max_tiles, m->pm.ntiles);
+        }
+    if ((rc = st->alloc(&st->x, (size_t)MAX_ROWS * H)) || (rc = st->alloc(&st->qkv, (size_t)MAX_ROWS * nqkv)) ||
+        (rc = st->alloc(&st->attn, (size_t)MAX_ROWS * QD)) || (rc = st->alloc(&st->act, (size_t)MAX_ROWS * F)) ||
+        (rc = st->alloc(&st->ssq, (size_t)MAX_ROWS * st->ntiles_h)) || (rc = st->alloc(&st->gpart, gpart)) ||
+        (rc = st->alloc(&st->apart, (size_t)MAX_ROWS * Hq * ATTN_MAX_SPLITS * (D + 2))) ||
+        (rc = st->alloc(&st->gcnt, max_tiles)) || (rc = st->alloc(&st->acnt, (size_t)MAX_ROWS * Hkv)))
+        return cleanup(rc);
+    if (hipMemset(st->gcnt, 0, max_tiles * sizeof(unsigned)) != hipSuccess ||
+        hipMemset(st->acnt, 0, (size_t)MAX_ROWS * Hkv * sizeof(unsigned)) != hipSuccess)
+        return cleanup(fail(STAGE_E_HIP, "counter init failed"));
+    for (int i = 0; i < META_RING; ++i)
+        if (hipEventCreateWithFlags(&st->meta_ev[i], hipEventDisableTiming) != hipSuccess)
+            return cleanup(fail(STAGE_E_HIP, "event creation failed"));
+    if ((rc = ensure_meta(st, 1 << 16))) return cleanup(rc);
+    if (hipDeviceSynchronize() != hipSuccess) return cleanup(fail(STAGE_E_HIP, "stage_create synchronize failed"));
+    *out = st;
+    return STAGE_OK;
+}
+
+int stage_destroy(Stage* stage) {
+    if (!stage) return fail(STAGE_E_INVALID, "stage is NULL");
+    delete stage;
+    return STAGE_OK;
+}
+
+int64_t stage_weight_bytes(const Stage* stage) { return stage ? stage->weight_bytes : -1; }
+
+int kv_state_alloc(Stage* stage, int n_slots, int capacity, KVState** out) {
+    if (!stage || !out) return fail(STAGE_E_INVALID, "NULL argument");
+    *out = nullptr;
+    if (n_slots < 1 || capacity < 1) return fail(STAGE_E_INVALID, "n_slots and capacity must be positive");
+    if (n_slots > MAX_ROWS) return fail(STAGE_E_CAPACITY, "n_slots exceeds STAGE_MAX_ROWS");
+    const StageConfig& c = stage->cfg;
+    HIP_TRY(hipSetDevice(stage->device));
+    KVState* kv = new KVState();
+    kv->stage = stage;
+    kv->S = n_slots;
+    kv->cap = capacity;
+    const size_t elems = (size_t)c.n_layers * n_slots * c.n_kv_heads * capacity * c.head_dim;
+    if (hipMalloc(&kv->kc, elems * 2) != hipSuccess || hipMalloc(&kv->vc, elems * 2) != hipSuccess ||
+        hipMalloc(&kv->table[0], (size_t)n_slots * capacity * 2) != hipSuccess ||
+        hipMalloc(&kv->table[1], (size_t)n_slots * capacity * 2) != hipSuccess) {
+        (void)hipGetLastError();
+        if (kv->kc) (void)hipFree(kv->kc);
+        if (kv->vc) (void)hipFree(kv->vc);
+        if (kv->table[0]) (void)hipFree(kv->table[0]);
+        delete kv;
+        return fail(STAGE_E_OOM, "KV state allocation failed");
+    }
+    *out = kv;
+    return STAGE_OK;
+}
+
+int kv_state_free(KVState* kv) {
+    if (!kv) return fail(STAGE_E_INVALID, "state is NULL");
+    (void)hipSetDevice(kv->stage->device);
+    (void)hipDeviceSynchronize();
+    (void)hipFree(kv->kc);
+    (void)hipFree(kv->vc);
+    (void)hipFree(kv->table[0]);
+    (void)hipFree(kv->table[1]);
+    delete kv;
+    return STAGE_OK;
+}
+
+int kv_state_reset(KVState* kv) {
+    if (!kv) return fail(STAGE_E_INVALID, "state is NULL");
+    kv->P = 0;
+    return STAGE_OK;
+}
+
+int kv_length(const KVState* kv, int* length_out) {
+    if (!kv || !length_out) return fail(STAGE_E_INVALID, "NULL argument");
+    *length_out = kv->P;
+    return STAGE_OK;
+}
+
+int kv_truncate(KVState* kv, int new_len) {
+    if (!kv) return fail(STAGE_E_INVALID, "state is NULL");
+    if (new_len < 0 || new_len > kv->P) return fail(STAGE_E_INVALID, "new_len must be in [0, P]");
+    kv->P = new_len;
+    return STAGE_OK;
+}
+
+int kv_append(KVState* kv, const void* k, const void* v, int n_tokens, int on_device, void* stream) {
+    if (!kv || !k || !v) return fail(STAGE_E_INVALID, "NULL argument");
+    if (n_tokens < 1) return fail(STAGE_E_INVALID, "n_tokens must be positive");
+    if (kv->P + n_tokens > kv->cap) return fail(STAGE_E_CAPACITY, "append exceeds the state's capacity");
+    Stage* st = kv->stage;
+    const StageConfig& c = st->cfg;
+    HIP_TRY(hipSetDevice(st->device));
+    hipStream_t s = (hipStream_t)stream;
+    const size_t bytes = (size_t)c.n_layers * kv->S * c.n_kv_heads * n_tokens * c.head_dim * 2;
+    const uint16_t* kd = (const uint16_t*)k;
+    const uint16_t* vd = (const uint16_t*)v;
+    void* tmp = nullptr;
+    if (!on_device) {
+        if (hipMalloc(&tmp, 2 * bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(STAGE_E_OOM, "staging allocation failed");
+        }
+        if (hipMemcpyAsync(tmp, k, bytes, hipMemcpyHostToDevice, s) != hipSuccess ||
+            hipMemcpyAsync((uint8_t*)tmp + bytes, v, bytes, hipMemcpyHostToDevice, s) != hipSuccess) {
+            (void)hipFree(tmp);
+            return fail(STAGE_E_HIP, "kv_append upload failed");
+        }
+        kd = (const uint16_t*)tmp;
+        vd = (const uint16_t*)((uint8_t*)tmp + bytes);
+    }
+    hipError_t e = launch_kv_append(kv->kc, kv->vc, kv->table[kv->cur], kd, vd, c.n_layers, kv->S, c.n_kv_heads, kv->cap,
+                                    c.head_dim, kv->P, n_tokens, s);
+    if (tmp) {
+        hipError_t e2 = hipStreamSynchronize(s);
+        (void)hipFree(tmp);
+        if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("kv_append: ") + hipGetErrorString(e));
+    kv->P += n_tokens;
+    return STAGE_OK;
+}
+
+int kv_read(KVState* kv, int layer, int slot, int start, int count, void* k_out, void* v_out, int out_on_device,
+            void* stream) {
+    if (!kv || !k_out || !v_out) return fail(STAGE_E_INVALID, "NULL argument");
+    Stage* st = kv->stage;
+    const StageConfig& c = st->cfg;
+    if (layer < 0 || layer >= c.n_layers || slot < 0 || slot >= kv->S) return fail(STAGE_E_INVALID, "layer or slot out of range");
+    if (start < 0 || count < 0 || start + count > kv->P) return fail(STAGE_E_INVALID, "row range exceeds P");
+    if (count == 0) return STAGE_OK;
+    HIP_TRY(hipSetDevice(st->device));
+    hipStream_t s = (hipStream_t)stream;
+    const size_t bytes = (size_t)c.n_kv_heads * count * c.head_dim * 2;
+    uint16_t* kd = (uint16_t*)k_out;
+    uint16_t* vd = (uint16_t*)v_out;
+    void* tmp = nullptr;
+    if (!out_on_device) {
+        if (hipMalloc(&tmp, 2 * bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(STAGE_E_OOM, "staging allocation failed");
+        }
+        kd = (uint16_t*)tmp;
+        vd = (uint16_t*)((uint8_t*)tmp + bytes);
+    }
+    hipError_t e = launch_kv_read(kv->kc, kv->vc, kv->table[kv->cur], layer, slot, start, count, kv->S, c.n_kv_heads,
+                                  kv->cap, c.head_dim, kd, vd, s);
+    if (tmp) {
+        if (e == hipSuccess) e = hipMemcpyAsync(k_out, kd, bytes, hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipMemcpyAsync(v_out, vd, bytes, hipMemcpyDeviceToHost, s);
+        hipError_t e2 = hipStreamSynchronize(s);
+        (void)hipFree(tmp);
+        if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("kv_read: ") + hipGetErrorString(e));
+    return STAGE_OK;
+}
+
+int stage_debug_dequant(Stage* stage, int layer, int which, float* out_host) {
+    if (!stage || !out_host) return fail(STAGE_E_INVALID, "NULL argument");
+    const StageConfig& c = stage->cfg;
+    if (layer < 0 || layer >= c.n_layers || which < 0 || which > 6) return fail(STAGE_E_INVALID, "layer or matrix index out of range");
+    HIP_TRY(hipSetDevice(stage->device));
+    const LayerDev& L = stage->layers[layer];
+    const int QD = c.n_q_heads * c.head_dim, KVD = c.n_kv_heads * c.head_dim;
+    const PackedMat* m = nullptr;
+    int off = 0, map = 0, rows = 0;
+    switch (which) {
+        case 0: m = &L.qkv.pm; off = 0; rows = QD; break;
+        case 1: m = &L.qkv.pm; off = QD; rows = KVD; break;
+        case 2: m = &L.qkv.pm; off = QD + KVD; rows = KVD; break;
+        case 3: m = &L.o.pm; rows = c.hidden; break;
+        case 4: m = &L.gu.pm; map = 1; rows = c.ffn; break;
+        case 5: m = &L.gu.pm; map = 2; rows = c.ffn; break;
+        default: m = &L.d.pm; rows = c.hidden; break;
+    }
+    float* tmp = nullptr;
+    const size_t bytes = (size_t)rows * m->k * sizeof(float);
+    if (hipMalloc(&tmp, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(STAGE_E_OOM, "staging allocation failed");
+    }
+    hipError_t e = launch_dequant(*m, off, map, rows, tmp, nullptr);
+    if (e == hipSuccess) e = hipMemcpy(out_host, tmp, bytes, hipMemcpyDeviceToHost);
+    (void)hipFree(tmp);
+    if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("debug dequant: ") + hipGetErrorString(e));
+    return STAGE_OK;
+}
+
+int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hidden_in, void* hidden_out, void* stream) {
+    if (!st || !reqs || !hidden_in || !hidden_out) return fail(STAGE_E_INVALID, "NULL argument");
+    if (n_req < 1) return fail(STAGE_E_INVALID, "n_req must be positive");
+    const StageConfig& c = st->cfg;
+    const int H = c.hidden, D = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
+    const int gs = Hq / Hkv;
+
+    // ---------------- validation (no side effects)
+    int M = 0, n_items = 0, max_rows_item = 0;
+    size_t mask_bytes = 0, beam_ints = 0;
+    for (int r = 0; r < n_req; ++r) {
+        const StageRequest& q = reqs[r];
+        const std::string who = "request " + std::to_string(r) + ": ";
+        if (!q.state) return fail(STAGE_E_INVALID, who + "state is NULL");
+        if (q.state->stage != st) return fail(STAGE_E_STATE_MISMATCH, who + "state belongs to another stage");
+        for (int r2 = 0; r2 < r; ++r2)
+            if (reqs[r2].state == q.state) return fail(STAGE_E_STATE_MISMATCH, who + "state used twice in one forward");
+        const int S = q.state->S, n = q.n_tokens, P = q.state->P;
+        if (n < 1) return fail(STAGE_E_INVALID, who + "n_tokens must be positive");
+        if (!q.positions || !q.attention_mask) return fail(STAGE_E_INVALID, who + "positions and attention_mask are required");
+        if (q.mask_len != P + n)
+            return fail(STAGE_E_SHAPE, who + "mask_len " + std::to_string(q.mask_len) + " != P + n = " + std::to_string(P + n));
+        if (P + n > q.state->cap) return fail(STAGE_E_CAPACITY, who + "P + n exceeds the state's capacity");
+        for (int i = 0; i < S * n; ++i)
+            if (q.positions[i] < 0 || q.positions[i] >= c.max_positions)
+                return fail(STAGE_E_CAPACITY, who + "position " + std::to_string(q.positions[i]) + " outside the rotary table");
+        if (q.beam_idx)
+            for (int b = 0; b < S; ++b)
+                if (q.beam_idx[b] < 0 || q.beam_idx[b] >= S) return fail(STAGE_E_INVALID, who + "beam_idx out of range");
+        for (int b = 0; b < S; ++b) {
+            const uint8_t* mk = q.attention_mask + (size_t)b * q.mask_len;
+            int first = -1;
+            for (int j = 0; j < P + n; ++j)
+                if (mk[j]) { first = j; break; }
+            if (first < 0 || first > P)   // query 0 sees rows 0..P; later queries see more
+                return fail(STAGE_E_INVALID, who + "slot " + std::to_string(b) + " has a query row with no visible key");
+        }
+        M += S * n;
+        n_items += S;
+        max_rows_item = std::max(max_rows_item, gs * n);
+        mask_bytes += (size_t)S * q.mask_len;
+        if (q.beam_idx) beam_ints += S;
+    }
+    if (M > MAX_ROWS) return fail(STAGE_E_CAPACITY, "total rows " + std::to_string(M) + " exceed STAGE_MAX_ROWS");
+    if ((const uint8_t*)hidden_in < (const uint8_t*)hidden_out + (size_t)M * H * 2 &&
+        (const uint8_t*)hidden_out < (const uint8_t*)hidden_in + (size_t)M * H * 2)
+        return fail(STAGE_E_INVALID, "hidden_in and hidden_out overlap");
+
+    HIP_TRY(hipSetDevice(st->device));
+    hipStream_t s = (hipStream_t)stream;
+
+    // ---------------- metadata into a pinned ring slot, one H2D copy
+    const size_t off_req = 0;
+    const size_t off_item = align16(off_req + sizeof(ReqDev) * n_req);
+    const size_t off_pos = align16(off_item + sizeof(ItemDev) * n_items);
+    const size_t off_beam = align16(off_pos + sizeof(int) * M);
+    const size_t off_mask = align16(off_beam + sizeof(int) * beam_ints);
+    const size_t total = align16(off_mask + mask_bytes);
+    int rc = ensure_meta(st, total);
+    if (rc) return rc;
+    const int slot_i = st->ring_i;
+    st->ring_i = (st->ring_i + 1) % META_RING;
+    if (st->meta_ev_used[slot_i]) HIP_TRY(hipEventSynchronize(st->meta_ev[slot_i]));
+    uint8_t* hb = st->meta_host[slot_i];
+    ReqDev* rd = (ReqDev*)(hb + off_req);
+    ItemDev* id = (ItemDev*)(hb + off_item);
+    int* pos = (int*)(hb + off_pos);
+    int* beam = (int*)(hb + off_beam);
+    uint8_t* masks = hb + off_mask;
+    std::vector<int> beam_off(n_req, -1);
+    std::vector<bool> do_gather(n_req, false);
+    {
+        int row = 0, item = 0;
+        size_t moff = 0, boff = 0;
+        for (int r = 0; r < n_req; ++r) {
+            const StageRequest& q = reqs[r];
+            KVState* kv = q.state;
+            const int S = kv->S, n = q.n_tokens;
+            bool ident = true;
+            if (q.beam_idx)
+                for (int b = 0; b < S; ++b) ident = ident && (q.beam_idx[b] == b);
+            do_gather[r] = !ident && kv->P > 0;
+            if (q.beam_idx) {
+                beam_off[r] = (int)boff;
+                std::memcpy(beam + boff, q.beam_idx, sizeof(int) * S);
+                boff += S;
+            }
+            ReqDev& d = rd[r];
+            d.P = kv->P;
+            d.n = n;
+            d.S = S;
+            d.row0 = row;
+            d.cap = kv->cap;
+            d.mask_off = (int)moff;
+            d.mask_len = q.mask_len;
+            d.item0 = item;
+            d.kc = kv->kc;
+            d.vc = kv->vc;
+            d.table = kv->table[do_gather[r] ? 1 - kv->cur : kv->cur];
+            for (int b = 0; b < S; ++b) id[item + b] = ItemDev{r, b};
+            std::memcpy(pos + row, q.positions, sizeof(int) * S * n);
+            std::memcpy(masks + moff, q.attention_mask, (size_t)S * q.mask_len);
+            row += S * n;
+            item += S;
+            moff += (size_t)S * q.mask_len;
+        }
+    }
+    uint8_t* db = st->meta_dev;
+    HIP_TRY(hipMemcpyAsync(db, hb, total, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipEventRecord(st->meta_ev[slot_i], s));
+    st->meta_ev_used[slot_i] = true;
+
+    // ---------------- beam reorder of the index tables (rows are never copied)
+    for (int r = 0; r < n_req; ++r) {
+        if (!do_gather[r]) continue;
+        KVState* kv = reqs[r].state;
+        HIP_TRY(launch_table_gather(kv->table[kv->cur], kv->table[1 - kv->cur], (const int*)(db + off_beam) + beam_off[r],
+                                    kv->S, kv->cap, kv->P, s));
+    }
+
+    MetaDev meta;
+    meta.reqs = (const ReqDev*)(db + off_req);
+    meta.items = (const ItemDev*)(db + off_item);
+    meta.positions = (const int*)(db + off_pos);
+    meta.masks = db + off_mask;
+    meta.n_items = n_items;
+    meta.M = M;
+
+    const int act_dt = dt_code(c.act_dtype);
+    const int nqkv = Hq * D + 2 * Hkv * D;
+    auto run_gemv = [&](const DevMat& m, GemvArgs a, size_t in_row_elems, size_t out_row_elems, size_t resid_row_elems,
+                        int in_elem_bytes, int resid_elem_bytes) -> hipError_t {
+        a.W = m.pm;
+        a.ksplit = m.ksplit;
+        a.cps = m.cps;
+        a.partial = st->gpart;
+        a.counters = st->gcnt;
+        for (int m0 = 0; m0 < M; m0 += GEMV_MAX_M) {
+            GemvArgs b = a;
+            b.M = std::min(GEMV_MAX_M, M - m0);
+            b.in = (const uint8_t*)a.in + (size_t)m0 * in_row_elems * in_elem_bytes;
+            b.out = a.out + (size_t)m0 * out_row_elems;
+            if (a.resid) b.resid = (const uint8_t*)a.resid + (size_t)m0 * resid_row_elems * resid_elem_bytes;
+            if (a.ssq_in) b.ssq_in = a.ssq_in + (size_t)m0 * a.ssq_tiles;
+            if (a.ssq_out) b.ssq_out = a.ssq_out + (size_t)m0 * m.pm.ntiles;
+            if (a.out_act) b.out_act = (uint8_t*)a.out_act + (size_t)m0 * a.out_act_ld * 2;
+            hipError_t e = launch_gemv(b, s);
+            if (e != hipSuccess) return e;
+        }
+        return hipSuccess;
+    };
+
+    for (int l = 0; l < c.n_layers; ++l) {
+        const LayerDev& Ld = st->layers[l];
+        const bool first = (l == 0), last = (l == c.n_layers - 1);
+        // q|k|v = RMSNorm(x) W_qkv^T
+        {
+            GemvArgs a{};
+            a.in = first ? hidden_in : (const void*)st->x;
+            a.in_dt = first ? act_dt : DT_F32;
+            a.in_ld = H;
+            a.gamma = Ld.attn_norm;
+            a.gamma_dt = act_dt;
+            a.rms = first ? RMS_FULLROW : RMS_PARTIALS;
+            a.eps = c.rms_eps;
+            a.ssq_in = first ? nullptr : st->ssq;
+            a.ssq_tiles = st->ntiles_h;
+            a.epi = EPI_STORE;
+            a.out = st->qkv;
+            a.out_ld = nqkv;
+            HIP_TRY(run_gemv(Ld.qkv, a, H, nqkv, 0, first ? 2 : 4, 0));
+        }
+        // attention (rotary, append, mask, online softmax, split merge)
+        {
+            AttnArgs a{};
+            a.qkv = st->qkv;
+            a.qkv_ld = nqkv;
+            a.out = st->attn;
+            a.out_ld = Hq * D;
+            a.meta = meta;
+            a.rope = st->rope;
+            a.layer = l;
+            a.Hq = Hq;
+            a.Hkv = Hkv;
+            a.kv_dt = dt_code(c.kv_dtype);
+            a.qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
+            a.part = st->apart;
+            a.counters = st->acnt;
+            a.nsplit_max = ATTN_MAX_SPLITS;
+            if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, atoi(e)));
+            HIP_TRY(launch_attention(a, D, max_rows_item, s));
+        }
+        // x = residual + o W_o^T
+        {
+            GemvArgs a{};
+            a.in = st->attn;
+            a.in_dt = DT_F32;
+            a.in_ld = Hq * D;
+            a.rms = RMS_NONE;
+            a.epi = EPI_RESID;
+            a.out = st->x;
+            a.out_ld = H;
+            a.resid = first ? hidden_in : (const void*)st->x;
+            a.resid_dt = first ? act_dt : DT_F32;
+            a.resid_ld = H;
+            a.ssq_out = st->ssq;
+            HIP_TRY(run_gemv(Ld.o, a, Hq * D, H, H, 4, first ? 2 : 4));
+        }
+        // act = silu(h2 W_g^T) * (h2 W_u^T), h2 = RMSNorm(x)
+        {
+            GemvArgs a{};
+            a.in = st->x;
+            a.in_dt = DT_F32;
+            a.in_ld = H;
+            a.gamma = Ld.ffn_norm;
+            a.gamma_dt = act_dt;
+            a.rms = RMS_PARTIALS;
+            a.eps = c.rms_eps;
+            a.ssq_in = st->ssq;
+            a.ssq_tiles = st->ntiles_h;
+            a.epi = EPI_SWIGLU;
+            a.out = st->act;
+            a.out_ld = F;
+            a.n_valid = F;
+            HIP_TRY(run_gemv(Ld.gu, a, H, F, 0, 4, 0));
+        }
+        // x = x + act W_d^T  (last layer also writes hidden_out)
+        {
+            GemvArgs a{};
+            a.in = st->act;
+            a.in_dt = DT_F32;
+            a.in_ld = F;
+            a.rms = RMS_NONE;
+            a.epi = EPI_RESID;
+            a.out = st->x;
+            a.out_ld = H;
+            a.resid = st->x;
+            a.resid_dt = DT_F32;
+            a.resid_ld = H;
+            a.ssq_out = st->ssq;
+            if (last) {
+                a.out_act = hidden_out;
+                a.out_act_dt = act_dt;
+                a.out_act_ld = H;
+            }
+            HIP_TRY(run_gemv(Ld.d, a, F, H, H, 4, 4));
+        }
+    }
+
+    // ---------------- commit host-side state
+    for (int r = 0; r < n_req; ++r) {
+        KVState* kv = reqs[r].state;
+        if (do_gather[r]) kv->cur = 1 - kv->cur;
+        kv->P += reqs[r].n_tokens;
+    }
+    return STAGE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,193 @@
+"""Python binding of libstage: argument marshalling only.
+
+Every step of the forward runs in the HIP kernels of libstage.so; torch is used
+for device buffers (``data_ptr``) and for the current HIP stream.
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import _lib
+from ._lib import check
+
+MATRIX_NAMES = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
+_DT = {"f16": _lib.DTYPE_F16, "bf16": _lib.DTYPE_BF16}
+_TORCH = {"f16": torch.float16, "bf16": torch.bfloat16}
+
+
+def _stream_ptr(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def _ptr(a) -> int:
+    if isinstance(a, torch.Tensor):
+        return a.data_ptr()
+    return a.ctypes.data
+
+
+class Stage:
+    """One pipeline stage on the current GPU.
+
+    ``shape`` provides n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn,
+    group_size, rms_eps, rope_theta, act_dtype ('f16'|'bf16'), kv_dtype,
+    max_positions.  ``layers[l]`` provides ``attn_norm``/``ffn_norm`` (torch
+    tensors in the act dtype) and ``mats[name]`` with ``q`` (uint8 [N, K/2]),
+    ``scales`` (float16 [N, K/G]), ``n``, ``k`` — host numpy arrays or device
+    torch tensors (``on_device=True``).
+    """
+
+    def __init__(self, shape, layers: Sequence, on_device: bool = False, stream=None):
+        self.lib = _lib.load()
+        self.shape = shape
+        cfg = _lib.StageConfig(
+            n_layers=shape.n_layers, hidden=shape.hidden, n_q_heads=shape.n_q_heads,
+            n_kv_heads=shape.n_kv_heads, head_dim=shape.head_dim, ffn=shape.ffn,
+            group_size=shape.group_size, rms_eps=shape.rms_eps, act_dtype=_DT[shape.act_dtype],
+            kv_dtype=_DT[shape.kv_dtype], rope_theta=shape.rope_theta,
+            max_positions=shape.max_positions, rope_cos_sin=None)
+        arr = (_lib.LayerWeights * shape.n_layers)()
+        keep = []
+        for l, lay in enumerate(layers):
+            an = lay.attn_norm.contiguous()
+            fn = lay.ffn_norm.contiguous()
+            if not on_device:
+                an, fn = an.cpu(), fn.cpu()
+            keep += [an, fn]
+            arr[l].attn_norm = an.data_ptr()
+            arr[l].ffn_norm = fn.data_ptr()
+            for name in MATRIX_NAMES:
+                m = lay.mats[name]
+                q, s = m.q, m.scales
+                if not on_device:
+                    q = np.ascontiguousarray(q, dtype=np.uint8)
+                    s = np.ascontiguousarray(s).view(np.uint16)
+                keep += [q, s]
+                setattr(arr[l], name, _lib.QuantMatrix(q=_ptr(q), scales=_ptr(s), n=m.n, k=m.k))
+        h = ctypes.c_void_p()
+        check(self.lib.stage_create(ctypes.byref(cfg), arr, int(on_device), ctypes.c_void_p(_stream_ptr(stream)),
+                                    ctypes.byref(h)))
+        self.handle = h
+        self.act_dtype = _TORCH[shape.act_dtype]
+        self.kv_dtype = _TORCH[shape.kv_dtype]
+
+    # ------------------------------------------------------------------
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            check(self.lib.stage_destroy(self.handle))
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def weight_bytes(self) -> int:
+        return int(self.lib.stage_weight_bytes(self.handle))
+
+    def new_state(self, n_slots: int, capacity: int) -> "KVState":
+        return KVState(self, n_slots, capacity)
+
+    def debug_dequant(self, layer: int, which: str) -> np.ndarray:
+        n, k = self.shape.matrix_shapes()[which]
+        out = np.empty((n, k), dtype=np.float32)
+        check(self.lib.stage_debug_dequant(self.handle, layer, MATRIX_NAMES.index(which), out.ctypes.data))
+        return out
+
+    def forward(self, requests: Sequence["Request"], hidden_in: torch.Tensor,
+                hidden_out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        """hidden_in: device [M, H] in the act dtype, rows request-major, then slot, then token."""
+        if hidden_out is None:
+            hidden_out = torch.empty_like(hidden_in)
+        arr = (_lib.StageRequest * len(requests))()
+        keep = []
+        for i, r in enumerate(requests):
+            pos = np.ascontiguousarray(r.positions, dtype=np.int32)
+            mask = np.ascontiguousarray(r.mask, dtype=np.uint8)
+            keep += [pos, mask]
+            beam = None
+            if r.beam_idx is not None:
+                beam = np.ascontiguousarray(r.beam_idx, dtype=np.int32)
+                keep.append(beam)
+            arr[i].state = r.state.handle
+            arr[i].n_tokens = int(r.n_tokens)
+            arr[i].positions = pos.ctypes.data
+            arr[i].beam_idx = beam.ctypes.data if beam is not None else None
+            arr[i].attention_mask = mask.ctypes.data
+            arr[i].mask_len = int(mask.shape[-1]) if mask.ndim else 0
+        check(self.lib.stage_forward(self.handle, arr, len(requests), ctypes.c_void_p(hidden_in.data_ptr()),
+                                     ctypes.c_void_p(hidden_out.data_ptr()), ctypes.c_void_p(_stream_ptr(stream))))
+        return hidden_out
+
+
+@dataclass
+class Request:
+    """One request of a forward: positions [S, n] int32, mask [S, P+n] uint8
+    (nonzero = visible), beam_idx [S] int32 or None."""
+
+    state: "KVState"
+    positions: np.ndarray
+    mask: np.ndarray
+    beam_idx: Optional[np.ndarray] = None
+
+    @property
+    def n_tokens(self) -> int:
+        return int(np.asarray(self.positions).shape[-1])
+
+
+class KVState:
+    def __init__(self, stage: Stage, n_slots: int, capacity: int):
+        self.stage = stage
+        self.lib = stage.lib
+        self.n_slots = n_slots
+        self.capacity = capacity
+        h = ctypes.c_void_p()
+        check(self.lib.kv_state_alloc(stage.handle, n_slots, capacity, ctypes.byref(h)))
+        self.handle = h
+
+    def free(self) -> None:
+        if getattr(self, "handle", None):
+            check(self.lib.kv_state_free(self.handle))
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+    @property
+    def length(self) -> int:
+        n = ctypes.c_int()
+        check(self.lib.kv_length(self.handle, ctypes.byref(n)))
+        return n.value
+
+    def reset(self) -> None:
+        check(self.lib.kv_state_reset(self.handle))
+
+    def truncate(self, new_len: int) -> None:
+        check(self.lib.kv_truncate(self.handle, int(new_len)))
+
+    def append(self, k: torch.Tensor, v: torch.Tensor, stream=None) -> None:
+        """k, v: [L][S][Hkv][n][D] in the KV dtype (host or device)."""
+        k = k.contiguous()
+        v = v.contiguous()
+        on_dev = int(k.is_cuda)
+        check(self.lib.kv_append(self.handle, ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(v.data_ptr()),
+                                 int(k.shape[3]), on_dev, ctypes.c_void_p(_stream_ptr(stream))))
+
+    def read(self, layer: int, slot: int, start: int, count: int, stream=None):
+        """Rows [start, start+count) of one layer and slot as the slot sees them: K, V [Hkv, count, D]."""
+        sh = self.stage.shape
+        k = torch.empty((sh.n_kv_heads, count, sh.head_dim), dtype=self.stage.kv_dtype, device="cuda")
+        v = torch.empty_like(k)
+        check(self.lib.kv_read(self.handle, layer, slot, start, count, ctypes.c_void_p(k.data_ptr()),
+                               ctypes.c_void_p(v.data_ptr()), 1, ctypes.c_void_p(_stream_ptr(stream))))
+        return k, v

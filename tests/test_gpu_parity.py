@@ -1,0 +1,308 @@
+"""HIP stage forward vs the fp64 oracle, and the paper's invariants on the GPU.
+
+Every call goes through the C ABI of libstage.so.  Tolerances: INT4 decode and
+gather indexing bit-exact; hidden_out max-abs-rel <= 2e-2 per stage forward;
+invariants that compare two GPU runs of the same kernels bitwise.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_cases import TOL_STAGE, Pair, full_mask, host, rel_err, req, run_gpu
+from oracle_cases import logical_positions
+from paper_2608_19147_amd import StageError
+
+pytestmark = pytest.mark.gpu
+
+TINY = synth.TINY
+TINY2 = synth.with_layers(synth.TINY, 2)
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    return Pair(TINY, 0)
+
+
+@pytest.fixture(scope="module")
+def tiny2():
+    return Pair(TINY2, 1)
+
+
+# ------------------------------------------------------------------ INT4 decode (bit-exact)
+
+def _forced_scales_layers(shape, seed):
+    layers = synth.make_weights(shape, seed)
+    for lay in layers:
+        for m in lay.mats.values():
+            b = m.scales.view(np.uint16)
+            b[0, 0] = 0x0001      # smallest fp16 subnormal
+            b[1, -1] = 0x03FF     # largest subnormal in the (ragged) last group
+            b[2, 0] = 0x8001      # negative subnormal
+            b[3, 0] = 0x0000
+    return layers
+
+
+def test_dequant_bitexact_tiny():
+    layers = _forced_scales_layers(TINY, 3)
+    p = Pair(TINY, layers=layers)
+    for name in synth.MATRICES:
+        m = layers[0].mats[name]
+        ref = oracle.dequant(m.q, m.scales, m.k, TINY.group_size)
+        got = p.gpu.debug_dequant(0, name)
+        assert np.array_equal(got.astype(np.float64), ref), name
+
+
+def test_dequant_bitexact_8b_layer():
+    shape = synth.with_layers(synth.LLAMA8B_HALF, 1)
+    layers = _forced_scales_layers(shape, 4)
+    p = Pair(shape, layers=layers)
+    for name in synth.MATRICES:
+        m = layers[0].mats[name]
+        ref = oracle.dequant(m.q, m.scales, m.k, shape.group_size)
+        got = p.gpu.debug_dequant(0, name)
+        assert np.array_equal(got.astype(np.float64), ref), name
+    del p
+
+
+# ------------------------------------------------------------------ tiny stage parity
+
+def test_tiny_decode(tiny):
+    P = 72
+    g, o = tiny.states(1, P, 128, seed=0)
+    x = synth.make_hidden(TINY, 1, 0, 1)
+    pos, mask = np.array([[P]]), full_mask(1, P + 1)
+    out = run_gpu(tiny, [req(g, pos, mask, [0])], x)
+    ref = oracle.forward(tiny.orc, o, host(x), pos, np.array([0]), mask)
+    assert rel_err(out, ref) <= TOL_STAGE
+    assert g.length == P + 1
+
+
+def test_tiny_verify_masked_then_decode(tiny):
+    """5-token verify with the last two drafts masked, then a decode on the
+    holed state vs the physically trimmed twin (mask rewind == trim)."""
+    P = 72
+    g, o = tiny.states(1, P, 128, seed=5)
+    gt, ot = tiny.states(1, P, 128, seed=5)                 # twin: will hold only accepted rows
+    x = synth.make_hidden(TINY, 5, 5, 1)
+    mask = full_mask(1, P + 5)
+    mask[0, P + 3:] = 0
+    pos = np.arange(P, P + 5)[None]
+    out = run_gpu(tiny, [req(g, pos, mask, [0])], x)
+    ref = oracle.forward(tiny.orc, o, host(x), pos, np.array([0]), mask)
+    assert rel_err(out, ref) <= TOL_STAGE
+    # twin: the same forward without the rejected drafts
+    out_t = run_gpu(tiny, [req(gt, pos[:, :3], full_mask(1, P + 3))], x[:3])
+    assert rel_err(out[:3], out_t) <= TOL_STAGE
+    # follow-up decode on the holed state (P+5 rows, two masked) vs the trimmed state (P+3 rows)
+    x2 = synth.make_hidden(TINY, 1, 5, 2)
+    mask2 = np.concatenate([mask, np.ones((1, 1), np.uint8)], axis=1)
+    pos2 = logical_positions(mask[0], 1)
+    assert pos2[0, 0] == P + 3
+    out2 = run_gpu(tiny, [req(g, pos2, mask2)], x2)
+    out2_t = run_gpu(tiny, [req(gt, pos2, full_mask(1, P + 4))], x2)
+    ref2 = oracle.forward(tiny.orc, o, host(x2), pos2, None, mask2)
+    assert rel_err(out2, ref2) <= TOL_STAGE
+    assert rel_err(out2, out2_t) <= TOL_STAGE
+
+
+def test_first_token_p0(tiny2):
+    g, o = tiny2.states(1, 0, 16)
+    x = synth.make_hidden(TINY2, 1, 7)
+    out = run_gpu(tiny2, [req(g, [[0]], full_mask(1, 1))], x)
+    ref = oracle.forward(tiny2.orc, o, host(x), np.array([[0]]))
+    assert rel_err(out, ref) <= TOL_STAGE
+
+
+def test_multistep_with_holes_and_beams(tiny2):
+    """Several verify steps on 3 slots: holes accumulate, beam_idx alternates
+    identity / permutation; every step vs the oracle."""
+    S, P0, n = 3, 40, 5
+    g, o = tiny2.states(S, P0, 128, seed=9)
+    valid = np.ones((S, P0), np.uint8)
+    r = np.random.default_rng(9)
+    for step in range(6):
+        beam = np.arange(S) if step % 2 == 0 else r.permutation(S)
+        valid = valid[beam]
+        mask = np.concatenate([valid, np.ones((S, n), np.uint8)], axis=1)
+        pos = logical_positions(valid, n)
+        x = synth.make_hidden(TINY2, S * n, 9, step)
+        out = run_gpu(tiny2, [req(g, pos, mask, beam)], x)
+        ref = oracle.forward(tiny2.orc, o, host(x), pos, beam, mask)
+        assert rel_err(out, ref) <= TOL_STAGE, step
+        acc = r.integers(0, n, S)                           # accepted drafts per slot
+        new = (np.arange(n)[None] <= acc[:, None]).astype(np.uint8)
+        valid = np.concatenate([valid, new], axis=1)
+
+
+# ------------------------------------------------------------------ invariants (GPU vs GPU)
+
+def test_identity_beam_equals_no_gather_bitwise(tiny2):
+    S, P = 3, 30
+    a, _ = tiny2.states(S, P, 64, seed=11, with_oracle=False)
+    b, _ = tiny2.states(S, P, 64, seed=11, with_oracle=False)
+    x = synth.make_hidden(TINY2, S * 2, 11)
+    pos = np.full((S, 2), P) + np.arange(2)
+    m = full_mask(S, P + 2)
+    oa = run_gpu(tiny2, [req(a, pos, m, np.arange(S))], x)
+    ob = run_gpu(tiny2, [req(b, pos, m, None)], x)
+    assert np.array_equal(oa, ob)
+
+
+def test_permuted_beam_equals_permuted_cache_bitwise(tiny2):
+    S, P = 3, 30
+    perm = np.array([2, 0, 2])
+    a, _ = tiny2.states(S, P, 64, seed=12, with_oracle=False)
+    src, _ = tiny2.states(S, P, 64, seed=12, with_oracle=False)
+    # b: rows physically permuted, built with kv_read -> kv_append
+    L, Hkv, D = TINY2.n_layers, TINY2.n_kv_heads, TINY2.head_dim
+    k = torch.empty((L, S, Hkv, P, D), dtype=torch.float16, device="cuda")
+    v = torch.empty_like(k)
+    for l in range(L):
+        for s in range(S):
+            k[l, s], v[l, s] = src.read(l, int(perm[s]), 0, P)
+    b = tiny2.gpu.new_state(S, 64)
+    b.append(k, v)
+    x = synth.make_hidden(TINY2, S, 12)
+    pos = np.full((S, 1), P)
+    m = full_mask(S, P + 1)
+    oa = run_gpu(tiny2, [req(a, pos, m, perm)], x)
+    ob = run_gpu(tiny2, [req(b, pos, m, None)], x)
+    assert np.array_equal(oa, ob)
+    # the reorder persists: next forward without beam_idx
+    x2 = synth.make_hidden(TINY2, S, 12, 1)
+    m2 = full_mask(S, P + 2)
+    assert np.array_equal(run_gpu(tiny2, [req(a, pos + 1, m2)], x2), run_gpu(tiny2, [req(b, pos + 1, m2)], x2))
+    # kv_read through the table returns the gathered rows bit-exactly
+    for l in range(L):
+        for s in range(S):
+            ka, va = a.read(l, s, 0, P)
+            kr, vr = src.read(l, int(perm[s]), 0, P)
+            assert torch.equal(ka, kr) and torch.equal(va, vr)
+
+
+def test_masked_rows_content_independent_bitwise(tiny2):
+    P = 50
+    a, _ = tiny2.states(1, P, 64, seed=13, with_oracle=False)
+    k, v = synth.make_kv(TINY2, 1, P, 13)
+    holes = np.ones(P, np.uint8)
+    holes[[0, 7, 8, 30, 49]] = 0
+    k2, v2 = k.clone(), v.clone()
+    idx = torch.from_numpy(np.flatnonzero(holes == 0))
+    k2[:, :, :, idx] = 1e4
+    v2[:, :, :, idx] = -1e4
+    b = tiny2.gpu.new_state(1, 64)
+    b.append(k2, v2)
+    mask = np.concatenate([holes, [1, 1]])[None]
+    pos = logical_positions(holes, 2)
+    x = synth.make_hidden(TINY2, 2, 13)
+    assert np.array_equal(run_gpu(tiny2, [req(a, pos, mask)], x), run_gpu(tiny2, [req(b, pos, mask)], x))
+
+
+def _mb_requests(pair, seed, pasts, ns, with_oracle=True):
+    out = []
+    for i, (past, n) in enumerate(zip(pasts, ns)):
+        g, o = pair.states(1, past, past + 8, seed=seed, stream=i, with_oracle=with_oracle)
+        holes = synth.hole_mask(past, 0.1, seed, i)
+        holes[-1] = 1
+        mask = np.concatenate([holes, np.ones(n, np.uint8)])[None]
+        out.append((g, o, logical_positions(holes, n), mask))
+    return out
+
+
+def test_microbatch_parity_and_isolation(tiny2):
+    pasts, ns = [17, 40, 9, 63], [1, 5, 2, 5]
+    rows = sum(ns)
+    x = synth.make_hidden(TINY2, rows, 21)
+    rq = _mb_requests(tiny2, 21, pasts, ns)
+    out = run_gpu(tiny2, [req(g, p, m) for g, _, p, m in rq], x)
+    ref = oracle.forward_batch(tiny2.orc, [dict(state=o, positions=p, mask=m) for _, o, p, m in rq], host(x))
+    assert rel_err(out, ref) <= TOL_STAGE
+    # request 1 alone (fresh states, same seeds) == its rows in the batch, bitwise
+    rq2 = _mb_requests(tiny2, 21, pasts, ns, with_oracle=False)
+    g, _, p, m = rq2[1]
+    alone = run_gpu(tiny2, [req(g, p, m)], x[1:6])
+    assert np.array_equal(alone, out[1:6])
+    # perturbing batch-mates leaves request 1 unchanged; perturbing it moves it
+    rq3 = _mb_requests(tiny2, 21, pasts, ns, with_oracle=False)
+    xm = x.clone()
+    xm[0] += 3
+    xm[6:] *= -1
+    assert np.array_equal(run_gpu(tiny2, [req(g, p, m) for g, _, p, m in rq3], xm)[1:6], out[1:6])
+    rq4 = _mb_requests(tiny2, 21, pasts, ns, with_oracle=False)
+    xo = x.clone()
+    xo[3] += 1
+    assert np.max(np.abs(run_gpu(tiny2, [req(g, p, m) for g, _, p, m in rq4], xo)[1:6] - out[1:6])) > 1e-3
+
+
+def test_request_permutation_bitwise(tiny2):
+    pasts, ns = [12, 25, 33], [2, 3, 1]
+    x = synth.make_hidden(TINY2, 6, 22)
+    a = _mb_requests(tiny2, 22, pasts, ns, with_oracle=False)
+    out = run_gpu(tiny2, [req(g, p, m) for g, _, p, m in a], x)
+    b = _mb_requests(tiny2, 22, pasts, ns, with_oracle=False)
+    order = [2, 0, 1]
+    xs = torch.cat([x[5:6], x[0:2], x[2:5]])
+    outp = run_gpu(tiny2, [req(*[b[i][j] for j in (0, 2, 3)]) for i in order], xs)
+    assert np.array_equal(outp, np.concatenate([out[5:6], out[0:2], out[2:5]]))
+
+
+def test_verify_equals_sequential_decodes(tiny2):
+    P = 30
+    a, _ = tiny2.states(1, P, 64, seed=23, with_oracle=False)
+    b, _ = tiny2.states(1, P, 64, seed=23, with_oracle=False)
+    x = synth.make_hidden(TINY2, 4, 23)
+    pos = np.arange(P, P + 4)[None]
+    ov = run_gpu(tiny2, [req(a, pos, full_mask(1, P + 4))], x)
+    od = np.concatenate([run_gpu(tiny2, [req(b, pos[:, i:i + 1], full_mask(1, P + i + 1))], x[i:i + 1]) for i in range(4)])
+    assert rel_err(ov, od) <= TOL_STAGE
+
+
+def test_gqa_as_mha_shape():
+    shape = synth.StageShape(**{**TINY.__dict__, "name": "tiny-mha", "n_kv_heads": TINY.n_q_heads})
+    p = Pair(shape, 24)
+    g, o = p.states(2, 20, 40, seed=24)
+    x = synth.make_hidden(shape, 4, 24)
+    pos = np.full((2, 2), 20) + np.arange(2)
+    m = full_mask(2, 22)
+    out = run_gpu(p, [req(g, pos, m)], x)
+    assert rel_err(out, oracle.forward(p.orc, o, host(x), pos, None, m)) <= TOL_STAGE
+
+
+# ------------------------------------------------------------------ ABI errors: all-or-nothing
+
+def test_errors_leave_state_unchanged(tiny):
+    P = 10
+    g, _ = tiny.states(2, P, 16, seed=30, with_oracle=False)
+    x = synth.make_hidden(TINY, 2, 30).cuda()
+    pos = np.full((2, 1), P)
+    good = full_mask(2, P + 1)
+    cases = []
+    cases.append((req(g, pos, full_mask(2, P)), "STAGE_E_SHAPE"))                  # mask_len != P + n
+    cases.append((req(g, pos, good, [0, 2]), "STAGE_E_INVALID"))                   # beam out of range
+    bad = good.copy()
+    bad[1, : P + 1] = 0
+    cases.append((req(g, pos, bad), "STAGE_E_INVALID"))                            # fully masked row
+    cases.append((req(g, np.full((2, 1), 10 ** 6), good), "STAGE_E_CAPACITY"))     # position beyond table
+    for r, code in cases:
+        with pytest.raises(StageError, match=code):
+            tiny.gpu.forward([r], x)
+        assert g.length == P
+    with pytest.raises(StageError, match="STAGE_E_CAPACITY"):                     # P + n > capacity
+        tiny.gpu.forward([req(g, np.full((2, 7), P) + np.arange(7), full_mask(2, P + 7))],
+                         synth.make_hidden(TINY, 14, 30).cuda())
+    with pytest.raises(StageError, match="STAGE_E_STATE_MISMATCH"):                # the same state twice
+        tiny.gpu.forward([req(g, pos, good), req(g, pos, good)], synth.make_hidden(TINY, 4, 30).cuda())
+    other = Pair(TINY, 31)
+    with pytest.raises(StageError, match="STAGE_E_STATE_MISMATCH"):                # state of another stage
+        other.gpu.forward([req(g, pos, good)], x)
+    assert g.length == P
+    with pytest.raises(StageError, match="STAGE_E_INVALID"):
+        g.truncate(P + 1)
+    # a fully masked *past* is fine when the new token sees itself
+    ok = good.copy()
+    ok[:, :P] = 0
+    tiny.gpu.forward([req(g, pos, ok)], x)
+    torch.cuda.synchronize()
+    assert g.length == P + 1
