@@ -1,0 +1,204 @@
+#!/usr/bin/env python3
+"""Stage decode throughput of the Llama-3.1-8B half stage on one MI355X.
+
+Workload: 16 Llama decoder layers (hidden 4096, 32/8 heads, head_dim 128,
+SwiGLU 14336) with INT4 group-128 weights and fp16 scales, bf16 activations
+and bf16 KV cache, batch 1, single-token decode over a KV cache of 2048 rows
+(also reported at 512), beam_idx = identity, all-ones mask.  A step is one
+stage_forward (every layer: RMSNorm, W4A16 q/k/v, rotary + KV append,
+split-KV attention, W4A16 o + residual, RMSNorm, W4A16 gate|up + SwiGLU,
+W4A16 down + residual) on hidden states already resident in HBM; the KV
+length is reset to the measured length after each step (metadata only).
+
+Prints one JSON line: tokens/s, algorithmic HBM bytes per step and the
+achieved fraction of the 8 TB/s HBM peak, the dominant kernel's roofline
+(timed with HIP events on its launch stream), and the fp64 CPU oracle timed
+on a bounded sample on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+DOMINANT = "gateup"
+
+
+def algorithmic_bytes(shape, kv_len: int, n_new: int = 1) -> dict:
+    """Each weight byte once (INT4 codes + fp16 scales + norm weights) plus each
+    KV row the step needs once per layer (the P cached rows and the new row)."""
+    w = shape.weight_bytes()
+    kv = shape.kv_bytes_per_token() * (kv_len + n_new)
+    return {"weights": w, "kv": kv, "total": w + kv}
+
+
+def gateup_bytes(shape) -> int:
+    """INT4 codes + fp16 scales of W_gate and W_up of one layer (one launch)."""
+    F, H, G = shape.ffn, shape.hidden, shape.group_size
+    return 2 * (F * (H // 2) + F * ((H + G - 1) // G) * 2)
+
+
+def cpu_baseline(shape, kv_len: int, layers_sampled: int, seed: int) -> dict:
+    """The fp64 oracle as it stands, streaming dequant per layer, on a bounded
+    sample: ``layers_sampled`` of the stage's layers for one decode step; the
+    per-step time is scaled to all layers."""
+    import numpy as np
+
+    import oracle
+    import synth
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        blas_threads = 1
+    sub = synth.with_layers(shape, layers_sampled)
+    layers = synth.make_weights(sub, seed)
+    ost = oracle.OracleStage(sub, layers, cache_weights=False)
+    state = oracle.OracleState(sub, 1, kv_len + 1)
+    k, v = synth.make_kv(sub, 1, kv_len, seed)
+    state.append(k.double().numpy(), v.double().numpy())
+    del k, v
+    x = synth.make_hidden(sub, 1, seed).double().numpy()
+    t0 = time.perf_counter()
+    oracle.forward(ost, state, x, np.array([[kv_len]]), np.array([0]), np.ones((1, kv_len + 1), np.uint8))
+    dt = time.perf_counter() - t0
+    step_s = dt * shape.n_layers / layers_sampled
+    return {
+        "value": round(1.0 / step_s, 5), "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
+        "sample": f"{layers_sampled} of {shape.n_layers} layers of one bs=1 decode step at KV {kv_len} "
+                  f"(fp64, per-layer streaming dequant) took {dt:.2f} s; scaled x{shape.n_layers / layers_sampled:g} "
+                  f"to a full step; BLAS threads {blas_threads}, elementwise numpy single-threaded",
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--kv", type=int, default=2048, help="KV length of the headline value")
+    ap.add_argument("--kv-also", type=int, default=512, help="second KV length reported (0 = none)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-layers", type=int, default=3, help="layers of the oracle sample (0 = skip)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
+              "this build has no multi-GPU path.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2608_19147_amd import Request, Stage
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    shape = synth.LLAMA8B_HALF
+    t0 = time.perf_counter()
+    layers = synth.make_weights(shape, args.seed)
+    stage = Stage(shape, layers)
+    del layers
+    kv_max = max(args.kv, args.kv_also)
+    state = stage.new_state(1, kv_max + 8)
+    k, v = synth.make_kv(shape, 1, kv_max, args.seed)
+    state.append(k, v)
+    del k, v
+    n_in = 8
+    xs = [synth.make_hidden(shape, 1, args.seed, 100 + i).cuda() for i in range(n_in)]
+    out = torch.empty_like(xs[0])
+    torch.cuda.synchronize()
+    print(f"# setup {time.perf_counter() - t0:.1f}s (weights {stage.weight_bytes() / 1e9:.3f} GB on device)",
+          file=sys.stderr, flush=True)
+
+    def run(kv_len: int, profile: bool):
+        state.truncate(kv_len)
+        req = Request(state, np.array([[kv_len]], np.int32), np.ones((1, kv_len + 1), np.uint8), np.array([0], np.int32))
+        for i in range(args.warmup):
+            stage.forward([req], xs[i % n_in], out)
+            state.truncate(kv_len)
+        torch.cuda.synchronize()
+        if profile:
+            stage.profile(DOMINANT)
+        t_start = time.perf_counter()
+        for i in range(args.steps):
+            stage.forward([req], xs[i % n_in], out)
+            state.truncate(kv_len)
+        torch.cuda.synchronize()
+        t_end = time.perf_counter()
+        prof = None
+        if profile:
+            prof = stage.profile_read()
+            stage.profile(None)
+        ms = (t_end - t_start) * 1e3 / args.steps
+        return ms, prof
+
+    ms_main, prof = run(args.kv, True)
+    ms_also = run(args.kv_also, False)[0] if args.kv_also else None
+    print(f"# decode kv={args.kv}: {ms_main:.4f} ms/step"
+          + (f"; kv={args.kv_also}: {ms_also:.4f} ms/step" if ms_also else ""), file=sys.stderr, flush=True)
+
+    b = algorithmic_bytes(shape, args.kv)
+    gbps = b["total"] / (ms_main * 1e-3) / 1e9
+    launches, prof_ms = prof
+    per_launch_ms = prof_ms / max(1, launches)
+    gu_bytes = gateup_bytes(shape)
+    gu_gbps = gu_bytes / (per_launch_ms * 1e-3) / 1e9
+    line = {
+        "metric": "stage decode tokens/s (8B half-stage, bs=1) + achieved HBM GB/s vs peak",
+        "value": round(1e3 / ms_main, 3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_main, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "w4a16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"llama3.1-8b half stage decode, bs=1, kv={args.kv}",
+            "layers": shape.n_layers, "hidden": shape.hidden, "q_heads": shape.n_q_heads,
+            "kv_heads": shape.n_kv_heads, "head_dim": shape.head_dim, "ffn": shape.ffn,
+            "group_size": shape.group_size, "kv_len": args.kv, "batch": 1, "act": "bf16", "kv_cache": "bf16",
+        },
+        "hbm_bytes_per_step": b["total"],
+        "achieved_gbps": round(gbps, 1),
+        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+        "roofline": {
+            "bound": "hbm", "kernel": "gemv_w4 gate|up (one launch per layer)",
+            "achieved": round(gu_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(gu_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+            "bytes_per_launch": gu_bytes, "avg_launch_us": round(per_launch_ms * 1e3, 3), "launches_timed": launches,
+        },
+    }
+    if ms_also:
+        bb = algorithmic_bytes(shape, args.kv_also)
+        g2 = bb["total"] / (ms_also * 1e-3) / 1e9
+        line["also"] = {"kv_len": args.kv_also, "tokens_per_s": round(1e3 / ms_also, 3), "ms_per_step": round(ms_also, 5),
+                        "hbm_bytes_per_step": bb["total"], "achieved_gbps": round(g2, 1),
+                        "hbm_frac": round(g2 / HBM_PEAK_GBPS, 4)}
+    state.free()
+    stage.close()
+    del xs, out
+    torch.cuda.empty_cache()
+    if args.cpu_layers > 0:
+        print("# timing the fp64 oracle sample on the host", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(shape, args.kv, args.cpu_layers, args.seed)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -56,8 +56,8 @@ extern "C" {
 #define STAGE_MAX_ROWS 64
 
 /* Model dimensions of the stage.  Requirements: head_dim in {64, 128};
- * n_q_heads a multiple of n_kv_heads; hidden, ffn and n_q_heads*head_dim
- * even; group_size a multiple of 32 (the paper's shards use 128). */
+ * n_q_heads a multiple of n_kv_heads; hidden and ffn multiples of 8;
+ * group_size a multiple of 32 (the paper's shards use 128). */
 typedef struct StageConfig {
     int32_t n_layers;
     int32_t hidden;          /* H */
@@ -182,6 +182,21 @@ int stage_forward(Stage* stage, const StageRequest* reqs, int n_req,
  * W[r][c] = code * scale exactly, written to out_host fp32 [n][k].
  * which: 0..6 = wq, wk, wv, wo, wg, wu, wd.  Synchronizes the device. */
 int stage_debug_dequant(Stage* stage, int layer, int which, float* out_host);
+
+/* Measurement support.  stage_profile_enable(stage, kernel_class) makes later
+ * forwards bracket every launch of that kernel class with a pair of hipEvents
+ * recorded on the launch stream (at most 65536 launches are recorded);
+ * kernel_class: STAGE_KERNEL_QKV, _ATTN, _OPROJ, _GATEUP, _DOWN, or -1 to stop.
+ * stage_profile_read synchronizes on the last recorded event, returns the number
+ * of recorded launches and the sum of their durations in milliseconds, and
+ * clears the record. */
+#define STAGE_KERNEL_QKV    0
+#define STAGE_KERNEL_ATTN   1
+#define STAGE_KERNEL_OPROJ  2
+#define STAGE_KERNEL_GATEUP 3
+#define STAGE_KERNEL_DOWN   4
+int stage_profile_enable(Stage* stage, int kernel_class);
+int stage_profile_read(Stage* stage, int* launches, double* total_ms);
 
 /* Bytes of device memory the stage holds for weights (packed codes + scales +
  * norm weights), as stored. */

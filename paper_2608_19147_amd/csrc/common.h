@@ -10,7 +10,7 @@ constexpr int TILE_ROWS = 64;        // weight rows per tile: one row per lane o
 constexpr int CHUNK_K = 32;          // k values per 16-byte chunk (32 nibbles)
 constexpr int MAX_ROWS = 64;         // activation rows per forward
 constexpr int GEMV_MAX_M = 8;        // rows one GEMV launch handles
-constexpr int GEMV_MAX_CPS = 64;     // chunks per workgroup (LDS holds 2048 k per row)
+constexpr int GEMV_MAX_CPS = 64;     // chunks per workgroup: 4 waves x at most 16 chunks
 constexpr int ATTN_MAX_SPLITS = 64;  // KV splits per (slot, kv head)
 constexpr int ATTN_MIN_SPLIT = 32;   // fewest keys per split
 constexpr int KGROUPS = 16;          // 16-lane key groups per attention workgroup

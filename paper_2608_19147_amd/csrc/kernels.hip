@@ -188,11 +188,71 @@ __device__ __forceinline__ float block_sum256(float v, float* buf) {
     return r;
 }
 
+// ------------------------------------------------------------------ coherent exchange
+// Workgroups of one launch exchange split partials through device-scope
+// ("sc1") stores and loads, which bypass the per-XCD L2s; the writer waits for
+// its stores with a workgroup-scope release before taking the ticket.  This
+// avoids the whole-L2 write-back and invalidate of an agent-scope fence.
+
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_coherent(const float* p) {
+    return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Returns true in exactly one workgroup: the last of `n` to arrive at counter *c,
+// which it resets.  Every thread of the workgroup must call it.
+__device__ __forceinline__ bool last_arrival(unsigned* c, unsigned n, int* flag) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");   // own coherent stores complete
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const unsigned prev = atomicAdd(c, 1u);
+        *flag = (prev == n - 1);
+        if (prev == n - 1) *c = 0u;                             // next launch starts from zero
+    }
+    __syncthreads();
+    return *flag != 0;
+}
+
 // ------------------------------------------------------------------ GEMV
 
+// Inverse RMS of M input rows of length K, fp32, deterministic order.
 template <int MT>
+__device__ __forceinline__ void rms_fullrow(const GemvArgs& a, int K, float* rs_s, float* bsum) {
+    const int tid = threadIdx.x;
+    for (int m = 0; m < a.M; ++m) {
+        float ss = 0.f;
+        for (int k8 = tid; k8 < K / 8; k8 += 256) {
+            float v[8];
+            const size_t base = (size_t)m * a.in_ld + 8 * k8;
+            if (a.in_dt == DT_F32) {
+                const float4 p = *(const float4*)((const float*)a.in + base);
+                const float4 q = *(const float4*)((const float*)a.in + base + 4);
+                v[0] = p.x; v[1] = p.y; v[2] = p.z; v[3] = p.w; v[4] = q.x; v[5] = q.y; v[6] = q.z; v[7] = q.w;
+            } else {
+                const u32x4 h = *(const u32x4*)((const uint16_t*)a.in + base);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t w = h[e >> 1];
+                    v[e] = half_bits_to_f32((uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFFu)), a.in_dt);
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) ss += v[e] * v[e];
+        }
+        ss = block_sum256(ss, bsum);
+        if (tid == 0) rs_s[m] = rsqrtf(ss / (float)K + a.eps);
+    }
+}
+
+template <int MT, int CPW>
 __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
-    __shared__ __attribute__((aligned(16))) uint32_t xs[MT][GEMV_MAX_CPS * 16];
+    constexpr int CPS = 4 * CPW;                 // chunks per workgroup
+    constexpr int KLEN = CPS * 32;               // k values per workgroup
+    constexpr int NI = (MT * KLEN / 8 + 255) / 256;
+    constexpr int NV = (MT * 64 + 255) / 256;
+    __shared__ __attribute__((aligned(16))) uint32_t xs[MT][KLEN / 2];
     __shared__ float red[4][MT][64];
     __shared__ float rs_s[MT];
     __shared__ float bsum[256];
@@ -202,89 +262,118 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
     const int t = blockIdx.x, s = blockIdx.y;
     const PackedMat W = a.W;
     const int M = a.M;
-    const int c0 = s * a.cps;
-    const int c1 = min(W.nchunk, c0 + a.cps);
-    const int npair = (c1 - c0) * 16;
+    const int K = W.k;
+    const int c0 = s * CPS;
+    const int k0 = c0 * 32;
+
+    // ---- weights of this wave: issue every load first (activation-independent)
+    const int cw0 = c0 + wave * CPW;
+    const u32x4* wbase = (const u32x4*)W.w + ((size_t)t * W.nchunk + cw0) * 64 + lane;
+    u32x4 wv[CPW];
+    uint16_t sraw[CPW];
+#pragma unroll
+    for (int u = 0; u < CPW; ++u) wv[u] = __builtin_nontemporal_load(wbase + (size_t)u * 64);
+    const uint16_t* sbase = W.s + (size_t)t * W.ngroups * 64 + lane;
+#pragma unroll
+    for (int u = 0; u < CPW; ++u) sraw[u] = sbase[(size_t)((cw0 + u) / W.gchunks) * 64];
 
     // ---- prologue: inverse RMS of each input row
     if (a.rms == RMS_FULLROW) {
-        for (int m = 0; m < M; ++m) {
-            float ss = 0.f;
-            for (int kk = tid; kk < W.k; kk += 256) {
-                const float v = load_val(a.in, a.in_dt, (size_t)m * a.in_ld + kk);
-                ss += v * v;
-            }
-            ss = block_sum256(ss, bsum);
-            if (tid == 0) rs_s[m] = rsqrtf(ss / (float)W.k + a.eps);
-        }
+        rms_fullrow<MT>(a, K, rs_s, bsum);
     } else if (a.rms == RMS_PARTIALS) {
+        for (int idx = tid; idx < M * a.ssq_tiles; idx += 256) bsum[idx] = a.ssq_in[idx];
+        __syncthreads();
         if (tid < M) {
             float ss = 0.f;
-            for (int tt = 0; tt < a.ssq_tiles; ++tt) ss += a.ssq_in[(size_t)tid * a.ssq_tiles + tt];
-            rs_s[tid] = rsqrtf(ss / (float)W.k + a.eps);
+            for (int tt = 0; tt < a.ssq_tiles; ++tt) ss += bsum[tid * a.ssq_tiles + tt];
+            rs_s[tid] = rsqrtf(ss / (float)K + a.eps);
         }
     }
     __syncthreads();
 
-    // ---- stage the activation slice as fp16 pairs
-    for (int idx = tid; idx < M * npair; idx += 256) {
-        const int m = idx / npair, p = idx - m * npair;
-        const int kk = c0 * 32 + 2 * p;
-        float v0 = 0.f, v1 = 0.f;
-        if (kk < W.k) v0 = load_val(a.in, a.in_dt, (size_t)m * a.in_ld + kk);
-        if (kk + 1 < W.k) v1 = load_val(a.in, a.in_dt, (size_t)m * a.in_ld + kk + 1);
-        if (a.rms != RMS_NONE) {
-            const float rs = rs_s[m];
-            if (kk < W.k) v0 = (v0 * rs) * half_bits_to_f32(a.gamma[kk], a.gamma_dt);
-            if (kk + 1 < W.k) v1 = (v1 * rs) * half_bits_to_f32(a.gamma[kk + 1], a.gamma_dt);
+    // ---- stage the activation slice [k0, k0 + KLEN) as fp16 pairs, 8 k per item
+    {
+        float v[NI][8];
+        float gm[NI][8];
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int it = tid + 256 * i;
+            const int m = it / (KLEN / 8);
+            const int kk = k0 + 8 * (it % (KLEN / 8));
+            const bool ok = (it < M * (KLEN / 8)) && (kk < K);
+            const size_t base = ok ? (size_t)m * a.in_ld + kk : 0;
+            if (a.in_dt == DT_F32) {
+                const float4 p = *(const float4*)((const float*)a.in + base);
+                const float4 q = *(const float4*)((const float*)a.in + base + 4);
+                v[i][0] = p.x; v[i][1] = p.y; v[i][2] = p.z; v[i][3] = p.w;
+                v[i][4] = q.x; v[i][5] = q.y; v[i][6] = q.z; v[i][7] = q.w;
+            } else {
+                const u32x4 h = *(const u32x4*)((const uint16_t*)a.in + base);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t w = h[e >> 1];
+                    v[i][e] = half_bits_to_f32((uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFFu)), a.in_dt);
+                }
+            }
+            if (a.rms != RMS_NONE) {
+                const u32x4 g = *(const u32x4*)(a.gamma + (ok ? kk : 0));
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t w = g[e >> 1];
+                    gm[i][e] = half_bits_to_f32((uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFFu)), a.gamma_dt);
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (!ok) v[i][e] = 0.f;
         }
-        xs[m][p] = pack_f16x2(v0, v1);
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+            const int it = tid + 256 * i;
+            if (it < M * (KLEN / 8)) {
+                const int m = it / (KLEN / 8);
+                const int p0 = 4 * (it % (KLEN / 8));
+                if (a.rms != RMS_NONE) {
+                    const float rs = rs_s[m];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) v[i][e] = (v[i][e] * rs) * gm[i][e];
+                }
+                u32x4 o;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) o[q] = pack_f16x2(v[i][2 * q], v[i][2 * q + 1]);
+                *(u32x4*)&xs[m][p0] = o;
+            }
+        }
     }
     __syncthreads();
 
-    // ---- stream the tile
+    // ---- dot products (codes exact in fp16, fp32 accumulation, scale per chunk)
     float acc[MT];
 #pragma unroll
     for (int m = 0; m < MT; ++m) acc[m] = 0.f;
-    const u32x4* wbase = (const u32x4*)W.w + (size_t)t * W.nchunk * 64 + lane;
-    const uint16_t* sbase = W.s + (size_t)t * W.ngroups * 64 + lane;
-    constexpr int U = 4;
-    for (int cb = c0 + wave; cb < c1; cb += 4 * U) {
-        u32x4 wv[U];
-        float sc[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int c = cb + 4 * u;
-            if (c < c1) {
-                wv[u] = __builtin_nontemporal_load(wbase + (size_t)c * 64);
-                sc[u] = f16_to_f32(sbase[(size_t)(c / W.gchunks) * 64]);
-            }
-        }
+    for (int u = 0; u < CPW; ++u) {
+        half2_t wq[16];
+        unpack_chunk(wv[u], wq);
+        const float sc = f16_to_f32(sraw[u]);
+        const int pc = (wave * CPW + u) * 16;
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int c = cb + 4 * u;
-            if (c < c1) {
-                half2_t wq[16];
-                unpack_chunk(wv[u], wq);
+        for (int m = 0; m < MT; ++m) {
+            if (m < M) {
+                const u32x4* xv = (const u32x4*)&xs[m][pc];
+                float d = 0.f;
 #pragma unroll
-                for (int m = 0; m < MT; ++m) {
-                    if (m < M) {
-                        const u32x4* xv = (const u32x4*)&xs[m][(c - c0) * 16];
-                        float d = 0.f;
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const u32x4 x4 = xv[q4];
 #pragma unroll
-                        for (int q4 = 0; q4 < 4; ++q4) {
-                            const u32x4 x4 = xv[q4];
-#pragma unroll
-                            for (int e = 0; e < 4; ++e) {
-                                // copy the element out first: a bit_cast of a vector-element
-                                // lvalue reads element 0 of the vector
-                                const uint32_t xe = x4[e];
-                                d = __builtin_amdgcn_fdot2(wq[4 * q4 + e], __builtin_bit_cast(half2_t, xe), d, false);
-                            }
-                        }
-                        acc[m] += sc[u] * d;
+                    for (int e = 0; e < 4; ++e) {
+                        // copy the element out first: a bit_cast of a vector-element
+                        // lvalue reads element 0 of the vector
+                        const uint32_t xe = x4[e];
+                        d = __builtin_amdgcn_fdot2(wq[4 * q4 + e], __builtin_bit_cast(half2_t, xe), d, false);
                     }
                 }
+                acc[m] += sc * d;
             }
         }
     }
@@ -293,11 +382,9 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
 #pragma unroll
     for (int m = 0; m < MT; ++m) red[wave][m][lane] = acc[m];
     __syncthreads();
-
-    const int ldp = W.ntiles * 64;
-    float vals[(MT * 64 + 255) / 256];
+    float vals[NV];
 #pragma unroll
-    for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
+    for (int q = 0; q < NV; ++q) {
         const int idx = tid + 256 * q;
         vals[q] = 0.f;
         if (idx < M * 64) {
@@ -306,32 +393,32 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
         }
     }
 
+    // ---- split-K: the last workgroup of the tile sums every split in split order
     if (a.ksplit > 1) {
+        const int ldp = W.ntiles * 64;
 #pragma unroll
-        for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
+        for (int q = 0; q < NV; ++q) {
+            const int idx = tid + 256 * q;
+            if (idx < M * 64)
+                store_coherent(&a.partial[((size_t)s * M + (idx >> 6)) * ldp + t * 64 + (idx & 63)], vals[q]);
+        }
+        if (!last_arrival(&a.counters[t], (unsigned)a.ksplit, &last_s)) return;
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
             const int idx = tid + 256 * q;
             if (idx < M * 64) {
-                const int m = idx >> 6, r = idx & 63;
-                a.partial[((size_t)s * M + m) * ldp + t * 64 + r] = vals[q];
-            }
-        }
-        __threadfence();
-        __syncthreads();
-        if (tid == 0) {
-            const unsigned prev = atomicAdd(&a.counters[t], 1u);
-            last_s = (prev == (unsigned)(a.ksplit - 1));
-        }
-        __syncthreads();
-        if (!last_s) return;
-        __threadfence();
-        if (tid == 0) a.counters[t] = 0u;
-#pragma unroll
-        for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
-            const int idx = tid + 256 * q;
-            if (idx < M * 64) {
-                const int m = idx >> 6, r = idx & 63;
+                const float* pp = &a.partial[(size_t)(idx >> 6) * ldp + t * 64 + (idx & 63)];
+                const size_t stride = (size_t)M * ldp;
                 float v = 0.f;
-                for (int ss = 0; ss < a.ksplit; ++ss) v += a.partial[((size_t)ss * M + m) * ldp + t * 64 + r];
+                int ss = 0;
+                for (; ss + 8 <= a.ksplit; ss += 8) {
+                    float b8[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) b8[e] = load_coherent(pp + (ss + e) * stride);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) v += b8[e];
+                }
+                for (; ss < a.ksplit; ++ss) v += load_coherent(pp + ss * stride);
                 vals[q] = v;
             }
         }
@@ -340,18 +427,17 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
     // ---- epilogue
     if (a.epi == EPI_STORE) {
 #pragma unroll
-        for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
+        for (int q = 0; q < NV; ++q) {
             const int idx = tid + 256 * q;
             if (idx < M * 64) {
-                const int m = idx >> 6, r = idx & 63;
-                const int n = t * 64 + r;
+                const int m = idx >> 6, n = t * 64 + (idx & 63);
                 if (n < W.n) a.out[(size_t)m * a.out_ld + n] = vals[q];
             }
         }
     } else if (a.epi == EPI_RESID) {
         __syncthreads();
 #pragma unroll
-        for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
+        for (int q = 0; q < NV; ++q) {
             const int idx = tid + 256 * q;
             if (idx < M * 64) {
                 const int m = idx >> 6, r = idx & 63;
@@ -374,7 +460,7 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
     } else {  // EPI_SWIGLU: rows 0..31 of the tile are gate rows, 32..63 the matching up rows
         __syncthreads();
 #pragma unroll
-        for (int q = 0; q < (MT * 64 + 255) / 256; ++q) {
+        for (int q = 0; q < NV; ++q) {
             const int idx = tid + 256 * q;
             if (idx < M * 64) red[0][idx >> 6][idx & 63] = vals[q];
         }
@@ -390,29 +476,52 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
     }
 }
 
-hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
+template <int MT>
+hipError_t launch_gemv_m(const GemvArgs& a, int cpw, hipStream_t st) {
     const dim3 grid(a.W.ntiles, a.ksplit), block(256);
-    switch (a.M) {
-        case 1: gemv_kernel<1><<<grid, block, 0, st>>>(a); break;
-        case 2: gemv_kernel<2><<<grid, block, 0, st>>>(a); break;
-        case 3: gemv_kernel<3><<<grid, block, 0, st>>>(a); break;
-        case 4: gemv_kernel<4><<<grid, block, 0, st>>>(a); break;
-        case 5: gemv_kernel<5><<<grid, block, 0, st>>>(a); break;
-        case 6: gemv_kernel<6><<<grid, block, 0, st>>>(a); break;
-        case 7: gemv_kernel<7><<<grid, block, 0, st>>>(a); break;
-        case 8: gemv_kernel<8><<<grid, block, 0, st>>>(a); break;
+    switch (cpw) {
+        case 1: gemv_kernel<MT, 1><<<grid, block, 0, st>>>(a); break;
+        case 2: gemv_kernel<MT, 2><<<grid, block, 0, st>>>(a); break;
+        case 4: gemv_kernel<MT, 4><<<grid, block, 0, st>>>(a); break;
+        case 8: gemv_kernel<MT, 8><<<grid, block, 0, st>>>(a); break;
+        case 16: gemv_kernel<MT, 16><<<grid, block, 0, st>>>(a); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
+hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
+    if (a.cps % 4) return hipErrorInvalidValue;
+    const int cpw = a.cps / 4;
+    switch (a.M) {
+        case 1: return launch_gemv_m<1>(a, cpw, st);
+        case 2: return launch_gemv_m<2>(a, cpw, st);
+        case 3: return launch_gemv_m<3>(a, cpw, st);
+        case 4: return launch_gemv_m<4>(a, cpw, st);
+        case 5: return launch_gemv_m<5>(a, cpw, st);
+        case 6: return launch_gemv_m<6>(a, cpw, st);
+        case 7: return launch_gemv_m<7>(a, cpw, st);
+        case 8: return launch_gemv_m<8>(a, cpw, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 // ------------------------------------------------------------------ attention
+
+// Rows [j0, j1) of one split are processed in blocks of ABLK keys whose mask
+// bytes and table entries are first staged in LDS; each 16-lane key group then
+// loads KB cache rows at once before scoring them.
+constexpr int ABLK = 256;
+constexpr int KB = 4;
 
 template <int D, int RC>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     constexpr int EPL = D / 16;
+    constexpr int HALF = D / 2;
     __shared__ float lo[KGROUPS][RC][D];
     __shared__ float lm[KGROUPS][RC], ll[KGROUPS][RC];
+    __shared__ uint8_t smask[ABLK];
+    __shared__ int16_t stab[ABLK];
     __shared__ int last_s;
 
     const int item = blockIdx.x, g = blockIdx.y, split = blockIdx.z;
@@ -438,7 +547,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const int16_t* tab = rq.table + (size_t)b * rq.cap;
     const int rowbase = rq.row0 + b * n;
     const int d0 = li * EPL;
-    constexpr int HALF = D / 2;
+    const int jc1 = min(j1, P);            // cached rows end here; [max(j0, P), j1) are new rows
 
     for (int r0 = 0; r0 < R; r0 += RC) {
         float q[RC][EPL];
@@ -476,55 +585,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
             for (int e = 0; e < EPL; ++e) o[rr][e] = 0.f;
         }
 
-        for (int j = j0 + kg; j < j1; j += KGROUPS) {
-            if (mask[j] == 0) continue;                       // hidden from every query of the slot
-            float kf[EPL], vf[EPL];
-            if (j < P) {
-                const int ps = tab[j];
-                const size_t off = (((size_t)ps * Hkv + g) * rq.cap + j) * D + d0;
-                uint16_t kb[EPL], vb[EPL];
-                if constexpr (EPL == 8) {
-                    *(u32x4*)kb = *(const u32x4*)(kl + off);
-                    *(u32x4*)vb = *(const u32x4*)(vl + off);
-                } else {
-                    *(u32x2*)kb = *(const u32x2*)(kl + off);
-                    *(u32x2*)vb = *(const u32x2*)(vl + off);
-                }
-#pragma unroll
-                for (int e = 0; e < EPL; ++e) {
-                    kf[e] = half_bits_to_f32(kb[e], a.kv_dt);
-                    vf[e] = half_bits_to_f32(vb[e], a.kv_dt);
-                }
-            } else {
-                const int i = j - P;
-                const int m = rowbase + i;
-                const int pos = a.meta.positions[m];
-                const float* krow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + g) * D;
-                const float* vrow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + Hkv + g) * D;
-                uint16_t kb[EPL], vb[EPL];
-#pragma unroll
-                for (int e = 0; e < EPL; ++e) {
-                    const int d = d0 + e;
-                    const bool lo_half = d < HALF;
-                    const float x = krow[d];
-                    const float xp = lo_half ? krow[d + HALF] : krow[d - HALF];
-                    const float2 cs = a.rope[(size_t)pos * HALF + (lo_half ? d : d - HALF)];
-                    const float y = lo_half ? (x * cs.x - xp * cs.y) : (x * cs.x + xp * cs.y);
-                    kb[e] = to_half_bits(y, a.kv_dt);
-                    vb[e] = to_half_bits(vrow[d], a.kv_dt);
-                    kf[e] = half_bits_to_f32(kb[e], a.kv_dt);
-                    vf[e] = half_bits_to_f32(vb[e], a.kv_dt);
-                }
-                if (r0 == 0) {                                 // append: owner of row j writes it
-                    const size_t off = (((size_t)b * Hkv + g) * rq.cap + j) * D + d0;
-#pragma unroll
-                    for (int e = 0; e < EPL; ++e) {
-                        kl[off + e] = kb[e];
-                        vl[off + e] = vb[e];
-                    }
-                    if (a.layer == 0 && g == 0 && li == 0) rq.table[(size_t)b * rq.cap + j] = (int16_t)b;
-                }
-            }
+        auto consume = [&](int j, const float* kf, const float* vf) {
 #pragma unroll
             for (int rr = 0; rr < RC; ++rr) {
                 if (qi[rr] < 0) continue;
@@ -541,9 +602,99 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
                 for (int e = 0; e < EPL; ++e) o[rr][e] = o[rr][e] * corr + p * vf[e];
                 mx[rr] = mn;
             }
+        };
+
+        // ---- cached rows: read through the beam table
+        for (int jb = j0; jb < jc1; jb += ABLK) {
+            const int nb = min(ABLK, jc1 - jb);
+            __syncthreads();
+            for (int x = tid; x < nb; x += 256) {
+                smask[x] = mask[jb + x];
+                stab[x] = tab[jb + x];
+            }
+            __syncthreads();
+            for (int x0 = kg; x0 < nb; x0 += KGROUPS * KB) {
+                uint16_t kb[KB][EPL], vb[KB][EPL];
+                bool vis[KB];
+#pragma unroll
+                for (int u = 0; u < KB; ++u) {
+                    const int x = x0 + u * KGROUPS;
+                    vis[u] = (x < nb) && smask[x] != 0;      // hidden from every query of the slot
+                    if (vis[u]) {
+                        const int j = jb + x;
+                        const size_t off = (((size_t)stab[x] * Hkv + g) * rq.cap + j) * D + d0;
+                        if constexpr (EPL == 8) {
+                            *(u32x4*)kb[u] = *(const u32x4*)(kl + off);
+                            *(u32x4*)vb[u] = *(const u32x4*)(vl + off);
+                        } else {
+                            *(u32x2*)kb[u] = *(const u32x2*)(kl + off);
+                            *(u32x2*)vb[u] = *(const u32x2*)(vl + off);
+                        }
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < KB; ++u) {
+                    if (!vis[u]) continue;
+                    float kf[EPL], vf[EPL];
+#pragma unroll
+                    for (int e = 0; e < EPL; ++e) {
+                        kf[e] = half_bits_to_f32(kb[u][e], a.kv_dt);
+                        vf[e] = half_bits_to_f32(vb[u][e], a.kv_dt);
+                    }
+                    consume(jb + x0 + u * KGROUPS, kf, vf);
+                }
+            }
         }
 
-        // ---- merge the 16 key groups (fixed order)
+        // ---- this forward's rows: rotate k, round k and v to the cache dtype, append
+        for (int j = max(j0, P) + kg; j < j1; j += KGROUPS) {
+            if (mask[j] == 0) continue;
+            const int i = j - P;
+            const int m = rowbase + i;
+            const int pos = a.meta.positions[m];
+            const float* krow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + g) * D;
+            const float* vrow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + Hkv + g) * D;
+            uint16_t kb[EPL], vb[EPL];
+            float kf[EPL], vf[EPL];
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) {
+                const int d = d0 + e;
+                const bool lo_half = d < HALF;
+                const float x = krow[d];
+                const float xp = lo_half ? krow[d + HALF] : krow[d - HALF];
+                const float2 cs = a.rope[(size_t)pos * HALF + (lo_half ? d : d - HALF)];
+                const float y = lo_half ? (x * cs.x - xp * cs.y) : (x * cs.x + xp * cs.y);
+                kb[e] = to_half_bits(y, a.kv_dt);
+                vb[e] = to_half_bits(vrow[d], a.kv_dt);
+                kf[e] = half_bits_to_f32(kb[e], a.kv_dt);
+                vf[e] = half_bits_to_f32(vb[e], a.kv_dt);
+            }
+            consume(j, kf, vf);
+        }
+        if (r0 == 0) {                                          // append: owner of row j writes it
+            for (int j = max(j0, P) + kg; j < j1; j += KGROUPS) {
+                const int i = j - P;
+                const int m = rowbase + i;
+                const int pos = a.meta.positions[m];
+                const float* krow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + g) * D;
+                const float* vrow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + Hkv + g) * D;
+                const size_t off = (((size_t)b * Hkv + g) * rq.cap + j) * D + d0;
+#pragma unroll
+                for (int e = 0; e < EPL; ++e) {
+                    const int d = d0 + e;
+                    const bool lo_half = d < HALF;
+                    const float x = krow[d];
+                    const float xp = lo_half ? krow[d + HALF] : krow[d - HALF];
+                    const float2 cs = a.rope[(size_t)pos * HALF + (lo_half ? d : d - HALF)];
+                    const float y = lo_half ? (x * cs.x - xp * cs.y) : (x * cs.x + xp * cs.y);
+                    kl[off + e] = to_half_bits(y, a.kv_dt);
+                    vl[off + e] = to_half_bits(vrow[d], a.kv_dt);
+                }
+                if (a.layer == 0 && g == 0 && li == 0) rq.table[(size_t)b * rq.cap + j] = (int16_t)b;
+            }
+        }
+
+        // ---- merge the 16 key groups (fixed order) into this split's partial
 #pragma unroll
         for (int rr = 0; rr < RC; ++rr) {
             if (li == 0) {
@@ -570,41 +721,57 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
             const int i = r / gs, h = g * gs + (r % gs);
             const int m = rowbase + i;
             float* pp = a.part + (((size_t)m * Hq + h) * a.nsplit_max + split) * (D + 2);
-            pp[2 + d] = O;
+            store_coherent(pp + 2 + d, O);
             if (d == 0) {
-                pp[0] = M;
-                pp[1] = S;
+                store_coherent(pp, M);
+                store_coherent(pp + 1, S);
             }
         }
         __syncthreads();
     }
 
-    // ---- last split of this (slot, kv head) merges all splits (fixed order)
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-        const unsigned prev = atomicAdd(&a.counters[item * Hkv + g], 1u);
-        last_s = (prev == (unsigned)(nsplit - 1));
-    }
-    __syncthreads();
-    if (!last_s) return;
-    __threadfence();
-    if (tid == 0) a.counters[item * Hkv + g] = 0u;
-    for (int idx = tid; idx < R * D; idx += 256) {
-        const int r = idx / D, d = idx % D;
-        const int i = r / gs, h = g * gs + (r % gs);
-        const int m = rowbase + i;
-        const float* pp = a.part + ((size_t)m * Hq + h) * a.nsplit_max * (D + 2);
-        float M = -INFINITY;
-        for (int s2 = 0; s2 < nsplit; ++s2) M = fmaxf(M, pp[(size_t)s2 * (D + 2)]);
-        float O = 0.f, S = 0.f;
-        for (int s2 = 0; s2 < nsplit; ++s2) {
-            const float ms = pp[(size_t)s2 * (D + 2)];
-            const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - M);
-            O += pp[(size_t)s2 * (D + 2) + 2 + d] * w;
-            S += pp[(size_t)s2 * (D + 2) + 1] * w;
+    // ---- the last split of this (slot, kv head) merges all splits (fixed order)
+    if (!last_arrival(&a.counters[item * Hkv + g], (unsigned)nsplit, &last_s)) return;
+    {
+        float* wgt = &lo[0][0][0];                 // [R][nsplit] weights exp2(m_s - M), reuses LDS
+        float* inv = wgt + R * nsplit;             // [R] 1 / sum_s S_s w_s
+        for (int idx = tid; idx < R * nsplit; idx += 256) {
+            const int r = idx / nsplit, s2 = idx % nsplit;
+            const int m = rowbase + r / gs, h = g * gs + (r % gs);
+            wgt[idx] = load_coherent(a.part + (((size_t)m * Hq + h) * a.nsplit_max + s2) * (D + 2));
+            inv[R + idx] = load_coherent(a.part + (((size_t)m * Hq + h) * a.nsplit_max + s2) * (D + 2) + 1);
         }
-        a.out[(size_t)m * a.out_ld + (size_t)h * D + d] = O / S;
+        __syncthreads();
+        for (int r = tid; r < R; r += 256) {
+            float M = -INFINITY;
+            for (int s2 = 0; s2 < nsplit; ++s2) M = fmaxf(M, wgt[r * nsplit + s2]);
+            float S = 0.f;
+            for (int s2 = 0; s2 < nsplit; ++s2) {
+                const float ms = wgt[r * nsplit + s2];
+                const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - M);
+                wgt[r * nsplit + s2] = w;
+                S += inv[R + r * nsplit + s2] * w;
+            }
+            inv[r] = 1.0f / S;
+        }
+        __syncthreads();
+        for (int idx = tid; idx < R * D; idx += 256) {
+            const int r = idx / D, d = idx % D;
+            const int i = r / gs, h = g * gs + (r % gs);
+            const int m = rowbase + i;
+            const float* pp = a.part + ((size_t)m * Hq + h) * a.nsplit_max * (D + 2) + 2 + d;
+            float O = 0.f;
+            int s2 = 0;
+            for (; s2 + 8 <= nsplit; s2 += 8) {
+                float b8[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) b8[e] = load_coherent(pp + (size_t)(s2 + e) * (D + 2));
+#pragma unroll
+                for (int e = 0; e < 8; ++e) O += b8[e] * wgt[r * nsplit + s2 + e];
+            }
+            for (; s2 < nsplit; ++s2) O += load_coherent(pp + (size_t)s2 * (D + 2)) * wgt[r * nsplit + s2];
+            a.out[(size_t)m * a.out_ld + (size_t)h * D + d] = O * inv[r];
+        }
     }
 }
 

@@ -62,8 +62,12 @@ struct Stage {
     bool meta_ev_used[META_RING] = {};
     int ring_i = 0;
     int64_t weight_bytes = 0;
+    int prof_class = -1;
+    std::vector<hipEvent_t> prof_ev;   // start/stop pairs
+    size_t prof_used = 0;              // events recorded
 
     ~Stage() {
+        for (hipEvent_t e : prof_ev) (void)hipEventDestroy(e);
         (void)hipSetDevice(device);
         (void)hipDeviceSynchronize();
         for (void* p : allocs) (void)hipFree(p);
@@ -99,22 +103,29 @@ struct KVState {
 
 namespace {
 
-void plan_split(DevMat& m) {
+// Chunks per wave (CPW) of a matrix: the largest of 16, 8, 4, 2, 1 that still
+// gives at least `target` workgroups (tiles x K-splits).  K is padded with zero
+// codes to a whole number of workgroup slices (4 * CPW chunks each).
+int plan_cpw(int ntiles, int nchunk) {
     int target = 1024;
     if (const char* e = std::getenv("STAGE_GEMV_WG_TARGET")) target = std::max(1, atoi(e));
-    const int nch = m.pm.nchunk;
-    int ks = std::max(1, std::min(nch, (target + m.pm.ntiles - 1) / m.pm.ntiles));
-    int cps = (nch + ks - 1) / ks;
-    cps = std::min(cps, GEMV_MAX_CPS);
-    ks = (nch + cps - 1) / cps;
-    m.ksplit = ks;
-    m.cps = cps;
+    for (int cpw : {16, 8, 4, 2}) {
+        const int cps = 4 * cpw;
+        const int nck = (nchunk + cps - 1) / cps * cps;
+        if (nck - nchunk > nchunk / 8) continue;           // at most 12.5% padding
+        if ((long)ntiles * (nck / cps) >= target) return cpw;
+    }
+    return 1;
 }
 
 int make_mat(Stage* st, DevMat& m, int n_rows_padded_tiles, int k, int g) {
     m.pm.k = k;
     m.pm.ntiles = n_rows_padded_tiles;
-    m.pm.nchunk = (k + CHUNK_K - 1) / CHUNK_K;
+    const int nchunk = (k + CHUNK_K - 1) / CHUNK_K;
+    const int cpw = plan_cpw(m.pm.ntiles, nchunk);
+    m.cps = 4 * cpw;
+    m.pm.nchunk = (nchunk + m.cps - 1) / m.cps * m.cps;
+    m.ksplit = m.pm.nchunk / m.cps;
     m.pm.gchunks = g / CHUNK_K;
     m.pm.ngroups = (m.pm.nchunk + m.pm.gchunks - 1) / m.pm.gchunks;
     uint8_t* w;
@@ -130,7 +141,6 @@ int make_mat(Stage* st, DevMat& m, int n_rows_padded_tiles, int k, int g) {
     m.pm.w = w;
     m.pm.s = s;
     st->weight_bytes += (int64_t)wbytes + (int64_t)selems * 2;
-    plan_split(m);
     return STAGE_OK;
 }
 
@@ -167,7 +177,7 @@ int check_config(const StageConfig* c) {
     if (!c) return fail(STAGE_E_INVALID, "config is NULL");
     if (c->n_layers < 1 || c->hidden < 2 || c->n_q_heads < 1 || c->n_kv_heads < 1 || c->ffn < 2 || c->max_positions < 1)
         return fail(STAGE_E_INVALID, "non-positive dimension in config");
-    if (c->hidden % 2 || c->ffn % 2) return fail(STAGE_E_UNSUPPORTED, "hidden and ffn must be even");
+    if (c->hidden % 8 || c->ffn % 8) return fail(STAGE_E_UNSUPPORTED, "hidden and ffn must be multiples of 8");
     if (c->head_dim != 64 && c->head_dim != 128) return fail(STAGE_E_UNSUPPORTED, "head_dim must be 64 or 128");
     if (c->n_q_heads % c->n_kv_heads) return fail(STAGE_E_INVALID, "n_q_heads must be a multiple of n_kv_heads");
     if (c->group_size < 32 || c->group_size % 32) return fail(STAGE_E_UNSUPPORTED, "group_size must be a multiple of 32");
@@ -205,6 +215,22 @@ int ensure_meta(Stage* st, size_t bytes) {
     }
     st->meta_cap = cap;
     return STAGE_OK;
+}
+
+constexpr size_t PROF_MAX_LAUNCHES = 65536;
+
+// Records the start (begin = true) or stop event of a profiled launch.
+hipError_t prof_mark(Stage* st, int kclass, bool begin, hipStream_t s) {
+    if (st->prof_class != kclass) return hipSuccess;
+    if (begin && st->prof_used + 2 > 2 * PROF_MAX_LAUNCHES) return hipSuccess;
+    if (!begin && (st->prof_used % 2) == 0) return hipSuccess;   // start was not recorded
+    if (st->prof_used == st->prof_ev.size()) {
+        hipEvent_t e;
+        hipError_t err = hipEventCreate(&e);
+        if (err != hipSuccess) return err;
+        st->prof_ev.push_back(e);
+    }
+    return hipEventRecord(st->prof_ev[st->prof_used++], s);
 }
 
 }  // namespace
@@ -361,6 +387,35 @@ int stage_destroy(Stage* stage) {
 }
 
 int64_t stage_weight_bytes(const Stage* stage) { return stage ? stage->weight_bytes : -1; }
+
+int stage_profile_enable(Stage* stage, int kernel_class) {
+    if (!stage) return fail(STAGE_E_INVALID, "stage is NULL");
+    if (kernel_class < -1 || kernel_class > STAGE_KERNEL_DOWN) return fail(STAGE_E_INVALID, "unknown kernel class");
+    stage->prof_class = kernel_class;
+    stage->prof_used = 0;
+    return STAGE_OK;
+}
+
+int stage_profile_read(Stage* stage, int* launches, double* total_ms) {
+    if (!stage || !launches || !total_ms) return fail(STAGE_E_INVALID, "NULL argument");
+    *launches = 0;
+    *total_ms = 0.0;
+    const size_t pairs = stage->prof_used / 2;
+    if (pairs) {
+        HIP_TRY(hipSetDevice(stage->device));
+        HIP_TRY(hipEventSynchronize(stage->prof_ev[2 * pairs - 1]));
+        double tot = 0.0;
+        for (size_t i = 0; i < pairs; ++i) {
+            float ms = 0.f;
+            HIP_TRY(hipEventElapsedTime(&ms, stage->prof_ev[2 * i], stage->prof_ev[2 * i + 1]));
+            tot += ms;
+        }
+        *launches = (int)pairs;
+        *total_ms = tot;
+    }
+    stage->prof_used = 0;
+    return STAGE_OK;
+}
 
 int kv_state_alloc(Stage* stage, int n_slots, int capacity, KVState** out) {
     if (!stage || !out) return fail(STAGE_E_INVALID, "NULL argument");
@@ -692,7 +747,9 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             a.epi = EPI_STORE;
             a.out = st->qkv;
             a.out_ld = nqkv;
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_QKV, true, s));
             HIP_TRY(run_gemv(Ld.qkv, a, H, nqkv, 0, first ? 2 : 4, 0));
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_QKV, false, s));
         }
         // attention (rotary, append, mask, online softmax, split merge)
         {
@@ -712,7 +769,12 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             a.counters = st->acnt;
             a.nsplit_max = ATTN_MAX_SPLITS;
             if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, atoi(e)));
+            // the split merge keeps 2 * nsplit + 1 floats per query row in the kernel's LDS tile
+            const int lds_floats = KGROUPS * (max_rows_item > 4 ? 8 : 4) * D;
+            a.nsplit_max = std::max(1, std::min(a.nsplit_max, (lds_floats / max_rows_item - 1) / 2));
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, true, s));
             HIP_TRY(launch_attention(a, D, max_rows_item, s));
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, false, s));
         }
         // x = residual + o W_o^T
         {
@@ -728,7 +790,9 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             a.resid_dt = first ? act_dt : DT_F32;
             a.resid_ld = H;
             a.ssq_out = st->ssq;
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_OPROJ, true, s));
             HIP_TRY(run_gemv(Ld.o, a, Hq * D, H, H, 4, first ? 2 : 4));
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_OPROJ, false, s));
         }
         // act = silu(h2 W_g^T) * (h2 W_u^T), h2 = RMSNorm(x)
         {
@@ -746,7 +810,9 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             a.out = st->act;
             a.out_ld = F;
             a.n_valid = F;
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_GATEUP, true, s));
             HIP_TRY(run_gemv(Ld.gu, a, H, F, 0, 4, 0));
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_GATEUP, false, s));
         }
         // x = x + act W_d^T  (last layer also writes hidden_out)
         {
@@ -767,7 +833,9 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
                 a.out_act_dt = act_dt;
                 a.out_act_ld = H;
             }
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_DOWN, true, s));
             HIP_TRY(run_gemv(Ld.d, a, F, H, H, 4, 4));
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_DOWN, false, s));
         }
     }
 

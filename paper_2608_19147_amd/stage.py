@@ -92,6 +92,18 @@ class Stage:
     def weight_bytes(self) -> int:
         return int(self.lib.stage_weight_bytes(self.handle))
 
+    def profile(self, kernel_class: Optional[str]) -> None:
+        """Bracket every launch of one kernel class ('qkv', 'attn', 'oproj',
+        'gateup', 'down') with hipEvents on the launch stream; None stops."""
+        check(self.lib.stage_profile_enable(self.handle, -1 if kernel_class is None else _lib.KERNEL_CLASSES[kernel_class]))
+
+    def profile_read(self):
+        """(launches, total_ms) recorded since profile() or the last read."""
+        n = ctypes.c_int()
+        ms = ctypes.c_double()
+        check(self.lib.stage_profile_read(self.handle, ctypes.byref(n), ctypes.byref(ms)))
+        return n.value, ms.value
+
     def new_state(self, n_slots: int, capacity: int) -> "KVState":
         return KVState(self, n_slots, capacity)
 

@@ -61,7 +61,7 @@ def _create(lib, cfg, layers=None):
     (dict(act_dtype=7), -1),
     (dict(n_layers=0), -1),
     (dict(rms_eps=0.0), -1),
-    (dict(hidden=255), -7),
+    (dict(hidden=252), -7),
 ])
 def test_config_rejected(lib, kw, code):
     rc, h = _create(lib, _cfg(**kw))
