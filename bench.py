@@ -27,7 +27,6 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-DOMINANT = "gateup"
 
 
 def algorithmic_bytes(shape, kv_len: int, n_new: int = 1) -> dict:
@@ -121,7 +120,7 @@ def main() -> int:
     print(f"# setup {time.perf_counter() - t0:.1f}s (weights {stage.weight_bytes() / 1e9:.3f} GB on device)",
           file=sys.stderr, flush=True)
 
-    def run(kv_len: int, profile: bool):
+    def run(kv_len: int, profile):
         state.truncate(kv_len)
         req = Request(state, np.array([[kv_len]], np.int32), np.ones((1, kv_len + 1), np.uint8), np.array([0], np.int32))
         for i in range(args.warmup):
@@ -129,7 +128,7 @@ def main() -> int:
             state.truncate(kv_len)
         torch.cuda.synchronize()
         if profile:
-            stage.profile(DOMINANT)
+            stage.profile(profile)
         t_start = time.perf_counter()
         for i in range(args.steps):
             stage.forward([req], xs[i % n_in], out)
@@ -143,8 +142,14 @@ def main() -> int:
         ms = (t_end - t_start) * 1e3 / args.steps
         return ms, prof
 
-    ms_main, prof = run(args.kv, True)
-    ms_also = run(args.kv_also, False)[0] if args.kv_also else None
+    # the dominant kernel: the single-launch forward when the stage uses it,
+    # else the gate|up GEMV of the multi-kernel path (54% of the weight bytes)
+    ms_main, prof = run(args.kv, "persistent")
+    dominant = "persistent"
+    if prof[0] == 0:
+        ms_main, prof = run(args.kv, "gateup")
+        dominant = "gateup"
+    ms_also = run(args.kv_also, None)[0] if args.kv_also else None
     print(f"# decode kv={args.kv}: {ms_main:.4f} ms/step"
           + (f"; kv={args.kv_also}: {ms_also:.4f} ms/step" if ms_also else ""), file=sys.stderr, flush=True)
 
@@ -152,8 +157,11 @@ def main() -> int:
     gbps = b["total"] / (ms_main * 1e-3) / 1e9
     launches, prof_ms = prof
     per_launch_ms = prof_ms / max(1, launches)
-    gu_bytes = gateup_bytes(shape)
-    gu_gbps = gu_bytes / (per_launch_ms * 1e-3) / 1e9
+    if dominant == "persistent":
+        k_bytes, k_name = b["total"], "stage_persistent_kernel (whole stage forward, one launch per step)"
+    else:
+        k_bytes, k_name = gateup_bytes(shape), "gemv_kernel gate|up (one launch per layer)"
+    k_gbps = k_bytes / (per_launch_ms * 1e-3) / 1e9
     line = {
         "metric": "stage decode tokens/s (8B half-stage, bs=1) + achieved HBM GB/s vs peak",
         "value": round(1e3 / ms_main, 3),
@@ -177,10 +185,10 @@ def main() -> int:
         "achieved_gbps": round(gbps, 1),
         "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
         "roofline": {
-            "bound": "hbm", "kernel": "gemv_w4 gate|up (one launch per layer)",
-            "achieved": round(gu_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-            "frac": round(gu_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
-            "bytes_per_launch": gu_bytes, "avg_launch_us": round(per_launch_ms * 1e3, 3), "launches_timed": launches,
+            "bound": "hbm", "kernel": k_name,
+            "achieved": round(k_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(k_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+            "bytes_per_launch": k_bytes, "avg_launch_us": round(per_launch_ms * 1e3, 3), "launches_timed": launches,
         },
     }
     if ms_also:

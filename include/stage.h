@@ -180,13 +180,19 @@ int stage_forward(Stage* stage, const StageRequest* reqs, int n_req,
 
 /* Test support: the dequantized weight matrix as the kernels decode it,
  * W[r][c] = code * scale exactly, written to out_host fp32 [n][k].
- * which: 0..6 = wq, wk, wv, wo, wg, wu, wd.  Synchronizes the device. */
+ * which: 0..6 = wq, wk, wv, wo, wg, wu, wd in the tiled layout of the
+ * multi-kernel path; 8..14 = the same matrices in the row layout of the
+ * persistent path (STAGE_E_UNSUPPORTED when the stage keeps none).
+ * Synchronizes the device. */
 int stage_debug_dequant(Stage* stage, int layer, int which, float* out_host);
 
 /* Measurement support.  stage_profile_enable(stage, kernel_class) makes later
  * forwards bracket every launch of that kernel class with a pair of hipEvents
  * recorded on the launch stream (at most 65536 launches are recorded);
- * kernel_class: STAGE_KERNEL_QKV, _ATTN, _OPROJ, _GATEUP, _DOWN, or -1 to stop.
+ * kernel_class: STAGE_KERNEL_QKV, _ATTN, _OPROJ, _GATEUP, _DOWN (kernels of the
+ * multi-kernel path, which profiling of these classes selects), _PERSISTENT
+ * (the single-launch forward, when the stage and row count allow it), or -1
+ * to stop.
  * stage_profile_read synchronizes on the last recorded event, returns the number
  * of recorded launches and the sum of their durations in milliseconds, and
  * clears the record. */
@@ -195,8 +201,18 @@ int stage_debug_dequant(Stage* stage, int layer, int which, float* out_host);
 #define STAGE_KERNEL_OPROJ  2
 #define STAGE_KERNEL_GATEUP 3
 #define STAGE_KERNEL_DOWN   4
+#define STAGE_KERNEL_PERSISTENT 5
 int stage_profile_enable(Stage* stage, int kernel_class);
 int stage_profile_read(Stage* stage, int* launches, double* total_ms);
+
+/* Test and measurement support: phase-boundary timestamps of the last
+ * single-launch forward, recorded only when STAGE_PS_TRACE=1 was set in the
+ * environment at stage_create.  out_host receives [workgroups][n_layers][10]
+ * readings of the 100 MHz device real-time counter taken by each workgroup at:
+ * layer start, q|k|v end, attention start, attention end, o start, o end,
+ * gate|up start, gate|up end, down start, down end.  n = capacity of out_host
+ * in entries.  Synchronizes the device. */
+int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n);
 
 /* Bytes of device memory the stage holds for weights (packed codes + scales +
  * norm weights), as stored. */

@@ -21,9 +21,9 @@ EXPORTS = (
     "stage_create", "stage_destroy", "kv_state_alloc", "kv_state_free", "kv_state_reset",
     "kv_append", "kv_length", "kv_read", "kv_truncate", "stage_forward",
     "stage_debug_dequant", "stage_weight_bytes", "stage_last_error",
-    "stage_profile_enable", "stage_profile_read",
+    "stage_profile_enable", "stage_profile_read", "stage_debug_phase_trace",
 )
-KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4}
+KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "persistent": 5}
 
 
 class StageConfig(ctypes.Structure):
@@ -82,6 +82,7 @@ def load() -> ctypes.CDLL:
         "stage_last_error": (ctypes.c_char_p, []),
         "stage_profile_enable": (I, [V, I]),
         "stage_profile_read": (I, [V, P(I), P(ctypes.c_double)]),
+        "stage_debug_phase_trace": (I, [V, V, I]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

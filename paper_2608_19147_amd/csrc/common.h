@@ -83,6 +83,64 @@ struct AttnArgs {
     int nsplit_max;
 };
 
+// ---- persistent stage kernel (persistent.hip)
+constexpr int PS_MAX_M = 1;          // rows of one persistent forward (decode of one slot)
+constexpr int PS_KCHUNK = 2048;      // row-layout K is padded to a multiple of this
+constexpr int PS_MAXU = 64;          // units (rows or row pairs) one wave may own in a phase
+constexpr int PS_WAVES_PER_WG = 4;   // waves per persistent workgroup
+
+// Row layout: w [N][kc][16 bytes] (chunk c of row n holds k in [32c, 32c+32),
+// same nibble order as PackedMat), s [N][ng] fp16 scales.
+struct PsMat {
+    const uint8_t* w;
+    const uint16_t* s;
+};
+
+struct PsLayer {
+    PsMat qkv, o, gu, d;                 // gu rows interleave gate (2f) and up (2f+1)
+    const uint16_t* attn_norm;
+    const uint16_t* ffn_norm;
+};
+
+struct PsArgs {
+    const PsLayer* layers;               // device array
+    int n_layers;
+    int H, Hq, Hkv, F, QD, NQKV;
+    int kc_h, kc_q, kc_f;                // chunks per row for K = H, Hq*D, F
+    int ng_h, ng_q, ng_f;                // scale groups per row
+    int gchunks;
+    float eps;
+    int act_dt, kv_dt;
+    const void* hidden_in;
+    void* hidden_out;
+    int M;
+    float *x, *qkv, *o, *act;            // fp32 [64][...] rows, exchanged coherently
+    MetaDev meta;
+    const float2* rope;
+    float qscale;
+    float* apart;
+    unsigned* acnt;
+    int nsplit_max;
+    unsigned long long* bar;             // 16 barrier counters, 64 words apart
+    unsigned long long bar_epoch;        // barriers completed by earlier launches
+    unsigned* err;                       // set when a barrier wait gives up
+    unsigned long long* trace;           // optional [nwg][10 * n_layers] real-time stamps
+    float* junk;                         // >= 128 floats: per-lane targets of discarded results
+};
+constexpr int PS_TRACE_PER_LAYER = 10;
+
+bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int M, int rows_per_item);
+// Private-segment (stack/scratch) bytes per lane of the instantiation for this
+// shape; the persistent path is only used when it is zero.
+size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int rows_per_item);
+size_t ps_lds_bytes(int H, int QD, int F, int kc_h, int kc_q, int kc_f, int D, int M);
+hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int rows_per_item, int nwg,
+                             size_t lds, hipStream_t st);
+hipError_t launch_repack_rows(const uint8_t* q, const uint16_t* s, int n, int k, int g, uint8_t* w_out, uint16_t* s_out,
+                              int kc, int ng, int row_off, int row_map, hipStream_t st);
+hipError_t launch_dequant_rows(const PsMat& m, int kc, int ng, int gchunks, int k, int row_off, int row_map, int n_rows,
+                               float* out, hipStream_t st);
+
 // Kernel launchers (kernels.hip).
 hipError_t launch_repack(const uint8_t* q, const uint16_t* s, int n, int k, int g,
                          uint8_t* w_out, uint16_t* s_out, int ntiles, int nchunk, int ngroups,

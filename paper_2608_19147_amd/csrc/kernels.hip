@@ -18,60 +18,9 @@
 //                and written to the cache by their owner.  Mask and causality
 //                decide visibility inside an online softmax (exp2 domain);
 //                partials are merged by the last split's workgroup.
-#include "common.h"
+#include "device.h"
 
 namespace stg {
-
-typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-
-// ------------------------------------------------------------------ conversions
-
-__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
-
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
-    u += 0x7fffu + ((u >> 16) & 1u);                                           // ties to even
-    return (uint16_t)(u >> 16);
-}
-
-__device__ __forceinline__ float f16_to_f32(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
-__device__ __forceinline__ uint16_t f32_to_f16(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
-
-__device__ __forceinline__ float load_val(const void* p, int dt, size_t i) {
-    if (dt == DT_F32) return ((const float*)p)[i];
-    const uint16_t b = ((const uint16_t*)p)[i];
-    return dt == DT_BF16 ? bf16_to_f32(b) : f16_to_f32(b);
-}
-
-__device__ __forceinline__ uint16_t to_half_bits(float f, int dt) { return dt == DT_BF16 ? f32_to_bf16(f) : f32_to_f16(f); }
-__device__ __forceinline__ float half_bits_to_f32(uint16_t b, int dt) { return dt == DT_BF16 ? bf16_to_f32(b) : f16_to_f32(b); }
-
-__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
-    return (uint32_t)f32_to_f16(lo) | ((uint32_t)f32_to_f16(hi) << 16);
-}
-
-// 16-byte chunk (32 codes) -> 16 fp16 pairs of consecutive k holding q = u - 8 exactly.
-__device__ __forceinline__ void unpack_chunk(const u32x4 w, half2_t* out) {
-    const half2_t sub = {(_Float16)1032.0f, (_Float16)1032.0f};
-    const half2_t s16 = {(_Float16)0.0625f, (_Float16)0.0625f};
-    const half2_t m72 = {(_Float16)-72.0f, (_Float16)-72.0f};
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-        const uint32_t x = w[d];
-        const uint32_t y = x >> 8;
-        const uint32_t p0 = (x & 0x000F000Fu) | 0x64006400u;   // 1024 + u      (k, k+1)
-        const uint32_t p1 = (x & 0x00F000F0u) | 0x64006400u;   // 1024 + 16 u   (k+2, k+3)
-        const uint32_t p2 = (y & 0x000F000Fu) | 0x64006400u;   //               (k+4, k+5)
-        const uint32_t p3 = (y & 0x00F000F0u) | 0x64006400u;   //               (k+6, k+7)
-        out[4 * d + 0] = __builtin_bit_cast(half2_t, p0) - sub;
-        out[4 * d + 1] = __builtin_elementwise_fma(__builtin_bit_cast(half2_t, p1), s16, m72);
-        out[4 * d + 2] = __builtin_bit_cast(half2_t, p2) - sub;
-        out[4 * d + 3] = __builtin_elementwise_fma(__builtin_bit_cast(half2_t, p3), s16, m72);
-    }
-}
 
 __device__ __forceinline__ int dest_row(int r, int row_off, int row_map) {
     if (row_map == 0) return row_off + r;
@@ -155,64 +104,6 @@ hipError_t launch_dequant(const PackedMat& m, int row_off, int row_map, int n_ro
     const size_t nc = (size_t)n_rows * m.nchunk;
     dequant_kernel<<<dim3((unsigned)((nc + 255) / 256)), dim3(256), 0, st>>>(m, row_off, row_map, n_rows, out);
     return hipGetLastError();
-}
-
-// ------------------------------------------------------------------ reductions
-
-template <int CTRL>
-__device__ __forceinline__ float dpp_f(float v) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
-}
-
-// Sum over the 16 lanes of a DPP row; every lane receives the identical value.
-__device__ __forceinline__ float sum16(float v) {
-    v += dpp_f<0xB1>(v);    // quad_perm [1,0,3,2]
-    v += dpp_f<0x4E>(v);    // quad_perm [2,3,0,1]
-    v += dpp_f<0x141>(v);   // row_half_mirror
-    v += dpp_f<0x140>(v);   // row_mirror
-    return v;
-}
-
-// Deterministic block sum (256 threads): fixed-order tree in LDS.
-__device__ __forceinline__ float block_sum256(float v, float* buf) {
-    const int tid = threadIdx.x;
-    buf[tid] = v;
-    __syncthreads();
-#pragma unroll
-    for (int w = 128; w > 0; w >>= 1) {
-        if (tid < w) buf[tid] += buf[tid + w];
-        __syncthreads();
-    }
-    const float r = buf[0];
-    __syncthreads();
-    return r;
-}
-
-// ------------------------------------------------------------------ coherent exchange
-// Workgroups of one launch exchange split partials through device-scope
-// ("sc1") stores and loads, which bypass the per-XCD L2s; the writer waits for
-// its stores with a workgroup-scope release before taking the ticket.  This
-// avoids the whole-L2 write-back and invalidate of an agent-scope fence.
-
-__device__ __forceinline__ void store_coherent(float* p, float v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float load_coherent(const float* p) {
-    return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Returns true in exactly one workgroup: the last of `n` to arrive at counter *c,
-// which it resets.  Every thread of the workgroup must call it.
-__device__ __forceinline__ bool last_arrival(unsigned* c, unsigned n, int* flag) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");   // own coherent stores complete
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const unsigned prev = atomicAdd(c, 1u);
-        *flag = (prev == n - 1);
-        if (prev == n - 1) *c = 0u;                             // next launch starts from zero
-    }
-    __syncthreads();
-    return *flag != 0;
 }
 
 // ------------------------------------------------------------------ GEMV

@@ -62,6 +62,17 @@ struct Stage {
     bool meta_ev_used[META_RING] = {};
     int ring_i = 0;
     int64_t weight_bytes = 0;
+    // persistent-kernel weights (row layout) and barrier state
+    bool ps_ok = false;
+    int cpl_h = 0, cpl_q = 0, cpl_f = 0, kc_h = 0, kc_q = 0, kc_f = 0, ng_h = 0, ng_q = 0, ng_f = 0;
+    std::vector<PsLayer> ps_host;
+    PsLayer* ps_layers = nullptr;
+    unsigned long long* bar = nullptr;
+    unsigned* err = nullptr;
+    float* junk = nullptr;
+    unsigned long long bar_epoch = 0;
+    int ps_nwg = 0;
+    unsigned long long* trace = nullptr;   // phase stamps of the last persistent forward (STAGE_PS_TRACE=1)
     int prof_class = -1;
     std::vector<hipEvent_t> prof_ev;   // start/stop pairs
     size_t prof_used = 0;              // events recorded
@@ -144,9 +155,10 @@ int make_mat(Stage* st, DevMat& m, int n_rows_padded_tiles, int k, int g) {
     return STAGE_OK;
 }
 
-// Copy one canonical matrix into the tiled layout of `m` (rows placed per row_off / row_map).
+// Copy one canonical matrix into the tiled layout of `m` (rows placed per
+// row_off / row_map) and, when `pm` is given, into the row layout as well.
 int upload_mat(Stage* st, DevMat& m, const QuantMatrix& q, int on_device, int row_off, int row_map,
-               uint8_t* tmp_q, uint16_t* tmp_s, hipStream_t stream) {
+               uint8_t* tmp_q, uint16_t* tmp_s, hipStream_t stream, const PsMat* pm = nullptr, int kc = 0, int ng = 0) {
     const int g = st->cfg.group_size;
     const size_t qbytes = (size_t)q.n * ((q.k + 1) / 2);
     const size_t sbytes = (size_t)q.n * ((q.k + g - 1) / g) * 2;
@@ -160,7 +172,24 @@ int upload_mat(Stage* st, DevMat& m, const QuantMatrix& q, int on_device, int ro
     }
     HIP_TRY(launch_repack(qsrc, ssrc, q.n, q.k, g, (uint8_t*)m.pm.w, (uint16_t*)m.pm.s, m.pm.ntiles, m.pm.nchunk,
                           m.pm.ngroups, row_off, row_map, stream));
+    if (pm)
+        HIP_TRY(launch_repack_rows(qsrc, ssrc, q.n, q.k, g, (uint8_t*)pm->w, (uint16_t*)pm->s, kc, ng, row_off, row_map,
+                                   stream));
     if (!on_device) HIP_TRY(hipStreamSynchronize(stream));   // tmp buffers are reused by the next matrix
+    return STAGE_OK;
+}
+
+int make_rows(Stage* st, PsMat& pm, int n, int kc, int ng) {
+    uint8_t* w;
+    uint16_t* s;
+    int rc = st->alloc(&w, (size_t)n * kc * 16);
+    if (rc) return rc;
+    rc = st->alloc(&s, (size_t)n * ng);
+    if (rc) return rc;
+    HIP_TRY(hipMemset(w, 0x88, (size_t)n * kc * 16));
+    HIP_TRY(hipMemset(s, 0, (size_t)n * ng * 2));
+    pm.w = w;
+    pm.s = s;
     return STAGE_OK;
 }
 
@@ -296,9 +325,31 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         if (tmp_s) (void)hipFree(tmp_s);
     };
 
+    {
+        auto cpl = [](int k) { return (k + PS_KCHUNK - 1) / PS_KCHUNK; };
+        st->cpl_h = cpl(H);
+        st->cpl_q = cpl(QD);
+        st->cpl_f = cpl(F);
+        st->kc_h = st->cpl_h * 64;
+        st->kc_q = st->cpl_q * 64;
+        st->kc_f = st->cpl_f * 64;
+        const int gch = g / CHUNK_K;
+        st->ng_h = (st->kc_h + gch - 1) / gch;
+        st->ng_q = (st->kc_q + gch - 1) / gch;
+        st->ng_f = (st->kc_f + gch - 1) / gch;
+        const char* e = std::getenv("STAGE_PERSISTENT");
+        st->ps_ok = ps_supported(st->cpl_h, st->cpl_q, st->cpl_f, D, 1, 1) && !(e && atoi(e) == 0);
+        if (st->ps_ok) st->ps_host.resize(c.n_layers);
+    }
     for (int l = 0; l < c.n_layers; ++l) {
         LayerDev& L = st->layers[l];
         const LayerWeights& w = layers[l];
+        PsLayer* P = st->ps_ok ? &st->ps_host[l] : nullptr;
+        if (P && ((rc = make_rows(st, P->qkv, nqkv, st->kc_h, st->ng_h)) || (rc = make_rows(st, P->o, H, st->kc_q, st->ng_q)) ||
+                  (rc = make_rows(st, P->gu, 2 * F, st->kc_h, st->ng_h)) || (rc = make_rows(st, P->d, H, st->kc_f, st->ng_f)))) {
+            free_tmp();
+            return cleanup(rc);
+        }
         if ((rc = make_mat(st, L.qkv, (nqkv + 63) / 64, H, g)) || (rc = make_mat(st, L.o, (H + 63) / 64, QD, g)) ||
             (rc = make_mat(st, L.gu, (F + 31) / 32, H, g)) || (rc = make_mat(st, L.d, (H + 63) / 64, F, g))) {
             free_tmp();
@@ -308,13 +359,14 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         L.o.pm.n = H;
         L.gu.pm.n = 2 * F;
         L.d.pm.n = H;
-        if ((rc = upload_mat(st, L.qkv, w.wq, weights_on_device, 0, 0, tmp_q, tmp_s, s)) ||
-            (rc = upload_mat(st, L.qkv, w.wk, weights_on_device, QD, 0, tmp_q, tmp_s, s)) ||
-            (rc = upload_mat(st, L.qkv, w.wv, weights_on_device, QD + KVD, 0, tmp_q, tmp_s, s)) ||
-            (rc = upload_mat(st, L.o, w.wo, weights_on_device, 0, 0, tmp_q, tmp_s, s)) ||
-            (rc = upload_mat(st, L.gu, w.wg, weights_on_device, 0, 1, tmp_q, tmp_s, s)) ||
-            (rc = upload_mat(st, L.gu, w.wu, weights_on_device, 0, 2, tmp_q, tmp_s, s)) ||
-            (rc = upload_mat(st, L.d, w.wd, weights_on_device, 0, 0, tmp_q, tmp_s, s))) {
+        const int kh = st->kc_h, kq = st->kc_q, kf = st->kc_f, gh = st->ng_h, gq = st->ng_q, gf = st->ng_f;
+        if ((rc = upload_mat(st, L.qkv, w.wq, weights_on_device, 0, 0, tmp_q, tmp_s, s, P ? &P->qkv : nullptr, kh, gh)) ||
+            (rc = upload_mat(st, L.qkv, w.wk, weights_on_device, QD, 0, tmp_q, tmp_s, s, P ? &P->qkv : nullptr, kh, gh)) ||
+            (rc = upload_mat(st, L.qkv, w.wv, weights_on_device, QD + KVD, 0, tmp_q, tmp_s, s, P ? &P->qkv : nullptr, kh, gh)) ||
+            (rc = upload_mat(st, L.o, w.wo, weights_on_device, 0, 0, tmp_q, tmp_s, s, P ? &P->o : nullptr, kq, gq)) ||
+            (rc = upload_mat(st, L.gu, w.wg, weights_on_device, 0, 1, tmp_q, tmp_s, s, P ? &P->gu : nullptr, kh, gh)) ||
+            (rc = upload_mat(st, L.gu, w.wu, weights_on_device, 0, 2, tmp_q, tmp_s, s, P ? &P->gu : nullptr, kh, gh)) ||
+            (rc = upload_mat(st, L.d, w.wd, weights_on_device, 0, 0, tmp_q, tmp_s, s, P ? &P->d : nullptr, kf, gf))) {
             free_tmp();
             return cleanup(rc);
         }
@@ -329,6 +381,10 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
             return cleanup(fail(STAGE_E_HIP, "norm weight copy failed"));
         }
         st->weight_bytes += 4 * (int64_t)H;
+        if (P) {
+            P->attn_norm = L.attn_norm;
+            P->ffn_norm = L.ffn_norm;
+        }
     }
     if (hipStreamSynchronize(s) != hipSuccess) {
         free_tmp();
@@ -365,7 +421,7 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
     if ((rc = st->alloc(&st->x, (size_t)MAX_ROWS * H)) || (rc = st->alloc(&st->qkv, (size_t)MAX_ROWS * nqkv)) ||
         (rc = st->alloc(&st->attn, (size_t)MAX_ROWS * QD)) || (rc = st->alloc(&st->act, (size_t)MAX_ROWS * F)) ||
         (rc = st->alloc(&st->ssq, (size_t)MAX_ROWS * st->ntiles_h)) || (rc = st->alloc(&st->gpart, gpart)) ||
-        (rc = st->alloc(&st->apart, (size_t)MAX_ROWS * Hq * ATTN_MAX_SPLITS * (D + 2))) ||
+        (rc = st->alloc(&st->apart, (size_t)MAX_ROWS * Hq * ATTN_MAX_SPLITS * (D + 4))) ||
         (rc = st->alloc(&st->gcnt, max_tiles)) || (rc = st->alloc(&st->acnt, (size_t)MAX_ROWS * Hkv)))
         return cleanup(rc);
     if (hipMemset(st->gcnt, 0, max_tiles * sizeof(unsigned)) != hipSuccess ||
@@ -375,6 +431,32 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         if (hipEventCreateWithFlags(&st->meta_ev[i], hipEventDisableTiming) != hipSuccess)
             return cleanup(fail(STAGE_E_HIP, "event creation failed"));
     if ((rc = ensure_meta(st, 1 << 16))) return cleanup(rc);
+    if (st->ps_ok) {
+        if ((rc = st->alloc(&st->ps_layers, c.n_layers)) || (rc = st->alloc(&st->bar, 16 * 64)) || (rc = st->alloc(&st->err, 4)) ||
+            (rc = st->alloc(&st->junk, 256)))
+            return cleanup(rc);
+        if (hipMemcpy(st->ps_layers, st->ps_host.data(), sizeof(PsLayer) * c.n_layers, hipMemcpyHostToDevice) != hipSuccess ||
+            hipMemset(st->bar, 0, 16 * 64 * 8) != hipSuccess || hipMemset(st->err, 0, 4) != hipSuccess)
+            return cleanup(fail(STAGE_E_HIP, "persistent state init failed"));
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+            return cleanup(fail(STAGE_E_HIP, "CU count query failed"));
+        st->ps_nwg = cus;
+        {   // every wave must own at most PS_MAXU units in each GEMV phase
+            const int nw = cus * PS_WAVES_PER_WG;
+            for (int nu : {nqkv, H, F})
+                if ((nu + nw - 1) / nw > PS_MAXU) st->ps_ok = false;
+        }
+        if (const char* e = std::getenv("STAGE_PS_TRACE"))
+            if (atoi(e) && (rc = st->alloc(&st->trace, (size_t)cus * c.n_layers * PS_TRACE_PER_LAYER)))
+                return cleanup(rc);
+        // the single-launch forward is only used when its kernels need no private
+        // segment (no stack, no scratch spills) for this shape
+        const int gs = Hq / Hkv;
+        for (int rows : {gs}) {
+            if (ps_private_bytes(st->cpl_h, st->cpl_q, st->cpl_f, D, rows) != 0) st->ps_ok = false;
+        }
+    }
     if (hipDeviceSynchronize() != hipSuccess) return cleanup(fail(STAGE_E_HIP, "stage_create synchronize failed"));
     *out = st;
     return STAGE_OK;
@@ -388,9 +470,19 @@ int stage_destroy(Stage* stage) {
 
 int64_t stage_weight_bytes(const Stage* stage) { return stage ? stage->weight_bytes : -1; }
 
+int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n) {
+    if (!stage || !out_host) return fail(STAGE_E_INVALID, "NULL argument");
+    if (!stage->trace) return fail(STAGE_E_UNSUPPORTED, "phase trace is off (set STAGE_PS_TRACE=1 before stage_create)");
+    const size_t total = (size_t)stage->ps_nwg * stage->cfg.n_layers * PS_TRACE_PER_LAYER;
+    if (n < (long long)total) return fail(STAGE_E_CAPACITY, "trace needs " + std::to_string(total) + " entries");
+    HIP_TRY(hipSetDevice(stage->device));
+    HIP_TRY(hipMemcpy(out_host, stage->trace, total * 8, hipMemcpyDeviceToHost));
+    return STAGE_OK;
+}
+
 int stage_profile_enable(Stage* stage, int kernel_class) {
     if (!stage) return fail(STAGE_E_INVALID, "stage is NULL");
-    if (kernel_class < -1 || kernel_class > STAGE_KERNEL_DOWN) return fail(STAGE_E_INVALID, "unknown kernel class");
+    if (kernel_class < -1 || kernel_class > STAGE_KERNEL_PERSISTENT) return fail(STAGE_E_INVALID, "unknown kernel class");
     stage->prof_class = kernel_class;
     stage->prof_used = 0;
     return STAGE_OK;
@@ -549,10 +641,38 @@ int kv_read(KVState* kv, int layer, int slot, int start, int count, void* k_out,
 int stage_debug_dequant(Stage* stage, int layer, int which, float* out_host) {
     if (!stage || !out_host) return fail(STAGE_E_INVALID, "NULL argument");
     const StageConfig& c = stage->cfg;
+    const bool row_layout = which >= 8;
+    if (row_layout) which -= 8;
     if (layer < 0 || layer >= c.n_layers || which < 0 || which > 6) return fail(STAGE_E_INVALID, "layer or matrix index out of range");
+    if (row_layout && !stage->ps_ok) return fail(STAGE_E_UNSUPPORTED, "this stage keeps no row-layout weights");
     HIP_TRY(hipSetDevice(stage->device));
     const LayerDev& L = stage->layers[layer];
     const int QD = c.n_q_heads * c.head_dim, KVD = c.n_kv_heads * c.head_dim;
+    if (row_layout) {
+        const PsLayer& P = stage->ps_host[layer];
+        const PsMat* pm = nullptr;
+        int off = 0, map = 0, nr = 0, kc = stage->kc_h, ng = stage->ng_h, k = c.hidden;
+        switch (which) {
+            case 0: pm = &P.qkv; nr = QD; break;
+            case 1: pm = &P.qkv; off = QD; nr = KVD; break;
+            case 2: pm = &P.qkv; off = QD + KVD; nr = KVD; break;
+            case 3: pm = &P.o; nr = c.hidden; kc = stage->kc_q; ng = stage->ng_q; k = QD; break;
+            case 4: pm = &P.gu; map = 1; nr = c.ffn; break;
+            case 5: pm = &P.gu; map = 2; nr = c.ffn; break;
+            default: pm = &P.d; nr = c.hidden; kc = stage->kc_f; ng = stage->ng_f; k = c.ffn; break;
+        }
+        float* tmp = nullptr;
+        const size_t bytes = (size_t)nr * k * sizeof(float);
+        if (hipMalloc(&tmp, bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(STAGE_E_OOM, "staging allocation failed");
+        }
+        hipError_t e = launch_dequant_rows(*pm, kc, ng, c.group_size / CHUNK_K, k, off, map, nr, tmp, nullptr);
+        if (e == hipSuccess) e = hipMemcpy(out_host, tmp, bytes, hipMemcpyDeviceToHost);
+        (void)hipFree(tmp);
+        if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("debug dequant: ") + hipGetErrorString(e));
+        return STAGE_OK;
+    }
     const PackedMat* m = nullptr;
     int off = 0, map = 0, rows = 0;
     switch (which) {
@@ -707,6 +827,51 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
 
     const int act_dt = dt_code(c.act_dtype);
     const int nqkv = Hq * D + 2 * Hkv * D;
+
+    // ---------------- one persistent launch when the shape and row count allow it
+    if (st->ps_ok && ps_supported(st->cpl_h, st->cpl_q, st->cpl_f, D, M, max_rows_item) &&
+        (st->prof_class < 0 || st->prof_class == STAGE_KERNEL_PERSISTENT)) {
+        PsArgs a{};
+        a.layers = st->ps_layers;
+        a.n_layers = c.n_layers;
+        a.H = H; a.Hq = Hq; a.Hkv = Hkv; a.F = F; a.QD = Hq * D; a.NQKV = nqkv;
+        a.kc_h = st->kc_h; a.kc_q = st->kc_q; a.kc_f = st->kc_f;
+        a.ng_h = st->ng_h; a.ng_q = st->ng_q; a.ng_f = st->ng_f;
+        a.gchunks = c.group_size / CHUNK_K;
+        a.eps = c.rms_eps;
+        a.act_dt = act_dt;
+        a.kv_dt = dt_code(c.kv_dtype);
+        a.hidden_in = hidden_in;
+        a.hidden_out = hidden_out;
+        a.M = M;
+        a.x = st->x; a.qkv = st->qkv; a.o = st->attn; a.act = st->act;
+        a.meta = meta;
+        a.rope = st->rope;
+        a.qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
+        a.apart = st->apart;
+        a.acnt = st->acnt;
+        a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, st->ps_nwg / std::max(1, n_items * Hkv)));
+        if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, atoi(e)));
+        a.bar = st->bar;
+        a.bar_epoch = st->bar_epoch;
+        a.err = st->err;
+        a.trace = st->trace;
+        a.junk = st->junk;
+        const size_t lds = ps_lds_bytes(H, Hq * D, F, st->kc_h, st->kc_q, st->kc_f, D, M);
+        if (lds <= 160 * 1024) {
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, true, s));
+            hipError_t e = launch_persistent(a, st->cpl_h, st->cpl_q, st->cpl_f, D, max_rows_item, st->ps_nwg, lds, s);
+            if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("persistent launch: ") + hipGetErrorString(e));
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, false, s));
+            st->bar_epoch += (unsigned long long)(5 * c.n_layers - 1);
+            for (int r = 0; r < n_req; ++r) {
+                KVState* kv = reqs[r].state;
+                if (do_gather[r]) kv->cur = 1 - kv->cur;
+                kv->P += reqs[r].n_tokens;
+            }
+            return STAGE_OK;
+        }
+    }
     auto run_gemv = [&](const DevMat& m, GemvArgs a, size_t in_row_elems, size_t out_row_elems, size_t resid_row_elems,
                         int in_elem_bytes, int resid_elem_bytes) -> hipError_t {
         a.W = m.pm;

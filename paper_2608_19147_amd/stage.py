@@ -104,13 +104,24 @@ class Stage:
         check(self.lib.stage_profile_read(self.handle, ctypes.byref(n), ctypes.byref(ms)))
         return n.value, ms.value
 
+    def phase_trace(self) -> np.ndarray:
+        """[workgroups, layers, 10] device real-time stamps (100 MHz) of the last
+        single-launch forward (needs STAGE_PS_TRACE=1 at creation)."""
+        n = torch.cuda.get_device_properties(0).multi_processor_count * self.shape.n_layers * 10
+        out = np.empty(n, dtype=np.uint64)
+        check(self.lib.stage_debug_phase_trace(self.handle, out.ctypes.data, n))
+        return out.reshape(-1, self.shape.n_layers, 10)
+
     def new_state(self, n_slots: int, capacity: int) -> "KVState":
         return KVState(self, n_slots, capacity)
 
-    def debug_dequant(self, layer: int, which: str) -> np.ndarray:
+    def debug_dequant(self, layer: int, which: str, row_layout: bool = False) -> np.ndarray:
+        """The matrix as the kernels decode it (tiled layout, or the row layout
+        of the persistent kernel)."""
         n, k = self.shape.matrix_shapes()[which]
         out = np.empty((n, k), dtype=np.float32)
-        check(self.lib.stage_debug_dequant(self.handle, layer, MATRIX_NAMES.index(which), out.ctypes.data))
+        code = MATRIX_NAMES.index(which) + (8 if row_layout else 0)
+        check(self.lib.stage_debug_dequant(self.handle, layer, code, out.ctypes.data))
         return out
 
     def forward(self, requests: Sequence["Request"], hidden_in: torch.Tensor,
