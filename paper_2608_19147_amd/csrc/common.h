@@ -83,14 +83,17 @@ struct AttnArgs {
     int nsplit_max;
 };
 
-// ---- persistent stage kernel (persistent.hip)
-constexpr int PS_MAX_M = 1;          // rows of one persistent forward (decode of one slot)
+// ---- single-launch stage forward (persistent.hip)
+constexpr int PS_MAX_M = 1;          // rows of one single-launch forward (decode of one slot)
 constexpr int PS_KCHUNK = 2048;      // row-layout K is padded to a multiple of this
-constexpr int PS_MAXU = 64;          // units (rows or row pairs) one wave may own in a phase
-constexpr int PS_WAVES_PER_WG = 4;   // waves per persistent workgroup
+constexpr int SK_CW = 4;             // compute waves per workgroup (plus one control wave)
+constexpr int SK_SLOT = 1024;        // bytes per ring slot: one 16-byte load per lane
+constexpr int SK_TMAX = 16;          // cache-row slot pairs (K, V) per compute wave per layer
 
 // Row layout: w [N][kc][16 bytes] (chunk c of row n holds k in [32c, 32c+32),
-// same nibble order as PackedMat), s [N][ng] fp16 scales.
+// same nibble order as PackedMat), s [N][ng] fp16 scales.  The q|k|v matrix
+// stores each head's rows d and d + D/2 next to each other (row 2d and 2d + 1
+// of the head's block), so one workgroup owns both rows of every rotary pair.
 struct PsMat {
     const uint8_t* w;
     const uint16_t* s;
@@ -108,38 +111,69 @@ struct PsArgs {
     int H, Hq, Hkv, F, QD, NQKV;
     int kc_h, kc_q, kc_f;                // chunks per row for K = H, Hq*D, F
     int ng_h, ng_q, ng_f;                // scale groups per row
-    int gchunks;
+    int gchunks;                         // chunks per scale group
     float eps;
     int act_dt, kv_dt;
     const void* hidden_in;
     void* hidden_out;
-    int M;
-    float *x, *qkv, *o, *act;            // fp32 [64][...] rows, exchanged coherently
+    int rpw_qkv, rpw_h, rpw_gu;          // rows per workgroup: q|k|v, o and down, gate|up
+    float* x;                            // [H] fp32 residual stream, exchanged coherently
+    float* qkv;                          // [NQKV] fp32: rotated q, rotated k, v
+    uint16_t* o;                         // [QD] fp16 attention output
+    uint16_t* act;                       // [F] fp16 SwiGLU output
     MetaDev meta;
     const float2* rope;
-    float qscale;
-    float* apart;
-    unsigned* acnt;
-    int nsplit_max;
+    float qscale;                        // log2(e) / sqrt(D)
+    int nsplit, split_len, att_T;        // splits per kv head (power of two), cache rows per split, slot pairs per wave
+    float* apart;                        // [Hkv][nsplit][Hq/Hkv][D + 4] split partials
+    unsigned* acnt;                      // [Hkv] arrival counters (only ever incremented)
     unsigned long long* bar;             // 16 barrier counters, 64 words apart
     unsigned long long bar_epoch;        // barriers completed by earlier launches
     unsigned* err;                       // set when a barrier wait gives up
     unsigned long long* trace;           // optional [nwg][10 * n_layers] real-time stamps
-    float* junk;                         // >= 128 floats: per-lane targets of discarded results
+    // LDS byte offsets
+    int l_xs, l_sb0, l_sb1, l_res, l_q, l_nkv, l_part, l_rope, l_end;
 };
 constexpr int PS_TRACE_PER_LAYER = 10;
 
-bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int M, int rows_per_item);
-// Private-segment (stack/scratch) bytes per lane of the instantiation for this
-// shape; the persistent path is only used when it is zero.
-size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int rows_per_item);
-size_t ps_lds_bytes(int H, int QD, int F, int kc_h, int kc_q, int kc_f, int D, int M);
-hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int rows_per_item, int nwg,
-                             size_t lds, hipStream_t st);
+// LDS layout of the stream kernel with `slots` ring slots per compute wave;
+// returns the total bytes.
+inline int ps_layout(PsArgs& a, int slots, int D, int gs) {
+    auto up = [](int v, int m) { return (v + m - 1) / m * m; };
+    const int kcmax = a.kc_h > a.kc_q ? (a.kc_h > a.kc_f ? a.kc_h : a.kc_f) : (a.kc_q > a.kc_f ? a.kc_q : a.kc_f);
+    int sb = a.rpw_qkv * a.ng_h;
+    sb = sb > a.rpw_h * a.ng_q ? sb : a.rpw_h * a.ng_q;
+    sb = sb > a.rpw_gu * a.ng_h ? sb : a.rpw_gu * a.ng_h;
+    sb = sb > a.rpw_h * a.ng_f ? sb : a.rpw_h * a.ng_f;
+    sb = up(sb * 2, SK_SLOT);
+    int rows = a.rpw_qkv > a.rpw_h ? a.rpw_qkv : a.rpw_h;
+    rows = rows > a.rpw_gu ? rows : a.rpw_gu;
+    int off = SK_CW * slots * SK_SLOT;
+    a.l_xs = off;   off += kcmax * 64;
+    a.l_sb0 = off;  off += sb;
+    a.l_sb1 = off;  off += sb;
+    a.l_res = off;  off += up(rows * 4, 16);
+    a.l_q = off;    off += gs * D * 4;
+    a.l_nkv = off;  off += 2 * D * 4;
+    a.l_part = off; off += SK_CW * gs * (D + 4) * 4;
+    a.l_rope = off; off += (D / 2) * 8;
+    a.l_end = off;
+    return off;
+}
+
+// Shapes with a single-launch instantiation: chunks-per-lane of K = H, Hq*D, F
+// (K / 2048), head_dim and query heads per kv head.
+bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int gs);
+// Private-segment (stack/scratch) bytes per lane of the instantiation; the
+// single launch is only used when this is zero.
+size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int gs);
+int ps_slots(int cpl_h, int cpl_q, int cpl_f, int D, int gs);   // ring slots per compute wave
+hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int gs, int nwg, size_t lds,
+                             hipStream_t st);
 hipError_t launch_repack_rows(const uint8_t* q, const uint16_t* s, int n, int k, int g, uint8_t* w_out, uint16_t* s_out,
-                              int kc, int ng, int row_off, int row_map, hipStream_t st);
+                              int kc, int ng, int row_off, int row_map, int head_dim, hipStream_t st);
 hipError_t launch_dequant_rows(const PsMat& m, int kc, int ng, int gchunks, int k, int row_off, int row_map, int n_rows,
-                               float* out, hipStream_t st);
+                               int head_dim, float* out, hipStream_t st);
 
 // Kernel launchers (kernels.hip).
 hipError_t launch_repack(const uint8_t* q, const uint16_t* s, int n, int k, int g,

@@ -1,747 +1,949 @@
-// Persistent stage kernel: every layer of one stage forward in a single
-// cooperative launch (one 256-thread workgroup per CU; one wave per SIMD, so
-// each wave owns the full unified register file).
+// Single-launch stage forward for one decode row (the "stream kernel").
 //
-// Phases per layer: q|k|v GEMV -> attention -> o GEMV (+ residual) ->
-// gate|up GEMV (+ SwiGLU) -> down GEMV (+ residual).  Consecutive phases are
-// separated by a grid barrier built from 16 monotonically increasing 64-bit
-// counters (each workgroup bumps one; wave 0 polls all of them with one
-// device-coherent load per lane).  Activations cross workgroups only through
-// device-coherent stores and loads, so no barrier writes back or invalidates
-// the per-XCD L2s.
+// One workgroup per CU, made of SK_CW compute waves and one control wave.
 //
-// GEMV phases: a wave owns whole weight rows (all of K), so a row's result is
-// final inside the wave and no split-K exchange exists.  Lane l reads chunks
-// l, l+64, ... of the row (16 bytes = 32 INT4 codes each; every wave load is
-// 1 KB contiguous).  The input vector sits in LDS as fp16 pairs laid out so
-// that consecutive lanes read consecutive 16 bytes.  Each wave issues the
-// loads of its first weight batch of the next phase before it waits at the
-// barrier, so HBM keeps streaming while the grid synchronizes, and
-// double-buffers batches inside a phase.
+// Compute waves read every byte the step needs exactly once, in one fixed
+// order per wave: for each layer, the wave's q|k|v weight rows, its cache rows
+// (K, V) of the layer's attention, then its o, gate|up and down weight rows.
+// Each wave keeps S direct-to-LDS loads (global_load_lds_dwordx4, 1 KB per
+// wave) in flight in a private LDS ring and refills a slot as soon as it has
+// consumed it, so the stream runs ahead across phase and layer boundaries
+// while the grid synchronizes.  Compute waves touch global memory only
+// through these loads, never wait for all of them, synchronize with the
+// control wave through s_barrier only, and read LDS through inline ds_read
+// with explicit waits (the compiler does not track direct-to-LDS loads).
+//
+// The control wave does the work on the critical path between phases: the
+// epilogues (rotary embedding, residual, SwiGLU), the device-coherent stores
+// of each phase's outputs, the grid barrier, loading and normalizing the next
+// phase's input into LDS, the next phase's scale rows, and the split-KV merge.
+//
+// GEMV phases: a wave owns whole weight rows (all of K); lane l multiplies
+// chunks l, l + 64, ... (32 codes each) with its slice of the input, which it
+// keeps in registers for the whole phase.  Attention: workgroup w < Hkv *
+// nsplit owns kv head w / nsplit and one contiguous split of the cached rows;
+// each compute wave reduces its share of the split to an online-softmax
+// partial, the control wave merges the waves (and this forward's own new row),
+// and the last workgroup of the kv head to arrive merges the splits.
 #include "device.h"
 
 namespace stg {
 
 typedef unsigned long long u64;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-constexpr int PS_THREADS = 256;
-constexpr int PS_WAVES = PS_THREADS / 64;
-static_assert(PS_WAVES == PS_WAVES_PER_WG, "host and kernel disagree on waves per workgroup");
-constexpr int PS_KG = PS_THREADS / 16;       // 16-lane key groups
-constexpr int PS_NC = 16;                    // barrier counters, 512 bytes apart
-constexpr unsigned PS_SPIN_LIMIT = 1u << 20; // a barrier that never completes gives up (error flag)
+constexpr int SK_THREADS = (SK_CW + 1) * 64;
+constexpr int SK_NC = 16;                    // barrier counters, 512 bytes apart
+constexpr unsigned SK_SPIN_LIMIT = 1u << 20; // a barrier that never completes gives up (error flag)
+
+// ------------------------------------------------------------------ LDS by address, explicit waits
+
+__device__ __forceinline__ void vm_wait_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+    static_assert(N >= 0 && N <= 63, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void lgkm_wait_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Workgroup barrier that does not wait for outstanding global loads.
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+__device__ __forceinline__ u32x4 lds_rd16(uint32_t a) {
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
+    return v;
+}
+__device__ __forceinline__ uint32_t lds_rdu16(uint32_t a) {
+    uint32_t v;
+    asm volatile("ds_read_u16 %0, %1" : "=v"(v) : "v"(a));
+    return v;
+}
+__device__ __forceinline__ void lds_wr4(uint32_t a, float v) {
+    asm volatile("ds_write_b32 %0, %1" ::"v"(a), "v"(v) : "memory");
+}
+__device__ __forceinline__ void lds_wr16(uint32_t a, f32x4 v) {
+    asm volatile("ds_write_b128 %0, %1" ::"v"(a), "v"(v) : "memory");
+}
+// After lgkm_wait_all: makes `v` depend on the wait, so no use moves above it.
+__device__ __forceinline__ void touch(u32x4& v) { asm volatile("" : "+v"(v)); }
+__device__ __forceinline__ void touch(uint32_t& v) { asm volatile("" : "+v"(v)); }
+
+// (x & m) | c for c free of m's bits, in one instruction (mask from an SGPR,
+// constant from a VGPR: a VOP3 encoding takes no literal operands).
+__device__ __forceinline__ uint32_t bfi(uint32_t m, uint32_t x, uint32_t c) {
+    uint32_t r;
+    asm volatile("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "s"(m), "v"(x), "v"(c));
+    return r;
+}
+
+// Direct-to-LDS load: lane l's 16 bytes at g land at LDS byte lds + 16 l (lds is wave-uniform).
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+    __builtin_amdgcn_global_load_lds(g, (lds_ptr_t)(uintptr_t)lds, 16, 0, 2 /* nt: streamed once */);
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+
+// ------------------------------------------------------------------ device-coherent exchange
 
 __device__ __forceinline__ u64 load_coherent_u64(const u64* p) {
     return __hip_atomic_load(const_cast<u64*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-
-// Grid barrier number `idx` of this launch.
-__device__ __forceinline__ void grid_sync(const PsArgs& a, int idx) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");   // own coherent stores have completed
-    __syncthreads();
-    if (threadIdx.x < 64) {
-        const int lane = threadIdx.x;
-        const unsigned n = gridDim.x;
-        if (lane == 0) atomicAdd(&a.bar[(blockIdx.x % PS_NC) * 64], 1ull);
-        const u64 per = (lane < PS_NC) ? (u64)((n - lane + PS_NC - 1) / PS_NC) : 0ull;
-        const u64 target = (a.bar_epoch + (u64)idx + 1ull) * per;
-        unsigned spins = 0;
-        while (true) {
-            bool ok = true;
-            if (lane < PS_NC) ok = load_coherent_u64(&a.bar[lane * 64]) >= target;
-            if (lane == PS_NC) ok = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u;
-            if (__all(ok)) break;
-            if (!__all(lane != PS_NC || ok)) break;            // another workgroup already gave up
-            __builtin_amdgcn_s_sleep(1);
-            if (++spins > PS_SPIN_LIMIT) {
-                if (lane == 0) atomicOr(a.err, 1u);
-                break;
-            }
-        }
-    }
-    __syncthreads();
+__device__ __forceinline__ void store_coherent_u32(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-
-// ------------------------------------------------------------------ weight batches
-
-template <int NCH>
-struct WBuf {
-    u32x4 w[NCH];
-    uint16_t s[NCH];
-};
-
-// Rows handled by wave `gw` of `nw` in a phase with `nu` units of `RU` rows:
-// units u = gw, gw + nw, ...; batch b holds units b*RB .. b*RB+RB-1 of the wave.
-template <int CPL, int RB, int RU>
-__device__ __forceinline__ void load_batch(WBuf<RB * RU * CPL>& B, const PsMat& W, int kc, int ng, int gchunks,
-                                           int gw, int nw, int nu, int b) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int j = 0; j < RB; ++j) {
-        int u = gw + nw * (b * RB + j);
-        if (u >= nu) u = nu - 1;                              // in-bounds dummy, result discarded
-#pragma unroll
-        for (int ru = 0; ru < RU; ++ru) {
-            const size_t row = (size_t)u * RU + ru;
-#pragma unroll
-            for (int i = 0; i < CPL; ++i) {
-                const int c = lane + 64 * i;
-                B.w[(j * RU + ru) * CPL + i] = __builtin_nontemporal_load((const u32x4*)(W.w + (row * kc + c) * 16));
-                B.s[(j * RU + ru) * CPL + i] = W.s[row * ng + c / gchunks];
-            }
-        }
-    }
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, size_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+// 16 bytes at byte offset `off`, device-coherent ("sc1": bypasses the per-XCD L2).
+__device__ __forceinline__ f32x4 load4_coherent(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 16));
 }
 
 template <int CTRL, int ROWS>
 __device__ __forceinline__ float dpp_rows(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, ROWS, 0xF, false));
 }
-
-// Wave-wide sum in a fixed order, returned as a wave-uniform value: row sums
-// (DPP within 16 lanes), then row 1 += row 0 and row 3 += row 2 (row_bcast15),
-// then rows 2-3 += row 1 (row_bcast31); lane 63 holds the total.
+// Wave-wide sum in a fixed order, returned as a wave-uniform value.
 __device__ __forceinline__ float wave_sum(float v) {
     v = sum16(v);
-    v += dpp_rows<0x142, 0xA>(v);
-    v += dpp_rows<0x143, 0xC>(v);
+    v += dpp_rows<0x142, 0xA>(v);     // row_bcast15: rows 1, 3 += rows 0, 2
+    v += dpp_rows<0x143, 0xC>(v);     // row_bcast31: rows 2, 3 += row 1
     return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
 }
+// Sum over aligned groups of N lanes (8 or 16); every lane of a group receives it.
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+    static_assert(N == 8 || N == 16, "group size");
+    v += dpp_f<0xB1>(v);
+    v += dpp_f<0x4E>(v);
+    v += dpp_f<0x141>(v);             // row_half_mirror: sums of 8
+    if constexpr (N == 16) v += dpp_f<0x140>(v);
+    return v;
+}
 
-// The wave's slice of the staged input: chunk lane + 64 i of every row, as 16
-// fp16 pairs per chunk.  Loaded from LDS once per phase when it fits registers.
-template <int MT, int CPL>
-struct XSlice {
-    u32x4 q[MT][CPL][4];
-};
-
-template <int MT, int CPL>
-__device__ __forceinline__ void load_xslice(XSlice<MT, CPL>& X, const uint32_t* xs, int kc, int M) {
+// Grid barrier number `idx` of this launch (control wave only).  Returns false
+// once any workgroup has given up waiting; the error flag stays set.
+__device__ __forceinline__ bool grid_sync(const PsArgs& a, int idx) {
     const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-        for (int i = 0; i < CPL; ++i)
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4)
-                X.q[m][i][q4] = (m < M) ? *(const u32x4*)&xs[(((size_t)m * 4 + q4) * kc + lane + 64 * i) * 4]
-                                        : u32x4{0u, 0u, 0u, 0u};
-}
-
-// Dot products of one batch with the input slice (registers when XREG, else
-// LDS); returns wave-uniform row sums in out[row][m].  Each 32-code chunk uses
-// four independent accumulators (one per dword of codes) to keep the dot2
-// chains short.
-template <int MT, int CPL, int RB, int RU, bool XREG>
-__device__ __forceinline__ void dot_batch(const WBuf<RB * RU * CPL>& B, const XSlice<MT, CPL>& X, const uint32_t* xs,
-                                          int kc, int M, float (&out)[RB * RU][MT]) {
-    const int lane = threadIdx.x & 63;
-    float acc[RB * RU][MT];
-#pragma unroll
-    for (int r = 0; r < RB * RU; ++r)
-#pragma unroll
-        for (int m = 0; m < MT; ++m) acc[r][m] = 0.f;
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-        u32x4 xq[MT][4];
-#pragma unroll
-        for (int m = 0; m < MT; ++m)
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                if constexpr (XREG) {
-                    xq[m][q4] = X.q[m][i][q4];
-                } else {
-                    xq[m][q4] = (m < M) ? *(const u32x4*)&xs[(((size_t)m * 4 + q4) * kc + lane + 64 * i) * 4]
-                                        : u32x4{0u, 0u, 0u, 0u};
-                }
-            }
-#pragma unroll
-        for (int r = 0; r < RB * RU; ++r) {
-            half2_t wq[16];
-            unpack_chunk(B.w[r * CPL + i], wq);
-            const float sc = f16_to_f32(B.s[r * CPL + i]);
-#pragma unroll
-            for (int m = 0; m < MT; ++m) {
-                if (m < M) {
-                    float d4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-#pragma unroll
-                        for (int q4 = 0; q4 < 4; ++q4) {
-                            const uint32_t xe = xq[m][q4][e];
-                            d4[q4] = __builtin_amdgcn_fdot2(wq[4 * q4 + e], __builtin_bit_cast(half2_t, xe), d4[q4], false);
-                        }
-                    acc[r][m] += sc * ((d4[0] + d4[1]) + (d4[2] + d4[3]));
-                }
-            }
-        }
-    }
-#pragma unroll
-    for (int r = 0; r < RB * RU; ++r)
-#pragma unroll
-        for (int m = 0; m < MT; ++m) out[r][m] = (m < M) ? wave_sum(acc[r][m]) : 0.f;
-}
-
-// ------------------------------------------------------------------ input staging
-
-// Index of the uint32 holding fp16 pair p (k = 2p, 2p+1) of row m in the staged input.
-__device__ __forceinline__ int xs_index(int m, int p, int kc) {
-    const int c = p >> 4, pc = p & 15;
-    return (((m * 4 + (pc >> 2)) * kc + c) << 2) + (pc & 3);
-}
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-// Buffer resource over `bytes` bytes at p (raw dwords; out-of-range loads return 0).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, size_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
-}
-
-// 16 bytes at byte offset `off`, device-coherent ("sc1": bypasses the per-XCD L2).
-__device__ __forceinline__ f32x4 load4_coherent(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 16));
-}
-
-// Stage M rows of length K (a multiple of 8, padded to kc chunks with zeros)
-// as fp16 pairs.  src_kind 0: fp32 rows written by other workgroups of this
-// launch (coherent 16-byte loads, all issued before any is used, 8 per thread
-// at a time); src_kind 1: act-dtype rows written before the launch.  With
-// gamma, rows are RMS-normalized (x * rsqrt(mean(x^2) + eps) * gamma) and the
-// fp32 input is also kept in xres[m][K] for the residual epilogues.
-__device__ void stage_input(const void* src, int src_kind, int src_dt, int ld, int M, int K, int kc,
-                            const uint16_t* gamma, int gamma_dt, float eps, uint32_t* xs, float* xres, float* red) {
-    const int tid = threadIdx.x;
-    const int npair = kc * 16;
-    const int n4 = M * (K / 4);                      // 4-value items over all rows
-    // padding pairs of every row are zero
-    for (int idx = tid; idx < M * (npair - K / 2); idx += PS_THREADS) {
-        const int m = idx / (npair - K / 2), p = K / 2 + idx % (npair - K / 2);
-        xs[xs_index(m, p, kc)] = 0u;
-    }
-    auto put = [&](int it, f32x4 v) {                // item it = 4 values of row m
-        const int m = it / (K / 4), k = 4 * (it % (K / 4));
-        if (gamma) {
-            *(f32x4*)&xres[m * K + k] = v;
-        } else {
-            xs[xs_index(m, k / 2, kc)] = pack_f16x2(v[0], v[1]);
-            xs[xs_index(m, k / 2 + 1, kc)] = pack_f16x2(v[2], v[3]);
-        }
-    };
-    if (src_kind == 0) {
-        const __amdgpu_buffer_rsrc_t r = make_rsrc(src, (size_t)M * ld * 4);
-        constexpr int B = 8;
-        for (int base = 0; base < n4; base += B * PS_THREADS) {
-            f32x4 v[B];
-#pragma unroll
-            for (int u = 0; u < B; ++u) {
-                const int it = base + u * PS_THREADS + tid;
-                const int m = it / (K / 4), k = 4 * (it % (K / 4));
-                v[u] = load4_coherent(r, it < n4 ? (m * ld + k) * 4 : 0);
-            }
-#pragma unroll
-            for (int u = 0; u < B; ++u) {
-                const int it = base + u * PS_THREADS + tid;
-                if (it < n4) put(it, v[u]);
-            }
-        }
-    } else {
-        for (int it = tid; it < n4; it += PS_THREADS) {
-            const int m = it / (K / 4), k = 4 * (it % (K / 4));
-            const u32x2 h = *(const u32x2*)((const uint16_t*)src + (size_t)m * ld + k);
-            f32x4 v;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t w = h[e >> 1];
-                v[e] = half_bits_to_f32((uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFFu)), src_dt);
-            }
-            put(it, v);
-        }
-    }
-    __syncthreads();
-    if (gamma) {
-        for (int m = 0; m < M; ++m) {
-            float ss = 0.f;
-            for (int k = tid; k < K; k += PS_THREADS) ss += xres[m * K + k] * xres[m * K + k];
-            red[tid] = ss;
-            __syncthreads();
-            for (int w = PS_THREADS / 2; w > 0; w >>= 1) {
-                if (tid < w) red[tid] += red[tid + w];
-                __syncthreads();
-            }
-            if (tid == 0) red[PS_THREADS + m] = rsqrtf(red[0] / (float)K + eps);
-            __syncthreads();
-        }
-        for (int idx = tid; idx < M * (K / 2); idx += PS_THREADS) {
-            const int m = idx / (K / 2), p = idx % (K / 2);
-            const int k = 2 * p;
-            const float rs = red[PS_THREADS + m];
-            const uint32_t gw = *(const uint32_t*)(gamma + k);
-            const float v0 = (xres[m * K + k] * rs) * half_bits_to_f32((uint16_t)(gw & 0xFFFFu), gamma_dt);
-            const float v1 = (xres[m * K + k + 1] * rs) * half_bits_to_f32((uint16_t)(gw >> 16), gamma_dt);
-            xs[xs_index(m, p, kc)] = pack_f16x2(v0, v1);
-        }
-    }
-    __syncthreads();
-}
-
-// ------------------------------------------------------------------ GEMV phase
-
-enum PsEpi : int { PE_QKV = 0, PE_RESID = 1, PE_SWIGLU = 2 };
-
-
-// One GEMV phase of a workgroup.  Wave gw owns units gw, gw + nw, ... and
-// streams them in batches of RB units, two batches in flight (slot 0 was
-// issued before the barrier).  The streaming loop issues every load on every
-// path (refills past the last batch re-read the wave's last batch) and keeps
-// results in LDS, so the compiler waits for exactly the batch it consumes.
-// The epilogue (residual, SwiGLU, stores) runs once per workgroup afterwards.
-// res: LDS [PS_WAVES][PS_MAXU][RU][MT] floats.
-template <int MT, int CPL, int RB, int RU, int EPI>
-__device__ __forceinline__ void gemv_phase(const PsArgs& a, const PsMat& W, int kc, int ng, int nu,
-                                           WBuf<RB * RU * CPL>& A, const uint32_t* xs, const float* xres,
-                                           float* res, bool last_layer) {
-    const int wave = threadIdx.x >> 6;
-    const int gw = blockIdx.x * PS_WAVES + wave;
-    const int nw = gridDim.x * PS_WAVES;
-    const int units_w = (gw < nu) ? (nu - gw + nw - 1) / nw : 0;
-    const int nb = (units_w + RB - 1) / RB;
-    const int M = a.M;
-    constexpr bool XREG = (MT * CPL <= 4);
-    XSlice<MT, (XREG ? CPL : 1)> X;
-    if constexpr (XREG) load_xslice<MT, CPL>(X, xs, kc, M);
-    float* wres = res + wave * PS_MAXU * RU * MT;
-    auto finish = [&](const WBuf<RB * RU * CPL>& buf, int b) {
-        float v[RB * RU][MT];
-        if constexpr (XREG)
-            dot_batch<MT, CPL, RB, RU, true>(buf, X, xs, kc, M, v);
-        else
-            dot_batch<MT, CPL, RB, RU, false>(buf, *(const XSlice<MT, CPL>*)nullptr, xs, kc, M, v);
-#pragma unroll
-        for (int j = 0; j < RB; ++j) {
-            const int lu = b * RB + j;
-            if (lu < units_w) {                                  // wave-uniform; LDS only
-#pragma unroll
-                for (int r = 0; r < RU; ++r)
-#pragma unroll
-                    for (int m = 0; m < MT; ++m) wres[(lu * RU + r) * MT + m] = v[j * RU + r][m];
-            }
-        }
-    };
-    WBuf<RB * RU * CPL> B;
-    load_batch<CPL, RB, RU>(B, W, kc, ng, a.gchunks, gw, nw, nu, min(1, max(nb - 1, 0)));
-    for (int b0 = 0; b0 < nb; b0 += 2) {
-        finish(A, b0);
-        load_batch<CPL, RB, RU>(A, W, kc, ng, a.gchunks, gw, nw, nu, min(b0 + 2, max(nb - 1, 0)));
-        finish(B, b0 + 1);
-        load_batch<CPL, RB, RU>(B, W, kc, ng, a.gchunks, gw, nw, nu, min(b0 + 3, max(nb - 1, 0)));
-    }
-    __syncthreads();
-    // ---- epilogue: one pass over the workgroup's results
-    const int maxu = (nu + nw - 1) / nw;
-    for (int idx = threadIdx.x; idx < PS_WAVES * maxu * M; idx += PS_THREADS) {
-        const int w = idx / (maxu * M), lu = (idx / M) % maxu, m = idx % M;
-        const int u = blockIdx.x * PS_WAVES + w + nw * lu;
-        if (u >= nu) continue;
-        const float* rv = res + (w * PS_MAXU + lu) * RU * MT;
-        if constexpr (EPI == PE_QKV) {
-            store_coherent(&a.qkv[(size_t)m * a.NQKV + u], rv[m]);
-        } else if constexpr (EPI == PE_RESID) {
-            const float xn = xres[m * a.H + u] + rv[m];
-            store_coherent(&a.x[(size_t)m * a.H + u], xn);
-            if (last_layer) ((uint16_t*)a.hidden_out)[(size_t)m * a.H + u] = to_half_bits(xn, a.act_dt);
-        } else {
-            const float gt = rv[m], up = rv[MT + m];
-            store_coherent(&a.act[(size_t)m * a.F + u], (gt / (1.0f + expf(-gt))) * up);
+    vm_wait_all();                                         // own coherent stores are complete
+    if (lane == 0) atomicAdd(&a.bar[(blockIdx.x % SK_NC) * 64], 1ull);
+    const unsigned n = gridDim.x;
+    const u64 per = (lane < SK_NC) ? (u64)((n - lane + SK_NC - 1) / SK_NC) : 0ull;
+    const u64 target = (a.bar_epoch + (u64)idx + 1ull) * per;
+    unsigned spins = 0;
+    while (true) {
+        bool ok = true;
+        if (lane < SK_NC) ok = load_coherent_u64(&a.bar[lane * 64]) >= target;
+        if (lane == SK_NC) ok = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u;
+        if (__all(ok)) return true;
+        if (!__all(lane != SK_NC || ok)) return false;     // another workgroup already gave up
+        __builtin_amdgcn_s_sleep(1);
+        if (++spins > SK_SPIN_LIMIT) {
+            if (lane == 0) atomicOr(a.err, 1u);
+            return false;
         }
     }
 }
 
-// ------------------------------------------------------------------ attention phase
-
-// One (slot, kv head, split) unit; the last split of a (slot, kv head) merges.
-// Split partials are [m][h][split][D + 4] floats: max, sum, 2 pad, then D
-// outputs (16-byte aligned).
-template <int D, int RC>
-__device__ __forceinline__ void attn_unit(const PsArgs& a, int layer, int item, int g, int split, int nsplit_of_L,
-                                          float* lds) {
-    constexpr int EPL = D / 16;
-    constexpr int HALF = D / 2;
-    constexpr int PST = D + 4;
-    constexpr int KB = (RC * EPL > 32) ? 2 : 4;             // cache rows per key group per round
-    const ItemDev it = a.meta.items[item];
-    const ReqDev rq = a.meta.reqs[it.req];
-    const int b = it.slot;
-    const int P = rq.P, n = rq.n;
-    const int L = P + n;
-    int split_len = (L + nsplit_of_L - 1) / nsplit_of_L;
-    split_len = (split_len + PS_KG - 1) / PS_KG * PS_KG;
-    const int nsplit = (L + split_len - 1) / split_len;
-    if (split >= nsplit) return;
-    const int j0 = split * split_len, j1 = min(L, j0 + split_len);
-    const int tid = threadIdx.x, kg = tid >> 4, li = tid & 15, wv = tid >> 6;
-    const int Hq = a.Hq, Hkv = a.Hkv;
-    const int gs = Hq / Hkv;
-    const int R = gs * n;
-    const int jn0 = max(j0, P);                              // this forward's rows in [jn0, j1)
-    const int nn = max(0, j1 - jn0);
-
-    float* lo = lds;                                         // [PS_WAVES][RC][D]
-    float* lm = lo + PS_WAVES * RC * D;                      // [PS_WAVES][RC]
-    float* ll = lm + PS_WAVES * RC;
-    float* qs = ll + PS_WAVES * RC;                          // [R][D] raw q rows
-    float* kn = qs + R * D;                                  // [nn][D] raw k of the new rows
-    float* vn = kn + n * D;                                  // [nn][D] raw v
-    uint8_t* smask = (uint8_t*)(vn + n * D);                 // [256]
-    int16_t* stab = (int16_t*)(smask + 256);                 // [256]
-    int* flag = (int*)(stab + 256);
-
-    const size_t lstride = (size_t)rq.S * Hkv * rq.cap * D;
-    uint16_t* kl = rq.kc + (size_t)layer * lstride;
-    uint16_t* vl = rq.vc + (size_t)layer * lstride;
-    const uint8_t* mask = a.meta.masks + rq.mask_off + (size_t)b * rq.mask_len;
-    const int16_t* tab = rq.table + (size_t)b * rq.cap;
-    const int rowbase = rq.row0 + b * n;
-    const int d0 = li * EPL;
-    const int jc1 = min(j1, P);
-
-    // ---- one round of coherent 16-byte loads: q rows of this kv head group, new k and v rows
-    {
-        const __amdgpu_buffer_rsrc_t r = make_rsrc(a.qkv, (size_t)(rowbase + n) * a.NQKV * 4);
-        const int nq4 = R * D / 4, nk4 = nn * D / 4;
-        for (int x = tid; x < nq4 + 2 * nk4; x += PS_THREADS) {
-            int off;
-            float* dst;
-            if (x < nq4) {
-                const int rr = x / (D / 4), d = 4 * (x % (D / 4));
-                const int i = rr / gs, h = g * gs + (rr % gs);
-                off = ((rowbase + i) * a.NQKV + h * D + d) * 4;
-                dst = qs + rr * D + d;
-            } else {
-                const int y = (x - nq4) % nk4, isv = (x - nq4) / nk4;
-                const int i = (jn0 - P) + y / (D / 4), d = 4 * (y % (D / 4));
-                off = ((rowbase + i) * a.NQKV + (Hq + isv * Hkv + g) * D + d) * 4;
-                dst = (isv ? vn : kn) + (y / (D / 4)) * D + d;
-            }
-            *(f32x4*)dst = load4_coherent(r, off);
-        }
-    }
-    __syncthreads();
-
-    for (int r0 = 0; r0 < R; r0 += RC) {
-        float q[RC][EPL];
-        int qi[RC];
-#pragma unroll
-        for (int rr = 0; rr < RC; ++rr) {
-            const int r = r0 + rr;
-            qi[rr] = -1;
-#pragma unroll
-            for (int e = 0; e < EPL; ++e) q[rr][e] = 0.f;
-            if (r < R) {
-                const int i = r / gs;
-                const int pos = a.meta.positions[rowbase + i];
-                qi[rr] = i;
-#pragma unroll
-                for (int e = 0; e < EPL; ++e) {
-                    const int d = d0 + e;
-                    const bool lo_half = d < HALF;
-                    const float x = qs[r * D + d];
-                    const float xp = qs[r * D + (lo_half ? d + HALF : d - HALF)];
-                    const float2 cs = a.rope[(size_t)pos * HALF + (lo_half ? d : d - HALF)];
-                    const float y = lo_half ? (x * cs.x - xp * cs.y) : (x * cs.x + xp * cs.y);
-                    q[rr][e] = y * a.qscale;
-                }
-            }
-        }
-        float mx[RC], sl[RC], o[RC][EPL];
-#pragma unroll
-        for (int rr = 0; rr < RC; ++rr) {
-            mx[rr] = -INFINITY;
-            sl[rr] = 0.f;
-#pragma unroll
-            for (int e = 0; e < EPL; ++e) o[rr][e] = 0.f;
-        }
-        auto consume = [&](int j, const float* kf, const float* vf) {
-#pragma unroll
-            for (int rr = 0; rr < RC; ++rr) {
-                if (qi[rr] < 0) continue;
-                float sd = 0.f;
-#pragma unroll
-                for (int e = 0; e < EPL; ++e) sd += q[rr][e] * kf[e];
-                sd = sum16(sd);
-                if (j > P + qi[rr]) continue;
-                const float mn = fmaxf(mx[rr], sd);
-                const float corr = exp2f(mx[rr] - mn);
-                const float p = exp2f(sd - mn);
-                sl[rr] = sl[rr] * corr + p;
-#pragma unroll
-                for (int e = 0; e < EPL; ++e) o[rr][e] = o[rr][e] * corr + p * vf[e];
-                mx[rr] = mn;
-            }
-        };
-        // cached rows through the beam table, 256 at a time
-        for (int jb = j0; jb < jc1; jb += 256) {
-            const int nbk = min(256, jc1 - jb);
-            __syncthreads();
-            for (int x = tid; x < nbk; x += PS_THREADS) {
-                smask[x] = mask[jb + x];
-                stab[x] = tab[jb + x];
-            }
-            __syncthreads();
-            for (int x0 = kg; x0 < nbk; x0 += PS_KG * KB) {
-                uint16_t kb[KB][EPL], vb[KB][EPL];
-                bool vis[KB];
-#pragma unroll
-                for (int u = 0; u < KB; ++u) {
-                    const int x = x0 + u * PS_KG;
-                    vis[u] = (x < nbk) && smask[x] != 0;
-                    if (vis[u]) {
-                        const size_t off = (((size_t)stab[x] * Hkv + g) * rq.cap + (jb + x)) * D + d0;
-                        if constexpr (EPL == 8) {
-                            *(u32x4*)kb[u] = *(const u32x4*)(kl + off);
-                            *(u32x4*)vb[u] = *(const u32x4*)(vl + off);
-                        } else {
-                            *(u32x2*)kb[u] = *(const u32x2*)(kl + off);
-                            *(u32x2*)vb[u] = *(const u32x2*)(vl + off);
-                        }
-                    }
-                }
-#pragma unroll
-                for (int u = 0; u < KB; ++u) {
-                    if (!vis[u]) continue;
-                    float kf[EPL], vf[EPL];
-#pragma unroll
-                    for (int e = 0; e < EPL; ++e) {
-                        kf[e] = half_bits_to_f32(kb[u][e], a.kv_dt);
-                        vf[e] = half_bits_to_f32(vb[u][e], a.kv_dt);
-                    }
-                    consume(jb + x0 + u * PS_KG, kf, vf);
-                }
-            }
-        }
-        // this forward's rows: rotate k, round k and v to the cache dtype; the
-        // first row pass also appends them to the cache
-        for (int j = jn0 + kg; j < j1; j += PS_KG) {
-            const int i = j - P;
-            const int y = j - jn0;
-            const int pos = a.meta.positions[rowbase + i];
-            uint16_t kb[EPL], vb[EPL];
-            float kf[EPL], vf[EPL];
-#pragma unroll
-            for (int e = 0; e < EPL; ++e) {
-                const int d = d0 + e;
-                const bool lo_half = d < HALF;
-                const float x = kn[y * D + d];
-                const float xp = kn[y * D + (lo_half ? d + HALF : d - HALF)];
-                const float2 cs = a.rope[(size_t)pos * HALF + (lo_half ? d : d - HALF)];
-                const float yv = lo_half ? (x * cs.x - xp * cs.y) : (x * cs.x + xp * cs.y);
-                kb[e] = to_half_bits(yv, a.kv_dt);
-                vb[e] = to_half_bits(vn[y * D + d], a.kv_dt);
-                kf[e] = half_bits_to_f32(kb[e], a.kv_dt);
-                vf[e] = half_bits_to_f32(vb[e], a.kv_dt);
-            }
-            if (r0 == 0) {
-                const size_t off = (((size_t)b * Hkv + g) * rq.cap + j) * D + d0;
-#pragma unroll
-                for (int e = 0; e < EPL; ++e) {
-                    kl[off + e] = kb[e];
-                    vl[off + e] = vb[e];
-                }
-                if (layer == 0 && g == 0 && li == 0) rq.table[(size_t)b * rq.cap + j] = (int16_t)b;
-            }
-            if (mask[j] != 0) consume(j, kf, vf);
-        }
-        // merge the 4 key groups of each wave (lanes 16 apart), then the waves
-#pragma unroll
-        for (int rr = 0; rr < RC; ++rr) {
-#pragma unroll
-            for (int sh = 16; sh <= 32; sh <<= 1) {
-                const float m2 = __shfl_xor(mx[rr], sh);
-                const float l2 = __shfl_xor(sl[rr], sh);
-                const float mn = fmaxf(mx[rr], m2);
-                const float w1 = (mx[rr] == -INFINITY) ? 0.f : exp2f(mx[rr] - mn);
-                const float w2 = (m2 == -INFINITY) ? 0.f : exp2f(m2 - mn);
-#pragma unroll
-                for (int e = 0; e < EPL; ++e) {
-                    const float o2 = __shfl_xor(o[rr][e], sh);
-                    o[rr][e] = o[rr][e] * w1 + o2 * w2;
-                }
-                sl[rr] = sl[rr] * w1 + l2 * w2;
-                mx[rr] = mn;
-            }
-        }
-        if ((tid & 63) < 16) {
-#pragma unroll
-            for (int rr = 0; rr < RC; ++rr) {
-                if (li == 0) {
-                    lm[wv * RC + rr] = mx[rr];
-                    ll[wv * RC + rr] = sl[rr];
-                }
-#pragma unroll
-                for (int e = 0; e < EPL; ++e) lo[(wv * RC + rr) * D + d0 + e] = o[rr][e];
-            }
-        }
-        __syncthreads();
-        for (int idx = tid; idx < RC * D; idx += PS_THREADS) {
-            const int rr = idx / D, d = idx % D;
-            const int r = r0 + rr;
-            if (r >= R) continue;
-            float Mx = -INFINITY;
-            for (int w = 0; w < PS_WAVES; ++w) Mx = fmaxf(Mx, lm[w * RC + rr]);
-            float O = 0.f, S = 0.f;
-            for (int w = 0; w < PS_WAVES; ++w) {
-                const float mk = lm[w * RC + rr];
-                const float wt = (mk == -INFINITY) ? 0.f : exp2f(mk - Mx);
-                O += lo[(w * RC + rr) * D + d] * wt;
-                S += ll[w * RC + rr] * wt;
-            }
-            const int i = r / gs, h = g * gs + (r % gs);
-            const int m = rowbase + i;
-            float* pp = a.apart + (((size_t)m * Hq + h) * a.nsplit_max + split) * PST;
-            store_coherent(pp + 4 + d, O);
-            if (d == 0) {
-                store_coherent(pp, Mx);
-                store_coherent(pp + 1, S);
-            }
-        }
-        __syncthreads();
-    }
-
-    if (!last_arrival(&a.acnt[item * Hkv + g], (unsigned)nsplit, flag)) return;
-    // ---- merge the splits: weights from (max, sum) pairs, then 4 outputs per thread
-    float* wgt = lo;                       // [R][nsplit]
-    float* inv = wgt + R * nsplit;         // [R]
-    const __amdgpu_buffer_rsrc_t pr = make_rsrc(a.apart, (size_t)MAX_ROWS * Hq * a.nsplit_max * PST * 4);
-    for (int idx = tid; idx < R * nsplit; idx += PS_THREADS) {
-        const int r = idx / nsplit, s2 = idx % nsplit;
-        const int m = rowbase + r / gs, h = g * gs + (r % gs);
-        const f32x4 ms = load4_coherent(pr, (int)(((((size_t)m * Hq + h) * a.nsplit_max + s2) * PST) * 4));
-        wgt[idx] = ms[0];
-        inv[R + idx] = ms[1];
-    }
-    __syncthreads();
-    for (int r = tid; r < R; r += PS_THREADS) {
-        float Mx = -INFINITY;
-        for (int s2 = 0; s2 < nsplit; ++s2) Mx = fmaxf(Mx, wgt[r * nsplit + s2]);
-        float S = 0.f;
-        for (int s2 = 0; s2 < nsplit; ++s2) {
-            const float ms = wgt[r * nsplit + s2];
-            const float w = (ms == -INFINITY) ? 0.f : exp2f(ms - Mx);
-            wgt[r * nsplit + s2] = w;
-            S += inv[R + r * nsplit + s2] * w;
-        }
-        inv[r] = 1.0f / S;
-    }
-    __syncthreads();
-    for (int idx = tid; idx < R * D / 4; idx += PS_THREADS) {
-        const int r = idx / (D / 4), d = 4 * (idx % (D / 4));
-        const int i = r / gs, h = g * gs + (r % gs);
-        const int m = rowbase + i;
-        const size_t base = (((size_t)m * Hq + h) * a.nsplit_max) * PST + 4 + d;
-        f32x4 O = {0.f, 0.f, 0.f, 0.f};
-        int s2 = 0;
-        for (; s2 + 8 <= nsplit; s2 += 8) {
-            f32x4 b8[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) b8[e] = load4_coherent(pr, (int)((base + (size_t)(s2 + e) * PST) * 4));
-#pragma unroll
-            for (int e = 0; e < 8; ++e) O += b8[e] * wgt[r * nsplit + s2 + e];
-        }
-        for (; s2 < nsplit; ++s2) O += load4_coherent(pr, (int)((base + (size_t)s2 * PST) * 4)) * wgt[r * nsplit + s2];
-        float* dst = &a.o[(size_t)m * a.QD + (size_t)h * D + d];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) store_coherent(dst + e, O[e] * inv[r]);
-    }
-    __syncthreads();
-}
-
-// ------------------------------------------------------------------ the kernel
-
-// Phase-boundary timestamp (100 MHz real-time counter) for the optional trace.
 __device__ __forceinline__ void stamp(const PsArgs& a, int l, int e) {
-    if (a.trace && threadIdx.x == 0)
+    if (a.trace && (threadIdx.x & 63) == 0)
         a.trace[(size_t)blockIdx.x * a.n_layers * PS_TRACE_PER_LAYER + l * PS_TRACE_PER_LAYER + e] = wall_clock64();
 }
 
-template <int MT, int CPL_H, int CPL_Q, int CPL_F, int D, int RC>
-__global__ __launch_bounds__(PS_THREADS) void stage_persistent_kernel(PsArgs a) {
-    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-    float* xres = (float*)smem;                                  // [M][H] fp32 residual rows
-    float* red = xres + (size_t)a.M * a.H;                       // [PS_THREADS + 16]
-    float* res = red + PS_THREADS + 16;                          // [PS_WAVES][PS_MAXU][2][MT] row results
-    uint32_t* xs = (uint32_t*)(res + PS_WAVES * PS_MAXU * 2 * MT);  // staged GEMV input (fp16 pairs)
-    float* alds = (float*)xs;                                    // attention scratch (same space)
+// ------------------------------------------------------------------ row partition
 
-    // units per batch: about 8 chunks (8 KB per wave) per batch, two batches in flight
-    constexpr int RB_H = (CPL_H >= 8) ? 1 : 8 / CPL_H;           // rows of K = H
-    constexpr int RB_Q = (CPL_Q >= 8) ? 1 : 8 / CPL_Q;
-    constexpr int RB_G = (CPL_H >= 4) ? 1 : 4 / CPL_H;           // gate|up row pairs
-    constexpr int RB_F = (CPL_F >= 8) ? 1 : 8 / CPL_F;
+// Rows [first, first + count) of an N-row matrix owned by workgroup w (rpw
+// rows each) and, within it, by compute wave cw.
+struct Rows {
+    int first, count, local;   // local: index of `first` within the workgroup's rows
+};
+__device__ __forceinline__ Rows wave_rows(int N, int rpw, int w, int cw) {
+    const int rpc = (rpw + SK_CW - 1) / SK_CW;
+    const int wg0 = w * rpw;
+    const int wg1 = min(N, wg0 + rpw);
+    const int a0 = min(wg1, wg0 + cw * rpc);
+    const int a1 = min(wg1, a0 + rpc);
+    return Rows{a0, max(0, a1 - a0), a0 - wg0};
+}
 
-    const int gw = blockIdx.x * PS_WAVES + (threadIdx.x >> 6);
-    const int nw = gridDim.x * PS_WAVES;
-    const int n_items = a.meta.n_items;
+// ------------------------------------------------------------------ compute waves
+
+// Attention split geometry shared by both roles.
+template <int D>
+struct AttGeo {
+    static constexpr int LPR = D / 8;         // lanes per cache row (16 bytes each)
+    static constexpr int RPS = 64 / LPR;      // cache rows per slot
+};
+
+// Position bookkeeping of one compute wave's ring: p is the stream position
+// of the next slot to consume, ri its ring index; loads are issued strictly in
+// stream order, S positions ahead, so before consuming position q (with the
+// refill of q - 1 issued) exactly S - 1 younger loads may be in flight while
+// q <= pmax, and fewer near the end of the stream.
+struct Ring {
+    uint32_t base;            // LDS byte address of slot 0 + 16 * lane
+    int p, ri, pmax;
+    __device__ __forceinline__ uint32_t addr(int r) const { return base + (uint32_t)r * SK_SLOT; }
+    __device__ __forceinline__ static int next(int r, int S) { return r + 1 == S ? 0 : r + 1; }
+};
+
+// One GEMV segment: `nrows` rows (whole K each) from the ring, results to LDS res.
+//
+// INT4 decode: a dword of codes holds k..k+7; masking with 0x000F000F /
+// 0x00F000F0 (of x and x >> 8) and or-ing 0x6400 gives fp16 pairs equal to
+// 1024 + u (pairs (k, k+1), (k+4, k+5)) or 1024 + 16u (pairs (k+2, k+3),
+// (k+6, k+7)) with u = q + 8.  Their dot products with the input are
+// corrected once per chunk: sum q x = lo + hi / 16 - (1032 S_lo + 72 S_hi),
+// where S_lo, S_hi are the chunk's input sums over the two kinds of position.
+template <int CPL, int S, class Issue>
+__device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg, int nrows, int rlocal, int ng,
+                                         uint32_t sb, uint32_t xs, uint32_t res) {
+    if (nrows == 0) return;
+    // the input slice stays in registers for short rows; longer rows read it from LDS with each slot
+    constexpr bool XR = CPL <= 4;
+    constexpr int XN = XR ? CPL : 1;
+    constexpr int UNR = XR ? CPL : 1;                        // the chunk index only selects addresses when !XR
+    const int lane = threadIdx.x & 63;
+    const half2_t one2 = {(_Float16)1.0f, (_Float16)1.0f};
+    // chunk lane + 64 i of the input as 16 fp16 pairs, and its correction term
+    auto x_corr = [&](const u32x4 (&xc)[4]) {
+        float slo = 0.f, shi = 0.f;
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+            const uint32_t e0 = xc[q4][0], e1 = xc[q4][1], e2 = xc[q4][2], e3 = xc[q4][3];
+            slo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e0), one2, slo, false);
+            slo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e2), one2, slo, false);
+            shi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e1), one2, shi, false);
+            shi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e3), one2, shi, false);
+        }
+        return 1032.0f * slo + 72.0f * shi;
+    };
+    u32x4 xq[XN][4];
+    float corr[XN];
+    if constexpr (XR) {
+#pragma unroll
+        for (int i = 0; i < CPL; ++i)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) xq[i][q4] = lds_rd16(xs + 64 * (lane + 64 * i) + 16 * q4);
+        lgkm_wait_all();
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) {
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) touch(xq[i][q4]);
+            corr[i] = x_corr(xq[i]);
+        }
+    }
+    const int gstep = 128 / a.gchunks;                      // scale bytes between chunk i and i + 1 of a row
+    const uint32_t sl = sb + 2 * (uint32_t)(lane / a.gchunks);
+    const uint32_t lane16 = 16 * lane;
+    const uint32_t xl = xs + 64 * lane;                      // chunk `lane` of the input; chunk lane + 64 i is 4 KB i further
+    uint32_t magic = 0x64006400u;
+    asm volatile("" : "+v"(magic));                         // kept in a VGPR for v_bfi
+
+    // first slot of the segment
+    if (rg.p <= rg.pmax) vm_wait<S - 1>(); else vm_wait_all();
+    u32x4 cw = lds_rd16(rg.addr(rg.ri) + lane16);
+    uint32_t cs = lds_rdu16(sl + 2 * rlocal * ng);
+    u32x4 cx[4];
+    if constexpr (!XR) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) cx[q4] = lds_rd16(xl + 16 * q4);
+    }
+    lgkm_wait_all();
+    touch(cw);
+    touch(cs);
+    if constexpr (!XR) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) touch(cx[q4]);
+    }
+
+    for (int r = 0; r < nrows; ++r) {
+        const uint32_t srow = sl + 2 * (rlocal + r) * ng;
+        float acc = 0.f;
+#pragma unroll UNR
+        for (int i = 0; i < CPL; ++i) {
+            const bool more = (i + 1 < CPL) || (r + 1 < nrows);
+            const int rn = Ring::next(rg.ri, S);
+            u32x4 nw = {0u, 0u, 0u, 0u};
+            uint32_t ns = 0u;
+            u32x4 nx[4];
+            if (more) {                                   // read the next slot while this one computes
+                if (rg.p <= rg.pmax) vm_wait<S - 2>(); else vm_wait_all();
+                nw = lds_rd16(rg.addr(rn) + lane16);
+                ns = lds_rdu16(i + 1 < CPL ? srow + gstep * (i + 1) : srow + 2 * ng);
+                if constexpr (!XR) {
+                    const uint32_t xa = xl + 4096 * (i + 1 < CPL ? i + 1 : 0);
+#pragma unroll
+                    for (int q4 = 0; q4 < 4; ++q4) nx[q4] = lds_rd16(xa + 16 * q4);
+                }
+            }
+            issue(rg.addr(rg.ri));                        // refill the slot just read into registers
+            const u32x4(&xc)[4] = XR ? xq[XR ? i : 0] : cx;
+            const float ci = XR ? corr[XR ? i : 0] : x_corr(cx);
+            float lo0 = 0.f, lo1 = 0.f, hi0 = 0.f, hi1 = 0.f;
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const uint32_t x = cw[q4];
+                const uint32_t y = x >> 8;
+                const uint32_t p0 = bfi(0x000F000Fu, x, magic);
+                const uint32_t p1 = bfi(0x00F000F0u, x, magic);
+                const uint32_t p2 = bfi(0x000F000Fu, y, magic);
+                const uint32_t p3 = bfi(0x00F000F0u, y, magic);
+                const uint32_t x0 = xc[q4][0], x1 = xc[q4][1], x2 = xc[q4][2], x3 = xc[q4][3];
+                float& lo = (q4 & 1) ? lo1 : lo0;
+                float& hi = (q4 & 1) ? hi1 : hi0;
+                lo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p0), __builtin_bit_cast(half2_t, x0), lo, false);
+                lo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p2), __builtin_bit_cast(half2_t, x2), lo, false);
+                hi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p1), __builtin_bit_cast(half2_t, x1), hi, false);
+                hi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p3), __builtin_bit_cast(half2_t, x3), hi, false);
+            }
+            const float dq = __builtin_fmaf(hi0 + hi1, 0.0625f, (lo0 + lo1) - ci);
+            acc = __builtin_fmaf(f16_to_f32((uint16_t)cs), dq, acc);
+            if (more) {
+                lgkm_wait_all();
+                touch(nw);
+                touch(ns);
+                if constexpr (!XR) {
+#pragma unroll
+                    for (int q4 = 0; q4 < 4; ++q4) {
+                        touch(nx[q4]);
+                        cx[q4] = nx[q4];
+                    }
+                }
+            }
+            ++rg.p;
+            rg.ri = rn;
+            cw = nw;
+            cs = ns;
+        }
+        const float rs = wave_sum(acc);
+        if (lane == 0) lds_wr4(res + 4 * (rlocal + r), rs);
+    }
+}
+
+// This wave's cache rows of the layer's attention: T slot pairs (K then V),
+// RPS rows per slot, LPR lanes per row.  Writes the wave's online-softmax
+// partial (max, sum, unnormalized output per query head) to LDS part.
+template <int GS, int D, int S, class Issue>
+__device__ __forceinline__ void att_seg(const PsArgs& a, Issue& issue, Ring& rg, int T, uint32_t mbits, uint32_t qlds,
+                                        uint32_t part) {
+    constexpr int LPR = AttGeo<D>::LPR;
+    const int lane = threadIdx.x & 63;
+    const int li = lane % LPR;
+    const int kvdt = a.kv_dt;
+    float m[GS], l[GS], o[GS][8];
+#pragma unroll
+    for (int h = 0; h < GS; ++h) {
+        m[h] = -INFINITY;
+        l[h] = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
+    }
+    if (T > 0) {
+        u32x4 qv[GS][2];
+#pragma unroll
+        for (int h = 0; h < GS; ++h)
+#pragma unroll
+            for (int k = 0; k < 2; ++k) qv[h][k] = lds_rd16(qlds + 4 * (h * D + 8 * li + 4 * k));
+        lgkm_wait_all();
+        float qf[GS][8];
+#pragma unroll
+        for (int h = 0; h < GS; ++h)
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                touch(qv[h][k]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t qe = qv[h][k][e];   // a scalar copy: bit_cast of a vector element reads element 0
+                    qf[h][4 * k + e] = __builtin_bit_cast(float, qe);
+                }
+            }
+        for (int t = 0; t < T; ++t) {
+            if (rg.p <= rg.pmax) vm_wait<S - 2>(); else vm_wait_all();
+            const int r1 = Ring::next(rg.ri, S);
+            u32x4 kw = lds_rd16(rg.addr(rg.ri) + 16 * lane);
+            u32x4 vw = lds_rd16(rg.addr(r1) + 16 * lane);
+            lgkm_wait_all();
+            touch(kw);
+            touch(vw);
+            issue(rg.addr(rg.ri));
+            issue(rg.addr(r1));
+            rg.p += 2;
+            rg.ri = Ring::next(r1, S);
+            float kf[8], vf[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const uint32_t kd = kw[e >> 1], vd = vw[e >> 1];
+                kf[e] = half_bits_to_f32((uint16_t)((e & 1) ? (kd >> 16) : (kd & 0xFFFFu)), kvdt);
+                vf[e] = half_bits_to_f32((uint16_t)((e & 1) ? (vd >> 16) : (vd & 0xFFFFu)), kvdt);
+            }
+            const bool vis = (mbits >> t) & 1u;
+#pragma unroll
+            for (int h = 0; h < GS; ++h) {
+                float sd = 0.f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) sd = __builtin_fmaf(qf[h][e], kf[e], sd);
+                sd = group_sum<LPR>(sd);
+                if (vis) {
+                    const float mn = fmaxf(m[h], sd);
+                    const float corr = exp2f(m[h] - mn);
+                    const float pw = exp2f(sd - mn);
+                    l[h] = l[h] * corr + pw;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) o[h][e] = o[h][e] * corr + pw * vf[e];
+                    m[h] = mn;
+                }
+            }
+        }
+        // merge the row groups (lanes LPR, 2 LPR, ... apart)
+#pragma unroll
+        for (int h = 0; h < GS; ++h) {
+#pragma unroll
+            for (int sh = LPR; sh < 64; sh <<= 1) {
+                const float m2 = __shfl_xor(m[h], sh);
+                const float l2 = __shfl_xor(l[h], sh);
+                const float mn = fmaxf(m[h], m2);
+                const float w1 = (m[h] == -INFINITY) ? 0.f : exp2f(m[h] - mn);
+                const float w2 = (m2 == -INFINITY) ? 0.f : exp2f(m2 - mn);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float o2 = __shfl_xor(o[h][e], sh);
+                    o[h][e] = o[h][e] * w1 + o2 * w2;
+                }
+                l[h] = l[h] * w1 + l2 * w2;
+                m[h] = mn;
+            }
+        }
+    }
+    const int cw = threadIdx.x >> 6;
+    if (lane < LPR) {
+#pragma unroll
+        for (int h = 0; h < GS; ++h) {
+            const uint32_t base = part + 4 * ((cw * GS + h) * (D + 4));
+            lds_wr16(base + 16 + 32 * li, f32x4{o[h][0], o[h][1], o[h][2], o[h][3]});
+            lds_wr16(base + 32 + 32 * li, f32x4{o[h][4], o[h][5], o[h][6], o[h][7]});
+            if (li == 0) lds_wr16(base, f32x4{m[h], l[h], 0.f, 0.f});
+        }
+    }
+}
+
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
+__device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
+    constexpr int LPR = AttGeo<D>::LPR, RPS = AttGeo<D>::RPS;
+    const int lane = threadIdx.x & 63;
+    const int cw = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int w = blockIdx.x;
+    const int L = a.n_layers;
+
+    const Rows rq_ = wave_rows(a.NQKV, a.rpw_qkv, w, cw);
+    const Rows ro_ = wave_rows(a.H, a.rpw_h, w, cw);
+    const Rows rg_ = wave_rows(2 * a.F, a.rpw_gu, w, cw);
+    // attention rows of this wave: [j0, j0 + T * RPS) of this workgroup's split
+    const ReqDev& rq = a.meta.reqs[0];
+    const int P = rq.P;
+    const bool has_att = w < a.Hkv * a.nsplit;
+    const int T = has_att ? a.att_T : 0;
+    const int g = has_att ? w / a.nsplit : 0;
+    const int split = has_att ? w % a.nsplit : 0;
+    const int sp0 = split * a.split_len, sp1 = min(P, sp0 + a.split_len);
+    const int j0 = sp0 + cw * T * RPS;
+    const int b = a.meta.items[0].slot;
+    const u64 lstride_b = (u64)rq.S * a.Hkv * rq.cap * D * 2;
+    const uint8_t* kbase = (const uint8_t*)rq.kc;
+    const uint8_t* vbase = (const uint8_t*)rq.vc;
+    uint32_t mbits = 0u;
+    uint32_t aoff[SK_TMAX];       // per-lane byte offset of cache-row slot pair t within one layer
+    {
+        const uint8_t* mask = a.meta.masks + rq.mask_off + (size_t)b * rq.mask_len;
+        const int16_t* tab = rq.table + (size_t)b * rq.cap;
+#pragma unroll
+        for (int t = 0; t < SK_TMAX; ++t) {
+            const int j = j0 + t * RPS + lane / LPR;
+            const bool valid = t < T && j < sp1;
+            const int jj = valid ? j : 0;
+            const int phys = valid ? (int)tab[jj] : b;
+            if (valid && mask[jj] != 0) mbits |= 1u << t;
+            aoff[t] = (uint32_t)(((((u64)phys * a.Hkv + g) * rq.cap + jj) * D + 8 * (lane % LPR)) * 2);
+        }
+    }
+    // slots per segment of one layer: q|k|v rows, K/V slot pairs, o, gate|up, down rows
+    const int n0 = rq_.count * CPL_H, n1 = 2 * T, n2 = ro_.count * CPL_Q, n3 = rg_.count * CPL_H, n4 = ro_.count * CPL_F;
+    const int total = (n0 + n1 + n2 + n3 + n4) * L;
+    // The weight rows of one wave in one segment are contiguous in the row layout
+    // (kc = 64 * CPL chunks per row), so a segment streams one block of 1 KB slots.
+    typedef __attribute__((address_space(4))) const PsLayer* layer_cptr;   // never written during the launch:
+    const layer_cptr layers = (layer_cptr)a.layers;                          // scalar loads
+    int gl = 0, gs = -1, gleft = 0, gt = 0;
+    const uint8_t* gptr = nullptr;
+    auto next_seg = [&]() {
+        do {
+            if (++gs == 5) {
+                gs = 0;
+                ++gl;
+            }
+        } while (gl < L && (gs == 0 ? n0 : gs == 1 ? n1 : gs == 2 ? n2 : gs == 3 ? n3 : n4) == 0);
+        if (gl >= L) {
+            gleft = 0;
+            return;
+        }
+        gleft = gs == 0 ? n0 : gs == 1 ? n1 : gs == 2 ? n2 : gs == 3 ? n3 : n4;
+        gt = 0;
+        if (gs == 0) gptr = layers[gl].qkv.w + (u64)rq_.first * a.kc_h * 16;
+        else if (gs == 2) gptr = layers[gl].o.w + (u64)ro_.first * a.kc_q * 16;
+        else if (gs == 3) gptr = layers[gl].gu.w + (u64)rg_.first * a.kc_h * 16;
+        else if (gs == 4) gptr = layers[gl].d.w + (u64)ro_.first * a.kc_f * 16;
+    };
+    auto issue = [&](uint32_t dst) {
+        if (gleft == 0) return;
+        if (gs == 1) {
+            const int t = gt >> 1;
+            uint32_t off = aoff[0];
+#pragma unroll
+            for (int k = 1; k < SK_TMAX; ++k) {
+                int kk = k;
+                asm volatile("" : "+s"(kk));          // keeps this a select chain, not an indexed array
+                off = (t == kk) ? aoff[k] : off;
+            }
+            dma16(((gt & 1) ? vbase : kbase) + (u64)gl * lstride_b + off, dst);
+            ++gt;
+        } else {
+            dma16(gptr + 16 * lane, dst);
+            gptr += SK_SLOT;
+        }
+        if (--gleft == 0) next_seg();
+    };
+    next_seg();
+    vm_wait_all();                                          // table and mask reads are done
+    const uint32_t ring = lb + (uint32_t)(cw * S * SK_SLOT);
+    for (int k = 0; k < S; ++k) issue(ring + (uint32_t)k * SK_SLOT);
+
+    Ring rg{ring, 0, 0, total - S};
+    for (int l = 0; l < L; ++l) {
+        wg_barrier();                                       // input of q|k|v is staged
+        gemv_seg<CPL_H, S>(a, issue, rg, rq_.count, rq_.local, a.ng_h, lb + a.l_sb0, lb + a.l_xs, lb + a.l_res);
+        wg_barrier();                                       // q|k|v rows are in LDS
+        wg_barrier();                                       // q and the new row are staged
+        att_seg<GS, D, S>(a, issue, rg, T, mbits, lb + a.l_q, lb + a.l_part);
+        wg_barrier();                                       // wave partials are in LDS
+        wg_barrier();                                       // attention output is staged
+        gemv_seg<CPL_Q, S>(a, issue, rg, ro_.count, ro_.local, a.ng_q, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
+        wg_barrier();
+        wg_barrier();                                       // RMSNorm(x) is staged
+        gemv_seg<CPL_H, S>(a, issue, rg, rg_.count, rg_.local, a.ng_h, lb + a.l_sb0, lb + a.l_xs, lb + a.l_res);
+        wg_barrier();
+        wg_barrier();                                       // SwiGLU output is staged
+        gemv_seg<CPL_F, S>(a, issue, rg, ro_.count, ro_.local, a.ng_f, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
+        wg_barrier();
+    }
+}
+
+// ------------------------------------------------------------------ control wave
+
+// Scale rows [first, first + count) of a matrix with ng groups per row into LDS
+// (direct loads of 1 KB; the allocation is padded so the last one stays in bounds).
+__device__ __forceinline__ void load_scales(const uint16_t* s, int first, int count, int ng, uint32_t dst) {
+    const int lane = threadIdx.x & 63;
+    const uint8_t* src = (const uint8_t*)(s + (size_t)first * ng);
+    const int bytes = count * ng * 2;
+    for (int off = 0; off < bytes; off += SK_SLOT) dma16(src + off + 16 * lane, dst + off);
+}
+
+// Input of an RMSNorm'd GEMV: K values (fp32 coherent, or act dtype written
+// before the launch when src_dt != DT_F32) -> x * rsqrt(mean(x^2) + eps) * gamma
+// as fp16 in LDS xs; padding up to kpad is zeroed.
+template <int NT>
+__device__ __forceinline__ void stage_norm(const void* src, int src_dt, int K, int kpad, const uint16_t* gamma,
+                                           int gamma_dt, float eps, uint8_t* xs) {
+    const int lane = threadIdx.x & 63;
+    const int n4 = K / 4;
+    f32x4 v[NT];
+    if (src_dt == DT_F32) {
+        const __amdgpu_buffer_rsrc_t r = make_rsrc(src, (size_t)K * 4);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int it = lane + 64 * t;
+            v[t] = load4_coherent(r, it < n4 ? it * 16 : 0);
+        }
+    } else {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int it = lane + 64 * t;
+            const u32x2 h = *(const u32x2*)((const uint16_t*)src + 4 * (it < n4 ? it : 0));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t wd = h[e >> 1];
+                v[t][e] = half_bits_to_f32((uint16_t)((e & 1) ? (wd >> 16) : (wd & 0xFFFFu)), src_dt);
+            }
+        }
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+        if (lane + 64 * t < n4) ss += v[t][0] * v[t][0] + v[t][1] * v[t][1] + v[t][2] * v[t][2] + v[t][3] * v[t][3];
+    const float rs = rsqrtf(wave_sum(ss) / (float)K + eps);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        const int it = lane + 64 * t;
+        if (it < n4) {
+            const u32x2 gv = *(const u32x2*)(gamma + 4 * it);
+            float y[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t wd = gv[e >> 1];
+                y[e] = (v[t][e] * rs) * half_bits_to_f32((uint16_t)((e & 1) ? (wd >> 16) : (wd & 0xFFFFu)), gamma_dt);
+            }
+            *(u32x2*)(xs + 8 * it) = u32x2{pack_f16x2(y[0], y[1]), pack_f16x2(y[2], y[3])};
+        }
+    }
+    for (int it = n4 + lane; it < kpad / 4; it += 64) *(u32x2*)(xs + 8 * it) = u32x2{0u, 0u};
+}
+
+// Input of a plain GEMV: K fp16 values written coherently by this launch -> LDS xs.
+template <int NT>
+__device__ __forceinline__ void stage_plain(const uint16_t* src, int K, int kpad, uint8_t* xs) {
+    const int lane = threadIdx.x & 63;
+    const int n8 = K / 8;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(src, (size_t)K * 2);
+    constexpr int NB = NT < 16 ? NT : 16;                 // loads in flight per round
+#pragma unroll
+    for (int t0 = 0; t0 < NT; t0 += NB) {
+        f32x4 v[NB];
+#pragma unroll
+        for (int t = 0; t < NB; ++t) {
+            const int it = lane + 64 * (t0 + t);
+            v[t] = load4_coherent(r, (t0 + t < NT && it < n8) ? it * 16 : 0);
+        }
+#pragma unroll
+        for (int t = 0; t < NB; ++t) {
+            const int it = lane + 64 * (t0 + t);
+            if (t0 + t < NT && it < n8) *(f32x4*)(xs + 16 * it) = v[t];
+        }
+    }
+    for (int it = n8 + lane; it < kpad / 8; it += 64) *(f32x4*)(xs + 16 * it) = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
+__device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
+    const int lane = threadIdx.x & 63;
+    const int w = blockIdx.x;
+    const uint32_t lb = lds_addr(smem);
+    uint8_t* xs = smem + a.l_xs;
+    const float* res = (const float*)(smem + a.l_res);
+    float* qs = (float*)(smem + a.l_q);
+    float* nkv = (float*)(smem + a.l_nkv);
+    const float* part = (const float*)(smem + a.l_part);
+    const float2* rope = (const float2*)(smem + a.l_rope);
+    constexpr int NT_H = CPL_H * 8;          // float4 items per lane of a K = H input (K padded to 2048 * CPL_H)
+    constexpr int NT_Q = CPL_Q * 4;          // 8-value items per lane of the attention output
+    constexpr int NT_F = CPL_F * 4;
+    constexpr int OPL = GS * D / 64;         // merged outputs per lane
+    constexpr int LPH = D / OPL;             // lanes per query head in the merge
+    static_assert(OPL == 2 || OPL == 4 || OPL == 8, "merge layout");
+
+    const ReqDev& rq = a.meta.reqs[0];
+    const int P = rq.P;
+    const int b = a.meta.items[0].slot;
+    const int pos = a.meta.positions[0];
+    const uint8_t* mask = a.meta.masks + rq.mask_off + (size_t)b * rq.mask_len;
+    const bool has_att = w < a.Hkv * a.nsplit;
+    const int g = has_att ? w / a.nsplit : 0;
+    const int split = has_att ? w % a.nsplit : 0;
+    const bool owns_new = has_att && split == a.nsplit - 1;
+    const int KVD = a.Hkv * D;
+    const size_t lstride = (size_t)rq.S * a.Hkv * rq.cap * D;
+    const int hq = lane / LPH, d0 = (lane % LPH) * OPL;     // merge lane layout
+
+    // own rows of the residual stream (o and down rows of this workgroup)
+    const int xr0 = w * a.rpw_h;
+    const int nxr = max(0, min(a.H, xr0 + a.rpw_h) - xr0);
+    float xrow = 0.f;
+    if (lane < nxr) xrow = half_bits_to_f32(((const uint16_t*)a.hidden_in)[xr0 + lane], a.act_dt);
+    if (lane < D / 2) ((float2*)rope)[lane] = a.rope[(size_t)pos * (D / 2) + lane];
+    load_scales(a.layers[0].qkv.s, w * a.rpw_qkv, max(0, min(a.NQKV, (w + 1) * a.rpw_qkv) - w * a.rpw_qkv), a.ng_h,
+                lb + a.l_sb0);
+    stage_norm<NT_H>(a.hidden_in, a.act_dt, a.H, a.kc_h * 32, a.layers[0].attn_norm, a.act_dt, a.eps, xs);
+    bool ok = true;
     int bar = 0;
-
-    WBuf<RB_H * CPL_H> pq;                                       // q|k|v batch 0 of the coming layer
-    load_batch<CPL_H, RB_H, 1>(pq, a.layers[0].qkv, a.kc_h, a.ng_h, a.gchunks, gw, nw, a.NQKV, 0);
+    vm_wait_all();
+    wg_barrier();                                             // q|k|v input staged
 
     for (int l = 0; l < a.n_layers; ++l) {
         const PsLayer& Ly = a.layers[l];
         const bool last = (l == a.n_layers - 1);
         stamp(a, l, 0);
-        // ---- q|k|v = RMSNorm(x) Wqkv^T
-        if (l == 0)
-            stage_input(a.hidden_in, 1, a.act_dt, a.H, a.M, a.H, a.kc_h, Ly.attn_norm, a.act_dt, a.eps, xs, xres, red);
-        else
-            stage_input(a.x, 0, DT_F32, a.H, a.M, a.H, a.kc_h, Ly.attn_norm, a.act_dt, a.eps, xs, xres, red);
-        gemv_phase<MT, CPL_H, RB_H, 1, PE_QKV>(a, Ly.qkv, a.kc_h, a.ng_h, a.NQKV, pq, xs, xres, res, last);
+        load_scales(Ly.o.s, xr0, nxr, a.ng_q, lb + a.l_sb1);
+        wg_barrier();                                         // q|k|v rows are in LDS
         stamp(a, l, 1);
-        grid_sync(a, bar++);
-        stamp(a, l, 2);
-        // ---- attention over the cache
+        // ---- rotary embedding of q and k (rows 2d, 2d + 1 of a head are d, d + D/2), coherent stores
         {
-            const int units = n_items * a.Hkv * a.nsplit_max;
-            for (int u = blockIdx.x; u < units; u += gridDim.x) {
-                const int split = u % a.nsplit_max;
-                const int ig = u / a.nsplit_max;
-                attn_unit<D, RC>(a, l, ig / a.Hkv, ig % a.Hkv, split, a.nsplit_max, alds);
+            const int r0 = w * a.rpw_qkv;
+            const int n = max(0, min(a.NQKV, r0 + a.rpw_qkv) - r0);
+            for (int k = lane; k < n / 2; k += 64) {
+                const int pr = r0 + 2 * k;
+                const int hb = pr / D, d = (pr % D) / 2;
+                float lo = res[2 * k], hi = res[2 * k + 1];
+                if (hb < a.Hq + a.Hkv) {
+                    const float2 cs = rope[d];
+                    const float l2 = lo * cs.x - hi * cs.y;
+                    hi = hi * cs.x + lo * cs.y;
+                    lo = l2;
+                }
+                store_coherent(&a.qkv[hb * D + d], lo);
+                store_coherent(&a.qkv[hb * D + d + D / 2], hi);
             }
         }
-        WBuf<RB_Q * CPL_Q> po;                                   // o-projection weights stream during the barrier
-        load_batch<CPL_Q, RB_Q, 1>(po, Ly.o, a.kc_q, a.ng_q, a.gchunks, gw, nw, a.H, 0);
+        if (ok) ok = grid_sync(a, bar);
+        ++bar;
+        stamp(a, l, 2);
+        // ---- stage this split's query heads and, for the last split, this forward's cache row
+        if (has_att) {
+            const __amdgpu_buffer_rsrc_t r = make_rsrc(a.qkv, (size_t)a.NQKV * 4);
+            constexpr int NQ4 = GS * D / 4 / 64 > 0 ? GS * D / 4 / 64 : 1;
+            f32x4 qv[NQ4];
+#pragma unroll
+            for (int t = 0; t < NQ4; ++t) {
+                const int it = lane + 64 * t;
+                qv[t] = load4_coherent(r, it < GS * D / 4 ? (g * GS * D + 4 * it) * 4 : 0);
+            }
+            float kn[D / 64 > 0 ? D / 64 : 1], vn[D / 64 > 0 ? D / 64 : 1];
+            if (owns_new) {
+#pragma unroll
+                for (int e = 0; e < D / 64; ++e) {
+                    kn[e] = load_coherent(&a.qkv[a.QD + g * D + lane + 64 * e]);
+                    vn[e] = load_coherent(&a.qkv[a.QD + KVD + g * D + lane + 64 * e]);
+                }
+            }
+#pragma unroll
+            for (int t = 0; t < NQ4; ++t) {
+                const int it = lane + 64 * t;
+                if (it < GS * D / 4) *(f32x4*)(qs + 4 * it) = qv[t] * a.qscale;
+            }
+            if (owns_new) {
+                uint16_t* kl = rq.kc + (size_t)l * lstride + (((size_t)b * a.Hkv + g) * rq.cap + P) * D;
+                uint16_t* vl = rq.vc + (size_t)l * lstride + (((size_t)b * a.Hkv + g) * rq.cap + P) * D;
+#pragma unroll
+                for (int e = 0; e < D / 64; ++e) {
+                    const int d = lane + 64 * e;
+                    const uint16_t kb = to_half_bits(kn[e], a.kv_dt), vb = to_half_bits(vn[e], a.kv_dt);
+                    kl[d] = kb;
+                    vl[d] = vb;
+                    nkv[d] = half_bits_to_f32(kb, a.kv_dt);
+                    nkv[D + d] = half_bits_to_f32(vb, a.kv_dt);
+                }
+                if (l == 0 && g == 0 && lane == 0) rq.table[(size_t)b * rq.cap + P] = (int16_t)b;
+            }
+        }
+        load_scales(Ly.gu.s, w * a.rpw_gu, max(0, min(2 * a.F, (w + 1) * a.rpw_gu) - w * a.rpw_gu), a.ng_h, lb + a.l_sb0);
+        vm_wait_all();
+        wg_barrier();                                         // q and the new row are staged
+        wg_barrier();                                         // wave partials are in LDS
         stamp(a, l, 3);
-        grid_sync(a, bar++);
+        // ---- merge the waves (and the new row) into this split's partial; the last split merges the splits
+        if (has_att) {
+            float s_new = -INFINITY;
+            if (owns_new && mask[P] != 0) {
+                float sd = 0.f;
+#pragma unroll
+                for (int e = 0; e < OPL; ++e) sd += qs[hq * D + d0 + e] * nkv[d0 + e];
+                sd = (LPH == 16) ? group_sum<16>(sd) : (LPH == 8) ? group_sum<8>(sd) : sd;
+                if constexpr (LPH == 32) {
+                    sd = group_sum<16>(sd);
+                    sd += dpp_rows<0x142, 0xA>(sd);                       // row 1 += row 0, row 3 += row 2
+                    sd = __shfl(sd, (lane & 32) + 31);
+                }
+                s_new = sd;
+            }
+            float mx = s_new;
+#pragma unroll
+            for (int c = 0; c < SK_CW; ++c) mx = fmaxf(mx, part[(c * GS + hq) * (D + 4)]);
+            float L = 0.f, O[OPL];
+#pragma unroll
+            for (int e = 0; e < OPL; ++e) O[e] = 0.f;
+            if (s_new != -INFINITY) {
+                const float wn = exp2f(s_new - mx);
+                L = wn;
+#pragma unroll
+                for (int e = 0; e < OPL; ++e) O[e] = wn * nkv[D + d0 + e];
+            }
+#pragma unroll
+            for (int c = 0; c < SK_CW; ++c) {
+                const float* pc = part + (c * GS + hq) * (D + 4);
+                const float mc = pc[0];
+                const float wc = (mc == -INFINITY) ? 0.f : exp2f(mc - mx);
+                L += wc * pc[1];
+#pragma unroll
+                for (int e = 0; e < OPL; ++e) O[e] += wc * pc[4 + d0 + e];
+            }
+            float* pp = a.apart + (((size_t)g * a.nsplit + split) * GS + hq) * (D + 4);
+#pragma unroll
+            for (int e = 0; e < OPL; ++e) store_coherent(pp + 4 + d0 + e, O[e]);
+            if (d0 == 0) {
+                store_coherent(pp, mx);
+                store_coherent(pp + 1, L);
+            }
+            vm_wait_all();
+            unsigned prev = 0;
+            if (lane == 0) prev = atomicAdd(&a.acnt[g], 1u);
+            prev = __builtin_amdgcn_readfirstlane(prev);
+            if (((prev + 1u) & (unsigned)(a.nsplit - 1)) == 0u) {
+                // last arrival of this kv head: merge its nsplit partials
+                const __amdgpu_buffer_rsrc_t r =
+                    make_rsrc(a.apart, (size_t)a.Hkv * a.nsplit * GS * (D + 4) * 4);
+                float Mx = -INFINITY, Ls = 0.f, Os[OPL];
+#pragma unroll
+                for (int e = 0; e < OPL; ++e) Os[e] = 0.f;
+                constexpr int MB = 4;                            // splits per round
+                for (int s0 = 0; s0 < a.nsplit; s0 += MB) {
+                    f32x4 st4[MB], ov[MB][(OPL + 3) / 4];
+#pragma unroll
+                    for (int k = 0; k < MB; ++k) {
+                        const int s2 = min(s0 + k, a.nsplit - 1);
+                        const int base = (int)((((size_t)g * a.nsplit + s2) * GS + hq) * (D + 4)) * 4;
+                        st4[k] = load4_coherent(r, base);
+#pragma unroll
+                        for (int q4 = 0; q4 < (OPL + 3) / 4; ++q4) ov[k][q4] = load4_coherent(r, base + 16 + 4 * d0 + 16 * q4);
+                    }
+#pragma unroll
+                    for (int k = 0; k < MB; ++k) {
+                        if (s0 + k >= a.nsplit) break;
+                        const float ms = st4[k][0];
+                        if (ms == -INFINITY) continue;
+                        const float mn = fmaxf(Mx, ms);
+                        const float c1 = (Mx == -INFINITY) ? 0.f : exp2f(Mx - mn);
+                        const float c2 = exp2f(ms - mn);
+                        Ls = Ls * c1 + st4[k][1] * c2;
+#pragma unroll
+                        for (int e = 0; e < OPL; ++e) Os[e] = Os[e] * c1 + ov[k][e / 4][e % 4] * c2;
+                        Mx = mn;
+                    }
+                }
+                const float inv = 1.0f / Ls;
+                uint32_t* dst = (uint32_t*)(a.o + (size_t)(g * GS + hq) * D + d0);
+#pragma unroll
+                for (int e = 0; e < OPL; e += 2) store_coherent_u32(dst + e / 2, pack_f16x2(Os[e] * inv, Os[e + 1] * inv));
+            }
+        }
+        if (ok) ok = grid_sync(a, bar);
+        ++bar;
         stamp(a, l, 4);
-        // ---- x += o Wo^T
-        stage_input(a.o, 0, DT_F32, a.QD, a.M, a.QD, a.kc_q, nullptr, 0, 0.f, xs, nullptr, red);
-        gemv_phase<MT, CPL_Q, RB_Q, 1, PE_RESID>(a, Ly.o, a.kc_q, a.ng_q, a.H, po, xs, xres, res, false);
-        WBuf<RB_G * 2 * CPL_H> pg;
-        load_batch<CPL_H, RB_G, 2>(pg, Ly.gu, a.kc_h, a.ng_h, a.gchunks, gw, nw, a.F, 0);
+        stage_plain<NT_Q>(a.o, a.QD, a.kc_q * 32, xs);
+        vm_wait_all();
+        wg_barrier();                                         // attention output staged
+        wg_barrier();                                         // o rows are in LDS
         stamp(a, l, 5);
-        grid_sync(a, bar++);
+        // ---- x += o Wo^T (own rows)
+        if (lane < nxr) {
+            xrow += res[lane];
+            store_coherent(&a.x[xr0 + lane], xrow);
+        }
+        if (ok) ok = grid_sync(a, bar);
+        ++bar;
         stamp(a, l, 6);
-        // ---- act = silu(h2 Wg^T) * (h2 Wu^T), h2 = RMSNorm(x)
-        stage_input(a.x, 0, DT_F32, a.H, a.M, a.H, a.kc_h, Ly.ffn_norm, a.act_dt, a.eps, xs, xres, red);
-        gemv_phase<MT, CPL_H, RB_G, 2, PE_SWIGLU>(a, Ly.gu, a.kc_h, a.ng_h, a.F, pg, xs, xres, res, false);
-        WBuf<RB_F * CPL_F> pd;
-        load_batch<CPL_F, RB_F, 1>(pd, Ly.d, a.kc_f, a.ng_f, a.gchunks, gw, nw, a.H, 0);
+        stage_norm<NT_H>(a.x, DT_F32, a.H, a.kc_h * 32, Ly.ffn_norm, a.act_dt, a.eps, xs);
+        load_scales(Ly.d.s, xr0, nxr, a.ng_f, lb + a.l_sb1);
+        vm_wait_all();
+        wg_barrier();                                         // RMSNorm(x) staged
+        wg_barrier();                                         // gate|up rows are in LDS
         stamp(a, l, 7);
-        grid_sync(a, bar++);
+        // ---- act = silu(gate) * up, two values per lane as one coherent dword
+        {
+            const int r0 = w * a.rpw_gu;
+            const int n = max(0, min(2 * a.F, r0 + a.rpw_gu) - r0);
+            for (int k = lane; k < n / 4; k += 64) {
+                float y[2];
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    const float gt = res[4 * k + 2 * e], up = res[4 * k + 2 * e + 1];
+                    y[e] = (gt / (1.0f + expf(-gt))) * up;
+                }
+                store_coherent_u32((uint32_t*)(a.act + r0 / 2 + 2 * k), pack_f16x2(y[0], y[1]));
+            }
+        }
+        if (ok) ok = grid_sync(a, bar);
+        ++bar;
         stamp(a, l, 8);
-        // ---- x += act Wd^T (the last layer also writes hidden_out)
-        stage_input(a.act, 0, DT_F32, a.F, a.M, a.F, a.kc_f, nullptr, 0, 0.f, xs, nullptr, red);
-        gemv_phase<MT, CPL_F, RB_F, 1, PE_RESID>(a, Ly.d, a.kc_f, a.ng_f, a.H, pd, xs, xres, res, last);
-        stamp(a, l, 9);
+        stage_plain<NT_F>(a.act, a.F, a.kc_f * 32, xs);
+        vm_wait_all();
+        wg_barrier();                                         // SwiGLU output staged
         if (!last) {
-            load_batch<CPL_H, RB_H, 1>(pq, a.layers[l + 1].qkv, a.kc_h, a.ng_h, a.gchunks, gw, nw, a.NQKV, 0);
-            grid_sync(a, bar++);
+            const PsLayer& Ln = a.layers[l + 1];
+            load_scales(Ln.qkv.s, w * a.rpw_qkv, max(0, min(a.NQKV, (w + 1) * a.rpw_qkv) - w * a.rpw_qkv), a.ng_h,
+                        lb + a.l_sb0);
+        }
+        wg_barrier();                                         // down rows are in LDS
+        stamp(a, l, 9);
+        // ---- x += act Wd^T (own rows); the last layer writes hidden_out
+        if (lane < nxr) {
+            xrow += res[lane];
+            if (last)
+                ((uint16_t*)a.hidden_out)[xr0 + lane] = to_half_bits(xrow, a.act_dt);
+            else
+                store_coherent(&a.x[xr0 + lane], xrow);
+        }
+        if (!last) {
+            if (ok) ok = grid_sync(a, bar);
+            ++bar;
+            stage_norm<NT_H>(a.x, DT_F32, a.H, a.kc_h * 32, a.layers[l + 1].attn_norm, a.act_dt, a.eps, xs);
+            vm_wait_all();
+            wg_barrier();                                     // next layer's q|k|v input staged
         }
     }
 }
 
-template <int MT, int CPL_H, int CPL_Q, int CPL_F, int D, int RC>
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
+__global__ __launch_bounds__(SK_THREADS) void stage_stream_kernel(PsArgs a) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    if ((threadIdx.x >> 6) < SK_CW)
+        compute_main<CPL_H, CPL_Q, CPL_F, D, GS, S>(a, lds_addr(smem));
+    else
+        control_main<CPL_H, CPL_Q, CPL_F, D, GS, S>(a, smem);
+}
+
+// ------------------------------------------------------------------ host side
+
+// Instantiations: (K / 2048 for K = H, Hq*D, F), head_dim, query heads per kv head, ring slots.
+#define PS_SHAPES(X)                 \
+    X(2, 2, 7, 128, 4, 24)   /* Llama-3.1-8B layers */ \
+    X(1, 1, 1, 64, 2, 24)    /* small test stages */
+
+bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int gs) {
+#define PS_MATCH(H_, Q_, F_, D_, G_, S_) \
+    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return true;
+    PS_SHAPES(PS_MATCH)
+#undef PS_MATCH
+    return false;
+}
+
+int ps_slots(int cpl_h, int cpl_q, int cpl_f, int D, int gs) {
+#define PS_MATCH(H_, Q_, F_, D_, G_, S_) \
+    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return S_;
+    PS_SHAPES(PS_MATCH)
+#undef PS_MATCH
+    return 0;
+}
+
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
+size_t ps_private_of() {
+    hipFuncAttributes at{};
+    if (hipFuncGetAttributes(&at, (const void*)stage_stream_kernel<CPL_H, CPL_Q, CPL_F, D, GS, S>) != hipSuccess) {
+        (void)hipGetLastError();
+        return (size_t)-1;
+    }
+    return at.localSizeBytes;
+}
+
+size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int gs) {
+#define PS_MATCH(H_, Q_, F_, D_, G_, S_) \
+    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return ps_private_of<H_, Q_, F_, D_, G_, S_>();
+    PS_SHAPES(PS_MATCH)
+#undef PS_MATCH
+    return (size_t)-1;
+}
+
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
 hipError_t launch_ps(const PsArgs& a, int nwg, size_t lds, hipStream_t st) {
-    const void* fn = (const void*)stage_persistent_kernel<MT, CPL_H, CPL_Q, CPL_F, D, RC>;
+    const void* fn = (const void*)stage_stream_kernel<CPL_H, CPL_Q, CPL_F, D, GS, S>;
     static bool configured = false;
     if (!configured) {
         hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
@@ -750,66 +952,39 @@ hipError_t launch_ps(const PsArgs& a, int nwg, size_t lds, hipStream_t st) {
     }
     PsArgs copy = a;
     void* args[] = {&copy};
-    return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(PS_THREADS), args, (unsigned)lds, st);
+    return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(SK_THREADS), args, (unsigned)lds, st);
 }
 
-// Shapes with a persistent instantiation: (K/2048 for K = H, Hq*D, F), head_dim,
-// query rows per (slot, kv head).
-bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int M, int rows_per_item) {
-    if (M < 1 || M > PS_MAX_M) return false;
-    if (cpl_h == 2 && cpl_q == 2 && cpl_f == 7 && D == 128) return rows_per_item <= 4;     // Llama-3.1-8B layers
-    if (cpl_h == 4 && cpl_q == 4 && cpl_f == 14 && D == 128) return rows_per_item <= 8;    // Llama-3-70B layers
-    if (cpl_h == 1 && cpl_q == 1 && cpl_f == 1 && D == 64) return rows_per_item <= 8;      // small test stages
-    return false;
-}
-
-template <int MT, int CPL_H, int CPL_Q, int CPL_F, int D, int RC>
-size_t ps_private_of() {
-    hipFuncAttributes at{};
-    if (hipFuncGetAttributes(&at, (const void*)stage_persistent_kernel<MT, CPL_H, CPL_Q, CPL_F, D, RC>) != hipSuccess) {
-        (void)hipGetLastError();
-        return (size_t)-1;
-    }
-    return at.localSizeBytes;
-}
-
-size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int rows_per_item) {
-    if (cpl_h == 2 && cpl_q == 2 && cpl_f == 7 && D == 128) return ps_private_of<1, 2, 2, 7, 128, 4>();
-    if (cpl_h == 4 && cpl_q == 4 && cpl_f == 14 && D == 128) return ps_private_of<1, 4, 4, 14, 128, 8>();
-    if (cpl_h == 1 && cpl_q == 1 && cpl_f == 1 && D == 64)
-        return rows_per_item <= 4 ? ps_private_of<1, 1, 1, 1, 64, 4>() : ps_private_of<1, 1, 1, 1, 64, 8>();
-    return (size_t)-1;
-}
-
-hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int rows_per_item, int nwg,
-                             size_t lds, hipStream_t st) {
-    if (!ps_supported(cpl_h, cpl_q, cpl_f, D, a.M, rows_per_item)) return hipErrorInvalidValue;
-    if (cpl_h == 2 && cpl_q == 2 && cpl_f == 7 && D == 128) return launch_ps<1, 2, 2, 7, 128, 4>(a, nwg, lds, st);
-    if (cpl_h == 4 && cpl_q == 4 && cpl_f == 14 && D == 128) return launch_ps<1, 4, 4, 14, 128, 8>(a, nwg, lds, st);
-    if (cpl_h == 1 && cpl_q == 1 && cpl_f == 1 && D == 64)
-        return rows_per_item <= 4 ? launch_ps<1, 1, 1, 1, 64, 4>(a, nwg, lds, st) : launch_ps<1, 1, 1, 1, 64, 8>(a, nwg, lds, st);
+hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int gs, int nwg, size_t lds,
+                             hipStream_t st) {
+#define PS_MATCH(H_, Q_, F_, D_, G_, S_) \
+    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return launch_ps<H_, Q_, F_, D_, G_, S_>(a, nwg, lds, st);
+    PS_SHAPES(PS_MATCH)
+#undef PS_MATCH
     return hipErrorInvalidValue;
 }
 
-// Largest dynamic LDS any instantiation asks for at this shape and row count.
-size_t ps_lds_bytes(int H, int QD, int F, int kc_h, int kc_q, int kc_f, int D, int M) {
-    (void)QD; (void)F;
-    const int kcmax = kc_h > kc_q ? (kc_h > kc_f ? kc_h : kc_f) : (kc_q > kc_f ? kc_q : kc_f);
-    const size_t xs = (size_t)M * kcmax * 64;                                // fp16 pairs
-    const size_t att = (size_t)PS_WAVES * 8 * D * 4 + 2 * PS_WAVES * 8 * 4 + (8 + 2 * M) * D * 4 + 768 + 16;
-    const size_t head = (size_t)M * H * 4 + (PS_THREADS + 16) * 4 + (size_t)PS_WAVES * PS_MAXU * 2 * M * 4;
-    return head + (xs > att ? xs : att);
+// Destination row of source row r: row_off + r (map 0), 2r (map 1, gate),
+// 2r + 1 (map 2, up), or row_off + the rotary-pair order inside each head of
+// head_dim rows (map 3: d -> 2d for d < D/2, d -> 2(d - D/2) + 1 otherwise).
+__host__ __device__ __forceinline__ int row_dest(int r, int row_off, int row_map, int head_dim) {
+    if (row_map == 1) return 2 * r;
+    if (row_map == 2) return 2 * r + 1;
+    if (row_map == 3) {
+        const int h = r / head_dim, d = r % head_dim, half = head_dim / 2;
+        return row_off + h * head_dim + (d < half ? 2 * d : 2 * (d - half) + 1);
+    }
+    return row_off + r;
 }
 
-// Row-layout repack: dest row = row_off + r (map 0), 2r (map 1, gate), 2r + 1 (map 2, up).
 __global__ void repack_rows_kernel(const uint8_t* __restrict__ q, const uint16_t* __restrict__ s, int n, int k, int g,
                                    uint8_t* __restrict__ w_out, uint16_t* __restrict__ s_out, int kc, int ng,
-                                   int row_off, int row_map) {
+                                   int row_off, int row_map, int head_dim) {
     const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
     if (idx >= (size_t)n * kc) return;
     const int r = (int)(idx / kc), c = (int)(idx % kc);
     const int kb = (k + 1) / 2;
-    const int dr = row_map == 0 ? row_off + r : 2 * r + (row_map == 2 ? 1 : 0);
+    const int dr = row_dest(r, row_off, row_map, head_dim);
     u32x4 o;
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
@@ -833,19 +1008,19 @@ __global__ void repack_rows_kernel(const uint8_t* __restrict__ q, const uint16_t
 }
 
 hipError_t launch_repack_rows(const uint8_t* q, const uint16_t* s, int n, int k, int g, uint8_t* w_out, uint16_t* s_out,
-                              int kc, int ng, int row_off, int row_map, hipStream_t st) {
+                              int kc, int ng, int row_off, int row_map, int head_dim, hipStream_t st) {
     const size_t nc = (size_t)n * kc;
     repack_rows_kernel<<<dim3((unsigned)((nc + 255) / 256)), dim3(256), 0, st>>>(q, s, n, k, g, w_out, s_out, kc, ng,
-                                                                                row_off, row_map);
+                                                                                row_off, row_map, head_dim);
     return hipGetLastError();
 }
 
 __global__ void dequant_rows_kernel(PsMat m, int kc, int ng, int gchunks, int k, int row_off, int row_map, int n_rows,
-                                    float* __restrict__ out) {
+                                    int head_dim, float* __restrict__ out) {
     const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
     if (idx >= (size_t)n_rows * kc) return;
     const int r = (int)(idx / kc), c = (int)(idx % kc);
-    const int dr = row_map == 0 ? row_off + r : 2 * r + (row_map == 2 ? 1 : 0);
+    const int dr = row_dest(r, row_off, row_map, head_dim);
     const u32x4 w = *(const u32x4*)(m.w + ((size_t)dr * kc + c) * 16);
     half2_t h[16];
     unpack_chunk(w, h);
@@ -860,10 +1035,10 @@ __global__ void dequant_rows_kernel(PsMat m, int kc, int ng, int gchunks, int k,
 }
 
 hipError_t launch_dequant_rows(const PsMat& m, int kc, int ng, int gchunks, int k, int row_off, int row_map, int n_rows,
-                               float* out, hipStream_t st) {
+                               int head_dim, float* out, hipStream_t st) {
     const size_t nc = (size_t)n_rows * kc;
     dequant_rows_kernel<<<dim3((unsigned)((nc + 255) / 256)), dim3(256), 0, st>>>(m, kc, ng, gchunks, k, row_off, row_map,
-                                                                                  n_rows, out);
+                                                                                  n_rows, head_dim, out);
     return hipGetLastError();
 }
 

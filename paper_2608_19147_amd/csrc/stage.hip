@@ -69,9 +69,10 @@ struct Stage {
     PsLayer* ps_layers = nullptr;
     unsigned long long* bar = nullptr;
     unsigned* err = nullptr;
-    float* junk = nullptr;
     unsigned long long bar_epoch = 0;
     int ps_nwg = 0;
+    int ps_rpw_qkv = 0, ps_rpw_h = 0, ps_rpw_gu = 0;    // rows per workgroup of the single-launch forward
+    unsigned* acnt_ps = nullptr;                        // its split arrival counters (only ever incremented)
     unsigned long long* trace = nullptr;   // phase stamps of the last persistent forward (STAGE_PS_TRACE=1)
     int prof_class = -1;
     std::vector<hipEvent_t> prof_ev;   // start/stop pairs
@@ -158,7 +159,8 @@ int make_mat(Stage* st, DevMat& m, int n_rows_padded_tiles, int k, int g) {
 // Copy one canonical matrix into the tiled layout of `m` (rows placed per
 // row_off / row_map) and, when `pm` is given, into the row layout as well.
 int upload_mat(Stage* st, DevMat& m, const QuantMatrix& q, int on_device, int row_off, int row_map,
-               uint8_t* tmp_q, uint16_t* tmp_s, hipStream_t stream, const PsMat* pm = nullptr, int kc = 0, int ng = 0) {
+               uint8_t* tmp_q, uint16_t* tmp_s, hipStream_t stream, const PsMat* pm = nullptr, int kc = 0, int ng = 0,
+               int pm_map = -1) {
     const int g = st->cfg.group_size;
     const size_t qbytes = (size_t)q.n * ((q.k + 1) / 2);
     const size_t sbytes = (size_t)q.n * ((q.k + g - 1) / g) * 2;
@@ -173,8 +175,8 @@ int upload_mat(Stage* st, DevMat& m, const QuantMatrix& q, int on_device, int ro
     HIP_TRY(launch_repack(qsrc, ssrc, q.n, q.k, g, (uint8_t*)m.pm.w, (uint16_t*)m.pm.s, m.pm.ntiles, m.pm.nchunk,
                           m.pm.ngroups, row_off, row_map, stream));
     if (pm)
-        HIP_TRY(launch_repack_rows(qsrc, ssrc, q.n, q.k, g, (uint8_t*)pm->w, (uint16_t*)pm->s, kc, ng, row_off, row_map,
-                                   stream));
+        HIP_TRY(launch_repack_rows(qsrc, ssrc, q.n, q.k, g, (uint8_t*)pm->w, (uint16_t*)pm->s, kc, ng, row_off,
+                                   pm_map < 0 ? row_map : pm_map, st->cfg.head_dim, stream));
     if (!on_device) HIP_TRY(hipStreamSynchronize(stream));   // tmp buffers are reused by the next matrix
     return STAGE_OK;
 }
@@ -184,10 +186,10 @@ int make_rows(Stage* st, PsMat& pm, int n, int kc, int ng) {
     uint16_t* s;
     int rc = st->alloc(&w, (size_t)n * kc * 16);
     if (rc) return rc;
-    rc = st->alloc(&s, (size_t)n * ng);
+    rc = st->alloc(&s, (size_t)n * ng + SK_SLOT / 2);   // scale rows are read in whole 1 KB blocks
     if (rc) return rc;
     HIP_TRY(hipMemset(w, 0x88, (size_t)n * kc * 16));
-    HIP_TRY(hipMemset(s, 0, (size_t)n * ng * 2));
+    HIP_TRY(hipMemset(s, 0, ((size_t)n * ng + SK_SLOT / 2) * 2));
     pm.w = w;
     pm.s = s;
     return STAGE_OK;
@@ -338,7 +340,7 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         st->ng_q = (st->kc_q + gch - 1) / gch;
         st->ng_f = (st->kc_f + gch - 1) / gch;
         const char* e = std::getenv("STAGE_PERSISTENT");
-        st->ps_ok = ps_supported(st->cpl_h, st->cpl_q, st->cpl_f, D, 1, 1) && !(e && atoi(e) == 0);
+        st->ps_ok = ps_supported(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv) && !(e && atoi(e) == 0);
         if (st->ps_ok) st->ps_host.resize(c.n_layers);
     }
     for (int l = 0; l < c.n_layers; ++l) {
@@ -360,9 +362,10 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         L.gu.pm.n = 2 * F;
         L.d.pm.n = H;
         const int kh = st->kc_h, kq = st->kc_q, kf = st->kc_f, gh = st->ng_h, gq = st->ng_q, gf = st->ng_f;
-        if ((rc = upload_mat(st, L.qkv, w.wq, weights_on_device, 0, 0, tmp_q, tmp_s, s, P ? &P->qkv : nullptr, kh, gh)) ||
-            (rc = upload_mat(st, L.qkv, w.wk, weights_on_device, QD, 0, tmp_q, tmp_s, s, P ? &P->qkv : nullptr, kh, gh)) ||
-            (rc = upload_mat(st, L.qkv, w.wv, weights_on_device, QD + KVD, 0, tmp_q, tmp_s, s, P ? &P->qkv : nullptr, kh, gh)) ||
+        if ((rc = upload_mat(st, L.qkv, w.wq, weights_on_device, 0, 0, tmp_q, tmp_s, s, P ? &P->qkv : nullptr, kh, gh, 3)) ||
+            (rc = upload_mat(st, L.qkv, w.wk, weights_on_device, QD, 0, tmp_q, tmp_s, s, P ? &P->qkv : nullptr, kh, gh, 3)) ||
+            (rc = upload_mat(st, L.qkv, w.wv, weights_on_device, QD + KVD, 0, tmp_q, tmp_s, s, P ? &P->qkv : nullptr, kh, gh,
+                             3)) ||
             (rc = upload_mat(st, L.o, w.wo, weights_on_device, 0, 0, tmp_q, tmp_s, s, P ? &P->o : nullptr, kq, gq)) ||
             (rc = upload_mat(st, L.gu, w.wg, weights_on_device, 0, 1, tmp_q, tmp_s, s, P ? &P->gu : nullptr, kh, gh)) ||
             (rc = upload_mat(st, L.gu, w.wu, weights_on_device, 0, 2, tmp_q, tmp_s, s, P ? &P->gu : nullptr, kh, gh)) ||
@@ -432,8 +435,7 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
             return cleanup(fail(STAGE_E_HIP, "event creation failed"));
     if ((rc = ensure_meta(st, 1 << 16))) return cleanup(rc);
     if (st->ps_ok) {
-        if ((rc = st->alloc(&st->ps_layers, c.n_layers)) || (rc = st->alloc(&st->bar, 16 * 64)) || (rc = st->alloc(&st->err, 4)) ||
-            (rc = st->alloc(&st->junk, 256)))
+        if ((rc = st->alloc(&st->ps_layers, c.n_layers)) || (rc = st->alloc(&st->bar, 16 * 64)) || (rc = st->alloc(&st->err, 4)))
             return cleanup(rc);
         if (hipMemcpy(st->ps_layers, st->ps_host.data(), sizeof(PsLayer) * c.n_layers, hipMemcpyHostToDevice) != hipSuccess ||
             hipMemset(st->bar, 0, 16 * 64 * 8) != hipSuccess || hipMemset(st->err, 0, 4) != hipSuccess)
@@ -442,20 +444,31 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
             return cleanup(fail(STAGE_E_HIP, "CU count query failed"));
         st->ps_nwg = cus;
-        {   // every wave must own at most PS_MAXU units in each GEMV phase
-            const int nw = cus * PS_WAVES_PER_WG;
-            for (int nu : {nqkv, H, F})
-                if ((nu + nw - 1) / nw > PS_MAXU) st->ps_ok = false;
-        }
+        // rows per workgroup: rotary pairs stay in one workgroup (even), gate|up
+        // pairs are stored two per dword (multiple of 4)
+        auto cdiv = [](int a_, int b_) { return (a_ + b_ - 1) / b_; };
+        st->ps_rpw_qkv = (cdiv(nqkv, cus) + 1) / 2 * 2;
+        st->ps_rpw_h = cdiv(H, cus);
+        st->ps_rpw_gu = (cdiv(2 * F, cus) + 3) / 4 * 4;
+        if (st->ps_rpw_h > 64) st->ps_ok = false;              // one residual row per control lane
+        for (long bytes : {(long)st->ps_rpw_qkv * st->ng_h, (long)st->ps_rpw_h * st->ng_q, (long)st->ps_rpw_gu * st->ng_h,
+                           (long)st->ps_rpw_h * st->ng_f})
+            if ((bytes * 2) % 16 != 0) st->ps_ok = false;      // scale rows are loaded in 16-byte pieces
+        PsArgs probe{};
+        probe.kc_h = st->kc_h; probe.kc_q = st->kc_q; probe.kc_f = st->kc_f;
+        probe.ng_h = st->ng_h; probe.ng_q = st->ng_q; probe.ng_f = st->ng_f;
+        probe.rpw_qkv = st->ps_rpw_qkv; probe.rpw_h = st->ps_rpw_h; probe.rpw_gu = st->ps_rpw_gu;
+        const int slots = ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv);
+        if (slots <= 0 || ps_layout(probe, slots, D, Hq / Hkv) > 160 * 1024) st->ps_ok = false;
+        if ((rc = st->alloc(&st->acnt_ps, Hkv))) return cleanup(rc);
+        if (hipMemset(st->acnt_ps, 0, Hkv * sizeof(unsigned)) != hipSuccess)
+            return cleanup(fail(STAGE_E_HIP, "counter init failed"));
         if (const char* e = std::getenv("STAGE_PS_TRACE"))
             if (atoi(e) && (rc = st->alloc(&st->trace, (size_t)cus * c.n_layers * PS_TRACE_PER_LAYER)))
                 return cleanup(rc);
-        // the single-launch forward is only used when its kernels need no private
+        // the single-launch forward is only used when its kernel needs no private
         // segment (no stack, no scratch spills) for this shape
-        const int gs = Hq / Hkv;
-        for (int rows : {gs}) {
-            if (ps_private_bytes(st->cpl_h, st->cpl_q, st->cpl_f, D, rows) != 0) st->ps_ok = false;
-        }
+        if (st->ps_ok && ps_private_bytes(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv) != 0) st->ps_ok = false;
     }
     if (hipDeviceSynchronize() != hipSuccess) return cleanup(fail(STAGE_E_HIP, "stage_create synchronize failed"));
     *out = st;
@@ -653,9 +666,9 @@ int stage_debug_dequant(Stage* stage, int layer, int which, float* out_host) {
         const PsMat* pm = nullptr;
         int off = 0, map = 0, nr = 0, kc = stage->kc_h, ng = stage->ng_h, k = c.hidden;
         switch (which) {
-            case 0: pm = &P.qkv; nr = QD; break;
-            case 1: pm = &P.qkv; off = QD; nr = KVD; break;
-            case 2: pm = &P.qkv; off = QD + KVD; nr = KVD; break;
+            case 0: pm = &P.qkv; map = 3; nr = QD; break;
+            case 1: pm = &P.qkv; map = 3; off = QD; nr = KVD; break;
+            case 2: pm = &P.qkv; map = 3; off = QD + KVD; nr = KVD; break;
             case 3: pm = &P.o; nr = c.hidden; kc = stage->kc_q; ng = stage->ng_q; k = QD; break;
             case 4: pm = &P.gu; map = 1; nr = c.ffn; break;
             case 5: pm = &P.gu; map = 2; nr = c.ffn; break;
@@ -667,7 +680,7 @@ int stage_debug_dequant(Stage* stage, int layer, int which, float* out_host) {
             (void)hipGetLastError();
             return fail(STAGE_E_OOM, "staging allocation failed");
         }
-        hipError_t e = launch_dequant_rows(*pm, kc, ng, c.group_size / CHUNK_K, k, off, map, nr, tmp, nullptr);
+        hipError_t e = launch_dequant_rows(*pm, kc, ng, c.group_size / CHUNK_K, k, off, map, nr, c.head_dim, tmp, nullptr);
         if (e == hipSuccess) e = hipMemcpy(out_host, tmp, bytes, hipMemcpyDeviceToHost);
         (void)hipFree(tmp);
         if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("debug dequant: ") + hipGetErrorString(e));
@@ -828,9 +841,25 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     const int act_dt = dt_code(c.act_dtype);
     const int nqkv = Hq * D + 2 * Hkv * D;
 
-    // ---------------- one persistent launch when the shape and row count allow it
-    if (st->ps_ok && ps_supported(st->cpl_h, st->cpl_q, st->cpl_f, D, M, max_rows_item) &&
-        (st->prof_class < 0 || st->prof_class == STAGE_KERNEL_PERSISTENT)) {
+    // ---------------- one launch for the whole stage: a single decode row
+    const int RPS = 512 / D;                               // cache rows per 1 KB slot
+    int nsplit = 0, split_len = 0, att_T = 0;
+    bool single = st->ps_ok && M == 1 && (st->prof_class < 0 || st->prof_class == STAGE_KERNEL_PERSISTENT);
+    if (single) {
+        const int P = reqs[0].state->P;
+        int cap_split = 16;
+        if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) cap_split = std::max(1, atoi(e));
+        nsplit = 1;
+        while (nsplit * 2 <= cap_split && nsplit * 2 * Hkv <= st->ps_nwg) nsplit *= 2;
+        for (;;) {
+            split_len = (P + nsplit - 1) / nsplit;
+            att_T = ((split_len + SK_CW - 1) / SK_CW + RPS - 1) / RPS;
+            if (att_T <= SK_TMAX || nsplit * 2 * Hkv > st->ps_nwg) break;
+            nsplit *= 2;
+        }
+        if (att_T > SK_TMAX) single = false;               // cache too long for one pass: per-layer kernels
+    }
+    if (single) {
         PsArgs a{};
         a.layers = st->ps_layers;
         a.n_layers = c.n_layers;
@@ -843,34 +872,30 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         a.kv_dt = dt_code(c.kv_dtype);
         a.hidden_in = hidden_in;
         a.hidden_out = hidden_out;
-        a.M = M;
-        a.x = st->x; a.qkv = st->qkv; a.o = st->attn; a.act = st->act;
+        a.rpw_qkv = st->ps_rpw_qkv; a.rpw_h = st->ps_rpw_h; a.rpw_gu = st->ps_rpw_gu;
+        a.x = st->x; a.qkv = st->qkv; a.o = (uint16_t*)st->attn; a.act = (uint16_t*)st->act;
         a.meta = meta;
         a.rope = st->rope;
         a.qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
+        a.nsplit = nsplit; a.split_len = split_len; a.att_T = att_T;
         a.apart = st->apart;
-        a.acnt = st->acnt;
-        a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, st->ps_nwg / std::max(1, n_items * Hkv)));
-        if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, atoi(e)));
+        a.acnt = st->acnt_ps;
         a.bar = st->bar;
         a.bar_epoch = st->bar_epoch;
         a.err = st->err;
         a.trace = st->trace;
-        a.junk = st->junk;
-        const size_t lds = ps_lds_bytes(H, Hq * D, F, st->kc_h, st->kc_q, st->kc_f, D, M);
-        if (lds <= 160 * 1024) {
-            HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, true, s));
-            hipError_t e = launch_persistent(a, st->cpl_h, st->cpl_q, st->cpl_f, D, max_rows_item, st->ps_nwg, lds, s);
-            if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("persistent launch: ") + hipGetErrorString(e));
-            HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, false, s));
-            st->bar_epoch += (unsigned long long)(5 * c.n_layers - 1);
-            for (int r = 0; r < n_req; ++r) {
-                KVState* kv = reqs[r].state;
-                if (do_gather[r]) kv->cur = 1 - kv->cur;
-                kv->P += reqs[r].n_tokens;
-            }
-            return STAGE_OK;
+        const int lds = ps_layout(a, ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, gs), D, gs);
+        HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, true, s));
+        hipError_t e = launch_persistent(a, st->cpl_h, st->cpl_q, st->cpl_f, D, gs, st->ps_nwg, (size_t)lds, s);
+        if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("single-launch forward: ") + hipGetErrorString(e));
+        HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, false, s));
+        st->bar_epoch += (unsigned long long)(5 * c.n_layers - 1);
+        for (int r = 0; r < n_req; ++r) {
+            KVState* kv = reqs[r].state;
+            if (do_gather[r]) kv->cur = 1 - kv->cur;
+            kv->P += reqs[r].n_tokens;
         }
+        return STAGE_OK;
     }
     auto run_gemv = [&](const DevMat& m, GemvArgs a, size_t in_row_elems, size_t out_row_elems, size_t resid_row_elems,
                         int in_elem_bytes, int resid_elem_bytes) -> hipError_t {
