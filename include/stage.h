@@ -207,11 +207,15 @@ int stage_profile_read(Stage* stage, int* launches, double* total_ms);
 
 /* Test and measurement support: phase-boundary timestamps of the last
  * single-launch forward, recorded only when STAGE_PS_TRACE=1 was set in the
- * environment at stage_create.  out_host receives [workgroups][n_layers][10]
- * readings of the 100 MHz device real-time counter taken by each workgroup at:
- * layer start, q|k|v end, attention start, attention end, o start, o end,
- * gate|up start, gate|up end, down start, down end.  n = capacity of out_host
- * in entries.  Synchronizes the device. */
+ * environment at stage_create.  out_host receives [workgroups][n_layers][16]
+ * readings of the 100 MHz device real-time counter.  Entries 0-9 are taken by
+ * each workgroup's control wave at: layer start (q|k|v input staged), q|k|v
+ * rows done, after the q|k|v -> attention grid barrier, attention partials
+ * done, after the attention -> o barrier, o rows done, after the o -> gate|up
+ * barrier, gate|up rows done, after the gate|up -> down barrier, down rows
+ * done.  Entries 10-15 are taken by its first compute wave at the start and
+ * end of its attention, gate|up and down work.  n = capacity of out_host in
+ * entries.  Synchronizes the device. */
 int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n);
 
 /* Bytes of device memory the stage holds for weights (packed codes + scales +

@@ -86,7 +86,7 @@ struct AttnArgs {
 // ---- single-launch stage forward (persistent.hip)
 constexpr int PS_MAX_M = 1;          // rows of one single-launch forward (decode of one slot)
 constexpr int PS_KCHUNK = 2048;      // row-layout K is padded to a multiple of this
-constexpr int SK_CW = 4;             // compute waves per workgroup (plus one control wave)
+constexpr int SK_CW = 7;             // compute waves per workgroup; with the control wave, two waves per SIMD
 constexpr int SK_SLOT = 1024;        // bytes per ring slot: one 16-byte load per lane
 constexpr int SK_TMAX = 16;          // cache-row slot pairs (K, V) per compute wave per layer
 
@@ -130,11 +130,11 @@ struct PsArgs {
     unsigned long long* bar;             // 16 barrier counters, 64 words apart
     unsigned long long bar_epoch;        // barriers completed by earlier launches
     unsigned* err;                       // set when a barrier wait gives up
-    unsigned long long* trace;           // optional [nwg][10 * n_layers] real-time stamps
+    unsigned long long* trace;           // optional [nwg][n_layers][PS_TRACE_PER_LAYER] real-time stamps
     // LDS byte offsets
-    int l_xs, l_sb0, l_sb1, l_res, l_q, l_nkv, l_part, l_rope, l_end;
+    int l_xs, l_gff, l_sb0, l_sb1, l_res, l_q, l_nkv, l_part, l_rope, l_dbg, l_end;
 };
-constexpr int PS_TRACE_PER_LAYER = 10;
+constexpr int PS_TRACE_PER_LAYER = 16;   // 10 control-wave boundaries + 6 from compute wave 0
 
 // LDS layout of the stream kernel with `slots` ring slots per compute wave;
 // returns the total bytes.
@@ -146,17 +146,24 @@ inline int ps_layout(PsArgs& a, int slots, int D, int gs) {
     sb = sb > a.rpw_gu * a.ng_h ? sb : a.rpw_gu * a.ng_h;
     sb = sb > a.rpw_h * a.ng_f ? sb : a.rpw_h * a.ng_f;
     sb = up(sb * 2, SK_SLOT);
-    int rows = a.rpw_qkv > a.rpw_h ? a.rpw_qkv : a.rpw_h;
+    int rows = a.rpw_qkv > 2 * a.rpw_h ? a.rpw_qkv : 2 * a.rpw_h;   // down rows may carry two partials
     rows = rows > a.rpw_gu ? rows : a.rpw_gu;
     int off = SK_CW * slots * SK_SLOT;
-    a.l_xs = off;   off += kcmax * 64;
+    // staged input; past the K = H / Hq*D part it also holds the ffn RMSNorm weights
+    // from the end of one down phase until the next down input is staged
+    const int kch = a.kc_h > a.kc_q ? a.kc_h : a.kc_q;
+    const int xsz = kch * 64 + up(a.H * 2, SK_SLOT);
+    a.l_xs = off;
+    a.l_gff = off + kch * 64;
+    off += kcmax * 64 > xsz ? kcmax * 64 : xsz;
     a.l_sb0 = off;  off += sb;
     a.l_sb1 = off;  off += sb;
     a.l_res = off;  off += up(rows * 4, 16);
     a.l_q = off;    off += gs * D * 4;
     a.l_nkv = off;  off += 2 * D * 4;
-    a.l_part = off; off += SK_CW * gs * (D + 4) * 4;
+    a.l_part = off; off += up(SK_CW * gs * (D + 4) * 4 > a.H * 2 ? SK_CW * gs * (D + 4) * 4 : a.H * 2, SK_SLOT);   // also RMSNorm weights
     a.l_rope = off; off += (D / 2) * 8;
+    a.l_dbg = off;  off += 64;                                        // compute-wave trace stamps
     a.l_end = off;
     return off;
 }

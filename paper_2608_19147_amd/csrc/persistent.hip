@@ -82,6 +82,12 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
     __builtin_amdgcn_global_load_lds(g, (lds_ptr_t)(uintptr_t)lds, 16, 0, 2 /* nt: streamed once */);
 }
 
+// The same with device-coherent reads ("sc1"), for data written by other
+// workgroups of this launch.
+__device__ __forceinline__ void dma16_coherent(const void* g, uint32_t lds) {
+    __builtin_amdgcn_global_load_lds(g, (lds_ptr_t)(uintptr_t)lds, 16, 0, 16 /* sc1 */);
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
 
 // ------------------------------------------------------------------ device-coherent exchange
@@ -146,6 +152,14 @@ __device__ __forceinline__ bool grid_sync(const PsArgs& a, int idx) {
     }
 }
 
+// Compute wave 0 keeps its stamps in LDS (a global store would join its load count).
+__device__ __forceinline__ void cstamp(const PsArgs& a, uint32_t dbg, int k) {
+    if (a.trace && threadIdx.x == 0) {
+        const u64 t = wall_clock64();
+        asm volatile("ds_write_b64 %0, %1" ::"v"(dbg + 8 * k), "v"(t) : "memory");
+    }
+}
+
 __device__ __forceinline__ void stamp(const PsArgs& a, int l, int e) {
     if (a.trace && (threadIdx.x & 63) == 0)
         a.trace[(size_t)blockIdx.x * a.n_layers * PS_TRACE_PER_LAYER + l * PS_TRACE_PER_LAYER + e] = wall_clock64();
@@ -199,11 +213,10 @@ struct Ring {
 template <int CPL, int S, class Issue>
 __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg, int nrows, int rlocal, int ng,
                                          uint32_t sb, uint32_t xs, uint32_t res) {
+    static_assert(S >= 2 * CPL, "the ring must hold two rows");
     if (nrows == 0) return;
-    // the input slice stays in registers for short rows; longer rows read it from LDS with each slot
+    // the input slice stays in registers for short rows; longer rows read it from LDS with each row
     constexpr bool XR = CPL <= 4;
-    constexpr int XN = XR ? CPL : 1;
-    constexpr int UNR = XR ? CPL : 1;                        // the chunk index only selects addresses when !XR
     const int lane = threadIdx.x & 63;
     const half2_t one2 = {(_Float16)1.0f, (_Float16)1.0f};
     // chunk lane + 64 i of the input as 16 fp16 pairs, and its correction term
@@ -219,13 +232,14 @@ __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg
         }
         return 1032.0f * slo + 72.0f * shi;
     };
-    u32x4 xq[XN][4];
-    float corr[XN];
+    const uint32_t xl = xs + 64 * lane;                      // chunk `lane`; chunk lane + 64 i is 4 KB i further
+    u32x4 xq[XR ? CPL : 1][4];
+    float corr[XR ? CPL : 1];
     if constexpr (XR) {
 #pragma unroll
         for (int i = 0; i < CPL; ++i)
 #pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) xq[i][q4] = lds_rd16(xs + 64 * (lane + 64 * i) + 16 * q4);
+            for (int q4 = 0; q4 < 4; ++q4) xq[i][q4] = lds_rd16(xl + 4096 * i + 16 * q4);
         lgkm_wait_all();
 #pragma unroll
         for (int i = 0; i < CPL; ++i) {
@@ -235,56 +249,70 @@ __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg
         }
     }
     const int gstep = 128 / a.gchunks;                      // scale bytes between chunk i and i + 1 of a row
-    const uint32_t sl = sb + 2 * (uint32_t)(lane / a.gchunks);
+    const uint32_t sl = sb + 2 * (uint32_t)(lane / a.gchunks) + 2 * rlocal * ng;
     const uint32_t lane16 = 16 * lane;
-    const uint32_t xl = xs + 64 * lane;                      // chunk `lane` of the input; chunk lane + 64 i is 4 KB i further
     uint32_t magic = 0x64006400u;
     asm volatile("" : "+v"(magic));                         // kept in a VGPR for v_bfi
 
-    // first slot of the segment
-    if (rg.p <= rg.pmax) vm_wait<S - 1>(); else vm_wait_all();
-    u32x4 cw = lds_rd16(rg.addr(rg.ri) + lane16);
-    uint32_t cs = lds_rdu16(sl + 2 * rlocal * ng);
-    u32x4 cx[4];
-    if constexpr (!XR) {
+    // rows are consumed whole: codes and scales of row r are read (one wait) while
+    // row r - 1 computes; the row's slots are refilled as soon as they are in registers
+    u32x4 cw[CPL];
+    uint32_t cs[CPL];
+    auto read_row = [&](int r, u32x4 (&w)[CPL], uint32_t (&sc)[CPL]) {
+        int ri = rg.ri;
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) cx[q4] = lds_rd16(xl + 16 * q4);
-    }
+        for (int i = 0; i < CPL; ++i) {
+            w[i] = lds_rd16(rg.addr(ri) + lane16);
+            sc[i] = lds_rdu16(sl + 2 * r * ng + gstep * i);
+            ri = Ring::next(ri, S);
+        }
+    };
+    if (rg.p <= rg.pmax) vm_wait<S - CPL>(); else vm_wait_all();   // S + p <= total: S - CPL younger loads
+    read_row(0, cw, cs);
     lgkm_wait_all();
-    touch(cw);
-    touch(cs);
-    if constexpr (!XR) {
 #pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) touch(cx[q4]);
+    for (int i = 0; i < CPL; ++i) {
+        touch(cw[i]);
+        touch(cs[i]);
     }
-
     for (int r = 0; r < nrows; ++r) {
-        const uint32_t srow = sl + 2 * (rlocal + r) * ng;
+        // refill this row's slots, then start reading the next row
+#pragma unroll
+        for (int i = 0; i < CPL; ++i) {
+            issue(rg.addr(rg.ri));
+            rg.ri = Ring::next(rg.ri, S);
+        }
+        rg.p += CPL;
+        const bool more = r + 1 < nrows;
+        u32x4 nw[CPL];
+        uint32_t ns[CPL];
+        if (more) {
+            // younger than the next row's last slot: S - CPL while the stream is not near its end
+            if (rg.p <= rg.pmax) vm_wait<S - CPL>(); else vm_wait_all();
+            read_row(r + 1, nw, ns);
+        }
         float acc = 0.f;
+        constexpr int UNR = XR ? CPL : 1;
 #pragma unroll UNR
         for (int i = 0; i < CPL; ++i) {
-            const bool more = (i + 1 < CPL) || (r + 1 < nrows);
-            const int rn = Ring::next(rg.ri, S);
-            u32x4 nw = {0u, 0u, 0u, 0u};
-            uint32_t ns = 0u;
-            u32x4 nx[4];
-            if (more) {                                   // read the next slot while this one computes
-                if (rg.p <= rg.pmax) vm_wait<S - 2>(); else vm_wait_all();
-                nw = lds_rd16(rg.addr(rn) + lane16);
-                ns = lds_rdu16(i + 1 < CPL ? srow + gstep * (i + 1) : srow + 2 * ng);
-                if constexpr (!XR) {
-                    const uint32_t xa = xl + 4096 * (i + 1 < CPL ? i + 1 : 0);
+            u32x4 xc[4];
+            float ci;
+            if constexpr (XR) {
 #pragma unroll
-                    for (int q4 = 0; q4 < 4; ++q4) nx[q4] = lds_rd16(xa + 16 * q4);
-                }
+                for (int q4 = 0; q4 < 4; ++q4) xc[q4] = xq[i][q4];
+                ci = corr[i];
+            } else {
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) xc[q4] = lds_rd16(xl + 4096 * i + 16 * q4);
+                asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(acc)::"memory");
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) touch(xc[q4]);
+                ci = x_corr(xc);
             }
-            issue(rg.addr(rg.ri));                        // refill the slot just read into registers
-            const u32x4(&xc)[4] = XR ? xq[XR ? i : 0] : cx;
-            const float ci = XR ? corr[XR ? i : 0] : x_corr(cx);
             float lo0 = 0.f, lo1 = 0.f, hi0 = 0.f, hi1 = 0.f;
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
-                const uint32_t x = cw[q4];
+                const uint32_t x = cw[i][q4];
                 const uint32_t y = x >> 8;
                 const uint32_t p0 = bfi(0x000F000Fu, x, magic);
                 const uint32_t p1 = bfi(0x00F000F0u, x, magic);
@@ -299,26 +327,116 @@ __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg
                 hi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p3), __builtin_bit_cast(half2_t, x3), hi, false);
             }
             const float dq = __builtin_fmaf(hi0 + hi1, 0.0625f, (lo0 + lo1) - ci);
-            acc = __builtin_fmaf(f16_to_f32((uint16_t)cs), dq, acc);
-            if (more) {
-                lgkm_wait_all();
-                touch(nw);
-                touch(ns);
-                if constexpr (!XR) {
+            acc = __builtin_fmaf(f16_to_f32((uint16_t)cs[i]), dq, acc);
+        }
+        if (more) {
+            // the wait takes acc as an operand, so this row's arithmetic is issued before it
+            asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(acc)::"memory");
 #pragma unroll
-                    for (int q4 = 0; q4 < 4; ++q4) {
-                        touch(nx[q4]);
-                        cx[q4] = nx[q4];
-                    }
-                }
+            for (int i = 0; i < CPL; ++i) {
+                touch(nw[i]);
+                touch(ns[i]);
+                cw[i] = nw[i];
+                cs[i] = ns[i];
             }
-            ++rg.p;
-            rg.ri = rn;
-            cw = nw;
-            cs = ns;
         }
         const float rs = wave_sum(acc);
         if (lane == 0) lds_wr4(res + 4 * (rlocal + r), rs);
+    }
+}
+
+// Slot range of one wave in a long-row GEMV segment (input chunks read from
+// LDS): the workgroup's rows x CPL chunks are split evenly over its compute
+// waves in row-major order, so a row may be shared by two waves.  Partials go
+// to res[2 r] (the part holding the row's first chunk) and res[2 r + 1].
+__host__ __device__ __forceinline__ int kslot_per_wave(int rows, int cpl) { return (rows * cpl + SK_CW - 1) / SK_CW; }
+
+template <int CPL, int S, class Issue>
+__device__ __forceinline__ void gemv_seg_k(const PsArgs& a, Issue& issue, Ring& rg, int s0, int ns, int ng, uint32_t sb,
+                                           uint32_t xs, uint32_t res) {
+    if (ns == 0) return;
+    const int lane = threadIdx.x & 63;
+    const half2_t one2 = {(_Float16)1.0f, (_Float16)1.0f};
+    const uint32_t xl = xs + 64 * lane;                      // chunk `lane`; chunk lane + 64 i is 4 KB i further
+    const int gstep = 128 / a.gchunks;
+    const uint32_t sl = sb + 2 * (uint32_t)(lane / a.gchunks);
+    const uint32_t lane16 = 16 * lane;
+    uint32_t magic = 0x64006400u;
+    asm volatile("" : "+v"(magic));
+    int r = s0 / CPL, i = s0 % CPL;                         // row (within the workgroup) and chunk of the current slot
+    auto read_slot = [&](int rr, int ii, int ri, u32x4& w, uint32_t& sc, u32x4 (&x)[4]) {
+        w = lds_rd16(rg.addr(ri) + lane16);
+        sc = lds_rdu16(sl + 2 * rr * ng + gstep * ii);
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) x[q4] = lds_rd16(xl + 4096 * ii + 16 * q4);
+    };
+    u32x4 cw, cx[4];
+    uint32_t cs;
+    if (rg.p <= rg.pmax) vm_wait<S - 1>(); else vm_wait_all();
+    read_slot(r, i, rg.ri, cw, cs, cx);
+    lgkm_wait_all();
+    touch(cw);
+    touch(cs);
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) touch(cx[q4]);
+    float acc = 0.f;
+    bool first_part = (i == 0);
+    for (int k = 0; k < ns; ++k) {
+        const bool more = k + 1 < ns;
+        const int rn = Ring::next(rg.ri, S);
+        const int i2 = (i + 1 == CPL) ? 0 : i + 1, r2 = (i + 1 == CPL) ? r + 1 : r;
+        u32x4 nw, nx[4];
+        uint32_t ns_ = 0u;
+        if (more) {
+            if (rg.p <= rg.pmax) vm_wait<S - 2>(); else vm_wait_all();
+            read_slot(r2, i2, rn, nw, ns_, nx);
+        }
+        issue(rg.addr(rg.ri));                              // refill the slot just read into registers
+        float slo = 0.f, shi = 0.f, lo0 = 0.f, lo1 = 0.f, hi0 = 0.f, hi1 = 0.f;
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+            const uint32_t x = cw[q4];
+            const uint32_t y = x >> 8;
+            const uint32_t p0 = bfi(0x000F000Fu, x, magic);
+            const uint32_t p1 = bfi(0x00F000F0u, x, magic);
+            const uint32_t p2 = bfi(0x000F000Fu, y, magic);
+            const uint32_t p3 = bfi(0x00F000F0u, y, magic);
+            const uint32_t x0 = cx[q4][0], x1 = cx[q4][1], x2 = cx[q4][2], x3 = cx[q4][3];
+            float& lo = (q4 & 1) ? lo1 : lo0;
+            float& hi = (q4 & 1) ? hi1 : hi0;
+            lo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p0), __builtin_bit_cast(half2_t, x0), lo, false);
+            lo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p2), __builtin_bit_cast(half2_t, x2), lo, false);
+            hi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p1), __builtin_bit_cast(half2_t, x1), hi, false);
+            hi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p3), __builtin_bit_cast(half2_t, x3), hi, false);
+            slo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, x0), one2, slo, false);
+            slo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, x2), one2, slo, false);
+            shi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, x1), one2, shi, false);
+            shi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, x3), one2, shi, false);
+        }
+        const float dq = __builtin_fmaf(hi0 + hi1, 0.0625f, (lo0 + lo1) - (1032.0f * slo + 72.0f * shi));
+        acc = __builtin_fmaf(f16_to_f32((uint16_t)cs), dq, acc);
+        if (i + 1 == CPL || !more) {                        // this wave's part of row r is complete
+            const float rs = wave_sum(acc);
+            if (lane == 0) lds_wr4(res + 4 * (2 * r + (first_part ? 0 : 1)), rs);
+            acc = 0.f;
+            first_part = true;
+        }
+        if (more) {
+            asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(acc)::"memory");
+            touch(nw);
+            touch(ns_);
+            cw = nw;
+            cs = ns_;
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                touch(nx[q4]);
+                cx[q4] = nx[q4];
+            }
+        }
+        ++rg.p;
+        rg.ri = rn;
+        r = r2;
+        i = i2;
     }
 }
 
@@ -468,7 +586,14 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         }
     }
     // slots per segment of one layer: q|k|v rows, K/V slot pairs, o, gate|up, down rows
-    const int n0 = rq_.count * CPL_H, n1 = 2 * T, n2 = ro_.count * CPL_Q, n3 = rg_.count * CPL_H, n4 = ro_.count * CPL_F;
+    // down rows: whole rows per wave when the input slice fits registers, else an even slot range
+    constexpr bool XR_F = CPL_F <= 4;
+    const int wg_rows_h = max(0, min(a.H, (w + 1) * a.rpw_h) - w * a.rpw_h);
+    const int kspw = kslot_per_wave(wg_rows_h, CPL_F);
+    const int ks0 = min(wg_rows_h * CPL_F, cw * kspw);
+    const int kns = min(wg_rows_h * CPL_F, ks0 + kspw) - ks0;
+    const int n0 = rq_.count * CPL_H, n1 = 2 * T, n2 = ro_.count * CPL_Q, n3 = rg_.count * CPL_H;
+    const int n4 = XR_F ? ro_.count * CPL_F : kns;
     const int total = (n0 + n1 + n2 + n3 + n4) * L;
     // The weight rows of one wave in one segment are contiguous in the row layout
     // (kc = 64 * CPL chunks per row), so a segment streams one block of 1 KB slots.
@@ -492,7 +617,8 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         if (gs == 0) gptr = layers[gl].qkv.w + (u64)rq_.first * a.kc_h * 16;
         else if (gs == 2) gptr = layers[gl].o.w + (u64)ro_.first * a.kc_q * 16;
         else if (gs == 3) gptr = layers[gl].gu.w + (u64)rg_.first * a.kc_h * 16;
-        else if (gs == 4) gptr = layers[gl].d.w + (u64)ro_.first * a.kc_f * 16;
+        else if (gs == 4)
+            gptr = layers[gl].d.w + (XR_F ? (u64)ro_.first * a.kc_f * 16 : (u64)w * a.rpw_h * a.kc_f * 16 + (u64)ks0 * SK_SLOT);
     };
     auto issue = [&](uint32_t dst) {
         if (gleft == 0) return;
@@ -524,16 +650,25 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         gemv_seg<CPL_H, S>(a, issue, rg, rq_.count, rq_.local, a.ng_h, lb + a.l_sb0, lb + a.l_xs, lb + a.l_res);
         wg_barrier();                                       // q|k|v rows are in LDS
         wg_barrier();                                       // q and the new row are staged
+        cstamp(a, lb + a.l_dbg, 0);
         att_seg<GS, D, S>(a, issue, rg, T, mbits, lb + a.l_q, lb + a.l_part);
+        cstamp(a, lb + a.l_dbg, 1);
         wg_barrier();                                       // wave partials are in LDS
         wg_barrier();                                       // attention output is staged
         gemv_seg<CPL_Q, S>(a, issue, rg, ro_.count, ro_.local, a.ng_q, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
         wg_barrier();
         wg_barrier();                                       // RMSNorm(x) is staged
+        cstamp(a, lb + a.l_dbg, 2);
         gemv_seg<CPL_H, S>(a, issue, rg, rg_.count, rg_.local, a.ng_h, lb + a.l_sb0, lb + a.l_xs, lb + a.l_res);
+        cstamp(a, lb + a.l_dbg, 3);
         wg_barrier();
         wg_barrier();                                       // SwiGLU output is staged
-        gemv_seg<CPL_F, S>(a, issue, rg, ro_.count, ro_.local, a.ng_f, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
+        cstamp(a, lb + a.l_dbg, 4);
+        if constexpr (XR_F)
+            gemv_seg<CPL_F, S>(a, issue, rg, ro_.count, ro_.local, a.ng_f, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
+        else
+            gemv_seg_k<CPL_F, S>(a, issue, rg, ks0, kns, a.ng_f, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
+        cstamp(a, lb + a.l_dbg, 5);
         wg_barrier();
     }
 }
@@ -552,8 +687,15 @@ __device__ __forceinline__ void load_scales(const uint16_t* s, int first, int co
 // Input of an RMSNorm'd GEMV: K values (fp32 coherent, or act dtype written
 // before the launch when src_dt != DT_F32) -> x * rsqrt(mean(x^2) + eps) * gamma
 // as fp16 in LDS xs; padding up to kpad is zeroed.
+// RMSNorm weights (K values, 2 bytes each) into LDS with direct loads, issued a
+// phase ahead so their latency is hidden; the buffer must hold whole 1 KB blocks.
+__device__ __forceinline__ void load_gamma(const uint16_t* gamma, int K, uint32_t dst) {
+    const int lane = threadIdx.x & 63;
+    for (int off = 0; off < K * 2; off += SK_SLOT) dma16((const uint8_t*)gamma + off + 16 * lane, dst + off);
+}
+
 template <int NT>
-__device__ __forceinline__ void stage_norm(const void* src, int src_dt, int K, int kpad, const uint16_t* gamma,
+__device__ __forceinline__ void stage_norm(const void* src, int src_dt, int K, int kpad, const uint8_t* gl,
                                            int gamma_dt, float eps, uint8_t* xs) {
     const int lane = threadIdx.x & 63;
     const int n4 = K / 4;
@@ -586,7 +728,7 @@ __device__ __forceinline__ void stage_norm(const void* src, int src_dt, int K, i
     for (int t = 0; t < NT; ++t) {
         const int it = lane + 64 * t;
         if (it < n4) {
-            const u32x2 gv = *(const u32x2*)(gamma + 4 * it);
+            const u32x2 gv = *(const u32x2*)(gl + 8 * it);
             float y[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -599,28 +741,16 @@ __device__ __forceinline__ void stage_norm(const void* src, int src_dt, int K, i
     for (int it = n4 + lane; it < kpad / 4; it += 64) *(u32x2*)(xs + 8 * it) = u32x2{0u, 0u};
 }
 
-// Input of a plain GEMV: K fp16 values written coherently by this launch -> LDS xs.
-template <int NT>
-__device__ __forceinline__ void stage_plain(const uint16_t* src, int K, int kpad, uint8_t* xs) {
+// Input of a plain GEMV: K fp16 values written coherently by this launch -> LDS xs,
+// with direct loads (whole 1 KB blocks: the source buffers are padded); the caller
+// waits for them (vm_wait_all) and then zeroes the padding past K with zero_pad.
+__device__ __forceinline__ void stage_plain(const uint16_t* src, int K, uint32_t xs) {
     const int lane = threadIdx.x & 63;
-    const int n8 = K / 8;
-    const __amdgpu_buffer_rsrc_t r = make_rsrc(src, (size_t)K * 2);
-    constexpr int NB = NT < 16 ? NT : 16;                 // loads in flight per round
-#pragma unroll
-    for (int t0 = 0; t0 < NT; t0 += NB) {
-        f32x4 v[NB];
-#pragma unroll
-        for (int t = 0; t < NB; ++t) {
-            const int it = lane + 64 * (t0 + t);
-            v[t] = load4_coherent(r, (t0 + t < NT && it < n8) ? it * 16 : 0);
-        }
-#pragma unroll
-        for (int t = 0; t < NB; ++t) {
-            const int it = lane + 64 * (t0 + t);
-            if (t0 + t < NT && it < n8) *(f32x4*)(xs + 16 * it) = v[t];
-        }
-    }
-    for (int it = n8 + lane; it < kpad / 8; it += 64) *(f32x4*)(xs + 16 * it) = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int off = 0; off < K * 2; off += SK_SLOT) dma16_coherent((const uint8_t*)src + off + 16 * lane, xs + off);
+}
+__device__ __forceinline__ void zero_pad(int K, int kpad, uint8_t* xs) {
+    const int lane = threadIdx.x & 63;
+    for (int it = K / 8 + lane; it < kpad / 8; it += 64) *(f32x4*)(xs + 16 * it) = f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
 template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
@@ -635,8 +765,6 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     const float* part = (const float*)(smem + a.l_part);
     const float2* rope = (const float2*)(smem + a.l_rope);
     constexpr int NT_H = CPL_H * 8;          // float4 items per lane of a K = H input (K padded to 2048 * CPL_H)
-    constexpr int NT_Q = CPL_Q * 4;          // 8-value items per lane of the attention output
-    constexpr int NT_F = CPL_F * 4;
     constexpr int OPL = GS * D / 64;         // merged outputs per lane
     constexpr int LPH = D / OPL;             // lanes per query head in the merge
     static_assert(OPL == 2 || OPL == 4 || OPL == 8, "merge layout");
@@ -662,7 +790,12 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     if (lane < D / 2) ((float2*)rope)[lane] = a.rope[(size_t)pos * (D / 2) + lane];
     load_scales(a.layers[0].qkv.s, w * a.rpw_qkv, max(0, min(a.NQKV, (w + 1) * a.rpw_qkv) - w * a.rpw_qkv), a.ng_h,
                 lb + a.l_sb0);
-    stage_norm<NT_H>(a.hidden_in, a.act_dt, a.H, a.kc_h * 32, a.layers[0].attn_norm, a.act_dt, a.eps, xs);
+    // RMSNorm weights of the next normalization live in the attention-partials
+    // region while it is free (after the split merge until the next attention)
+    const uint8_t* gam = smem + a.l_part;
+    load_gamma(a.layers[0].attn_norm, a.H, lb + a.l_part);
+    vm_wait_all();
+    stage_norm<NT_H>(a.hidden_in, a.act_dt, a.H, a.kc_h * 32, gam, a.act_dt, a.eps, xs);
     bool ok = true;
     int bar = 0;
     vm_wait_all();
@@ -673,6 +806,7 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         const bool last = (l == a.n_layers - 1);
         stamp(a, l, 0);
         load_scales(Ly.o.s, xr0, nxr, a.ng_q, lb + a.l_sb1);
+        load_gamma(Ly.ffn_norm, a.H, lb + a.l_gff);            // free since the last down phase
         wg_barrier();                                         // q|k|v rows are in LDS
         stamp(a, l, 1);
         // ---- rotary embedding of q and k (rows 2d, 2d + 1 of a head are d, d + D/2), coherent stores
@@ -734,9 +868,10 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
                 if (l == 0 && g == 0 && lane == 0) rq.table[(size_t)b * rq.cap + P] = (int16_t)b;
             }
         }
-        load_scales(Ly.gu.s, w * a.rpw_gu, max(0, min(2 * a.F, (w + 1) * a.rpw_gu) - w * a.rpw_gu), a.ng_h, lb + a.l_sb0);
         vm_wait_all();
         wg_barrier();                                         // q and the new row are staged
+        // gate|up scales (q|k|v finished with this buffer) load while the compute waves run the attention
+        load_scales(Ly.gu.s, w * a.rpw_gu, max(0, min(2 * a.F, (w + 1) * a.rpw_gu) - w * a.rpw_gu), a.ng_h, lb + a.l_sb0);
         wg_barrier();                                         // wave partials are in LDS
         stamp(a, l, 3);
         // ---- merge the waves (and the new row) into this split's partial; the last split merges the splits
@@ -783,52 +918,61 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
                 store_coherent(pp + 1, L);
             }
             vm_wait_all();
+            // every split of this kv head waits for all of them, then merges its own
+            // 1/nsplit slice of the head group's outputs (one round of loads)
             unsigned prev = 0;
             if (lane == 0) prev = atomicAdd(&a.acnt[g], 1u);
             prev = __builtin_amdgcn_readfirstlane(prev);
-            if (((prev + 1u) & (unsigned)(a.nsplit - 1)) == 0u) {
-                // last arrival of this kv head: merge its nsplit partials
-                const __amdgpu_buffer_rsrc_t r =
-                    make_rsrc(a.apart, (size_t)a.Hkv * a.nsplit * GS * (D + 4) * 4);
-                float Mx = -INFINITY, Ls = 0.f, Os[OPL];
-#pragma unroll
-                for (int e = 0; e < OPL; ++e) Os[e] = 0.f;
-                constexpr int MB = 4;                            // splits per round
-                for (int s0 = 0; s0 < a.nsplit; s0 += MB) {
-                    f32x4 st4[MB], ov[MB][(OPL + 3) / 4];
-#pragma unroll
-                    for (int k = 0; k < MB; ++k) {
-                        const int s2 = min(s0 + k, a.nsplit - 1);
-                        const int base = (int)((((size_t)g * a.nsplit + s2) * GS + hq) * (D + 4)) * 4;
-                        st4[k] = load4_coherent(r, base);
-#pragma unroll
-                        for (int q4 = 0; q4 < (OPL + 3) / 4; ++q4) ov[k][q4] = load4_coherent(r, base + 16 + 4 * d0 + 16 * q4);
-                    }
-#pragma unroll
-                    for (int k = 0; k < MB; ++k) {
-                        if (s0 + k >= a.nsplit) break;
-                        const float ms = st4[k][0];
-                        if (ms == -INFINITY) continue;
-                        const float mn = fmaxf(Mx, ms);
-                        const float c1 = (Mx == -INFINITY) ? 0.f : exp2f(Mx - mn);
-                        const float c2 = exp2f(ms - mn);
-                        Ls = Ls * c1 + st4[k][1] * c2;
-#pragma unroll
-                        for (int e = 0; e < OPL; ++e) Os[e] = Os[e] * c1 + ov[k][e / 4][e % 4] * c2;
-                        Mx = mn;
+            const unsigned target = (prev & ~(unsigned)(a.nsplit - 1)) + (unsigned)a.nsplit;
+            if (ok) {
+                unsigned spins = 0;
+                while ((int)(__hip_atomic_load(&a.acnt[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
+                    __builtin_amdgcn_s_sleep(1);
+                    if (++spins > SK_SPIN_LIMIT) {
+                        if (lane == 0) atomicOr(a.err, 1u);
+                        ok = false;
+                        break;
                     }
                 }
-                const float inv = 1.0f / Ls;
-                uint32_t* dst = (uint32_t*)(a.o + (size_t)(g * GS + hq) * D + d0);
+            }
+            const int SL = GS * D / a.nsplit;                 // outputs per slice (multiple of 8)
+            const int CH = SL / 8;                            // 8-output chunks per slice
+            const int s2 = lane / CH, c = lane % CH;          // lane: one split's chunk of the slice
+            const bool act = s2 < a.nsplit;
+            const int o0 = split * SL + 8 * c;                // first output of the chunk within the head group
+            const int hh = o0 / D, dd = o0 % D;
+            const __amdgpu_buffer_rsrc_t r = make_rsrc(a.apart, (size_t)a.Hkv * a.nsplit * GS * (D + 4) * 4);
+            const int base = act ? (int)((((size_t)g * a.nsplit + s2) * GS + hh) * (D + 4)) * 4 : 0;
+            const f32x4 st4 = load4_coherent(r, base);
+            const f32x4 oa = load4_coherent(r, base + 16 + 4 * dd);
+            const f32x4 ob = load4_coherent(r, base + 32 + 4 * dd);
+            float ms = act ? st4[0] : -INFINITY, ls = act ? st4[1] : 0.f;
+            float ov[8] = {oa[0], oa[1], oa[2], oa[3], ob[0], ob[1], ob[2], ob[3]};
+            // combine the splits: lanes c, c + CH, c + 2 CH, ... (fixed butterfly order)
+            float Mx = ms;
+            for (int sh = CH; sh < 64; sh <<= 1) Mx = fmaxf(Mx, __shfl_xor(Mx, sh));
+            const float wgt = (ms == -INFINITY) ? 0.f : exp2f(ms - Mx);
+            float Ls = wgt * ls;
 #pragma unroll
-                for (int e = 0; e < OPL; e += 2) store_coherent_u32(dst + e / 2, pack_f16x2(Os[e] * inv, Os[e + 1] * inv));
+            for (int e = 0; e < 8; ++e) ov[e] *= wgt;
+            for (int sh = CH; sh < 64; sh <<= 1) {
+                Ls += __shfl_xor(Ls, sh);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) ov[e] += __shfl_xor(ov[e], sh);
+            }
+            if (act && s2 == 0) {
+                const float inv = 1.0f / Ls;
+                uint32_t* dst = (uint32_t*)(a.o + (size_t)(g * GS + hh) * D + dd);
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) store_coherent_u32(dst + e / 2, pack_f16x2(ov[e] * inv, ov[e + 1] * inv));
             }
         }
         if (ok) ok = grid_sync(a, bar);
         ++bar;
         stamp(a, l, 4);
-        stage_plain<NT_Q>(a.o, a.QD, a.kc_q * 32, xs);
+        stage_plain(a.o, a.QD, lb + a.l_xs);
         vm_wait_all();
+        zero_pad(a.QD, a.kc_q * 32, xs);
         wg_barrier();                                         // attention output staged
         wg_barrier();                                         // o rows are in LDS
         stamp(a, l, 5);
@@ -840,10 +984,10 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         if (ok) ok = grid_sync(a, bar);
         ++bar;
         stamp(a, l, 6);
-        stage_norm<NT_H>(a.x, DT_F32, a.H, a.kc_h * 32, Ly.ffn_norm, a.act_dt, a.eps, xs);
-        load_scales(Ly.d.s, xr0, nxr, a.ng_f, lb + a.l_sb1);
+        stage_norm<NT_H>(a.x, DT_F32, a.H, a.kc_h * 32, smem + a.l_gff, a.act_dt, a.eps, xs);
         vm_wait_all();
         wg_barrier();                                         // RMSNorm(x) staged
+        load_scales(Ly.d.s, xr0, nxr, a.ng_f, lb + a.l_sb1);   // o finished with this buffer
         wg_barrier();                                         // gate|up rows are in LDS
         stamp(a, l, 7);
         // ---- act = silu(gate) * up, two values per lane as one coherent dword
@@ -863,19 +1007,29 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         if (ok) ok = grid_sync(a, bar);
         ++bar;
         stamp(a, l, 8);
-        stage_plain<NT_F>(a.act, a.F, a.kc_f * 32, xs);
+        stage_plain(a.act, a.F, lb + a.l_xs);
         vm_wait_all();
+        zero_pad(a.F, a.kc_f * 32, xs);
         wg_barrier();                                         // SwiGLU output staged
         if (!last) {
             const PsLayer& Ln = a.layers[l + 1];
             load_scales(Ln.qkv.s, w * a.rpw_qkv, max(0, min(a.NQKV, (w + 1) * a.rpw_qkv) - w * a.rpw_qkv), a.ng_h,
                         lb + a.l_sb0);
+            load_gamma(Ln.attn_norm, a.H, lb + a.l_part);
         }
         wg_barrier();                                         // down rows are in LDS
         stamp(a, l, 9);
+        if (a.trace && lane < 6)
+            a.trace[((size_t)blockIdx.x * a.n_layers + l) * PS_TRACE_PER_LAYER + 10 + lane] = ((const u64*)(smem + a.l_dbg))[lane];
         // ---- x += act Wd^T (own rows); the last layer writes hidden_out
         if (lane < nxr) {
-            xrow += res[lane];
+            if constexpr (CPL_F <= 4) {
+                xrow += res[lane];
+            } else {                                          // rows shared by two waves have two partials
+                const int kspw = kslot_per_wave(nxr, CPL_F);
+                const bool two = (lane * CPL_F) / kspw != (lane * CPL_F + CPL_F - 1) / kspw;
+                xrow += two ? res[2 * lane] + res[2 * lane + 1] : res[2 * lane];
+            }
             if (last)
                 ((uint16_t*)a.hidden_out)[xr0 + lane] = to_half_bits(xrow, a.act_dt);
             else
@@ -884,7 +1038,7 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         if (!last) {
             if (ok) ok = grid_sync(a, bar);
             ++bar;
-            stage_norm<NT_H>(a.x, DT_F32, a.H, a.kc_h * 32, a.layers[l + 1].attn_norm, a.act_dt, a.eps, xs);
+            stage_norm<NT_H>(a.x, DT_F32, a.H, a.kc_h * 32, gam, a.act_dt, a.eps, xs);
             vm_wait_all();
             wg_barrier();                                     // next layer's q|k|v input staged
         }
@@ -904,8 +1058,8 @@ __global__ __launch_bounds__(SK_THREADS) void stage_stream_kernel(PsArgs a) {
 
 // Instantiations: (K / 2048 for K = H, Hq*D, F), head_dim, query heads per kv head, ring slots.
 #define PS_SHAPES(X)                 \
-    X(2, 2, 7, 128, 4, 24)   /* Llama-3.1-8B layers */ \
-    X(1, 1, 1, 64, 2, 24)    /* small test stages */
+    X(2, 2, 7, 128, 4, 14)   /* Llama-3.1-8B layers */ \
+    X(1, 1, 1, 64, 2, 14)    /* small test stages */
 
 bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int gs) {
 #define PS_MATCH(H_, Q_, F_, D_, G_, S_) \

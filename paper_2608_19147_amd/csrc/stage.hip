@@ -373,7 +373,8 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
             free_tmp();
             return cleanup(rc);
         }
-        if ((rc = st->alloc(&L.attn_norm, H)) || (rc = st->alloc(&L.ffn_norm, H))) {
+        const size_t nalloc = ((size_t)H + SK_SLOT / 2 - 1) / (SK_SLOT / 2) * (SK_SLOT / 2);   // whole 1 KB blocks
+        if ((rc = st->alloc(&L.attn_norm, nalloc)) || (rc = st->alloc(&L.ffn_norm, nalloc))) {
             free_tmp();
             return cleanup(rc);
         }
@@ -458,6 +459,7 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         probe.kc_h = st->kc_h; probe.kc_q = st->kc_q; probe.kc_f = st->kc_f;
         probe.ng_h = st->ng_h; probe.ng_q = st->ng_q; probe.ng_f = st->ng_f;
         probe.rpw_qkv = st->ps_rpw_qkv; probe.rpw_h = st->ps_rpw_h; probe.rpw_gu = st->ps_rpw_gu;
+        probe.H = H;
         const int slots = ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv);
         if (slots <= 0 || ps_layout(probe, slots, D, Hq / Hkv) > 160 * 1024) st->ps_ok = false;
         if ((rc = st->alloc(&st->acnt_ps, Hkv))) return cleanup(rc);
@@ -847,14 +849,16 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     bool single = st->ps_ok && M == 1 && (st->prof_class < 0 || st->prof_class == STAGE_KERNEL_PERSISTENT);
     if (single) {
         const int P = reqs[0].state->P;
+        // splits per kv head: a power of two; each split's merge slice is a multiple of 8 outputs
+        const int max_split = std::min(st->ps_nwg / Hkv, gs * D / 8);
         int cap_split = 16;
         if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) cap_split = std::max(1, atoi(e));
         nsplit = 1;
-        while (nsplit * 2 <= cap_split && nsplit * 2 * Hkv <= st->ps_nwg) nsplit *= 2;
+        while (nsplit * 2 <= std::min(cap_split, max_split)) nsplit *= 2;
         for (;;) {
             split_len = (P + nsplit - 1) / nsplit;
             att_T = ((split_len + SK_CW - 1) / SK_CW + RPS - 1) / RPS;
-            if (att_T <= SK_TMAX || nsplit * 2 * Hkv > st->ps_nwg) break;
+            if (att_T <= SK_TMAX || nsplit * 2 > max_split) break;
             nsplit *= 2;
         }
         if (att_T > SK_TMAX) single = false;               // cache too long for one pass: per-layer kernels

@@ -105,12 +105,12 @@ class Stage:
         return n.value, ms.value
 
     def phase_trace(self) -> np.ndarray:
-        """[workgroups, layers, 10] device real-time stamps (100 MHz) of the last
+        """[workgroups, layers, 16] device real-time stamps (100 MHz) of the last
         single-launch forward (needs STAGE_PS_TRACE=1 at creation)."""
-        n = torch.cuda.get_device_properties(0).multi_processor_count * self.shape.n_layers * 10
+        n = torch.cuda.get_device_properties(0).multi_processor_count * self.shape.n_layers * 16
         out = np.empty(n, dtype=np.uint64)
         check(self.lib.stage_debug_phase_trace(self.handle, out.ctypes.data, n))
-        return out.reshape(-1, self.shape.n_layers, 10)
+        return out.reshape(-1, self.shape.n_layers, 16)
 
     def new_state(self, n_slots: int, capacity: int) -> "KVState":
         return KVState(self, n_slots, capacity)
