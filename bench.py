@@ -158,7 +158,7 @@ def main() -> int:
     launches, prof_ms = prof
     per_launch_ms = prof_ms / max(1, launches)
     if dominant == "persistent":
-        k_bytes, k_name = b["total"], "stage_persistent_kernel (whole stage forward, one launch per step)"
+        k_bytes, k_name = b["total"], "stage_stream_kernel (whole stage forward, one launch per step)"
     else:
         k_bytes, k_name = gateup_bytes(shape), "gemv_kernel gate|up (one launch per layer)"
     k_gbps = k_bytes / (per_launch_ms * 1e-3) / 1e9

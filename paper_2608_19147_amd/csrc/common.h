@@ -175,8 +175,10 @@ bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int gs);
 // single launch is only used when this is zero.
 size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int gs);
 int ps_slots(int cpl_h, int cpl_q, int cpl_f, int D, int gs);   // ring slots per compute wave
+// coop = false launches without the co-residency check (one workgroup per CU on an
+// otherwise idle device; a profiling aid for tools that do not follow cooperative launches).
 hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int gs, int nwg, size_t lds,
-                             hipStream_t st);
+                             bool coop, hipStream_t st);
 hipError_t launch_repack_rows(const uint8_t* q, const uint16_t* s, int n, int k, int g, uint8_t* w_out, uint16_t* s_out,
                               int kc, int ng, int row_off, int row_map, int head_dim, hipStream_t st);
 hipError_t launch_dequant_rows(const PsMat& m, int kc, int ng, int gchunks, int k, int row_off, int row_map, int n_rows,

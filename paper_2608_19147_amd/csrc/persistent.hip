@@ -1096,7 +1096,7 @@ size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int gs) {
 }
 
 template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
-hipError_t launch_ps(const PsArgs& a, int nwg, size_t lds, hipStream_t st) {
+hipError_t launch_ps(const PsArgs& a, int nwg, size_t lds, bool coop, hipStream_t st) {
     const void* fn = (const void*)stage_stream_kernel<CPL_H, CPL_Q, CPL_F, D, GS, S>;
     static bool configured = false;
     if (!configured) {
@@ -1106,13 +1106,14 @@ hipError_t launch_ps(const PsArgs& a, int nwg, size_t lds, hipStream_t st) {
     }
     PsArgs copy = a;
     void* args[] = {&copy};
-    return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(SK_THREADS), args, (unsigned)lds, st);
+    if (coop) return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(SK_THREADS), args, (unsigned)lds, st);
+    return hipLaunchKernel(fn, dim3(nwg), dim3(SK_THREADS), args, (unsigned)lds, st);
 }
 
 hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int gs, int nwg, size_t lds,
-                             hipStream_t st) {
+                             bool coop, hipStream_t st) {
 #define PS_MATCH(H_, Q_, F_, D_, G_, S_) \
-    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return launch_ps<H_, Q_, F_, D_, G_, S_>(a, nwg, lds, st);
+    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return launch_ps<H_, Q_, F_, D_, G_, S_>(a, nwg, lds, coop, st);
     PS_SHAPES(PS_MATCH)
 #undef PS_MATCH
     return hipErrorInvalidValue;

@@ -73,6 +73,7 @@ struct Stage {
     int ps_nwg = 0;
     int ps_rpw_qkv = 0, ps_rpw_h = 0, ps_rpw_gu = 0;    // rows per workgroup of the single-launch forward
     unsigned* acnt_ps = nullptr;                        // its split arrival counters (only ever incremented)
+    bool ps_coop = true;                                // cooperative launch (STAGE_COOP=0: plain launch, for profilers)
     unsigned long long* trace = nullptr;   // phase stamps of the last persistent forward (STAGE_PS_TRACE=1)
     int prof_class = -1;
     std::vector<hipEvent_t> prof_ev;   // start/stop pairs
@@ -465,6 +466,7 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         if ((rc = st->alloc(&st->acnt_ps, Hkv))) return cleanup(rc);
         if (hipMemset(st->acnt_ps, 0, Hkv * sizeof(unsigned)) != hipSuccess)
             return cleanup(fail(STAGE_E_HIP, "counter init failed"));
+        if (const char* e = std::getenv("STAGE_COOP")) st->ps_coop = atoi(e) != 0;
         if (const char* e = std::getenv("STAGE_PS_TRACE"))
             if (atoi(e) && (rc = st->alloc(&st->trace, (size_t)cus * c.n_layers * PS_TRACE_PER_LAYER)))
                 return cleanup(rc);
@@ -890,7 +892,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         a.trace = st->trace;
         const int lds = ps_layout(a, ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, gs), D, gs);
         HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, true, s));
-        hipError_t e = launch_persistent(a, st->cpl_h, st->cpl_q, st->cpl_f, D, gs, st->ps_nwg, (size_t)lds, s);
+        hipError_t e = launch_persistent(a, st->cpl_h, st->cpl_q, st->cpl_f, D, gs, st->ps_nwg, (size_t)lds, st->ps_coop, s);
         if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("single-launch forward: ") + hipGetErrorString(e));
         HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, false, s));
         st->bar_epoch += (unsigned long long)(5 * c.n_layers - 1);
