@@ -207,16 +207,21 @@ int stage_profile_read(Stage* stage, int* launches, double* total_ms);
 
 /* Test and measurement support: phase-boundary timestamps of the last
  * single-launch forward, recorded only when STAGE_PS_TRACE=1 was set in the
- * environment at stage_create.  out_host receives [workgroups][n_layers][16]
- * readings of the 100 MHz device real-time counter.  Entries 0-9 are taken by
- * each workgroup's control wave at: layer start (q|k|v input staged), q|k|v
- * rows done, after the q|k|v -> attention grid barrier, attention partials
- * done, after the attention -> o barrier, o rows done, after the o -> gate|up
- * barrier, gate|up rows done, after the gate|up -> down barrier, down rows
- * done.  Entries 10-15 are taken by its first compute wave at the start and
- * end of its attention, gate|up and down work.  n = capacity of out_host in
- * entries.  Synchronizes the device. */
-int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n);
+ * environment at stage_create.  out_host receives [workgroups][n_layers][32]
+ * entries; *n_workgroups (if not NULL) receives the workgroup count of that
+ * launch.  Times are readings of the 100 MHz device real-time counter.
+ * Entries 0-9 are taken by each workgroup's control wave at: layer start
+ * (q|k|v input staged), q|k|v rows done, q|k|v published, attention partials
+ * done, split merge done, o rows done, residual published, gate|up rows done,
+ * SwiGLU output published, down rows done.  Entries 10-15 are taken by its
+ * first compute wave at the start and end of its attention, gate|up and down
+ * work.  Entries 16-21 count the polling passes of the control wave's six
+ * exchange waits of the layer (queries and new cache row, split partials,
+ * attention output, residual after o, SwiGLU output, residual after down),
+ * entries 22-27 are the times those waits ended, entries 28-30 the times the
+ * first pass of the residual-after-o, residual-after-down and remaining waits
+ * returned.  n = capacity of out_host in entries.  Synchronizes the device. */
+int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n, int* n_workgroups);
 
 /* Bytes of device memory the stage holds for weights (packed codes + scales +
  * norm weights), as stored. */

@@ -82,7 +82,7 @@ def load() -> ctypes.CDLL:
         "stage_last_error": (ctypes.c_char_p, []),
         "stage_profile_enable": (I, [V, I]),
         "stage_profile_read": (I, [V, P(I), P(ctypes.c_double)]),
-        "stage_debug_phase_trace": (I, [V, V, I]),
+        "stage_debug_phase_trace": (I, [V, V, I, V]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

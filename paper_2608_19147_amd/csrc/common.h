@@ -117,24 +117,27 @@ struct PsArgs {
     const void* hidden_in;
     void* hidden_out;
     int rpw_qkv, rpw_h, rpw_gu;          // rows per workgroup: q|k|v, o and down, gate|up
-    float* x;                            // [H] fp32 residual stream, exchanged coherently
-    float* qkv;                          // [NQKV] fp32: rotated q, rotated k, v
-    uint16_t* o;                         // [QD] fp16 attention output
-    uint16_t* act;                       // [F] fp16 SwiGLU output
+    unsigned* ll_x;                      // [H] 4-byte flag words (fp16): published residual rows, then
+                                         // [nwg rounded up to even] 8-byte flag words (fp32): their sums of squares
+    unsigned long long* ll_qkv;          // [NQKV] flag words (fp32 values): rotated q, rotated k, v
+    unsigned long long* ll_o;            // [QD / 2] flag words (fp16 pairs): attention output
+    unsigned long long* ll_act;          // [F / 2] flag words (fp16 pairs): SwiGLU output
     MetaDev meta;
     const float2* rope;
     float qscale;                        // log2(e) / sqrt(D)
     int nsplit, split_len, att_T;        // splits per kv head (power of two), cache rows per split, slot pairs per wave
-    float* apart;                        // [Hkv][nsplit][Hq/Hkv][D + 4] split partials
-    unsigned* acnt;                      // [Hkv] arrival counters (only ever incremented)
-    unsigned long long* bar;             // 16 barrier counters, 64 words apart
-    unsigned long long bar_epoch;        // barriers completed by earlier launches
-    unsigned* err;                       // set when a barrier wait gives up
+    unsigned long long* ll_part;         // [Hkv][nsplit][Hq/Hkv][D + 2] flag words (fp32): max, sum, D outputs
+    unsigned ll_epoch;                   // flag numbers used by earlier launches (PS_LL_PER_LAYER per layer)
+    int pf;                              // ring slots a compute wave may prefetch into a segment whose input is not staged
+    unsigned* err;                       // set when an exchange wait gives up
     unsigned long long* trace;           // optional [nwg][n_layers][PS_TRACE_PER_LAYER] real-time stamps
     // LDS byte offsets
-    int l_xs, l_gff, l_sb0, l_sb1, l_res, l_q, l_nkv, l_part, l_rope, l_dbg, l_end;
+    int l_xs, l_sb0, l_sb1, l_res, l_q, l_nkv, l_part, l_rope, l_dbg, l_end;
 };
-constexpr int PS_TRACE_PER_LAYER = 16;   // 10 control-wave boundaries + 6 from compute wave 0
+constexpr int PS_LL_PER_LAYER = 6;      // flag-word exchanges per layer: q|k|v, split partials, attention
+                                        // output, residual after o, SwiGLU output, residual after down
+constexpr int PS_TRACE_PER_LAYER = 32;   // 10 control-wave boundaries, 6 from compute wave 0, 6 exchange pass
+                                         // counts, 6 exchange end times, 3 first-pass times, 1 spare
 
 // LDS layout of the stream kernel with `slots` ring slots per compute wave;
 // returns the total bytes.
@@ -149,19 +152,13 @@ inline int ps_layout(PsArgs& a, int slots, int D, int gs) {
     int rows = a.rpw_qkv > 2 * a.rpw_h ? a.rpw_qkv : 2 * a.rpw_h;   // down rows may carry two partials
     rows = rows > a.rpw_gu ? rows : a.rpw_gu;
     int off = SK_CW * slots * SK_SLOT;
-    // staged input; past the K = H / Hq*D part it also holds the ffn RMSNorm weights
-    // from the end of one down phase until the next down input is staged
-    const int kch = a.kc_h > a.kc_q ? a.kc_h : a.kc_q;
-    const int xsz = kch * 64 + up(a.H * 2, SK_SLOT);
-    a.l_xs = off;
-    a.l_gff = off + kch * 64;
-    off += kcmax * 64 > xsz ? kcmax * 64 : xsz;
+    a.l_xs = off;   off += kcmax * 64;                                // staged GEMV input (fp16)
     a.l_sb0 = off;  off += sb;
     a.l_sb1 = off;  off += sb;
     a.l_res = off;  off += up(rows * 4, 16);
     a.l_q = off;    off += gs * D * 4;
     a.l_nkv = off;  off += 2 * D * 4;
-    a.l_part = off; off += up(SK_CW * gs * (D + 4) * 4 > a.H * 2 ? SK_CW * gs * (D + 4) * 4 : a.H * 2, SK_SLOT);   // also RMSNorm weights
+    a.l_part = off; off += up(SK_CW * gs * (D + 4) * 4 > a.H * 2 ? SK_CW * gs * (D + 4) * 4 : a.H * 2, SK_SLOT);   // also the first RMSNorm weights
     a.l_rope = off; off += (D / 2) * 8;
     a.l_dbg = off;  off += 64;                                        // compute-wave trace stamps
     a.l_end = off;

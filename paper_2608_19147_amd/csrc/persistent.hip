@@ -34,8 +34,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 constexpr int SK_THREADS = (SK_CW + 1) * 64;
-constexpr int SK_NC = 16;                    // barrier counters, 512 bytes apart
-constexpr unsigned SK_SPIN_LIMIT = 1u << 20; // a barrier that never completes gives up (error flag)
+constexpr unsigned SK_SPIN_LIMIT = 1u << 20; // an exchange wait that never completes gives up (error flag)
 
 // ------------------------------------------------------------------ LDS by address, explicit waits
 
@@ -82,11 +81,6 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
     __builtin_amdgcn_global_load_lds(g, (lds_ptr_t)(uintptr_t)lds, 16, 0, 2 /* nt: streamed once */);
 }
 
-// The same with device-coherent reads ("sc1"), for data written by other
-// workgroups of this launch.
-__device__ __forceinline__ void dma16_coherent(const void* g, uint32_t lds) {
-    __builtin_amdgcn_global_load_lds(g, (lds_ptr_t)(uintptr_t)lds, 16, 0, 16 /* sc1 */);
-}
 
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
 
@@ -128,23 +122,87 @@ __device__ __forceinline__ float group_sum(float v) {
     return v;
 }
 
-// Grid barrier number `idx` of this launch (control wave only).  Returns false
-// once any workgroup has given up waiting; the error flag stays set.
-__device__ __forceinline__ bool grid_sync(const PsArgs& a, int idx) {
+// ------------------------------------------------------------------ flag-in-data exchange
+//
+// A 32-bit value exchanged between workgroups travels in one 8-byte word with
+// the number of the write that produced it in the high half, written with one
+// device-coherent 8-byte store.  A reader polls the words it needs until each
+// carries the expected number: no acknowledgement, counter or barrier sits
+// between producer and consumer.  A buffer is only rewritten (with a higher
+// number) after every reader of its previous contents has finished with it,
+// which the data dependencies of the forward guarantee (see control_main).
+
+__device__ __forceinline__ void ll_store(u64* p, uint32_t v, uint32_t flag) {
+    __hip_atomic_store(p, ((u64)flag << 32) | (u64)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// A 16-bit value with the low 16 bits of the write number in one 4-byte word.
+// Every buffer is rewritten at each use, so a stale word carries a number at
+// most a few hundred writes old, never equal to the expected one modulo 2^16.
+__device__ __forceinline__ void ll_store16(uint32_t* p, uint16_t v, uint32_t flag) {
+    __hip_atomic_store(p, (uint32_t)v | (flag << 16), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The lane index, recomputed where it is called: offsets derived from it are
+// then not hoisted out of the layer loop (where they would stay live throughout).
+__device__ __forceinline__ int fresh_lane() {
+    int l = threadIdx.x & 63;
+    asm volatile("" : "+v"(l));
+    return l;
+}
+
+// Polls NP 16-byte pieces of the buffer behind r, piece i at byte offset off[i]
+// and wanted when bit i of `use` is set, until every word of every wanted piece
+// carries `flag` (pieces i < N16 hold four 4-byte words, the others two 8-byte
+// words); take(i, piece) receives each piece once, as
+// soon as it is complete.  Every pass issues all its loads at once: a piece
+// already taken gets an offset past the end of the buffer, which the hardware
+// answers with zeros without a memory access.  Returns false when the wait
+// gives up (error flag set) or once any workgroup has given up; with ok false
+// it makes one pass and does not wait.
+// With tracing on, wait number tw (0..5) of layer tl records its passes and end time.
+template <int NP, int N16 = 0, class Take>
+__device__ __forceinline__ bool ll_wait(const PsArgs& a, __amdgpu_buffer_rsrc_t r, const int (&off)[NP], uint32_t use,
+                                        uint32_t flag, Take&& take, bool ok, int tl = -1, int tw = -1) {
+    static_assert(NP <= 32, "one bit per piece");
+    constexpr int OOB = 0x7FFFFFF0;
     const int lane = threadIdx.x & 63;
-    vm_wait_all();                                         // own coherent stores are complete
-    if (lane == 0) atomicAdd(&a.bar[(blockIdx.x % SK_NC) * 64], 1ull);
-    const unsigned n = gridDim.x;
-    const u64 per = (lane < SK_NC) ? (u64)((n - lane + SK_NC - 1) / SK_NC) : 0ull;
-    const u64 target = (a.bar_epoch + (u64)idx + 1ull) * per;
+    uint32_t pend = use;
     unsigned spins = 0;
     while (true) {
-        bool ok = true;
-        if (lane < SK_NC) ok = load_coherent_u64(&a.bar[lane * 64]) >= target;
-        if (lane == SK_NC) ok = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u;
-        if (__all(ok)) return true;
-        if (!__all(lane != SK_NC || ok)) return false;     // another workgroup already gave up
-        __builtin_amdgcn_s_sleep(1);
+        u32x4 v[NP];
+#pragma unroll
+        for (int i = 0; i < NP; ++i)
+            v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, ((pend >> i) & 1u) ? off[i] : OOB, 0, 16));
+        uint32_t bad = 0u;
+        if (lane == 0) bad = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int i = 0; i < NP; ++i) {
+            bool rd;
+            if (i < N16) {
+                const uint32_t w0 = v[i][0], w1 = v[i][1], w2 = v[i][2], w3 = v[i][3];
+                const uint32_t f16 = flag & 0xFFFFu;
+                rd = (w0 >> 16) == f16 && (w1 >> 16) == f16 && (w2 >> 16) == f16 && (w3 >> 16) == f16;
+            } else {
+                const uint32_t f0 = v[i][1], f1 = v[i][3];
+                rd = f0 == flag && f1 == flag;
+            }
+            if (((pend >> i) & 1u) && rd) {
+                take(i, v[i]);
+                pend &= ~(1u << i);
+            }
+        }
+        if (a.trace && tw >= 0 && lane == 0 && spins == 0)
+            a.trace[((size_t)blockIdx.x * a.n_layers + tl) * PS_TRACE_PER_LAYER + 28 + (tw == 3 ? 0 : tw == 5 ? 1 : 2)] = wall_clock64();
+        if (__all(pend == 0u)) {
+            if (a.trace && tw >= 0 && lane == 0) {
+                u64* tr = a.trace + ((size_t)blockIdx.x * a.n_layers + tl) * PS_TRACE_PER_LAYER;
+                tr[16 + tw] = spins + 1;
+                tr[22 + tw] = wall_clock64();
+            }
+            return ok;
+        }
+        if (!ok) return false;
+        if (__any(bad != 0u)) return false;                // another workgroup already gave up
         if (++spins > SK_SPIN_LIMIT) {
             if (lane == 0) atomicOr(a.err, 1u);
             return false;
@@ -599,7 +657,7 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
     // (kc = 64 * CPL chunks per row), so a segment streams one block of 1 KB slots.
     typedef __attribute__((address_space(4))) const PsLayer* layer_cptr;   // never written during the launch:
     const layer_cptr layers = (layer_cptr)a.layers;                          // scalar loads
-    int gl = 0, gs = -1, gleft = 0, gt = 0;
+    int gl = 0, gs = -1, gleft = 0, gt = 0, gpos = 0;      // gpos: stream position of the next real load
     const uint8_t* gptr = nullptr;
     auto next_seg = [&]() {
         do {
@@ -620,8 +678,9 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         else if (gs == 4)
             gptr = layers[gl].d.w + (XR_F ? (u64)ro_.first * a.kc_f * 16 : (u64)w * a.rpw_h * a.kc_f * 16 + (u64)ks0 * SK_SLOT);
     };
-    auto issue = [&](uint32_t dst) {
+    auto issue_real = [&](uint32_t dst) {
         if (gleft == 0) return;
+        ++gpos;
         if (gs == 1) {
             const int t = gt >> 1;
             uint32_t off = aoff[0];
@@ -639,30 +698,72 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         }
         if (--gleft == 0) next_seg();
     };
+    // Prefetch into a segment whose input is not staged yet is capped at a.pf
+    // slots: the exchange loads that stage the input queue behind every load
+    // this CU issued before them.  A refill past the cap is issued as an
+    // out-of-range buffer load (answered without a memory access, its zeros
+    // land in the consumed slot) so the ring's fixed wait counts stay exact;
+    // the real loads follow, in stream order, once the input is staged.
+    // The attention slots are not capped: their input (this head group's
+    // queries) is staged from data that is usually complete by then.
+    const int NL = n0 + n1 + n2 + n3 + n4;
+    auto seg_start = [&](int j) {
+        const int k = j % 5;
+        return (j / 5) * NL + (k > 0 ? n0 : 0) + (k > 1 ? n1 : 0) + (k > 2 ? n2 : 0) + (k > 3 ? n3 : 0);
+    };
+    auto limit_of = [&](int j) {                            // j: first segment whose input is not staged
+        if (j % 5 == 1) ++j;
+        return j >= 5 * L ? total : min(total, seg_start(j) + a.pf);
+    };
+    const __amdgpu_buffer_rsrc_t none = make_rsrc(a.err, 0);
+    const uint32_t ring = lb + (uint32_t)(cw * S * SK_SLOT);
+    int rel = 1, lim = limit_of(1), ndef = 0;               // q|k|v of layer 0 is not capped
+    auto issue = [&](uint32_t dst) {
+        if (ndef > 0 || gpos >= lim) {
+            if (gpos + ndef >= total) return;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(none, (lds_ptr_t)(uintptr_t)dst, 16, 0x7FFFFFF0, 0, 0, 0);
+            ++ndef;
+            return;
+        }
+        issue_real(dst);
+    };
+    auto release = [&]() {                                  // the input of segment `rel` is staged
+        lim = limit_of(++rel);
+        while (ndef > 0 && gpos < lim) {
+            --ndef;
+            issue_real(ring + (uint32_t)(gpos % S) * SK_SLOT);
+        }
+    };
     next_seg();
     vm_wait_all();                                          // table and mask reads are done
-    const uint32_t ring = lb + (uint32_t)(cw * S * SK_SLOT);
     for (int k = 0; k < S; ++k) issue(ring + (uint32_t)k * SK_SLOT);
 
     Ring rg{ring, 0, 0, total - S};
     for (int l = 0; l < L; ++l) {
         wg_barrier();                                       // input of q|k|v is staged
+        if (l > 0) release();
         gemv_seg<CPL_H, S>(a, issue, rg, rq_.count, rq_.local, a.ng_h, lb + a.l_sb0, lb + a.l_xs, lb + a.l_res);
         wg_barrier();                                       // q|k|v rows are in LDS
         wg_barrier();                                       // q and the new row are staged
+        release();
         cstamp(a, lb + a.l_dbg, 0);
         att_seg<GS, D, S>(a, issue, rg, T, mbits, lb + a.l_q, lb + a.l_part);
         cstamp(a, lb + a.l_dbg, 1);
         wg_barrier();                                       // wave partials are in LDS
         wg_barrier();                                       // attention output is staged
+        release();
         gemv_seg<CPL_Q, S>(a, issue, rg, ro_.count, ro_.local, a.ng_q, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
         wg_barrier();
         wg_barrier();                                       // RMSNorm(x) is staged
+        release();
         cstamp(a, lb + a.l_dbg, 2);
         gemv_seg<CPL_H, S>(a, issue, rg, rg_.count, rg_.local, a.ng_h, lb + a.l_sb0, lb + a.l_xs, lb + a.l_res);
         cstamp(a, lb + a.l_dbg, 3);
-        wg_barrier();
+        wg_barrier();                                       // gate|up rows are in LDS: the input is free
+        // this wave's share of the SwiGLU output (ring loads already in flight complete first)
+        stage_act<CPL_F>(a, cw, a.ll_epoch + PS_LL_PER_LAYER * l + 5, lb + a.l_xs, true);
         wg_barrier();                                       // SwiGLU output is staged
+        release();
         cstamp(a, lb + a.l_dbg, 4);
         if constexpr (XR_F)
             gemv_seg<CPL_F, S>(a, issue, rg, ro_.count, ro_.local, a.ng_f, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
@@ -684,39 +785,30 @@ __device__ __forceinline__ void load_scales(const uint16_t* s, int first, int co
     for (int off = 0; off < bytes; off += SK_SLOT) dma16(src + off + 16 * lane, dst + off);
 }
 
-// Input of an RMSNorm'd GEMV: K values (fp32 coherent, or act dtype written
-// before the launch when src_dt != DT_F32) -> x * rsqrt(mean(x^2) + eps) * gamma
-// as fp16 in LDS xs; padding up to kpad is zeroed.
-// RMSNorm weights (K values, 2 bytes each) into LDS with direct loads, issued a
-// phase ahead so their latency is hidden; the buffer must hold whole 1 KB blocks.
+// RMSNorm weights (K values, 2 bytes each) into LDS with direct loads; the
+// buffer must hold whole 1 KB blocks.
 __device__ __forceinline__ void load_gamma(const uint16_t* gamma, int K, uint32_t dst) {
     const int lane = threadIdx.x & 63;
     for (int off = 0; off < K * 2; off += SK_SLOT) dma16((const uint8_t*)gamma + off + 16 * lane, dst + off);
 }
 
+// Input of the first q|k|v GEMV: the stage input h (K values of dtype src_dt,
+// written before the launch) -> h * rsqrt(mean(h^2) + eps) * gamma as fp16 in
+// LDS xs, padding up to kpad zeroed; returns the RMSNorm scale.
 template <int NT>
-__device__ __forceinline__ void stage_norm(const void* src, int src_dt, int K, int kpad, const uint8_t* gl,
-                                           int gamma_dt, float eps, uint8_t* xs) {
+__device__ __forceinline__ float stage_norm(const void* src, int src_dt, int K, int kpad, const uint8_t* gl,
+                                            int gamma_dt, float eps, uint8_t* xs) {
     const int lane = threadIdx.x & 63;
     const int n4 = K / 4;
     f32x4 v[NT];
-    if (src_dt == DT_F32) {
-        const __amdgpu_buffer_rsrc_t r = make_rsrc(src, (size_t)K * 4);
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const int it = lane + 64 * t;
-            v[t] = load4_coherent(r, it < n4 ? it * 16 : 0);
-        }
-    } else {
+    for (int t = 0; t < NT; ++t) {
+        const int it = lane + 64 * t;
+        const u32x2 h = *(const u32x2*)((const uint16_t*)src + 4 * (it < n4 ? it : 0));
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const int it = lane + 64 * t;
-            const u32x2 h = *(const u32x2*)((const uint16_t*)src + 4 * (it < n4 ? it : 0));
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t wd = h[e >> 1];
-                v[t][e] = half_bits_to_f32((uint16_t)((e & 1) ? (wd >> 16) : (wd & 0xFFFFu)), src_dt);
-            }
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t wd = h[e >> 1];
+            v[t][e] = half_bits_to_f32((uint16_t)((e & 1) ? (wd >> 16) : (wd & 0xFFFFu)), src_dt);
         }
     }
     float ss = 0.f;
@@ -739,18 +831,105 @@ __device__ __forceinline__ void stage_norm(const void* src, int src_dt, int K, i
         }
     }
     for (int it = n4 + lane; it < kpad / 4; it += 64) *(u32x2*)(xs + 8 * it) = u32x2{0u, 0u};
+    return rs;
 }
 
-// Input of a plain GEMV: K fp16 values written coherently by this launch -> LDS xs,
-// with direct loads (whole 1 KB blocks: the source buffers are padded); the caller
-// waits for them (vm_wait_all) and then zeroes the padding past K with zero_pad.
-__device__ __forceinline__ void stage_plain(const uint16_t* src, int K, uint32_t xs) {
-    const int lane = threadIdx.x & 63;
-    for (int off = 0; off < K * 2; off += SK_SLOT) dma16_coherent((const uint8_t*)src + off + 16 * lane, xs + off);
-}
 __device__ __forceinline__ void zero_pad(int K, int kpad, uint8_t* xs) {
     const int lane = threadIdx.x & 63;
     for (int it = K / 8 + lane; it < kpad / 8; it += 64) *(f32x4*)(xs + 16 * it) = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+__device__ __forceinline__ void lds_wr8(uint32_t a, u32x2 v) {
+    asm volatile("ds_write_b64 %0, %1" ::"v"(a), "v"(v) : "memory");
+}
+
+// ---- the residual stream between workgroups
+//
+// RMSNorm(x) W^T = rs * ((x * gamma) W^T) with the scalar rs = rsqrt(mean(x^2) + eps):
+// each row owner publishes u = fp16(x * gamma * c) for its rows together with
+// the rows' sum of squares, and a consumer applies rs / c to the GEMV results.
+// c is the previous normalization's rs, identical in every workgroup, which
+// keeps u in the range the normalized input would have.  The exchange buffer
+// holds H 4-byte words (u) followed by one 8-byte word per workgroup (its sum
+// of squares; the count is rounded up to even).
+
+__device__ __forceinline__ int ss_words(int nwg) { return (nwg + 1) & ~1; }
+
+__device__ __forceinline__ void publish_x(const PsArgs& a, int xr0, int nxr, float xrow, float gamma, float c,
+                                          uint32_t flag) {
+    const int lane = threadIdx.x & 63;
+    if (lane < nxr) ll_store16(a.ll_x + xr0 + lane, f32_to_f16(xrow * gamma * c), flag);
+    const float ss = wave_sum(lane < nxr ? xrow * xrow : 0.f);
+    u64* sw = (u64*)(a.ll_x + a.H);
+    if (lane == 0) ll_store(sw + blockIdx.x, __float_as_uint(ss), flag);
+    if (lane == 1 && (gridDim.x & 1) && blockIdx.x == gridDim.x - 1) ll_store(sw + gridDim.x, 0u, flag);
+}
+
+// Polls the published u into LDS xs (fp16, padding up to kpad zeroed) and
+// returns rs from the workgroups' sums of squares (added in a fixed order).
+template <int CPL_H>
+__device__ __forceinline__ float stage_x(const PsArgs& a, uint32_t flag, uint8_t* xs, int kpad, bool& ok, int tl, int tw) {
+    constexpr int NXP = CPL_H * 8;         // pieces (four u) per lane: H <= 2048 CPL_H
+    constexpr int NSP = 2;                 // pieces (two sums) per lane: up to 256 workgroups
+    const int lane = fresh_lane();
+    const int nss = ss_words(gridDim.x);
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_x, (size_t)a.H * 4 + (size_t)nss * 8);
+    int off[NXP + NSP];
+    uint32_t use = 0u;
+#pragma unroll
+    for (int t = 0; t < NXP; ++t) {
+        const int it = lane + 64 * t;
+        const bool u = it < a.H / 4;
+        off[t] = u ? 16 * it : 0;
+        use |= (u ? 1u : 0u) << t;
+    }
+#pragma unroll
+    for (int t = 0; t < NSP; ++t) {
+        const int it = lane + 64 * t;
+        const bool u = it < nss / 2;
+        off[NXP + t] = u ? 4 * a.H + 16 * it : 0;
+        use |= (u ? 1u : 0u) << (NXP + t);
+    }
+    float ssv[2 * NSP];
+#pragma unroll
+    for (int j = 0; j < 2 * NSP; ++j) ssv[j] = 0.f;
+    ok = ll_wait<NXP + NSP, NXP>(a, r, off, use, flag, [&](int i, const u32x4& pc) {
+        const uint32_t w0 = pc[0], w1 = pc[1], w2 = pc[2], w3 = pc[3];
+        if (i < NXP) {
+            *(u32x2*)(xs + 8 * (lane + 64 * i)) = u32x2{(w0 & 0xFFFFu) | (w1 << 16), (w2 & 0xFFFFu) | (w3 << 16)};
+        } else {
+            ssv[2 * (i - NXP)] = __uint_as_float(w0);
+            ssv[2 * (i - NXP) + 1] = __uint_as_float(w2);
+        }
+    }, ok, tl, tw);
+    zero_pad(a.H, kpad, xs);
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < 2 * NSP; ++j) ss += ssv[j];
+    return rsqrtf(wave_sum(ss) / (float)a.H + a.eps);
+}
+
+// This wave's share (wave wv of the eight) of the SwiGLU output, from its flag
+// words into LDS xs (fp16).  All waves of the workgroup take part.
+template <int CPL_F>
+__device__ __forceinline__ bool stage_act(const PsArgs& a, int wv, uint32_t flag, uint32_t xs, bool ok, int tl = -1,
+                                          int tw = -1) {
+    constexpr int NTW = CPL_F;             // pieces (four outputs) per lane and wave: F <= 2048 CPL_F
+    const int lane = fresh_lane();
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_act, (size_t)a.F / 2 * 8);
+    int off[NTW];
+    uint32_t use = 0u;
+#pragma unroll
+    for (int t = 0; t < NTW; ++t) {
+        const int it = lane + 64 * (wv + 8 * t);
+        const bool u = it < a.F / 4;
+        off[t] = u ? 16 * it : 0;
+        use |= (u ? 1u : 0u) << t;
+    }
+    return ll_wait<NTW>(a, r, off, use, flag, [&](int i, const u32x4& pc) {
+        const uint32_t p0 = pc[0], p1 = pc[2];
+        lds_wr8(xs + 8 * (lane + 64 * (wv + 8 * i)), u32x2{p0, p1});
+    }, ok, tl, tw);
 }
 
 template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
@@ -782,7 +961,7 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     const size_t lstride = (size_t)rq.S * a.Hkv * rq.cap * D;
     const int hq = lane / LPH, d0 = (lane % LPH) * OPL;     // merge lane layout
 
-    // own rows of the residual stream (o and down rows of this workgroup)
+    // own rows of the residual stream (o and down rows of this workgroup), one per lane
     const int xr0 = w * a.rpw_h;
     const int nxr = max(0, min(a.H, xr0 + a.rpw_h) - xr0);
     float xrow = 0.f;
@@ -790,85 +969,106 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     if (lane < D / 2) ((float2*)rope)[lane] = a.rope[(size_t)pos * (D / 2) + lane];
     load_scales(a.layers[0].qkv.s, w * a.rpw_qkv, max(0, min(a.NQKV, (w + 1) * a.rpw_qkv) - w * a.rpw_qkv), a.ng_h,
                 lb + a.l_sb0);
-    // RMSNorm weights of the next normalization live in the attention-partials
-    // region while it is free (after the split merge until the next attention)
-    const uint8_t* gam = smem + a.l_part;
+    // the first normalization reads the stage input directly (RMSNorm weights staged
+    // in the attention-partials region, free until the first attention)
     load_gamma(a.layers[0].attn_norm, a.H, lb + a.l_part);
     vm_wait_all();
-    stage_norm<NT_H>(a.hidden_in, a.act_dt, a.H, a.kc_h * 32, gam, a.act_dt, a.eps, xs);
+    // c: scale of the last published residual (the last RMSNorm scale); mq, mg: the
+    // factors rs / c applied to the q|k|v and gate|up results
+    float c = stage_norm<NT_H>(a.hidden_in, a.act_dt, a.H, a.kc_h * 32, smem + a.l_part, a.act_dt, a.eps, xs);
+    float mq = 1.f, mg = 1.f;
     bool ok = true;
-    int bar = 0;
     vm_wait_all();
     wg_barrier();                                             // q|k|v input staged
 
     for (int l = 0; l < a.n_layers; ++l) {
         const PsLayer& Ly = a.layers[l];
         const bool last = (l == a.n_layers - 1);
+        // flag numbers of this layer's exchanges
+        const uint32_t f_qkv = a.ll_epoch + PS_LL_PER_LAYER * l + 1, f_part = f_qkv + 1, f_o = f_qkv + 2,
+                       f_xo = f_qkv + 3, f_act = f_qkv + 4, f_xd = f_qkv + 5;
         stamp(a, l, 0);
         load_scales(Ly.o.s, xr0, nxr, a.ng_q, lb + a.l_sb1);
-        load_gamma(Ly.ffn_norm, a.H, lb + a.l_gff);            // free since the last down phase
+        // RMSNorm weights of the own rows, for the residuals published after o and after down
+        float gam_f = 0.f, gam_a = 0.f;
+        if (lane < nxr) {
+            gam_f = half_bits_to_f32(Ly.ffn_norm[xr0 + lane], a.act_dt);
+            if (!last) gam_a = half_bits_to_f32(a.layers[l + 1].attn_norm[xr0 + lane], a.act_dt);
+        }
         wg_barrier();                                         // q|k|v rows are in LDS
         stamp(a, l, 1);
-        // ---- rotary embedding of q and k (rows 2d, 2d + 1 of a head are d, d + D/2), coherent stores
+        // ---- RMSNorm scale and rotary embedding of q and k (rows 2d, 2d + 1 of a head are d, d + D/2), as flag words
         {
             const int r0 = w * a.rpw_qkv;
             const int n = max(0, min(a.NQKV, r0 + a.rpw_qkv) - r0);
             for (int k = lane; k < n / 2; k += 64) {
                 const int pr = r0 + 2 * k;
                 const int hb = pr / D, d = (pr % D) / 2;
-                float lo = res[2 * k], hi = res[2 * k + 1];
+                float lo = res[2 * k] * mq, hi = res[2 * k + 1] * mq;
                 if (hb < a.Hq + a.Hkv) {
                     const float2 cs = rope[d];
                     const float l2 = lo * cs.x - hi * cs.y;
                     hi = hi * cs.x + lo * cs.y;
                     lo = l2;
                 }
-                store_coherent(&a.qkv[hb * D + d], lo);
-                store_coherent(&a.qkv[hb * D + d + D / 2], hi);
+                ll_store(&a.ll_qkv[hb * D + d], __float_as_uint(lo), f_qkv);
+                ll_store(&a.ll_qkv[hb * D + d + D / 2], __float_as_uint(hi), f_qkv);
             }
         }
-        if (ok) ok = grid_sync(a, bar);
-        ++bar;
         stamp(a, l, 2);
         // ---- stage this split's query heads and, for the last split, this forward's cache row
         if (has_att) {
-            const __amdgpu_buffer_rsrc_t r = make_rsrc(a.qkv, (size_t)a.NQKV * 4);
-            constexpr int NQ4 = GS * D / 4 / 64 > 0 ? GS * D / 4 / 64 : 1;
-            f32x4 qv[NQ4];
+            constexpr int NQP = GS * D / 128 > 0 ? GS * D / 128 : 1;   // 16-byte pieces (two values) of q per lane
+            constexpr int NKP = D / 128 > 0 ? D / 128 : 1;             // pieces of the new k (and of v) per lane
+            constexpr int NP = NQP + 2 * NKP;
+            const int lane = fresh_lane();
+            const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_qkv, (size_t)a.NQKV * 8);
+            int off[NP];
+            uint32_t use = 0u;
 #pragma unroll
-            for (int t = 0; t < NQ4; ++t) {
+            for (int t = 0; t < NQP; ++t) {
                 const int it = lane + 64 * t;
-                qv[t] = load4_coherent(r, it < GS * D / 4 ? (g * GS * D + 4 * it) * 4 : 0);
-            }
-            float kn[D / 64 > 0 ? D / 64 : 1], vn[D / 64 > 0 ? D / 64 : 1];
-            if (owns_new) {
-#pragma unroll
-                for (int e = 0; e < D / 64; ++e) {
-                    kn[e] = load_coherent(&a.qkv[a.QD + g * D + lane + 64 * e]);
-                    vn[e] = load_coherent(&a.qkv[a.QD + KVD + g * D + lane + 64 * e]);
-                }
+                const bool u = it < GS * D / 2;
+                off[t] = u ? (g * GS * D + 2 * it) * 8 : 0;
+                use |= (u ? 1u : 0u) << t;
             }
 #pragma unroll
-            for (int t = 0; t < NQ4; ++t) {
+            for (int t = 0; t < NKP; ++t) {
                 const int it = lane + 64 * t;
-                if (it < GS * D / 4) *(f32x4*)(qs + 4 * it) = qv[t] * a.qscale;
+                const bool u = owns_new && it < D / 2;
+                off[NQP + t] = u ? (a.QD + g * D + 2 * it) * 8 : 0;
+                off[NQP + NKP + t] = u ? (a.QD + KVD + g * D + 2 * it) * 8 : 0;
+                use |= (u ? 1u : 0u) << (NQP + t);
+                use |= (u ? 1u : 0u) << (NQP + NKP + t);
             }
+            u32x4 kv[2 * NKP];                                 // new k, v pieces
+            ok = ll_wait<NP>(a, r, off, use, f_qkv, [&](int i, const u32x4& pc) {
+                const uint32_t p0 = pc[0], p1 = pc[2];
+                if (i < NQP)
+                    *(float2*)(qs + 2 * (lane + 64 * i)) = float2{__uint_as_float(p0) * a.qscale, __uint_as_float(p1) * a.qscale};
+                else
+                    kv[i - NQP] = pc;
+            }, ok, l, 0);
             if (owns_new) {
                 uint16_t* kl = rq.kc + (size_t)l * lstride + (((size_t)b * a.Hkv + g) * rq.cap + P) * D;
                 uint16_t* vl = rq.vc + (size_t)l * lstride + (((size_t)b * a.Hkv + g) * rq.cap + P) * D;
 #pragma unroll
-                for (int e = 0; e < D / 64; ++e) {
-                    const int d = lane + 64 * e;
-                    const uint16_t kb = to_half_bits(kn[e], a.kv_dt), vb = to_half_bits(vn[e], a.kv_dt);
-                    kl[d] = kb;
-                    vl[d] = vb;
-                    nkv[d] = half_bits_to_f32(kb, a.kv_dt);
-                    nkv[D + d] = half_bits_to_f32(vb, a.kv_dt);
+                for (int t = 0; t < NKP; ++t) {
+                    const int it = lane + 64 * t;
+                    if (it < D / 2) {
+                        const uint32_t k0 = kv[t][0], k1 = kv[t][2];
+                        const uint32_t v0 = kv[NKP + t][0], v1 = kv[NKP + t][2];
+                        const uint16_t kb0 = to_half_bits(__uint_as_float(k0), a.kv_dt), kb1 = to_half_bits(__uint_as_float(k1), a.kv_dt);
+                        const uint16_t vb0 = to_half_bits(__uint_as_float(v0), a.kv_dt), vb1 = to_half_bits(__uint_as_float(v1), a.kv_dt);
+                        *(uint32_t*)(kl + 2 * it) = (uint32_t)kb0 | ((uint32_t)kb1 << 16);
+                        *(uint32_t*)(vl + 2 * it) = (uint32_t)vb0 | ((uint32_t)vb1 << 16);
+                        *(float2*)(nkv + 2 * it) = float2{half_bits_to_f32(kb0, a.kv_dt), half_bits_to_f32(kb1, a.kv_dt)};
+                        *(float2*)(nkv + D + 2 * it) = float2{half_bits_to_f32(vb0, a.kv_dt), half_bits_to_f32(vb1, a.kv_dt)};
+                    }
                 }
                 if (l == 0 && g == 0 && lane == 0) rq.table[(size_t)b * rq.cap + P] = (int16_t)b;
             }
         }
-        vm_wait_all();
         wg_barrier();                                         // q and the new row are staged
         // gate|up scales (q|k|v finished with this buffer) load while the compute waves run the attention
         load_scales(Ly.gu.s, w * a.rpw_gu, max(0, min(2 * a.F, (w + 1) * a.rpw_gu) - w * a.rpw_gu), a.ng_h, lb + a.l_sb0);
@@ -910,44 +1110,42 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
 #pragma unroll
                 for (int e = 0; e < OPL; ++e) O[e] += wc * pc[4 + d0 + e];
             }
-            float* pp = a.apart + (((size_t)g * a.nsplit + split) * GS + hq) * (D + 4);
+            u64* pp = a.ll_part + (((size_t)g * a.nsplit + split) * GS + hq) * (D + 2);
 #pragma unroll
-            for (int e = 0; e < OPL; ++e) store_coherent(pp + 4 + d0 + e, O[e]);
+            for (int e = 0; e < OPL; ++e) ll_store(pp + 2 + d0 + e, __float_as_uint(O[e]), f_part);
             if (d0 == 0) {
-                store_coherent(pp, mx);
-                store_coherent(pp + 1, L);
+                ll_store(pp, __float_as_uint(mx), f_part);
+                ll_store(pp + 1, __float_as_uint(L), f_part);
             }
-            vm_wait_all();
-            // every split of this kv head waits for all of them, then merges its own
-            // 1/nsplit slice of the head group's outputs (one round of loads)
-            unsigned prev = 0;
-            if (lane == 0) prev = atomicAdd(&a.acnt[g], 1u);
-            prev = __builtin_amdgcn_readfirstlane(prev);
-            const unsigned target = (prev & ~(unsigned)(a.nsplit - 1)) + (unsigned)a.nsplit;
-            if (ok) {
-                unsigned spins = 0;
-                while ((int)(__hip_atomic_load(&a.acnt[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
-                    __builtin_amdgcn_s_sleep(1);
-                    if (++spins > SK_SPIN_LIMIT) {
-                        if (lane == 0) atomicOr(a.err, 1u);
-                        ok = false;
-                        break;
-                    }
-                }
-            }
+            // every split of this kv head reads the partials of all of them for its own
+            // 1/nsplit slice of the head group's outputs and merges that slice
             const int SL = GS * D / a.nsplit;                 // outputs per slice (multiple of 8)
             const int CH = SL / 8;                            // 8-output chunks per slice
-            const int s2 = lane / CH, c = lane % CH;          // lane: one split's chunk of the slice
+            const int ml = fresh_lane();
+            const int s2 = ml / CH, c = ml % CH;              // lane: one split's chunk of the slice
             const bool act = s2 < a.nsplit;
             const int o0 = split * SL + 8 * c;                // first output of the chunk within the head group
             const int hh = o0 / D, dd = o0 % D;
-            const __amdgpu_buffer_rsrc_t r = make_rsrc(a.apart, (size_t)a.Hkv * a.nsplit * GS * (D + 4) * 4);
-            const int base = act ? (int)((((size_t)g * a.nsplit + s2) * GS + hh) * (D + 4)) * 4 : 0;
-            const f32x4 st4 = load4_coherent(r, base);
-            const f32x4 oa = load4_coherent(r, base + 16 + 4 * dd);
-            const f32x4 ob = load4_coherent(r, base + 32 + 4 * dd);
-            float ms = act ? st4[0] : -INFINITY, ls = act ? st4[1] : 0.f;
-            float ov[8] = {oa[0], oa[1], oa[2], oa[3], ob[0], ob[1], ob[2], ob[3]};
+            const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_part, (size_t)a.Hkv * a.nsplit * GS * (D + 2) * 8);
+            const int base = act ? (int)((((size_t)g * a.nsplit + s2) * GS + hh) * (D + 2)) * 8 : 0;
+            const int off[5] = {base, base + 8 * (2 + dd), base + 8 * (2 + dd) + 16, base + 8 * (2 + dd) + 32,
+                                base + 8 * (2 + dd) + 48};
+            u32x4 pv[5];
+            ok = ll_wait<5>(a, r, off, act ? 0x1Fu : 0u, f_part, [&](int i, const u32x4& pc) { pv[i] = pc; }, ok, l, 1);
+            float ms = -INFINITY, ls = 0.f, ov[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) ov[e] = 0.f;
+            if (act) {
+                const uint32_t m0 = pv[0][0], l0 = pv[0][2];
+                ms = __uint_as_float(m0);
+                ls = __uint_as_float(l0);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t x0 = pv[1 + j][0], x1 = pv[1 + j][2];
+                    ov[2 * j] = __uint_as_float(x0);
+                    ov[2 * j + 1] = __uint_as_float(x1);
+                }
+            }
             // combine the splits: lanes c, c + CH, c + 2 CH, ... (fixed butterfly order)
             float Mx = ms;
             for (int sh = CH; sh < 64; sh <<= 1) Mx = fmaxf(Mx, __shfl_xor(Mx, sh));
@@ -962,35 +1160,50 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
             }
             if (act && s2 == 0) {
                 const float inv = 1.0f / Ls;
-                uint32_t* dst = (uint32_t*)(a.o + (size_t)(g * GS + hh) * D + dd);
+                u64* dst = a.ll_o + ((size_t)(g * GS + hh) * D + dd) / 2;
 #pragma unroll
-                for (int e = 0; e < 8; e += 2) store_coherent_u32(dst + e / 2, pack_f16x2(ov[e] * inv, ov[e + 1] * inv));
+                for (int e = 0; e < 8; e += 2) ll_store(dst + e / 2, pack_f16x2(ov[e] * inv, ov[e + 1] * inv), f_o);
             }
         }
-        if (ok) ok = grid_sync(a, bar);
-        ++bar;
         stamp(a, l, 4);
-        stage_plain(a.o, a.QD, lb + a.l_xs);
-        vm_wait_all();
-        zero_pad(a.QD, a.kc_q * 32, xs);
+        // ---- the attention output (every head) as this workgroup's o input
+        {
+            constexpr int NOP = CPL_Q * 8;                    // 16-byte pieces (4 outputs) per lane; K = Hq*D <= 2048 CPL_Q
+            static_assert(NOP <= 32, "one bit per piece");
+            const int lane = fresh_lane();
+            const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_o, (size_t)a.QD / 2 * 8);
+            int off[NOP];
+            uint32_t use = 0u;
+#pragma unroll
+            for (int t = 0; t < NOP; ++t) {
+                const int it = lane + 64 * t;
+                const bool u = it < a.QD / 4;
+                off[t] = u ? 16 * it : 0;
+                use |= (u ? 1u : 0u) << t;
+            }
+            ok = ll_wait<NOP>(a, r, off, use, f_o, [&](int i, const u32x4& pc) {
+                const uint32_t p0 = pc[0], p1 = pc[2];
+                *(u32x2*)(xs + 8 * (lane + 64 * i)) = u32x2{p0, p1};
+            }, ok, l, 2);
+            zero_pad(a.QD, a.kc_q * 32, xs);
+        }
         wg_barrier();                                         // attention output staged
         wg_barrier();                                         // o rows are in LDS
         stamp(a, l, 5);
-        // ---- x += o Wo^T (own rows)
-        if (lane < nxr) {
-            xrow += res[lane];
-            store_coherent(&a.x[xr0 + lane], xrow);
-        }
-        if (ok) ok = grid_sync(a, bar);
-        ++bar;
+        // ---- x += o Wo^T (own rows), published for the ffn RMSNorm
+        if (lane < nxr) xrow += res[lane];
+        publish_x(a, xr0, nxr, xrow, gam_f, c, f_xo);
         stamp(a, l, 6);
-        stage_norm<NT_H>(a.x, DT_F32, a.H, a.kc_h * 32, smem + a.l_gff, a.act_dt, a.eps, xs);
-        vm_wait_all();
+        {
+            const float rs = stage_x<CPL_H>(a, f_xo, xs, a.kc_h * 32, ok, l, 3);
+            mg = rs / c;
+            c = rs;
+        }
         wg_barrier();                                         // RMSNorm(x) staged
         load_scales(Ly.d.s, xr0, nxr, a.ng_f, lb + a.l_sb1);   // o finished with this buffer
         wg_barrier();                                         // gate|up rows are in LDS
         stamp(a, l, 7);
-        // ---- act = silu(gate) * up, two values per lane as one coherent dword
+        // ---- act = silu(gate) * up, two outputs per flag word
         {
             const int r0 = w * a.rpw_gu;
             const int n = max(0, min(2 * a.F, r0 + a.rpw_gu) - r0);
@@ -998,24 +1211,20 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
                 float y[2];
 #pragma unroll
                 for (int e = 0; e < 2; ++e) {
-                    const float gt = res[4 * k + 2 * e], up = res[4 * k + 2 * e + 1];
+                    const float gt = res[4 * k + 2 * e] * mg, up = res[4 * k + 2 * e + 1] * mg;
                     y[e] = (gt / (1.0f + expf(-gt))) * up;
                 }
-                store_coherent_u32((uint32_t*)(a.act + r0 / 2 + 2 * k), pack_f16x2(y[0], y[1]));
+                ll_store(a.ll_act + r0 / 4 + k, pack_f16x2(y[0], y[1]), f_act);
             }
         }
-        if (ok) ok = grid_sync(a, bar);
-        ++bar;
         stamp(a, l, 8);
-        stage_plain(a.act, a.F, lb + a.l_xs);
-        vm_wait_all();
+        ok = stage_act<CPL_F>(a, SK_CW, f_act, lb + a.l_xs, ok, l, 4);
         zero_pad(a.F, a.kc_f * 32, xs);
         wg_barrier();                                         // SwiGLU output staged
         if (!last) {
             const PsLayer& Ln = a.layers[l + 1];
             load_scales(Ln.qkv.s, w * a.rpw_qkv, max(0, min(a.NQKV, (w + 1) * a.rpw_qkv) - w * a.rpw_qkv), a.ng_h,
                         lb + a.l_sb0);
-            load_gamma(Ln.attn_norm, a.H, lb + a.l_part);
         }
         wg_barrier();                                         // down rows are in LDS
         stamp(a, l, 9);
@@ -1030,16 +1239,13 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
                 const bool two = (lane * CPL_F) / kspw != (lane * CPL_F + CPL_F - 1) / kspw;
                 xrow += two ? res[2 * lane] + res[2 * lane + 1] : res[2 * lane];
             }
-            if (last)
-                ((uint16_t*)a.hidden_out)[xr0 + lane] = to_half_bits(xrow, a.act_dt);
-            else
-                store_coherent(&a.x[xr0 + lane], xrow);
+            if (last) ((uint16_t*)a.hidden_out)[xr0 + lane] = to_half_bits(xrow, a.act_dt);
         }
         if (!last) {
-            if (ok) ok = grid_sync(a, bar);
-            ++bar;
-            stage_norm<NT_H>(a.x, DT_F32, a.H, a.kc_h * 32, gam, a.act_dt, a.eps, xs);
-            vm_wait_all();
+            publish_x(a, xr0, nxr, xrow, gam_a, c, f_xd);
+            const float rs = stage_x<CPL_H>(a, f_xd, xs, a.kc_h * 32, ok, l, 5);
+            mq = rs / c;
+            c = rs;
             wg_barrier();                                     // next layer's q|k|v input staged
         }
     }

@@ -67,13 +67,14 @@ struct Stage {
     int cpl_h = 0, cpl_q = 0, cpl_f = 0, kc_h = 0, kc_q = 0, kc_f = 0, ng_h = 0, ng_q = 0, ng_f = 0;
     std::vector<PsLayer> ps_host;
     PsLayer* ps_layers = nullptr;
-    unsigned long long* bar = nullptr;
     unsigned* err = nullptr;
-    unsigned long long bar_epoch = 0;
     int ps_nwg = 0;
     int ps_rpw_qkv = 0, ps_rpw_h = 0, ps_rpw_gu = 0;    // rows per workgroup of the single-launch forward
-    unsigned* acnt_ps = nullptr;                        // its split arrival counters (only ever incremented)
+    unsigned long long *ll_qkv = nullptr, *ll_o = nullptr, *ll_part = nullptr, *ll_act = nullptr;   // its flag-word
+    unsigned* ll_x = nullptr;                                                                       // exchange buffers
+    unsigned ll_epoch = 0;                              // flag numbers used so far
     bool ps_coop = true;                                // cooperative launch (STAGE_COOP=0: plain launch, for profilers)
+    int ps_pf = 64;                                     // prefetch cap into unstaged segments (STAGE_PREFETCH)
     unsigned long long* trace = nullptr;   // phase stamps of the last persistent forward (STAGE_PS_TRACE=1)
     int prof_class = -1;
     std::vector<hipEvent_t> prof_ev;   // start/stop pairs
@@ -437,22 +438,33 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
             return cleanup(fail(STAGE_E_HIP, "event creation failed"));
     if ((rc = ensure_meta(st, 1 << 16))) return cleanup(rc);
     if (st->ps_ok) {
-        if ((rc = st->alloc(&st->ps_layers, c.n_layers)) || (rc = st->alloc(&st->bar, 16 * 64)) || (rc = st->alloc(&st->err, 4)))
-            return cleanup(rc);
+        if ((rc = st->alloc(&st->ps_layers, c.n_layers)) || (rc = st->alloc(&st->err, 4))) return cleanup(rc);
         if (hipMemcpy(st->ps_layers, st->ps_host.data(), sizeof(PsLayer) * c.n_layers, hipMemcpyHostToDevice) != hipSuccess ||
-            hipMemset(st->bar, 0, 16 * 64 * 8) != hipSuccess || hipMemset(st->err, 0, 4) != hipSuccess)
+            hipMemset(st->err, 0, 4) != hipSuccess)
             return cleanup(fail(STAGE_E_HIP, "persistent state init failed"));
         int cus = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
             return cleanup(fail(STAGE_E_HIP, "CU count query failed"));
-        st->ps_nwg = cus;
-        // rows per workgroup: rotary pairs stay in one workgroup (even), gate|up
-        // pairs are stored two per dword (multiple of 4)
+        // Workgroups (at most one per CU, at most 256): rotary pairs stay in one
+        // workgroup (even row counts), gate|up rows come four to a flag word pair
+        // (multiples of 4), and every workgroup must own rows of q|k|v, of o/down
+        // and of gate|up.  The exchanges have no barriers: a buffer is rewritten
+        // only after every workgroup has produced data that depends on having
+        // read it, which takes every workgroup producing in every phase.
         auto cdiv = [](int a_, int b_) { return (a_ + b_ - 1) / b_; };
-        st->ps_rpw_qkv = (cdiv(nqkv, cus) + 1) / 2 * 2;
-        st->ps_rpw_h = cdiv(H, cus);
-        st->ps_rpw_gu = (cdiv(2 * F, cus) + 3) / 4 * 4;
+        auto rq_of = [&](int n) { return (cdiv(nqkv, n) + 1) / 2 * 2; };
+        auto rh_of = [&](int n) { return cdiv(H, n); };
+        auto rg_of = [&](int n) { return (cdiv(2 * F, n) + 3) / 4 * 4; };
+        int nwg = std::min(cus, 256);
+        while (nwg > 1 && ((nwg - 1) * rq_of(nwg) >= nqkv || (nwg - 1) * rh_of(nwg) >= H || (nwg - 1) * rg_of(nwg) >= 2 * F))
+            --nwg;
+        st->ps_nwg = nwg;
+        st->ps_rpw_qkv = rq_of(nwg);
+        st->ps_rpw_h = rh_of(nwg);
+        st->ps_rpw_gu = rg_of(nwg);
         if (st->ps_rpw_h > 64) st->ps_ok = false;              // one residual row per control lane
+        if (Hkv > nwg) st->ps_ok = false;                      // every kv head needs a workgroup
+        if (H % 4 || F % 4 || (Hq * D) % 4) st->ps_ok = false; // flag words are polled four values at a time
         for (long bytes : {(long)st->ps_rpw_qkv * st->ng_h, (long)st->ps_rpw_h * st->ng_q, (long)st->ps_rpw_gu * st->ng_h,
                            (long)st->ps_rpw_h * st->ng_f})
             if ((bytes * 2) % 16 != 0) st->ps_ok = false;      // scale rows are loaded in 16-byte pieces
@@ -463,12 +475,22 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         probe.H = H;
         const int slots = ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv);
         if (slots <= 0 || ps_layout(probe, slots, D, Hq / Hkv) > 160 * 1024) st->ps_ok = false;
-        if ((rc = st->alloc(&st->acnt_ps, Hkv))) return cleanup(rc);
-        if (hipMemset(st->acnt_ps, 0, Hkv * sizeof(unsigned)) != hipSuccess)
-            return cleanup(fail(STAGE_E_HIP, "counter init failed"));
+        // flag-word buffers start with flag number 0, which no exchange uses
+        const size_t max_split = (size_t)std::max(1, std::min(nwg / Hkv, (Hq / Hkv) * D / 8));
+        const size_t n_part = (size_t)Hkv * max_split * (Hq / Hkv) * (D + 2);
+        const size_t x_words = (size_t)H + 2 * (size_t)((nwg + 1) & ~1);   // 4-byte words
+        if ((rc = st->alloc(&st->ll_qkv, nqkv)) || (rc = st->alloc(&st->ll_o, (size_t)Hq * D / 2)) ||
+            (rc = st->alloc(&st->ll_part, n_part)) || (rc = st->alloc(&st->ll_x, x_words)) ||
+            (rc = st->alloc(&st->ll_act, (size_t)F / 2)))
+            return cleanup(rc);
+        if (hipMemset(st->ll_qkv, 0, (size_t)nqkv * 8) != hipSuccess || hipMemset(st->ll_o, 0, (size_t)Hq * D / 2 * 8) != hipSuccess ||
+            hipMemset(st->ll_part, 0, n_part * 8) != hipSuccess || hipMemset(st->ll_x, 0, x_words * 4) != hipSuccess ||
+            hipMemset(st->ll_act, 0, (size_t)F / 2 * 8) != hipSuccess)
+            return cleanup(fail(STAGE_E_HIP, "exchange buffer init failed"));
         if (const char* e = std::getenv("STAGE_COOP")) st->ps_coop = atoi(e) != 0;
+        if (const char* e = std::getenv("STAGE_PREFETCH")) st->ps_pf = std::max(0, atoi(e));
         if (const char* e = std::getenv("STAGE_PS_TRACE"))
-            if (atoi(e) && (rc = st->alloc(&st->trace, (size_t)cus * c.n_layers * PS_TRACE_PER_LAYER)))
+            if (atoi(e) && (rc = st->alloc(&st->trace, (size_t)nwg * c.n_layers * PS_TRACE_PER_LAYER)))
                 return cleanup(rc);
         // the single-launch forward is only used when its kernel needs no private
         // segment (no stack, no scratch spills) for this shape
@@ -487,13 +509,14 @@ int stage_destroy(Stage* stage) {
 
 int64_t stage_weight_bytes(const Stage* stage) { return stage ? stage->weight_bytes : -1; }
 
-int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n) {
+int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n, int* n_workgroups) {
     if (!stage || !out_host) return fail(STAGE_E_INVALID, "NULL argument");
     if (!stage->trace) return fail(STAGE_E_UNSUPPORTED, "phase trace is off (set STAGE_PS_TRACE=1 before stage_create)");
     const size_t total = (size_t)stage->ps_nwg * stage->cfg.n_layers * PS_TRACE_PER_LAYER;
     if (n < (long long)total) return fail(STAGE_E_CAPACITY, "trace needs " + std::to_string(total) + " entries");
     HIP_TRY(hipSetDevice(stage->device));
     HIP_TRY(hipMemcpy(out_host, stage->trace, total * 8, hipMemcpyDeviceToHost));
+    if (n_workgroups) *n_workgroups = stage->ps_nwg;
     return STAGE_OK;
 }
 
@@ -879,15 +902,14 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         a.hidden_in = hidden_in;
         a.hidden_out = hidden_out;
         a.rpw_qkv = st->ps_rpw_qkv; a.rpw_h = st->ps_rpw_h; a.rpw_gu = st->ps_rpw_gu;
-        a.x = st->x; a.qkv = st->qkv; a.o = (uint16_t*)st->attn; a.act = (uint16_t*)st->act;
+        a.ll_x = st->ll_x; a.ll_qkv = st->ll_qkv; a.ll_o = st->ll_o; a.ll_act = st->ll_act;
         a.meta = meta;
         a.rope = st->rope;
         a.qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
         a.nsplit = nsplit; a.split_len = split_len; a.att_T = att_T;
-        a.apart = st->apart;
-        a.acnt = st->acnt_ps;
-        a.bar = st->bar;
-        a.bar_epoch = st->bar_epoch;
+        a.ll_part = st->ll_part;
+        a.ll_epoch = st->ll_epoch;
+        a.pf = st->ps_pf;
         a.err = st->err;
         a.trace = st->trace;
         const int lds = ps_layout(a, ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, gs), D, gs);
@@ -895,7 +917,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         hipError_t e = launch_persistent(a, st->cpl_h, st->cpl_q, st->cpl_f, D, gs, st->ps_nwg, (size_t)lds, st->ps_coop, s);
         if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("single-launch forward: ") + hipGetErrorString(e));
         HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, false, s));
-        st->bar_epoch += (unsigned long long)(5 * c.n_layers - 1);
+        st->ll_epoch += (unsigned)(PS_LL_PER_LAYER * c.n_layers);
         for (int r = 0; r < n_req; ++r) {
             KVState* kv = reqs[r].state;
             if (do_gather[r]) kv->cur = 1 - kv->cur;

@@ -105,12 +105,14 @@ class Stage:
         return n.value, ms.value
 
     def phase_trace(self) -> np.ndarray:
-        """[workgroups, layers, 16] device real-time stamps (100 MHz) of the last
-        single-launch forward (needs STAGE_PS_TRACE=1 at creation)."""
-        n = torch.cuda.get_device_properties(0).multi_processor_count * self.shape.n_layers * 16
+        """[workgroups, layers, 32] device real-time stamps (100 MHz) and exchange
+        pass counts of the last single-launch forward (needs STAGE_PS_TRACE=1 at
+        creation)."""
+        n = torch.cuda.get_device_properties(0).multi_processor_count * self.shape.n_layers * 32
         out = np.empty(n, dtype=np.uint64)
-        check(self.lib.stage_debug_phase_trace(self.handle, out.ctypes.data, n))
-        return out.reshape(-1, self.shape.n_layers, 16)
+        nwg = ctypes.c_int()
+        check(self.lib.stage_debug_phase_trace(self.handle, out.ctypes.data, n, ctypes.byref(nwg)))
+        return out[: nwg.value * self.shape.n_layers * 32].reshape(nwg.value, self.shape.n_layers, 32)
 
     def new_state(self, n_slots: int, capacity: int) -> "KVState":
         return KVState(self, n_slots, capacity)
