@@ -14,6 +14,20 @@ Prints one JSON line: tokens/s, algorithmic HBM bytes per step and the
 achieved fraction of the 8 TB/s HBM peak, the dominant kernel's roofline
 (timed with HIP events on its launch stream), and the fp64 CPU oracle timed
 on a bounded sample on the host cores.
+
+--workload selects the other measured configurations (one JSON line per case,
+same fields, no CPU baseline):
+  verify8b      speculative verify on the 8B half stage: 4 cache slots x 5
+                tokens, KV 2048 growing to 2368 over 64 steps, draft outcomes
+                Bernoulli(0.6) truncated at the first rejection (rejected rows
+                stay as masked holes), beam_idx identity on even steps and a
+                seeded permutation on odd steps;
+  microbatch8b  2, 4 and 8 independent requests in one forward, KV lengths
+                U{128..4096} with 10% masked holes, all-decode and mixed
+                (half the requests verify 5 tokens) modes;
+  decode70b     Llama-3-70B quarter stage (20 layers), bs=1 decode at KV 8192;
+  verify70b     the same stage, 5-token verify at KV 4096 with Bernoulli(0.6)
+                rejections masked over 16 steps.
 """
 from __future__ import annotations
 
@@ -78,6 +92,188 @@ def cpu_baseline(shape, kv_len: int, layers_sampled: int, seed: int) -> dict:
     }
 
 
+WORKLOADS = ("decode8b", "verify8b", "microbatch8b", "decode70b", "verify70b")
+
+
+def _line(metric, value, unit, args, steps, ms, config, bytes_per_step, roof, higher=True, **extra):
+    gbps = bytes_per_step / (ms * 1e-3) / 1e9
+    line = {
+        "metric": metric, "value": round(value, 3), "unit": unit, "n_gpus": 1, "steps": steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": higher, "scaling": "weak",
+        "vs_baseline": None, "dtype": "w4a16", "data": "synthetic", "config": config,
+        "hbm_bytes_per_step": int(bytes_per_step), "achieved_gbps": round(gbps, 1),
+        "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4), "roofline": roof,
+    }
+    line.update(extra)
+    return line
+
+
+def _gateup_roofline(shape, prof):
+    launches, total_ms = prof
+    per = total_ms / max(1, launches)
+    b = gateup_bytes(shape)
+    g = b / (per * 1e-3) / 1e9
+    return {"bound": "hbm", "kernel": "gemv_kernel gate|up (one launch per layer)", "achieved": round(g, 1),
+            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(g / HBM_PEAK_GBPS, 4), "traffic": None,
+            "bytes_per_launch": b, "avg_launch_us": round(per * 1e3, 3), "launches_timed": launches}
+
+
+def other_workload(args) -> int:
+    """The measured configurations besides the headline decode (see --workload)."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2608_19147_amd import Request, Stage
+    from paper_2608_19147_amd.driver import VerifyDriver
+
+    big = args.workload.endswith("70b")
+    shape = synth.LLAMA70B_QUARTER if big else synth.LLAMA8B_HALF
+    t0 = time.perf_counter()
+    stage = Stage(shape, synth.make_weights(shape, args.seed))
+    torch.cuda.synchronize()
+    print(f"# setup {time.perf_counter() - t0:.1f}s (weights {stage.weight_bytes() / 1e9:.3f} GB on device)",
+          file=sys.stderr, flush=True)
+    kvb = shape.kv_bytes_per_token()
+    wbytes = shape.weight_bytes()
+    base_cfg = {"layers": shape.n_layers, "hidden": shape.hidden, "q_heads": shape.n_q_heads,
+                "kv_heads": shape.n_kv_heads, "head_dim": shape.head_dim, "ffn": shape.ffn,
+                "group_size": shape.group_size, "act": shape.act_dtype, "kv_cache": shape.kv_dtype}
+    lines = []
+
+    if args.workload in ("verify8b", "verify70b"):
+        S, n, K = (4, 5, 64) if not big else (1, 5, 16)
+        P0 = 2048 if not big else 4096
+        steps = args.steps if args.steps > 0 else K
+        state = stage.new_state(S, P0 + K * n + 8)
+        k, v = synth.make_kv(shape, S, P0, args.seed)
+        state.append(k, v)
+        del k, v
+        xs = [synth.make_hidden(shape, S * n, args.seed, 200 + i).cuda() for i in range(8)]
+        out = torch.empty_like(xs[0])
+
+        def episode(n_steps, step0, timed):
+            """n_steps verify steps from a fresh P0-row state; returns (seconds, emitted, bytes)."""
+            state.truncate(P0)
+            drv = VerifyDriver(S, P0)
+            emitted, nbytes, el = 0, 0, 0.0
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            for i in range(n_steps):
+                st = step0 + i
+                beam = None if S == 1 else (np.arange(S, dtype=np.int32) if st % 2 == 0
+                                            else synth.beam_permutation(S, args.seed, st))
+                P = drv.physical_len
+                pos, mask, beam = drv.step_inputs(n, beam)
+                stage.forward([Request(state, pos, mask, beam)], xs[st % len(xs)], out)
+                emitted += int(drv.accept(synth.acceptance_draws(S, n - 1, 0.6, args.seed, st)).sum())
+                nbytes += wbytes + S * (P + n) * kvb
+            torch.cuda.synchronize()
+            el = time.perf_counter() - t
+            return el, emitted, nbytes
+
+        if args.warmup:
+            episode(min(args.warmup, K), 10_000, False)
+        stage.profile("gateup")
+        tot_s, tot_em, tot_b, done = 0.0, 0, 0, 0
+        while done < steps:
+            m = min(K, steps - done)
+            el, em, nb = episode(m, done, True)
+            tot_s, tot_em, tot_b, done = tot_s + el, tot_em + em, tot_b + nb, done + m
+        prof = stage.profile_read()
+        stage.profile(None)
+        ms = tot_s * 1e3 / steps
+        cfg = {"workload": (f"llama3.1-8b half stage speculative verify, {S} slots x {n} tokens, kv {P0} growing "
+                            f"by up to {n} per step, drafts Bernoulli(0.6) truncated, beam identity/permutation "
+                            f"alternating") if not big else
+               f"llama3-70b quarter stage verify, 1 slot x {n} tokens, kv {P0} growing, drafts Bernoulli(0.6) truncated",
+               **base_cfg, "slots": S, "tokens_per_slot": n, "kv_len_start": P0}
+        lines.append(_line(f"spec-verify steps/s ({'8B half' if not big else '70B quarter'}-stage, {S}x{n} tokens)",
+                           1e3 / ms, "steps/s", args, steps, ms, cfg, tot_b / steps, _gateup_roofline(shape, prof),
+                           query_tokens_per_s=round(S * n * 1e3 / ms, 1),
+                           emitted_tokens_per_s=round(tot_em / tot_s, 1),
+                           mean_tokens_kept_per_slot_step=round(tot_em / (steps * S), 4)))
+
+    elif args.workload == "decode70b":
+        P = 8192
+        state = stage.new_state(1, P + 8)
+        k, v = synth.make_kv(shape, 1, P, args.seed)
+        state.append(k, v)
+        del k, v
+        xs = [synth.make_hidden(shape, 1, args.seed, 100 + i).cuda() for i in range(8)]
+        out = torch.empty_like(xs[0])
+        req = Request(state, np.array([[P]], np.int32), np.ones((1, P + 1), np.uint8), np.array([0], np.int32))
+        steps = args.steps
+        for i in range(args.warmup):
+            stage.forward([req], xs[i % 8], out)
+            state.truncate(P)
+        torch.cuda.synchronize()
+        stage.profile("gateup")
+        t = time.perf_counter()
+        for i in range(steps):
+            stage.forward([req], xs[i % 8], out)
+            state.truncate(P)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t) * 1e3 / steps
+        prof = stage.profile_read()
+        stage.profile(None)
+        cfg = {"workload": f"llama3-70b quarter stage decode, bs=1, kv={P}", **base_cfg, "kv_len": P, "batch": 1}
+        lines.append(_line("stage decode tokens/s (70B quarter-stage, bs=1)", 1e3 / ms, "tokens/s", args, steps, ms,
+                           cfg, wbytes + (P + 1) * kvb, _gateup_roofline(shape, prof)))
+
+    else:  # microbatch8b
+        lens = {nr: synth.kv_lengths(nr, 128, 4096, args.seed) for nr in (2, 4, 8)}
+        for nr in (2, 4, 8):
+            for mode in ("decode", "mixed"):
+                ns = [1] * nr if mode == "decode" else [5 if r % 2 == 0 else 1 for r in range(nr)]
+                reqs, states, nbytes = [], [], wbytes
+                for r in range(nr):
+                    P = int(lens[nr][r])
+                    st = stage.new_state(1, P + 8)
+                    k, v = synth.make_kv(shape, 1, P, args.seed, r)
+                    st.append(k, v)
+                    del k, v
+                    holes = synth.hole_mask(P, 0.1, args.seed, r)
+                    holes[-1] = 1
+                    mask = np.concatenate([holes, np.ones(ns[r], np.uint8)])[None]
+                    pos = (int(holes.sum()) + np.arange(ns[r], dtype=np.int32))[None]
+                    reqs.append((st, P, Request(st, pos, mask, None)))
+                    nbytes += (P + ns[r]) * kvb
+                rows = sum(ns)
+                xs = [synth.make_hidden(shape, rows, args.seed, 300 + i).cuda() for i in range(4)]
+                out = torch.empty_like(xs[0])
+
+                def one(i):
+                    stage.forward([q for _, _, q in reqs], xs[i % 4], out)
+                    for st, P, _ in reqs:
+                        st.truncate(P)
+
+                for i in range(args.warmup):
+                    one(i)
+                torch.cuda.synchronize()
+                stage.profile("gateup")
+                t = time.perf_counter()
+                for i in range(args.steps):
+                    one(i)
+                torch.cuda.synchronize()
+                ms = (time.perf_counter() - t) * 1e3 / args.steps
+                prof = stage.profile_read()
+                stage.profile(None)
+                cfg = {"workload": f"llama3.1-8b half stage micro-batch, {nr} requests, {mode} "
+                                   f"(tokens per request {ns}), kv lengths {[int(x) for x in lens[nr]]}, 10% holes",
+                       **base_cfg, "requests": nr, "mode": mode, "rows": rows}
+                lines.append(_line(f"micro-batch steps/s (8B half-stage, {nr} requests, {mode})", 1e3 / ms, "steps/s",
+                                   args, args.steps, ms, cfg, nbytes, _gateup_roofline(shape, prof),
+                                   tokens_per_s=round(rows * 1e3 / ms, 1)))
+                for st, _, _ in reqs:
+                    st.free()
+                del xs, out
+    stage.close()
+    for ln in lines:
+        print(json.dumps(ln), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -87,6 +283,7 @@ def main() -> int:
     ap.add_argument("--kv-also", type=int, default=512, help="second KV length reported (0 = none)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-layers", type=int, default=3, help="layers of the oracle sample (0 = skip)")
+    ap.add_argument("--workload", default="decode8b", choices=WORKLOADS)
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -103,6 +300,8 @@ def main() -> int:
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.workload != "decode8b":
+        return other_workload(args)
     shape = synth.LLAMA8B_HALF
     t0 = time.perf_counter()
     layers = synth.make_weights(shape, args.seed)

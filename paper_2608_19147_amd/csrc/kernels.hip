@@ -172,12 +172,14 @@ __global__ __launch_bounds__(256) void gemv_kernel(GemvArgs a) {
     if (a.rms == RMS_FULLROW) {
         rms_fullrow<MT>(a, K, rs_s, bsum);
     } else if (a.rms == RMS_PARTIALS) {
-        for (int idx = tid; idx < M * a.ssq_tiles; idx += 256) bsum[idx] = a.ssq_in[idx];
-        __syncthreads();
-        if (tid < M) {
+        // wave w reduces rows w, w + 4, ...: lane l adds tiles l, l + 64, ... in order,
+        // then lane 0 receives a fixed-order butterfly sum
+        for (int m = wave; m < M; m += 4) {
             float ss = 0.f;
-            for (int tt = 0; tt < a.ssq_tiles; ++tt) ss += bsum[tid * a.ssq_tiles + tt];
-            rs_s[tid] = rsqrtf(ss / (float)K + a.eps);
+            for (int tt = lane; tt < a.ssq_tiles; tt += 64) ss += a.ssq_in[(size_t)m * a.ssq_tiles + tt];
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+            if (lane == 0) rs_s[m] = rsqrtf(ss / (float)K + a.eps);
         }
     }
     __syncthreads();
