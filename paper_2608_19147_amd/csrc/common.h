@@ -49,7 +49,7 @@ struct MetaDev {
     const ItemDev* items;
     const int* positions;   // [M]: rotary position of each activation row
     const uint8_t* masks;   // concatenated [S][P+n] per request
-    int n_items, M;
+    int n_items, M, n_req;
 };
 
 enum GemvRms : int { RMS_NONE = 0, RMS_FULLROW = 1, RMS_PARTIALS = 2 };
@@ -60,14 +60,14 @@ struct GemvArgs {
     const void* in; int in_dt; int in_ld;          // input rows [M][K]
     const uint16_t* gamma; int gamma_dt;           // RMSNorm weight [K]
     int rms; float eps;
-    const float* ssq_in; int ssq_tiles;            // [ssq_tiles][M] sums of squares
+    const float* ssq_in; int ssq_tiles;            // [M][ssq_tiles] sums of squares
     int M;
     int ksplit, cps;
     float* partial; unsigned* counters;            // [ksplit][M][ntiles*64], [ntiles]
     int epi;
     float* out; int out_ld;                        // STORE: out, RESID: new x, SWIGLU: act
     const void* resid; int resid_dt; int resid_ld; // RESID source
-    float* ssq_out;                                // RESID: [ntiles][M]
+    float* ssq_out;                                // RESID: [M][ntiles]
     void* out_act; int out_act_dt; int out_act_ld; // RESID: optional copy in act dtype
     int n_valid;                                   // SWIGLU: F
 };
@@ -186,6 +186,9 @@ hipError_t launch_repack(const uint8_t* q, const uint16_t* s, int n, int k, int 
                          uint8_t* w_out, uint16_t* s_out, int ntiles, int nchunk, int ngroups,
                          int row_off, int row_map, hipStream_t st);
 hipError_t launch_gemv(const GemvArgs& a, hipStream_t st);
+// Matrix-core product of 1..64 rows (group size 128); a.ksplit splits K.
+hipError_t launch_gemm(const GemvArgs& a, hipStream_t st);
+int gemm_groups_per_slice(int M);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int rows_per_item_max, hipStream_t st);
 hipError_t launch_table_gather(const int16_t* src, int16_t* dst, const int* beam, int S, int cap, int P, hipStream_t st);
 hipError_t launch_kv_append(uint16_t* kc, uint16_t* vc, int16_t* table, const uint16_t* k, const uint16_t* v,

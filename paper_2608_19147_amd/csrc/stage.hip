@@ -75,6 +75,8 @@ struct Stage {
     unsigned ll_epoch = 0;                              // flag numbers used so far
     bool ps_coop = true;                                // cooperative launch (STAGE_COOP=0: plain launch, for profilers)
     int ps_pf = 64;                                     // prefetch cap into unstaged segments (STAGE_PREFETCH)
+    int gemm_min_rows = 9;                              // rows from which products use the matrix cores (STAGE_GEMM_MIN_ROWS)
+    int gemm_slices = 1;                                // K slices per matrix-core workgroup (STAGE_GEMM_SLICES)
     unsigned long long* trace = nullptr;   // phase stamps of the last persistent forward (STAGE_PS_TRACE=1)
     int prof_class = -1;
     std::vector<hipEvent_t> prof_ev;   // start/stop pairs
@@ -130,6 +132,14 @@ int plan_cpw(int ntiles, int nchunk) {
         if ((long)ntiles * (nck / cps) >= target) return cpw;
     }
     return 1;
+}
+
+// K-splits of the matrix-core product for M rows: `slices` K slices per
+// workgroup (fewer splits mean less partial-sum traffic, more means shorter
+// dependent chains per workgroup).
+int gemm_split(const DevMat& m, int M, int slices) {
+    const int gps = gemm_groups_per_slice(M) * std::max(1, slices);
+    return std::max(1, (m.pm.ngroups + gps - 1) / gps);
 }
 
 int make_mat(Stage* st, DevMat& m, int n_rows_padded_tiles, int k, int g) {
@@ -345,6 +355,8 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         st->ps_ok = ps_supported(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv) && !(e && atoi(e) == 0);
         if (st->ps_ok) st->ps_host.resize(c.n_layers);
     }
+    if (const char* e = std::getenv("STAGE_GEMM_MIN_ROWS")) st->gemm_min_rows = std::max(1, atoi(e));
+    if (const char* e = std::getenv("STAGE_GEMM_SLICES")) st->gemm_slices = std::max(1, atoi(e));
     for (int l = 0; l < c.n_layers; ++l) {
         LayerDev& L = st->layers[l];
         const LayerWeights& w = layers[l];
@@ -422,6 +434,7 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
     for (auto& L : st->layers)
         for (DevMat* m : {&L.qkv, &L.o, &L.gu, &L.d}) {
             gpart = std::max(gpart, (size_t)m->ksplit * GEMV_MAX_M * m->pm.ntiles * 64);
+            gpart = std::max(gpart, (size_t)gemm_split(*m, MAX_ROWS, 1) * MAX_ROWS * m->pm.ntiles * 64);
             max_tiles = std::max<unsigned>(max_tiles, m->pm.ntiles);
         }
     if ((rc = st->alloc(&st->x, (size_t)MAX_ROWS * H)) || (rc = st->alloc(&st->qkv, (size_t)MAX_ROWS * nqkv)) ||
@@ -864,6 +877,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     meta.masks = db + off_mask;
     meta.n_items = n_items;
     meta.M = M;
+    meta.n_req = n_req;
 
     const int act_dt = dt_code(c.act_dtype);
     const int nqkv = Hq * D + 2 * Hkv * D;
@@ -932,6 +946,11 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         a.cps = m.cps;
         a.partial = st->gpart;
         a.counters = st->gcnt;
+        if (M >= st->gemm_min_rows && m.pm.gchunks == 4 && m.pm.k % 8 == 0 && M <= MAX_ROWS) {   // matrix cores
+            a.M = M;
+            a.ksplit = gemm_split(m, M, st->gemm_slices);
+            return launch_gemm(a, s);
+        }
         for (int m0 = 0; m0 < M; m0 += GEMV_MAX_M) {
             GemvArgs b = a;
             b.M = std::min(GEMV_MAX_M, M - m0);
@@ -985,11 +1004,9 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             a.qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
             a.part = st->apart;
             a.counters = st->acnt;
-            a.nsplit_max = ATTN_MAX_SPLITS;
+            // splits per (slot, kv head): about 512 workgroups in all
+            a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, (512 + n_items * Hkv - 1) / (n_items * Hkv)));
             if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, atoi(e)));
-            // the split merge keeps 2 * nsplit + 1 floats per query row in the kernel's LDS tile
-            const int lds_floats = KGROUPS * (max_rows_item > 4 ? 8 : 4) * D;
-            a.nsplit_max = std::max(1, std::min(a.nsplit_max, (lds_floats / max_rows_item - 1) / 2));
             HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, true, s));
             HIP_TRY(launch_attention(a, D, max_rows_item, s));
             HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, false, s));
