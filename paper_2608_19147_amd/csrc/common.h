@@ -12,7 +12,7 @@ constexpr int MAX_ROWS = 64;         // activation rows per forward
 constexpr int GEMV_MAX_M = 8;        // rows one GEMV launch handles
 constexpr int GEMV_MAX_CPS = 64;     // chunks per workgroup: 4 waves x at most 16 chunks
 constexpr int ATTN_MAX_SPLITS = 64;  // KV splits per (slot, kv head)
-constexpr int ATTN_MIN_SPLIT = 32;   // fewest keys per split
+constexpr int ATTN_MIN_SPLIT = 128;  // fewest keys per split
 constexpr int KGROUPS = 16;          // 16-lane key groups per attention workgroup
 
 enum Dt : int { DT_F32 = 0, DT_F16 = 1, DT_BF16 = 2 };
@@ -151,6 +151,7 @@ inline int ps_layout(PsArgs& a, int slots, int D, int gs) {
     sb = up(sb * 2, SK_SLOT);
     int rows = a.rpw_qkv > 2 * a.rpw_h ? a.rpw_qkv : 2 * a.rpw_h;   // down rows may carry two partials
     rows = rows > a.rpw_gu ? rows : a.rpw_gu;
+    rows = rows > SK_CW * a.rpw_h ? rows : SK_CW * a.rpw_h;         // or one per compute wave
     int off = SK_CW * slots * SK_SLOT;
     a.l_xs = off;   off += kcmax * 64;                                // staged GEMV input (fp16)
     a.l_sb0 = off;  off += sb;

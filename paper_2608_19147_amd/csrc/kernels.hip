@@ -695,7 +695,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemvArgs a) {
     }
 }
 
-// Groups of 128 k per slice: a workgroup's LDS stays within about 60 KB.
+// Groups of 128 k per slice (a workgroup's LDS stays within about 60 KB); the
+// result does not depend on it: groups are accumulated one at a time in order.
 int gemm_groups_per_slice(int M) { return M <= 16 ? 8 : M <= 32 ? 4 : 2; }
 
 hipError_t launch_gemm(const GemvArgs& a, hipStream_t st) {

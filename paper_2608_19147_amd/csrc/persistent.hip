@@ -645,13 +645,16 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
     }
     // slots per segment of one layer: q|k|v rows, K/V slot pairs, o, gate|up, down rows
     // down rows: whole rows per wave when the input slice fits registers, else an even slot range
+    // with one 1 KB block per compute wave (K = 2048 * SK_CW), wave cw takes block cw of every
+    // down row of the workgroup: its input slice stays in registers for the whole segment
     constexpr bool XR_F = CPL_F <= 4;
+    constexpr bool COL_F = CPL_F == SK_CW;
     const int wg_rows_h = max(0, min(a.H, (w + 1) * a.rpw_h) - w * a.rpw_h);
     const int kspw = kslot_per_wave(wg_rows_h, CPL_F);
     const int ks0 = min(wg_rows_h * CPL_F, cw * kspw);
     const int kns = min(wg_rows_h * CPL_F, ks0 + kspw) - ks0;
     const int n0 = rq_.count * CPL_H, n1 = 2 * T, n2 = ro_.count * CPL_Q, n3 = rg_.count * CPL_H;
-    const int n4 = XR_F ? ro_.count * CPL_F : kns;
+    const int n4 = COL_F ? wg_rows_h : XR_F ? ro_.count * CPL_F : kns;
     const int total = (n0 + n1 + n2 + n3 + n4) * L;
     // The weight rows of one wave in one segment are contiguous in the row layout
     // (kc = 64 * CPL chunks per row), so a segment streams one block of 1 KB slots.
@@ -659,6 +662,7 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
     const layer_cptr layers = (layer_cptr)a.layers;                          // scalar loads
     int gl = 0, gs = -1, gleft = 0, gt = 0, gpos = 0;      // gpos: stream position of the next real load
     const uint8_t* gptr = nullptr;
+    u64 gstride = SK_SLOT;                                  // bytes between a segment's consecutive slots
     auto next_seg = [&]() {
         do {
             if (++gs == 5) {
@@ -672,11 +676,14 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         }
         gleft = gs == 0 ? n0 : gs == 1 ? n1 : gs == 2 ? n2 : gs == 3 ? n3 : n4;
         gt = 0;
+        gstride = (COL_F && gs == 4) ? (u64)a.kc_f * 16 : (u64)SK_SLOT;
         if (gs == 0) gptr = layers[gl].qkv.w + (u64)rq_.first * a.kc_h * 16;
         else if (gs == 2) gptr = layers[gl].o.w + (u64)ro_.first * a.kc_q * 16;
         else if (gs == 3) gptr = layers[gl].gu.w + (u64)rg_.first * a.kc_h * 16;
         else if (gs == 4)
-            gptr = layers[gl].d.w + (XR_F ? (u64)ro_.first * a.kc_f * 16 : (u64)w * a.rpw_h * a.kc_f * 16 + (u64)ks0 * SK_SLOT);
+            gptr = layers[gl].d.w + (COL_F  ? (u64)w * a.rpw_h * a.kc_f * 16 + (u64)cw * SK_SLOT
+                                     : XR_F ? (u64)ro_.first * a.kc_f * 16
+                                            : (u64)w * a.rpw_h * a.kc_f * 16 + (u64)ks0 * SK_SLOT);
     };
     auto issue_real = [&](uint32_t dst) {
         if (gleft == 0) return;
@@ -694,7 +701,7 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
             ++gt;
         } else {
             dma16(gptr + 16 * lane, dst);
-            gptr += SK_SLOT;
+            gptr += gstride;
         }
         if (--gleft == 0) next_seg();
     };
@@ -765,7 +772,10 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         wg_barrier();                                       // SwiGLU output is staged
         release();
         cstamp(a, lb + a.l_dbg, 4);
-        if constexpr (XR_F)
+        if constexpr (COL_F)
+            gemv_seg<1, S>(a, issue, rg, wg_rows_h, 0, a.ng_f, lb + a.l_sb1 + (uint32_t)(cw * (128 / a.gchunks)),
+                           lb + a.l_xs + 4096u * cw, lb + a.l_res + 4u * cw * a.rpw_h);
+        else if constexpr (XR_F)
             gemv_seg<CPL_F, S>(a, issue, rg, ro_.count, ro_.local, a.ng_f, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
         else
             gemv_seg_k<CPL_F, S>(a, issue, rg, ks0, kns, a.ng_f, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
@@ -1232,7 +1242,12 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
             a.trace[((size_t)blockIdx.x * a.n_layers + l) * PS_TRACE_PER_LAYER + 10 + lane] = ((const u64*)(smem + a.l_dbg))[lane];
         // ---- x += act Wd^T (own rows); the last layer writes hidden_out
         if (lane < nxr) {
-            if constexpr (CPL_F <= 4) {
+            if constexpr (CPL_F == SK_CW) {                   // one partial per compute wave, added in wave order
+                float d = 0.f;
+#pragma unroll
+                for (int c = 0; c < SK_CW; ++c) d += res[c * a.rpw_h + lane];
+                xrow += d;
+            } else if constexpr (CPL_F <= 4) {
                 xrow += res[lane];
             } else {                                          // rows shared by two waves have two partials
                 const int kspw = kslot_per_wave(nxr, CPL_F);

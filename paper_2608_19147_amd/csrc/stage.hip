@@ -75,8 +75,7 @@ struct Stage {
     unsigned ll_epoch = 0;                              // flag numbers used so far
     bool ps_coop = true;                                // cooperative launch (STAGE_COOP=0: plain launch, for profilers)
     int ps_pf = 64;                                     // prefetch cap into unstaged segments (STAGE_PREFETCH)
-    int gemm_min_rows = 9;                              // rows from which products use the matrix cores (STAGE_GEMM_MIN_ROWS)
-    int gemm_slices = 1;                                // K slices per matrix-core workgroup (STAGE_GEMM_SLICES)
+    int gemm_min_rows = 2;                              // rows from which products use the matrix cores (STAGE_GEMM_MIN_ROWS)
     unsigned long long* trace = nullptr;   // phase stamps of the last persistent forward (STAGE_PS_TRACE=1)
     int prof_class = -1;
     std::vector<hipEvent_t> prof_ev;   // start/stop pairs
@@ -134,13 +133,10 @@ int plan_cpw(int ntiles, int nchunk) {
     return 1;
 }
 
-// K-splits of the matrix-core product for M rows: `slices` K slices per
-// workgroup (fewer splits mean less partial-sum traffic, more means shorter
-// dependent chains per workgroup).
-int gemm_split(const DevMat& m, int M, int slices) {
-    const int gps = gemm_groups_per_slice(M) * std::max(1, slices);
-    return std::max(1, (m.pm.ngroups + gps - 1) / gps);
-}
+// K-splits of the matrix-core product: eight 128-k groups per split, fixed per
+// matrix, so that a row's result never depends on how many rows share the call
+// (a workgroup walks its split in slices sized for the row count).
+int gemm_split(const DevMat& m) { return std::max(1, (m.pm.ngroups + 7) / 8); }
 
 int make_mat(Stage* st, DevMat& m, int n_rows_padded_tiles, int k, int g) {
     m.pm.k = k;
@@ -356,7 +352,6 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         if (st->ps_ok) st->ps_host.resize(c.n_layers);
     }
     if (const char* e = std::getenv("STAGE_GEMM_MIN_ROWS")) st->gemm_min_rows = std::max(1, atoi(e));
-    if (const char* e = std::getenv("STAGE_GEMM_SLICES")) st->gemm_slices = std::max(1, atoi(e));
     for (int l = 0; l < c.n_layers; ++l) {
         LayerDev& L = st->layers[l];
         const LayerWeights& w = layers[l];
@@ -434,7 +429,7 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
     for (auto& L : st->layers)
         for (DevMat* m : {&L.qkv, &L.o, &L.gu, &L.d}) {
             gpart = std::max(gpart, (size_t)m->ksplit * GEMV_MAX_M * m->pm.ntiles * 64);
-            gpart = std::max(gpart, (size_t)gemm_split(*m, MAX_ROWS, 1) * MAX_ROWS * m->pm.ntiles * 64);
+            gpart = std::max(gpart, (size_t)gemm_split(*m) * MAX_ROWS * m->pm.ntiles * 64);
             max_tiles = std::max<unsigned>(max_tiles, m->pm.ntiles);
         }
     if ((rc = st->alloc(&st->x, (size_t)MAX_ROWS * H)) || (rc = st->alloc(&st->qkv, (size_t)MAX_ROWS * nqkv)) ||
@@ -948,7 +943,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         a.counters = st->gcnt;
         if (M >= st->gemm_min_rows && m.pm.gchunks == 4 && m.pm.k % 8 == 0 && M <= MAX_ROWS) {   // matrix cores
             a.M = M;
-            a.ksplit = gemm_split(m, M, st->gemm_slices);
+            a.ksplit = gemm_split(m);
             return launch_gemm(a, s);
         }
         for (int m0 = 0; m0 < M; m0 += GEMV_MAX_M) {
@@ -1004,8 +999,9 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             a.qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
             a.part = st->apart;
             a.counters = st->acnt;
-            // splits per (slot, kv head): about 512 workgroups in all
-            a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, (512 + n_items * Hkv - 1) / (n_items * Hkv)));
+            // splits per (slot, kv head) follow the request's own length only (at least
+            // ATTN_MIN_SPLIT keys each), so batch-mates never change a request's result
+            a.nsplit_max = ATTN_MAX_SPLITS;
             if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, atoi(e)));
             HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, true, s));
             HIP_TRY(launch_attention(a, D, max_rows_item, s));
