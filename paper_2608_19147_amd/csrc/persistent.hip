@@ -757,10 +757,16 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         att_seg<GS, D, S>(a, issue, rg, T, mbits, lb + a.l_q, lb + a.l_part);
         cstamp(a, lb + a.l_dbg, 1);
         wg_barrier();                                       // wave partials are in LDS
+        wg_barrier();                                       // this workgroup's merge is done: polling starts now
+        {                                                   // the attention output of every head
+            constexpr int NTO = (CPL_Q * 512 + 64 * SK_CW - 1) / (64 * SK_CW);   // Hq*D <= 2048 CPL_Q
+            stage_pairs<NTO>(a, a.ll_o, a.QD / 4, cw, a.ll_epoch + PS_LL_PER_LAYER * l + 3, lb + a.l_xs, true);
+        }
         wg_barrier();                                       // attention output is staged
         release();
         gemv_seg<CPL_Q, S>(a, issue, rg, ro_.count, ro_.local, a.ng_q, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
-        wg_barrier();
+        wg_barrier();                                       // o rows are in LDS: the input is free
+        stage_x_words<CPL_H>(a, cw, a.ll_epoch + PS_LL_PER_LAYER * l + 4, lb + a.l_xs, true);
         wg_barrier();                                       // RMSNorm(x) is staged
         release();
         cstamp(a, lb + a.l_dbg, 2);
@@ -768,7 +774,10 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         cstamp(a, lb + a.l_dbg, 3);
         wg_barrier();                                       // gate|up rows are in LDS: the input is free
         // this wave's share of the SwiGLU output (ring loads already in flight complete first)
-        stage_act<CPL_F>(a, cw, a.ll_epoch + PS_LL_PER_LAYER * l + 5, lb + a.l_xs, true);
+        {
+            constexpr int NTA = (CPL_F * 512 + 64 * SK_CW - 1) / (64 * SK_CW);   // F <= 2048 CPL_F
+            stage_pairs<NTA>(a, a.ll_act, a.F / 4, cw, a.ll_epoch + PS_LL_PER_LAYER * l + 5, lb + a.l_xs, true);
+        }
         wg_barrier();                                       // SwiGLU output is staged
         release();
         cstamp(a, lb + a.l_dbg, 4);
@@ -780,7 +789,8 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         else
             gemv_seg_k<CPL_F, S>(a, issue, rg, ks0, kns, a.ng_f, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
         cstamp(a, lb + a.l_dbg, 5);
-        wg_barrier();
+        wg_barrier();                                       // down rows are in LDS: the input is free
+        if (l + 1 < L) stage_x_words<CPL_H>(a, cw, a.ll_epoch + PS_LL_PER_LAYER * l + 6, lb + a.l_xs, true);
     }
 }
 
@@ -875,71 +885,133 @@ __device__ __forceinline__ void publish_x(const PsArgs& a, int xr0, int nxr, flo
     if (lane == 1 && (gridDim.x & 1) && blockIdx.x == gridDim.x - 1) ll_store(sw + gridDim.x, 0u, flag);
 }
 
-// Polls the published u into LDS xs (fp16, padding up to kpad zeroed) and
-// returns rs from the workgroups' sums of squares (added in a fixed order).
+// The published u, polled by the compute waves (compute wave wv of SK_CW takes
+// pieces lane + 64 (wv + SK_CW t)) into LDS xs: a wave that only polls is not
+// held up by the acknowledgement of stores of its own.
 template <int CPL_H>
-__device__ __forceinline__ float stage_x(const PsArgs& a, uint32_t flag, uint8_t* xs, int kpad, bool& ok, int tl, int tw) {
-    constexpr int NXP = CPL_H * 8;         // pieces (four u) per lane: H <= 2048 CPL_H
-    constexpr int NSP = 2;                 // pieces (two sums) per lane: up to 256 workgroups
+__device__ __forceinline__ bool stage_x_words(const PsArgs& a, int wv, uint32_t flag, uint32_t xs, bool ok) {
+    constexpr int NTX = (CPL_H * 512 + 64 * SK_CW - 1) / (64 * SK_CW);   // pieces (four u) per lane: H <= 2048 CPL_H
     const int lane = fresh_lane();
-    const int nss = ss_words(gridDim.x);
-    const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_x, (size_t)a.H * 4 + (size_t)nss * 8);
-    int off[NXP + NSP];
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_x, (size_t)a.H * 4);
+    int off[NTX];
     uint32_t use = 0u;
 #pragma unroll
-    for (int t = 0; t < NXP; ++t) {
-        const int it = lane + 64 * t;
+    for (int t = 0; t < NTX; ++t) {
+        const int it = lane + 64 * (wv + SK_CW * t);
         const bool u = it < a.H / 4;
         off[t] = u ? 16 * it : 0;
         use |= (u ? 1u : 0u) << t;
     }
+    return ll_wait<NTX, NTX>(a, r, off, use, flag, [&](int i, const u32x4& pc) {
+        const uint32_t w0 = pc[0], w1 = pc[1], w2 = pc[2], w3 = pc[3];
+        lds_wr8(xs + 8 * (lane + 64 * (wv + SK_CW * i)), u32x2{(w0 & 0xFFFFu) | (w1 << 16), (w2 & 0xFFFFu) | (w3 << 16)});
+    }, ok);
+}
+
+// rs from the workgroups' published sums of squares (added in a fixed order);
+// the control wave, which published, polls only these.
+__device__ __forceinline__ float stage_x_rs(const PsArgs& a, uint32_t flag, bool& ok, int tl, int tw) {
+    constexpr int NSP = 2;                 // pieces (two sums) per lane: up to 256 workgroups
+    const int lane = fresh_lane();
+    const int nss = ss_words(gridDim.x);
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_x, (size_t)a.H * 4 + (size_t)nss * 8);
+    int off[NSP];
+    uint32_t use = 0u;
 #pragma unroll
     for (int t = 0; t < NSP; ++t) {
         const int it = lane + 64 * t;
         const bool u = it < nss / 2;
-        off[NXP + t] = u ? 4 * a.H + 16 * it : 0;
-        use |= (u ? 1u : 0u) << (NXP + t);
+        off[t] = u ? 4 * a.H + 16 * it : 0;
+        use |= (u ? 1u : 0u) << t;
     }
     float ssv[2 * NSP];
 #pragma unroll
     for (int j = 0; j < 2 * NSP; ++j) ssv[j] = 0.f;
-    ok = ll_wait<NXP + NSP, NXP>(a, r, off, use, flag, [&](int i, const u32x4& pc) {
-        const uint32_t w0 = pc[0], w1 = pc[1], w2 = pc[2], w3 = pc[3];
-        if (i < NXP) {
-            *(u32x2*)(xs + 8 * (lane + 64 * i)) = u32x2{(w0 & 0xFFFFu) | (w1 << 16), (w2 & 0xFFFFu) | (w3 << 16)};
-        } else {
-            ssv[2 * (i - NXP)] = __uint_as_float(w0);
-            ssv[2 * (i - NXP) + 1] = __uint_as_float(w2);
-        }
+    ok = ll_wait<NSP>(a, r, off, use, flag, [&](int i, const u32x4& pc) {
+        const uint32_t w0 = pc[0], w2 = pc[2];
+        ssv[2 * i] = __uint_as_float(w0);
+        ssv[2 * i + 1] = __uint_as_float(w2);
     }, ok, tl, tw);
-    zero_pad(a.H, kpad, xs);
     float ss = 0.f;
 #pragma unroll
     for (int j = 0; j < 2 * NSP; ++j) ss += ssv[j];
     return rsqrtf(wave_sum(ss) / (float)a.H + a.eps);
 }
 
-// This wave's share (wave wv of the eight) of the SwiGLU output, from its flag
-// words into LDS xs (fp16).  All waves of the workgroup take part.
-template <int CPL_F>
-__device__ __forceinline__ bool stage_act(const PsArgs& a, int wv, uint32_t flag, uint32_t xs, bool ok, int tl = -1,
-                                          int tw = -1) {
-    constexpr int NTW = CPL_F;             // pieces (four outputs) per lane and wave: F <= 2048 CPL_F
+// A buffer of fp16 pairs in 8-byte flag words (attention output, SwiGLU output),
+// polled by NW compute waves into LDS xs: wave wv of them takes pieces (four
+// values) lane + 64 (wv + NW t), t < NT.
+template <int NT, int NW = SK_CW>
+__device__ __forceinline__ bool stage_pairs(const PsArgs& a, const u64* buf, int npieces, int wv, uint32_t flag,
+                                            uint32_t xs, bool ok) {
     const int lane = fresh_lane();
-    const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_act, (size_t)a.F / 2 * 8);
-    int off[NTW];
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(buf, (size_t)npieces * 16);
+    int off[NT];
     uint32_t use = 0u;
 #pragma unroll
-    for (int t = 0; t < NTW; ++t) {
-        const int it = lane + 64 * (wv + 8 * t);
-        const bool u = it < a.F / 4;
+    for (int t = 0; t < NT; ++t) {
+        const int it = lane + 64 * (wv + NW * t);
+        const bool u = it < npieces;
         off[t] = u ? 16 * it : 0;
         use |= (u ? 1u : 0u) << t;
     }
-    return ll_wait<NTW>(a, r, off, use, flag, [&](int i, const u32x4& pc) {
+    return ll_wait<NT>(a, r, off, use, flag, [&](int i, const u32x4& pc) {
         const uint32_t p0 = pc[0], p1 = pc[2];
-        lds_wr8(xs + 8 * (lane + 64 * (wv + 8 * i)), u32x2{p0, p1});
-    }, ok, tl, tw);
+        lds_wr8(xs + 8 * (lane + 64 * (wv + NW * i)), u32x2{p0, p1});
+    }, ok);
+}
+
+// Split merge (control wave of each attention workgroup): every split of a
+// kv head reads the partials (max, sum, outputs) of all the head group's splits
+// for its own 1/nsplit slice of the group's outputs, combines them in a fixed
+// butterfly order and publishes that slice of the attention output.
+template <int GS, int D>
+__device__ __forceinline__ void merge_slices(const PsArgs& a, int g, int split, uint32_t f_part, uint32_t f_o) {
+    const int SL = GS * D / a.nsplit;                 // outputs per slice (multiple of 8)
+    const int CH = SL / 8;                            // 8-output chunks per slice
+    const int ml = fresh_lane();
+    const int s2 = ml / CH, c = ml % CH;              // lane: one split's chunk of the slice
+    const bool act = s2 < a.nsplit;
+    const int o0 = split * SL + 8 * c;                // first output of the chunk within the head group
+    const int hh = o0 / D, dd = o0 % D;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_part, (size_t)a.Hkv * a.nsplit * GS * (D + 2) * 8);
+    const int base = act ? (int)((((size_t)g * a.nsplit + s2) * GS + hh) * (D + 2)) * 8 : 0;
+    const int off[5] = {base, base + 8 * (2 + dd), base + 8 * (2 + dd) + 16, base + 8 * (2 + dd) + 32,
+                        base + 8 * (2 + dd) + 48};
+    u32x4 pv[5];
+    ll_wait<5>(a, r, off, act ? 0x1Fu : 0u, f_part, [&](int i, const u32x4& pc) { pv[i] = pc; }, true);
+    float ms = -INFINITY, ls = 0.f, ov[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ov[e] = 0.f;
+    if (act) {
+        const uint32_t m0 = pv[0][0], l0 = pv[0][2];
+        ms = __uint_as_float(m0);
+        ls = __uint_as_float(l0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t x0 = pv[1 + j][0], x1 = pv[1 + j][2];
+            ov[2 * j] = __uint_as_float(x0);
+            ov[2 * j + 1] = __uint_as_float(x1);
+        }
+    }
+    // combine the splits: lanes c, c + CH, c + 2 CH, ... (fixed butterfly order)
+    float Mx = ms;
+    for (int sh = CH; sh < 64; sh <<= 1) Mx = fmaxf(Mx, __shfl_xor(Mx, sh));
+    const float wgt = (ms == -INFINITY) ? 0.f : exp2f(ms - Mx);
+    float Ls = wgt * ls;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ov[e] *= wgt;
+    for (int sh = CH; sh < 64; sh <<= 1) {
+        Ls += __shfl_xor(Ls, sh);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ov[e] += __shfl_xor(ov[e], sh);
+    }
+    if (act && s2 == 0) {
+        const float inv = 1.0f / Ls;
+        u64* dst = a.ll_o + ((size_t)(g * GS + hh) * D + dd) / 2;
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) ll_store(dst + e / 2, pack_f16x2(ov[e] * inv, ov[e + 1] * inv), f_o);
+    }
 }
 
 template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
@@ -1127,76 +1199,11 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
                 ll_store(pp, __float_as_uint(mx), f_part);
                 ll_store(pp + 1, __float_as_uint(L), f_part);
             }
-            // every split of this kv head reads the partials of all of them for its own
-            // 1/nsplit slice of the head group's outputs and merges that slice
-            const int SL = GS * D / a.nsplit;                 // outputs per slice (multiple of 8)
-            const int CH = SL / 8;                            // 8-output chunks per slice
-            const int ml = fresh_lane();
-            const int s2 = ml / CH, c = ml % CH;              // lane: one split's chunk of the slice
-            const bool act = s2 < a.nsplit;
-            const int o0 = split * SL + 8 * c;                // first output of the chunk within the head group
-            const int hh = o0 / D, dd = o0 % D;
-            const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_part, (size_t)a.Hkv * a.nsplit * GS * (D + 2) * 8);
-            const int base = act ? (int)((((size_t)g * a.nsplit + s2) * GS + hh) * (D + 2)) * 8 : 0;
-            const int off[5] = {base, base + 8 * (2 + dd), base + 8 * (2 + dd) + 16, base + 8 * (2 + dd) + 32,
-                                base + 8 * (2 + dd) + 48};
-            u32x4 pv[5];
-            ok = ll_wait<5>(a, r, off, act ? 0x1Fu : 0u, f_part, [&](int i, const u32x4& pc) { pv[i] = pc; }, ok, l, 1);
-            float ms = -INFINITY, ls = 0.f, ov[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) ov[e] = 0.f;
-            if (act) {
-                const uint32_t m0 = pv[0][0], l0 = pv[0][2];
-                ms = __uint_as_float(m0);
-                ls = __uint_as_float(l0);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const uint32_t x0 = pv[1 + j][0], x1 = pv[1 + j][2];
-                    ov[2 * j] = __uint_as_float(x0);
-                    ov[2 * j + 1] = __uint_as_float(x1);
-                }
-            }
-            // combine the splits: lanes c, c + CH, c + 2 CH, ... (fixed butterfly order)
-            float Mx = ms;
-            for (int sh = CH; sh < 64; sh <<= 1) Mx = fmaxf(Mx, __shfl_xor(Mx, sh));
-            const float wgt = (ms == -INFINITY) ? 0.f : exp2f(ms - Mx);
-            float Ls = wgt * ls;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) ov[e] *= wgt;
-            for (int sh = CH; sh < 64; sh <<= 1) {
-                Ls += __shfl_xor(Ls, sh);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) ov[e] += __shfl_xor(ov[e], sh);
-            }
-            if (act && s2 == 0) {
-                const float inv = 1.0f / Ls;
-                u64* dst = a.ll_o + ((size_t)(g * GS + hh) * D + dd) / 2;
-#pragma unroll
-                for (int e = 0; e < 8; e += 2) ll_store(dst + e / 2, pack_f16x2(ov[e] * inv, ov[e + 1] * inv), f_o);
-            }
+            merge_slices<GS, D>(a, g, split, f_part, f_o);
         }
         stamp(a, l, 4);
-        // ---- the attention output (every head) as this workgroup's o input
-        {
-            constexpr int NOP = CPL_Q * 8;                    // 16-byte pieces (4 outputs) per lane; K = Hq*D <= 2048 CPL_Q
-            static_assert(NOP <= 32, "one bit per piece");
-            const int lane = fresh_lane();
-            const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_o, (size_t)a.QD / 2 * 8);
-            int off[NOP];
-            uint32_t use = 0u;
-#pragma unroll
-            for (int t = 0; t < NOP; ++t) {
-                const int it = lane + 64 * t;
-                const bool u = it < a.QD / 4;
-                off[t] = u ? 16 * it : 0;
-                use |= (u ? 1u : 0u) << t;
-            }
-            ok = ll_wait<NOP>(a, r, off, use, f_o, [&](int i, const u32x4& pc) {
-                const uint32_t p0 = pc[0], p1 = pc[2];
-                *(u32x2*)(xs + 8 * (lane + 64 * i)) = u32x2{p0, p1};
-            }, ok, l, 2);
-            zero_pad(a.QD, a.kc_q * 32, xs);
-        }
+        wg_barrier();                                         // merge done: the compute waves poll the attention output
+        zero_pad(a.QD, a.kc_q * 32, xs);                      // (they stage it)
         wg_barrier();                                         // attention output staged
         wg_barrier();                                         // o rows are in LDS
         stamp(a, l, 5);
@@ -1205,7 +1212,8 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         publish_x(a, xr0, nxr, xrow, gam_f, c, f_xo);
         stamp(a, l, 6);
         {
-            const float rs = stage_x<CPL_H>(a, f_xo, xs, a.kc_h * 32, ok, l, 3);
+            const float rs = stage_x_rs(a, f_xo, ok, l, 3);      // the compute waves stage the published x
+            zero_pad(a.H, a.kc_h * 32, xs);
             mg = rs / c;
             c = rs;
         }
@@ -1228,8 +1236,7 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
             }
         }
         stamp(a, l, 8);
-        ok = stage_act<CPL_F>(a, SK_CW, f_act, lb + a.l_xs, ok, l, 4);
-        zero_pad(a.F, a.kc_f * 32, xs);
+        zero_pad(a.F, a.kc_f * 32, xs);                       // the compute waves stage the SwiGLU output
         wg_barrier();                                         // SwiGLU output staged
         if (!last) {
             const PsLayer& Ln = a.layers[l + 1];
@@ -1258,7 +1265,8 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         }
         if (!last) {
             publish_x(a, xr0, nxr, xrow, gam_a, c, f_xd);
-            const float rs = stage_x<CPL_H>(a, f_xd, xs, a.kc_h * 32, ok, l, 5);
+            const float rs = stage_x_rs(a, f_xd, ok, l, 5);
+            zero_pad(a.H, a.kc_h * 32, xs);
             mq = rs / c;
             c = rs;
             wg_barrier();                                     // next layer's q|k|v input staged

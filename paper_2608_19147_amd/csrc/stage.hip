@@ -885,7 +885,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         const int P = reqs[0].state->P;
         // splits per kv head: a power of two; each split's merge slice is a multiple of 8 outputs
         const int max_split = std::min(st->ps_nwg / Hkv, gs * D / 8);
-        int cap_split = 16;
+        int cap_split = 32;
         if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) cap_split = std::max(1, atoi(e));
         nsplit = 1;
         while (nsplit * 2 <= std::min(cap_split, max_split)) nsplit *= 2;
