@@ -128,7 +128,6 @@ struct PsArgs {
     int nsplit, split_len, att_T;        // splits per kv head (power of two), cache rows per split, slot pairs per wave
     unsigned long long* ll_part;         // [Hkv][nsplit][Hq/Hkv][D + 2] flag words (fp32): max, sum, D outputs
     unsigned ll_epoch;                   // flag numbers used by earlier launches (PS_LL_PER_LAYER per layer)
-    int pf;                              // ring slots a compute wave may prefetch into a segment whose input is not staged
     unsigned* err;                       // set when an exchange wait gives up
     unsigned long long* trace;           // optional [nwg][n_layers][PS_TRACE_PER_LAYER] real-time stamps
     // LDS byte offsets

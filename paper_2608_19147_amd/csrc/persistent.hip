@@ -122,6 +122,46 @@ __device__ __forceinline__ float group_sum(float v) {
     return v;
 }
 
+// The values of v in this lane and in lane ^ sh.  For sh = 16 and 32 one swap
+// instruction returns, in every lane, the value of the lower and of the upper
+// lane of the pair (a = lower, b = upper); otherwise a is this lane's value.
+__device__ __forceinline__ void lane_pair(float v, int sh, float& a, float& b) {
+    const uint32_t u = __float_as_uint(v);
+    if (sh == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+        a = __uint_as_float(r[0]);
+        b = __uint_as_float(r[1]);
+    } else if (sh == 32) {
+        const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+        a = __uint_as_float(r[0]);
+        b = __uint_as_float(r[1]);
+    } else {
+        a = v;
+        b = __shfl_xor(v, sh);
+    }
+}
+
+// Sums of four rows' per-lane partials v0..v3 at once, in a fixed order:
+// lane l < 4 receives the sum of v_l over the wave.  Each step halves the
+// values per lane by exchanging the one the partner keeps (xor 1, xor 2), then
+// the 16-lane rows and the four rows of the wave are added.
+__device__ __forceinline__ float sum4_rows(float v0, float v1, float v2, float v3, int lane) {
+    const bool b0 = (lane & 1) != 0, b1 = (lane & 2) != 0;
+    float k0 = b0 ? v1 : v0;
+    k0 += dpp_f<0xB1>(b0 ? v0 : v1);  // quad_perm [1,0,3,2]: lane ^ 1
+    float k1 = b0 ? v3 : v2;
+    k1 += dpp_f<0xB1>(b0 ? v2 : v3);
+    float k = b1 ? k1 : k0;
+    k += dpp_f<0x4E>(b1 ? k0 : k1);   // quad_perm [2,3,0,1]: lane ^ 2; lane holds row lane & 3
+    k += dpp_f<0x124>(k);             // row_ror:4
+    k += dpp_f<0x128>(k);             // row_ror:8: the 16-lane row
+    float lo, hi;
+    lane_pair(k, 16, lo, hi);
+    k = lo + hi;
+    lane_pair(k, 32, lo, hi);
+    return lo + hi;
+}
+
 // ------------------------------------------------------------------ flag-in-data exchange
 //
 // A 32-bit value exchanged between workgroups travels in one 8-byte word with
@@ -333,6 +373,7 @@ __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg
         touch(cw[i]);
         touch(cs[i]);
     }
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;          // per-lane partials of rows 4 (r / 4) + 0..3
     for (int r = 0; r < nrows; ++r) {
         // refill this row's slots, then start reading the next row
 #pragma unroll
@@ -398,8 +439,15 @@ __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg
                 cs[i] = ns[i];
             }
         }
-        const float rs = wave_sum(acc);
-        if (lane == 0) lds_wr4(res + 4 * (rlocal + r), rs);
+        const int q = r & 3;
+        a0 = q == 0 ? acc : a0;
+        a1 = q == 1 ? acc : a1;
+        a2 = q == 2 ? acc : a2;
+        a3 = q == 3 ? acc : a3;
+        if (q == 3 || !more) {                              // rows r - q .. r are complete (later ones hold stale sums)
+            const float rs = sum4_rows(a0, a1, a2, a3, lane);
+            if (lane <= q) lds_wr4(res + 4 * (rlocal + r - q + lane), rs);
+        }
     }
 }
 
@@ -572,22 +620,26 @@ __device__ __forceinline__ void att_seg(const PsArgs& a, Issue& issue, Ring& rg,
                 }
             }
         }
-        // merge the row groups (lanes LPR, 2 LPR, ... apart)
+        // merge the row groups (lanes LPR, 2 LPR, ... apart); for groups 16 and 32
+        // lanes apart both partners of a pair receive the same two operands in the
+        // same order, so they compute identical merges
 #pragma unroll
         for (int h = 0; h < GS; ++h) {
 #pragma unroll
             for (int sh = LPR; sh < 64; sh <<= 1) {
-                const float m2 = __shfl_xor(m[h], sh);
-                const float l2 = __shfl_xor(l[h], sh);
-                const float mn = fmaxf(m[h], m2);
-                const float w1 = (m[h] == -INFINITY) ? 0.f : exp2f(m[h] - mn);
-                const float w2 = (m2 == -INFINITY) ? 0.f : exp2f(m2 - mn);
+                float mA, mB, lA, lB;
+                lane_pair(m[h], sh, mA, mB);
+                lane_pair(l[h], sh, lA, lB);
+                const float mn = fmaxf(mA, mB);
+                const float wA = (mA == -INFINITY) ? 0.f : exp2f(mA - mn);
+                const float wB = (mB == -INFINITY) ? 0.f : exp2f(mB - mn);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    const float o2 = __shfl_xor(o[h][e], sh);
-                    o[h][e] = o[h][e] * w1 + o2 * w2;
+                    float oA, oB;
+                    lane_pair(o[h][e], sh, oA, oB);
+                    o[h][e] = oA * wA + oB * wB;
                 }
-                l[h] = l[h] * w1 + l2 * w2;
+                l[h] = lA * wA + lB * wB;
                 m[h] = mn;
             }
         }
@@ -660,7 +712,11 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
     // (kc = 64 * CPL chunks per row), so a segment streams one block of 1 KB slots.
     typedef __attribute__((address_space(4))) const PsLayer* layer_cptr;   // never written during the launch:
     const layer_cptr layers = (layer_cptr)a.layers;                          // scalar loads
-    int gl = 0, gs = -1, gleft = 0, gt = 0, gpos = 0;      // gpos: stream position of the next real load
+    // Stream state: segment gs of layer gl, gleft slots left in it.  In a weight
+    // segment every slot but the last is issued by the fast path (gfast counts
+    // them); the last one, the attention slots and the end of the stream take
+    // the general path, which also moves to the next segment.
+    int gl = 0, gs = -1, gleft = 0, gt = 0, gfast = 0;
     const uint8_t* gptr = nullptr;
     u64 gstride = SK_SLOT;                                  // bytes between a segment's consecutive slots
     auto next_seg = [&]() {
@@ -672,6 +728,7 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         } while (gl < L && (gs == 0 ? n0 : gs == 1 ? n1 : gs == 2 ? n2 : gs == 3 ? n3 : n4) == 0);
         if (gl >= L) {
             gleft = 0;
+            gfast = 0;
             return;
         }
         gleft = gs == 0 ? n0 : gs == 1 ? n1 : gs == 2 ? n2 : gs == 3 ? n3 : n4;
@@ -684,10 +741,15 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
             gptr = layers[gl].d.w + (COL_F  ? (u64)w * a.rpw_h * a.kc_f * 16 + (u64)cw * SK_SLOT
                                      : XR_F ? (u64)ro_.first * a.kc_f * 16
                                             : (u64)w * a.rpw_h * a.kc_f * 16 + (u64)ks0 * SK_SLOT);
-    };
-    auto issue_real = [&](uint32_t dst) {
-        if (gleft == 0) return;
-        ++gpos;
+        if (gs != 1) {
+            gfast = gleft - 1;
+            gleft = 1;
+        }
+        asm volatile("" ::"s"(gptr));                       // the pointer's scalar load completes here, not at
+    };                                                      // every later refill
+    const uint32_t lane16 = 16u * (uint32_t)lane;
+    auto issue_general = [&](uint32_t dst) {
+        if (gleft == 0) return;                             // past the end of the stream: nothing to load
         if (gs == 1) {
             const int t = gt >> 1;
             uint32_t off = aoff[0];
@@ -700,47 +762,20 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
             dma16(((gt & 1) ? vbase : kbase) + (u64)gl * lstride_b + off, dst);
             ++gt;
         } else {
-            dma16(gptr + 16 * lane, dst);
-            gptr += gstride;
+            dma16(gptr + lane16, dst);
         }
         if (--gleft == 0) next_seg();
     };
-    // Prefetch into a segment whose input is not staged yet is capped at a.pf
-    // slots: the exchange loads that stage the input queue behind every load
-    // this CU issued before them.  A refill past the cap is issued as an
-    // out-of-range buffer load (answered without a memory access, its zeros
-    // land in the consumed slot) so the ring's fixed wait counts stay exact;
-    // the real loads follow, in stream order, once the input is staged.
-    // The attention slots are not capped: their input (this head group's
-    // queries) is staged from data that is usually complete by then.
-    const int NL = n0 + n1 + n2 + n3 + n4;
-    auto seg_start = [&](int j) {
-        const int k = j % 5;
-        return (j / 5) * NL + (k > 0 ? n0 : 0) + (k > 1 ? n1 : 0) + (k > 2 ? n2 : 0) + (k > 3 ? n3 : 0);
-    };
-    auto limit_of = [&](int j) {                            // j: first segment whose input is not staged
-        if (j % 5 == 1) ++j;
-        return j >= 5 * L ? total : min(total, seg_start(j) + a.pf);
-    };
-    const __amdgpu_buffer_rsrc_t none = make_rsrc(a.err, 0);
-    const uint32_t ring = lb + (uint32_t)(cw * S * SK_SLOT);
-    int rel = 1, lim = limit_of(1), ndef = 0;               // q|k|v of layer 0 is not capped
     auto issue = [&](uint32_t dst) {
-        if (ndef > 0 || gpos >= lim) {
-            if (gpos + ndef >= total) return;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(none, (lds_ptr_t)(uintptr_t)dst, 16, 0x7FFFFFF0, 0, 0, 0);
-            ++ndef;
-            return;
-        }
-        issue_real(dst);
-    };
-    auto release = [&]() {                                  // the input of segment `rel` is staged
-        lim = limit_of(++rel);
-        while (ndef > 0 && gpos < lim) {
-            --ndef;
-            issue_real(ring + (uint32_t)(gpos % S) * SK_SLOT);
+        if (gfast > 0) {
+            --gfast;
+            dma16(gptr + lane16, dst);
+            gptr += gstride;
+        } else {
+            issue_general(dst);
         }
     };
+    const uint32_t ring = lb + (uint32_t)(cw * S * SK_SLOT);
     next_seg();
     vm_wait_all();                                          // table and mask reads are done
     for (int k = 0; k < S; ++k) issue(ring + (uint32_t)k * SK_SLOT);
@@ -748,11 +783,9 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
     Ring rg{ring, 0, 0, total - S};
     for (int l = 0; l < L; ++l) {
         wg_barrier();                                       // input of q|k|v is staged
-        if (l > 0) release();
         gemv_seg<CPL_H, S>(a, issue, rg, rq_.count, rq_.local, a.ng_h, lb + a.l_sb0, lb + a.l_xs, lb + a.l_res);
         wg_barrier();                                       // q|k|v rows are in LDS
         wg_barrier();                                       // q and the new row are staged
-        release();
         cstamp(a, lb + a.l_dbg, 0);
         att_seg<GS, D, S>(a, issue, rg, T, mbits, lb + a.l_q, lb + a.l_part);
         cstamp(a, lb + a.l_dbg, 1);
@@ -763,12 +796,10 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
             stage_pairs<NTO>(a, a.ll_o, a.QD / 4, cw, a.ll_epoch + PS_LL_PER_LAYER * l + 3, lb + a.l_xs, true);
         }
         wg_barrier();                                       // attention output is staged
-        release();
         gemv_seg<CPL_Q, S>(a, issue, rg, ro_.count, ro_.local, a.ng_q, lb + a.l_sb1, lb + a.l_xs, lb + a.l_res);
         wg_barrier();                                       // o rows are in LDS: the input is free
         stage_x_words<CPL_H>(a, cw, a.ll_epoch + PS_LL_PER_LAYER * l + 4, lb + a.l_xs, true);
         wg_barrier();                                       // RMSNorm(x) is staged
-        release();
         cstamp(a, lb + a.l_dbg, 2);
         gemv_seg<CPL_H, S>(a, issue, rg, rg_.count, rg_.local, a.ng_h, lb + a.l_sb0, lb + a.l_xs, lb + a.l_res);
         cstamp(a, lb + a.l_dbg, 3);
@@ -779,7 +810,6 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
             stage_pairs<NTA>(a, a.ll_act, a.F / 4, cw, a.ll_epoch + PS_LL_PER_LAYER * l + 5, lb + a.l_xs, true);
         }
         wg_barrier();                                       // SwiGLU output is staged
-        release();
         cstamp(a, lb + a.l_dbg, 4);
         if constexpr (COL_F)
             gemv_seg<1, S>(a, issue, rg, wg_rows_h, 0, a.ng_f, lb + a.l_sb1 + (uint32_t)(cw * (128 / a.gchunks)),

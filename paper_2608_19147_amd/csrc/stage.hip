@@ -74,7 +74,6 @@ struct Stage {
     unsigned* ll_x = nullptr;                                                                       // exchange buffers
     unsigned ll_epoch = 0;                              // flag numbers used so far
     bool ps_coop = true;                                // cooperative launch (STAGE_COOP=0: plain launch, for profilers)
-    int ps_pf = 64;                                     // prefetch cap into unstaged segments (STAGE_PREFETCH)
     int gemm_min_rows = 2;                              // rows from which products use the matrix cores (STAGE_GEMM_MIN_ROWS)
     unsigned long long* trace = nullptr;   // phase stamps of the last persistent forward (STAGE_PS_TRACE=1)
     int prof_class = -1;
@@ -496,7 +495,6 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
             hipMemset(st->ll_act, 0, (size_t)F / 2 * 8) != hipSuccess)
             return cleanup(fail(STAGE_E_HIP, "exchange buffer init failed"));
         if (const char* e = std::getenv("STAGE_COOP")) st->ps_coop = atoi(e) != 0;
-        if (const char* e = std::getenv("STAGE_PREFETCH")) st->ps_pf = std::max(0, atoi(e));
         if (const char* e = std::getenv("STAGE_PS_TRACE"))
             if (atoi(e) && (rc = st->alloc(&st->trace, (size_t)nwg * c.n_layers * PS_TRACE_PER_LAYER)))
                 return cleanup(rc);
@@ -918,7 +916,6 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         a.nsplit = nsplit; a.split_len = split_len; a.att_T = att_T;
         a.ll_part = st->ll_part;
         a.ll_epoch = st->ll_epoch;
-        a.pf = st->ps_pf;
         a.err = st->err;
         a.trace = st->trace;
         const int lds = ps_layout(a, ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, gs), D, gs);
