@@ -81,6 +81,7 @@ struct AttnArgs {
     float qscale;            // log2(e) / sqrt(D)
     float* part; unsigned* counters;
     int nsplit_max;
+    int vector_path;         // 1: attn_kernel (vector units) instead of attn_mma_kernel
 };
 
 // ---- single-launch stage forward (persistent.hip)
@@ -107,6 +108,11 @@ struct PsLayer {
 
 struct PsArgs {
     const PsLayer* layers;               // device array
+    // Code rows of each matrix kind (q|k|v, o, gate|up, down) for all layers in
+    // one allocation: layer l's rows start at wb[m] + l * wl[m] (equal to
+    // layers[l].<m>.w), so the compute waves form stream addresses without loads.
+    const uint8_t* wb[4];
+    unsigned long long wl[4];
     int n_layers;
     int H, Hq, Hkv, F, QD, NQKV;
     int kc_h, kc_q, kc_f;                // chunks per row for K = H, Hq*D, F

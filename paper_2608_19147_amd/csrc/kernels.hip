@@ -974,16 +974,350 @@ __global__ __launch_bounds__(D) void attn_merge_kernel(AttnArgs a) {
     a.out[(size_t)m * a.out_ld + (size_t)h * D + d] = O * inv_s;
 }
 
+// ------------------------------------------------------------------ matrix-core attention
+//
+// Same work split, partial format and append as attn_kernel, with the products
+// on the matrix cores: every query vector of the (item, kv head) meets each
+// 32-key step once.  Per 16-key subtile the scores are S^T = K Q^T (cache rows
+// are the A operand as stored; q is split into a rounded part and its residual,
+// both in the cache dtype, so the scores carry nearly fp32 precision), and the
+// output is O^T += V^T P^T with P^T taken straight from the score registers
+// (lane l holds keys 4 (l / 16) + j of both subtiles: exactly the k-slots of
+// the B operand) and V^T read from a transposed copy of the value tile in LDS
+// whose key slots follow the same order.  Keys a query may not see enter as
+// zero rows with a -inf score.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+constexpr int AK = 32;                   // keys per step
+constexpr int ACH = 512;                 // keys whose table entry and mask byte are staged at once
+
+template <int KVDT>
+__device__ __forceinline__ f32x4_t mma_kv(const u32x4& A, const u32x4& B, f32x4_t c) {
+    if constexpr (KVDT == DT_BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, A), __builtin_bit_cast(bf16x8_t, B), c,
+                                                       0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, A), __builtin_bit_cast(half8_t, B), c, 0,
+                                                      0, 0);
+}
+template <int KVDT>
+__device__ __forceinline__ uint16_t kv_round(float f) { return KVDT == DT_BF16 ? f32_to_bf16(f) : f32_to_f16(f); }
+template <int KVDT>
+__device__ __forceinline__ float kv_float(uint16_t b) { return KVDT == DT_BF16 ? bf16_to_f32(b) : f16_to_f32(b); }
+
+// The values of v in this lane and in lane ^ sh (sh = 16 or 32): every lane of
+// the pair receives the lower lane's value in a and the upper lane's in b.
+__device__ __forceinline__ void lane_pair_k(float v, int sh, float& a, float& b) {
+    const uint32_t u = __float_as_uint(v);
+    if (sh == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+        a = __uint_as_float(r[0]);
+        b = __uint_as_float(r[1]);
+    } else {
+        const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+        a = __uint_as_float(r[0]);
+        b = __uint_as_float(r[1]);
+    }
+}
+
+template <int D, int KVDT>
+__global__ __launch_bounds__(256) void attn_mma_kernel(AttnArgs a) {
+    constexpr int HALF = D / 2;
+    constexpr int NCH = D / 8;               // 16-byte chunks per cache row
+    constexpr int DB = D / 32;               // k-blocks of the score products
+    constexpr int MB = D / 16;               // row blocks of O^T
+    constexpr int NU = AK * NCH / 256;       // chunks per thread per step (K and V each)
+    constexpr int QTW = 2;                   // query tiles per wave per pass
+    constexpr int VST = 40;                  // V^T row stride in elements (32 key slots + padding)
+    static_assert(NU >= 1 && AK * NCH % 256 == 0, "tile staging");
+    __shared__ __attribute__((aligned(16))) uint16_t ks[2][AK][D];   // key rows, chunk c at c ^ (key mod NCH)
+    __shared__ __attribute__((aligned(16))) uint16_t vt[2][D][VST];  // values transposed, key slots permuted
+    __shared__ int16_t stab[ACH];                                    // physical slot of each key of the chunk
+    __shared__ uint8_t smk[ACH];                                     // its mask byte
+
+    const int item = blockIdx.x, g = blockIdx.y, split = blockIdx.z;
+    const ItemDev it = a.meta.items[item];
+    const ReqDev rq = a.meta.reqs[it.req];
+    const int b = it.slot;
+    const int P = rq.P, n = rq.n;
+    const int L = P + n;
+    int split_len = max(ATTN_MIN_SPLIT, (L + a.nsplit_max - 1) / a.nsplit_max);
+    split_len = (split_len + KGROUPS - 1) / KGROUPS * KGROUPS;
+    const int nsplit = (L + split_len - 1) / split_len;
+    if (split >= nsplit) return;
+    const int j0 = split * split_len, j1 = min(L, j0 + split_len);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int ql = lane & 15, lg = lane >> 4;
+    const int Hq = a.Hq, Hkv = a.Hkv;
+    const int gs = Hq / Hkv;
+    const int R = gs * n;
+    const int nqt = (R + 15) / 16;
+    const size_t lstride = (size_t)rq.S * Hkv * rq.cap * D;
+    uint16_t* kl = rq.kc + (size_t)a.layer * lstride;
+    uint16_t* vl = rq.vc + (size_t)a.layer * lstride;
+    const uint8_t* mask = a.meta.masks + rq.mask_off + (size_t)b * rq.mask_len;
+    const int16_t* tab = rq.table + (size_t)b * rq.cap;
+    const int rowbase = rq.row0 + b * n;
+
+    // ---- one step's keys (chunk-relative key x0 + k): cache rows through the
+    // table, this forward's rows from q|k|v
+    u32x4 kreg[NU], vreg[NU];
+    int c0 = j0, c1 = j0;                                    // keys of the staged chunk
+    auto fetch = [&](int x0, bool append) {
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            const int q = tid + 256 * u, k = q / NCH, c = q % NCH;
+            const int x = min(x0 + k, ACH - 1), j = c0 + x0 + k;
+            kreg[u] = u32x4{0u, 0u, 0u, 0u};
+            vreg[u] = u32x4{0u, 0u, 0u, 0u};
+            if (j >= c1) continue;
+            const bool vis = smk[x] != 0;
+            if (j < P) {
+                if (vis) {
+                    const size_t off = (((size_t)stab[x] * Hkv + g) * rq.cap + j) * D + 8 * c;
+                    kreg[u] = *(const u32x4*)(kl + off);
+                    vreg[u] = *(const u32x4*)(vl + off);
+                }
+            } else {
+                const int i = j - P;
+                const int m = rowbase + i;
+                const int pos = a.meta.positions[m];
+                const float* krow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + g) * D;
+                const float* vrow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + Hkv + g) * D;
+                uint16_t kb[8], vb[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int d = 8 * c + e;
+                    const bool lo_half = d < HALF;
+                    const float x = krow[d];
+                    const float xp = lo_half ? krow[d + HALF] : krow[d - HALF];
+                    const float2 cs = a.rope[(size_t)pos * HALF + (lo_half ? d : d - HALF)];
+                    const float y = lo_half ? (x * cs.x - xp * cs.y) : (x * cs.x + xp * cs.y);
+                    kb[e] = kv_round<KVDT>(y);
+                    vb[e] = kv_round<KVDT>(vrow[d]);
+                }
+                u32x4 kk, vv;
+#pragma unroll
+                for (int w2 = 0; w2 < 4; ++w2) {
+                    kk[w2] = (uint32_t)kb[2 * w2] | ((uint32_t)kb[2 * w2 + 1] << 16);
+                    vv[w2] = (uint32_t)vb[2 * w2] | ((uint32_t)vb[2 * w2 + 1] << 16);
+                }
+                if (append) {                            // append: owner of row j writes it
+                    const size_t off = (((size_t)b * Hkv + g) * rq.cap + j) * D + 8 * c;
+                    *(u32x4*)(kl + off) = kk;
+                    *(u32x4*)(vl + off) = vv;
+                    if (a.layer == 0 && g == 0 && c == 0) rq.table[(size_t)b * rq.cap + j] = (int16_t)b;
+                }
+                if (vis) {
+                    kreg[u] = kk;
+                    vreg[u] = vv;
+                }
+            }
+        }
+    };
+    auto stash = [&](int buf) {
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+            const int q = tid + 256 * u, k = q / NCH, c = q % NCH;
+            *(u32x4*)&ks[buf][k][8 * (c ^ (k % NCH))] = kreg[u];
+            const int slot = 8 * ((k & 15) >> 2) + 4 * (k >> 4) + (k & 3);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) vt[buf][8 * c + e][slot] = (uint16_t)(vreg[u][e >> 1] >> (16 * (e & 1)));
+        }
+    };
+
+    for (int qg = 0; qg < nqt; qg += 4 * QTW) {
+        // ---- this wave's query tiles: rotated, scaled, split into rounded part and residual
+        u32x4 qh[QTW][DB], qr[QTW][DB];
+        int qtok[QTW];
+        float mrun[QTW], lsum[QTW];
+        f32x4_t o[QTW][MB];
+#pragma unroll
+        for (int u = 0; u < QTW; ++u) {
+            const int qt = qg + wave + 4 * u;
+            const int r = 16 * qt + ql;
+            const bool ok = qt < nqt && r < R;
+            const int i = ok ? r / gs : 0, h = g * gs + (ok ? r % gs : 0);
+            const int m = rowbase + i;
+            const int pos = a.meta.positions[m];
+            const float* qrow = a.qkv + (size_t)m * a.qkv_ld + (size_t)h * D;
+            qtok[u] = ok ? i : n;
+#pragma unroll
+            for (int ib = 0; ib < DB; ++ib) {
+                // dims d0 .. d0 + 7 lie in one rotary half: 16-byte loads of q, its partner and (cos, sin)
+                const int d0 = 32 * ib + 8 * lg;
+                const bool lo_half = d0 < HALF;
+                float xv[8], xpv[8], cv[8], sv[8];
+                if (ok) {
+                    const float4* q4 = (const float4*)(qrow + d0);
+                    const float4* p4 = (const float4*)(qrow + (lo_half ? d0 + HALF : d0 - HALF));
+                    const float4* r4 = (const float4*)(a.rope + (size_t)pos * HALF + (lo_half ? d0 : d0 - HALF));
+#pragma unroll
+                    for (int h2 = 0; h2 < 2; ++h2) {
+                        const float4 x4 = q4[h2], y4 = p4[h2];
+                        xv[4 * h2] = x4.x; xv[4 * h2 + 1] = x4.y; xv[4 * h2 + 2] = x4.z; xv[4 * h2 + 3] = x4.w;
+                        xpv[4 * h2] = y4.x; xpv[4 * h2 + 1] = y4.y; xpv[4 * h2 + 2] = y4.z; xpv[4 * h2 + 3] = y4.w;
+                    }
+#pragma unroll
+                    for (int h4 = 0; h4 < 4; ++h4) {
+                        const float4 c4 = r4[h4];
+                        cv[2 * h4] = c4.x; sv[2 * h4] = c4.y; cv[2 * h4 + 1] = c4.z; sv[2 * h4 + 1] = c4.w;
+                    }
+                }
+                uint16_t hb[8], rb[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    float y = 0.f;
+                    if (ok) y = (lo_half ? (xv[e] * cv[e] - xpv[e] * sv[e]) : (xv[e] * cv[e] + xpv[e] * sv[e])) * a.qscale;
+                    hb[e] = kv_round<KVDT>(y);
+                    rb[e] = kv_round<KVDT>(y - kv_float<KVDT>(hb[e]));
+                }
+#pragma unroll
+                for (int w2 = 0; w2 < 4; ++w2) {
+                    qh[u][ib][w2] = (uint32_t)hb[2 * w2] | ((uint32_t)hb[2 * w2 + 1] << 16);
+                    qr[u][ib][w2] = (uint32_t)rb[2 * w2] | ((uint32_t)rb[2 * w2 + 1] << 16);
+                }
+            }
+            mrun[u] = -INFINITY;
+            lsum[u] = 0.f;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) o[u][mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+
+        for (c0 = j0; c0 < j1; c0 += ACH) {
+        c1 = min(j1, c0 + ACH);
+        __syncthreads();                                     // the previous chunk's entries are no longer read
+        for (int x = tid; x < c1 - c0; x += 256) {
+            const int j = c0 + x;
+            smk[x] = mask[j];
+            stab[x] = j < P ? tab[j] : (int16_t)b;
+        }
+        __syncthreads();
+        const int nsteps = (c1 - c0 + AK - 1) / AK;
+        fetch(0, qg == 0);
+        stash(0);
+        __syncthreads();
+        for (int st = 0; st < nsteps; ++st) {
+            const int buf = st & 1;
+            if (st + 1 < nsteps) fetch((st + 1) * AK, qg == 0);   // next step's loads fly during this one
+            u32x4 ka[2][DB], va[MB];
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int ib = 0; ib < DB; ++ib) {
+                    const int k = 16 * t + ql, c = 4 * ib + lg;
+                    ka[t][ib] = *(const u32x4*)&ks[buf][k][8 * (c ^ (k % NCH))];
+                }
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) va[mb] = *(const u32x4*)&vt[buf][16 * mb + ql][8 * lg];
+            bool kvis[8];
+            int kidx[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int x = st * AK + ((e < 4) ? 4 * lg + e : 16 + 4 * lg + (e - 4));
+                kidx[e] = c0 + x;
+                kvis[e] = kidx[e] < c1 && smk[min(x, ACH - 1)] != 0;
+            }
+#pragma unroll
+            for (int u = 0; u < QTW; ++u) {
+                if (qg + wave + 4 * u >= nqt) continue;      // wave-uniform
+                f32x4_t s0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+#pragma unroll
+                for (int ib = 0; ib < DB; ++ib) {
+                    s0 = mma_kv<KVDT>(ka[0][ib], qh[u][ib], s0);
+                    s0 = mma_kv<KVDT>(ka[0][ib], qr[u][ib], s0);
+                    s1 = mma_kv<KVDT>(ka[1][ib], qh[u][ib], s1);
+                    s1 = mma_kv<KVDT>(ka[1][ib], qr[u][ib], s1);
+                }
+                float sv[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float x = e < 4 ? s0[e] : s1[e - 4];
+                    sv[e] = (kvis[e] && kidx[e] <= P + qtok[u]) ? x : -INFINITY;
+                }
+                float mx = sv[0];
+#pragma unroll
+                for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
+                float x0, x1;
+                lane_pair_k(mx, 16, x0, x1);
+                mx = fmaxf(x0, x1);
+                lane_pair_k(mx, 32, x0, x1);
+                mx = fmaxf(x0, x1);
+                const float mn = fmaxf(mrun[u], mx);
+                float corr = 1.f, pv[8];
+                if (mn == -INFINITY) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) pv[e] = 0.f;
+                } else {
+                    corr = exp2f(mrun[u] - mn);
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) pv[e] = exp2f(sv[e] - mn);
+                }
+                float ps = 0.f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) ps += pv[e];
+                lsum[u] = lsum[u] * corr + ps;
+                mrun[u] = mn;
+                u32x4 pb;
+#pragma unroll
+                for (int w2 = 0; w2 < 4; ++w2)
+                    pb[w2] = (uint32_t)kv_round<KVDT>(pv[2 * w2]) | ((uint32_t)kv_round<KVDT>(pv[2 * w2 + 1]) << 16);
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj) o[u][mb][jj] *= corr;
+                    o[u][mb] = mma_kv<KVDT>(va[mb], pb, o[u][mb]);
+                }
+            }
+            if (st + 1 < nsteps) stash(buf ^ 1);
+            __syncthreads();
+        }
+        }
+
+        // ---- this split's partial of each query vector: (max, sum, unnormalized output)
+#pragma unroll
+        for (int u = 0; u < QTW; ++u) {
+            const int qt = qg + wave + 4 * u;
+            if (qt >= nqt) continue;
+            float x0, x1, lt = lsum[u];
+            lane_pair_k(lt, 16, x0, x1);
+            lt = x0 + x1;
+            lane_pair_k(lt, 32, x0, x1);
+            lt = x0 + x1;
+            const int r = 16 * qt + ql;
+            if (r >= R) continue;
+            const int i = r / gs, h = g * gs + (r % gs);
+            const int m = rowbase + i;
+            float* pp = a.part + (((size_t)m * Hq + h) * a.nsplit_max + split) * (D + 2);
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) pp[2 + 16 * mb + 4 * lg + jj] = o[u][mb][jj];
+            if (lg == 0) {
+                pp[0] = mrun[u];
+                pp[1] = lt;
+            }
+        }
+    }
+}
+
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int rows_per_item_max, hipStream_t st) {
     const dim3 grid(a.meta.n_items, a.Hkv, a.nsplit_max), block(256);
     const dim3 mgrid(a.meta.M, a.Hq);
     const bool wide = rows_per_item_max > 4;
+    const bool bf = a.kv_dt == DT_BF16;
     if (head_dim == 128) {
-        if (wide) attn_kernel<128, 8><<<grid, block, 0, st>>>(a);
+        if (!a.vector_path) {
+            if (bf) attn_mma_kernel<128, DT_BF16><<<grid, block, 0, st>>>(a);
+            else attn_mma_kernel<128, DT_F16><<<grid, block, 0, st>>>(a);
+        } else if (wide) attn_kernel<128, 8><<<grid, block, 0, st>>>(a);
         else attn_kernel<128, 4><<<grid, block, 0, st>>>(a);
         attn_merge_kernel<128><<<mgrid, dim3(128), 0, st>>>(a);
     } else if (head_dim == 64) {
-        if (wide) attn_kernel<64, 8><<<grid, block, 0, st>>>(a);
+        if (!a.vector_path) {
+            if (bf) attn_mma_kernel<64, DT_BF16><<<grid, block, 0, st>>>(a);
+            else attn_mma_kernel<64, DT_F16><<<grid, block, 0, st>>>(a);
+        } else if (wide) attn_kernel<64, 8><<<grid, block, 0, st>>>(a);
         else attn_kernel<64, 4><<<grid, block, 0, st>>>(a);
         attn_merge_kernel<64><<<mgrid, dim3(64), 0, st>>>(a);
     } else {

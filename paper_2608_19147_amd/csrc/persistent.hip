@@ -710,8 +710,6 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
     const int total = (n0 + n1 + n2 + n3 + n4) * L;
     // The weight rows of one wave in one segment are contiguous in the row layout
     // (kc = 64 * CPL chunks per row), so a segment streams one block of 1 KB slots.
-    typedef __attribute__((address_space(4))) const PsLayer* layer_cptr;   // never written during the launch:
-    const layer_cptr layers = (layer_cptr)a.layers;                          // scalar loads
     // Stream state: segment gs of layer gl, gleft slots left in it.  In a weight
     // segment every slot but the last is issued by the fast path (gfast counts
     // them); the last one, the attention slots and the end of the stream take
@@ -734,19 +732,19 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         gleft = gs == 0 ? n0 : gs == 1 ? n1 : gs == 2 ? n2 : gs == 3 ? n3 : n4;
         gt = 0;
         gstride = (COL_F && gs == 4) ? (u64)a.kc_f * 16 : (u64)SK_SLOT;
-        if (gs == 0) gptr = layers[gl].qkv.w + (u64)rq_.first * a.kc_h * 16;
-        else if (gs == 2) gptr = layers[gl].o.w + (u64)ro_.first * a.kc_q * 16;
-        else if (gs == 3) gptr = layers[gl].gu.w + (u64)rg_.first * a.kc_h * 16;
+        if (gs == 0) gptr = a.wb[0] + gl * a.wl[0] + (u64)rq_.first * a.kc_h * 16;
+        else if (gs == 2) gptr = a.wb[1] + gl * a.wl[1] + (u64)ro_.first * a.kc_q * 16;
+        else if (gs == 3) gptr = a.wb[2] + gl * a.wl[2] + (u64)rg_.first * a.kc_h * 16;
         else if (gs == 4)
-            gptr = layers[gl].d.w + (COL_F  ? (u64)w * a.rpw_h * a.kc_f * 16 + (u64)cw * SK_SLOT
-                                     : XR_F ? (u64)ro_.first * a.kc_f * 16
-                                            : (u64)w * a.rpw_h * a.kc_f * 16 + (u64)ks0 * SK_SLOT);
+            gptr = a.wb[3] + gl * a.wl[3] +
+                   (COL_F  ? (u64)w * a.rpw_h * a.kc_f * 16 + (u64)cw * SK_SLOT
+                    : XR_F ? (u64)ro_.first * a.kc_f * 16
+                           : (u64)w * a.rpw_h * a.kc_f * 16 + (u64)ks0 * SK_SLOT);
         if (gs != 1) {
             gfast = gleft - 1;
             gleft = 1;
         }
-        asm volatile("" ::"s"(gptr));                       // the pointer's scalar load completes here, not at
-    };                                                      // every later refill
+    };
     const uint32_t lane16 = 16u * (uint32_t)lane;
     auto issue_general = [&](uint32_t dst) {
         if (gleft == 0) return;                             // past the end of the stream: nothing to load

@@ -67,6 +67,8 @@ struct Stage {
     int cpl_h = 0, cpl_q = 0, cpl_f = 0, kc_h = 0, kc_q = 0, kc_f = 0, ng_h = 0, ng_q = 0, ng_f = 0;
     std::vector<PsLayer> ps_host;
     PsLayer* ps_layers = nullptr;
+    uint8_t* ps_wb[4] = {nullptr, nullptr, nullptr, nullptr};   // code slabs per matrix kind (all layers)
+    size_t ps_wl[4] = {0, 0, 0, 0};                            // bytes per layer in each slab
     unsigned* err = nullptr;
     int ps_nwg = 0;
     int ps_rpw_qkv = 0, ps_rpw_h = 0, ps_rpw_gu = 0;    // rows per workgroup of the single-launch forward
@@ -74,6 +76,7 @@ struct Stage {
     unsigned* ll_x = nullptr;                                                                       // exchange buffers
     unsigned ll_epoch = 0;                              // flag numbers used so far
     bool ps_coop = true;                                // cooperative launch (STAGE_COOP=0: plain launch, for profilers)
+    int attn_vector = 0;                                // attention on the vector units (STAGE_ATTN_VECTOR=1)
     int gemm_min_rows = 2;                              // rows from which products use the matrix cores (STAGE_GEMM_MIN_ROWS)
     unsigned long long* trace = nullptr;   // phase stamps of the last persistent forward (STAGE_PS_TRACE=1)
     int prof_class = -1;
@@ -188,17 +191,27 @@ int upload_mat(Stage* st, DevMat& m, const QuantMatrix& q, int on_device, int ro
     return STAGE_OK;
 }
 
-int make_rows(Stage* st, PsMat& pm, int n, int kc, int ng) {
+// Row-layout storage of one matrix kind for all layers: codes in one slab
+// (layer l at l * n * kc * 16 bytes), scales in another; padding codes are
+// zero (0x88) and the scale slab has a tail so whole 1 KB blocks stay in bounds.
+int make_rows(Stage* st, int m, int n_layers, int n, int kc, int ng) {
     uint8_t* w;
     uint16_t* s;
-    int rc = st->alloc(&w, (size_t)n * kc * 16);
+    const size_t wl = (size_t)n * kc * 16, sl = (size_t)n * ng;
+    int rc = st->alloc(&w, wl * n_layers);
     if (rc) return rc;
-    rc = st->alloc(&s, (size_t)n * ng + SK_SLOT / 2);   // scale rows are read in whole 1 KB blocks
+    rc = st->alloc(&s, sl * n_layers + SK_SLOT / 2);
     if (rc) return rc;
-    HIP_TRY(hipMemset(w, 0x88, (size_t)n * kc * 16));
-    HIP_TRY(hipMemset(s, 0, ((size_t)n * ng + SK_SLOT / 2) * 2));
-    pm.w = w;
-    pm.s = s;
+    HIP_TRY(hipMemset(w, 0x88, wl * n_layers));
+    HIP_TRY(hipMemset(s, 0, (sl * n_layers + SK_SLOT / 2) * 2));
+    st->ps_wb[m] = w;
+    st->ps_wl[m] = wl;
+    for (int l = 0; l < n_layers; ++l) {
+        PsLayer& P = st->ps_host[l];
+        PsMat& pm = m == 0 ? P.qkv : m == 1 ? P.o : m == 2 ? P.gu : P.d;
+        pm.w = w + l * wl;
+        pm.s = s + l * sl;
+    }
     return STAGE_OK;
 }
 
@@ -351,12 +364,16 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         if (st->ps_ok) st->ps_host.resize(c.n_layers);
     }
     if (const char* e = std::getenv("STAGE_GEMM_MIN_ROWS")) st->gemm_min_rows = std::max(1, atoi(e));
+    if (const char* e = std::getenv("STAGE_ATTN_VECTOR")) st->attn_vector = atoi(e) != 0;
     for (int l = 0; l < c.n_layers; ++l) {
         LayerDev& L = st->layers[l];
         const LayerWeights& w = layers[l];
         PsLayer* P = st->ps_ok ? &st->ps_host[l] : nullptr;
-        if (P && ((rc = make_rows(st, P->qkv, nqkv, st->kc_h, st->ng_h)) || (rc = make_rows(st, P->o, H, st->kc_q, st->ng_q)) ||
-                  (rc = make_rows(st, P->gu, 2 * F, st->kc_h, st->ng_h)) || (rc = make_rows(st, P->d, H, st->kc_f, st->ng_f)))) {
+        if (P && l == 0 &&
+            ((rc = make_rows(st, 0, c.n_layers, nqkv, st->kc_h, st->ng_h)) ||
+             (rc = make_rows(st, 1, c.n_layers, H, st->kc_q, st->ng_q)) ||
+             (rc = make_rows(st, 2, c.n_layers, 2 * F, st->kc_h, st->ng_h)) ||
+             (rc = make_rows(st, 3, c.n_layers, H, st->kc_f, st->ng_f)))) {
             free_tmp();
             return cleanup(rc);
         }
@@ -898,6 +915,10 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     if (single) {
         PsArgs a{};
         a.layers = st->ps_layers;
+        for (int m = 0; m < 4; ++m) {
+            a.wb[m] = st->ps_wb[m];
+            a.wl[m] = st->ps_wl[m];
+        }
         a.n_layers = c.n_layers;
         a.H = H; a.Hq = Hq; a.Hkv = Hkv; a.F = F; a.QD = Hq * D; a.NQKV = nqkv;
         a.kc_h = st->kc_h; a.kc_q = st->kc_q; a.kc_f = st->kc_f;
@@ -999,6 +1020,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             // splits per (slot, kv head) follow the request's own length only (at least
             // ATTN_MIN_SPLIT keys each), so batch-mates never change a request's result
             a.nsplit_max = ATTN_MAX_SPLITS;
+            a.vector_path = st->attn_vector;
             if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, atoi(e)));
             HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, true, s));
             HIP_TRY(launch_attention(a, D, max_rows_item, s));
