@@ -1019,14 +1019,16 @@ __device__ __forceinline__ void lane_pair_k(float v, int sh, float& a, float& b)
     }
 }
 
-template <int D, int KVDT>
-__global__ __launch_bounds__(256) void attn_mma_kernel(AttnArgs a) {
+// QTW: query tiles per wave per pass (which wave computes a query vector, and
+// when, does not change its arithmetic).
+template <int D, int KVDT, int QTW>
+__global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArgs a) {
     constexpr int HALF = D / 2;
     constexpr int NCH = D / 8;               // 16-byte chunks per cache row
     constexpr int DB = D / 32;               // k-blocks of the score products
     constexpr int MB = D / 16;               // row blocks of O^T
     constexpr int NU = AK * NCH / 256;       // chunks per thread per step (K and V each)
-    constexpr int QTW = 2;                   // query tiles per wave per pass
+    constexpr int NS = ACH / 256;            // staged table entries per thread
     constexpr int VST = 40;                  // V^T row stride in elements (32 key slots + padding)
     static_assert(NU >= 1 && AK * NCH % 256 == 0, "tile staging");
     __shared__ __attribute__((aligned(16))) uint16_t ks[2][AK][D];   // key rows, chunk c at c ^ (key mod NCH)
@@ -1126,6 +1128,16 @@ __global__ __launch_bounds__(256) void attn_mma_kernel(AttnArgs a) {
         }
     };
 
+    // table entries and mask bytes of the first chunk: loaded with the queries, stored after
+    int16_t ptab[NS];
+    uint8_t pmsk[NS];
+#pragma unroll
+    for (int t2 = 0; t2 < NS; ++t2) {
+        const int j = j0 + tid + 256 * t2;
+        const bool in = j < min(j1, j0 + ACH);
+        pmsk[t2] = in ? mask[j] : 0;
+        ptab[t2] = (in && j < P) ? tab[j] : (int16_t)b;
+    }
     for (int qg = 0; qg < nqt; qg += 4 * QTW) {
         // ---- this wave's query tiles: rotated, scaled, split into rounded part and residual
         u32x4 qh[QTW][DB], qr[QTW][DB];
@@ -1187,10 +1199,18 @@ __global__ __launch_bounds__(256) void attn_mma_kernel(AttnArgs a) {
         for (c0 = j0; c0 < j1; c0 += ACH) {
         c1 = min(j1, c0 + ACH);
         __syncthreads();                                     // the previous chunk's entries are no longer read
-        for (int x = tid; x < c1 - c0; x += 256) {
-            const int j = c0 + x;
-            smk[x] = mask[j];
-            stab[x] = j < P ? tab[j] : (int16_t)b;
+        if (qg == 0 && c0 == j0) {
+#pragma unroll
+            for (int t2 = 0; t2 < NS; ++t2) {
+                smk[tid + 256 * t2] = pmsk[t2];
+                stab[tid + 256 * t2] = ptab[t2];
+            }
+        } else {
+            for (int x = tid; x < c1 - c0; x += 256) {
+                const int j = c0 + x;
+                smk[x] = mask[j];
+                stab[x] = j < P ? tab[j] : (int16_t)b;
+            }
         }
         __syncthreads();
         const int nsteps = (c1 - c0 + AK - 1) / AK;
@@ -1200,23 +1220,14 @@ __global__ __launch_bounds__(256) void attn_mma_kernel(AttnArgs a) {
         for (int st = 0; st < nsteps; ++st) {
             const int buf = st & 1;
             if (st + 1 < nsteps) fetch((st + 1) * AK, qg == 0);   // next step's loads fly during this one
-            u32x4 ka[2][DB], va[MB];
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int ib = 0; ib < DB; ++ib) {
-                    const int k = 16 * t + ql, c = 4 * ib + lg;
-                    ka[t][ib] = *(const u32x4*)&ks[buf][k][8 * (c ^ (k % NCH))];
-                }
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) va[mb] = *(const u32x4*)&vt[buf][16 * mb + ql][8 * lg];
-            bool kvis[8];
-            int kidx[8];
+            // the lane's 8 keys: step key 4 lg + e (e < 4) or 16 + 4 lg + e - 4; visible ones as bits
+            const int kbase = c0 + st * AK + 4 * lg;
+            uint32_t vbits = 0u;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const int x = st * AK + ((e < 4) ? 4 * lg + e : 16 + 4 * lg + (e - 4));
-                kidx[e] = c0 + x;
-                kvis[e] = kidx[e] < c1 && smk[min(x, ACH - 1)] != 0;
+                const int ko = (e < 4) ? e : 12 + e;
+                const int x = st * AK + 4 * lg + ko;
+                vbits |= ((kbase + ko < c1 && smk[min(x, ACH - 1)] != 0) ? 1u : 0u) << e;
             }
 #pragma unroll
             for (int u = 0; u < QTW; ++u) {
@@ -1224,16 +1235,21 @@ __global__ __launch_bounds__(256) void attn_mma_kernel(AttnArgs a) {
                 f32x4_t s0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, s1 = s0;
 #pragma unroll
                 for (int ib = 0; ib < DB; ++ib) {
-                    s0 = mma_kv<KVDT>(ka[0][ib], qh[u][ib], s0);
-                    s0 = mma_kv<KVDT>(ka[0][ib], qr[u][ib], s0);
-                    s1 = mma_kv<KVDT>(ka[1][ib], qh[u][ib], s1);
-                    s1 = mma_kv<KVDT>(ka[1][ib], qr[u][ib], s1);
+                    const int c = 4 * ib + lg;
+                    const u32x4 k0 = *(const u32x4*)&ks[buf][ql][8 * (c ^ (ql % NCH))];
+                    const u32x4 k1 = *(const u32x4*)&ks[buf][16 + ql][8 * (c ^ ((16 + ql) % NCH))];
+                    s0 = mma_kv<KVDT>(k0, qh[u][ib], s0);
+                    s0 = mma_kv<KVDT>(k0, qr[u][ib], s0);
+                    s1 = mma_kv<KVDT>(k1, qh[u][ib], s1);
+                    s1 = mma_kv<KVDT>(k1, qr[u][ib], s1);
                 }
+                const int last = P + qtok[u] - kbase;         // keys up to kbase + last are causal
                 float sv[8];
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
+                    const int ko = (e < 4) ? e : 12 + e;
                     const float x = e < 4 ? s0[e] : s1[e - 4];
-                    sv[e] = (kvis[e] && kidx[e] <= P + qtok[u]) ? x : -INFINITY;
+                    sv[e] = (((vbits >> e) & 1u) && ko <= last) ? x : -INFINITY;
                 }
                 float mx = sv[0];
 #pragma unroll
@@ -1264,9 +1280,10 @@ __global__ __launch_bounds__(256) void attn_mma_kernel(AttnArgs a) {
                     pb[w2] = (uint32_t)kv_round<KVDT>(pv[2 * w2]) | ((uint32_t)kv_round<KVDT>(pv[2 * w2 + 1]) << 16);
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb) {
+                    const u32x4 va = *(const u32x4*)&vt[buf][16 * mb + ql][8 * lg];
 #pragma unroll
                     for (int jj = 0; jj < 4; ++jj) o[u][mb][jj] *= corr;
-                    o[u][mb] = mma_kv<KVDT>(va[mb], pb, o[u][mb]);
+                    o[u][mb] = mma_kv<KVDT>(va, pb, o[u][mb]);
                 }
             }
             if (st + 1 < nsteps) stash(buf ^ 1);
@@ -1306,23 +1323,28 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int rows_per_item_m
     const dim3 mgrid(a.meta.M, a.Hq);
     const bool wide = rows_per_item_max > 4;
     const bool bf = a.kv_dt == DT_BF16;
+    const bool one = rows_per_item_max * (a.Hq / a.Hkv) <= 64;   // every item's query tiles: one per wave
+#define ATTN_MMA(D_)                                                                              \
+    do {                                                                                          \
+        if (bf && one) attn_mma_kernel<D_, DT_BF16, 1><<<grid, block, 0, st>>>(a);                \
+        else if (bf) attn_mma_kernel<D_, DT_BF16, 2><<<grid, block, 0, st>>>(a);                  \
+        else if (one) attn_mma_kernel<D_, DT_F16, 1><<<grid, block, 0, st>>>(a);                  \
+        else attn_mma_kernel<D_, DT_F16, 2><<<grid, block, 0, st>>>(a);                           \
+    } while (0)
     if (head_dim == 128) {
-        if (!a.vector_path) {
-            if (bf) attn_mma_kernel<128, DT_BF16><<<grid, block, 0, st>>>(a);
-            else attn_mma_kernel<128, DT_F16><<<grid, block, 0, st>>>(a);
-        } else if (wide) attn_kernel<128, 8><<<grid, block, 0, st>>>(a);
+        if (!a.vector_path) ATTN_MMA(128);
+        else if (wide) attn_kernel<128, 8><<<grid, block, 0, st>>>(a);
         else attn_kernel<128, 4><<<grid, block, 0, st>>>(a);
         attn_merge_kernel<128><<<mgrid, dim3(128), 0, st>>>(a);
     } else if (head_dim == 64) {
-        if (!a.vector_path) {
-            if (bf) attn_mma_kernel<64, DT_BF16><<<grid, block, 0, st>>>(a);
-            else attn_mma_kernel<64, DT_F16><<<grid, block, 0, st>>>(a);
-        } else if (wide) attn_kernel<64, 8><<<grid, block, 0, st>>>(a);
+        if (!a.vector_path) ATTN_MMA(64);
+        else if (wide) attn_kernel<64, 8><<<grid, block, 0, st>>>(a);
         else attn_kernel<64, 4><<<grid, block, 0, st>>>(a);
         attn_merge_kernel<64><<<mgrid, dim3(64), 0, st>>>(a);
     } else {
         return hipErrorInvalidValue;
     }
+#undef ATTN_MMA
     return hipGetLastError();
 }
 
