@@ -70,6 +70,15 @@ struct GemvArgs {
     float* ssq_out;                                // RESID: [M][ntiles]
     void* out_act; int out_act_dt; int out_act_ld; // RESID: optional copy in act dtype
     int n_valid;                                   // SWIGLU: F
+    // prepared-operand products (gemm_bp_kernel): input rows in matrix-core form
+    const uint16_t* bp_in; const float* bc_in;     // [M][kp] codes, [M][kp/32] corrections
+    const float* cb_in;                            // norm 1: scale c each row was prepared with
+    int norm;                                      // 0: none, 1: deferred RMSNorm (factor rs / c), 2: prepared normalized
+    int kp, kg;                                    // prepared row stride; groups of 128 k per wave
+    float* rs_out;                                 // norm 1: rs of each row, for the next residual product
+    uint16_t* bp_out; float* bc_out; float* cb_out;  // RESID / SWIGLU: the next product's input
+    const uint16_t* gamma_next; int gamma_next_dt; // RESID: RMSNorm weight of the next product
+    const float* rs_in;                            // RESID: scale c to prepare with (previous rs)
 };
 
 struct AttnArgs {
@@ -82,6 +91,7 @@ struct AttnArgs {
     float* part; unsigned* counters;
     int nsplit_max;
     int vector_path;         // 1: attn_kernel (vector units) instead of attn_mma_kernel
+    uint16_t* bp_out; float* bc_out; int kp;   // the attention output also in prepared form (o product input)
 };
 
 // ---- single-launch stage forward (persistent.hip)
@@ -194,6 +204,10 @@ hipError_t launch_repack(const uint8_t* q, const uint16_t* s, int n, int k, int 
 hipError_t launch_gemv(const GemvArgs& a, hipStream_t st);
 // Matrix-core product of 1..64 rows (group size 128); a.ksplit splits K.
 hipError_t launch_gemm(const GemvArgs& a, hipStream_t st);
+// Product of 2..64 prepared rows (group size 128); a.ksplit splits K, a.kg groups per wave.
+hipError_t launch_gemm_bp(const GemvArgs& a, hipStream_t st);
+hipError_t launch_bprep(const void* in, int in_dt, int in_ld, const uint16_t* gamma, int gamma_dt, int K, float eps,
+                        int M, uint16_t* bp, float* bc, int kp, float* rs_out, hipStream_t st);
 int gemm_groups_per_slice(int M);
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int rows_per_item_max, hipStream_t st);
 hipError_t launch_table_gather(const int16_t* src, int16_t* dst, const int* beam, int S, int cap, int P, hipStream_t st);

@@ -712,6 +712,326 @@ hipError_t launch_gemm(const GemvArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ prepared-operand products
+//
+// For 2..64 rows the input of every product is written once by the kernel that
+// produces it, in the form the matrix cores take: fp16 h with the values at
+// positions 2, 3, 6, 7 of every 8 k divided by 16 (they meet codes decoded as
+// 1024 + 16u), plus per 32 k the correction 1032 * sum(h at 0, 1, 4, 5) +
+// 72 * sum(h at 2, 3, 6, 7) that removes the decode offsets.  An RMSNorm input
+// is prepared as h = x * gamma * c with c the row's previous normalization
+// scale; the product multiplies its results by rs / c once rs is known
+// (RMSNorm(x) W^T = rs ((x * gamma) W^T)).
+
+__device__ __forceinline__ uint16_t bp_code(float h16, int k) { return f32_to_f16((k & 2) ? h16 * 0.0625f : h16); }
+__device__ __forceinline__ float bp_corr(float h16, int k) { return ((k & 2) ? 72.0f : 1032.0f) * h16; }
+
+// Sum over the 64 lanes of a wave, identical in every lane.
+__device__ __forceinline__ float wave_sum_all(float v) {
+    v = sum16(v);
+    uint32_t u = __float_as_uint(v);
+    const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    v = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    u = __float_as_uint(v);
+    const auto q = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+
+// Sum over aligned groups of 32 lanes, identical in every lane of the group.
+__device__ __forceinline__ float sum32_lanes(float v) {
+    v += dpp_f<0xB1>(v);              // lane ^ 1
+    v += dpp_f<0x4E>(v);              // lane ^ 2
+    v += dpp_f<0x124>(v);             // row_ror:4
+    v += dpp_f<0x128>(v);             // row_ror:8: the 16-lane row
+    const uint32_t u = __float_as_uint(v);
+    const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// One element of a prepared row: lanes 32 c .. 32 c + 31 of a wave hold k = 32 c' + (lane mod 32)
+// of one row (valid = k < K); writes the code and, from lane 0 of the 32, the chunk's correction.
+__device__ __forceinline__ void bp_put(uint16_t* bp, float* bc, int kp, int m, int k, float h, bool valid) {
+    const float h16 = valid ? f16_to_f32(f32_to_f16(h)) : 0.f;
+    const float cs = sum32_lanes(valid ? bp_corr(h16, k) : 0.f);
+    if (valid) bp[(size_t)m * kp + k] = bp_code(h16, k);
+    if (valid && (k & 31) == 0) bc[(size_t)m * (kp / 32) + (k >> 5)] = cs;
+}
+
+// First q|k|v input of a forward: RMSNorm of the stage input row m, fully
+// normalized (c = rs; the product's factor is 1); rs also goes to rs_out for
+// the residual product that prepares the next input.
+__global__ __launch_bounds__(256) void bprep_kernel(const void* in, int in_dt, int in_ld, const uint16_t* gamma,
+                                                    int gamma_dt, int K, float eps, uint16_t* bp, float* bc, int kp,
+                                                    float* rs_out) {
+    __shared__ float red[4];
+    const int m = blockIdx.x, tid = threadIdx.x;
+    float ss = 0.f;
+    for (int k = tid; k < K; k += 256) {
+        const float v = load_val(in, in_dt, (size_t)m * in_ld + k);
+        ss += v * v;
+    }
+    ss = wave_sum_all(ss);
+    if ((tid & 63) == 0) red[tid >> 6] = ss;
+    __syncthreads();
+    const float rs = rsqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)K + eps);
+    for (int k0 = 0; k0 < K; k0 += 256) {
+        const int k = k0 + tid;
+        const bool ok = k < K;
+        const float h = ok ? load_val(in, in_dt, (size_t)m * in_ld + k) * rs * half_bits_to_f32(gamma[k], gamma_dt) : 0.f;
+        bp_put(bp, bc, kp, m, k, h, ok);
+    }
+    if (tid == 0) rs_out[m] = rs;
+}
+
+// Product of the prepared input with one matrix: a workgroup's 4 waves take
+// one 64-row tile and 4 consecutive ranges of a.kg groups of 128 k; blockIdx.y
+// is the split of K (fixed per matrix, so results do not depend on M).  A lane
+// loads 16 bytes of codes per row block and group (chunk 4 gi + lane / 16 of row
+// 16 rt + lane mod 16): dword i of it is the A operand of the group's i-th
+// product, whose k are 32 (4 gi + lane / 16) + 8 i + e; the B operand of that
+// product is read from the prepared row at the same k.
+template <int NCB>
+__global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs a) {
+    constexpr int MP = 16 * NCB;
+    constexpr int NV = MP * 64 / 256;
+    __shared__ float red[4][MP][65];
+    __shared__ float fs[64];
+    __shared__ int last_s;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int l16 = lane & 15, lg = lane >> 4;
+    const int t = blockIdx.x, s = blockIdx.y;
+    const PackedMat W = a.W;
+    const int M = a.M, K = W.k;
+    const int g0 = (4 * s + w) * a.kg, g1 = min(W.ngroups, g0 + a.kg);
+    const int kc = a.kp / 32;
+    uint32_t magic = 0x64006400u;
+    asm volatile("" : "+v"(magic));
+
+    auto ldw = [&](int gi, u32x4 (&wv)[4], u32x2 (&sv)[4]) {
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+            wv[rt] = __builtin_nontemporal_load(
+                (const u32x4*)(W.w + (((size_t)t * W.nchunk + 4 * gi + lg) * 64 + 16 * rt + l16) * 16));
+            sv[rt] = *(const u32x2*)(W.s + ((size_t)t * W.ngroups + gi) * 64 + 16 * rt + 4 * lg);
+        }
+    };
+    auto ldb = [&](int gi, u32x4 (&bv)[NCB][4], float (&cv)[NCB]) {
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+            const int m = 16 * cb + l16;
+            const uint16_t* row = a.bp_in + (size_t)m * a.kp;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int k = 128 * gi + 32 * lg + 8 * i;
+                bv[cb][i] = k < K ? *(const u32x4*)(row + k) : u32x4{0u, 0u, 0u, 0u};
+            }
+            const float4 c4 = *(const float4*)(a.bc_in + (size_t)m * kc + 4 * gi);
+            const int kb = 128 * gi;
+            cv[cb] = ((kb < K ? c4.x : 0.f) + (kb + 32 < K ? c4.y : 0.f)) + ((kb + 64 < K ? c4.z : 0.f) + (kb + 96 < K ? c4.w : 0.f));
+        }
+    };
+
+    f32x4_t acc[4][NCB];
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) acc[rt][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (g0 < g1) {
+        u32x4 wv[4], bv[NCB][4];
+        u32x2 sv[4];
+        float cv[NCB];
+        ldw(g0, wv, sv);
+        ldb(g0, bv, cv);
+        for (int gi = g0; gi < g1; ++gi) {
+            const bool more = gi + 1 < g1;
+            u32x4 wn[4], bn[NCB][4];
+            u32x2 sn[4];
+            float cn[NCB];
+            if (more) {                                  // the next group's loads fly during this one
+                ldw(gi + 1, wn, sn);
+                ldb(gi + 1, bn, cn);
+            }
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt) {
+                half8_t A[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t x = wv[rt][i], y = x >> 8;
+                    u32x4 av;
+                    av[0] = bfi_u32(0x000F000Fu, x, magic);
+                    av[1] = bfi_u32(0x00F000F0u, x, magic);
+                    av[2] = bfi_u32(0x000F000Fu, y, magic);
+                    av[3] = bfi_u32(0x00F000F0u, y, magic);
+                    A[i] = __builtin_bit_cast(half8_t, av);
+                }
+                float scl[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t h = sv[rt][j >> 1];
+                    scl[j] = f16_to_f32((uint16_t)((j & 1) ? (h >> 16) : (h & 0xFFFFu)));
+                }
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) {
+                    f32x4_t c = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(A[i], __builtin_bit_cast(half8_t, bv[cb][i]), c, 0, 0, 0);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[rt][cb][j] = __builtin_fmaf(scl[j], c[j] - cv[cb], acc[rt][cb][j]);
+                }
+            }
+            if (more) {
+#pragma unroll
+                for (int rt = 0; rt < 4; ++rt) {
+                    wv[rt] = wn[rt];
+                    sv[rt] = sn[rt];
+                }
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) {
+                    cv[cb] = cn[cb];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) bv[cb][i] = bn[cb][i];
+                }
+            }
+        }
+    }
+    // ---- the 4 waves' sums of each output (lane: rows 16 rt + 4 lg + j of column 16 cb + l16), in wave order
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) red[w][16 * cb + l16][16 * rt + 4 * lg + j] = acc[rt][cb][j];
+    __syncthreads();
+    float vals[NV];
+#pragma unroll
+    for (int q = 0; q < NV; ++q) {
+        const int idx = tid + 256 * q, m = idx >> 6, r = idx & 63;
+        vals[q] = (red[0][m][r] + red[1][m][r]) + (red[2][m][r] + red[3][m][r]);
+    }
+
+    // ---- split-K: the last workgroup of the tile sums every split in split order
+    if (a.ksplit > 1) {
+        const int ldp = W.ntiles * 64;
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
+            const int idx = tid + 256 * q;
+            if (idx < M * 64)
+                store_coherent(&a.partial[((size_t)s * M + (idx >> 6)) * ldp + t * 64 + (idx & 63)], vals[q]);
+        }
+        if (!last_arrival(&a.counters[t], (unsigned)a.ksplit, &last_s)) return;
+        const size_t stride = (size_t)M * ldp;
+#pragma unroll
+        for (int q = 0; q < NV; ++q) vals[q] = 0.f;
+        for (int s0 = 0; s0 < a.ksplit; s0 += 4) {
+            float b4[NV][4];
+#pragma unroll
+            for (int q = 0; q < NV; ++q) {
+                const int idx = tid + 256 * q;
+                const float* pp = &a.partial[(size_t)(idx >> 6) * ldp + t * 64 + (idx & 63)];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    b4[q][e] = (idx < M * 64 && s0 + e < a.ksplit) ? load_coherent(pp + (s0 + e) * stride) : 0.f;
+            }
+#pragma unroll
+            for (int q = 0; q < NV; ++q)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) vals[q] += b4[q][e];
+        }
+    }
+
+    // ---- factor of each row: rs / c for a deferred RMSNorm input, else 1
+    if (tid < 64) {
+        float f = 1.f;
+        if (a.norm == 1 && tid < M) {
+            float ss = 0.f;
+            for (int tt = 0; tt < a.ssq_tiles; ++tt) ss += a.ssq_in[(size_t)tid * a.ssq_tiles + tt];
+            const float rs = rsqrtf(ss / (float)K + a.eps);
+            f = rs / a.cb_in[tid];
+            if (t == 0 && a.rs_out) a.rs_out[tid] = rs;
+        }
+        fs[tid] = f;
+    }
+    __syncthreads();
+
+    // ---- epilogue
+    if (a.epi == EPI_STORE) {
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
+            const int idx = tid + 256 * q;
+            if (idx < M * 64) {
+                const int m = idx >> 6, n = t * 64 + (idx & 63);
+                if (n < W.n) a.out[(size_t)m * a.out_ld + n] = vals[q] * fs[m];
+            }
+        }
+    } else if (a.epi == EPI_RESID) {
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
+            const int idx = tid + 256 * q;
+            const int m = idx >> 6, r = idx & 63;                     // one row per wave: whole waves take part
+            const int n = t * 64 + r;
+            const bool ok = m < M && n < W.n;
+            float xn = 0.f;
+            if (ok) {
+                xn = load_val(a.resid, a.resid_dt, (size_t)m * a.resid_ld + n) + vals[q] * fs[m];
+                a.out[(size_t)m * a.out_ld + n] = xn;
+                if (a.out_act) ((uint16_t*)a.out_act)[(size_t)m * a.out_act_ld + n] = to_half_bits(xn, a.out_act_dt);
+            }
+            if (m < M) red[0][m][r] = xn * xn;
+            if (a.bp_out && m < M) {                                    // the next product's input
+                const float c = a.rs_in[m];
+                const float h = ok ? xn * half_bits_to_f32(a.gamma_next[n], a.gamma_next_dt) * c : 0.f;
+                bp_put(a.bp_out, a.bc_out, a.kp, m, n, h, ok);
+                if (t == 0 && r == 0) a.cb_out[m] = c;
+            }
+        }
+        __syncthreads();
+        if (a.ssq_out && tid < M) {
+            float ss = 0.f;
+            for (int r = 0; r < 64; ++r) ss += red[0][tid][r];
+            a.ssq_out[(size_t)tid * W.ntiles + t] = ss;
+        }
+    } else {  // EPI_SWIGLU: rows 0..31 of the tile are gate rows, 32..63 the matching up rows
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
+            const int idx = tid + 256 * q;
+            if (idx < M * 64) red[0][idx >> 6][idx & 63] = vals[q] * fs[idx >> 6];
+        }
+        __syncthreads();
+        for (int i0 = 0; i0 < MP * 32; i0 += 256) {                    // whole waves: two rows each
+            const int idx = i0 + tid;
+            const int m = idx >> 5, r = idx & 31;
+            const int f = t * 32 + r;
+            const bool ok = m < M && f < a.n_valid;
+            float y = 0.f;
+            if (ok) {
+                const float gt = red[0][m][r], up = red[0][m][r + 32];
+                y = (gt / (1.0f + expf(-gt))) * up;
+                a.out[(size_t)m * a.out_ld + f] = y;
+            }
+            if (a.bp_out && m < M) bp_put(a.bp_out, a.bc_out, a.kp, m, f, y, ok);
+        }
+    }
+}
+
+hipError_t launch_gemm_bp(const GemvArgs& a, hipStream_t st) {
+    if (a.M < 1 || a.M > 64 || a.W.gchunks != 4 || a.kg < 1 || a.kp % 128) return hipErrorInvalidValue;
+    const dim3 grid(a.W.ntiles, a.ksplit), block(256);
+    switch ((a.M + 15) / 16) {
+        case 1: gemm_bp_kernel<1><<<grid, block, 0, st>>>(a); break;
+        case 2: gemm_bp_kernel<2><<<grid, block, 0, st>>>(a); break;
+        case 3: gemm_bp_kernel<3><<<grid, block, 0, st>>>(a); break;
+        default: gemm_bp_kernel<4><<<grid, block, 0, st>>>(a); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_bprep(const void* in, int in_dt, int in_ld, const uint16_t* gamma, int gamma_dt, int K, float eps,
+                        int M, uint16_t* bp, float* bc, int kp, float* rs_out, hipStream_t st) {
+    bprep_kernel<<<M, 256, 0, st>>>(in, in_dt, in_ld, gamma, gamma_dt, K, eps, bp, bc, kp, rs_out);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ attention
 
 // Rows [j0, j1) of one split are processed in blocks of ABLK keys whose mask
@@ -972,6 +1292,7 @@ __global__ __launch_bounds__(D) void attn_merge_kernel(AttnArgs a) {
     float O = 0.f;
     for (int s2 = 0; s2 < nsplit; ++s2) O += pp[(size_t)s2 * (D + 2) + 2 + d] * wgt[s2];
     a.out[(size_t)m * a.out_ld + (size_t)h * D + d] = O * inv_s;
+    if (a.bp_out) bp_put(a.bp_out, a.bc_out, a.kp, m, h * D + d, O * inv_s, true);   // the o product's input
 }
 
 // ------------------------------------------------------------------ matrix-core attention

@@ -32,7 +32,19 @@ constexpr int META_RING = 4;
 struct DevMat {
     PackedMat pm;
     int ksplit = 1, cps = 1;
+    int bp_split = 1, bp_kg = 1;   // prepared-operand product: splits of K, groups of 128 k per wave
 };
+
+// K split of a prepared-operand product (a function of the matrix only): about
+// 512 workgroups of 4 waves, each wave a range of whole groups.
+void bp_plan(DevMat& m) {
+    const int ng = m.pm.ngroups, nt = m.pm.ntiles;
+    int S = std::max(1, (512 + nt - 1) / nt);
+    const int kg = std::max(1, (ng + 4 * S - 1) / (4 * S));
+    S = (ng + 4 * kg - 1) / (4 * kg);
+    m.bp_split = S;
+    m.bp_kg = kg;
+}
 
 struct LayerDev {
     DevMat qkv, o, gu, d;
@@ -55,6 +67,13 @@ struct Stage {
     float *x = nullptr, *qkv = nullptr, *attn = nullptr, *act = nullptr, *gpart = nullptr, *apart = nullptr, *ssq = nullptr;
     unsigned *gcnt = nullptr, *acnt = nullptr;
     int ntiles_h = 0;
+    // prepared inputs of the matrix-core products (2..64 rows), double-buffered
+    bool bp_ok = false;
+    int kp = 0;                                        // row stride: max K rounded up to 128
+    uint16_t* bp[2] = {nullptr, nullptr};              // [MAX_ROWS][kp] codes
+    float* bc[2] = {nullptr, nullptr};                 // [MAX_ROWS][kp / 32] corrections
+    float* cbf[2] = {nullptr, nullptr};                // [MAX_ROWS] scale each row was prepared with
+    float* rsb = nullptr;                              // [MAX_ROWS] rs of the last normalization
     uint8_t* meta_dev = nullptr;
     size_t meta_cap = 0;
     uint8_t* meta_host[META_RING] = {};
@@ -442,12 +461,27 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
     st->ntiles_h = (H + 63) / 64;
     size_t gpart = 0;
     unsigned max_tiles = 0;
+    st->bp_ok = true;
     for (auto& L : st->layers)
         for (DevMat* m : {&L.qkv, &L.o, &L.gu, &L.d}) {
+            bp_plan(*m);
+            st->bp_ok = st->bp_ok && m->pm.gchunks == 4 && m->pm.k % 8 == 0;
             gpart = std::max(gpart, (size_t)m->ksplit * GEMV_MAX_M * m->pm.ntiles * 64);
             gpart = std::max(gpart, (size_t)gemm_split(*m) * MAX_ROWS * m->pm.ntiles * 64);
+            gpart = std::max(gpart, (size_t)m->bp_split * MAX_ROWS * m->pm.ntiles * 64);
             max_tiles = std::max<unsigned>(max_tiles, m->pm.ntiles);
         }
+    st->kp = (std::max(H, std::max(QD, F)) + 127) / 128 * 128;
+    for (int i = 0; i < 2; ++i)
+        if ((rc = st->alloc(&st->bp[i], (size_t)MAX_ROWS * st->kp)) || (rc = st->alloc(&st->bc[i], (size_t)MAX_ROWS * st->kp / 32)) ||
+            (rc = st->alloc(&st->cbf[i], (size_t)MAX_ROWS)))
+            return cleanup(rc);
+    if ((rc = st->alloc(&st->rsb, (size_t)MAX_ROWS))) return cleanup(rc);
+    for (int i = 0; i < 2; ++i)
+        if (hipMemset(st->bp[i], 0, (size_t)MAX_ROWS * st->kp * 2) != hipSuccess ||
+            hipMemset(st->bc[i], 0, (size_t)MAX_ROWS * st->kp / 32 * 4) != hipSuccess ||
+            hipMemset(st->cbf[i], 0, (size_t)MAX_ROWS * 4) != hipSuccess)
+            return cleanup(fail(STAGE_E_HIP, "workspace init failed"));
     if ((rc = st->alloc(&st->x, (size_t)MAX_ROWS * H)) || (rc = st->alloc(&st->qkv, (size_t)MAX_ROWS * nqkv)) ||
         (rc = st->alloc(&st->attn, (size_t)MAX_ROWS * QD)) || (rc = st->alloc(&st->act, (size_t)MAX_ROWS * F)) ||
         (rc = st->alloc(&st->ssq, (size_t)MAX_ROWS * st->ntiles_h)) || (rc = st->alloc(&st->gpart, gpart)) ||
@@ -979,11 +1013,55 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         return hipSuccess;
     };
 
+    // 2..64 rows: each product reads its input prepared by the kernel before it
+    const bool use_bp = st->bp_ok && M >= st->gemm_min_rows && M <= MAX_ROWS;
+    int bcur = 0;                                           // buffer holding the next product's input
+    auto bp_in = [&](GemvArgs& a, int norm) {
+        a.bp_in = st->bp[bcur];
+        a.bc_in = st->bc[bcur];
+        a.cb_in = st->cbf[bcur];
+        a.norm = norm;
+    };
+    auto bp_out = [&](GemvArgs& a) {
+        a.bp_out = st->bp[1 - bcur];
+        a.bc_out = st->bc[1 - bcur];
+        a.cb_out = st->cbf[1 - bcur];
+    };
+    auto run_bp = [&](const DevMat& m, GemvArgs a) -> hipError_t {
+        a.W = m.pm;
+        a.M = M;
+        a.ksplit = m.bp_split;
+        a.kg = m.bp_kg;
+        a.kp = st->kp;
+        a.partial = st->gpart;
+        a.counters = st->gcnt;
+        return launch_gemm_bp(a, s);
+    };
+
     for (int l = 0; l < c.n_layers; ++l) {
         const LayerDev& Ld = st->layers[l];
         const bool first = (l == 0), last = (l == c.n_layers - 1);
         // q|k|v = RMSNorm(x) W_qkv^T
-        {
+        if (use_bp) {
+            GemvArgs a{};
+            a.eps = c.rms_eps;
+            a.ssq_in = st->ssq;
+            a.ssq_tiles = st->ntiles_h;
+            a.epi = EPI_STORE;
+            a.out = st->qkv;
+            a.out_ld = nqkv;
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_QKV, true, s));
+            if (first) {
+                HIP_TRY(launch_bprep(hidden_in, act_dt, H, Ld.attn_norm, act_dt, H, c.rms_eps, M, st->bp[bcur], st->bc[bcur],
+                                     st->kp, st->rsb, s));
+                bp_in(a, 2);
+            } else {
+                bp_in(a, 1);
+                a.rs_out = st->rsb;
+            }
+            HIP_TRY(run_bp(Ld.qkv, a));
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_QKV, false, s));
+        } else {
             GemvArgs a{};
             a.in = first ? hidden_in : (const void*)st->x;
             a.in_dt = first ? act_dt : DT_F32;
@@ -1022,9 +1100,15 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             a.nsplit_max = ATTN_MAX_SPLITS;
             a.vector_path = st->attn_vector;
             if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, atoi(e)));
+            if (use_bp) {
+                a.bp_out = st->bp[1 - bcur];
+                a.bc_out = st->bc[1 - bcur];
+                a.kp = st->kp;
+            }
             HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, true, s));
             HIP_TRY(launch_attention(a, D, max_rows_item, s));
             HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, false, s));
+            if (use_bp) bcur = 1 - bcur;
         }
         // x = residual + o W_o^T
         {
@@ -1041,7 +1125,17 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             a.resid_ld = H;
             a.ssq_out = st->ssq;
             HIP_TRY(prof_mark(st, STAGE_KERNEL_OPROJ, true, s));
-            HIP_TRY(run_gemv(Ld.o, a, Hq * D, H, H, 4, first ? 2 : 4));
+            if (use_bp) {                                   // also prepares RMSNorm_ffn's input (c = rs_attn)
+                bp_in(a, 0);
+                bp_out(a);
+                a.gamma_next = Ld.ffn_norm;
+                a.gamma_next_dt = act_dt;
+                a.rs_in = st->rsb;
+                HIP_TRY(run_bp(Ld.o, a));
+                bcur = 1 - bcur;
+            } else {
+                HIP_TRY(run_gemv(Ld.o, a, Hq * D, H, H, 4, first ? 2 : 4));
+            }
             HIP_TRY(prof_mark(st, STAGE_KERNEL_OPROJ, false, s));
         }
         // act = silu(h2 W_g^T) * (h2 W_u^T), h2 = RMSNorm(x)
@@ -1061,7 +1155,15 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             a.out_ld = F;
             a.n_valid = F;
             HIP_TRY(prof_mark(st, STAGE_KERNEL_GATEUP, true, s));
-            HIP_TRY(run_gemv(Ld.gu, a, H, F, 0, 4, 0));
+            if (use_bp) {                                   // also prepares the down product's input
+                bp_in(a, 1);
+                bp_out(a);
+                a.rs_out = st->rsb;
+                HIP_TRY(run_bp(Ld.gu, a));
+                bcur = 1 - bcur;
+            } else {
+                HIP_TRY(run_gemv(Ld.gu, a, H, F, 0, 4, 0));
+            }
             HIP_TRY(prof_mark(st, STAGE_KERNEL_GATEUP, false, s));
         }
         // x = x + act W_d^T  (last layer also writes hidden_out)
@@ -1084,7 +1186,19 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
                 a.out_act_ld = H;
             }
             HIP_TRY(prof_mark(st, STAGE_KERNEL_DOWN, true, s));
-            HIP_TRY(run_gemv(Ld.d, a, F, H, H, 4, 4));
+            if (use_bp) {                                   // also prepares the next layer's q|k|v input (c = rs_ffn)
+                bp_in(a, 0);
+                if (!last) {
+                    bp_out(a);
+                    a.gamma_next = st->layers[l + 1].attn_norm;
+                    a.gamma_next_dt = act_dt;
+                    a.rs_in = st->rsb;
+                }
+                HIP_TRY(run_bp(Ld.d, a));
+                if (!last) bcur = 1 - bcur;
+            } else {
+                HIP_TRY(run_gemv(Ld.d, a, F, H, H, 4, 4));
+            }
             HIP_TRY(prof_mark(st, STAGE_KERNEL_DOWN, false, s));
         }
     }
