@@ -763,22 +763,27 @@ __device__ __forceinline__ void bp_put(uint16_t* bp, float* bc, int kp, int m, i
 __global__ __launch_bounds__(256) void bprep_kernel(const void* in, int in_dt, int in_ld, const uint16_t* gamma,
                                                     int gamma_dt, int K, float eps, uint16_t* bp, float* bc, int kp,
                                                     float* rs_out) {
+    constexpr int NPT = 32;                              // values per thread held in registers: K <= 8192
     __shared__ float red[4];
     const int m = blockIdx.x, tid = threadIdx.x;
-    float ss = 0.f;
-    for (int k = tid; k < K; k += 256) {
-        const float v = load_val(in, in_dt, (size_t)m * in_ld + k);
-        ss += v * v;
+    float v[NPT], gm[NPT];
+#pragma unroll
+    for (int i = 0; i < NPT; ++i) {                      // every load issued before any is used
+        const int k = tid + 256 * i;
+        v[i] = k < K ? load_val(in, in_dt, (size_t)m * in_ld + k) : 0.f;
+        gm[i] = k < K ? half_bits_to_f32(gamma[k], gamma_dt) : 0.f;
     }
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < NPT; ++i) ss += v[i] * v[i];
     ss = wave_sum_all(ss);
     if ((tid & 63) == 0) red[tid >> 6] = ss;
     __syncthreads();
     const float rs = rsqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)K + eps);
-    for (int k0 = 0; k0 < K; k0 += 256) {
-        const int k = k0 + tid;
-        const bool ok = k < K;
-        const float h = ok ? load_val(in, in_dt, (size_t)m * in_ld + k) * rs * half_bits_to_f32(gamma[k], gamma_dt) : 0.f;
-        bp_put(bp, bc, kp, m, k, h, ok);
+#pragma unroll
+    for (int i = 0; i < NPT; ++i) {
+        const int k = tid + 256 * i;
+        if (256 * i < K) bp_put(bp, bc, kp, m, k, v[i] * rs * gm[i], k < K);   // whole 32-lane groups
     }
     if (tid == 0) rs_out[m] = rs;
 }
@@ -821,9 +826,11 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
             const int m = 16 * cb + l16;
             const uint16_t* row = a.bp_in + (size_t)m * a.kp;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < 4; ++i) {                // rows are kp >= 128 ngroups long: load, then drop k >= K
                 const int k = 128 * gi + 32 * lg + 8 * i;
-                bv[cb][i] = k < K ? *(const u32x4*)(row + k) : u32x4{0u, 0u, 0u, 0u};
+                const u32x4 v = *(const u32x4*)(row + k);
+                const bool in = k < K;
+                bv[cb][i] = u32x4{in ? v[0] : 0u, in ? v[1] : 0u, in ? v[2] : 0u, in ? v[3] : 0u};
             }
             const float4 c4 = *(const float4*)(a.bc_in + (size_t)m * kc + 4 * gi);
             const int kb = 128 * gi;
@@ -836,63 +843,59 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
     for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) acc[rt][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // Two register sets, each the codes, scales and prepared operand of one group:
+    // while one group computes, the next one's loads are in flight.  The loads
+    // are issued unconditionally (the group index is clamped to the wave's last;
+    // a repeated group is simply not computed), so no branch sits between a load
+    // and its use and the compiler waits for exactly the loads each product needs.
+    u32x4 w0[4], w1[4], b0[NCB][4], b1[NCB][4];
+    u32x2 s0[4], s1[4];
+    float c0[NCB], c1[NCB];
+    auto compute = [&](const u32x4 (&wv)[4], const u32x2 (&sv)[4], const u32x4 (&bv)[NCB][4], const float (&cv)[NCB]) {
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+            half8_t A[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t x = wv[rt][i], y = x >> 8;
+                u32x4 av;
+                av[0] = bfi_u32(0x000F000Fu, x, magic);
+                av[1] = bfi_u32(0x00F000F0u, x, magic);
+                av[2] = bfi_u32(0x000F000Fu, y, magic);
+                av[3] = bfi_u32(0x00F000F0u, y, magic);
+                A[i] = __builtin_bit_cast(half8_t, av);
+            }
+            float scl[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t h = sv[rt][j >> 1];
+                scl[j] = f16_to_f32((uint16_t)((j & 1) ? (h >> 16) : (h & 0xFFFFu)));
+            }
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) {
+                f32x4_t c = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(A[i], __builtin_bit_cast(half8_t, bv[cb][i]), c, 0, 0, 0);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[rt][cb][j] = __builtin_fmaf(scl[j], c[j] - cv[cb], acc[rt][cb][j]);
+            }
+        }
+    };
     if (g0 < g1) {
-        u32x4 wv[4], bv[NCB][4];
-        u32x2 sv[4];
-        float cv[NCB];
-        ldw(g0, wv, sv);
-        ldb(g0, bv, cv);
-        for (int gi = g0; gi < g1; ++gi) {
-            const bool more = gi + 1 < g1;
-            u32x4 wn[4], bn[NCB][4];
-            u32x2 sn[4];
-            float cn[NCB];
-            if (more) {                                  // the next group's loads fly during this one
-                ldw(gi + 1, wn, sn);
-                ldb(gi + 1, bn, cn);
-            }
-#pragma unroll
-            for (int rt = 0; rt < 4; ++rt) {
-                half8_t A[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const uint32_t x = wv[rt][i], y = x >> 8;
-                    u32x4 av;
-                    av[0] = bfi_u32(0x000F000Fu, x, magic);
-                    av[1] = bfi_u32(0x00F000F0u, x, magic);
-                    av[2] = bfi_u32(0x000F000Fu, y, magic);
-                    av[3] = bfi_u32(0x00F000F0u, y, magic);
-                    A[i] = __builtin_bit_cast(half8_t, av);
-                }
-                float scl[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const uint32_t h = sv[rt][j >> 1];
-                    scl[j] = f16_to_f32((uint16_t)((j & 1) ? (h >> 16) : (h & 0xFFFFu)));
-                }
-#pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) {
-                    f32x4_t c = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        c = __builtin_amdgcn_mfma_f32_16x16x32_f16(A[i], __builtin_bit_cast(half8_t, bv[cb][i]), c, 0, 0, 0);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) acc[rt][cb][j] = __builtin_fmaf(scl[j], c[j] - cv[cb], acc[rt][cb][j]);
-                }
-            }
-            if (more) {
-#pragma unroll
-                for (int rt = 0; rt < 4; ++rt) {
-                    wv[rt] = wn[rt];
-                    sv[rt] = sn[rt];
-                }
-#pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) {
-                    cv[cb] = cn[cb];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) bv[cb][i] = bn[cb][i];
-                }
-            }
+        const int gl = g1 - 1;
+        ldw(g0, w0, s0);
+        ldb(g0, b0, c0);
+        for (int gi = g0; gi < g1; gi += 2) {
+            ldw(min(gi + 1, gl), w1, s1);
+            ldb(min(gi + 1, gl), b1, c1);
+            __builtin_amdgcn_sched_barrier(0);           // the loads issue before this group's products
+            compute(w0, s0, b0, c0);
+            if (gi + 1 >= g1) break;
+            ldw(min(gi + 2, gl), w0, s0);
+            ldb(min(gi + 2, gl), b0, c0);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(w1, s1, b1, c1);
         }
     }
     // ---- the 4 waves' sums of each output (lane: rows 16 rt + 4 lg + j of column 16 cb + l16), in wave order
