@@ -748,13 +748,24 @@ __device__ __forceinline__ float sum32_lanes(float v) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Prepared operands are stored in the order the products read them: per group
+// of 128 k, per column block cb (16 rows) and product i (k = 32 lg + 8 i + e
+// within the group, lg = 0..3), the 64 lanes' 16 bytes (lane 16 lg + row mod
+// 16) one after the other, so every operand load is one contiguous kilobyte.
+// Corrections are [group][row][4 chunks of 32 k].
+__device__ __forceinline__ size_t bp_index(int m, int k) {
+    return ((((size_t)(k >> 7) * 16 + (m >> 4) * 4 + ((k >> 3) & 3)) * 64 + ((k >> 5) & 3) * 16 + (m & 15)) << 3) + (k & 7);
+}
+__device__ __forceinline__ size_t bc_index(int m, int k) { return ((size_t)(k >> 7) * 64 + m) * 4 + ((k >> 5) & 3); }
+
 // One element of a prepared row: lanes 32 c .. 32 c + 31 of a wave hold k = 32 c' + (lane mod 32)
 // of one row (valid = k < K); writes the code and, from lane 0 of the 32, the chunk's correction.
 __device__ __forceinline__ void bp_put(uint16_t* bp, float* bc, int kp, int m, int k, float h, bool valid) {
+    (void)kp;
     const float h16 = valid ? f16_to_f32(f32_to_f16(h)) : 0.f;
     const float cs = sum32_lanes(valid ? bp_corr(h16, k) : 0.f);
-    if (valid) bp[(size_t)m * kp + k] = bp_code(h16, k);
-    if (valid && (k & 31) == 0) bc[(size_t)m * (kp / 32) + (k >> 5)] = cs;
+    if (valid) bp[bp_index(m, k)] = bp_code(h16, k);
+    if (valid && (k & 31) == 0) bc[bc_index(m, k)] = cs;
 }
 
 // First q|k|v input of a forward: RMSNorm of the stage input row m, fully
@@ -786,6 +797,39 @@ __global__ __launch_bounds__(256) void bprep_kernel(const void* in, int in_dt, i
         if (256 * i < K) bp_put(bp, bc, kp, m, k, v[i] * rs * gm[i], k < K);   // whole 32-lane groups
     }
     if (tid == 0) rs_out[m] = rs;
+}
+
+// Factor of every row m < 64 of a product's results into fs (1 unless the
+// input is a deferred RMSNorm: then rs / c, rs from the row's sums of squares,
+// which 4 threads per row add (each a quarter of the partials, all loads in
+// flight) and combine in a fixed order); with write_rs, rs also goes to
+// a.rs_out.  Ends with a workgroup barrier.
+__device__ __forceinline__ void row_factors(const GemvArgs& a, int K, bool write_rs, float* fs) {
+    const int tid = threadIdx.x, m = tid >> 2, part = tid & 3;
+    float ss = 0.f;
+    if (a.norm == 1 && m < a.M) {
+        const int per = (a.ssq_tiles + 3) / 4;
+        const float* src = a.ssq_in + (size_t)m * a.ssq_tiles + part * per;
+        const int cnt = max(0, min(per, a.ssq_tiles - part * per));
+        float acc4[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int tt = 0; tt < cnt; tt += 4) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc4[e] += (tt + e < cnt) ? src[min(tt + e, cnt - 1)] : 0.f;
+        }
+        ss = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
+    }
+    ss += dpp_f<0xB1>(ss);                                    // lane ^ 1
+    ss += dpp_f<0x4E>(ss);                                    // lane ^ 2: the row's 4 parts
+    if (part == 0) {
+        float f = 1.f;
+        if (a.norm == 1 && m < a.M) {
+            const float rs = rsqrtf(ss / (float)K + a.eps);
+            f = rs / a.cb_in[m];
+            if (write_rs && a.rs_out) a.rs_out[m] = rs;
+        }
+        fs[m] = f;
+    }
+    __syncthreads();
 }
 
 // Product of the prepared input with one matrix: a workgroup's 4 waves take
@@ -824,15 +868,14 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
             const int m = 16 * cb + l16;
-            const uint16_t* row = a.bp_in + (size_t)m * a.kp;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {                // rows are kp >= 128 ngroups long: load, then drop k >= K
+            for (int i = 0; i < 4; ++i) {                // groups are whole in the buffer: load, then drop k >= K
                 const int k = 128 * gi + 32 * lg + 8 * i;
-                const u32x4 v = *(const u32x4*)(row + k);
+                const u32x4 v = *(const u32x4*)(a.bp_in + ((((size_t)gi * 16 + cb * 4 + i) * 64 + lane) << 3));
                 const bool in = k < K;
                 bv[cb][i] = u32x4{in ? v[0] : 0u, in ? v[1] : 0u, in ? v[2] : 0u, in ? v[3] : 0u};
             }
-            const float4 c4 = *(const float4*)(a.bc_in + (size_t)m * kc + 4 * gi);
+            const float4 c4 = *(const float4*)(a.bc_in + ((size_t)gi * 64 + m) * 4);
             const int kb = 128 * gi;
             cv[cb] = ((kb < K ? c4.x : 0.f) + (kb + 32 < K ? c4.y : 0.f)) + ((kb + 64 < K ? c4.z : 0.f) + (kb + 96 < K ? c4.w : 0.f));
         }
@@ -883,17 +926,23 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
         }
     };
     if (g0 < g1) {
-        const int gl = g1 - 1;
-        ldw(g0, w0, s0);
-        ldb(g0, b0, c0);
-        for (int gi = g0; gi < g1; gi += 2) {
-            ldw(min(gi + 1, gl), w1, s1);
-            ldb(min(gi + 1, gl), b1, c1);
+        // each tile starts its range at its own group (rotation by the tile index): at
+        // any moment the workgroups read different parts of the prepared operand
+        const int n = g1 - g0, rot = t % n;
+        auto G = [&](int q) {
+            q = min(q, n - 1) + rot;
+            return g0 + (q >= n ? q - n : q);
+        };
+        ldw(G(0), w0, s0);
+        ldb(G(0), b0, c0);
+        for (int q = 0; q < n; q += 2) {
+            ldw(G(q + 1), w1, s1);
+            ldb(G(q + 1), b1, c1);
             __builtin_amdgcn_sched_barrier(0);           // the loads issue before this group's products
             compute(w0, s0, b0, c0);
-            if (gi + 1 >= g1) break;
-            ldw(min(gi + 2, gl), w0, s0);
-            ldb(min(gi + 2, gl), b0, c0);
+            if (q + 1 >= n) break;
+            ldw(G(q + 2), w0, s0);
+            ldb(G(q + 2), b0, c0);
             __builtin_amdgcn_sched_barrier(0);
             compute(w1, s1, b1, c1);
         }
@@ -944,18 +993,7 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
     }
 
     // ---- factor of each row: rs / c for a deferred RMSNorm input, else 1
-    if (tid < 64) {
-        float f = 1.f;
-        if (a.norm == 1 && tid < M) {
-            float ss = 0.f;
-            for (int tt = 0; tt < a.ssq_tiles; ++tt) ss += a.ssq_in[(size_t)tid * a.ssq_tiles + tt];
-            const float rs = rsqrtf(ss / (float)K + a.eps);
-            f = rs / a.cb_in[tid];
-            if (t == 0 && a.rs_out) a.rs_out[tid] = rs;
-        }
-        fs[tid] = f;
-    }
-    __syncthreads();
+    row_factors(a, K, t == 0, fs);
 
     // ---- epilogue
     if (a.epi == EPI_STORE) {

@@ -1031,11 +1031,11 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     auto run_bp = [&](const DevMat& m, GemvArgs a) -> hipError_t {
         a.W = m.pm;
         a.M = M;
-        a.ksplit = m.bp_split;
-        a.kg = m.bp_kg;
         a.kp = st->kp;
         a.partial = st->gpart;
         a.counters = st->gcnt;
+        a.ksplit = m.bp_split;
+        a.kg = m.bp_kg;
         return launch_gemm_bp(a, s);
     };
 
