@@ -48,7 +48,7 @@ HBM_PEAK_GBPS = 8000.0
 # the same counters read for a plain 1 GiB device copy (x2.0 and x1.0).  Keyed
 # by a digest of the sources that define the kernel and its launch: after any
 # change to them the figure no longer applies and ``traffic`` is null.
-MEASURED_TRAFFIC = {("b7acbaeaed4c1884", 2048): 2_107_602_214}
+MEASURED_TRAFFIC = {("d1348f0b3503761b", 2048): 2_107_337_793}
 KERNEL_SOURCES = ("persistent.hip", "common.h", "device.h", "stage.hip")
 
 
@@ -76,10 +76,10 @@ def gateup_bytes(shape) -> int:
     return 2 * (F * (H // 2) + F * ((H + G - 1) // G) * 2)
 
 
-def cpu_baseline(shape, kv_len: int, layers_sampled: int, seed: int) -> dict:
+def cpu_baseline(shape, kv_len: int, layers_sampled: int, seed: int, min_seconds: float = 10.0) -> dict:
     """The fp64 oracle as it stands, streaming dequant per layer, on a bounded
-    sample: ``layers_sampled`` of the stage's layers for one decode step; the
-    per-step time is scaled to all layers."""
+    sample: ``layers_sampled`` of the stage's layers for one decode step, repeated
+    for about ``min_seconds``; the mean per-step time is scaled to all layers."""
     import numpy as np
 
     import oracle
@@ -99,15 +99,21 @@ def cpu_baseline(shape, kv_len: int, layers_sampled: int, seed: int) -> dict:
     state.append(k.double().numpy(), v.double().numpy())
     del k, v
     x = synth.make_hidden(sub, 1, seed).double().numpy()
-    t0 = time.perf_counter()
-    oracle.forward(ost, state, x, np.array([[kv_len]]), np.array([0]), np.ones((1, kv_len + 1), np.uint8))
-    dt = time.perf_counter() - t0
-    step_s = dt * shape.n_layers / layers_sampled
+    # repeat the sampled step (each on a fresh copy of the state) for about 10 s
+    dt, reps = 0.0, 0
+    while reps < 1 or (dt < min_seconds and reps < 64):
+        s = state.copy()
+        t0 = time.perf_counter()
+        oracle.forward(ost, s, x, np.array([[kv_len]]), np.array([0]), np.ones((1, kv_len + 1), np.uint8))
+        dt += time.perf_counter() - t0
+        reps += 1
+    step_s = dt / reps * shape.n_layers / layers_sampled
     return {
         "value": round(1.0 / step_s, 5), "unit": "tokens/s", "cores": int(blas_threads), "kind": "oracle",
         "sample": f"{layers_sampled} of {shape.n_layers} layers of one bs=1 decode step at KV {kv_len} "
-                  f"(fp64, per-layer streaming dequant) took {dt:.2f} s; scaled x{shape.n_layers / layers_sampled:g} "
-                  f"to a full step; BLAS threads {blas_threads}, elementwise numpy single-threaded",
+                  f"(fp64, per-layer streaming dequant), run {reps} times: {dt:.2f} s, {dt / reps:.3f} s each; "
+                  f"scaled x{shape.n_layers / layers_sampled:g} to a full step; BLAS threads {blas_threads}, "
+                  f"elementwise numpy single-threaded",
     }
 
 
@@ -127,12 +133,15 @@ def _line(metric, value, unit, args, steps, ms, config, bytes_per_step, roof, hi
     return line
 
 
-def _gateup_roofline(shape, prof):
+def _gateup_roofline(shape, prof, rows):
+    """Roofline of the gate|up product of the multi-kernel path: gemv_kernel for
+    one row, gemm_bp_kernel (matrix cores, prepared input) for 2..64 rows."""
     launches, total_ms = prof
     per = total_ms / max(1, launches)
     b = gateup_bytes(shape)
     g = b / (per * 1e-3) / 1e9
-    return {"bound": "hbm", "kernel": "gemv_kernel gate|up (one launch per layer)", "achieved": round(g, 1),
+    name = "gemv_kernel" if rows == 1 else "gemm_bp_kernel"
+    return {"bound": "hbm", "kernel": f"{name} gate|up (one launch per layer)", "achieved": round(g, 1),
             "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(g / HBM_PEAK_GBPS, 4), "traffic": None,
             "bytes_per_launch": b, "avg_launch_us": round(per * 1e3, 3), "launches_timed": launches}
 
@@ -223,7 +232,7 @@ def other_workload(args) -> int:
                f"llama3-70b quarter stage verify, 1 slot x {n} tokens, kv {P0} growing, drafts Bernoulli(0.6) truncated",
                **base_cfg, "slots": S, "tokens_per_slot": n, "kv_len_start": P0}
         lines.append(_line(f"spec-verify steps/s ({'8B half' if not big else '70B quarter'}-stage, {S}x{n} tokens)",
-                           1e3 / ms, "steps/s", args, steps, ms, cfg, tot_b / steps, _gateup_roofline(shape, prof),
+                           1e3 / ms, "steps/s", args, steps, ms, cfg, tot_b / steps, _gateup_roofline(shape, prof, S * n),
                            query_tokens_per_s=round(S * n * 1e3 / ms, 1),
                            emitted_tokens_per_s=round(tot_em / tot_s, 1),
                            mean_tokens_kept_per_slot_step=round(tot_em / (steps * S), 4)))
@@ -253,7 +262,7 @@ def other_workload(args) -> int:
         stage.profile(None)
         cfg = {"workload": f"llama3-70b quarter stage decode, bs=1, kv={P}", **base_cfg, "kv_len": P, "batch": 1}
         lines.append(_line("stage decode tokens/s (70B quarter-stage, bs=1)", 1e3 / ms, "tokens/s", args, steps, ms,
-                           cfg, wbytes + (P + 1) * kvb, _gateup_roofline(shape, prof)))
+                           cfg, wbytes + (P + 1) * kvb, _gateup_roofline(shape, prof, 1)))
 
     else:  # microbatch8b
         lens = {nr: synth.kv_lengths(nr, 128, 4096, args.seed) for nr in (2, 4, 8)}
@@ -297,7 +306,7 @@ def other_workload(args) -> int:
                                    f"(tokens per request {ns}), kv lengths {[int(x) for x in lens[nr]]}, 10% holes",
                        **base_cfg, "requests": nr, "mode": mode, "rows": rows}
                 lines.append(_line(f"micro-batch steps/s (8B half-stage, {nr} requests, {mode})", 1e3 / ms, "steps/s",
-                                   args, args.steps, ms, cfg, nbytes, _gateup_roofline(shape, prof),
+                                   args, args.steps, ms, cfg, nbytes, _gateup_roofline(shape, prof, rows),
                                    tokens_per_s=round(rows * 1e3 / ms, 1)))
                 for st, _, _ in reqs:
                     st.free()

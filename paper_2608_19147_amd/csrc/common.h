@@ -188,8 +188,11 @@ bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int gs);
 // single launch is only used when this is zero.
 size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int gs);
 int ps_slots(int cpl_h, int cpl_q, int cpl_f, int D, int gs);   // ring slots per compute wave
-// coop = false launches without the co-residency check (one workgroup per CU on an
-// otherwise idle device; a profiling aid for tools that do not follow cooperative launches).
+// Workgroups of the instantiation that fit on one CU with `lds` bytes of LDS.
+int ps_blocks_per_cu(int cpl_h, int cpl_q, int cpl_f, int D, int gs, size_t lds);
+// coop = true launches through hipLaunchCooperativeKernel, which checks that every
+// workgroup is resident at once; coop = false is a plain launch, for which the
+// caller has checked that nwg workgroups fit on the device (at most one per CU).
 hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int gs, int nwg, size_t lds,
                              bool coop, hipStream_t st);
 hipError_t launch_repack_rows(const uint8_t* q, const uint16_t* s, int n, int k, int g, uint8_t* w_out, uint16_t* s_out,

@@ -1353,6 +1353,29 @@ size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int gs) {
 }
 
 template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
+int ps_blocks_of(size_t lds) {
+    const void* fn = (const void*)stage_stream_kernel<CPL_H, CPL_Q, CPL_F, D, GS, S>;
+    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, SK_THREADS, lds) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    return n;
+}
+
+int ps_blocks_per_cu(int cpl_h, int cpl_q, int cpl_f, int D, int gs, size_t lds) {
+#define PS_MATCH(H_, Q_, F_, D_, G_, S_) \
+    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return ps_blocks_of<H_, Q_, F_, D_, G_, S_>(lds);
+    PS_SHAPES(PS_MATCH)
+#undef PS_MATCH
+    return 0;
+}
+
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
 hipError_t launch_ps(const PsArgs& a, int nwg, size_t lds, bool coop, hipStream_t st) {
     const void* fn = (const void*)stage_stream_kernel<CPL_H, CPL_Q, CPL_F, D, GS, S>;
     static bool configured = false;

@@ -95,7 +95,7 @@ struct Stage {
     unsigned long long *ll_qkv = nullptr, *ll_o = nullptr, *ll_part = nullptr, *ll_act = nullptr;   // its flag-word
     unsigned* ll_x = nullptr;                                                                       // exchange buffers
     unsigned ll_epoch = 0;                              // flag numbers used so far
-    bool ps_coop = true;                                // cooperative launch (STAGE_COOP=0: plain launch, for profilers)
+    bool ps_coop = false;                               // cooperative launch (STAGE_COOP=1), else a plain launch
     int attn_vector = 0;                                // attention on the vector units (STAGE_ATTN_VECTOR=1)
     int gemm_min_rows = 2;                              // rows from which products use the matrix cores (STAGE_GEMM_MIN_ROWS)
     unsigned long long* trace = nullptr;   // phase stamps of the last persistent forward (STAGE_PS_TRACE=1)
@@ -553,6 +553,14 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         // the single-launch forward is only used when its kernel needs no private
         // segment (no stack, no scratch spills) for this shape
         if (st->ps_ok && ps_private_bytes(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv) != 0) st->ps_ok = false;
+        // Workgroups wait on each other's flag words, so all nwg must be resident at
+        // once: nwg <= CUs and one workgroup fits per CU.  The plain launch (default:
+        // the cooperative one adds ~17 us per forward on MI355X) relies on this check;
+        // a workgroup held back by other work on the device delays the others, and
+        // an exchange that never completes ends in STAGE_E_DEVICE, not a hang.
+        if (st->ps_ok && (nwg > cus || ps_blocks_per_cu(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv,
+                                                        (size_t)ps_layout(probe, slots, D, Hq / Hkv)) < 1))
+            st->ps_ok = false;
     }
     if (hipDeviceSynchronize() != hipSuccess) return cleanup(fail(STAGE_E_HIP, "stage_create synchronize failed"));
     *out = st;
