@@ -1680,12 +1680,12 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
     }
 }
 
-hipError_t launch_attention(const AttnArgs& a, int head_dim, int rows_per_item_max, hipStream_t st) {
+hipError_t launch_attention(const AttnArgs& a, int head_dim, int queries_per_item_max, hipStream_t st) {
     const dim3 grid(a.meta.n_items, a.Hkv, a.nsplit_max), block(256);
     const dim3 mgrid(a.meta.M, a.Hq);
-    const bool wide = rows_per_item_max > 4;
+    const bool wide = queries_per_item_max > 4;
     const bool bf = a.kv_dt == DT_BF16;
-    const bool one = rows_per_item_max * (a.Hq / a.Hkv) <= 64;   // every item's query tiles: one per wave
+    const bool one = queries_per_item_max <= 64;                // every item's query tiles: one per wave
 #define ATTN_MMA(D_)                                                                              \
     do {                                                                                          \
         if (bf && one) attn_mma_kernel<D_, DT_BF16, 1><<<grid, block, 0, st>>>(a);                \

@@ -811,7 +811,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     const int gs = Hq / Hkv;
 
     // ---------------- validation (no side effects)
-    int M = 0, n_items = 0, max_rows_item = 0;
+    int M = 0, n_items = 0, max_queries_item = 0;
     size_t mask_bytes = 0, beam_ints = 0;
     for (int r = 0; r < n_req; ++r) {
         const StageRequest& q = reqs[r];
@@ -842,7 +842,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         }
         M += S * n;
         n_items += S;
-        max_rows_item = std::max(max_rows_item, gs * n);
+        max_queries_item = std::max(max_queries_item, gs * n);
         mask_bytes += (size_t)S * q.mask_len;
         if (q.beam_idx) beam_ints += S;
     }
@@ -1115,7 +1115,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
                 a.kp = st->kp;
             }
             HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, true, s));
-            HIP_TRY(launch_attention(a, D, max_rows_item, s));
+            HIP_TRY(launch_attention(a, D, max_queries_item, s));
             HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, false, s));
             if (use_bp) bcur = 1 - bcur;
         }
