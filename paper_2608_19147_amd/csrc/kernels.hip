@@ -846,7 +846,7 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
     __shared__ float red[4][MP][65];
     __shared__ float fs[64];
     __shared__ int last_s;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar loop control
     const int l16 = lane & 15, lg = lane >> 4;
     const int t = blockIdx.x, s = blockIdx.y;
     const PackedMat W = a.W;
@@ -864,20 +864,17 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
             sv[rt] = *(const u32x2*)(W.s + ((size_t)t * W.ngroups + gi) * 64 + 16 * rt + 4 * lg);
         }
     };
-    auto ldb = [&](int gi, u32x4 (&bv)[NCB][4], float (&cv)[NCB]) {
+    // prepared operand and corrections of one group as stored; entries at k >= K
+    // (past the end of a ragged last group) are dropped when the group computes,
+    // so nothing waits for these loads before then
+    auto ldb = [&](int gi, u32x4 (&bv)[NCB][4], float4 (&cv)[NCB]) {
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
             const int m = 16 * cb + l16;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {                // groups are whole in the buffer: load, then drop k >= K
-                const int k = 128 * gi + 32 * lg + 8 * i;
-                const u32x4 v = *(const u32x4*)(a.bp_in + ((((size_t)gi * 16 + cb * 4 + i) * 64 + lane) << 3));
-                const bool in = k < K;
-                bv[cb][i] = u32x4{in ? v[0] : 0u, in ? v[1] : 0u, in ? v[2] : 0u, in ? v[3] : 0u};
-            }
-            const float4 c4 = *(const float4*)(a.bc_in + ((size_t)gi * 64 + m) * 4);
-            const int kb = 128 * gi;
-            cv[cb] = ((kb < K ? c4.x : 0.f) + (kb + 32 < K ? c4.y : 0.f)) + ((kb + 64 < K ? c4.z : 0.f) + (kb + 96 < K ? c4.w : 0.f));
+            for (int i = 0; i < 4; ++i)
+                bv[cb][i] = *(const u32x4*)(a.bp_in + ((((size_t)gi * 16 + cb * 4 + i) * 64 + lane) << 3));
+            cv[cb] = *(const float4*)(a.bc_in + ((size_t)gi * 64 + m) * 4);
         }
     };
 
@@ -886,15 +883,30 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
     for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) acc[rt][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    // Two register sets, each the codes, scales and prepared operand of one group:
-    // while one group computes, the next one's loads are in flight.  The loads
-    // are issued unconditionally (the group index is clamped to the wave's last;
-    // a repeated group is simply not computed), so no branch sits between a load
-    // and its use and the compiler waits for exactly the loads each product needs.
-    u32x4 w0[4], w1[4], b0[NCB][4], b1[NCB][4];
-    u32x2 s0[4], s1[4];
-    float c0[NCB], c1[NCB];
-    auto compute = [&](const u32x4 (&wv)[4], const u32x2 (&sv)[4], const u32x4 (&bv)[NCB][4], const float (&cv)[NCB]) {
+    // Two register sets, each the codes, scales, prepared operand and corrections
+    // of one group: while one group computes, the next one's loads are in flight.
+    // A group's loads are issued together (loads retire from the wait counter in
+    // issue order) and unconditionally (the group index is clamped to the wave's
+    // last; a repeated group is simply not computed), and nothing reads them
+    // before the group computes, so no branch or select sits between a load and
+    // its use and the compiler waits for exactly the loads each product needs.
+    u32x4 wr[2][4], br[2][NCB][4];
+    u32x2 sr[2][4];
+    float4 cr[2][NCB];
+    auto compute = [&](int gi, const u32x4 (&wv)[4], const u32x2 (&sv)[4], u32x4 (&bv)[NCB][4], const float4 (&cq)[NCB]) {
+        const int kb = 128 * gi;
+        float cv[NCB];
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {                // in place: the set is reloaded after this group
+                const bool in = kb + 32 * lg + 8 * i < K;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) bv[cb][i][e] = in ? bv[cb][i][e] : 0u;
+            }
+            const float4 c4 = cq[cb];
+            cv[cb] = ((kb < K ? c4.x : 0.f) + (kb + 32 < K ? c4.y : 0.f)) + ((kb + 64 < K ? c4.z : 0.f) + (kb + 96 < K ? c4.w : 0.f));
+        }
 #pragma unroll
         for (int rt = 0; rt < 4; ++rt) {
             half8_t A[4];
@@ -933,18 +945,26 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
             q = min(q, n - 1) + rot;
             return g0 + (q >= n ? q - n : q);
         };
-        ldw(G(0), w0, s0);
-        ldb(G(0), b0, c0);
-        for (int q = 0; q < n; q += 2) {
-            ldw(G(q + 1), w1, s1);
-            ldb(G(q + 1), b1, c1);
+        // group q computes from set q & 1 while group q + 1 loads into the other set:
+        // whole pairs of groups, then a last single group
+        ldw(G(0), wr[0], sr[0]);
+        ldb(G(0), br[0], cr[0]);
+        int q = 0;
+        for (; q + 2 <= n; q += 2) {
+            ldw(G(q + 1), wr[1], sr[1]);
+            ldb(G(q + 1), br[1], cr[1]);
             __builtin_amdgcn_sched_barrier(0);           // the loads issue before this group's products
-            compute(w0, s0, b0, c0);
-            if (q + 1 >= n) break;
-            ldw(G(q + 2), w0, s0);
-            ldb(G(q + 2), b0, c0);
+            compute(G(q), wr[0], sr[0], br[0], cr[0]);
+            ldw(G(q + 2), wr[0], sr[0]);
+            ldb(G(q + 2), br[0], cr[0]);
             __builtin_amdgcn_sched_barrier(0);
-            compute(w1, s1, b1, c1);
+            compute(G(q + 1), wr[1], sr[1], br[1], cr[1]);
+        }
+        if (q < n) {
+            ldw(G(q + 1), wr[1], sr[1]);
+            ldb(G(q + 1), br[1], cr[1]);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(G(q), wr[0], sr[0], br[0], cr[0]);
         }
     }
     // ---- the 4 waves' sums of each output (lane: rows 16 rt + 4 lg + j of column 16 cb + l16), in wave order
