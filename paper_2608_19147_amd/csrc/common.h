@@ -206,12 +206,10 @@ hipError_t launch_repack(const uint8_t* q, const uint16_t* s, int n, int k, int 
                          int row_off, int row_map, hipStream_t st);
 hipError_t launch_gemv(const GemvArgs& a, hipStream_t st);
 // Matrix-core product of 1..64 rows (group size 128); a.ksplit splits K.
-hipError_t launch_gemm(const GemvArgs& a, hipStream_t st);
 // Product of 2..64 prepared rows (group size 128); a.ksplit splits K, a.kg groups per wave.
 hipError_t launch_gemm_bp(const GemvArgs& a, hipStream_t st);
 hipError_t launch_bprep(const void* in, int in_dt, int in_ld, const uint16_t* gamma, int gamma_dt, int K, float eps,
                         int M, uint16_t* bp, float* bc, int kp, float* rs_out, hipStream_t st);
-int gemm_groups_per_slice(int M);
 // queries_per_item_max: the largest (rows of an item) x (query heads per kv head).
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int queries_per_item_max, hipStream_t st);
 hipError_t launch_table_gather(const int16_t* src, int16_t* dst, const int* beam, int S, int cap, int P, hipStream_t st);

@@ -411,307 +411,6 @@ __device__ __forceinline__ uint32_t bfi_u32(uint32_t m, uint32_t x, uint32_t c) 
     return r;
 }
 
-// W4A16 product of 2..64 activation rows on the matrix cores
-// (v_mfma_f32_16x16x32_f16), for verify and micro-batch row counts where the
-// VALU GEMV's cost grows with the rows.  It streams the same tiles and scales
-// as gemv_kernel: wave w of a workgroup takes rows 16w..16w+15 of a 64-row
-// tile, and in the tiled layout the dword of (row r, 8-k subgroup d) of a chunk
-// sits at lane r, dword d, which is the MFMA A operand of lane 16d + (r mod 16).
-// The mask-and-or decode gives fp16 1024 + u at operand positions 0, 1, 4, 5
-// and 1024 + 16u at 2, 3, 6, 7 (u = q + 8), so the B operand (the activation
-// rows, staged in LDS) carries x / 16 at the latter positions, and each group's
-// result is corrected by 1032 S_lo + 72 S_hi (sums of the group's inputs over
-// the two kinds of position) before its scale is applied: sum q x exactly as
-// the VALU kernel computes it, up to fp32 rounding order.  K is walked in
-// slices of GPW groups (128 k each); the grid's second axis splits K further,
-// merged like gemv_kernel's splits.  Requires group size 128.
-template <int NCB, int GPW>
-__global__ __launch_bounds__(256) void gemm_kernel(GemvArgs a) {
-    constexpr int MP = 16 * NCB;                 // padded activation rows (B columns)
-    constexpr int KS = GPW * 16;                 // 8-k subgroups per slice
-    constexpr int NI = (MP * KS + 255) / 256;    // staging items per thread
-    constexpr int NV = (MP * 64 + 255) / 256;
-    __shared__ __attribute__((aligned(16))) uint32_t bs[KS][MP][4];
-    __shared__ float cpart[KS][MP];
-    __shared__ float corr[GPW][MP];
-    __shared__ float red[MP][64];
-    __shared__ float rs_s[MP];
-    __shared__ float bsum[256];
-    __shared__ int last_s;
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int t = blockIdx.x, s = blockIdx.y;
-    const PackedMat W = a.W;
-    const int M = a.M, K = W.k;
-    const int gper = (W.ngroups + a.ksplit - 1) / a.ksplit;   // groups of this split
-    const int gbeg = s * gper, gend = min(W.ngroups, gbeg + gper);
-
-    if (a.rms == RMS_FULLROW) {
-        rms_fullrow<MP>(a, K, rs_s, bsum);
-    } else if (a.rms == RMS_PARTIALS) {
-        for (int m = wave; m < M; m += 4) {
-            float ss = 0.f;
-            for (int tt = lane; tt < a.ssq_tiles; tt += 64) ss += a.ssq_in[(size_t)m * a.ssq_tiles + tt];
-#pragma unroll
-            for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
-            if (lane == 0) rs_s[m] = rsqrtf(ss / (float)K + a.eps);
-        }
-    }
-    __syncthreads();
-
-    uint32_t magic = 0x64006400u;
-    asm volatile("" : "+v"(magic));
-    const int wrow = 16 * wave + (lane & 15);    // A-operand row of this lane within the tile
-    const int sub = lane >> 4;                   // A/B k subgroup of this lane
-    const int srow = 16 * wave + 4 * sub;        // first of the 4 output rows of this lane
-    f32x4_t acc[NCB];
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) acc[cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-    // weights and scales of one slice (zero codes past the split's last group)
-    auto load_slice = [&](int g0, uint32_t (&wd)[GPW][4], u32x2 (&sc)[GPW]) {
-        const int ng = min(GPW, gend - g0);
-#pragma unroll
-        for (int gi = 0; gi < GPW; ++gi) {
-            if (gi < ng) {
-#pragma unroll
-                for (int cc = 0; cc < 4; ++cc) {
-                    const size_t c = (size_t)(g0 + gi) * 4 + cc;
-                    wd[gi][cc] = __builtin_nontemporal_load(
-                        (const uint32_t*)(W.w + (((size_t)t * W.nchunk + c) * 64 + wrow) * 16) + sub);
-                }
-                sc[gi] = *(const u32x2*)(W.s + ((size_t)t * W.ngroups + g0 + gi) * 64 + srow);
-            } else {
-#pragma unroll
-                for (int cc = 0; cc < 4; ++cc) wd[gi][cc] = 0x88888888u;
-                sc[gi] = u32x2{0u, 0u};
-            }
-        }
-    };
-    uint32_t wd[GPW][4];
-    u32x2 sc[GPW];
-    if (gbeg < gend) load_slice(gbeg, wd, sc);
-    for (int g0 = gbeg; g0 < gend; g0 += GPW) {
-        const int ng = min(GPW, gend - g0);
-        // ---- stage the activation slice as B operands (x / 16 at positions 2, 3, 6, 7)
-        __syncthreads();                           // the previous slice's operands are consumed
-#pragma unroll
-        for (int i = 0; i < NI; ++i) {
-            const int it = tid + 256 * i;
-            if (it < MP * KS) {
-                const int m = it % MP, ks = it / MP;    // m fastest: consecutive LDS addresses
-                const int kk = g0 * 128 + 8 * ks;
-                float v[8];
-                const bool ok = m < M && kk < K;
-                if (ok) {
-                    const size_t base = (size_t)m * a.in_ld + kk;
-                    if (a.in_dt == DT_F32) {
-                        const float4 p = *(const float4*)((const float*)a.in + base);
-                        const float4 q = *(const float4*)((const float*)a.in + base + 4);
-                        v[0] = p.x; v[1] = p.y; v[2] = p.z; v[3] = p.w; v[4] = q.x; v[5] = q.y; v[6] = q.z; v[7] = q.w;
-                    } else {
-                        const u32x4 h = *(const u32x4*)((const uint16_t*)a.in + base);
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            const uint32_t w = h[e >> 1];
-                            v[e] = half_bits_to_f32((uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFFu)), a.in_dt);
-                        }
-                    }
-                    if (a.rms != RMS_NONE) {
-                        const float rs = rs_s[m];
-                        const u32x4 gv = *(const u32x4*)(a.gamma + kk);
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            const uint32_t w = gv[e >> 1];
-                            v[e] = (v[e] * rs) * half_bits_to_f32((uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFFu)), a.gamma_dt);
-                        }
-                    }
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) v[e] = 0.f;
-                }
-                float h[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) h[e] = f16_to_f32(f32_to_f16(v[e]));
-                cpart[ks][m] = 1032.0f * ((h[0] + h[1]) + (h[4] + h[5])) + 72.0f * ((h[2] + h[3]) + (h[6] + h[7]));
-                u32x4 o;
-                o[0] = pack_f16x2(h[0], h[1]);
-                o[1] = pack_f16x2(h[2] * 0.0625f, h[3] * 0.0625f);
-                o[2] = pack_f16x2(h[4], h[5]);
-                o[3] = pack_f16x2(h[6] * 0.0625f, h[7] * 0.0625f);
-                *(u32x4*)bs[ks][m] = o;
-            }
-        }
-        __syncthreads();
-        for (int idx = tid; idx < GPW * MP; idx += 256) {
-            const int gi = idx / MP, m = idx % MP;
-            float c = 0.f;
-#pragma unroll
-            for (int j = 0; j < 16; ++j) c += cpart[16 * gi + j][m];
-            corr[gi][m] = c;
-        }
-        __syncthreads();
-        // the next slice's weights load while this one computes
-        uint32_t wn[GPW][4];
-        u32x2 sn[GPW];
-        if (g0 + GPW < gend) load_slice(g0 + GPW, wn, sn);
-        // ---- matrix-core products, one scale group at a time
-#pragma unroll
-        for (int gi = 0; gi < GPW; ++gi) {
-            if (gi < ng) {
-                f32x4_t c[NCB];
-#pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) c[cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int cc = 0; cc < 4; ++cc) {
-                    const uint32_t x = wd[gi][cc], y = x >> 8;
-                    u32x4 av;
-                    av[0] = bfi_u32(0x000F000Fu, x, magic);
-                    av[1] = bfi_u32(0x00F000F0u, x, magic);
-                    av[2] = bfi_u32(0x000F000Fu, y, magic);
-                    av[3] = bfi_u32(0x00F000F0u, y, magic);
-                    const half8_t A = __builtin_bit_cast(half8_t, av);
-#pragma unroll
-                    for (int cb = 0; cb < NCB; ++cb) {
-                        const half8_t B = __builtin_bit_cast(half8_t, *(const u32x4*)bs[4 * (4 * gi + cc) + sub][16 * cb + (lane & 15)]);
-                        c[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A, B, c[cb], 0, 0, 0);
-                    }
-                }
-                float scl[4];
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const uint32_t w = sc[gi][j >> 1];
-                    scl[j] = f16_to_f32((uint16_t)((j & 1) ? (w >> 16) : (w & 0xFFFFu)));
-                }
-#pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) {
-                    const float cr = corr[gi][16 * cb + (lane & 15)];
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) acc[cb][j] = __builtin_fmaf(scl[j], c[cb][j] - cr, acc[cb][j]);
-                }
-            }
-        }
-        if (g0 + GPW < gend) {
-#pragma unroll
-            for (int gi = 0; gi < GPW; ++gi) {
-#pragma unroll
-                for (int cc = 0; cc < 4; ++cc) wd[gi][cc] = wn[gi][cc];
-                sc[gi] = sn[gi];
-            }
-        }
-    }
-    // ---- results of the tile to LDS: lane holds rows srow..srow+3 of column 16 cb + (lane mod 16)
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) red[16 * cb + (lane & 15)][srow + j] = acc[cb][j];
-    __syncthreads();
-    float vals[NV];
-#pragma unroll
-    for (int q = 0; q < NV; ++q) {
-        const int idx = tid + 256 * q;
-        vals[q] = (idx < M * 64) ? red[idx >> 6][idx & 63] : 0.f;
-    }
-
-    // ---- split-K: the last workgroup of the tile sums every split in split order
-    if (a.ksplit > 1) {
-        const int ldp = W.ntiles * 64;
-#pragma unroll
-        for (int q = 0; q < NV; ++q) {
-            const int idx = tid + 256 * q;
-            if (idx < M * 64)
-                store_coherent(&a.partial[((size_t)s * M + (idx >> 6)) * ldp + t * 64 + (idx & 63)], vals[q]);
-        }
-        if (!last_arrival(&a.counters[t], (unsigned)a.ksplit, &last_s)) return;
-        // every output's partials of 4 splits at a time are in flight together
-        const size_t stride = (size_t)M * ldp;
-#pragma unroll
-        for (int q = 0; q < NV; ++q) vals[q] = 0.f;
-        for (int s0 = 0; s0 < a.ksplit; s0 += 4) {
-            float b4[NV][4];
-#pragma unroll
-            for (int q = 0; q < NV; ++q) {
-                const int idx = tid + 256 * q;
-                const float* pp = &a.partial[(size_t)(idx >> 6) * ldp + t * 64 + (idx & 63)];
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    b4[q][e] = (idx < M * 64 && s0 + e < a.ksplit) ? load_coherent(pp + (s0 + e) * stride) : 0.f;
-            }
-#pragma unroll
-            for (int q = 0; q < NV; ++q)
-#pragma unroll
-                for (int e = 0; e < 4; ++e) vals[q] += b4[q][e];
-        }
-    }
-
-    // ---- epilogue (as gemv_kernel's)
-    __syncthreads();
-    if (a.epi == EPI_STORE) {
-#pragma unroll
-        for (int q = 0; q < NV; ++q) {
-            const int idx = tid + 256 * q;
-            if (idx < M * 64) {
-                const int m = idx >> 6, n = t * 64 + (idx & 63);
-                if (n < W.n) a.out[(size_t)m * a.out_ld + n] = vals[q];
-            }
-        }
-    } else if (a.epi == EPI_RESID) {
-#pragma unroll
-        for (int q = 0; q < NV; ++q) {
-            const int idx = tid + 256 * q;
-            if (idx < M * 64) {
-                const int m = idx >> 6, r = idx & 63;
-                const int n = t * 64 + r;
-                float xn = 0.f;
-                if (n < W.n) {
-                    xn = load_val(a.resid, a.resid_dt, (size_t)m * a.resid_ld + n) + vals[q];
-                    a.out[(size_t)m * a.out_ld + n] = xn;
-                    if (a.out_act) ((uint16_t*)a.out_act)[(size_t)m * a.out_act_ld + n] = to_half_bits(xn, a.out_act_dt);
-                }
-                red[m][r] = xn * xn;
-            }
-        }
-        __syncthreads();
-        if (a.ssq_out && tid < M) {
-            float ss = 0.f;
-            for (int r = 0; r < 64; ++r) ss += red[tid][r];
-            a.ssq_out[(size_t)tid * W.ntiles + t] = ss;
-        }
-    } else {  // EPI_SWIGLU: rows 0..31 of the tile are gate rows, 32..63 the matching up rows
-#pragma unroll
-        for (int q = 0; q < NV; ++q) {
-            const int idx = tid + 256 * q;
-            if (idx < M * 64) red[idx >> 6][idx & 63] = vals[q];
-        }
-        __syncthreads();
-        for (int idx = tid; idx < M * 32; idx += 256) {
-            const int m = idx >> 5, r = idx & 31;
-            const int f = t * 32 + r;
-            if (f < a.n_valid) {
-                const float gt = red[m][r], up = red[m][r + 32];
-                a.out[(size_t)m * a.out_ld + f] = (gt / (1.0f + expf(-gt))) * up;
-            }
-        }
-    }
-}
-
-// Groups of 128 k per slice (a workgroup's LDS stays within about 60 KB); the
-// result does not depend on it: groups are accumulated one at a time in order.
-int gemm_groups_per_slice(int M) { return M <= 16 ? 8 : M <= 32 ? 4 : 2; }
-
-hipError_t launch_gemm(const GemvArgs& a, hipStream_t st) {
-    if (a.M < 1 || a.M > 64 || a.W.gchunks != 4) return hipErrorInvalidValue;
-    const dim3 grid(a.W.ntiles, a.ksplit), block(256);
-    const int ncb = (a.M + 15) / 16;
-    switch (ncb) {
-        case 1: gemm_kernel<1, 8><<<grid, block, 0, st>>>(a); break;
-        case 2: gemm_kernel<2, 4><<<grid, block, 0, st>>>(a); break;
-        case 3: gemm_kernel<3, 2><<<grid, block, 0, st>>>(a); break;
-        default: gemm_kernel<4, 2><<<grid, block, 0, st>>>(a); break;
-    }
-    return hipGetLastError();
-}
-
 // ------------------------------------------------------------------ prepared-operand products
 //
 // For 2..64 rows the input of every product is written once by the kernel that

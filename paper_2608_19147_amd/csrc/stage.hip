@@ -155,11 +155,6 @@ int plan_cpw(int ntiles, int nchunk) {
     return 1;
 }
 
-// K-splits of the matrix-core product: eight 128-k groups per split, fixed per
-// matrix, so that a row's result never depends on how many rows share the call
-// (a workgroup walks its split in slices sized for the row count).
-int gemm_split(const DevMat& m) { return std::max(1, (m.pm.ngroups + 7) / 8); }
-
 int make_mat(Stage* st, DevMat& m, int n_rows_padded_tiles, int k, int g) {
     m.pm.k = k;
     m.pm.ntiles = n_rows_padded_tiles;
@@ -468,7 +463,6 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
             bp_plan(*m);
             st->bp_ok = st->bp_ok && m->pm.gchunks == 4 && m->pm.k % 8 == 0;
             gpart = std::max(gpart, (size_t)m->ksplit * GEMV_MAX_M * m->pm.ntiles * 64);
-            gpart = std::max(gpart, (size_t)gemm_split(*m) * MAX_ROWS * m->pm.ntiles * 64);
             gpart = std::max(gpart, (size_t)m->bp_split * MAX_ROWS * m->pm.ntiles * 64);
             max_tiles = std::max<unsigned>(max_tiles, m->pm.ntiles);
         }
@@ -1002,11 +996,6 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         a.cps = m.cps;
         a.partial = st->gpart;
         a.counters = st->gcnt;
-        if (M >= st->gemm_min_rows && m.pm.gchunks == 4 && m.pm.k % 8 == 0 && M <= MAX_ROWS) {   // matrix cores
-            a.M = M;
-            a.ksplit = gemm_split(m);
-            return launch_gemm(a, s);
-        }
         for (int m0 = 0; m0 < M; m0 += GEMV_MAX_M) {
             GemvArgs b = a;
             b.M = std::min(GEMV_MAX_M, M - m0);
