@@ -35,12 +35,13 @@ struct DevMat {
     int bp_split = 1, bp_kg = 1;   // prepared-operand product: splits of K, groups of 128 k per wave
 };
 
-// K split of a prepared-operand product (a function of the matrix only): at
-// most about 512 workgroups of 4 waves (one resident round at two per CU),
+// K split of a prepared-operand product (a function of the matrix only): about
+// one workgroup of 4 waves per CU (more splits of K lengthen the last-arrival
+// reduction more than they shorten the streaming; 128 to 2048 were measured),
 // each wave a range of whole groups.
 void bp_plan(DevMat& m) {
     const int ng = m.pm.ngroups, nt = m.pm.ntiles;
-    int S = std::max(1, 512 / nt);
+    int S = std::max(1, 256 / nt);
     const int kg = std::max(1, (ng + 4 * S - 1) / (4 * S));
     S = (ng + 4 * kg - 1) / (4 * kg);
     m.bp_split = S;
