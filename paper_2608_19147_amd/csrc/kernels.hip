@@ -505,17 +505,21 @@ __global__ __launch_bounds__(256) void bprep_kernel(const void* in, int in_dt, i
 // a.rs_out.  Ends with a workgroup barrier.
 __device__ __forceinline__ void row_factors(const GemvArgs& a, int K, bool write_rs, float* fs) {
     const int tid = threadIdx.x, m = tid >> 2, part = tid & 3;
-    float ss = 0.f;
+    float ss = 0.f, cb = 1.f;
     if (a.norm == 1 && m < a.M) {
+        cb = a.cb_in[m];
         const int per = (a.ssq_tiles + 3) / 4;
         const float* src = a.ssq_in + (size_t)m * a.ssq_tiles + part * per;
         const int cnt = max(0, min(per, a.ssq_tiles - part * per));
-        float acc4[4] = {0.f, 0.f, 0.f, 0.f};
-        for (int tt = 0; tt < cnt; tt += 4) {
+        // 32 partials per pass, all loads issued before any is added (clamped, then
+        // dropped past cnt), added in index order
+        for (int tt = 0; tt < cnt; tt += 32) {
+            float v[32];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) acc4[e] += (tt + e < cnt) ? src[min(tt + e, cnt - 1)] : 0.f;
+            for (int e = 0; e < 32; ++e) v[e] = src[min(tt + e, cnt - 1)];
+#pragma unroll
+            for (int e = 0; e < 32; ++e) ss += (tt + e < cnt) ? v[e] : 0.f;
         }
-        ss = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
     }
     ss += dpp_f<0xB1>(ss);                                    // lane ^ 1
     ss += dpp_f<0x4E>(ss);                                    // lane ^ 2: the row's 4 parts
@@ -523,7 +527,7 @@ __device__ __forceinline__ void row_factors(const GemvArgs& a, int K, bool write
         float f = 1.f;
         if (a.norm == 1 && m < a.M) {
             const float rs = rsqrtf(ss / (float)K + a.eps);
-            f = rs / a.cb_in[m];
+            f = rs / cb;
             if (write_rs && a.rs_out) a.rs_out[m] = rs;
         }
         fs[m] = f;
@@ -636,18 +640,23 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
             }
         }
     };
-    if (g0 < g1) {
-        // each tile starts its range at its own group (rotation by the tile index): at
-        // any moment the workgroups read different parts of the prepared operand
-        const int n = g1 - g0, rot = t % n;
-        auto G = [&](int q) {
-            q = min(q, n - 1) + rot;
-            return g0 + (q >= n ? q - n : q);
-        };
-        // group q computes from set q & 1 while group q + 1 loads into the other set:
-        // whole pairs of groups, then a last single group
+    // each tile starts its range at its own group (rotation by the tile index): at
+    // any moment the workgroups read different parts of the prepared operand
+    const int n = g1 - g0, rot = n > 0 ? t % n : 0;
+    auto G = [&](int q) {
+        q = min(q, n - 1) + rot;
+        return g0 + (q >= n ? q - n : q);
+    };
+    if (n > 0) {
         ldw(G(0), wr[0], sr[0]);
         ldb(G(0), br[0], cr[0]);
+    }
+    // factor of each row (rs / c for a deferred RMSNorm input, else 1): its inputs
+    // come from the kernel before, so its loads fly with the first group's
+    row_factors(a, K, t == 0 && s == 0, fs);
+    if (n > 0) {
+        // group q computes from set q & 1 while group q + 1 loads into the other set:
+        // whole pairs of groups, then a last single group
         int q = 0;
         for (; q + 2 <= n; q += 2) {
             ldw(G(q + 1), wr[1], sr[1]);
@@ -710,9 +719,6 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
                 for (int e = 0; e < 4; ++e) vals[q] += b4[q][e];
         }
     }
-
-    // ---- factor of each row: rs / c for a deferred RMSNorm input, else 1
-    row_factors(a, K, t == 0, fs);
 
     // ---- epilogue
     if (a.epi == EPI_STORE) {
