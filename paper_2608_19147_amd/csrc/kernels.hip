@@ -548,6 +548,7 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
     constexpr int NV = MP * 64 / 256;
     __shared__ float red[4][MP][65];
     __shared__ float fs[64];
+    __shared__ float sres[NCB >= 2 ? MP : 1][64], sgam[64], srs[NCB >= 2 ? MP : 1];   // residual-epilogue inputs read at the start
     __shared__ int last_s;
     const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar loop control
     const int l16 = lane & 15, lg = lane >> 4;
@@ -651,9 +652,37 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
         ldw(G(0), wr[0], sr[0]);
         ldb(G(0), br[0], cr[0]);
     }
+    // With 17 or more rows the residual epilogue's inputs (the tile's residual
+    // rows, the next norm's weights and the rows' rs) are read now by every split
+    // of the tile, off the last split's tail; the residual is rewritten only by
+    // the tile's last split to arrive, after all have started.  (With 16 rows the
+    // added start latency outweighs the shorter tail: measured.)
+    constexpr bool PRE = NCB >= 2;
+    const bool resid_epi = PRE && a.epi == EPI_RESID;
+    float pres[NV], pgam = 0.f, prs = 0.f;
+    if (resid_epi) {
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
+            const int idx = tid + 256 * q, m = idx >> 6, n = t * 64 + (idx & 63);
+            pres[q] = (m < M && n < W.n) ? load_val(a.resid, a.resid_dt, (size_t)m * a.resid_ld + n) : 0.f;
+        }
+        if (a.bp_out && tid < 64 && t * 64 + tid < W.n) pgam = half_bits_to_f32(a.gamma_next[t * 64 + tid], a.gamma_next_dt);
+        if (a.bp_out && tid < M) prs = a.rs_in[tid];
+    }
     // factor of each row (rs / c for a deferred RMSNorm input, else 1): its inputs
     // come from the kernel before, so its loads fly with the first group's
     row_factors(a, K, t == 0 && s == 0, fs);
+    if constexpr (PRE) {
+        if (resid_epi) {
+#pragma unroll
+            for (int q = 0; q < NV; ++q) {
+                const int idx = tid + 256 * q;
+                sres[idx >> 6][idx & 63] = pres[q];
+            }
+            if (tid < 64) sgam[tid] = pgam;
+            if (tid < MP) srs[tid] = prs;
+        }
+    }
     if (n > 0) {
         // group q computes from set q & 1 while group q + 1 loads into the other set:
         // whole pairs of groups, then a last single group
@@ -739,14 +768,24 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
             const bool ok = m < M && n < W.n;
             float xn = 0.f;
             if (ok) {
-                xn = load_val(a.resid, a.resid_dt, (size_t)m * a.resid_ld + n) + vals[q] * fs[m];
+                float xr;
+                if constexpr (PRE) xr = sres[m][r];
+                else xr = load_val(a.resid, a.resid_dt, (size_t)m * a.resid_ld + n);
+                xn = xr + vals[q] * fs[m];
                 a.out[(size_t)m * a.out_ld + n] = xn;
                 if (a.out_act) ((uint16_t*)a.out_act)[(size_t)m * a.out_act_ld + n] = to_half_bits(xn, a.out_act_dt);
             }
             if (m < M) red[0][m][r] = xn * xn;
             if (a.bp_out && m < M) {                                    // the next product's input
-                const float c = a.rs_in[m];
-                const float h = ok ? xn * half_bits_to_f32(a.gamma_next[n], a.gamma_next_dt) * c : 0.f;
+                float c, gm;
+                if constexpr (PRE) {
+                    c = srs[m];
+                    gm = sgam[r];
+                } else {
+                    c = a.rs_in[m];
+                    gm = half_bits_to_f32(a.gamma_next[n], a.gamma_next_dt);
+                }
+                const float h = ok ? xn * gm * c : 0.f;
                 bp_put(a.bp_out, a.bc_out, a.kp, m, n, h, ok);
                 if (t == 0 && r == 0) a.cb_out[m] = c;
             }
