@@ -35,6 +35,7 @@ struct PackedMat {
 // Per-request metadata on the device (one forward).
 struct ReqDev {
     int P, n, S, row0, cap, mask_off, mask_len, item0;
+    int splits;          // most attention splits per (slot, kv head): a function of the request alone
     uint16_t* kc;        // K cache, layer 0 base: [L][S][Hkv][cap][D]
     uint16_t* vc;        // V cache
     int16_t* table;      // current beam table [S][cap] (physical slot of each row)

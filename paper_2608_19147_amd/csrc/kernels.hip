@@ -860,7 +860,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const int b = it.slot;
     const int P = rq.P, n = rq.n;
     const int L = P + n;
-    int split_len = max(ATTN_MIN_SPLIT, (L + a.nsplit_max - 1) / a.nsplit_max);
+    int split_len = max(ATTN_MIN_SPLIT, (L + rq.splits - 1) / rq.splits);
     split_len = (split_len + KGROUPS - 1) / KGROUPS * KGROUPS;
     const int nsplit = (L + split_len - 1) / split_len;
     if (split >= nsplit) return;
@@ -1073,7 +1073,7 @@ __global__ __launch_bounds__(D) void attn_merge_kernel(AttnArgs a) {
     while (r + 1 < a.meta.n_req && a.meta.reqs[r + 1].row0 <= m) ++r;
     const ReqDev& rq = a.meta.reqs[r];
     const int L = rq.P + rq.n;
-    int split_len = max(ATTN_MIN_SPLIT, (L + a.nsplit_max - 1) / a.nsplit_max);
+    int split_len = max(ATTN_MIN_SPLIT, (L + rq.splits - 1) / rq.splits);
     split_len = (split_len + KGROUPS - 1) / KGROUPS * KGROUPS;
     const int nsplit = (L + split_len - 1) / split_len;
     const float* pp = a.part + ((size_t)m * a.Hq + h) * a.nsplit_max * (D + 2);
@@ -1168,7 +1168,7 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
     const int b = it.slot;
     const int P = rq.P, n = rq.n;
     const int L = P + n;
-    int split_len = max(ATTN_MIN_SPLIT, (L + a.nsplit_max - 1) / a.nsplit_max);
+    int split_len = max(ATTN_MIN_SPLIT, (L + rq.splits - 1) / rq.splits);
     split_len = (split_len + KGROUPS - 1) / KGROUPS * KGROUPS;
     const int nsplit = (L + split_len - 1) / split_len;
     if (split >= nsplit) return;

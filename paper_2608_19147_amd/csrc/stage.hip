@@ -92,6 +92,7 @@ struct Stage {
     size_t ps_wl[4] = {0, 0, 0, 0};                            // bytes per layer in each slab
     unsigned* err = nullptr;
     int ps_nwg = 0;
+    int n_cus = 0;                                      // compute units of the device
     int ps_rpw_qkv = 0, ps_rpw_h = 0, ps_rpw_gu = 0;    // rows per workgroup of the single-launch forward
     unsigned long long *ll_qkv = nullptr, *ll_o = nullptr, *ll_part = nullptr, *ll_act = nullptr;   // its flag-word
     unsigned* ll_x = nullptr;                                                                       // exchange buffers
@@ -491,14 +492,14 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         if (hipEventCreateWithFlags(&st->meta_ev[i], hipEventDisableTiming) != hipSuccess)
             return cleanup(fail(STAGE_E_HIP, "event creation failed"));
     if ((rc = ensure_meta(st, 1 << 16))) return cleanup(rc);
+    if (hipDeviceGetAttribute(&st->n_cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || st->n_cus < 1)
+        return cleanup(fail(STAGE_E_HIP, "CU count query failed"));
     if (st->ps_ok) {
         if ((rc = st->alloc(&st->ps_layers, c.n_layers)) || (rc = st->alloc(&st->err, 4))) return cleanup(rc);
         if (hipMemcpy(st->ps_layers, st->ps_host.data(), sizeof(PsLayer) * c.n_layers, hipMemcpyHostToDevice) != hipSuccess ||
             hipMemset(st->err, 0, 4) != hipSuccess)
             return cleanup(fail(STAGE_E_HIP, "persistent state init failed"));
-        int cus = 0;
-        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
-            return cleanup(fail(STAGE_E_HIP, "CU count query failed"));
+        const int cus = st->n_cus;
         // Workgroups (at most one per CU, at most 256): rotary pairs stay in one
         // workgroup (even row counts), gate|up rows come four to a flag word pair
         // (multiples of 4), and every workgroup must own rows of q|k|v, of o/down
@@ -806,7 +807,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     const int gs = Hq / Hkv;
 
     // ---------------- validation (no side effects)
-    int M = 0, n_items = 0, max_queries_item = 0;
+    int M = 0, n_items = 0, max_queries_item = 0, max_splits = 1;
     size_t mask_bytes = 0, beam_ints = 0;
     for (int r = 0; r < n_req; ++r) {
         const StageRequest& q = reqs[r];
@@ -894,6 +895,12 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             d.mask_off = (int)moff;
             d.mask_len = q.mask_len;
             d.item0 = item;
+            // attention splits: about two workgroups per CU over the request's own
+            // slots and kv heads (never its batch-mates, so they cannot change its
+            // result), at most ATTN_MAX_SPLITS
+            d.splits = std::max(1, std::min(ATTN_MAX_SPLITS, 2 * st->n_cus / (S * Hkv)));
+            if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) d.splits = std::max(1, std::min(ATTN_MAX_SPLITS, atoi(e)));
+            max_splits = std::max(max_splits, d.splits);
             d.kc = kv->kc;
             d.vc = kv->vc;
             d.table = kv->table[do_gather[r] ? 1 - kv->cur : kv->cur];
@@ -1094,11 +1101,12 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             a.qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
             a.part = st->apart;
             a.counters = st->acnt;
-            // splits per (slot, kv head) follow the request's own length only (at least
-            // ATTN_MIN_SPLIT keys each), so batch-mates never change a request's result
-            a.nsplit_max = ATTN_MAX_SPLITS;
+            // splits per (slot, kv head) follow the request's own length and slot count
+            // only (at least ATTN_MIN_SPLIT keys each, at most its `splits`), so
+            // batch-mates never change a request's result; nsplit_max bounds the grid
+            // and is the stride of the partials
+            a.nsplit_max = max_splits;
             a.vector_path = st->attn_vector;
-            if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) a.nsplit_max = std::max(1, std::min(ATTN_MAX_SPLITS, atoi(e)));
             if (use_bp) {
                 a.bp_out = st->bp[1 - bcur];
                 a.bc_out = st->bc[1 - bcur];
