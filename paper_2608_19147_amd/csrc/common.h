@@ -43,12 +43,14 @@ struct ReqDev {
 
 struct ItemDev {         // one (request, slot) pair: the unit of the attention grid
     int req, slot;
+    ReqDev rq;           // a copy of the request's record (one load instead of two dependent ones)
 };
 
 struct MetaDev {
     const ReqDev* reqs;
     const ItemDev* items;
     const int* positions;   // [M]: rotary position of each activation row
+    const int* row_item;    // [M]: item (request slot) of each activation row
     const uint8_t* masks;   // concatenated [S][P+n] per request
     int n_items, M, n_req;
 };

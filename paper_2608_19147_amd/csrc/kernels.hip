@@ -856,7 +856,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 
     const int item = blockIdx.x, g = blockIdx.y, split = blockIdx.z;
     const ItemDev it = a.meta.items[item];
-    const ReqDev rq = a.meta.reqs[it.req];
+    const ReqDev rq = it.rq;
     const int b = it.slot;
     const int P = rq.P, n = rq.n;
     const int L = P + n;
@@ -1068,10 +1068,7 @@ __global__ __launch_bounds__(D) void attn_merge_kernel(AttnArgs a) {
     __shared__ float wgt[ATTN_MAX_SPLITS];
     __shared__ float inv_s;
     const int m = blockIdx.x, h = blockIdx.y, d = threadIdx.x;
-    // the request of row m: items are (request, slot); rows of a request are slot-major
-    int r = 0;
-    while (r + 1 < a.meta.n_req && a.meta.reqs[r + 1].row0 <= m) ++r;
-    const ReqDev& rq = a.meta.reqs[r];
+    const ReqDev rq = a.meta.items[a.meta.row_item[m]].rq;    // the request of row m
     const int L = rq.P + rq.n;
     int split_len = max(ATTN_MIN_SPLIT, (L + rq.splits - 1) / rq.splits);
     split_len = (split_len + KGROUPS - 1) / KGROUPS * KGROUPS;
@@ -1164,7 +1161,7 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
 
     const int item = blockIdx.x, g = blockIdx.y, split = blockIdx.z;
     const ItemDev it = a.meta.items[item];
-    const ReqDev rq = a.meta.reqs[it.req];
+    const ReqDev rq = it.rq;
     const int b = it.slot;
     const int P = rq.P, n = rq.n;
     const int L = P + n;

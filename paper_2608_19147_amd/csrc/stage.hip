@@ -854,7 +854,8 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     const size_t off_req = 0;
     const size_t off_item = align16(off_req + sizeof(ReqDev) * n_req);
     const size_t off_pos = align16(off_item + sizeof(ItemDev) * n_items);
-    const size_t off_beam = align16(off_pos + sizeof(int) * M);
+    const size_t off_ritem = align16(off_pos + sizeof(int) * M);
+    const size_t off_beam = align16(off_ritem + sizeof(int) * M);
     const size_t off_mask = align16(off_beam + sizeof(int) * beam_ints);
     const size_t total = align16(off_mask + mask_bytes);
     int rc = ensure_meta(st, total);
@@ -866,6 +867,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     ReqDev* rd = (ReqDev*)(hb + off_req);
     ItemDev* id = (ItemDev*)(hb + off_item);
     int* pos = (int*)(hb + off_pos);
+    int* ritem = (int*)(hb + off_ritem);
     int* beam = (int*)(hb + off_beam);
     uint8_t* masks = hb + off_mask;
     std::vector<int> beam_off(n_req, -1);
@@ -904,7 +906,10 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             d.kc = kv->kc;
             d.vc = kv->vc;
             d.table = kv->table[do_gather[r] ? 1 - kv->cur : kv->cur];
-            for (int b = 0; b < S; ++b) id[item + b] = ItemDev{r, b};
+            for (int b = 0; b < S; ++b) {
+                id[item + b] = ItemDev{r, b, d};
+                for (int i = 0; i < n; ++i) ritem[row + b * n + i] = item + b;
+            }
             std::memcpy(pos + row, q.positions, sizeof(int) * S * n);
             std::memcpy(masks + moff, q.attention_mask, (size_t)S * q.mask_len);
             row += S * n;
@@ -929,6 +934,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     meta.reqs = (const ReqDev*)(db + off_req);
     meta.items = (const ItemDev*)(db + off_item);
     meta.positions = (const int*)(db + off_pos);
+    meta.row_item = (const int*)(db + off_ritem);
     meta.masks = db + off_mask;
     meta.n_items = n_items;
     meta.M = M;
