@@ -133,14 +133,14 @@ def _line(metric, value, unit, args, steps, ms, config, bytes_per_step, roof, hi
     return line
 
 
-def _gateup_roofline(shape, prof, rows):
-    """Roofline of the gate|up product of the multi-kernel path: gemv_kernel for
-    one row, gemm_bp_kernel (matrix cores, prepared input) for 2..64 rows."""
+def _gateup_roofline(shape, prof):
+    """Roofline of the gate|up product of the multi-kernel path (gemm_bp_kernel:
+    matrix cores, prepared input, 1..64 rows)."""
     launches, total_ms = prof
     per = total_ms / max(1, launches)
     b = gateup_bytes(shape)
     g = b / (per * 1e-3) / 1e9
-    name = "gemv_kernel" if rows == 1 else "gemm_bp_kernel"
+    name = "gemm_bp_kernel"
     return {"bound": "hbm", "kernel": f"{name} gate|up (one launch per layer)", "achieved": round(g, 1),
             "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(g / HBM_PEAK_GBPS, 4), "traffic": None,
             "bytes_per_launch": b, "avg_launch_us": round(per * 1e3, 3), "launches_timed": launches}
@@ -232,7 +232,7 @@ def other_workload(args) -> int:
                f"llama3-70b quarter stage verify, 1 slot x {n} tokens, kv {P0} growing, drafts Bernoulli(0.6) truncated",
                **base_cfg, "slots": S, "tokens_per_slot": n, "kv_len_start": P0}
         lines.append(_line(f"spec-verify steps/s ({'8B half' if not big else '70B quarter'}-stage, {S}x{n} tokens)",
-                           1e3 / ms, "steps/s", args, steps, ms, cfg, tot_b / steps, _gateup_roofline(shape, prof, S * n),
+                           1e3 / ms, "steps/s", args, steps, ms, cfg, tot_b / steps, _gateup_roofline(shape, prof),
                            query_tokens_per_s=round(S * n * 1e3 / ms, 1),
                            emitted_tokens_per_s=round(tot_em / tot_s, 1),
                            mean_tokens_kept_per_slot_step=round(tot_em / (steps * S), 4)))
@@ -262,7 +262,7 @@ def other_workload(args) -> int:
         stage.profile(None)
         cfg = {"workload": f"llama3-70b quarter stage decode, bs=1, kv={P}", **base_cfg, "kv_len": P, "batch": 1}
         lines.append(_line("stage decode tokens/s (70B quarter-stage, bs=1)", 1e3 / ms, "tokens/s", args, steps, ms,
-                           cfg, wbytes + (P + 1) * kvb, _gateup_roofline(shape, prof, 1)))
+                           cfg, wbytes + (P + 1) * kvb, _gateup_roofline(shape, prof)))
 
     else:  # microbatch8b
         lens = {nr: synth.kv_lengths(nr, 128, 4096, args.seed) for nr in (2, 4, 8)}
@@ -306,7 +306,7 @@ def other_workload(args) -> int:
                                    f"(tokens per request {ns}), kv lengths {[int(x) for x in lens[nr]]}, 10% holes",
                        **base_cfg, "requests": nr, "mode": mode, "rows": rows}
                 lines.append(_line(f"micro-batch steps/s (8B half-stage, {nr} requests, {mode})", 1e3 / ms, "steps/s",
-                                   args, args.steps, ms, cfg, nbytes, _gateup_roofline(shape, prof, rows),
+                                   args, args.steps, ms, cfg, nbytes, _gateup_roofline(shape, prof),
                                    tokens_per_s=round(rows * 1e3 / ms, 1)))
                 for st, _, _ in reqs:
                     st.free()
@@ -402,7 +402,7 @@ def main() -> int:
     if dominant == "persistent":
         k_bytes, k_name = b["total"], "stage_stream_kernel (whole stage forward, one launch per step)"
     else:
-        k_bytes, k_name = gateup_bytes(shape), "gemv_kernel gate|up (one launch per layer)"
+        k_bytes, k_name = gateup_bytes(shape), "gemm_bp_kernel gate|up (one launch per layer)"
     k_gbps = k_bytes / (per_launch_ms * 1e-3) / 1e9
     line = {
         "metric": "stage decode tokens/s (8B half-stage, bs=1) + achieved HBM GB/s vs peak",

@@ -99,7 +99,7 @@ struct Stage {
     unsigned ll_epoch = 0;                              // flag numbers used so far
     bool ps_coop = false;                               // cooperative launch (STAGE_COOP=1), else a plain launch
     int attn_vector = 0;                                // attention on the vector units (STAGE_ATTN_VECTOR=1)
-    int gemm_min_rows = 2;                              // rows from which products use the matrix cores (STAGE_GEMM_MIN_ROWS)
+    int gemm_min_rows = 1;                              // rows from which products use the matrix cores (STAGE_GEMM_MIN_ROWS)
     unsigned long long* trace = nullptr;   // phase stamps of the last persistent forward (STAGE_PS_TRACE=1)
     int prof_class = -1;
     std::vector<hipEvent_t> prof_ev;   // start/stop pairs
