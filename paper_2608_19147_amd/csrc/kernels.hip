@@ -1157,7 +1157,7 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
     __shared__ __attribute__((aligned(16))) uint16_t ks[2][AK][D];   // key rows, chunk c at c ^ (key mod NCH)
     __shared__ __attribute__((aligned(16))) uint16_t vt[2][D][VST];  // values transposed, key slots permuted
     __shared__ int16_t stab[ACH];                                    // physical slot of each key of the chunk
-    __shared__ uint8_t smk[ACH];                                     // its mask byte
+    __shared__ __attribute__((aligned(16))) uint8_t smk[ACH];        // its mask byte (read as words)
 
     const int item = blockIdx.x, g = blockIdx.y, split = blockIdx.z;
     const ItemDev it = a.meta.items[item];
@@ -1185,25 +1185,32 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
     const int rowbase = rq.row0 + b * n;
 
     // ---- one step's keys (chunk-relative key x0 + k): cache rows through the
-    // table, this forward's rows from q|k|v
+    // table, this forward's rows from q|k|v.  Cache rows are loaded without
+    // branches (clamped to an allocated row; whether a chunk is kept is a bit
+    // applied when it is staged), so the mask and table reads are all in flight
+    // at once and nothing waits for the loads before the staging.
     u32x4 kreg[NU], vreg[NU];
+    uint32_t keep = 0u;
     int c0 = j0, c1 = j0;                                    // keys of the staged chunk
     auto fetch = [&](int x0, bool append) {
+        uint32_t kb_ = 0u;
 #pragma unroll
         for (int u = 0; u < NU; ++u) {
             const int q = tid + 256 * u, k = q / NCH, c = q % NCH;
             const int x = min(x0 + k, ACH - 1), j = c0 + x0 + k;
-            kreg[u] = u32x4{0u, 0u, 0u, 0u};
-            vreg[u] = u32x4{0u, 0u, 0u, 0u};
-            if (j >= c1) continue;
-            const bool vis = smk[x] != 0;
-            if (j < P) {
-                if (vis) {
-                    const size_t off = (((size_t)stab[x] * Hkv + g) * rq.cap + j) * D + 8 * c;
-                    kreg[u] = *(const u32x4*)(kl + off);
-                    vreg[u] = *(const u32x4*)(vl + off);
-                }
-            } else {
+            const bool cached = j < min(c1, P);
+            const int slot = cached ? (int)stab[x] : b;
+            const size_t off = (((size_t)slot * Hkv + g) * rq.cap + (cached ? j : 0)) * D + 8 * c;
+            kreg[u] = *(const u32x4*)(kl + off);
+            vreg[u] = *(const u32x4*)(vl + off);
+            kb_ |= ((cached && smk[x] != 0) ? 1u : 0u) << u;
+        }
+        if (c0 + x0 + AK > P && c0 + x0 < c1) {              // the step holds rows of this forward (uniform)
+#pragma unroll
+            for (int u = 0; u < NU; ++u) {
+                const int q = tid + 256 * u, k = q / NCH, c = q % NCH;
+                const int x = min(x0 + k, ACH - 1), j = c0 + x0 + k;
+                if (j < P || j >= c1) continue;
                 const int i = j - P;
                 const int m = rowbase + i;
                 const int pos = a.meta.positions[m];
@@ -1214,10 +1221,10 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
                 for (int e = 0; e < 8; ++e) {
                     const int d = 8 * c + e;
                     const bool lo_half = d < HALF;
-                    const float x = krow[d];
+                    const float xk = krow[d];
                     const float xp = lo_half ? krow[d + HALF] : krow[d - HALF];
                     const float2 cs = a.rope[(size_t)pos * HALF + (lo_half ? d : d - HALF)];
-                    const float y = lo_half ? (x * cs.x - xp * cs.y) : (x * cs.x + xp * cs.y);
+                    const float y = lo_half ? (xk * cs.x - xp * cs.y) : (xk * cs.x + xp * cs.y);
                     kb[e] = kv_round<KVDT>(y);
                     vb[e] = kv_round<KVDT>(vrow[d]);
                 }
@@ -1227,27 +1234,29 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
                     kk[w2] = (uint32_t)kb[2 * w2] | ((uint32_t)kb[2 * w2 + 1] << 16);
                     vv[w2] = (uint32_t)vb[2 * w2] | ((uint32_t)vb[2 * w2 + 1] << 16);
                 }
-                if (append) {                            // append: owner of row j writes it
+                if (append) {                                // append: owner of row j writes it
                     const size_t off = (((size_t)b * Hkv + g) * rq.cap + j) * D + 8 * c;
                     *(u32x4*)(kl + off) = kk;
                     *(u32x4*)(vl + off) = vv;
                     if (a.layer == 0 && g == 0 && c == 0) rq.table[(size_t)b * rq.cap + j] = (int16_t)b;
                 }
-                if (vis) {
-                    kreg[u] = kk;
-                    vreg[u] = vv;
-                }
+                kreg[u] = kk;
+                vreg[u] = vv;
+                kb_ |= (smk[x] != 0 ? 1u : 0u) << u;
             }
         }
+        keep = kb_;
     };
     auto stash = [&](int buf) {
 #pragma unroll
         for (int u = 0; u < NU; ++u) {
             const int q = tid + 256 * u, k = q / NCH, c = q % NCH;
-            *(u32x4*)&ks[buf][k][8 * (c ^ (k % NCH))] = kreg[u];
+            const bool kp_ = (keep >> u) & 1u;               // dropped chunks enter as zero rows
+            const u32x4 kv = kreg[u], vv = vreg[u];
+            *(u32x4*)&ks[buf][k][8 * (c ^ (k % NCH))] = u32x4{kp_ ? kv[0] : 0u, kp_ ? kv[1] : 0u, kp_ ? kv[2] : 0u, kp_ ? kv[3] : 0u};
             const int slot = 8 * ((k & 15) >> 2) + 4 * (k >> 4) + (k & 3);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) vt[buf][8 * c + e][slot] = (uint16_t)(vreg[u][e >> 1] >> (16 * (e & 1)));
+            for (int e = 0; e < 8; ++e) vt[buf][8 * c + e][slot] = kp_ ? (uint16_t)(vv[e >> 1] >> (16 * (e & 1))) : (uint16_t)0;
         }
     };
 
@@ -1346,26 +1355,38 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
             // the lane's 8 keys: step key 4 lg + e (e < 4) or 16 + 4 lg + e - 4; visible ones as bits
             const int kbase = c0 + st * AK + 4 * lg;
             uint32_t vbits = 0u;
+            {
+                // mask bytes of keys 4 lg + 0..3 and 16 + 4 lg + 0..3 as two aligned words
+                const uint32_t w0 = *(const uint32_t*)&smk[st * AK + 4 * lg];
+                const uint32_t w1 = *(const uint32_t*)&smk[st * AK + 16 + 4 * lg];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int ko = (e < 4) ? e : 12 + e;
-                const int x = st * AK + 4 * lg + ko;
-                vbits |= ((kbase + ko < c1 && smk[min(x, ACH - 1)] != 0) ? 1u : 0u) << e;
+                for (int e = 0; e < 8; ++e) {
+                    const int ko = (e < 4) ? e : 12 + e;
+                    const uint32_t byte = ((e < 4 ? w0 : w1) >> (8 * (e & 3))) & 0xFFu;
+                    vbits |= ((kbase + ko < c1 && byte != 0u) ? 1u : 0u) << e;
+                }
             }
 #pragma unroll
             for (int u = 0; u < QTW; ++u) {
                 if (qg + wave + 4 * u >= nqt) continue;      // wave-uniform
                 f32x4_t s0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+                u32x4 kf0[DB], kf1[DB];                      // every key fragment of the step in flight at once
 #pragma unroll
                 for (int ib = 0; ib < DB; ++ib) {
                     const int c = 4 * ib + lg;
-                    const u32x4 k0 = *(const u32x4*)&ks[buf][ql][8 * (c ^ (ql % NCH))];
-                    const u32x4 k1 = *(const u32x4*)&ks[buf][16 + ql][8 * (c ^ ((16 + ql) % NCH))];
-                    s0 = mma_kv<KVDT>(k0, qh[u][ib], s0);
-                    s0 = mma_kv<KVDT>(k0, qr[u][ib], s0);
-                    s1 = mma_kv<KVDT>(k1, qh[u][ib], s1);
-                    s1 = mma_kv<KVDT>(k1, qr[u][ib], s1);
+                    kf0[ib] = *(const u32x4*)&ks[buf][ql][8 * (c ^ (ql % NCH))];
+                    kf1[ib] = *(const u32x4*)&ks[buf][16 + ql][8 * (c ^ ((16 + ql) % NCH))];
                 }
+#pragma unroll
+                for (int ib = 0; ib < DB; ++ib) {
+                    s0 = mma_kv<KVDT>(kf0[ib], qh[u][ib], s0);
+                    s1 = mma_kv<KVDT>(kf1[ib], qh[u][ib], s1);
+                    s0 = mma_kv<KVDT>(kf0[ib], qr[u][ib], s0);
+                    s1 = mma_kv<KVDT>(kf1[ib], qr[u][ib], s1);
+                }
+                u32x4 vf[MB];                                // value fragments: read during the softmax
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) vf[mb] = *(const u32x4*)&vt[buf][16 * mb + ql][8 * lg];
                 const int last = P + qtok[u] - kbase;         // keys up to kbase + last are causal
                 float sv[8];
 #pragma unroll
@@ -1403,10 +1424,9 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
                     pb[w2] = (uint32_t)kv_round<KVDT>(pv[2 * w2]) | ((uint32_t)kv_round<KVDT>(pv[2 * w2 + 1]) << 16);
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb) {
-                    const u32x4 va = *(const u32x4*)&vt[buf][16 * mb + ql][8 * lg];
 #pragma unroll
                     for (int jj = 0; jj < 4; ++jj) o[u][mb][jj] *= corr;
-                    o[u][mb] = mma_kv<KVDT>(va, pb, o[u][mb]);
+                    o[u][mb] = mma_kv<KVDT>(vf[mb], pb, o[u][mb]);
                 }
             }
             if (st + 1 < nsteps) stash(buf ^ 1);
