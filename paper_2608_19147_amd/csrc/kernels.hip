@@ -1260,7 +1260,7 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
         }
     };
 
-    // table entries and mask bytes of the first chunk: loaded with the queries, stored after
+    // table entries and mask bytes of the first chunk
     int16_t ptab[NS];
     uint8_t pmsk[NS];
 #pragma unroll
@@ -1270,6 +1270,16 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
         pmsk[t2] = in ? mask[j] : 0;
         ptab[t2] = (in && j < P) ? tab[j] : (int16_t)b;
     }
+    // ---- the first chunk's mask bytes and table entries are staged and its first
+    // step's loads issued before the queries are set up: they fly during it
+    c1 = min(j1, j0 + ACH);
+#pragma unroll
+    for (int t2 = 0; t2 < NS; ++t2) {
+        smk[tid + 256 * t2] = pmsk[t2];
+        stab[tid + 256 * t2] = ptab[t2];
+    }
+    __syncthreads();
+    fetch(0, true);
     for (int qg = 0; qg < nqt; qg += 4 * QTW) {
         // ---- this wave's query tiles: rotated, scaled, split into rounded part and residual
         u32x4 qh[QTW][DB], qr[QTW][DB];
@@ -1330,23 +1340,17 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
 
         for (c0 = j0; c0 < j1; c0 += ACH) {
         c1 = min(j1, c0 + ACH);
-        __syncthreads();                                     // the previous chunk's entries are no longer read
-        if (qg == 0 && c0 == j0) {
-#pragma unroll
-            for (int t2 = 0; t2 < NS; ++t2) {
-                smk[tid + 256 * t2] = pmsk[t2];
-                stab[tid + 256 * t2] = ptab[t2];
-            }
-        } else {
+        if (qg != 0 || c0 != j0) {                           // (the first chunk was staged above)
+            __syncthreads();                                 // the previous chunk's entries are no longer read
             for (int x = tid; x < c1 - c0; x += 256) {
                 const int j = c0 + x;
                 smk[x] = mask[j];
                 stab[x] = j < P ? tab[j] : (int16_t)b;
             }
+            __syncthreads();
+            fetch(0, qg == 0);
         }
-        __syncthreads();
         const int nsteps = (c1 - c0 + AK - 1) / AK;
-        fetch(0, qg == 0);
         stash(0);
         __syncthreads();
         for (int st = 0; st < nsteps; ++st) {
