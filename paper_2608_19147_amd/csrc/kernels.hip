@@ -775,7 +775,9 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
                 a.out[(size_t)m * a.out_ld + n] = xn;
                 if (a.out_act) ((uint16_t*)a.out_act)[(size_t)m * a.out_act_ld + n] = to_half_bits(xn, a.out_act_dt);
             }
-            if (m < M) red[0][m][r] = xn * xn;
+            // the row's sum of squares over the tile: row m is this wave's 64 lanes
+            const float ss = wave_sum_all(xn * xn);
+            if (a.ssq_out && m < M && r == 0) a.ssq_out[(size_t)m * W.ntiles + t] = ss;
             if (a.bp_out && m < M) {                                    // the next product's input
                 float c, gm;
                 if constexpr (PRE) {
@@ -789,12 +791,6 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
                 bp_put(a.bp_out, a.bc_out, a.kp, m, n, h, ok);
                 if (t == 0 && r == 0) a.cb_out[m] = c;
             }
-        }
-        __syncthreads();
-        if (a.ssq_out && tid < M) {
-            float ss = 0.f;
-            for (int r = 0; r < 64; ++r) ss += red[0][tid][r];
-            a.ssq_out[(size_t)tid * W.ntiles + t] = ss;
         }
     } else {  // EPI_SWIGLU: rows 0..31 of the tile are gate rows, 32..63 the matching up rows
 #pragma unroll
