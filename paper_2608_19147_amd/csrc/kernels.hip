@@ -469,19 +469,29 @@ __device__ __forceinline__ void bp_put(uint16_t* bp, float* bc, int kp, int m, i
 
 // First q|k|v input of a forward: RMSNorm of the stage input row m, fully
 // normalized (c = rs; the product's factor is 1); rs also goes to rs_out for
-// the residual product that prepares the next input.
+// the residual product that prepares the next input.  blockIdx.y takes one
+// slice of BPREP_SLICE k: every slice adds the whole row's squares in the same
+// order (so all get the same rs) and prepares only its own slice.
+constexpr int BPREP_SLICE = 1024;
 __global__ __launch_bounds__(256) void bprep_kernel(const void* in, int in_dt, int in_ld, const uint16_t* gamma,
                                                     int gamma_dt, int K, float eps, uint16_t* bp, float* bc, int kp,
                                                     float* rs_out) {
     constexpr int NPT = 32;                              // values per thread held in registers: K <= 8192
+    constexpr int SPT = BPREP_SLICE / 256;               // slice values per thread
     __shared__ float red[4];
-    const int m = blockIdx.x, tid = threadIdx.x;
-    float v[NPT], gm[NPT];
+    const int m = blockIdx.x, tid = threadIdx.x, k0 = BPREP_SLICE * blockIdx.y;
+    float v[NPT], xs[SPT], gs[SPT];
 #pragma unroll
-    for (int i = 0; i < NPT; ++i) {                      // every load issued before any is used
+    for (int i = 0; i < NPT; ++i) {                      // every load issued before any is used (clamped, then dropped)
         const int k = tid + 256 * i;
-        v[i] = k < K ? load_val(in, in_dt, (size_t)m * in_ld + k) : 0.f;
-        gm[i] = k < K ? half_bits_to_f32(gamma[k], gamma_dt) : 0.f;
+        const float x = load_val(in, in_dt, (size_t)m * in_ld + min(k, K - 1));
+        v[i] = k < K ? x : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < SPT; ++i) {
+        const int k = min(k0 + tid + 256 * i, K - 1);
+        xs[i] = load_val(in, in_dt, (size_t)m * in_ld + k);
+        gs[i] = half_bits_to_f32(gamma[k], gamma_dt);
     }
     float ss = 0.f;
 #pragma unroll
@@ -491,11 +501,11 @@ __global__ __launch_bounds__(256) void bprep_kernel(const void* in, int in_dt, i
     __syncthreads();
     const float rs = rsqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)K + eps);
 #pragma unroll
-    for (int i = 0; i < NPT; ++i) {
-        const int k = tid + 256 * i;
-        if (256 * i < K) bp_put(bp, bc, kp, m, k, v[i] * rs * gm[i], k < K);   // whole 32-lane groups
+    for (int i = 0; i < SPT; ++i) {
+        const int k = k0 + tid + 256 * i;
+        if (k0 + 256 * i < K) bp_put(bp, bc, kp, m, k, xs[i] * rs * gs[i], k < K);   // whole 32-lane groups
     }
-    if (tid == 0) rs_out[m] = rs;
+    if (blockIdx.y == 0 && tid == 0) rs_out[m] = rs;
 }
 
 // Factor of every row m < 64 of a product's results into fs (1 unless the
@@ -829,7 +839,9 @@ hipError_t launch_gemm_bp(const GemvArgs& a, hipStream_t st) {
 
 hipError_t launch_bprep(const void* in, int in_dt, int in_ld, const uint16_t* gamma, int gamma_dt, int K, float eps,
                         int M, uint16_t* bp, float* bc, int kp, float* rs_out, hipStream_t st) {
-    bprep_kernel<<<M, 256, 0, st>>>(in, in_dt, in_ld, gamma, gamma_dt, K, eps, bp, bc, kp, rs_out);
+    if (K < 1 || K > 32 * 256) return hipErrorInvalidValue;
+    bprep_kernel<<<dim3(M, (K + BPREP_SLICE - 1) / BPREP_SLICE), 256, 0, st>>>(in, in_dt, in_ld, gamma, gamma_dt, K, eps,
+                                                                              bp, bc, kp, rs_out);
     return hipGetLastError();
 }
 
