@@ -311,6 +311,7 @@ def other_workload(args) -> int:
                 for st, _, _ in reqs:
                     st.free()
                 del xs, out
+    stage.device_status()
     stage.close()
     for ln in lines:
         print(json.dumps(ln), flush=True)
@@ -440,6 +441,7 @@ def main() -> int:
         line["also"] = {"kv_len": args.kv_also, "tokens_per_s": round(1e3 / ms_also, 3), "ms_per_step": round(ms_also, 5),
                         "hbm_bytes_per_step": bb["total"], "achieved_gbps": round(g2, 1),
                         "hbm_frac": round(g2 / HBM_PEAK_GBPS, 4)}
+    stage.device_status()        # raises if a single-launch forward gave up waiting (its timing is void)
     state.free()
     stage.close()
     del xs, out

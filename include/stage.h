@@ -48,6 +48,7 @@ extern "C" {
 #define STAGE_E_HIP            -5   /* a HIP runtime call failed (message has the HIP error) */
 #define STAGE_E_STATE_MISMATCH -6   /* KV state belongs to another stage, or used twice in one call */
 #define STAGE_E_UNSUPPORTED    -7   /* configuration outside what the kernels implement */
+#define STAGE_E_DEVICE         -8   /* a single-launch forward gave up waiting on another workgroup: its outputs are invalid */
 
 #define STAGE_DTYPE_F16  1
 #define STAGE_DTYPE_BF16 2
@@ -174,7 +175,8 @@ typedef struct StageRequest {
  * advances its P by n_tokens once the work is enqueued.
  * Errors: INVALID (NULL, bad n, beam_idx out of range, fully masked row,
  * state repeated), SHAPE (mask_len != P + n), CAPACITY (P + n > capacity,
- * M > STAGE_MAX_ROWS, position >= max_positions), STATE_MISMATCH, HIP. */
+ * M > STAGE_MAX_ROWS, position >= max_positions), STATE_MISMATCH, HIP.  A
+ * failure inside a single-launch forward is reported by stage_device_status. */
 int stage_forward(Stage* stage, const StageRequest* reqs, int n_req,
                   const void* hidden_in, void* hidden_out, void* stream);
 
@@ -222,6 +224,14 @@ int stage_profile_read(Stage* stage, int* launches, double* total_ms);
  * first pass of the residual-after-o, residual-after-down and remaining waits
  * returned.  n = capacity of out_host in entries.  Synchronizes the device. */
 int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n, int* n_workgroups);
+
+/* Outcome of the single-launch forwards enqueued so far.  Workgroups of that
+ * launch wait on each other's published values; a wait that does not complete
+ * within a bounded number of polls (a workgroup held off the device) gives up,
+ * lets the launch finish, and flags the stage.  Synchronizes the device, then
+ * returns STAGE_OK, or STAGE_E_DEVICE once per flagged stage (the flag is
+ * cleared).  Call it where the caller synchronizes anyway. */
+int stage_device_status(Stage* stage);
 
 /* Bytes of device memory the stage holds for weights (packed codes + scales +
  * norm weights), as stored. */

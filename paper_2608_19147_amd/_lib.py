@@ -10,7 +10,7 @@ LIB_PATH = os.path.join(_HERE, "libstage.so")
 STAGE_OK = 0
 ERRORS = {
     -1: "STAGE_E_INVALID", -2: "STAGE_E_SHAPE", -3: "STAGE_E_CAPACITY", -4: "STAGE_E_OOM",
-    -5: "STAGE_E_HIP", -6: "STAGE_E_STATE_MISMATCH", -7: "STAGE_E_UNSUPPORTED",
+    -5: "STAGE_E_HIP", -6: "STAGE_E_STATE_MISMATCH", -7: "STAGE_E_UNSUPPORTED", -8: "STAGE_E_DEVICE",
 }
 DTYPE_F16 = 1
 DTYPE_BF16 = 2
@@ -21,7 +21,7 @@ EXPORTS = (
     "stage_create", "stage_destroy", "kv_state_alloc", "kv_state_free", "kv_state_reset",
     "kv_append", "kv_length", "kv_read", "kv_truncate", "stage_forward",
     "stage_debug_dequant", "stage_weight_bytes", "stage_last_error",
-    "stage_profile_enable", "stage_profile_read", "stage_debug_phase_trace",
+    "stage_profile_enable", "stage_profile_read", "stage_debug_phase_trace", "stage_device_status",
 )
 KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "persistent": 5}
 
@@ -83,6 +83,7 @@ def load() -> ctypes.CDLL:
         "stage_profile_enable": (I, [V, I]),
         "stage_profile_read": (I, [V, P(I), P(ctypes.c_double)]),
         "stage_debug_phase_trace": (I, [V, V, I, V]),
+        "stage_device_status": (I, [V]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

@@ -148,6 +148,7 @@ struct PsArgs {
     unsigned long long* ll_part;         // [Hkv][nsplit][Hq/Hkv][D + 2] flag words (fp32): max, sum, D outputs
     unsigned ll_epoch;                   // flag numbers used by earlier launches (PS_LL_PER_LAYER per layer)
     unsigned* err;                       // set when an exchange wait gives up
+    unsigned spin_limit;                 // polling passes after which an exchange wait gives up
     unsigned long long* trace;           // optional [nwg][n_layers][PS_TRACE_PER_LAYER] real-time stamps
     // LDS byte offsets
     int l_xs, l_sb0, l_sb1, l_res, l_q, l_nkv, l_part, l_rope, l_dbg, l_end;

@@ -34,7 +34,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 constexpr int SK_THREADS = (SK_CW + 1) * 64;
-constexpr unsigned SK_SPIN_LIMIT = 1u << 20; // an exchange wait that never completes gives up (error flag)
 
 // ------------------------------------------------------------------ LDS by address, explicit waits
 
@@ -243,7 +242,7 @@ __device__ __forceinline__ bool ll_wait(const PsArgs& a, __amdgpu_buffer_rsrc_t 
         }
         if (!ok) return false;
         if (__any(bad != 0u)) return false;                // another workgroup already gave up
-        if (++spins > SK_SPIN_LIMIT) {
+        if (++spins > a.spin_limit) {
             if (lane == 0) atomicOr(a.err, 1u);
             return false;
         }

@@ -91,6 +91,7 @@ struct Stage {
     uint8_t* ps_wb[4] = {nullptr, nullptr, nullptr, nullptr};   // code slabs per matrix kind (all layers)
     size_t ps_wl[4] = {0, 0, 0, 0};                            // bytes per layer in each slab
     unsigned* err = nullptr;
+    unsigned spin_limit = 1u << 20;                     // exchange wait passes (STAGE_PS_SPIN_LIMIT)
     int ps_nwg = 0;
     int n_cus = 0;                                      // compute units of the device
     int ps_rpw_qkv = 0, ps_rpw_h = 0, ps_rpw_gu = 0;    // rows per workgroup of the single-launch forward
@@ -496,6 +497,7 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         return cleanup(fail(STAGE_E_HIP, "CU count query failed"));
     if (st->ps_ok) {
         if ((rc = st->alloc(&st->ps_layers, c.n_layers)) || (rc = st->alloc(&st->err, 4))) return cleanup(rc);
+        if (const char* e = std::getenv("STAGE_PS_SPIN_LIMIT")) st->spin_limit = (unsigned)std::max(0, atoi(e));
         if (hipMemcpy(st->ps_layers, st->ps_host.data(), sizeof(PsLayer) * c.n_layers, hipMemcpyHostToDevice) != hipSuccess ||
             hipMemset(st->err, 0, 4) != hipSuccess)
             return cleanup(fail(STAGE_E_HIP, "persistent state init failed"));
@@ -570,6 +572,19 @@ int stage_destroy(Stage* stage) {
 }
 
 int64_t stage_weight_bytes(const Stage* stage) { return stage ? stage->weight_bytes : -1; }
+
+int stage_device_status(Stage* st) {
+    if (!st) return fail(STAGE_E_INVALID, "NULL argument");
+    if (!st->err) return STAGE_OK;                      // the stage has no single-launch forward
+    HIP_TRY(hipSetDevice(st->device));
+    HIP_TRY(hipDeviceSynchronize());
+    unsigned flag = 0u;
+    HIP_TRY(hipMemcpy(&flag, st->err, sizeof(unsigned), hipMemcpyDeviceToHost));
+    if (flag == 0u) return STAGE_OK;
+    HIP_TRY(hipMemset(st->err, 0, sizeof(unsigned)));
+    return fail(STAGE_E_DEVICE, "a single-launch forward gave up waiting on another workgroup (was the device "
+                                "shared?); its outputs and appended cache rows are invalid");
+}
 
 int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n, int* n_workgroups) {
     if (!stage || !out_host) return fail(STAGE_E_INVALID, "NULL argument");
@@ -989,6 +1004,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         a.ll_part = st->ll_part;
         a.ll_epoch = st->ll_epoch;
         a.err = st->err;
+        a.spin_limit = st->spin_limit;
         a.trace = st->trace;
         const int lds = ps_layout(a, ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, gs), D, gs);
         HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, true, s));

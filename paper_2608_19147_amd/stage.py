@@ -104,6 +104,12 @@ class Stage:
         check(self.lib.stage_profile_read(self.handle, ctypes.byref(n), ctypes.byref(ms)))
         return n.value, ms.value
 
+    def device_status(self) -> None:
+        """Wait for the last single-launch forward; raise StageError
+        (STAGE_E_DEVICE) once if a forward of this stage gave up waiting on
+        another workgroup."""
+        check(self.lib.stage_device_status(self.handle))
+
     def phase_trace(self) -> np.ndarray:
         """[workgroups, layers, 32] device real-time stamps (100 MHz) and exchange
         pass counts of the last single-launch forward (needs STAGE_PS_TRACE=1 at

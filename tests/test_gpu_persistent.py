@@ -109,3 +109,37 @@ def test_8b_two_layer_decode_persistent():
     out = run_gpu(p, [req(g, pos, mask, [0])], x)
     ref = oracle.forward(p.orc, o, host(x), pos, np.array([0]), mask)
     assert rel_err(out, ref) <= TOL_STAGE
+
+
+def test_exchange_give_up_is_reported():
+    """Failure handling of the single launch, forced from the host: with
+    STAGE_PS_SPIN_LIMIT=0 (set for this stage only) an exchange wait may poll
+    once, so some wait gives up; the launch still ends (every later wait polls
+    once), the stage reports STAGE_E_DEVICE once, and a stage with the default
+    limit is unaffected."""
+    from paper_2608_19147_amd import StageError
+
+    shape = synth.with_layers(synth.TINY, 2)
+    layers = synth.make_weights(shape, 44)
+    old = os.environ.get("STAGE_PS_SPIN_LIMIT")
+    os.environ["STAGE_PS_SPIN_LIMIT"] = "0"
+    try:
+        bad = _pair(shape, 44, True, layers)
+    finally:
+        if old is None:
+            del os.environ["STAGE_PS_SPIN_LIMIT"]
+        else:
+            os.environ["STAGE_PS_SPIN_LIMIT"] = old
+    good = _pair(shape, 44, True, layers)
+    P = 40
+    x = synth.make_hidden(shape, 1, 44)
+    pos, mask = np.array([[P]]), full_mask(1, P + 1)
+    gb, _ = bad.states(1, P, 64, seed=44, with_oracle=False)
+    run_gpu(bad, [req(gb, pos, mask, [0])], x)
+    with pytest.raises(StageError, match="STAGE_E_DEVICE"):
+        bad.gpu.device_status()
+    bad.gpu.device_status()                      # reported once, then clear
+    gg, o = good.states(1, P, 64, seed=44)
+    out = run_gpu(good, [req(gg, pos, mask, [0])], x)
+    good.gpu.device_status()
+    assert rel_err(out, oracle.forward(good.orc, o, host(x), pos, np.array([0]), mask)) <= TOL_STAGE
