@@ -1,30 +1,41 @@
 // Single-launch stage forward for one decode row (the "stream kernel").
 //
-// One workgroup per CU, made of SK_CW compute waves and one control wave.
+// One workgroup per CU, made of SK_CW compute waves and one control wave; all
+// workgroups are resident at once (checked when the stage is created) and hand
+// values to each other only through flag words (a value and the number of the
+// exchange it belongs to in one store), never through a grid barrier.
 //
-// Compute waves read every byte the step needs exactly once, in one fixed
-// order per wave: for each layer, the wave's q|k|v weight rows, its cache rows
-// (K, V) of the layer's attention, then its o, gate|up and down weight rows.
-// Each wave keeps S direct-to-LDS loads (global_load_lds_dwordx4, 1 KB per
-// wave) in flight in a private LDS ring and refills a slot as soon as it has
-// consumed it, so the stream runs ahead across phase and layer boundaries
-// while the grid synchronizes.  Compute waves touch global memory only
-// through these loads, never wait for all of them, synchronize with the
-// control wave through s_barrier only, and read LDS through inline ds_read
-// with explicit waits (the compiler does not track direct-to-LDS loads).
+// Compute waves read every weight and cache byte the step needs exactly once,
+// in one fixed order per wave: for each layer, the wave's q|k|v weight rows,
+// its cache rows (K, V) of the layer's attention, then its o, gate|up and down
+// weight rows.  Each wave keeps S direct-to-LDS loads (global_load_lds_dwordx4,
+// 1 KB per wave) in flight in a private LDS ring and refills a slot as soon as
+// it has consumed it, so the stream runs ahead across phase and layer
+// boundaries while the exchanges complete.  Compute waves also poll the
+// exchanged inputs (attention output, residual, SwiGLU output) into LDS; they
+// synchronize with the control wave through s_barrier only and read LDS
+// through inline ds_read with explicit waits (the compiler does not track
+// direct-to-LDS loads).
 //
 // The control wave does the work on the critical path between phases: the
-// epilogues (rotary embedding, residual, SwiGLU), the device-coherent stores
-// of each phase's outputs, the grid barrier, loading and normalizing the next
-// phase's input into LDS, the next phase's scale rows, and the split-KV merge.
+// epilogues (rotary embedding, residual, SwiGLU), publishing each phase's
+// outputs as flag words, the q|k|v and split-partial waits, the next phase's
+// scale rows and norm weights, and the split-KV merge.
 //
 // GEMV phases: a wave owns whole weight rows (all of K); lane l multiplies
 // chunks l, l + 64, ... (32 codes each) with its slice of the input, which it
-// keeps in registers for the whole phase.  Attention: workgroup w < Hkv *
-// nsplit owns kv head w / nsplit and one contiguous split of the cached rows;
-// each compute wave reduces its share of the split to an online-softmax
-// partial, the control wave merges the waves (and this forward's own new row),
-// and the last workgroup of the kv head to arrive merges the splits.
+// keeps in registers for the whole phase.  The down projection (K = SK_CW
+// blocks of 2048) is split by column block instead: wave c takes block c of
+// every row of the workgroup.  Attention: workgroup w < Hkv * nsplit owns kv
+// head w / nsplit and one contiguous split of the cached rows; each compute
+// wave reduces its share of the split to an online-softmax partial, the
+// control wave merges the waves (and this forward's own new row) and publishes
+// the split's partial, and every split's workgroup then merges one slice of
+// the head's outputs over all splits.
+//
+// A wait that does not complete within a.spin_limit polling passes gives up:
+// it sets the stage's error flag, every later wait of the launch polls once,
+// and the launch finishes with invalid outputs that the host reports.
 #include "device.h"
 
 namespace stg {
