@@ -225,6 +225,20 @@ int stage_profile_read(Stage* stage, int* launches, double* total_ms);
  * returned.  n = capacity of out_host in entries.  Synchronizes the device. */
 int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n, int* n_workgroups);
 
+/* Test support: attention record of one layer.  stage_debug_attn_arm(stage,
+ * layer, max_keys) makes later forwards (which then take the per-layer
+ * kernels) record, for that layer, the rotated query of every activation row
+ * and query head, fp32 [M][Hq][head_dim] (before the 1/sqrt(head_dim) scale),
+ * and the attention score q.k / sqrt(head_dim) of every key the row sees,
+ * fp32 [M][Hq][max_keys] by key index j < max_keys (keys it does not see, and
+ * j >= max_keys, are left NaN).  layer = -1 disarms.  UNSUPPORTED with the
+ * vector attention (STAGE_ATTN_VECTOR=1).  stage_debug_attn_read synchronizes
+ * the device and copies the last record to q_host [rows][Hq][head_dim] and
+ * logits_host [rows][Hq][keys] (rows = M of that forward, keys = max_keys; the
+ * caller sizes both for STAGE_MAX_ROWS rows). */
+int stage_debug_attn_arm(Stage* stage, int layer, int max_keys);
+int stage_debug_attn_read(Stage* stage, float* q_host, float* logits_host, int* rows, int* keys);
+
 /* Outcome of the single-launch forwards enqueued so far.  Workgroups of that
  * launch wait on each other's published values; a wait that does not complete
  * within a bounded number of polls (a workgroup held off the device) gives up,

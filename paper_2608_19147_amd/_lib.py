@@ -22,6 +22,7 @@ EXPORTS = (
     "kv_append", "kv_length", "kv_read", "kv_truncate", "stage_forward",
     "stage_debug_dequant", "stage_weight_bytes", "stage_last_error",
     "stage_profile_enable", "stage_profile_read", "stage_debug_phase_trace", "stage_device_status",
+    "stage_debug_attn_arm", "stage_debug_attn_read",
 )
 KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "persistent": 5}
 
@@ -84,6 +85,8 @@ def load() -> ctypes.CDLL:
         "stage_profile_read": (I, [V, P(I), P(ctypes.c_double)]),
         "stage_debug_phase_trace": (I, [V, V, I, V]),
         "stage_device_status": (I, [V]),
+        "stage_debug_attn_arm": (I, [V, I, I]),
+        "stage_debug_attn_read": (I, [V, V, V, P(I), P(I)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

@@ -95,6 +95,9 @@ struct AttnArgs {
     int nsplit_max;
     int vector_path;         // 1: attn_kernel (vector units) instead of attn_mma_kernel
     uint16_t* bp_out; float* bc_out; int kp;   // the attention output also in prepared form (o product input)
+    // test support (null unless armed): the rotated queries [M][Hq][D] and the
+    // scores q.k / sqrt(D) of every visible key [M][Hq][dbg_keys]
+    float* dbg_q; float* dbg_logits; int dbg_keys;
 };
 
 // ---- single-launch stage forward (persistent.hip)

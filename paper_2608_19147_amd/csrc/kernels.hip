@@ -1152,7 +1152,7 @@ __device__ __forceinline__ void lane_pair_k(float v, int sh, float& a, float& b)
 
 // QTW: query tiles per wave per pass (which wave computes a query vector, and
 // when, does not change its arithmetic).
-template <int D, int KVDT, int QTW>
+template <int D, int KVDT, int QTW, bool REC = false>
 __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArgs a) {
     constexpr int HALF = D / 2;
     constexpr int NCH = D / 8;               // 16-byte chunks per cache row
@@ -1330,7 +1330,9 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     float y = 0.f;
-                    if (ok) y = (lo_half ? (xv[e] * cv[e] - xpv[e] * sv[e]) : (xv[e] * cv[e] + xpv[e] * sv[e])) * a.qscale;
+                    if (ok) y = lo_half ? (xv[e] * cv[e] - xpv[e] * sv[e]) : (xv[e] * cv[e] + xpv[e] * sv[e]);
+                    if constexpr (REC) if (ok) a.dbg_q[((size_t)m * Hq + h) * D + d0 + e] = y;
+                    y *= a.qscale;
                     hb[e] = kv_round<KVDT>(y);
                     rb[e] = kv_round<KVDT>(y - kv_float<KVDT>(hb[e]));
                 }
@@ -1407,6 +1409,17 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
                     const float x = e < 4 ? s0[e] : s1[e - 4];
                     sv[e] = (((vbits >> e) & 1u) && ko <= last) ? x : -INFINITY;
                 }
+                if constexpr (REC) {                             // test support: this tile's visible scores
+                    const int r = 16 * (qg + wave + 4 * u) + ql;
+                    if (r < R) {
+                        const size_t row = ((size_t)(rowbase + r / gs) * Hq + g * gs + r % gs) * a.dbg_keys;
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const int j = kbase + ((e < 4) ? e : 12 + e);
+                            if (sv[e] != -INFINITY && j < a.dbg_keys) a.dbg_logits[row + j] = sv[e] * 0.69314718055994531f;
+                        }
+                    }
+                }
                 float mx = sv[0];
 #pragma unroll
                 for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
@@ -1479,12 +1492,17 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int queries_per_ite
     const bool wide = queries_per_item_max > 4;
     const bool bf = a.kv_dt == DT_BF16;
     const bool one = queries_per_item_max <= 64;                // every item's query tiles: one per wave
+#define ATTN_MMA_R(D_, R_)                                                                        \
+    do {                                                                                          \
+        if (bf && one) attn_mma_kernel<D_, DT_BF16, 1, R_><<<grid, block, 0, st>>>(a);            \
+        else if (bf) attn_mma_kernel<D_, DT_BF16, 2, R_><<<grid, block, 0, st>>>(a);              \
+        else if (one) attn_mma_kernel<D_, DT_F16, 1, R_><<<grid, block, 0, st>>>(a);              \
+        else attn_mma_kernel<D_, DT_F16, 2, R_><<<grid, block, 0, st>>>(a);                       \
+    } while (0)
 #define ATTN_MMA(D_)                                                                              \
     do {                                                                                          \
-        if (bf && one) attn_mma_kernel<D_, DT_BF16, 1><<<grid, block, 0, st>>>(a);                \
-        else if (bf) attn_mma_kernel<D_, DT_BF16, 2><<<grid, block, 0, st>>>(a);                  \
-        else if (one) attn_mma_kernel<D_, DT_F16, 1><<<grid, block, 0, st>>>(a);                  \
-        else attn_mma_kernel<D_, DT_F16, 2><<<grid, block, 0, st>>>(a);                           \
+        if (a.dbg_logits) ATTN_MMA_R(D_, true);          /* test support: record queries and scores */ \
+        else ATTN_MMA_R(D_, false);                                                               \
     } while (0)
     if (head_dim == 128) {
         if (!a.vector_path) ATTN_MMA(128);
@@ -1500,6 +1518,7 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int queries_per_ite
         return hipErrorInvalidValue;
     }
 #undef ATTN_MMA
+#undef ATTN_MMA_R
     return hipGetLastError();
 }
 

@@ -92,6 +92,9 @@ struct Stage {
     size_t ps_wl[4] = {0, 0, 0, 0};                            // bytes per layer in each slab
     unsigned* err = nullptr;
     unsigned spin_limit = 1u << 20;                     // exchange wait passes (STAGE_PS_SPIN_LIMIT)
+    int dbg_layer = -1, dbg_keys = 0, dbg_rows = 0;     // armed attention record (test support)
+    float* dbg_q = nullptr;                             // [MAX_ROWS][Hq][D]
+    float* dbg_logits = nullptr;                        // [MAX_ROWS][Hq][dbg_keys]
     int ps_nwg = 0;
     int n_cus = 0;                                      // compute units of the device
     int ps_rpw_qkv = 0, ps_rpw_h = 0, ps_rpw_gu = 0;    // rows per workgroup of the single-launch forward
@@ -573,6 +576,42 @@ int stage_destroy(Stage* stage) {
 
 int64_t stage_weight_bytes(const Stage* stage) { return stage ? stage->weight_bytes : -1; }
 
+int stage_debug_attn_arm(Stage* st, int layer, int max_keys) {
+    if (!st) return fail(STAGE_E_INVALID, "NULL argument");
+    if (layer < 0) {
+        st->dbg_layer = -1;
+        return STAGE_OK;
+    }
+    if (layer >= st->cfg.n_layers || max_keys < 1) return fail(STAGE_E_INVALID, "layer or max_keys out of range");
+    if (st->attn_vector) return fail(STAGE_E_UNSUPPORTED, "the attention record needs the matrix-core attention");
+    HIP_TRY(hipSetDevice(st->device));
+    const size_t Hq = (size_t)st->cfg.n_q_heads;
+    if (max_keys > st->dbg_keys) {                      // buffers grow only (freed with the stage)
+        int rc;
+        if ((rc = st->alloc(&st->dbg_q, (size_t)MAX_ROWS * Hq * st->cfg.head_dim)) ||
+            (rc = st->alloc(&st->dbg_logits, (size_t)MAX_ROWS * Hq * max_keys)))
+            return rc;
+        st->dbg_keys = max_keys;
+    }
+    st->dbg_layer = layer;
+    st->dbg_rows = 0;
+    return STAGE_OK;
+}
+
+int stage_debug_attn_read(Stage* st, float* q_host, float* logits_host, int* rows, int* keys) {
+    if (!st || !q_host || !logits_host || !rows || !keys) return fail(STAGE_E_INVALID, "NULL argument");
+    if (st->dbg_layer < 0 || st->dbg_rows == 0) return fail(STAGE_E_INVALID, "no armed attention record was taken");
+    HIP_TRY(hipSetDevice(st->device));
+    HIP_TRY(hipDeviceSynchronize());
+    const size_t Hq = (size_t)st->cfg.n_q_heads;
+    HIP_TRY(hipMemcpy(q_host, st->dbg_q, (size_t)st->dbg_rows * Hq * st->cfg.head_dim * sizeof(float), hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(logits_host, st->dbg_logits, (size_t)st->dbg_rows * Hq * st->dbg_keys * sizeof(float),
+                      hipMemcpyDeviceToHost));
+    *rows = st->dbg_rows;
+    *keys = st->dbg_keys;
+    return STAGE_OK;
+}
+
 int stage_device_status(Stage* st) {
     if (!st) return fail(STAGE_E_INVALID, "NULL argument");
     if (!st->err) return STAGE_OK;                      // the stage has no single-launch forward
@@ -961,7 +1000,8 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     // ---------------- one launch for the whole stage: a single decode row
     const int RPS = 512 / D;                               // cache rows per 1 KB slot
     int nsplit = 0, split_len = 0, att_T = 0;
-    bool single = st->ps_ok && M == 1 && (st->prof_class < 0 || st->prof_class == STAGE_KERNEL_PERSISTENT);
+    bool single = st->ps_ok && M == 1 && (st->prof_class < 0 || st->prof_class == STAGE_KERNEL_PERSISTENT) &&
+                  st->dbg_layer < 0;                        // an armed attention record takes the per-layer kernels
     if (single) {
         const int P = reqs[0].state->P;
         // splits per kv head: a power of two; each split's merge slice is a multiple of 8 outputs
@@ -1129,6 +1169,13 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             // and is the stride of the partials
             a.nsplit_max = max_splits;
             a.vector_path = st->attn_vector;
+            if (l == st->dbg_layer && !st->attn_vector) {    // test support: record this layer's queries and scores
+                HIP_TRY(hipMemsetAsync(st->dbg_logits, 0xFF, (size_t)M * Hq * st->dbg_keys * sizeof(float), s));   // NaN
+                a.dbg_q = st->dbg_q;
+                a.dbg_logits = st->dbg_logits;
+                a.dbg_keys = st->dbg_keys;
+                st->dbg_rows = M;
+            }
             if (use_bp) {
                 a.bp_out = st->bp[1 - bcur];
                 a.bc_out = st->bc[1 - bcur];

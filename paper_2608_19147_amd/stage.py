@@ -104,6 +104,25 @@ class Stage:
         check(self.lib.stage_profile_read(self.handle, ctypes.byref(n), ctypes.byref(ms)))
         return n.value, ms.value
 
+    def debug_attn_arm(self, layer: int, max_keys: int) -> None:
+        """Record `layer`'s rotated queries and visible scores in later forwards
+        (per-layer kernels); layer = -1 disarms."""
+        check(self.lib.stage_debug_attn_arm(self.handle, layer, max_keys))
+        if layer >= 0:
+            self._dbg_cap = max(getattr(self, "_dbg_cap", 0), max_keys)   # the library's buffers only grow
+
+    def debug_attn_read(self):
+        """(q [M, Hq, D], logits [M, Hq, max_keys]) of the last armed forward;
+        keys a row does not see are NaN."""
+        sh = self.shape
+        q = np.empty(64 * sh.n_q_heads * sh.head_dim, np.float32)
+        rows, keys = ctypes.c_int(), ctypes.c_int()
+        lg = np.empty(64 * sh.n_q_heads * self._dbg_cap, np.float32)
+        check(self.lib.stage_debug_attn_read(self.handle, q.ctypes.data, lg.ctypes.data, ctypes.byref(rows), ctypes.byref(keys)))
+        m, k = rows.value, keys.value
+        return (q[: m * sh.n_q_heads * sh.head_dim].reshape(m, sh.n_q_heads, sh.head_dim),
+                lg[: m * sh.n_q_heads * k].reshape(m, sh.n_q_heads, k))
+
     def device_status(self) -> None:
         """Wait for the last single-launch forward; raise StageError
         (STAGE_E_DEVICE) once if a forward of this stage gave up waiting on

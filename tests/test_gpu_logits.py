@@ -1,0 +1,138 @@
+"""Attention logits within 1e-3 relative, fp32-accumulated.
+
+The matrix-core attention records, for one armed layer, the rotated query of
+every activation row and query head and the score q.k / sqrt(D) of every key
+that row sees (stage_debug_attn_arm / _read).  Each recorded row is compared
+with the score recomputed in fp64 from the GPU's own recorded query and the
+cache rows as the slot sees them (kv_read), so the check measures the kernel's
+accumulation, not the upstream rounding of q (which the 2e-2 stage tolerance
+covers).  Bar: |s_gpu - s_ref| <= 1e-3 * max_j |s_ref| per (row, head); the
+set of keys that carry a score equals the visible set exactly (mask and
+causality are integer decisions); the recorded query matches the oracle's
+rotated query within the stage tolerance."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_cases import TOL_STAGE, Pair, host, rel_err, req, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+TOL_LOGIT = 1e-3
+
+
+def _per_layer_pair(shape, seed):
+    old = os.environ.get("STAGE_PERSISTENT")
+    os.environ["STAGE_PERSISTENT"] = "0"
+    try:
+        return Pair(shape, seed)
+    finally:
+        if old is None:
+            del os.environ["STAGE_PERSISTENT"]
+        else:
+            os.environ["STAGE_PERSISTENT"] = old
+
+
+def _check_logits(shape, q, logits, rows):
+    """rows: list of (m, state, slot, P, i, mask_row) for every activation row."""
+    D, gs = shape.head_dim, shape.n_q_heads // shape.n_kv_heads
+    worst = 0.0
+    for m, g, b, P, i, mrow in rows:
+        L = P + 1 + i                                     # keys 0 .. P + i (physical causality)
+        k, _ = g.read(0, b, 0, L)
+        K = k.double().cpu().numpy()                      # [Hkv, L, D] as the slot sees them
+        vis = np.nonzero(mrow[:L] != 0)[0]
+        for h in range(shape.n_q_heads):
+            got = logits[m, h]
+            assert np.array_equal(np.nonzero(np.isfinite(got))[0], vis), (m, h)
+            ref = K[h // gs, vis] @ q[m, h].astype(np.float64) / np.sqrt(D)
+            err = np.max(np.abs(got[vis] - ref)) / np.max(np.abs(ref))
+            worst = max(worst, err)
+    print(f"worst logit error {worst:.2e} of the row's largest |logit|")
+    assert worst <= TOL_LOGIT, worst
+    return worst
+
+
+def _oracle_q(p, layer0, x, positions):
+    """Layer-0 rotated queries of the oracle [rows, Hq, D] (before 1/sqrt(D))."""
+    sh = p.shape
+    h = oracle.rmsnorm(host(x), layer0.attn_norm.double().numpy(), sh.rms_eps)
+    wq = layer0.mats["wq"]
+    q = (oracle.dequant(wq.q, wq.scales, wq.k, sh.group_size) @ h.T).T.reshape(-1, sh.n_q_heads, sh.head_dim)
+    return np.stack([oracle.apply_rope(q[r], np.array([positions[r]]), sh.rope_theta) for r in range(len(q))])
+
+
+def test_tiny_logits_verify_holes_beams():
+    """Tiny 2-layer stage (fp16 cache), two slots with holes and a beam
+    permutation, 5-token verify with the last two drafts masked."""
+    shape = synth.with_layers(synth.TINY, 2)
+    p = _per_layer_pair(shape, 71)
+    S, P, n = 2, 72, 5
+    g, _ = p.states(S, P, 128, seed=71)
+    holes = np.ones((S, P), np.uint8)
+    holes[0, [3, 10, 40]] = 0
+    holes[1, [0, 7, 71]] = 0
+    mask = np.concatenate([holes, np.ones((S, n), np.uint8)], axis=1)
+    mask[:, P + 3:] = 0
+    pos = holes.sum(axis=1, keepdims=True) + np.arange(n)[None]
+    beam = np.array([1, 0], np.int32)
+    x = synth.make_hidden(shape, S * n, 71)
+    p.gpu.debug_attn_arm(0, P + n)
+    run_gpu(p, [req(g, pos, mask, beam)], x)
+    q, logits = p.gpu.debug_attn_read()
+    p.gpu.debug_attn_arm(-1, 1)
+    assert q.shape == (S * n, shape.n_q_heads, shape.head_dim)
+    rows = [(b * n + i, g, b, P, i, mask[b]) for b in range(S) for i in range(n)]
+    _check_logits(shape, q, logits, rows)
+    assert rel_err(q, _oracle_q(p, p.layers[0], x, pos.reshape(-1))) <= TOL_STAGE
+
+
+def test_tiny_logits_microbatch():
+    """Two requests (decode and verify) in one forward: rows of each request
+    are recorded against that request's own cache."""
+    shape = synth.TINY
+    p = _per_layer_pair(shape, 72)
+    plan = [(40, 1), (63, 5)]
+    reqs, rows, poss, m0 = [], [], [], 0
+    for r, (P, n) in enumerate(plan):
+        g, _ = p.states(1, P, P + 8, seed=72, stream=r)
+        holes = synth.hole_mask(P, 0.1, 72, r)
+        holes[-1] = 1
+        mrow = np.concatenate([holes, np.ones(n, np.uint8)])
+        pos = (int(holes.sum()) + np.arange(n))[None]
+        reqs.append(req(g, pos, mrow[None]))
+        rows += [(m0 + i, g, 0, P, i, mrow) for i in range(n)]
+        poss.append(pos.reshape(-1))
+        m0 += n
+    x = synth.make_hidden(shape, m0, 72)
+    p.gpu.debug_attn_arm(0, 80)
+    run_gpu(p, reqs, x)
+    q, logits = p.gpu.debug_attn_read()
+    p.gpu.debug_attn_arm(-1, 1)
+    _check_logits(shape, q, logits, rows)
+    assert rel_err(q, _oracle_q(p, p.layers[0], x, np.concatenate(poss))) <= TOL_STAGE
+
+
+def test_8b_layer_logits_verify_kv2048():
+    """One 8B layer (bf16 cache): 4 slots x 5 tokens from KV 2048, identity beam,
+    10% holes in the cache, the last draft of each slot masked."""
+    shape = synth.with_layers(synth.LLAMA8B_HALF, 1)
+    p = _per_layer_pair(shape, 73)
+    S, P, n = 4, 2048, 5
+    g, _ = p.states(S, P, P + 8, seed=73, with_oracle=False)
+    holes = np.stack([synth.hole_mask(P, 0.1, 73, b) for b in range(S)])
+    holes[:, -1] = 1
+    mask = np.concatenate([holes, np.ones((S, n), np.uint8)], axis=1)
+    mask[:, P + 4] = 0
+    pos = holes.sum(axis=1, keepdims=True) + np.arange(n)[None]
+    x = synth.make_hidden(shape, S * n, 73)
+    p.gpu.debug_attn_arm(0, P + n)
+    run_gpu(p, [req(g, pos, mask, np.arange(S, dtype=np.int32))], x)
+    q, logits = p.gpu.debug_attn_read()
+    p.gpu.debug_attn_arm(-1, 1)
+    rows = [(b * n + i, g, b, P, i, mask[b]) for b in range(S) for i in range(n)]
+    _check_logits(shape, q, logits, rows)
+    assert rel_err(q, _oracle_q(p, p.layers[0], x, pos.reshape(-1))) <= TOL_STAGE
