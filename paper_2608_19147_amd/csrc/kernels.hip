@@ -404,12 +404,11 @@ hipError_t launch_gemv(const GemvArgs& a, hipStream_t st) {
 typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-// (x & m) | c in one instruction (v_bfi_b32; mask from an SGPR, constant in a VGPR).
-__device__ __forceinline__ uint32_t bfi_u32(uint32_t m, uint32_t x, uint32_t c) {
-    uint32_t r;
-    asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "s"(m), "v"(x), "v"(c));
-    return r;
-}
+// (x & m) | c, written as plain arithmetic (one v_and_or_b32).  Its results feed
+// matrix-core operands, so it must stay visible to the compiler: the wait states
+// required between a vector write and a matrix-core read of the same register
+// are inserted only for instructions the compiler itself emits.
+__device__ __forceinline__ uint32_t and_or_u32(uint32_t m, uint32_t x, uint32_t c) { return (x & m) | c; }
 
 // ------------------------------------------------------------------ prepared-operand products
 //
@@ -628,10 +627,10 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
             for (int i = 0; i < 4; ++i) {
                 const uint32_t x = wv[rt][i], y = x >> 8;
                 u32x4 av;
-                av[0] = bfi_u32(0x000F000Fu, x, magic);
-                av[1] = bfi_u32(0x00F000F0u, x, magic);
-                av[2] = bfi_u32(0x000F000Fu, y, magic);
-                av[3] = bfi_u32(0x00F000F0u, y, magic);
+                av[0] = and_or_u32(0x000F000Fu, x, magic);
+                av[1] = and_or_u32(0x00F000F0u, x, magic);
+                av[2] = and_or_u32(0x000F000Fu, y, magic);
+                av[3] = and_or_u32(0x00F000F0u, y, magic);
                 A[i] = __builtin_bit_cast(half8_t, av);
             }
             float scl[4];
