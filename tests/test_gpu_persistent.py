@@ -143,3 +143,32 @@ def test_exchange_give_up_is_reported():
     out = run_gpu(good, [req(gg, pos, mask, [0])], x)
     good.gpu.device_status()
     assert rel_err(out, oracle.forward(good.orc, o, host(x), pos, np.array([0]), mask)) <= TOL_STAGE
+
+
+def test_cooperative_launch_matches_plain_launch():
+    """STAGE_COOP=1 launches the single-launch forward cooperatively (the
+    runtime checks co-residency per launch); the kernel and its arithmetic are
+    the same, so the output is bitwise that of the plain launch, and both
+    match the oracle (8B shape, two layers, KV 512)."""
+    shape = synth.with_layers(synth.LLAMA8B_HALF, 2)
+    layers = synth.make_weights(shape, 45)
+    plain = _pair(shape, 45, True, layers)
+    old = os.environ.get("STAGE_COOP")
+    os.environ["STAGE_COOP"] = "1"
+    try:
+        coop = _pair(shape, 45, True, layers)
+    finally:
+        if old is None:
+            del os.environ["STAGE_COOP"]
+        else:
+            os.environ["STAGE_COOP"] = old
+    P = 512
+    x = synth.make_hidden(shape, 1, 45)
+    pos, mask = np.array([[P]]), full_mask(1, P + 1)
+    gp, o = plain.states(1, P, P + 4, seed=45)
+    gc, _ = coop.states(1, P, P + 4, seed=45, with_oracle=False)
+    out_p = run_gpu(plain, [req(gp, pos, mask, [0])], x)
+    out_c = run_gpu(coop, [req(gc, pos, mask, [0])], x)
+    coop.gpu.device_status()
+    assert np.array_equal(out_p, out_c)
+    assert rel_err(out_c, oracle.forward(plain.orc, o, host(x), pos, np.array([0]), mask)) <= TOL_STAGE
