@@ -136,3 +136,26 @@ def test_8b_layer_logits_verify_kv2048():
     rows = [(b * n + i, g, b, P, i, mask[b]) for b in range(S) for i in range(n)]
     _check_logits(shape, q, logits, rows)
     assert rel_err(q, _oracle_q(p, p.layers[0], x, pos.reshape(-1))) <= TOL_STAGE
+
+
+def test_8b_layer_logits_64_tokens_kv2048():
+    """One 8B layer: one slot verifying 64 tokens (the row limit) from KV 2048
+    with 10% holes and the last 14 drafts masked: 256 query vectors per kv
+    head, so two query tiles per wave and two passes over each split's keys."""
+    shape = synth.with_layers(synth.LLAMA8B_HALF, 1)
+    p = _per_layer_pair(shape, 74)
+    P, n = 2048, 64
+    g, _ = p.states(1, P, P + n + 4, seed=74, with_oracle=False)
+    holes = synth.hole_mask(P, 0.1, 74, 0)
+    holes[-1] = 1
+    mask = np.concatenate([holes, np.ones(n, np.uint8)])[None]
+    mask[0, P + 50:] = 0
+    pos = (int(holes.sum()) + np.arange(n))[None]
+    x = synth.make_hidden(shape, n, 74)
+    p.gpu.debug_attn_arm(0, P + n)
+    run_gpu(p, [req(g, pos, mask)], x)
+    q, logits = p.gpu.debug_attn_read()
+    p.gpu.debug_attn_arm(-1, 1)
+    rows = [(i, g, 0, P, i, mask[0]) for i in range(n)]
+    _check_logits(shape, q, logits, rows)
+    assert rel_err(q, _oracle_q(p, p.layers[0], x, pos.reshape(-1))) <= TOL_STAGE
