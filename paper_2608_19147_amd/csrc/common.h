@@ -219,6 +219,7 @@ hipError_t launch_bprep(const void* in, int in_dt, int in_ld, const uint16_t* ga
                         int M, uint16_t* bp, float* bc, int kp, float* rs_out, hipStream_t st);
 // queries_per_item_max: the largest (rows of an item) x (query heads per kv head).
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int queries_per_item_max, hipStream_t st);
+hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t st);
 hipError_t launch_table_gather(const int16_t* src, int16_t* dst, const int* beam, int S, int cap, int P, hipStream_t st);
 hipError_t launch_kv_append(uint16_t* kc, uint16_t* vc, int16_t* table, const uint16_t* k, const uint16_t* v,
                             int L, int S, int Hkv, int cap, int D, int P, int n, hipStream_t st);

@@ -1521,6 +1521,20 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int queries_per_ite
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ fill
+
+// p[0 .. n) = v (a kernel rather than a memset node, so forwards stay safe to capture in graphs).
+__global__ __launch_bounds__(256) void fill_u32_kernel(uint32_t* __restrict__ p, size_t n, uint32_t v) {
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
+}
+
+hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t st) {
+    if (n == 0) return hipSuccess;
+    const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 4096);
+    fill_u32_kernel<<<blocks, 256, 0, st>>>(p, n, v);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ KV state kernels
 
 __global__ void table_gather_kernel(const int16_t* __restrict__ src, int16_t* __restrict__ dst, const int* __restrict__ beam,

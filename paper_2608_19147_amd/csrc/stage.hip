@@ -1170,7 +1170,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             a.nsplit_max = max_splits;
             a.vector_path = st->attn_vector;
             if (l == st->dbg_layer && !st->attn_vector) {    // test support: record this layer's queries and scores
-                HIP_TRY(hipMemsetAsync(st->dbg_logits, 0xFF, (size_t)M * Hq * st->dbg_keys * sizeof(float), s));   // NaN
+                HIP_TRY(launch_fill_u32((uint32_t*)st->dbg_logits, (size_t)M * Hq * st->dbg_keys, 0xFFFFFFFFu, s));   // NaN
                 a.dbg_q = st->dbg_q;
                 a.dbg_logits = st->dbg_logits;
                 a.dbg_keys = st->dbg_keys;
