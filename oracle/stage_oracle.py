@@ -59,9 +59,13 @@ ORACLE_BLOCK_ROWS = 1024
 
 def round_rne(x, fmt: str) -> np.ndarray:
     """Round fp64 values to the nearest value of an IEEE-style binary format
-    (ties to even), returned as fp64.  Subnormals are kept, not flushed."""
-    sig, emin = _FORMATS[fmt]
+    (ties to even), returned as fp64.  Subnormals are kept, not flushed.
+    ``"f64"`` keeps the values as they are: a cache stored at full precision,
+    which the composition pin uses to compare with an unrounded reference."""
     x = np.asarray(x, dtype=np.float64)
+    if fmt == "f64":
+        return x.copy()
+    sig, emin = _FORMATS[fmt]
     _, e = np.frexp(x)                      # x = m * 2**e with 0.5 <= |m| < 1
     e = np.maximum(e, emin + 1)             # below the normal range the spacing is fixed
     quantum = np.ldexp(np.ones_like(x), e - sig)

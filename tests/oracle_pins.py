@@ -390,4 +390,119 @@ def pin_gqa_is_repeated_mha():
     assert np.array_equal(oracle.forward(st_g, g_state, x, pos), oracle.forward(st_m, m_state, x, pos))
 
 
+# ------------------------------------------------------------------ layer composition vs the HF Llama layer
+
+def _hf_rope(positions, d, theta):
+    """(cos, sin) [1, T, D] in float64 in the HF layout (angles repeated over
+    both halves), for positions [T]."""
+    inv = theta ** (-torch.arange(0, d, 2, dtype=torch.float64) / d)
+    fr = torch.as_tensor(positions, dtype=torch.float64)[:, None] * inv[None]
+    emb = torch.cat([fr, fr], dim=-1)
+    return emb.cos()[None], emb.sin()[None]
+
+
+def _hf_layers(shape, layers):
+    """transformers' LlamaDecoderLayer per stage layer, in float64, holding the
+    oracle's dequantized weights and the stage's norm weights."""
+    from transformers import LlamaConfig
+    from transformers.models.llama.modeling_llama import LlamaDecoderLayer
+
+    cfg = LlamaConfig(hidden_size=shape.hidden, intermediate_size=shape.ffn, num_attention_heads=shape.n_q_heads,
+                      num_key_value_heads=shape.n_kv_heads, head_dim=shape.head_dim, rms_norm_eps=shape.rms_eps,
+                      num_hidden_layers=shape.n_layers, attention_bias=False, mlp_bias=False,
+                      rope_theta=shape.rope_theta)
+    cfg._attn_implementation = "sdpa"
+    out = []
+    for l, lay in enumerate(layers):
+        m = LlamaDecoderLayer(cfg, l).double()
+        g = shape.group_size
+
+        def wt(name):
+            q = lay.mats[name]
+            return torch.from_numpy(oracle.dequant(q.q, q.scales, q.k, g))
+
+        with torch.no_grad():
+            for mod, name in ((m.self_attn.q_proj, "wq"), (m.self_attn.k_proj, "wk"), (m.self_attn.v_proj, "wv"),
+                              (m.self_attn.o_proj, "wo"), (m.mlp.gate_proj, "wg"), (m.mlp.up_proj, "wu"),
+                              (m.mlp.down_proj, "wd")):
+                mod.weight.copy_(wt(name))
+            m.input_layernorm.weight.copy_(torch.from_numpy(f64(lay.attn_norm)))
+            m.post_attention_layernorm.weight.copy_(torch.from_numpy(f64(lay.ffn_norm)))
+        out.append(m)
+    return out
+
+
+def pin_layer_composition_matches_hf_llama():
+    """Two decoder layers of the oracle against transformers' LlamaDecoderLayer
+    in float64 (the Llama layer the paper's shards trace, "Per-Stage Export
+    Pipeline"): a 5-token prefill at P = 0, then 3 tokens over the stored cache
+    with one past column and one new-token column masked.  The KV cache keeps
+    full precision here (format "f64"), so the two sides differ only by
+    rounding: HF's RMSNorm computes in float32 (about 1e-8 relative), far below
+    what a wiring mistake (gate/up order, which norm weight goes where, a
+    residual tap) moves the output."""
+    import dataclasses
+
+    shape = dataclasses.replace(TINY2, name="tiny2-f64kv", kv_dtype="f64")
+    layers = synth.make_weights(TINY2, 101)
+    st, _ = oracle_stage(shape, layers=layers)
+    state = oracle.OracleState(shape, 1, 16)
+    x1 = f64(synth.make_hidden(TINY2, 5, 101, 1))
+    x2 = f64(synth.make_hidden(TINY2, 3, 101, 2))
+    out1 = oracle.forward(st, state, x1, np.arange(5)[None])
+    mask2 = np.ones((1, 8), dtype=np.uint8)
+    mask2[0, 2] = 0                                    # a rewound past position
+    mask2[0, 6] = 0                                    # a rejected draft among the new tokens
+    pos2 = logical_positions(mask2[0, :5], 3)
+    out2 = oracle.forward(st, state, x2, pos2, None, mask2)
+
+    allowed = np.tril(np.ones((8, 8), dtype=bool))
+    allowed[5:] &= mask2[0] != 0
+    cos, sin = _hf_rope(np.concatenate([np.arange(5), pos2[0]]), shape.head_dim, shape.rope_theta)
+    h = torch.from_numpy(np.concatenate([x1, x2]))[None]
+    am = torch.from_numpy(allowed)[None, None]
+    with torch.no_grad():
+        for m in _hf_layers(shape, layers):
+            h = m(h, attention_mask=am, position_embeddings=(cos, sin))
+    ref = h[0].numpy()
+    got = np.concatenate([out1, out2])
+    err = np.max(np.abs(got - ref)) / np.max(np.abs(ref))
+    assert err <= 1e-6, err
+
+
+def pin_stored_rows_closed_form():
+    """The cache rows a forward appends are round_kv(rotary(W_k rmsnorm(x)))
+    and round_kv(W_v rmsnorm(x)), with rotary after the projection and the
+    rounding last; checked with torch's rms_norm, HF's rotate-half rotary and
+    torch's fp16 / bf16 conversion, for both KV dtypes."""
+    import dataclasses
+
+    from transformers.models.llama.modeling_llama import apply_rotary_pos_emb
+
+    for kv in (synth.F16, synth.BF16):
+        shape = dataclasses.replace(TINY, name="tiny-" + kv, kv_dtype=kv)
+        layers = synth.make_weights(shape, 111)
+        st, _ = oracle_stage(shape, layers=layers)
+        state = oracle.OracleState(shape, 1, 8)
+        x = f64(synth.make_hidden(shape, 3, 111))
+        pos = np.array([7, 300, 4000])
+        oracle.forward(st, state, x, pos[None])
+        lay = layers[0]
+        g = shape.group_size
+        wk = torch.from_numpy(oracle.dequant(lay.mats["wk"].q, lay.mats["wk"].scales, lay.mats["wk"].k, g))
+        wv = torch.from_numpy(oracle.dequant(lay.mats["wv"].q, lay.mats["wv"].scales, lay.mats["wv"].k, g))
+        hn = F.rms_norm(torch.from_numpy(x), (shape.hidden,), weight=torch.from_numpy(f64(lay.attn_norm)),
+                        eps=shape.rms_eps)
+        d, hkv = shape.head_dim, shape.n_kv_heads
+        k = (hn @ wk.T).reshape(3, hkv, d).transpose(0, 1)[None]          # [1, Hkv, 3, D]
+        v = (hn @ wv.T).reshape(3, hkv, d).transpose(0, 1)
+        cos, sin = _hf_rope(pos, d, shape.rope_theta)
+        _, k_rot = apply_rotary_pos_emb(k, k, cos, sin)
+        tdt = torch.float16 if kv == synth.F16 else torch.bfloat16
+        k_ref = k_rot[0].to(tdt).double().numpy()
+        v_ref = v.to(tdt).double().numpy()
+        assert np.array_equal(state.K[0][0, :, :3], k_ref), kv
+        assert np.array_equal(state.V[0][0, :, :3], v_ref), kv
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

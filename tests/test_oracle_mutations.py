@@ -80,15 +80,74 @@ def _attn_factory(kind):
 
 
 def _round_trunc(x, fmt):
-    sig, emin = so._FORMATS[fmt]
     x = np.asarray(x, dtype=np.float64)
+    if fmt == "f64":
+        return x.copy()
+    sig, emin = so._FORMATS[fmt]
     _, e = np.frexp(x)
     e = np.maximum(e, emin + 1)
     q = np.ldexp(np.ones_like(x), e - sig)
     return np.trunc(x / q) * q
 
 
+def _forward_factory(kind):
+    """A copy of the oracle's forward with one wiring mistake in the layer."""
+
+    def fwd(stage, state, x, positions, beam_idx=None, mask=None):
+        sh = stage.shape
+        positions = np.asarray(positions, dtype=np.int64)
+        S, n = positions.shape
+        P = state.P
+        if mask is None:
+            mask = np.ones((S, P + n), dtype=np.uint8)
+        mask = np.asarray(mask)
+        x = np.array(x, dtype=np.float64).reshape(S * n, sh.hidden)
+        if beam_idx is not None:
+            bi = np.asarray(beam_idx, dtype=np.int64)
+            for l in range(sh.n_layers):
+                state.K[l] = state.K[l][bi].copy()
+                state.V[l] = state.V[l][bi].copy()
+        D, Hq, Hkv = sh.head_dim, sh.n_q_heads, sh.n_kv_heads
+        for l in range(sh.n_layers):
+            w = stage.weights(l)
+            n_attn, n_ffn = ("ffn_norm", "attn_norm") if kind == "norm_swap" else ("attn_norm", "ffn_norm")
+            h = so.rmsnorm(x, w[n_attn], sh.rms_eps)
+            q = so.gemv_rows(h, w["wq"]).reshape(S, n, Hq, D)
+            k = so.gemv_rows(h, w["wk"]).reshape(S, n, Hkv, D)
+            v = so.gemv_rows(h, w["wv"]).reshape(S, n, Hkv, D)
+            q = so.apply_rope(q, positions[:, :, None], sh.rope_theta)
+            if kind == "round_before_rope":
+                k = so.apply_rope(so.round_rne(k, sh.kv_dtype), positions[:, :, None], sh.rope_theta)
+            else:
+                k = so.apply_rope(k, positions[:, :, None], sh.rope_theta)
+                if kind != "no_kv_round":
+                    k = so.round_rne(k, sh.kv_dtype)
+            if kind != "no_kv_round":
+                v = so.round_rne(v, sh.kv_dtype)
+            state.K[l][:, :, P:P + n] = k.transpose(0, 2, 1, 3)
+            state.V[l][:, :, P:P + n] = v.transpose(0, 2, 1, 3)
+            o = np.empty_like(q)
+            for b in range(S):
+                o[b] = so.attention_slot(q[b], state.K[l][b], state.V[l][b], P, mask[b])
+            h_attn = x
+            x = x + so.gemv_rows(o.reshape(S * n, Hq * D), w["wo"])
+            h2 = so.rmsnorm(h_attn if kind == "ffn_norm_on_h" else x, w[n_ffn], sh.rms_eps)
+            if kind == "gate_up_swap":
+                act = so.silu(so.gemv_rows(h2, w["wu"])) * so.gemv_rows(h2, w["wg"])
+            else:
+                act = so.silu(so.gemv_rows(h2, w["wg"])) * so.gemv_rows(h2, w["wu"])
+            x = x + so.gemv_rows(act, w["wd"])
+        state.P = P + n
+        return x
+    return fwd
+
+
 MUTANTS = {
+    "gate_up_swap": ("forward", _forward_factory("gate_up_swap")),
+    "norm_swap": ("forward", _forward_factory("norm_swap")),
+    "round_before_rope": ("forward", _forward_factory("round_before_rope")),
+    "no_kv_round": ("forward", _forward_factory("no_kv_round")),
+    "ffn_norm_on_h": ("forward", _forward_factory("ffn_norm_on_h")),
     "nibble_order": ("unpack_int4", _unpack_swapped),
     "rope_sign": ("apply_rope", _rope_sign),
     "rope_interleaved": ("apply_rope", _rope_interleaved),
