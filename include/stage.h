@@ -27,8 +27,15 @@
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *    Device work is stream-ordered and asynchronous; host metadata arrays are
  *    copied before the call returns and may be reused immediately.
- *  - Calls on one Stage (and on the KV states it allocated) must be
- *    serialized by the caller.  Overlapping calls on one stage race.
+ *  - Calls on one Stage (and on the KV states it allocated) must be made
+ *    from one host thread at a time.  Their device work runs in call order
+ *    even across streams: a call issued on a different stream than the
+ *    previous call on the stage first makes its stream wait for that call's
+ *    work (the workspace, metadata buffer and exchange flag numbers are per
+ *    stage), so two forwards of one stage never overlap on the device.
+ *  - stage_forward must not be captured into a HIP graph: each call takes
+ *    its exchange flag numbers, metadata buffer slot and beam-table side from
+ *    host state at call time, and a replayed capture would reuse stale ones.
  *  - Dtype codes: STAGE_DTYPE_F16 = IEEE half, STAGE_DTYPE_BF16 = bfloat16.
  */
 #ifndef PAPER_2608_19147_STAGE_H
@@ -103,9 +110,12 @@ typedef struct LayerWeights {
 typedef struct Stage Stage;
 typedef struct KVState KVState;
 
-/* Create a stage.  Copies and repacks every weight into library-owned device
- * memory (the caller may free its copies when the call returns), builds the
- * rotary table and sizes the workspace for STAGE_MAX_ROWS rows.
+/* Create a stage: one shard of the paper's pipeline, a contiguous range of
+ * decoder layers ("Per-Stage Export Pipeline", Steps 1-4: layer range, rotary
+ * precomputation, stateful KV, INT4 group-128 weights).  Copies and repacks
+ * every weight into library-owned device memory (the caller may free its
+ * copies when the call returns), builds the rotary table and sizes the
+ * workspace for STAGE_MAX_ROWS rows.
  * layers: host array of cfg->n_layers entries; weight pointers are host
  * pointers if weights_on_device == 0, device pointers otherwise.
  * Errors: INVALID/SHAPE/UNSUPPORTED for a bad config or matrix dims, OOM, HIP. */
@@ -125,7 +135,8 @@ int kv_state_reset(KVState* state);
 
 /* Append n_tokens already-stored rows (K after rotary, V raw) for every
  * layer, slot and kv head at physical rows P..P+n-1 of each slot, then
- * P += n.  k, v: [L][S][Hkv][n][D] in kv_dtype; host pointers if on_device == 0
+ * P += n: the Concat -> Assign step of the paper's stateful KV ("Stateful
+ * KV-Cached Inference"), used to seed a state with an existing cache.  k, v: [L][S][Hkv][n][D] in kv_dtype; host pointers if on_device == 0
  * (copied before return), device pointers otherwise.
  * Errors: CAPACITY if P + n > capacity; INVALID for n < 1 or NULL. */
 int kv_append(KVState* state, const void* k, const void* v, int n_tokens, int on_device, void* stream);
@@ -133,7 +144,9 @@ int kv_append(KVState* state, const void* k, const void* v, int n_tokens, int on
 int kv_length(const KVState* state, int* length_out);
 
 /* Copy rows [start, start+count) of one layer and slot as the slot sees them
- * (resolved through the beam table) to k_out, v_out: [Hkv][count][D] in
+ * (resolved through the beam table, i.e. the rows the paper's
+ * Gather(ReadValue, beam_idx) would hold: "Reaching Monolithic Parity: the
+ * beam_idx Gather Injection") to k_out, v_out: [Hkv][count][D] in
  * kv_dtype; host pointers if out_on_device == 0 (the call then synchronizes
  * the stream), device pointers otherwise.
  * Errors: INVALID if the range exceeds P or layer/slot is out of range. */
@@ -168,8 +181,10 @@ typedef struct StageRequest {
     int32_t        mask_len;
 } StageRequest;
 
-/* The forward of the stage over n_req independent requests in one pass
- * (micro-batching).  hidden_in / hidden_out: device [M][H] in act_dtype with
+/* The forward of the stage ("Stateful KV-Cached Inference": hidden states,
+ * attention_mask, position ids and beam_idx in, hidden states out, KV state
+ * kept inside) over n_req independent requests in one pass (micro-batching,
+ * "Multi-User Throughput via Micro-Batching").  hidden_in / hidden_out: device [M][H] in act_dtype with
  * M = sum over requests of S * n_tokens, rows request-major, then slot, then
  * token.  They must not overlap.  Appends each request's new K/V rows and
  * advances its P by n_tokens once the work is enqueued.

@@ -90,9 +90,13 @@ __device__ __forceinline__ float block_sum256(float v, float* buf) {
 
 // ------------------------------------------------------------------ coherent exchange
 // Workgroups of one launch exchange split partials through device-scope
-// ("sc1") stores and loads, which bypass the per-XCD L2s; the writer waits for
-// its stores with a workgroup-scope release before taking the ticket.  This
-// avoids the whole-L2 write-back and invalidate of an agent-scope fence.
+// ("sc1") stores and loads, which bypass the per-XCD L2s.  Before the ticket
+// every wave waits for the acknowledgement of its own stores (s_waitcnt
+// vmcnt(0): a device-scope store is acknowledged once it is visible at device
+// scope), then the workgroup meets at a barrier, so every partial of the
+// workgroup is visible before the counter moves.  A workgroup-scope release
+// alone emits no such wait on gfx950, and an agent-scope fence would write
+// back and invalidate the whole L2.
 
 __device__ __forceinline__ void store_coherent(float* p, float v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -104,7 +108,7 @@ __device__ __forceinline__ float load_coherent(const float* p) {
 // Returns true in exactly one workgroup: the last of `n` to arrive at counter *c,
 // which it resets.  Every thread of the workgroup must call it.
 __device__ __forceinline__ bool last_arrival(unsigned* c, unsigned n, int* flag) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");   // own coherent stores complete
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");          // this wave's coherent stores are acknowledged
     __syncthreads();
     if (threadIdx.x == 0) {
         const unsigned prev = atomicAdd(c, 1u);

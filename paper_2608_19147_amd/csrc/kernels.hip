@@ -1523,7 +1523,7 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int queries_per_ite
 
 // ------------------------------------------------------------------ fill
 
-// p[0 .. n) = v (a kernel rather than a memset node, so forwards stay safe to capture in graphs).
+// p[0 .. n) = v.
 __global__ __launch_bounds__(256) void fill_u32_kernel(uint32_t* __restrict__ p, size_t n, uint32_t v) {
     for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
 }

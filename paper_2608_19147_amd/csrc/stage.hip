@@ -108,9 +108,16 @@ struct Stage {
     int prof_class = -1;
     std::vector<hipEvent_t> prof_ev;   // start/stop pairs
     size_t prof_used = 0;              // events recorded
+    // Device work of every call on this stage (and on its KV states) runs in call
+    // order: done_ev marks the end of the last call's work on last_stream, and a
+    // call on another stream waits for it first (see order_on / mark_done).
+    hipEvent_t done_ev = nullptr;
+    hipStream_t last_stream = nullptr;
+    bool done_used = false;
 
     ~Stage() {
         for (hipEvent_t e : prof_ev) (void)hipEventDestroy(e);
+        if (done_ev) (void)hipEventDestroy(done_ev);
         (void)hipSetDevice(device);
         (void)hipDeviceSynchronize();
         for (void* p : allocs) (void)hipFree(p);
@@ -287,6 +294,23 @@ int ensure_meta(Stage* st, size_t bytes) {
     }
     st->meta_cap = cap;
     return STAGE_OK;
+}
+
+// Calls on one stage run on the device in the order they were made, whatever
+// streams they are issued on: the workspace, the metadata buffer and the flag
+// numbers of the single-launch forward are per stage.  A call on a stream other
+// than the previous call's first makes its stream wait for that call's work.
+hipError_t order_on(Stage* st, hipStream_t s) {
+    if (st->done_used && s != st->last_stream) return hipStreamWaitEvent(s, st->done_ev, 0);
+    return hipSuccess;
+}
+hipError_t mark_done(Stage* st, hipStream_t s) {
+    const hipError_t e = hipEventRecord(st->done_ev, s);
+    if (e == hipSuccess) {
+        st->done_used = true;
+        st->last_stream = s;
+    }
+    return e;
 }
 
 constexpr size_t PROF_MAX_LAUNCHES = 65536;
@@ -495,6 +519,8 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
     for (int i = 0; i < META_RING; ++i)
         if (hipEventCreateWithFlags(&st->meta_ev[i], hipEventDisableTiming) != hipSuccess)
             return cleanup(fail(STAGE_E_HIP, "event creation failed"));
+    if (hipEventCreateWithFlags(&st->done_ev, hipEventDisableTiming) != hipSuccess)
+        return cleanup(fail(STAGE_E_HIP, "event creation failed"));
     if ((rc = ensure_meta(st, 1 << 16))) return cleanup(rc);
     if (hipDeviceGetAttribute(&st->n_cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || st->n_cus < 1)
         return cleanup(fail(STAGE_E_HIP, "CU count query failed"));
@@ -730,6 +756,7 @@ int kv_append(KVState* kv, const void* k, const void* v, int n_tokens, int on_de
     const StageConfig& c = st->cfg;
     HIP_TRY(hipSetDevice(st->device));
     hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(order_on(st, s));
     const size_t bytes = (size_t)c.n_layers * kv->S * c.n_kv_heads * n_tokens * c.head_dim * 2;
     const uint16_t* kd = (const uint16_t*)k;
     const uint16_t* vd = (const uint16_t*)v;
@@ -755,6 +782,7 @@ int kv_append(KVState* kv, const void* k, const void* v, int n_tokens, int on_de
         if (e == hipSuccess) e = e2;
     }
     if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("kv_append: ") + hipGetErrorString(e));
+    HIP_TRY(mark_done(st, s));
     kv->P += n_tokens;
     return STAGE_OK;
 }
@@ -769,6 +797,7 @@ int kv_read(KVState* kv, int layer, int slot, int start, int count, void* k_out,
     if (count == 0) return STAGE_OK;
     HIP_TRY(hipSetDevice(st->device));
     hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(order_on(st, s));
     const size_t bytes = (size_t)c.n_kv_heads * count * c.head_dim * 2;
     uint16_t* kd = (uint16_t*)k_out;
     uint16_t* vd = (uint16_t*)v_out;
@@ -791,6 +820,7 @@ int kv_read(KVState* kv, int layer, int slot, int start, int count, void* k_out,
         if (e == hipSuccess) e = e2;
     }
     if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("kv_read: ") + hipGetErrorString(e));
+    HIP_TRY(mark_done(st, s));
     return STAGE_OK;
 }
 
@@ -903,6 +933,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
 
     HIP_TRY(hipSetDevice(st->device));
     hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(order_on(st, s));
 
     // ---------------- metadata into a pinned ring slot, one H2D copy
     const size_t off_req = 0;
@@ -1052,6 +1083,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("single-launch forward: ") + hipGetErrorString(e));
         HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, false, s));
         st->ll_epoch += (unsigned)(PS_LL_PER_LAYER * c.n_layers);
+        HIP_TRY(mark_done(st, s));
         for (int r = 0; r < n_req; ++r) {
             KVState* kv = reqs[r].state;
             if (do_gather[r]) kv->cur = 1 - kv->cur;
@@ -1280,6 +1312,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     }
 
     // ---------------- commit host-side state
+    HIP_TRY(mark_done(st, s));
     for (int r = 0; r < n_req; ++r) {
         KVState* kv = reqs[r].state;
         if (do_gather[r]) kv->cur = 1 - kv->cur;

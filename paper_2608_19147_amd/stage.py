@@ -5,7 +5,9 @@ for device buffers (``data_ptr``) and for the current HIP stream.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
+import weakref
 from dataclasses import dataclass
 from typing import List, Optional, Sequence
 
@@ -18,6 +20,24 @@ from ._lib import check
 MATRIX_NAMES = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
 _DT = {"f16": _lib.DTYPE_F16, "bf16": _lib.DTYPE_BF16}
 _TORCH = {"f16": torch.float16, "bf16": torch.bfloat16}
+
+
+_LIVE_STATES: "weakref.WeakSet[KVState]" = weakref.WeakSet()
+_LIVE_STAGES: "weakref.WeakSet[Stage]" = weakref.WeakSet()
+
+
+def close_all() -> None:
+    """Free every live KV state, then every live stage.  Registered with
+    atexit, so the library's device synchronizations and frees run while the
+    interpreter and the HIP runtime are both still whole, rather than from
+    ``__del__`` during interpreter shutdown."""
+    for kv in list(_LIVE_STATES):
+        kv.free()
+    for st in list(_LIVE_STAGES):
+        st.close()
+
+
+atexit.register(close_all)
 
 
 def _stream_ptr(stream) -> int:
@@ -76,10 +96,15 @@ class Stage:
         self.handle = h
         self.act_dtype = _TORCH[shape.act_dtype]
         self.kv_dtype = _TORCH[shape.kv_dtype]
+        _LIVE_STAGES.add(self)
 
     # ------------------------------------------------------------------
     def close(self) -> None:
+        """Free the stage's device memory (its KV states first)."""
         if getattr(self, "handle", None):
+            for kv in list(_LIVE_STATES):
+                if kv.stage is self:
+                    kv.free()
             check(self.lib.stage_destroy(self.handle))
             self.handle = None
 
@@ -201,6 +226,7 @@ class KVState:
         h = ctypes.c_void_p()
         check(self.lib.kv_state_alloc(stage.handle, n_slots, capacity, ctypes.byref(h)))
         self.handle = h
+        _LIVE_STATES.add(self)
 
     def free(self) -> None:
         if getattr(self, "handle", None):
