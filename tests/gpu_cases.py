@@ -25,11 +25,15 @@ def host(t: torch.Tensor) -> np.ndarray:
 class Pair:
     """GPU stage + oracle stage over identical weights."""
 
-    def __init__(self, shape, seed=0, layers=None, cache_weights=True):
+    def __init__(self, shape, seed=0, layers=None, cache_weights=True, with_oracle=True):
         self.shape = shape
         self.layers = layers if layers is not None else synth.make_weights(shape, seed)
         self.gpu = Stage(shape, self.layers)
-        self.orc = oracle.OracleStage(shape, self.layers, cache_weights)
+        self.orc = oracle.OracleStage(shape, self.layers, cache_weights) if with_oracle else None
+
+    def close(self) -> None:
+        """Free the GPU stage (and every KV state it still holds) now."""
+        self.gpu.close()
 
     def states(self, n_slots, past, capacity, seed=0, stream=0, with_oracle=True):
         g = self.gpu.new_state(n_slots, capacity)

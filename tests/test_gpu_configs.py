@@ -3,11 +3,9 @@ configurations: the 8B half stage (bs=1 decode at KV 2048, speculative verify
 on 4 slots x 5 tokens, micro-batches) and the 70B quarter stage (decode at KV
 8192, verify at KV 4096).
 
-The oracle runs whole layers in fp64, so these use one or two layers of the
-real per-layer shape; the full 16-layer 8B stage is checked through
-properties that hold at any depth (determinism, the appended layer-0 cache row
-against the oracle computed for that row alone, and agreement of the two
-independent GPU paths)."""
+These use one or two layers of the real per-layer shape, so that several
+steps fit a test; the full-depth stages are compared with the oracle in
+test_gpu_full_stage.py."""
 import os
 
 import numpy as np
@@ -60,46 +58,6 @@ def _layer0_new_kv(shape, layer, x, position):
     k = oracle.apply_rope(k.reshape(shape.n_kv_heads, shape.head_dim), np.array([position]), shape.rope_theta)
     rnd = oracle.to_bf16 if shape.kv_dtype == "bf16" else oracle.to_fp16
     return rnd(k), rnd(v.reshape(shape.n_kv_heads, shape.head_dim))
-
-
-def test_8b_full_stage_decode_properties():
-    """The 16-layer 8B half stage at KV 2048 (the benchmark's workload):
-    bitwise-deterministic output; the layer-0 cache row it appends equals the
-    oracle's row; the single-launch and per-layer-kernel paths agree."""
-    shape = synth.LLAMA8B_HALF
-    layers = synth.make_weights(shape, 52)
-    P = 2048
-    k, v = synth.make_kv(shape, 1, P, 52)
-    x = synth.make_hidden(shape, 1, 52).cuda()
-    pos, mask = np.array([[P]], np.int32), full_mask(1, P + 1)
-    outs = {}
-    for persistent in (True, False):
-        old = os.environ.get("STAGE_PERSISTENT")
-        os.environ["STAGE_PERSISTENT"] = "1" if persistent else "0"
-        try:
-            from paper_2608_19147_amd import Stage
-            st = Stage(shape, layers)
-        finally:
-            if old is None:
-                del os.environ["STAGE_PERSISTENT"]
-            else:
-                os.environ["STAGE_PERSISTENT"] = old
-        g = st.new_state(1, P + 4)
-        g.append(k, v)
-        o1 = host(st.forward([req(g, pos, mask, [0])], x))
-        kn, vn = g.read(0, 0, P, 1)
-        g.truncate(P)
-        o2 = host(st.forward([req(g, pos, mask, [0])], x))
-        torch.cuda.synchronize()
-        assert np.all(np.isfinite(o1))
-        assert np.array_equal(o1, o2), "not deterministic"
-        kr, vr = _layer0_new_kv(shape, layers[0], x.cpu(), P)
-        assert rel_err(kn[:, 0].double().cpu().numpy(), kr) <= TOL_STAGE
-        assert rel_err(vn[:, 0].double().cpu().numpy(), vr) <= TOL_STAGE
-        outs[persistent] = o1
-        g.free()
-        st.close()
-    assert rel_err(outs[True], outs[False]) <= TOL_STAGE
 
 
 def test_8b_spec_verify_steps():
