@@ -189,19 +189,20 @@ inline int ps_layout(PsArgs& a, int slots, int D, int gs) {
 }
 
 // Shapes with a single-launch instantiation: chunks-per-lane of K = H, Hq*D, F
-// (K / 2048), head_dim and query heads per kv head.
-bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int gs);
+// (K / 2048), head_dim, query heads per kv head and the cache dtype (kvb = 1
+// for bf16, 0 for fp16).
+bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb);
 // Private-segment (stack/scratch) bytes per lane of the instantiation; the
 // single launch is only used when this is zero.
-size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int gs);
-int ps_slots(int cpl_h, int cpl_q, int cpl_f, int D, int gs);   // ring slots per compute wave
+size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb);
+int ps_slots(int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb);   // ring slots per compute wave
 // Workgroups of the instantiation that fit on one CU with `lds` bytes of LDS.
-int ps_blocks_per_cu(int cpl_h, int cpl_q, int cpl_f, int D, int gs, size_t lds);
+int ps_blocks_per_cu(int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb, size_t lds);
 // coop = true launches through hipLaunchCooperativeKernel, which checks that every
 // workgroup is resident at once; coop = false is a plain launch, for which the
 // caller has checked that nwg workgroups fit on the device (at most one per CU).
-hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int gs, int nwg, size_t lds,
-                             bool coop, hipStream_t st);
+hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb, int nwg,
+                             size_t lds, bool coop, hipStream_t st);
 hipError_t launch_repack_rows(const uint8_t* q, const uint16_t* s, int n, int k, int g, uint8_t* w_out, uint16_t* s_out,
                               int kc, int ng, int row_off, int row_map, int head_dim, hipStream_t st);
 hipError_t launch_dequant_rows(const PsMat& m, int kc, int ng, int gchunks, int k, int row_off, int row_map, int n_rows,

@@ -556,16 +556,82 @@ __device__ __forceinline__ void gemv_seg_k(const PsArgs& a, Issue& issue, Ring& 
     }
 }
 
+// 2^x on the transcendental unit, without the library's range handling:
+// softmax weights only take arguments <= 0, and weights below 2^-126 (flushed
+// to zero) are far below the accuracy of the result.
+__device__ __forceinline__ float exp2_raw(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// A chunk of tc (1..4) cache-row slot pairs: K and V of every pair are read
+// into registers at once (one wait for the ring, one for LDS), then their
+// refills are issued.  While the stream is not near its end, S - 2 tc younger
+// ring positions stay in flight.
+template <int S, class Issue>
+__device__ __forceinline__ void att_read_chunk(Issue& issue, Ring& rg, int tc, u32x4 (&kw)[4], u32x4 (&vw)[4]) {
+    static_assert(S >= 8, "a chunk of four pairs must fit the ring");
+    const int lane16 = 16 * (threadIdx.x & 63);
+    if (rg.p > rg.pmax) vm_wait_all();
+    else if (tc == 4) vm_wait<S - 8>();
+    else if (tc == 3) vm_wait<S - 6>();
+    else if (tc == 2) vm_wait<S - 4>();
+    else vm_wait<S - 2>();
+    int ri = rg.ri;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        if (t < tc) {
+            kw[t] = lds_rd16(rg.addr(ri) + lane16);
+            ri = Ring::next(ri, S);
+            vw[t] = lds_rd16(rg.addr(ri) + lane16);
+            ri = Ring::next(ri, S);
+        } else {
+            kw[t] = u32x4{0u, 0u, 0u, 0u};
+            vw[t] = u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+    lgkm_wait_all();
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        touch(kw[t]);
+        touch(vw[t]);
+    }
+#pragma nounroll
+    for (int t = 0; t < 2 * tc; ++t) {
+        issue(rg.addr(rg.ri));
+        rg.ri = Ring::next(rg.ri, S);
+    }
+    rg.p += 2 * tc;
+}
+
+// 8 cache values of one lane (16 bytes) as fp32.
+template <bool BF16>
+__device__ __forceinline__ void kv_to_f32(const u32x4& w, float (&f)[8]) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const uint32_t d = w[e];
+        if constexpr (BF16) {
+            f[2 * e] = __uint_as_float(d << 16);
+            f[2 * e + 1] = __uint_as_float(d & 0xFFFF0000u);
+        } else {
+            f[2 * e] = f16_to_f32((uint16_t)(d & 0xFFFFu));
+            f[2 * e + 1] = f16_to_f32((uint16_t)(d >> 16));
+        }
+    }
+}
+
 // This wave's cache rows of the layer's attention: T slot pairs (K then V),
 // RPS rows per slot, LPR lanes per row.  Writes the wave's online-softmax
 // partial (max, sum, unnormalized output per query head) to LDS part.
-template <int GS, int D, int S, class Issue>
-__device__ __forceinline__ void att_seg(const PsArgs& a, Issue& issue, Ring& rg, int T, uint32_t mbits, uint32_t qlds,
-                                        uint32_t part) {
+//
+// The rows are taken in chunks of up to four slot pairs.  Within a chunk every
+// score of every head is computed first (independent dot products and lane
+// reductions), then one softmax update per head: the chunk's maximum, the
+// weights of its rows and one rescale of the running sums, instead of one
+// dependent update per row.  Each 16-lane row group keeps its own running
+// (max, sum, output); the groups are combined at the end.
+template <int GS, int D, int S, bool BF16, class Issue>
+__device__ __forceinline__ void att_seg_t(Issue& issue, Ring& rg, int T, uint32_t mbits, uint32_t qlds, uint32_t part) {
     constexpr int LPR = AttGeo<D>::LPR;
     const int lane = threadIdx.x & 63;
     const int li = lane % LPR;
-    const int kvdt = a.kv_dt;
     float m[GS], l[GS], o[GS][8];
 #pragma unroll
     for (int h = 0; h < GS; ++h) {
@@ -593,41 +659,52 @@ __device__ __forceinline__ void att_seg(const PsArgs& a, Issue& issue, Ring& rg,
                     qf[h][4 * k + e] = __builtin_bit_cast(float, qe);
                 }
             }
-        for (int t = 0; t < T; ++t) {
-            if (rg.p <= rg.pmax) vm_wait<S - 2>(); else vm_wait_all();
-            const int r1 = Ring::next(rg.ri, S);
-            u32x4 kw = lds_rd16(rg.addr(rg.ri) + 16 * lane);
-            u32x4 vw = lds_rd16(rg.addr(r1) + 16 * lane);
-            lgkm_wait_all();
-            touch(kw);
-            touch(vw);
-            issue(rg.addr(rg.ri));
-            issue(rg.addr(r1));
-            rg.p += 2;
-            rg.ri = Ring::next(r1, S);
-            float kf[8], vf[8];
+        for (int t0 = 0; t0 < T; t0 += 4) {
+            const int tc = min(4, T - t0);
+            u32x4 kw[4], vw[4];
+            att_read_chunk<S>(issue, rg, tc, kw, vw);
+            // scores of every (row, head) of the chunk; rows not visible get -inf
+            float sc[4][GS];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const uint32_t kd = kw[e >> 1], vd = vw[e >> 1];
-                kf[e] = half_bits_to_f32((uint16_t)((e & 1) ? (kd >> 16) : (kd & 0xFFFFu)), kvdt);
-                vf[e] = half_bits_to_f32((uint16_t)((e & 1) ? (vd >> 16) : (vd & 0xFFFFu)), kvdt);
+            for (int t = 0; t < 4; ++t) {
+                float kf[8];
+                kv_to_f32<BF16>(kw[t], kf);
+                const bool vis = t < tc && ((mbits >> (t0 + t)) & 1u);
+#pragma unroll
+                for (int h = 0; h < GS; ++h) {
+                    float sd = 0.f;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) sd = __builtin_fmaf(qf[h][e], kf[e], sd);
+                    sd = group_sum<LPR>(sd);
+                    sc[t][h] = vis ? sd : -INFINITY;
+                }
             }
-            const bool vis = (mbits >> t) & 1u;
+            float vf[4][8];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) kv_to_f32<BF16>(vw[t], vf[t]);
 #pragma unroll
             for (int h = 0; h < GS; ++h) {
-                float sd = 0.f;
+                float mn = m[h];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) sd = __builtin_fmaf(qf[h][e], kf[e], sd);
-                sd = group_sum<LPR>(sd);
-                if (vis) {
-                    const float mn = fmaxf(m[h], sd);
-                    const float corr = exp2f(m[h] - mn);
-                    const float pw = exp2f(sd - mn);
-                    l[h] = l[h] * corr + pw;
+                for (int t = 0; t < 4; ++t) mn = fmaxf(mn, sc[t][h]);
+                const float mref = (mn == -INFINITY) ? 0.f : mn;    // no visible row yet: nothing changes
+                const float corr = exp2_raw(m[h] - mref);
+                float p[4];
+                float ls = 0.f;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) o[h][e] = o[h][e] * corr + pw * vf[e];
-                    m[h] = mn;
+                for (int t = 0; t < 4; ++t) {
+                    p[t] = exp2_raw(sc[t][h] - mref);
+                    ls += p[t];
                 }
+                l[h] = __builtin_fmaf(l[h], corr, ls);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    float acc = o[h][e] * corr;
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) acc = __builtin_fmaf(p[t], vf[t][e], acc);
+                    o[h][e] = acc;
+                }
+                m[h] = mn;
             }
         }
         // merge the row groups (lanes LPR, 2 LPR, ... apart); for groups 16 and 32
@@ -641,8 +718,9 @@ __device__ __forceinline__ void att_seg(const PsArgs& a, Issue& issue, Ring& rg,
                 lane_pair(m[h], sh, mA, mB);
                 lane_pair(l[h], sh, lA, lB);
                 const float mn = fmaxf(mA, mB);
-                const float wA = (mA == -INFINITY) ? 0.f : exp2f(mA - mn);
-                const float wB = (mB == -INFINITY) ? 0.f : exp2f(mB - mn);
+                const float mref = (mn == -INFINITY) ? 0.f : mn;
+                const float wA = exp2_raw(mA - mref);
+                const float wB = exp2_raw(mB - mref);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     float oA, oB;
@@ -666,7 +744,7 @@ __device__ __forceinline__ void att_seg(const PsArgs& a, Issue& issue, Ring& rg,
     }
 }
 
-template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S, bool KVB>
 __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
     constexpr int LPR = AttGeo<D>::LPR, RPS = AttGeo<D>::RPS;
     const int lane = threadIdx.x & 63;
@@ -795,7 +873,7 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         wg_barrier();                                       // q|k|v rows are in LDS
         wg_barrier();                                       // q and the new row are staged
         cstamp(a, lb + a.l_dbg, 0);
-        att_seg<GS, D, S>(a, issue, rg, T, mbits, lb + a.l_q, lb + a.l_part);
+        att_seg_t<GS, D, S, KVB>(issue, rg, T, mbits, lb + a.l_q, lb + a.l_part);
         cstamp(a, lb + a.l_dbg, 1);
         wg_barrier();                                       // wave partials are in LDS
         wg_barrier();                                       // this workgroup's merge is done: polling starts now
@@ -1312,59 +1390,60 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     }
 }
 
-template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S, bool KVB>
 __global__ __launch_bounds__(SK_THREADS) void stage_stream_kernel(PsArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     if ((threadIdx.x >> 6) < SK_CW)
-        compute_main<CPL_H, CPL_Q, CPL_F, D, GS, S>(a, lds_addr(smem));
+        compute_main<CPL_H, CPL_Q, CPL_F, D, GS, S, KVB>(a, lds_addr(smem));
     else
         control_main<CPL_H, CPL_Q, CPL_F, D, GS, S>(a, smem);
 }
 
 // ------------------------------------------------------------------ host side
 
-// Instantiations: (K / 2048 for K = H, Hq*D, F), head_dim, query heads per kv head, ring slots.
-#define PS_SHAPES(X)                 \
-    X(2, 2, 7, 128, 4, 14)   /* Llama-3.1-8B layers */ \
-    X(1, 1, 1, 64, 2, 14)    /* small test stages */
+// Instantiations: (K / 2048 for K = H, Hq*D, F), head_dim, query heads per kv
+// head, ring slots, KV cache in bf16 (1) or fp16 (0).
+#define PS_SHAPES(X)                     \
+    X(2, 2, 7, 128, 4, 14, 1)   /* Llama-3.1-8B layers, bf16 cache */ \
+    X(1, 1, 1, 64, 2, 14, 0)    /* small test stages, fp16 cache */
 
-bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int gs) {
-#define PS_MATCH(H_, Q_, F_, D_, G_, S_) \
-    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return true;
+#define PS_KEY(H_, Q_, F_, D_, G_, K_) (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_ && kvb == K_)
+#define PS_KERNEL(H_, Q_, F_, D_, G_, S_, K_) stage_stream_kernel<H_, Q_, F_, D_, G_, S_, (K_ != 0)>
+
+bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb) {
+#define PS_MATCH(H_, Q_, F_, D_, G_, S_, K_) \
+    if (PS_KEY(H_, Q_, F_, D_, G_, K_)) return true;
     PS_SHAPES(PS_MATCH)
 #undef PS_MATCH
     return false;
 }
 
-int ps_slots(int cpl_h, int cpl_q, int cpl_f, int D, int gs) {
-#define PS_MATCH(H_, Q_, F_, D_, G_, S_) \
-    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return S_;
+int ps_slots(int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb) {
+#define PS_MATCH(H_, Q_, F_, D_, G_, S_, K_) \
+    if (PS_KEY(H_, Q_, F_, D_, G_, K_)) return S_;
     PS_SHAPES(PS_MATCH)
 #undef PS_MATCH
     return 0;
 }
 
-template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
-size_t ps_private_of() {
+static size_t ps_private_of(const void* fn) {
     hipFuncAttributes at{};
-    if (hipFuncGetAttributes(&at, (const void*)stage_stream_kernel<CPL_H, CPL_Q, CPL_F, D, GS, S>) != hipSuccess) {
+    if (hipFuncGetAttributes(&at, fn) != hipSuccess) {
         (void)hipGetLastError();
         return (size_t)-1;
     }
     return at.localSizeBytes;
 }
 
-size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int gs) {
-#define PS_MATCH(H_, Q_, F_, D_, G_, S_) \
-    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return ps_private_of<H_, Q_, F_, D_, G_, S_>();
+size_t ps_private_bytes(int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb) {
+#define PS_MATCH(H_, Q_, F_, D_, G_, S_, K_) \
+    if (PS_KEY(H_, Q_, F_, D_, G_, K_)) return ps_private_of((const void*)PS_KERNEL(H_, Q_, F_, D_, G_, S_, K_));
     PS_SHAPES(PS_MATCH)
 #undef PS_MATCH
     return (size_t)-1;
 }
 
-template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
-int ps_blocks_of(size_t lds) {
-    const void* fn = (const void*)stage_stream_kernel<CPL_H, CPL_Q, CPL_F, D, GS, S>;
+static int ps_blocks_of(const void* fn, size_t lds) {
     if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024) != hipSuccess) {
         (void)hipGetLastError();
         return 0;
@@ -1377,37 +1456,33 @@ int ps_blocks_of(size_t lds) {
     return n;
 }
 
-int ps_blocks_per_cu(int cpl_h, int cpl_q, int cpl_f, int D, int gs, size_t lds) {
-#define PS_MATCH(H_, Q_, F_, D_, G_, S_) \
-    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return ps_blocks_of<H_, Q_, F_, D_, G_, S_>(lds);
+int ps_blocks_per_cu(int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb, size_t lds) {
+#define PS_MATCH(H_, Q_, F_, D_, G_, S_, K_) \
+    if (PS_KEY(H_, Q_, F_, D_, G_, K_)) return ps_blocks_of((const void*)PS_KERNEL(H_, Q_, F_, D_, G_, S_, K_), lds);
     PS_SHAPES(PS_MATCH)
 #undef PS_MATCH
     return 0;
 }
 
-template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
-hipError_t launch_ps(const PsArgs& a, int nwg, size_t lds, bool coop, hipStream_t st) {
-    const void* fn = (const void*)stage_stream_kernel<CPL_H, CPL_Q, CPL_F, D, GS, S>;
-    static bool configured = false;
-    if (!configured) {
-        hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-        if (e != hipSuccess) return e;
-        configured = true;
-    }
+static hipError_t launch_ps(const void* fn, const PsArgs& a, int nwg, size_t lds, bool coop, hipStream_t st) {
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
     PsArgs copy = a;
     void* args[] = {&copy};
     if (coop) return hipLaunchCooperativeKernel(fn, dim3(nwg), dim3(SK_THREADS), args, (unsigned)lds, st);
     return hipLaunchKernel(fn, dim3(nwg), dim3(SK_THREADS), args, (unsigned)lds, st);
 }
 
-hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int gs, int nwg, size_t lds,
+hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb, int nwg, size_t lds,
                              bool coop, hipStream_t st) {
-#define PS_MATCH(H_, Q_, F_, D_, G_, S_) \
-    if (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_) return launch_ps<H_, Q_, F_, D_, G_, S_>(a, nwg, lds, coop, st);
+#define PS_MATCH(H_, Q_, F_, D_, G_, S_, K_) \
+    if (PS_KEY(H_, Q_, F_, D_, G_, K_)) return launch_ps((const void*)PS_KERNEL(H_, Q_, F_, D_, G_, S_, K_), a, nwg, lds, coop, st);
     PS_SHAPES(PS_MATCH)
 #undef PS_MATCH
     return hipErrorInvalidValue;
 }
+#undef PS_KEY
+#undef PS_KERNEL
 
 // Destination row of source row r: row_off + r (map 0), 2r (map 1, gate),
 // 2r + 1 (map 2, up), or row_off + the rotary-pair order inside each head of

@@ -405,7 +405,8 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         st->ng_q = (st->kc_q + gch - 1) / gch;
         st->ng_f = (st->kc_f + gch - 1) / gch;
         const char* e = std::getenv("STAGE_PERSISTENT");
-        st->ps_ok = ps_supported(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv) && !(e && atoi(e) == 0);
+        st->ps_ok = ps_supported(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv, c.kv_dtype == STAGE_DTYPE_BF16) &&
+                    !(e && atoi(e) == 0);
         if (st->ps_ok) st->ps_host.resize(c.n_layers);
     }
     if (const char* e = std::getenv("STAGE_GEMM_MIN_ROWS")) st->gemm_min_rows = std::max(1, atoi(e));
@@ -559,7 +560,8 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         probe.ng_h = st->ng_h; probe.ng_q = st->ng_q; probe.ng_f = st->ng_f;
         probe.rpw_qkv = st->ps_rpw_qkv; probe.rpw_h = st->ps_rpw_h; probe.rpw_gu = st->ps_rpw_gu;
         probe.H = H;
-        const int slots = ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv);
+        const int kvb = c.kv_dtype == STAGE_DTYPE_BF16;
+        const int slots = ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv, kvb);
         if (slots <= 0 || ps_layout(probe, slots, D, Hq / Hkv) > 160 * 1024) st->ps_ok = false;
         // flag-word buffers start with flag number 0, which no exchange uses
         const size_t max_split = (size_t)std::max(1, std::min(nwg / Hkv, (Hq / Hkv) * D / 8));
@@ -579,13 +581,13 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
                 return cleanup(rc);
         // the single-launch forward is only used when its kernel needs no private
         // segment (no stack, no scratch spills) for this shape
-        if (st->ps_ok && ps_private_bytes(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv) != 0) st->ps_ok = false;
+        if (st->ps_ok && ps_private_bytes(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv, kvb) != 0) st->ps_ok = false;
         // Workgroups wait on each other's flag words, so all nwg must be resident at
         // once: nwg <= CUs and one workgroup fits per CU.  The plain launch (default:
         // the cooperative one adds ~17 us per forward on MI355X) relies on this check;
         // a workgroup held back by other work on the device delays the others, and
         // an exchange that never completes ends in STAGE_E_DEVICE, not a hang.
-        if (st->ps_ok && (nwg > cus || ps_blocks_per_cu(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv,
+        if (st->ps_ok && (nwg > cus || ps_blocks_per_cu(st->cpl_h, st->cpl_q, st->cpl_f, D, Hq / Hkv, kvb,
                                                         (size_t)ps_layout(probe, slots, D, Hq / Hkv)) < 1))
             st->ps_ok = false;
     }
@@ -1077,9 +1079,10 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         a.err = st->err;
         a.spin_limit = st->spin_limit;
         a.trace = st->trace;
-        const int lds = ps_layout(a, ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, gs), D, gs);
+        const int kvb = c.kv_dtype == STAGE_DTYPE_BF16;
+        const int lds = ps_layout(a, ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, gs, kvb), D, gs);
         HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, true, s));
-        hipError_t e = launch_persistent(a, st->cpl_h, st->cpl_q, st->cpl_f, D, gs, st->ps_nwg, (size_t)lds, st->ps_coop, s);
+        hipError_t e = launch_persistent(a, st->cpl_h, st->cpl_q, st->cpl_f, D, gs, kvb, st->ps_nwg, (size_t)lds, st->ps_coop, s);
         if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("single-launch forward: ") + hipGetErrorString(e));
         HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, false, s));
         st->ll_epoch += (unsigned)(PS_LL_PER_LAYER * c.n_layers);
