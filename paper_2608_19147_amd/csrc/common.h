@@ -181,7 +181,15 @@ inline int ps_layout(PsArgs& a, int slots, int D, int gs) {
     a.l_res = off;  off += up(rows * 4, 16);
     a.l_q = off;    off += gs * D * 4;
     a.l_nkv = off;  off += 2 * D * 4;
-    a.l_part = off; off += up(SK_CW * gs * (D + 4) * 4 > a.H * 2 ? SK_CW * gs * (D + 4) * 4 : a.H * 2, SK_SLOT);   // also the first RMSNorm weights
+    // the compute waves' attention partials live only between the q|k|v product
+    // (the last reader of the staged input) and the staging of the o input, so
+    // they share the staged-input region when they fit
+    const int part_b = SK_CW * gs * (D + 4) * 4;
+    if (part_b <= kcmax * 64) {
+        a.l_part = a.l_xs;
+    } else {
+        a.l_part = off; off += up(part_b, 16);
+    }
     a.l_rope = off; off += (D / 2) * 8;
     a.l_dbg = off;  off += 64;                                        // compute-wave trace stamps
     a.l_end = off;

@@ -921,13 +921,6 @@ __device__ __forceinline__ void load_scales(const uint16_t* s, int first, int co
     for (int off = 0; off < bytes; off += SK_SLOT) dma16(src + off + 16 * lane, dst + off);
 }
 
-// RMSNorm weights (K values, 2 bytes each) into LDS with direct loads; the
-// buffer must hold whole 1 KB blocks.
-__device__ __forceinline__ void load_gamma(const uint16_t* gamma, int K, uint32_t dst) {
-    const int lane = threadIdx.x & 63;
-    for (int off = 0; off < K * 2; off += SK_SLOT) dma16((const uint8_t*)gamma + off + 16 * lane, dst + off);
-}
-
 // Input of the first q|k|v GEMV: the stage input h (K values of dtype src_dt,
 // written before the launch) -> h * rsqrt(mean(h^2) + eps) * gamma as fp16 in
 // LDS xs, padding up to kpad zeroed; returns the RMSNorm scale.
@@ -1167,13 +1160,12 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     if (lane < D / 2) ((float2*)rope)[lane] = a.rope[(size_t)pos * (D / 2) + lane];
     load_scales(a.layers[0].qkv.s, w * a.rpw_qkv, max(0, min(a.NQKV, (w + 1) * a.rpw_qkv) - w * a.rpw_qkv), a.ng_h,
                 lb + a.l_sb0);
-    // the first normalization reads the stage input directly (RMSNorm weights staged
-    // in the attention-partials region, free until the first attention)
-    load_gamma(a.layers[0].attn_norm, a.H, lb + a.l_part);
     vm_wait_all();
     // c: scale of the last published residual (the last RMSNorm scale); mq, mg: the
-    // factors rs / c applied to the q|k|v and gate|up results
-    float c = stage_norm<NT_H>(a.hidden_in, a.act_dt, a.H, a.kc_h * 32, smem + a.l_part, a.act_dt, a.eps, xs);
+    // factors rs / c applied to the q|k|v and gate|up results.  The first
+    // normalization reads the stage input and its RMSNorm weights from memory.
+    float c = stage_norm<NT_H>(a.hidden_in, a.act_dt, a.H, a.kc_h * 32, (const uint8_t*)a.layers[0].attn_norm, a.act_dt,
+                               a.eps, xs);
     float mq = 1.f, mg = 1.f;
     bool ok = true;
     vm_wait_all();
@@ -1404,7 +1396,7 @@ __global__ __launch_bounds__(SK_THREADS) void stage_stream_kernel(PsArgs a) {
 // Instantiations: (K / 2048 for K = H, Hq*D, F), head_dim, query heads per kv
 // head, ring slots, KV cache in bf16 (1) or fp16 (0).
 #define PS_SHAPES(X)                     \
-    X(2, 2, 7, 128, 4, 14, 1)   /* Llama-3.1-8B layers, bf16 cache */ \
+    X(2, 2, 7, 128, 4, 16, 1)   /* Llama-3.1-8B layers, bf16 cache */ \
     X(1, 1, 1, 64, 2, 14, 0)    /* small test stages, fp16 cache */
 
 #define PS_KEY(H_, Q_, F_, D_, G_, K_) (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_ && kvb == K_)
