@@ -28,6 +28,11 @@ same fields, no CPU baseline):
   decode70b     Llama-3-70B quarter stage (20 layers), bs=1 decode at KV 8192;
   verify70b     the same stage, 5-token verify at KV 4096 with Bernoulli(0.6)
                 rejections masked over 16 steps;
+  compact8b     KV compaction and capture on the 8B half stage: 4 slots at the
+                speculative-verify length 2368 with the bloat of truncated
+                Bernoulli(0.6) acceptance (about 7% masked holes per slot);
+                kv_compact in place (state re-installed from a full blob before
+                each timed call) and kv_capture of the kept rows to a device blob;
   copycal       1 GiB device copies (calibration of HBM byte counters).
 """
 from __future__ import annotations
@@ -117,7 +122,7 @@ def cpu_baseline(shape, kv_len: int, layers_sampled: int, seed: int, min_seconds
     }
 
 
-WORKLOADS = ("decode8b", "verify8b", "microbatch8b", "decode70b", "verify70b", "copycal")
+WORKLOADS = ("decode8b", "verify8b", "microbatch8b", "decode70b", "verify70b", "compact8b", "copycal")
 
 
 def _line(metric, value, unit, args, steps, ms, config, bytes_per_step, roof, higher=True, **extra):
@@ -170,6 +175,8 @@ def other_workload(args) -> int:
                           "unit": "GB/s", "bytes_read_per_copy": nbytes, "bytes_written_per_copy": nbytes,
                           "copies": max(1, args.steps), "ms_per_copy": round(ms, 4)}), flush=True)
         return 0
+    if args.workload == "compact8b":
+        return compact_workload(args)
     big = args.workload.endswith("70b")
     shape = synth.LLAMA70B_QUARTER if big else synth.LLAMA8B_HALF
     t0 = time.perf_counter()
@@ -312,6 +319,80 @@ def other_workload(args) -> int:
                     st.free()
                 del xs, out
     stage.device_status()
+    stage.close()
+    for ln in lines:
+        print(json.dumps(ln), flush=True)
+    return 0
+
+
+def compact_workload(args) -> int:
+    """kv_compact and kv_capture on a 4-slot 8B half-stage state (16 layers)."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2608_19147_amd import Stage
+
+    shape = synth.LLAMA8B_HALF
+    t0 = time.perf_counter()
+    stage = Stage(shape, synth.make_weights(shape, args.seed))
+    S, P = 4, 2368
+    state = stage.new_state(S, P)
+    k, v = synth.make_kv(shape, S, P, args.seed)
+    state.append(k, v)
+    del k, v
+    full = state.capture(None, on_device=True)               # re-installs the holed state
+    keep = np.stack([synth.hole_mask(P, 0.0724, args.seed, b, config_id=2) for b in range(S)])
+    keep[:, 0] = 1
+    kept = keep.sum(axis=1)
+    row_b = shape.n_kv_heads * shape.head_dim * 2            # one of K, V: bytes of a row per layer
+    L = shape.n_layers
+    kept_bytes = 2 * int(kept.sum()) * L * row_b             # K and V rows kept
+    pad_bytes = 2 * int((kept.max() - kept).sum()) * L * row_b
+    nbytes = 2 * kept_bytes + pad_bytes                      # each kept row read once and written once, padding written
+    torch.cuda.synchronize()
+    print(f"# setup {time.perf_counter() - t0:.1f}s, kept rows per slot {kept.tolist()}", file=sys.stderr, flush=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    steps = max(1, args.steps)
+
+    def time_compact(n):
+        tot = 0.0
+        for _ in range(n):
+            state.restore(full)
+            ev[0].record()
+            state.compact(keep)
+            ev[1].record()
+            ev[1].synchronize()
+            tot += ev[0].elapsed_time(ev[1])
+        return tot / n
+
+    def time_capture(n):
+        ev[0].record()
+        for _ in range(n):
+            state.capture(keep, on_device=True)
+        ev[1].record()
+        ev[1].synchronize()
+        return ev[0].elapsed_time(ev[1]) / n
+
+    time_compact(max(1, args.warmup))
+    ms_c = time_compact(steps)
+    state.restore(full)
+    time_capture(max(1, args.warmup))
+    ms_cap = time_capture(steps)
+    lines = []
+    base = {"layers": L, "kv_heads": shape.n_kv_heads, "head_dim": shape.head_dim, "kv_cache": shape.kv_dtype,
+            "slots": S, "kv_len": P, "kept_rows_per_slot": kept.tolist()}
+    for name, ms, kern in (("kv_compact", ms_c, "kv_compact_kernel (in place, one workgroup per layer, kv head, K|V)"),
+                           ("kv_capture", ms_cap, "kv_gather_rows_kernel (kept rows into a device blob)")):
+        gbps = nbytes / (ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "kernel": kern, "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": None, "bytes_per_launch": nbytes,
+                "avg_launch_us": round(ms * 1e3, 3), "launches_timed": steps,
+                "timed": "HIP events around the call on its stream (metadata upload + kernels)"}
+        cfg = {"workload": f"llama3.1-8b half stage {name}, {S} slots x kv {P}, ~7% masked holes", **base}
+        lines.append(_line(f"{name} GB/s (8B half-stage KV state, {S} slots x {P})", gbps, "GB/s", args, steps, ms, cfg,
+                           nbytes, roof))
+    state.free()
     stage.close()
     for ln in lines:
         print(json.dumps(ln), flush=True)

@@ -136,8 +136,9 @@ int kv_state_reset(KVState* state);
 /* Append n_tokens already-stored rows (K after rotary, V raw) for every
  * layer, slot and kv head at physical rows P..P+n-1 of each slot, then
  * P += n: the Concat -> Assign step of the paper's stateful KV ("Stateful
- * KV-Cached Inference"), used to seed a state with an existing cache.  k, v: [L][S][Hkv][n][D] in kv_dtype; host pointers if on_device == 0
- * (copied before return), device pointers otherwise.
+ * KV-Cached Inference"), used to seed a state with an existing cache.
+ * k, v: [L][S][Hkv][n][D] in kv_dtype; host pointers if on_device == 0
+ * (copied before return), else device pointers aligned to 16 bytes.
  * Errors: CAPACITY if P + n > capacity; INVALID for n < 1 or NULL. */
 int kv_append(KVState* state, const void* k, const void* v, int n_tokens, int on_device, void* stream);
 
@@ -157,6 +158,71 @@ int kv_read(KVState* state, int layer, int slot, int start, int count,
  * the physical trim the paper replaces by masking ("The Trim Problem"); it is
  * provided for twins in tests and for fixed-length benchmarking. */
 int kv_truncate(KVState* state, int new_len);
+
+/* ------------------------------------------------------------------------
+ * Compaction and serialization ("Mask-Based Rewind": masked positions stay in
+ * the cache during generation and are removed when the state is serialized;
+ * "Prefix Caching: KV Capture and Warm-Resume": a stage serializes its own
+ * layers' KV state into a self-describing blob keeping only mask-valid rows,
+ * and a restore either installs the whole state or changes nothing).
+ *
+ * keep_mask (all three calls): host uint8 [S][P] or NULL (keep every row).
+ * Row j of slot b, as the slot sees it (through the beam table), is kept iff
+ * keep_mask[b*P + j] != 0.  Slot b keeps n_b rows; the compacted length is
+ * P' = max_b n_b.  Slot b's kept rows become its rows 0..n_b-1 in ascending
+ * j; its rows n_b..P'-1 are zero (a slot shorter than P' must hide them with
+ * a 0 in the next forward's attention_mask).  The beam table becomes the
+ * identity.  slot_lengths (optional host int32 [S]) receives n_b.
+ * ------------------------------------------------------------------------ */
+
+/* Remove the rows keep_mask drops, in place: after the call P = P' and every
+ * slot's rows are as described above.  One pass over the kept rows (each is
+ * read once and written once); stream-ordered like a forward.
+ * Errors: INVALID (NULL state), HIP; nothing changes on error. */
+int kv_compact(KVState* state, const uint8_t* keep_mask, int32_t* slot_lengths, void* stream);
+
+/* Blob layout (little endian): a StageKVBlobHeader, then int32
+ * slot_length[n_slots], zero padding to header_bytes (a multiple of 256),
+ * then K rows [n_layers][n_slots][n_kv_heads][length][head_dim] and V rows of
+ * the same shape, in kv_dtype.  `fingerprint` identifies the stage that wrote
+ * it (its StageConfig fields and norm weights); a restore into a stage with
+ * another fingerprint is refused. */
+#define STAGE_KV_BLOB_MAGIC   0x31505643564B5453ULL   /* "STKVCVP1" */
+#define STAGE_KV_BLOB_VERSION 1
+typedef struct StageKVBlobHeader {
+    uint64_t magic;
+    uint32_t version;
+    uint32_t header_bytes;
+    uint64_t fingerprint;
+    int32_t  n_layers, n_slots, n_kv_heads, head_dim, kv_dtype, length;
+} StageKVBlobHeader;
+
+/* Bytes of the blob kv_capture writes for this state and keep_mask. */
+int kv_capture_size(const KVState* state, const uint8_t* keep_mask, int64_t* bytes_out);
+
+/* Serialize the kept rows of every layer, slot and kv head (the state itself
+ * is unchanged).  blob: blob_bytes >= kv_capture_size bytes; a host pointer if
+ * blob_on_device == 0 (the rows are gathered into a device staging buffer the
+ * call allocates and frees, and the call synchronizes the stream), a device
+ * pointer aligned to 16 bytes otherwise (gathered straight into the blob,
+ * asynchronous).
+ * Errors: INVALID (NULL), CAPACITY (blob too small), OOM, HIP. */
+int kv_capture(KVState* state, const uint8_t* keep_mask, void* blob, int64_t blob_bytes, int blob_on_device,
+               void* stream);
+
+/* Install a captured state: P = the blob's length, rows as captured, identity
+ * beam table; the state's previous contents are discarded.  The blob must come
+ * from a stage with the same fingerprint, with the state's slot count, and fit
+ * the state's capacity.  blob is a host pointer if blob_on_device == 0 (copied
+ * through a staging buffer the call allocates; the call synchronizes the
+ * stream), else a device pointer aligned to 16 bytes (its header is read back
+ * synchronously).
+ * slot_lengths (optional host int32 [S]) receives the captured n_b.
+ * Errors: INVALID (NULL, bad magic or version), STATE_MISMATCH (another
+ * stage's blob, other slot count), SHAPE (blob_bytes does not match the
+ * header), CAPACITY, OOM, HIP; on error the state is unchanged. */
+int kv_restore(KVState* state, const void* blob, int64_t blob_bytes, int blob_on_device, int32_t* slot_lengths,
+               void* stream);
 
 /* One request of a forward: `state` with S slots and physical length P,
  * each slot carrying n_tokens new tokens (1 = decode, K+1 = verify).

@@ -45,7 +45,7 @@ import numpy as np
 __all__ = [
     "round_rne", "to_fp16", "to_bf16", "fp16_bits_to_f64", "unpack_int4", "dequant",
     "rmsnorm", "rope_inv_freq", "apply_rope", "silu", "attention_slot",
-    "OracleStage", "OracleState", "forward", "forward_batch", "trimmed_twin",
+    "OracleStage", "OracleState", "forward", "forward_batch", "trimmed_twin", "compact",
     "ORACLE_BLOCK_ROWS",
 ]
 
@@ -267,6 +267,32 @@ def trimmed_twin(state: OracleState, slot: int, keep: np.ndarray) -> OracleState
         t.V[l][0, :, : keep_idx.size] = state.V[l][slot][:, keep_idx]
     t.P = int(keep_idx.size)
     return t
+
+
+def compact(state: OracleState, keep=None):
+    """Physical removal of dropped rows from every slot (paper, "Mask-Based
+    Rewind": masked positions are compacted away when the state is
+    serialized; "Prefix Caching: KV Capture and Warm-Resume": the captured
+    state keeps only mask-valid positions).
+
+    keep [S, P] (nonzero = keep; None keeps every row).  Slot b's kept rows,
+    in their original order, become its rows 0..n_b-1; the new length is
+    max_b n_b and a shorter slot is padded with zero rows.  Returns
+    (new state with the same capacity, n_b per slot).  This is also the
+    content of a capture blob."""
+    S, P = state.n_slots, state.P
+    keep = np.ones((S, P), dtype=np.uint8) if keep is None else np.asarray(keep)
+    if keep.shape != (S, P):
+        raise ValueError(f"keep shape {keep.shape} != {(S, P)}")
+    idx = [np.flatnonzero(keep[b] != 0) for b in range(S)]
+    lens = np.array([i.size for i in idx], dtype=np.int64)
+    out = OracleState(state.shape, S, state.capacity)
+    for l in range(state.shape.n_layers):
+        for b in range(S):
+            out.K[l][b, :, : lens[b]] = state.K[l][b][:, idx[b]]
+            out.V[l][b, :, : lens[b]] = state.V[l][b][:, idx[b]]
+    out.P = int(lens.max()) if S else 0
+    return out, lens
 
 
 def forward(stage: OracleStage, state: OracleState, x, positions, beam_idx=None, mask=None) -> np.ndarray:

@@ -23,6 +23,7 @@ EXPORTS = (
     "stage_debug_dequant", "stage_weight_bytes", "stage_last_error",
     "stage_profile_enable", "stage_profile_read", "stage_debug_phase_trace", "stage_device_status",
     "stage_debug_attn_arm", "stage_debug_attn_read",
+    "kv_compact", "kv_capture_size", "kv_capture", "kv_restore",
 )
 KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "persistent": 5}
 
@@ -87,6 +88,10 @@ def load() -> ctypes.CDLL:
         "stage_device_status": (I, [V]),
         "stage_debug_attn_arm": (I, [V, I, I]),
         "stage_debug_attn_read": (I, [V, V, V, P(I), P(I)]),
+        "kv_compact": (I, [V, V, V, V]),
+        "kv_capture_size": (I, [V, V, P(ctypes.c_int64)]),
+        "kv_capture": (I, [V, V, V, ctypes.c_int64, I, V]),
+        "kv_restore": (I, [V, V, ctypes.c_int64, I, V, V]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

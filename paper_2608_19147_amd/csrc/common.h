@@ -236,5 +236,16 @@ hipError_t launch_kv_read(const uint16_t* kc, const uint16_t* vc, const int16_t*
                           int start, int count, int S, int Hkv, int cap, int D, uint16_t* k_out, uint16_t* v_out,
                           hipStream_t st);
 hipError_t launch_dequant(const PackedMat& m, int row_off, int row_map, int n_rows, float* out, hipStream_t st);
+// Rows src[b][i] (< 0: zero padding) of every slot's logical view, read through
+// `table`, to dst [L][S][Hkv][dst_stride][D] rows i < Pn.
+hipError_t launch_kv_gather_rows(const uint16_t* kc, const uint16_t* vc, const int16_t* table, const int* src, int L, int S,
+                                 int Hkv, int cap, int D, int Pn, int dst_stride, uint16_t* k_dst, uint16_t* v_dst,
+                                 hipStream_t st);
+// In place: row i of slot b (every layer, kv head, K and V) = the row src[b][i]
+// (src[b][i] >= i, ascending per slot; < 0: zero) of the slot's view through
+// `table`; rows i < Pn.
+hipError_t launch_kv_compact(uint16_t* kc, uint16_t* vc, const int16_t* table, const int* src, int L, int S, int Hkv,
+                             int cap, int D, int Pn, hipStream_t st);
+hipError_t launch_table_identity(int16_t* table, int S, int cap, int n, hipStream_t st);
 
 }  // namespace stg

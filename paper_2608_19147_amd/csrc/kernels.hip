@@ -1552,27 +1552,34 @@ hipError_t launch_table_gather(const int16_t* src, int16_t* dst, const int* beam
     return hipGetLastError();
 }
 
-__global__ void kv_append_kernel(uint16_t* __restrict__ kc, uint16_t* __restrict__ vc, int16_t* __restrict__ table,
-                                 const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-                                 int L, int S, int Hkv, int cap, int D, int P, int n) {
-    const size_t total = (size_t)L * S * Hkv * n * D;
+// Rows [L][S][Hkv][n][D] of k, v to physical rows P..P+n-1 of every slot; the
+// slots' table entries there become their own index.  One thread moves 16
+// bytes of K and of V (D is a multiple of 8).
+__global__ __launch_bounds__(256) void kv_append_kernel(uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
+                                                        int16_t* __restrict__ table, const uint16_t* __restrict__ k,
+                                                        const uint16_t* __restrict__ v, int L, int S, int Hkv, int cap, int D,
+                                                        int P, int n) {
+    const int tpr = D / 8;
+    const size_t total = (size_t)L * S * Hkv * n * tpr;
     const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
     if (idx >= total) return;
     size_t rem = idx;
-    const int d = (int)(rem % D); rem /= D;
+    const int e = (int)(rem % tpr); rem /= tpr;
     const int i = (int)(rem % n); rem /= n;
     const int g = (int)(rem % Hkv); rem /= Hkv;
     const int b = (int)(rem % S); rem /= S;
     const int l = (int)rem;
-    const size_t dst = ((((size_t)l * S + b) * Hkv + g) * cap + (P + i)) * D + d;
-    kc[dst] = k[idx];
-    vc[dst] = v[idx];
-    if (l == 0 && g == 0 && d == 0) table[(size_t)b * cap + P + i] = (int16_t)b;
+    const size_t dst = ((((size_t)l * S + b) * Hkv + g) * cap + (P + i)) * D + 8 * e;
+    *(uint4*)(kc + dst) = *(const uint4*)(k + 8 * idx);
+    *(uint4*)(vc + dst) = *(const uint4*)(v + 8 * idx);
+    if (l == 0 && g == 0 && e == 0) table[(size_t)b * cap + P + i] = (int16_t)b;
 }
 
 hipError_t launch_kv_append(uint16_t* kc, uint16_t* vc, int16_t* table, const uint16_t* k, const uint16_t* v,
                             int L, int S, int Hkv, int cap, int D, int P, int n, hipStream_t st) {
-    const size_t total = (size_t)L * S * Hkv * n * D;
+    if (D % 8) return hipErrorInvalidValue;
+    const size_t total = (size_t)L * S * Hkv * n * (D / 8);
+    if (total == 0) return hipSuccess;
     kv_append_kernel<<<dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st>>>(kc, vc, table, k, v, L, S, Hkv, cap, D, P, n);
     return hipGetLastError();
 }
@@ -1600,6 +1607,165 @@ hipError_t launch_kv_read(const uint16_t* kc, const uint16_t* vc, const int16_t*
     if (total == 0) return hipSuccess;
     kv_read_kernel<<<dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st>>>(kc, vc, table, layer, slot, start, count,
                                                                                   S, Hkv, cap, D, k_out, v_out);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ compaction and capture
+
+// dst row i of slot b (for every layer and kv head) = the row src[b][i] of the
+// slot's view, read through the beam table (physical slot table[b][j] holds
+// row j); src[b][i] < 0 writes a zero row.  One thread moves 16 bytes of K and
+// 16 of V; a row is D / 8 consecutive threads, so a wave's loads and stores
+// cover whole rows.  dst rows of one (layer, slot, kv head) are dst_stride
+// rows apart.
+__global__ __launch_bounds__(256) void kv_gather_rows_kernel(const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+                                                             const int16_t* __restrict__ table, const int* __restrict__ src,
+                                                             int L, int S, int Hkv, int cap, int D, int Pn, int dst_stride,
+                                                             uint16_t* __restrict__ k_dst, uint16_t* __restrict__ v_dst) {
+    const int tpr = D / 8;
+    const size_t rows = (size_t)L * S * Hkv * Pn;
+    const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+    if (idx >= rows * tpr) return;
+    const int e = (int)(idx % tpr);
+    size_t r = idx / tpr;
+    const int i = (int)(r % Pn); r /= Pn;
+    const int g = (int)(r % Hkv); r /= Hkv;
+    const int b = (int)(r % S);
+    const int l = (int)(r / S);
+    const size_t dst = ((((size_t)l * S + b) * Hkv + g) * dst_stride + i) * D + 8 * e;
+    const int j = src[(size_t)b * Pn + i];
+    uint4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
+    if (j >= 0) {
+        const int ps = table[(size_t)b * cap + j];
+        const size_t so = ((((size_t)l * S + ps) * Hkv + g) * cap + j) * D + 8 * e;
+        kv = *(const uint4*)(kc + so);
+        vv = *(const uint4*)(vc + so);
+    }
+    *(uint4*)(k_dst + dst) = kv;
+    *(uint4*)(v_dst + dst) = vv;
+}
+
+hipError_t launch_kv_gather_rows(const uint16_t* kc, const uint16_t* vc, const int16_t* table, const int* src, int L, int S,
+                                 int Hkv, int cap, int D, int Pn, int dst_stride, uint16_t* k_dst, uint16_t* v_dst,
+                                 hipStream_t st) {
+    if (D % 8) return hipErrorInvalidValue;
+    const size_t n = (size_t)L * S * Hkv * Pn * (D / 8);
+    if (n == 0) return hipSuccess;
+    kv_gather_rows_kernel<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st>>>(kc, vc, table, src, L, S, Hkv, cap, D,
+                                                                                    Pn, dst_stride, k_dst, v_dst);
+    return hipGetLastError();
+}
+
+// In-place compaction of one cache (K or V): row i of slot b becomes the row
+// src[b][i] of the slot's view (through the beam table), or zero where
+// src[b][i] < 0.  src[b][i] >= i (kept rows in ascending order), so a row read
+// for destination i is never a destination below i.  One workgroup owns one
+// column slice (KC_SLICES per row) of one (layer, kv head, K or V) for every
+// slot and walks the destination rows in chunks of `chunk` positions:
+//  - all of a chunk's loads complete before any of its stores (the wait and
+//    the barrier before the stores);
+//  - the loads of chunk c + 1 are issued before the stores of chunk c: they
+//    read rows at or above the first position of chunk c + 1, the stores of
+//    chunk c write rows below it, so the two never touch the same element;
+//  - rows read by later chunks lie at or above their destinations, above
+//    every row written so far.
+// So no element is overwritten before every read of it.  Column slices are
+// independent (a row's slice moves with the row).
+constexpr int KC_THREADS = 512;
+constexpr int KC_PIECES = 4;
+constexpr int KC_SLICES = 2;
+
+struct KcChunk {
+    uint4 v[KC_PIECES];
+};
+
+__device__ __forceinline__ void kc_load(const uint16_t* c, const int16_t* __restrict__ table, const int* __restrict__ src,
+                                        int l, int g, int S, int Hkv, int cap, int D, int Pn, int pps, int col0, int i0,
+                                        int cn, KcChunk& ch) {
+    const int pieces = S * cn * pps;
+#pragma unroll
+    for (int k = 0; k < KC_PIECES; ++k) {
+        const int p = threadIdx.x + k * KC_THREADS;
+        ch.v[k] = make_uint4(0u, 0u, 0u, 0u);
+        if (p < pieces) {
+            const int r = p / pps;
+            const int b = r / cn;
+            const int i = i0 + r % cn;
+            const int j = src[(size_t)b * Pn + i];
+            if (j >= 0) {
+                const int ps = table[(size_t)b * cap + j];
+                ch.v[k] = *(const uint4*)(c + ((((size_t)l * S + ps) * Hkv + g) * cap + j) * D + col0 + 8 * (p % pps));
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void kc_store(uint16_t* c, int l, int g, int S, int Hkv, int cap, int D, int pps, int col0,
+                                         int i0, int cn, const KcChunk& ch) {
+    const int pieces = S * cn * pps;
+#pragma unroll
+    for (int k = 0; k < KC_PIECES; ++k) {
+        const int p = threadIdx.x + k * KC_THREADS;
+        if (p < pieces) {
+            const int r = p / pps;
+            const int b = r / cn;
+            const int i = i0 + r % cn;
+            *(uint4*)(c + ((((size_t)l * S + b) * Hkv + g) * cap + i) * D + col0 + 8 * (p % pps)) = ch.v[k];
+        }
+    }
+}
+
+__global__ __launch_bounds__(KC_THREADS) void kv_compact_kernel(uint16_t* kc, uint16_t* vc, const int16_t* __restrict__ table,
+                                                                const int* __restrict__ src, int S, int Hkv, int cap,
+                                                                int D, int Pn, int chunk) {
+    const int slice = blockIdx.x % KC_SLICES;
+    const int u = blockIdx.x / KC_SLICES;
+    const int l = u / (2 * Hkv);
+    const int g = (u / 2) % Hkv;
+    uint16_t* c = (u & 1) ? vc : kc;
+    const int pps = D / 8 / KC_SLICES;                       // 16-byte pieces of a row slice
+    const int col0 = slice * pps * 8;                        // first element of the slice
+    KcChunk a, b;
+    kc_load(c, table, src, l, g, S, Hkv, cap, D, Pn, pps, col0, 0, min(chunk, Pn), a);
+    for (int i0 = 0; i0 < Pn; i0 += 2 * chunk) {
+        // chunk at i0 (in a), then chunk at i0 + chunk (in b)
+        const int i1 = i0 + chunk, i2 = i0 + 2 * chunk;
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");     // this wave's accesses have completed
+        __syncthreads();                                     // and so have every other wave's
+        if (i1 < Pn) kc_load(c, table, src, l, g, S, Hkv, cap, D, Pn, pps, col0, i1, min(chunk, Pn - i1), b);
+        kc_store(c, l, g, S, Hkv, cap, D, pps, col0, i0, min(chunk, Pn - i0), a);
+        if (i1 >= Pn) break;
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (i2 < Pn) kc_load(c, table, src, l, g, S, Hkv, cap, D, Pn, pps, col0, i2, min(chunk, Pn - i2), a);
+        kc_store(c, l, g, S, Hkv, cap, D, pps, col0, i1, min(chunk, Pn - i1), b);
+    }
+}
+
+hipError_t launch_kv_compact(uint16_t* kc, uint16_t* vc, const int16_t* table, const int* src, int L, int S, int Hkv,
+                             int cap, int D, int Pn, hipStream_t st) {
+    if (D % (8 * KC_SLICES)) return hipErrorInvalidValue;
+    if (Pn == 0 || L == 0) return hipSuccess;
+    const int pps = D / 8 / KC_SLICES;
+    if ((long)S * pps > (long)KC_THREADS * KC_PIECES) return hipErrorInvalidValue;   // a chunk holds every slot's row
+    const int chunk = KC_THREADS * KC_PIECES / (S * pps);
+    kv_compact_kernel<<<dim3((unsigned)(L * Hkv * 2 * KC_SLICES)), dim3(KC_THREADS), 0, st>>>(kc, vc, table, src, S, Hkv,
+                                                                                             cap, D, Pn, chunk);
+    return hipGetLastError();
+}
+
+// table[b][j] = b for j < n: every slot reads its own rows.
+__global__ void table_identity_kernel(int16_t* __restrict__ table, int S, int cap, int n) {
+    const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+    if (idx >= (size_t)S * n) return;
+    const int b = (int)(idx / n), j = (int)(idx % n);
+    table[(size_t)b * cap + j] = (int16_t)b;
+}
+
+hipError_t launch_table_identity(int16_t* table, int S, int cap, int n, hipStream_t st) {
+    const size_t t = (size_t)S * n;
+    if (t == 0) return hipSuccess;
+    table_identity_kernel<<<dim3((unsigned)((t + 255) / 256)), dim3(256), 0, st>>>(table, S, cap, n);
     return hipGetLastError();
 }
 

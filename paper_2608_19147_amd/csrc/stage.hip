@@ -83,6 +83,7 @@ struct Stage {
     bool meta_ev_used[META_RING] = {};
     int ring_i = 0;
     int64_t weight_bytes = 0;
+    uint64_t fingerprint = 0;                          // of the config, rotary table and norm weights (KV blobs)
     // persistent-kernel weights (row layout) and barrier state
     bool ps_ok = false;
     int cpl_h = 0, cpl_q = 0, cpl_f = 0, kc_h = 0, kc_q = 0, kc_f = 0, ng_h = 0, ng_q = 0, ng_f = 0;
@@ -327,6 +328,71 @@ hipError_t prof_mark(Stage* st, int kclass, bool begin, hipStream_t s) {
         st->prof_ev.push_back(e);
     }
     return hipEventRecord(st->prof_ev[st->prof_used++], s);
+}
+
+// FNV-1a, 64 bit.
+uint64_t fnv1a(uint64_t h, const void* p, size_t n) {
+    const uint8_t* b = (const uint8_t*)p;
+    for (size_t i = 0; i < n; ++i) h = (h ^ b[i]) * 0x100000001b3ULL;
+    return h;
+}
+
+// Copies `bytes` of host data into the next pinned metadata ring slot and from
+// there to the device metadata buffer (stream-ordered); *dev is its device copy.
+int meta_upload(Stage* st, const void* host, size_t bytes, hipStream_t s, const uint8_t** dev) {
+    int rc = ensure_meta(st, std::max<size_t>(bytes, 16));
+    if (rc) return rc;
+    const int slot_i = st->ring_i;
+    st->ring_i = (st->ring_i + 1) % META_RING;
+    if (st->meta_ev_used[slot_i]) HIP_TRY(hipEventSynchronize(st->meta_ev[slot_i]));
+    if (bytes) std::memcpy(st->meta_host[slot_i], host, bytes);
+    HIP_TRY(hipMemcpyAsync(st->meta_dev, st->meta_host[slot_i], std::max<size_t>(bytes, 16), hipMemcpyHostToDevice, s));
+    HIP_TRY(hipEventRecord(st->meta_ev[slot_i], s));
+    st->meta_ev_used[slot_i] = true;
+    *dev = st->meta_dev;
+    return STAGE_OK;
+}
+
+// Kept rows of every slot: src[b * Pn + i] = the i-th kept row of slot b
+// (ascending) or -1 past the slot's count; Pn = the largest count.
+void plan_keep(const KVState* kv, const uint8_t* keep, std::vector<int>& src, std::vector<int32_t>& lens, int& Pn) {
+    const int S = kv->S, P = kv->P;
+    lens.assign(S, 0);
+    for (int b = 0; b < S; ++b)
+        for (int j = 0; j < P; ++j) lens[b] += (!keep || keep[(size_t)b * P + j]) ? 1 : 0;
+    Pn = 0;
+    for (int b = 0; b < S; ++b) Pn = std::max(Pn, (int)lens[b]);
+    src.assign((size_t)S * Pn, -1);
+    for (int b = 0; b < S; ++b) {
+        int i = 0;
+        for (int j = 0; j < P; ++j)
+            if (!keep || keep[(size_t)b * P + j]) src[(size_t)b * Pn + i++] = j;
+    }
+}
+
+size_t blob_header_bytes(int S) { return (sizeof(StageKVBlobHeader) + 4 * (size_t)S + 255) / 256 * 256; }
+size_t blob_rows_bytes(const StageConfig& c, int S, int Pn) {
+    return (size_t)c.n_layers * S * c.n_kv_heads * Pn * c.head_dim * 2;   // one of K, V
+}
+
+// Header and slot lengths of a capture, zero-padded to header_bytes.
+std::vector<uint8_t> blob_header(const Stage* st, int S, int Pn, const std::vector<int32_t>& lens) {
+    const StageConfig& c = st->cfg;
+    std::vector<uint8_t> h(blob_header_bytes(S), 0);
+    StageKVBlobHeader hd{};
+    hd.magic = STAGE_KV_BLOB_MAGIC;
+    hd.version = STAGE_KV_BLOB_VERSION;
+    hd.header_bytes = (uint32_t)h.size();
+    hd.fingerprint = st->fingerprint;
+    hd.n_layers = c.n_layers;
+    hd.n_slots = S;
+    hd.n_kv_heads = c.n_kv_heads;
+    hd.head_dim = c.head_dim;
+    hd.kv_dtype = c.kv_dtype;
+    hd.length = Pn;
+    std::memcpy(h.data(), &hd, sizeof(hd));
+    std::memcpy(h.data() + sizeof(hd), lens.data(), 4 * (size_t)S);
+    return h;
 }
 
 }  // namespace
@@ -592,6 +658,24 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
             st->ps_ok = false;
     }
     if (hipDeviceSynchronize() != hipSuccess) return cleanup(fail(STAGE_E_HIP, "stage_create synchronize failed"));
+    {
+        // identity of the stage for KV blobs: config, rotary table, norm weights
+        uint64_t h = 0xcbf29ce484222325ULL;
+        const int32_t dims[] = {c.n_layers, c.hidden, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn, c.group_size,
+                                c.act_dtype, c.kv_dtype, c.max_positions};
+        h = fnv1a(h, dims, sizeof(dims));
+        h = fnv1a(h, &c.rms_eps, sizeof(c.rms_eps));
+        h = fnv1a(h, &c.rope_theta, sizeof(c.rope_theta));
+        h = fnv1a(h, rope.data(), rope.size() * sizeof(float2));
+        std::vector<uint16_t> nw((size_t)H);
+        for (const auto& L : st->layers)
+            for (const uint16_t* g : {L.attn_norm, L.ffn_norm}) {
+                if (hipMemcpy(nw.data(), g, (size_t)H * 2, hipMemcpyDeviceToHost) != hipSuccess)
+                    return cleanup(fail(STAGE_E_HIP, "norm weight read-back failed"));
+                h = fnv1a(h, nw.data(), nw.size() * 2);
+            }
+        st->fingerprint = h;
+    }
     *out = st;
     return STAGE_OK;
 }
@@ -754,6 +838,7 @@ int kv_append(KVState* kv, const void* k, const void* v, int n_tokens, int on_de
     if (!kv || !k || !v) return fail(STAGE_E_INVALID, "NULL argument");
     if (n_tokens < 1) return fail(STAGE_E_INVALID, "n_tokens must be positive");
     if (kv->P + n_tokens > kv->cap) return fail(STAGE_E_CAPACITY, "append exceeds the state's capacity");
+    if (on_device && (((uintptr_t)k | (uintptr_t)v) & 15)) return fail(STAGE_E_INVALID, "device rows must be 16-byte aligned");
     Stage* st = kv->stage;
     const StageConfig& c = st->cfg;
     HIP_TRY(hipSetDevice(st->device));
@@ -823,6 +908,159 @@ int kv_read(KVState* kv, int layer, int slot, int start, int count, void* k_out,
     }
     if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("kv_read: ") + hipGetErrorString(e));
     HIP_TRY(mark_done(st, s));
+    return STAGE_OK;
+}
+
+int kv_compact(KVState* kv, const uint8_t* keep_mask, int32_t* slot_lengths, void* stream) {
+    if (!kv) return fail(STAGE_E_INVALID, "state is NULL");
+    Stage* st = kv->stage;
+    const StageConfig& c = st->cfg;
+    std::vector<int> src;
+    std::vector<int32_t> lens;
+    int Pn = 0;
+    plan_keep(kv, keep_mask, src, lens, Pn);
+    HIP_TRY(hipSetDevice(st->device));
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(order_on(st, s));
+    if (Pn > 0) {
+        const uint8_t* d = nullptr;
+        int rc = meta_upload(st, src.data(), src.size() * sizeof(int), s, &d);
+        if (rc) return rc;
+        HIP_TRY(launch_kv_compact(kv->kc, kv->vc, kv->table[kv->cur], (const int*)d, c.n_layers, kv->S, c.n_kv_heads,
+                                  kv->cap, c.head_dim, Pn, s));
+        HIP_TRY(launch_table_identity(kv->table[kv->cur], kv->S, kv->cap, Pn, s));
+    }
+    HIP_TRY(mark_done(st, s));
+    kv->P = Pn;
+    if (slot_lengths) std::memcpy(slot_lengths, lens.data(), 4 * (size_t)kv->S);
+    return STAGE_OK;
+}
+
+int kv_capture_size(const KVState* kv, const uint8_t* keep_mask, int64_t* bytes_out) {
+    if (!kv || !bytes_out) return fail(STAGE_E_INVALID, "NULL argument");
+    std::vector<int> src;
+    std::vector<int32_t> lens;
+    int Pn = 0;
+    plan_keep(kv, keep_mask, src, lens, Pn);
+    *bytes_out = (int64_t)(blob_header_bytes(kv->S) + 2 * blob_rows_bytes(kv->stage->cfg, kv->S, Pn));
+    return STAGE_OK;
+}
+
+int kv_capture(KVState* kv, const uint8_t* keep_mask, void* blob, int64_t blob_bytes, int blob_on_device, void* stream) {
+    if (!kv || !blob) return fail(STAGE_E_INVALID, "NULL argument");
+    Stage* st = kv->stage;
+    const StageConfig& c = st->cfg;
+    std::vector<int> src;
+    std::vector<int32_t> lens;
+    int Pn = 0;
+    plan_keep(kv, keep_mask, src, lens, Pn);
+    const std::vector<uint8_t> hdr = blob_header(st, kv->S, Pn, lens);
+    const size_t rows = blob_rows_bytes(c, kv->S, Pn);
+    if (blob_bytes < 0 || (size_t)blob_bytes < hdr.size() + 2 * rows)
+        return fail(STAGE_E_CAPACITY, "blob smaller than kv_capture_size");
+    if (blob_on_device && ((uintptr_t)blob & 15)) return fail(STAGE_E_INVALID, "device blob must be 16-byte aligned");
+    HIP_TRY(hipSetDevice(st->device));
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(order_on(st, s));
+    // metadata slot: kept-row lists, then the header (copied to a device blob from there)
+    const size_t src_bytes = (src.size() * sizeof(int) + 255) / 256 * 256;
+    std::vector<uint8_t> meta(src_bytes + hdr.size(), 0);
+    std::memcpy(meta.data(), src.data(), src.size() * sizeof(int));
+    std::memcpy(meta.data() + src_bytes, hdr.data(), hdr.size());
+    const uint8_t* d = nullptr;
+    int rc = meta_upload(st, meta.data(), meta.size(), s, &d);
+    if (rc) return rc;
+    uint8_t* rows_dst = (uint8_t*)blob + hdr.size();   // K rows, then V rows
+    void* tmp = nullptr;
+    if (!blob_on_device) {
+        if (rows && hipMalloc(&tmp, 2 * rows) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(STAGE_E_OOM, "capture staging allocation failed");
+        }
+        rows_dst = (uint8_t*)tmp;
+    } else {
+        HIP_TRY(hipMemcpyAsync(blob, d + src_bytes, hdr.size(), hipMemcpyDeviceToDevice, s));
+    }
+    hipError_t e = hipSuccess;
+    if (rows)
+        e = launch_kv_gather_rows(kv->kc, kv->vc, kv->table[kv->cur], (const int*)d, c.n_layers, kv->S, c.n_kv_heads,
+                                  kv->cap, c.head_dim, Pn, Pn, (uint16_t*)rows_dst, (uint16_t*)(rows_dst + rows), s);
+    if (!blob_on_device) {
+        std::memcpy(blob, hdr.data(), hdr.size());
+        if (e == hipSuccess && rows) e = hipMemcpyAsync((uint8_t*)blob + hdr.size(), tmp, 2 * rows, hipMemcpyDeviceToHost, s);
+        const hipError_t e2 = hipStreamSynchronize(s);
+        if (tmp) (void)hipFree(tmp);
+        if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("kv_capture: ") + hipGetErrorString(e));
+    HIP_TRY(mark_done(st, s));
+    return STAGE_OK;
+}
+
+int kv_restore(KVState* kv, const void* blob, int64_t blob_bytes, int blob_on_device, int32_t* slot_lengths, void* stream) {
+    if (!kv || !blob) return fail(STAGE_E_INVALID, "NULL argument");
+    Stage* st = kv->stage;
+    const StageConfig& c = st->cfg;
+    HIP_TRY(hipSetDevice(st->device));
+    hipStream_t s = (hipStream_t)stream;
+    if ((size_t)std::max<int64_t>(blob_bytes, 0) < sizeof(StageKVBlobHeader))
+        return fail(STAGE_E_SHAPE, "blob shorter than its header");
+    if (blob_on_device && ((uintptr_t)blob & 15)) return fail(STAGE_E_INVALID, "device blob must be 16-byte aligned");
+    StageKVBlobHeader hd{};
+    std::vector<int32_t> lens;
+    if (blob_on_device) {
+        HIP_TRY(order_on(st, s));
+        HIP_TRY(hipMemcpyAsync(&hd, blob, sizeof(hd), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipStreamSynchronize(s));
+    } else {
+        std::memcpy(&hd, blob, sizeof(hd));
+    }
+    if (hd.magic != STAGE_KV_BLOB_MAGIC || hd.version != STAGE_KV_BLOB_VERSION)
+        return fail(STAGE_E_INVALID, "not a KV blob of this version");
+    if (hd.fingerprint != st->fingerprint || hd.n_layers != c.n_layers || hd.n_kv_heads != c.n_kv_heads ||
+        hd.head_dim != c.head_dim || hd.kv_dtype != c.kv_dtype)
+        return fail(STAGE_E_STATE_MISMATCH, "blob was captured by a different stage");
+    if (hd.n_slots != kv->S) return fail(STAGE_E_STATE_MISMATCH, "blob slot count differs from the state's");
+    const int S = kv->S, Pn = hd.length;
+    if (Pn < 0 || hd.header_bytes != blob_header_bytes(S)) return fail(STAGE_E_SHAPE, "malformed blob header");
+    const size_t rows = blob_rows_bytes(c, S, Pn);
+    if ((size_t)blob_bytes < hd.header_bytes + 2 * rows) return fail(STAGE_E_SHAPE, "blob shorter than its rows");
+    if (Pn > kv->cap) return fail(STAGE_E_CAPACITY, "blob length exceeds the state's capacity");
+    lens.resize(S);
+    if (blob_on_device) {
+        HIP_TRY(hipMemcpy(lens.data(), (const uint8_t*)blob + sizeof(hd), 4 * (size_t)S, hipMemcpyDeviceToHost));
+    } else {
+        std::memcpy(lens.data(), (const uint8_t*)blob + sizeof(hd), 4 * (size_t)S);
+    }
+    for (int b = 0; b < S; ++b)
+        if (lens[b] < 0 || lens[b] > Pn) return fail(STAGE_E_SHAPE, "malformed slot length in blob");
+    HIP_TRY(order_on(st, s));
+    const uint16_t* kd = (const uint16_t*)((const uint8_t*)blob + hd.header_bytes);
+    void* tmp = nullptr;
+    if (!blob_on_device && rows) {
+        if (hipMalloc(&tmp, 2 * rows) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(STAGE_E_OOM, "restore staging allocation failed");
+        }
+        if (hipMemcpyAsync(tmp, kd, 2 * rows, hipMemcpyHostToDevice, s) != hipSuccess) {
+            (void)hipFree(tmp);
+            return fail(STAGE_E_HIP, "restore upload failed");
+        }
+        kd = (const uint16_t*)tmp;
+    }
+    hipError_t e = hipSuccess;
+    if (Pn > 0)
+        e = launch_kv_append(kv->kc, kv->vc, kv->table[kv->cur], kd, (const uint16_t*)((const uint8_t*)kd + rows), c.n_layers,
+                             S, c.n_kv_heads, kv->cap, c.head_dim, 0, Pn, s);
+    if (tmp) {
+        const hipError_t e2 = hipStreamSynchronize(s);
+        (void)hipFree(tmp);
+        if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("kv_restore: ") + hipGetErrorString(e));
+    HIP_TRY(mark_done(st, s));
+    kv->P = Pn;
+    if (slot_lengths) std::memcpy(slot_lengths, lens.data(), 4 * (size_t)S);
     return STAGE_OK;
 }
 

@@ -259,6 +259,56 @@ class KVState:
         check(self.lib.kv_append(self.handle, ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(v.data_ptr()),
                                  int(k.shape[3]), on_dev, ctypes.c_void_p(_stream_ptr(stream))))
 
+    def _keep(self, keep):
+        if keep is None:
+            return None, None
+        keep = np.ascontiguousarray(keep, dtype=np.uint8)
+        if keep.shape != (self.n_slots, self.length):
+            raise ValueError(f"keep mask shape {keep.shape} != {(self.n_slots, self.length)}")
+        return keep, ctypes.c_void_p(keep.ctypes.data)
+
+    def compact(self, keep=None, stream=None) -> np.ndarray:
+        """Remove the rows keep [S, P] (nonzero = keep; None = all) drops, in
+        place.  Returns each slot's kept count; P becomes their maximum."""
+        keep, kp = self._keep(keep)
+        lens = np.zeros(self.n_slots, np.int32)
+        check(self.lib.kv_compact(self.handle, kp, ctypes.c_void_p(lens.ctypes.data),
+                                  ctypes.c_void_p(_stream_ptr(stream))))
+        return lens
+
+    def capture_size(self, keep=None) -> int:
+        keep, kp = self._keep(keep)
+        n = ctypes.c_int64()
+        check(self.lib.kv_capture_size(self.handle, kp, ctypes.byref(n)))
+        return n.value
+
+    def capture(self, keep=None, on_device: bool = True, stream=None):
+        """Serialized kept rows: a device uint8 tensor, or a host numpy array."""
+        keep_arr, kp = self._keep(keep)
+        n = self.capture_size(keep_arr)
+        if on_device:
+            blob = torch.empty(n, dtype=torch.uint8, device="cuda")
+            ptr = blob.data_ptr()
+        else:
+            blob = np.empty(n, dtype=np.uint8)
+            ptr = blob.ctypes.data
+        check(self.lib.kv_capture(self.handle, kp, ctypes.c_void_p(ptr), n, int(on_device),
+                                  ctypes.c_void_p(_stream_ptr(stream))))
+        return blob
+
+    def restore(self, blob, stream=None) -> np.ndarray:
+        """Install a captured state (device tensor or host array); returns each
+        slot's captured count."""
+        lens = np.zeros(self.n_slots, np.int32)
+        if isinstance(blob, torch.Tensor) and blob.is_cuda:
+            ptr, n, dev = blob.data_ptr(), blob.numel() * blob.element_size(), 1
+        else:
+            blob = np.ascontiguousarray(blob)
+            ptr, n, dev = blob.ctypes.data, blob.nbytes, 0
+        check(self.lib.kv_restore(self.handle, ctypes.c_void_p(ptr), int(n), dev, ctypes.c_void_p(lens.ctypes.data),
+                                  ctypes.c_void_p(_stream_ptr(stream))))
+        return lens
+
     def read(self, layer: int, slot: int, start: int, count: int, stream=None):
         """Rows [start, start+count) of one layer and slot as the slot sees them: K, V [Hkv, count, D]."""
         sh = self.stage.shape

@@ -505,4 +505,78 @@ def pin_stored_rows_closed_form():
         assert np.array_equal(state.V[0][0, :, :3], v_ref), kv
 
 
+# ------------------------------------------------------------------ compaction and capture
+
+def _holed_state(shape, seed, S, past, cap, n_holes):
+    st = oracle_state(shape, S, past, cap, seed)
+    r = np.random.default_rng(seed)
+    keep = np.ones((S, past), dtype=np.uint8)
+    for b in range(S):
+        keep[b, r.choice(past, n_holes[b], replace=False)] = 0
+    return st, keep
+
+
+def pin_compact_bruteforce():
+    """Compaction by per-element loops on a tiny state: slot b's kept rows, in
+    order, at rows 0..n_b-1, zero rows after, length max_b n_b."""
+    shape = TINY2
+    st, keep = _holed_state(shape, 71, 3, 12, 16, [3, 0, 7])
+    keep[2, :] = 0
+    keep[2, [1, 4]] = 1                                   # slot 2 keeps two rows
+    out, lens = oracle.compact(st, keep)
+    counts = [int(sum(1 for j in range(12) if keep[b][j])) for b in range(3)]
+    assert list(lens) == counts == [9, 12, 2] and out.P == 12 and out.capacity == 16
+    for l in range(shape.n_layers):
+        for b in range(3):
+            for g in range(shape.n_kv_heads):
+                i = 0
+                for j in range(12):
+                    if keep[b][j]:
+                        for d in range(shape.head_dim):
+                            assert out.K[l][b, g, i, d] == st.K[l][b, g, j, d]
+                            assert out.V[l][b, g, i, d] == st.V[l][b, g, j, d]
+                        i += 1
+                for i2 in range(i, out.P):
+                    for d in range(shape.head_dim):
+                        assert out.K[l][b, g, i2, d] == 0.0 and out.V[l][b, g, i2, d] == 0.0
+
+
+def pin_compact_keep_all_is_identity():
+    shape = TINY2
+    st = oracle_state(shape, 2, 9, 12, 72)
+    out, lens = oracle.compact(st, None)
+    assert out.P == 9 and list(lens) == [9, 9]
+    for l in range(shape.n_layers):
+        assert np.array_equal(out.K[l][:, :, :9], st.K[l][:, :, :9])
+        assert np.array_equal(out.V[l][:, :, :9], st.V[l][:, :, :9])
+
+
+def pin_compacted_forward_equals_masked_forward():
+    """A forward on the compacted state (padding hidden by the mask) equals the
+    forward on the holed state with its mask, bitwise (paper, "Mask-Based
+    Rewind": masking is exact, compaction only removes what the mask hid), for
+    a 3-token verify and the decode after it."""
+    shape = TINY2
+    st, _ = oracle_stage(shape, 73)
+    S, past = 2, 40
+    holed, keep = _holed_state(shape, 73, S, past, 64, [6, 13])
+    comp, lens = oracle.compact(holed, keep)
+    n = 3
+    x = f64(synth.make_hidden(shape, S * n, 73, 1))
+    pos = logical_positions(keep, n)
+    mask_h = np.concatenate([keep, np.ones((S, n), np.uint8)], axis=1)
+    mask_c = np.zeros((S, comp.P + n), np.uint8)
+    for b in range(S):
+        mask_c[b, : lens[b]] = 1
+        mask_c[b, comp.P:] = 1
+    oh = oracle.forward(st, holed, x, pos, None, mask_h)
+    oc = oracle.forward(st, comp, x, pos, None, mask_c)
+    assert np.array_equal(oh, oc), np.max(np.abs(oh - oc))
+    x2 = f64(synth.make_hidden(shape, S, 73, 2))
+    pos2 = pos[:, -1:] + 1
+    oh2 = oracle.forward(st, holed, x2, pos2, None, np.concatenate([mask_h, np.ones((S, 1), np.uint8)], 1))
+    oc2 = oracle.forward(st, comp, x2, pos2, None, np.concatenate([mask_c, np.ones((S, 1), np.uint8)], 1))
+    assert np.array_equal(oh2, oc2)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

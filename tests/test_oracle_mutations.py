@@ -142,7 +142,33 @@ def _forward_factory(kind):
     return fwd
 
 
+def _compact_factory(kind):
+    orig = so.compact
+
+    def comp(state, keep=None):
+        S, P = state.n_slots, state.P
+        keep = np.ones((S, P), np.uint8) if keep is None else np.asarray(keep)
+        idx = [np.flatnonzero(keep[b] != 0) for b in range(S)]
+        if kind == "reversed":
+            idx = [i[::-1] for i in idx]
+        lens = np.array([i.size for i in idx])
+        out = so.OracleState(state.shape, S, state.capacity)
+        for l in range(state.shape.n_layers):
+            for b in range(S):
+                out.K[l][b, :, : lens[b]] = state.K[l][b][:, idx[b]]
+                out.V[l][b, :, : lens[b]] = state.V[l][b][:, idx[b]]
+                if kind == "stale_padding":   # padding keeps the old rows instead of zeros
+                    out.K[l][b, :, lens[b]:P] = state.K[l][b][:, lens[b]:P]
+                    out.V[l][b, :, lens[b]:P] = state.V[l][b][:, lens[b]:P]
+        out.P = int(lens.min() if kind == "min_length" else lens.max())
+        return out, lens
+    return comp
+
+
 MUTANTS = {
+    "compact_reversed": ("compact", _compact_factory("reversed")),
+    "compact_stale_padding": ("compact", _compact_factory("stale_padding")),
+    "compact_min_length": ("compact", _compact_factory("min_length")),
     "gate_up_swap": ("forward", _forward_factory("gate_up_swap")),
     "norm_swap": ("forward", _forward_factory("norm_swap")),
     "round_before_rope": ("forward", _forward_factory("round_before_rope")),
