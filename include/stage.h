@@ -210,6 +210,23 @@ int kv_capture_size(const KVState* state, const uint8_t* keep_mask, int64_t* byt
 int kv_capture(KVState* state, const uint8_t* keep_mask, void* blob, int64_t blob_bytes, int blob_on_device,
                void* stream);
 
+/* kv_capture into a host blob for callers that cannot allocate device
+ * memory (serving loops that forbid hipMalloc, code next to a graph capture):
+ * the same blob bytes as kv_capture with blob_on_device == 0, staged through
+ * a fixed device array inside the library (STAGE_STATIC_SCRATCH_BYTES per
+ * GPU, set up at the first stage_create on that GPU and held until the
+ * process ends) instead of an allocated buffer.  The call allocates no device
+ * or pinned memory.  Rows move a whole number of layers at a time: the kept
+ * row lists (4 x S x P' bytes, rounded up to 256) plus one layer's kept K and
+ * V rows (2 x S x n_kv_heads x P' x head_dim x 2 bytes) must fit the array,
+ * else STAGE_E_CAPACITY before any work.  Synchronizes the stream.  Every
+ * call on one GPU shares that GPU's array, which keeps the last call's
+ * contents: calls that overlap on one GPU (other threads, other streams)
+ * race and must be serialized by the caller.
+ * Errors: INVALID (NULL), CAPACITY (blob too small, array too small), HIP. */
+#define STAGE_STATIC_SCRATCH_BYTES (64u << 20)
+int kv_capture_noalloc(KVState* state, const uint8_t* keep_mask, void* blob_host, int64_t blob_bytes, void* stream);
+
 /* Install a captured state: P = the blob's length, rows as captured, identity
  * beam table; the state's previous contents are discarded.  The blob must come
  * from a stage with the same fingerprint, with the state's slot count, and fit

@@ -15,6 +15,7 @@ ERRORS = {
 DTYPE_F16 = 1
 DTYPE_BF16 = 2
 MAX_ROWS = 64
+STATIC_SCRATCH_BYTES = 64 << 20   # STAGE_STATIC_SCRATCH_BYTES
 
 # Every function that include/stage.h declares.
 EXPORTS = (
@@ -23,7 +24,7 @@ EXPORTS = (
     "stage_debug_dequant", "stage_weight_bytes", "stage_last_error",
     "stage_profile_enable", "stage_profile_read", "stage_debug_phase_trace", "stage_device_status",
     "stage_debug_attn_arm", "stage_debug_attn_read",
-    "kv_compact", "kv_capture_size", "kv_capture", "kv_restore",
+    "kv_compact", "kv_capture_size", "kv_capture", "kv_restore", "kv_capture_noalloc",
 )
 KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "persistent": 5}
 
@@ -92,6 +93,7 @@ def load() -> ctypes.CDLL:
         "kv_capture_size": (I, [V, V, P(ctypes.c_int64)]),
         "kv_capture": (I, [V, V, V, ctypes.c_int64, I, V]),
         "kv_restore": (I, [V, V, ctypes.c_int64, I, V, V]),
+        "kv_capture_noalloc": (I, [V, V, V, ctypes.c_int64, V]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

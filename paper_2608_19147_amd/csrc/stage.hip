@@ -4,15 +4,28 @@
 #include "common.h"
 
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
 using namespace stg;
 
+// Fixed device staging of kv_capture_noalloc: one copy per GPU the library
+// runs on, held until the process ends.  Host code never passes this name to
+// a kernel or copy (on the host it is only a stand-in for the symbol): it uses
+// the per-device address hipGetSymbolAddress returned at stage creation.
+static __device__ __align__(256) uint8_t scratch[STAGE_STATIC_SCRATCH_BYTES];
+
 namespace {
+
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+std::array<uint8_t*, SCRATCH_MAX_DEVICES> g_scratch_ptr{};   // address of `scratch` on each device
+
 
 thread_local std::string g_err;
 
@@ -28,6 +41,24 @@ int fail(int code, const std::string& msg) {
     } while (0)
 
 constexpr int META_RING = 4;
+
+// Looks up the address of `scratch` on the current device `dev` once.
+int scratch_init(int dev) {
+    if (dev < 0 || dev >= SCRATCH_MAX_DEVICES) return fail(STAGE_E_UNSUPPORTED, "device index beyond the static scratch table");
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (g_scratch_ptr[dev]) return STAGE_OK;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return fail(STAGE_E_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch_ptr[dev] = (uint8_t*)p;
+    return STAGE_OK;
+}
+
+uint8_t* scratch_ptr(int dev) {
+    if (dev < 0 || dev >= SCRATCH_MAX_DEVICES) return nullptr;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    return g_scratch_ptr[dev];
+}
 
 struct DevMat {
     PackedMat pm;
@@ -425,6 +456,7 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
     HIP_TRY(hipGetDevice(&dev));
     hipStream_t s = (hipStream_t)stream;
 
+    if (int rc0 = scratch_init(dev)) return rc0;
     Stage* st = new Stage();
     st->cfg = c;
     st->cfg.rope_cos_sin = nullptr;
@@ -993,6 +1025,52 @@ int kv_capture(KVState* kv, const uint8_t* keep_mask, void* blob, int64_t blob_b
         if (e == hipSuccess) e = e2;
     }
     if (e != hipSuccess) return fail(STAGE_E_HIP, std::string("kv_capture: ") + hipGetErrorString(e));
+    HIP_TRY(mark_done(st, s));
+    return STAGE_OK;
+}
+
+int kv_capture_noalloc(KVState* kv, const uint8_t* keep_mask, void* blob_host, int64_t blob_bytes, void* stream) {
+    if (!kv || !blob_host) return fail(STAGE_E_INVALID, "NULL argument");
+    Stage* st = kv->stage;
+    const StageConfig& c = st->cfg;
+    std::vector<int> src;
+    std::vector<int32_t> lens;
+    int Pn = 0;
+    plan_keep(kv, keep_mask, src, lens, Pn);
+    const std::vector<uint8_t> hdr = blob_header(st, kv->S, Pn, lens);
+    const size_t rows = blob_rows_bytes(c, kv->S, Pn);
+    if (blob_bytes < 0 || (size_t)blob_bytes < hdr.size() + 2 * rows)
+        return fail(STAGE_E_CAPACITY, "blob smaller than kv_capture_size");
+    const size_t src_bytes = (src.size() * sizeof(int) + 255) / 256 * 256;
+    const size_t layer_rows = rows / (size_t)c.n_layers;    // one layer's K (or V) rows
+    const size_t room = STAGE_STATIC_SCRATCH_BYTES > src_bytes ? STAGE_STATIC_SCRATCH_BYTES - src_bytes : 0;
+    const int per = layer_rows ? (int)std::min<size_t>((size_t)c.n_layers, room / (2 * layer_rows)) : c.n_layers;
+    if (src_bytes > STAGE_STATIC_SCRATCH_BYTES || per < 1)
+        return fail(STAGE_E_CAPACITY, "one layer's kept rows (" + std::to_string(2 * layer_rows) + " bytes) and row lists (" +
+                                          std::to_string(src_bytes) + " bytes) exceed STAGE_STATIC_SCRATCH_BYTES");
+    HIP_TRY(hipSetDevice(st->device));
+    uint8_t* sp = scratch_ptr(st->device);
+    if (!sp) return fail(STAGE_E_HIP, "static scratch address unknown on this device");
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(order_on(st, s));
+    std::memcpy(blob_host, hdr.data(), hdr.size());
+    uint8_t* kdst = (uint8_t*)blob_host + hdr.size();
+    uint8_t* vdst = kdst + rows;
+    if (rows) {
+        HIP_TRY(hipMemcpyAsync(sp, src.data(), src.size() * sizeof(int), hipMemcpyHostToDevice, s));
+        const size_t layer_elems = (size_t)kv->S * c.n_kv_heads * kv->cap * c.head_dim;
+        for (int l0 = 0; l0 < c.n_layers; l0 += per) {
+            const int nl = std::min(per, c.n_layers - l0);
+            uint8_t* ks = sp + src_bytes;
+            uint8_t* vs = ks + (size_t)nl * layer_rows;
+            HIP_TRY(launch_kv_gather_rows(kv->kc + (size_t)l0 * layer_elems, kv->vc + (size_t)l0 * layer_elems,
+                                          kv->table[kv->cur], (const int*)sp, nl, kv->S, c.n_kv_heads, kv->cap, c.head_dim,
+                                          Pn, Pn, (uint16_t*)ks, (uint16_t*)vs, s));
+            HIP_TRY(hipMemcpyAsync(kdst + (size_t)l0 * layer_rows, ks, (size_t)nl * layer_rows, hipMemcpyDeviceToHost, s));
+            HIP_TRY(hipMemcpyAsync(vdst + (size_t)l0 * layer_rows, vs, (size_t)nl * layer_rows, hipMemcpyDeviceToHost, s));
+        }
+    }
+    HIP_TRY(hipStreamSynchronize(s));
     HIP_TRY(mark_done(st, s));
     return STAGE_OK;
 }

@@ -296,6 +296,15 @@ class KVState:
                                   ctypes.c_void_p(_stream_ptr(stream))))
         return blob
 
+    def capture_noalloc(self, keep=None, stream=None) -> np.ndarray:
+        """kv_capture into a host blob through the library's fixed device
+        staging array (no device allocation)."""
+        keep_arr, kp = self._keep(keep)
+        blob = np.empty(self.capture_size(keep_arr), dtype=np.uint8)
+        check(self.lib.kv_capture_noalloc(self.handle, kp, ctypes.c_void_p(blob.ctypes.data), blob.size,
+                                          ctypes.c_void_p(_stream_ptr(stream))))
+        return blob
+
     def restore(self, blob, stream=None) -> np.ndarray:
         """Install a captured state (device tensor or host array); returns each
         slot's captured count."""
