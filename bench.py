@@ -33,6 +33,8 @@ same fields, no CPU baseline):
                 Bernoulli(0.6) acceptance (about 7% masked holes per slot);
                 kv_compact in place (state re-installed from a full blob before
                 each timed call) and kv_capture of the kept rows to a device blob;
+  head8b        final-stage epilogue: final RMSNorm + INT4 LM head (128256 x 4096,
+                group 128) + on-device top-1 (token, probability), 1 and 20 rows;
   copycal       1 GiB device copies (calibration of HBM byte counters).
 """
 from __future__ import annotations
@@ -122,7 +124,7 @@ def cpu_baseline(shape, kv_len: int, layers_sampled: int, seed: int, min_seconds
     }
 
 
-WORKLOADS = ("decode8b", "verify8b", "microbatch8b", "decode70b", "verify70b", "compact8b", "copycal")
+WORKLOADS = ("decode8b", "verify8b", "microbatch8b", "decode70b", "verify70b", "compact8b", "head8b", "copycal")
 
 
 def _line(metric, value, unit, args, steps, ms, config, bytes_per_step, roof, higher=True, **extra):
@@ -177,6 +179,8 @@ def other_workload(args) -> int:
         return 0
     if args.workload == "compact8b":
         return compact_workload(args)
+    if args.workload == "head8b":
+        return head_workload(args)
     big = args.workload.endswith("70b")
     shape = synth.LLAMA70B_QUARTER if big else synth.LLAMA8B_HALF
     t0 = time.perf_counter()
@@ -318,6 +322,52 @@ def other_workload(args) -> int:
                 for st, _, _ in reqs:
                     st.free()
                 del xs, out
+    stage.device_status()
+    stage.close()
+    for ln in lines:
+        print(json.dumps(ln), flush=True)
+    return 0
+
+
+def head_workload(args) -> int:
+    """stage_head_top1 with the Llama-3 vocabulary on the 8B hidden size."""
+    import torch
+
+    import synth
+    from paper_2608_19147_amd import Stage
+
+    shape = synth.with_layers(synth.LLAMA8B_HALF, 1)     # the head needs only the stage's hidden size and dtypes
+    stage = Stage(shape, synth.make_weights(shape, args.seed))
+    V = synth.LLAMA3_VOCAB
+    fn, lm = synth.make_head(shape, V, args.seed)
+    stage.attach_head(fn, lm)
+    del lm
+    H, G = shape.hidden, shape.group_size
+    head_bytes = V * (H // 2) + V * (H // G) * 2 + 2 * H    # codes + scales + final norm
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    steps = max(1, args.steps)
+    lines = []
+    for M in (1, 20):
+        xs = [synth.make_hidden(shape, M, args.seed, 400 + i).cuda() for i in range(4)]
+        for i in range(max(1, args.warmup)):
+            stage.head_top1(xs[i % 4])
+        torch.cuda.synchronize()
+        ev[0].record()
+        for i in range(steps):
+            stage.head_top1(xs[i % 4])
+        ev[1].record()
+        ev[1].synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / steps
+        nbytes = head_bytes + M * H * 2
+        gbps = nbytes / (ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "kernel": "bprep_kernel + gemm_bp_kernel (top-1 epilogue) + top1_merge_kernel",
+                "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                "traffic": None, "bytes_per_launch": nbytes, "avg_launch_us": round(ms * 1e3, 3), "launches_timed": steps,
+                "timed": "HIP events around the call on its stream (three kernels)"}
+        cfg = {"workload": f"final-stage head: RMSNorm + INT4 lm_head {V} x {H} + top-1, {M} rows", "vocab": V,
+               "hidden": H, "group_size": G, "rows": M, "act": shape.act_dtype}
+        lines.append(_line(f"final-stage top-1 rows/s (LM head {V} x {H}, {M} rows)", M * 1e3 / ms, "rows/s", args,
+                           steps, ms, cfg, nbytes, roof))
     stage.device_status()
     stage.close()
     for ln in lines:

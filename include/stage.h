@@ -278,6 +278,36 @@ typedef struct StageRequest {
 int stage_forward(Stage* stage, const StageRequest* reqs, int n_req,
                   const void* hidden_in, void* hidden_out, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Final-stage epilogue ("Top-1 Logits Compression": the last stage returns
+ * the top-1 token and its probability instead of a full logits row; the last
+ * stage of the pipeline owns the final norm and the LM head).
+ * ------------------------------------------------------------------------ */
+
+/* Attach the model's final RMSNorm weight (final_norm [H] in act_dtype) and
+ * INT4 LM head (lm_head [vocab][H], the canonical QuantMatrix layout, group
+ * size of the stage, which must be 128) to the stage.  Copies and repacks both
+ * into library-owned memory; host pointers if weights_on_device == 0, else
+ * device pointers.  Synchronizes the stream.  Once per stage.
+ * Errors: INVALID (NULL), SHAPE (k != hidden), UNSUPPORTED (already attached,
+ * group size), CAPACITY, OOM, HIP. */
+int stage_head_attach(Stage* stage, const uint16_t* final_norm, const QuantMatrix* lm_head, int weights_on_device,
+                      void* stream);
+
+/* For each of the M rows of hidden (device [M][H] in act_dtype, e.g. the
+ * stage's hidden_out): logits = RMSNorm(row) * final_norm, times lm_head^T
+ * (fp32 accumulation), then on the device
+ *   token_out[m] = argmax_j logits[m][j] (the smallest j among equal maxima),
+ *   p_out[m]     = its softmax probability 1 / sum_j exp(logits[m][j] - max),
+ *   logit_out[m] = the maximum (optional, NULL skips it),
+ *   logits_out   = the full rows, fp32 [M][vocab] (optional, NULL skips the
+ *                  write; test support).
+ * All outputs are device pointers; 1 <= M <= STAGE_MAX_ROWS.  Stream-ordered
+ * with the stage's other calls (it uses the stage's workspace).
+ * Errors: INVALID (NULL, no head), CAPACITY (M), HIP. */
+int stage_head_top1(Stage* stage, const void* hidden, int M, int32_t* token_out, float* p_out, float* logit_out,
+                    float* logits_out, void* stream);
+
 /* Test support: the dequantized weight matrix as the kernels decode it,
  * W[r][c] = code * scale exactly, written to out_host fp32 [n][k].
  * which: 0..6 = wq, wk, wv, wo, wg, wu, wd in the tiled layout of the

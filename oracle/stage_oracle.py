@@ -45,7 +45,7 @@ import numpy as np
 __all__ = [
     "round_rne", "to_fp16", "to_bf16", "fp16_bits_to_f64", "unpack_int4", "dequant",
     "rmsnorm", "rope_inv_freq", "apply_rope", "silu", "attention_slot",
-    "OracleStage", "OracleState", "forward", "forward_batch", "trimmed_twin", "compact",
+    "OracleStage", "OracleState", "forward", "forward_batch", "trimmed_twin", "compact", "head_logits", "top1",
     "ORACLE_BLOCK_ROWS",
 ]
 
@@ -293,6 +293,30 @@ def compact(state: OracleState, keep=None):
             out.V[l][b, :, : lens[b]] = state.V[l][b][:, idx[b]]
     out.P = int(lens.max()) if S else 0
     return out, lens
+
+
+def head_logits(x, final_norm, lm_q, lm_scales, vocab: int, group: int, eps: float) -> np.ndarray:
+    """The last stage's logits: RMSNorm of each hidden row with the final norm
+    weight, then the dequantized LM head [vocab, H] (paper, "Top-1 Logits
+    Compression": the final stage computes the full logits row before
+    reducing it).  x [M, H] -> [M, vocab] fp64, one matrix-vector product per row."""
+    x = np.atleast_2d(np.asarray(x, dtype=np.float64))
+    h = rmsnorm(x, _as_f64(final_norm), eps)
+    w = dequant(lm_q, lm_scales, x.shape[1], group)
+    assert w.shape[0] == vocab
+    return gemv_rows(h, w)
+
+
+def top1(logits) -> tuple:
+    """Per row: the index of the largest logit (the first one among equal
+    maxima), its softmax probability 1 / sum_j exp(l_j - l_max), and the
+    maximum.  This is what the paper's top-1 compression sends back instead
+    of the full row."""
+    logits = np.atleast_2d(np.asarray(logits, dtype=np.float64))
+    idx = np.argmax(logits, axis=1)
+    mx = logits[np.arange(logits.shape[0]), idx]
+    p = 1.0 / np.exp(logits - mx[:, None]).sum(axis=1)
+    return idx, p, mx
 
 
 def forward(stage: OracleStage, state: OracleState, x, positions, beam_idx=None, mask=None) -> np.ndarray:

@@ -56,7 +56,7 @@ struct MetaDev {
 };
 
 enum GemvRms : int { RMS_NONE = 0, RMS_FULLROW = 1, RMS_PARTIALS = 2 };
-enum GemvEpi : int { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+enum GemvEpi : int { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_TOP1 = 3 };
 
 struct GemvArgs {
     PackedMat W;
@@ -82,6 +82,7 @@ struct GemvArgs {
     uint16_t* bp_out; float* bc_out; float* cb_out;  // RESID / SWIGLU: the next product's input
     const uint16_t* gamma_next; int gamma_next_dt; // RESID: RMSNorm weight of the next product
     const float* rs_in;                            // RESID: scale c to prepare with (previous rs)
+    float4* top1_part;                             // TOP1: [M][ntiles] (max, index bits, sum of exp(v - max), 0)
 };
 
 struct AttnArgs {
@@ -247,5 +248,8 @@ hipError_t launch_kv_gather_rows(const uint16_t* kc, const uint16_t* vc, const i
 hipError_t launch_kv_compact(uint16_t* kc, uint16_t* vc, const int16_t* table, const int* src, int L, int S, int Hkv,
                              int cap, int D, int Pn, hipStream_t st);
 hipError_t launch_table_identity(int16_t* table, int S, int cap, int n, hipStream_t st);
+// Per row m < M: the largest of the tiles' maxima, its smallest index, and
+// 1 / sum over tiles of se * exp(max_t - max) (the softmax probability of it).
+hipError_t launch_top1_merge(const float4* part, int M, int ntiles, int32_t* token, float* p, float* logit, hipStream_t st);
 
 }  // namespace stg

@@ -20,6 +20,8 @@
 //                attn_merge_kernel then combines the split partials.
 #include "device.h"
 
+#include <climits>
+
 namespace stg {
 
 __device__ __forceinline__ int dest_row(int r, int row_off, int row_map) {
@@ -435,6 +437,18 @@ __device__ __forceinline__ float wave_sum_all(float v) {
     return __uint_as_float(q[0]) + __uint_as_float(q[1]);
 }
 
+// Largest value / smallest integer over the wave, identical in every lane.
+__device__ __forceinline__ float wave_max_all(float v) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+__device__ __forceinline__ int wave_min_all(int v) {
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) v = min(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
 // Sum over aligned groups of 32 lanes, identical in every lane of the group.
 __device__ __forceinline__ float sum32_lanes(float v) {
     v += dpp_f<0xB1>(v);              // lane ^ 1
@@ -800,6 +814,22 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
                 bp_put(a.bp_out, a.bc_out, a.kp, m, n, h, ok);
                 if (t == 0 && r == 0) a.cb_out[m] = c;
             }
+        }
+    } else if (a.epi == EPI_TOP1) {
+        // per row: the tile's largest value, its smallest index among equal ones,
+        // and the sum of exp(v - max) over the tile (row m is one wave's 64 lanes)
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
+            const int idx = tid + 256 * q;
+            const int m = idx >> 6, r = idx & 63;
+            const int n = t * 64 + r;
+            const bool ok = m < M && n < W.n;
+            const float v = ok ? vals[q] * fs[m] : -INFINITY;
+            if (ok && a.out) a.out[(size_t)m * a.out_ld + n] = v;
+            const float mx = wave_max_all(v);
+            const int arg = wave_min_all((ok && v == mx) ? n : INT_MAX);
+            const float se = wave_sum_all(ok ? expf(v - mx) : 0.f);
+            if (m < M && r == 0) a.top1_part[(size_t)m * W.ntiles + t] = make_float4(mx, __int_as_float(arg), se, 0.f);
         }
     } else {  // EPI_SWIGLU: rows 0..31 of the tile are gate rows, 32..63 the matching up rows
 #pragma unroll
@@ -1751,6 +1781,67 @@ hipError_t launch_kv_compact(uint16_t* kc, uint16_t* vc, const int16_t* table, c
     const int chunk = KC_THREADS * KC_PIECES / (S * pps);
     kv_compact_kernel<<<dim3((unsigned)(L * Hkv * 2 * KC_SLICES)), dim3(KC_THREADS), 0, st>>>(kc, vc, table, src, S, Hkv,
                                                                                              cap, D, Pn, chunk);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ top-1 of the LM head
+
+// One workgroup per row: the tiles' (max, index, sum of exp(v - max)) reduced
+// in a fixed order (strided per thread, then a tree), so the result does not
+// depend on timing.  Ties on the value take the smallest index.
+__global__ __launch_bounds__(256) void top1_merge_kernel(const float4* __restrict__ part, int ntiles, int32_t* __restrict__ token,
+                                                         float* __restrict__ p, float* __restrict__ logit) {
+    __shared__ float smx[256];
+    __shared__ int sarg[256];
+    __shared__ float sse[256];
+    const int m = blockIdx.x, tid = threadIdx.x;
+    const float4* row = part + (size_t)m * ntiles;
+    float mx = -INFINITY;
+    int arg = INT_MAX;
+    for (int t = tid; t < ntiles; t += 256) {
+        const float4 e = row[t];
+        const int ei = __float_as_int(e.y);
+        if (e.x > mx || (e.x == mx && ei < arg)) {
+            mx = e.x;
+            arg = ei;
+        }
+    }
+    smx[tid] = mx;
+    sarg[tid] = arg;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if (tid < o) {
+            const float x2 = smx[tid + o];
+            const int a2 = sarg[tid + o];
+            if (x2 > smx[tid] || (x2 == smx[tid] && a2 < sarg[tid])) {
+                smx[tid] = x2;
+                sarg[tid] = a2;
+            }
+        }
+        __syncthreads();
+    }
+    const float gmx = smx[0];
+    float se = 0.f;
+    for (int t = tid; t < ntiles; t += 256) {
+        const float4 e = row[t];
+        se += e.z * expf(e.x - gmx);
+    }
+    sse[tid] = se;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if (tid < o) sse[tid] += sse[tid + o];
+        __syncthreads();
+    }
+    if (tid == 0) {
+        token[m] = sarg[0];
+        p[m] = 1.0f / sse[0];
+        if (logit) logit[m] = gmx;
+    }
+}
+
+hipError_t launch_top1_merge(const float4* part, int M, int ntiles, int32_t* token, float* p, float* logit, hipStream_t st) {
+    if (M < 1 || ntiles < 1) return hipErrorInvalidValue;
+    top1_merge_kernel<<<dim3((unsigned)M), dim3(256), 0, st>>>(part, ntiles, token, p, logit);
     return hipGetLastError();
 }
 

@@ -115,6 +115,12 @@ struct Stage {
     int ring_i = 0;
     int64_t weight_bytes = 0;
     uint64_t fingerprint = 0;                          // of the config, rotary table and norm weights (KV blobs)
+    // final-stage epilogue: final RMSNorm weight and INT4 LM head (stage_head_attach)
+    bool head_ok = false;
+    int vocab = 0;
+    DevMat head;
+    uint16_t* final_norm = nullptr;
+    float4* top1_part = nullptr;                       // [MAX_ROWS][head tiles]
     // persistent-kernel weights (row layout) and barrier state
     bool ps_ok = false;
     int cpl_h = 0, cpl_q = 0, cpl_f = 0, kc_h = 0, kc_q = 0, kc_f = 0, ng_h = 0, ng_q = 0, ng_f = 0;
@@ -1139,6 +1145,89 @@ int kv_restore(KVState* kv, const void* blob, int64_t blob_bytes, int blob_on_de
     HIP_TRY(mark_done(st, s));
     kv->P = Pn;
     if (slot_lengths) std::memcpy(slot_lengths, lens.data(), 4 * (size_t)S);
+    return STAGE_OK;
+}
+
+int stage_head_attach(Stage* st, const uint16_t* final_norm, const QuantMatrix* lm_head, int weights_on_device, void* stream) {
+    if (!st || !final_norm || !lm_head || !lm_head->q || !lm_head->scales) return fail(STAGE_E_INVALID, "NULL argument");
+    if (st->head_ok) return fail(STAGE_E_UNSUPPORTED, "the stage already has a head");
+    const StageConfig& c = st->cfg;
+    const int H = c.hidden;
+    if (lm_head->n < 1 || lm_head->k != H) return fail(STAGE_E_SHAPE, "lm_head must be [vocab >= 1, hidden]");
+    if (!st->bp_ok) return fail(STAGE_E_UNSUPPORTED, "the head needs 128-wide quantization groups");
+    if (lm_head->n > (1 << 30)) return fail(STAGE_E_CAPACITY, "vocab too large");
+    HIP_TRY(hipSetDevice(st->device));
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(order_on(st, s));
+    const int V = lm_head->n, g = c.group_size;
+    DevMat m{};
+    int rc = make_mat(st, m, (V + 63) / 64, H, g);
+    if (rc) return rc;
+    m.pm.n = V;
+    // no split of K: the epilogue's per-tile maxima need a tile's whole sums
+    m.bp_split = 1;
+    m.bp_kg = (m.pm.ngroups + 3) / 4;
+    uint8_t* tmp_q = nullptr;
+    uint16_t* tmp_s = nullptr;
+    if (!weights_on_device) {
+        const size_t qbytes = (size_t)V * ((H + 1) / 2), sbytes = (size_t)V * ((H + g - 1) / g) * 2;
+        if (hipMalloc(&tmp_q, qbytes) != hipSuccess || hipMalloc(&tmp_s, sbytes) != hipSuccess) {
+            (void)hipGetLastError();
+            if (tmp_q) (void)hipFree(tmp_q);
+            return fail(STAGE_E_OOM, "head upload staging allocation failed");
+        }
+    }
+    rc = upload_mat(st, m, *lm_head, weights_on_device, 0, 0, tmp_q, tmp_s, s);
+    if (tmp_q) (void)hipFree(tmp_q);
+    if (tmp_s) (void)hipFree(tmp_s);
+    if (rc) return rc;
+    uint16_t* fn = nullptr;
+    float4* part = nullptr;
+    const size_t nalloc = ((size_t)H + SK_SLOT / 2 - 1) / (SK_SLOT / 2) * (SK_SLOT / 2);
+    if ((rc = st->alloc(&fn, nalloc)) || (rc = st->alloc(&part, (size_t)MAX_ROWS * m.pm.ntiles))) return rc;
+    HIP_TRY(hipMemcpyAsync(fn, final_norm, (size_t)H * 2, weights_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    st->weight_bytes += 2 * (int64_t)H;
+    st->head = m;
+    st->final_norm = fn;
+    st->top1_part = part;
+    st->vocab = V;
+    st->head_ok = true;
+    HIP_TRY(mark_done(st, s));
+    return STAGE_OK;
+}
+
+int stage_head_top1(Stage* st, const void* hidden, int M, int32_t* token_out, float* p_out, float* logit_out,
+                    float* logits_out, void* stream) {
+    if (!st || !hidden || !token_out || !p_out) return fail(STAGE_E_INVALID, "NULL argument");
+    if (!st->head_ok) return fail(STAGE_E_INVALID, "no head attached (stage_head_attach)");
+    if (M < 1 || M > MAX_ROWS) return fail(STAGE_E_CAPACITY, "M must be in [1, STAGE_MAX_ROWS]");
+    const StageConfig& c = st->cfg;
+    const int H = c.hidden, act_dt = dt_code(c.act_dtype);
+    HIP_TRY(hipSetDevice(st->device));
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(order_on(st, s));
+    HIP_TRY(launch_bprep(hidden, act_dt, H, st->final_norm, act_dt, H, c.rms_eps, M, st->bp[0], st->bc[0], st->kp,
+                         st->rsb, s));
+    GemvArgs a{};
+    a.W = st->head.pm;
+    a.M = M;
+    a.kp = st->kp;
+    a.kg = st->head.bp_kg;
+    a.ksplit = 1;
+    a.partial = st->gpart;
+    a.counters = st->gcnt;
+    a.bp_in = st->bp[0];
+    a.bc_in = st->bc[0];
+    a.cb_in = st->cbf[0];
+    a.norm = 2;
+    a.epi = EPI_TOP1;
+    a.out = logits_out;
+    a.out_ld = st->vocab;
+    a.top1_part = st->top1_part;
+    HIP_TRY(launch_gemm_bp(a, s));
+    HIP_TRY(launch_top1_merge(st->top1_part, M, st->head.pm.ntiles, token_out, p_out, logit_out, s));
+    HIP_TRY(mark_done(st, s));
     return STAGE_OK;
 }
 

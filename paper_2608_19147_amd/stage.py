@@ -164,6 +164,35 @@ class Stage:
         check(self.lib.stage_debug_phase_trace(self.handle, out.ctypes.data, n, ctypes.byref(nwg)))
         return out[: nwg.value * self.shape.n_layers * 32].reshape(nwg.value, self.shape.n_layers, 32)
 
+    def attach_head(self, final_norm: torch.Tensor, lm_head, on_device: bool = False, stream=None) -> None:
+        """Final RMSNorm weight [H] (act dtype) and INT4 LM head (``q`` uint8
+        [vocab, H/2], ``scales`` float16 [vocab, H/G], ``n``, ``k``)."""
+        fn = final_norm.contiguous()
+        q, s = lm_head.q, lm_head.scales
+        if not on_device:
+            fn = fn.cpu()
+            q = np.ascontiguousarray(q, dtype=np.uint8)
+            s = np.ascontiguousarray(s).view(np.uint16)
+        qm = _lib.QuantMatrix(q=_ptr(q), scales=_ptr(s), n=lm_head.n, k=lm_head.k)
+        check(self.lib.stage_head_attach(self.handle, ctypes.c_void_p(fn.data_ptr()), ctypes.byref(qm), int(on_device),
+                                         ctypes.c_void_p(_stream_ptr(stream))))
+        self.vocab = int(lm_head.n)
+
+    def head_top1(self, hidden: torch.Tensor, with_logits: bool = False, stream=None):
+        """(token int32 [M], p_max fp32 [M], max logit fp32 [M], logits fp32
+        [M, vocab] or None) on the device for the rows of ``hidden``."""
+        M = int(hidden.shape[0])
+        tok = torch.empty(M, dtype=torch.int32, device=hidden.device)
+        p = torch.empty(M, dtype=torch.float32, device=hidden.device)
+        lg = torch.empty(M, dtype=torch.float32, device=hidden.device)
+        full = torch.empty((M, self.vocab), dtype=torch.float32, device=hidden.device) if with_logits else None
+        check(self.lib.stage_head_top1(self.handle, ctypes.c_void_p(hidden.contiguous().data_ptr()), M,
+                                       ctypes.c_void_p(tok.data_ptr()), ctypes.c_void_p(p.data_ptr()),
+                                       ctypes.c_void_p(lg.data_ptr()),
+                                       ctypes.c_void_p(full.data_ptr() if full is not None else None),
+                                       ctypes.c_void_p(_stream_ptr(stream))))
+        return tok, p, lg, full
+
     def new_state(self, n_slots: int, capacity: int) -> "KVState":
         return KVState(self, n_slots, capacity)
 

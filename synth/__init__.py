@@ -158,6 +158,17 @@ def make_weights(shape: StageShape, seed: int = 0) -> List[LayerData]:
     return [make_layer(shape, l, seed) for l in range(shape.n_layers)]
 
 
+LLAMA3_VOCAB = 128256
+
+
+def make_head(shape: StageShape, vocab: int, seed: int = 0) -> Tuple[torch.Tensor, QuantMatrixData]:
+    """The final stage's RMSNorm weight [H] (act dtype, U(0.8, 1.2)) and INT4
+    LM head [vocab, H] (same recipe as the layer matrices)."""
+    r = rng(seed, shape.config_id, 900_001)
+    fn = round_to(r.uniform(0.8, 1.2, shape.hidden), shape.act_dtype)
+    return fn, make_quant_matrix(vocab, shape.hidden, shape.group_size, rng(seed, shape.config_id, 900_002))
+
+
 def make_kv(shape: StageShape, n_slots: int, n_tokens: int, seed: int = 0, stream: int = 0) -> Tuple[torch.Tensor, torch.Tensor]:
     """Already-stored cache rows ~N(0,1): K and V [L][S][Hkv][n][D] in the KV dtype."""
     dims = (shape.n_layers, n_slots, shape.n_kv_heads, n_tokens, shape.head_dim)

@@ -579,4 +579,62 @@ def pin_compacted_forward_equals_masked_forward():
     assert np.array_equal(oh2, oc2)
 
 
+# ------------------------------------------------------------------ final-stage epilogue
+
+def pin_head_logits_and_top1_against_torch():
+    """Logits against torch (rms_norm and a float64 matmul of the hand-decoded
+    head), top-1 against torch.softmax / torch.max."""
+    shape = TINY
+    fn, lm = synth.make_head(shape, 300, 81)
+    x = f64(synth.make_hidden(shape, 5, 81))
+    got = oracle.head_logits(x, fn, lm.q, lm.scales, 300, shape.group_size, shape.rms_eps)
+    codes = np.empty((300, shape.hidden), np.float64)
+    codes[:, 0::2] = (lm.q & 0x0F).astype(np.float64) - 8
+    codes[:, 1::2] = (lm.q >> 4).astype(np.float64) - 8
+    sc = np.repeat(lm.scales.astype(np.float64), shape.group_size, axis=1)[:, : shape.hidden]
+    w = torch.from_numpy(codes * sc)
+    h = F.rms_norm(torch.from_numpy(x), (shape.hidden,), weight=fn.double(), eps=shape.rms_eps)
+    ref = (h @ w.T).numpy()
+    assert np.max(np.abs(got - ref)) <= 1e-12 * np.max(np.abs(ref))
+    idx, p, mx = oracle.top1(got)
+    pt = torch.softmax(torch.from_numpy(got), dim=1)
+    vt, it = torch.max(torch.from_numpy(got), dim=1)
+    assert np.array_equal(idx, it.numpy()) and np.array_equal(mx, vt.numpy())
+    assert np.allclose(p, pt.numpy()[np.arange(5), idx], rtol=1e-13, atol=0)
+
+
+def pin_top1_bruteforce_and_closed_forms():
+    """Pure-Python loops on small rows; equal logits give p = 1/V at index 0;
+    ties take the first index; one dominant logit gives p -> 1."""
+    r = np.random.default_rng(82)
+    lg = r.standard_normal((3, 17)) * 3
+    lg[1, 4] = lg[1, 11] = lg[1].max() + 1.0                 # a tie: the first index wins
+    idx, p, mx = oracle.top1(lg)
+    for m in range(3):
+        best, bi = -math.inf, -1
+        for j in range(17):
+            if lg[m, j] > best:
+                best, bi = lg[m, j], j
+        tot = 0.0
+        for j in range(17):
+            tot += math.exp(lg[m, j] - best)
+        assert idx[m] == bi and mx[m] == best and abs(p[m] - 1.0 / tot) <= 1e-15
+    assert idx[1] == 4
+    i2, p2, _ = oracle.top1(np.zeros((1, 40)))
+    assert i2[0] == 0 and abs(p2[0] - 1 / 40) <= 1e-16
+    i3, p3, _ = oracle.top1(np.array([[0.0, 60.0, -3.0]]))
+    assert i3[0] == 1 and 1 - p3[0] < 1e-25
+
+
+def pin_head_zero_weights():
+    """A head whose scales are all zero gives zero logits: token 0, p = 1/V."""
+    shape = TINY
+    fn, lm = synth.make_head(shape, 64, 83)
+    lm.scales[:] = 0
+    x = f64(synth.make_hidden(shape, 2, 83))
+    lg = oracle.head_logits(x, fn, lm.q, lm.scales, 64, shape.group_size, shape.rms_eps)
+    idx, p, mx = oracle.top1(lg)
+    assert np.all(lg == 0) and np.all(idx == 0) and np.allclose(p, 1 / 64, rtol=0, atol=1e-16)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -165,7 +165,29 @@ def _compact_factory(kind):
     return comp
 
 
+def _top1_last_tie(logits):
+    logits = np.atleast_2d(np.asarray(logits, dtype=np.float64))
+    idx = logits.shape[1] - 1 - np.argmax(logits[:, ::-1], axis=1)
+    mx = logits[np.arange(logits.shape[0]), idx]
+    return idx, 1.0 / np.exp(logits - mx[:, None]).sum(axis=1), mx
+
+
+def _top1_prob_of_first(logits):
+    logits = np.atleast_2d(np.asarray(logits, dtype=np.float64))
+    idx = np.argmax(logits, axis=1)
+    mx = logits[np.arange(logits.shape[0]), idx]
+    return idx, np.exp(logits[:, 0] - mx) / np.exp(logits - mx[:, None]).sum(axis=1), mx
+
+
+def _head_no_norm(x, final_norm, lm_q, lm_scales, vocab, group, eps):
+    x = np.atleast_2d(np.asarray(x, dtype=np.float64))
+    return so.gemv_rows(x * so._as_f64(final_norm), so.dequant(lm_q, lm_scales, x.shape[1], group))
+
+
 MUTANTS = {
+    "top1_last_tie": ("top1", _top1_last_tie),
+    "top1_prob_of_first": ("top1", _top1_prob_of_first),
+    "head_no_norm": ("head_logits", _head_no_norm),
     "compact_reversed": ("compact", _compact_factory("reversed")),
     "compact_stale_padding": ("compact", _compact_factory("stale_padding")),
     "compact_min_length": ("compact", _compact_factory("min_length")),
