@@ -33,6 +33,10 @@ same fields, no CPU baseline):
                 Bernoulli(0.6) acceptance (about 7% masked holes per slot);
                 kv_compact in place (state re-installed from a full blob before
                 each timed call) and kv_capture of the kept rows to a device blob;
+  tree8b        tree-shaped speculative verify on the 8B half stage: one slot at KV
+                2048, a 15-node binary draft tree (depth 3) in one forward with a
+                per-query-row mask (each node sees the cache and its ancestors);
+                beside it the 5-token linear verify of one path;
   head8b        final-stage epilogue: final RMSNorm + INT4 LM head (128256 x 4096,
                 group 128) + on-device top-1 (token, probability), 1 and 20 rows;
   copycal       1 GiB device copies (calibration of HBM byte counters).
@@ -124,7 +128,7 @@ def cpu_baseline(shape, kv_len: int, layers_sampled: int, seed: int, min_seconds
     }
 
 
-WORKLOADS = ("decode8b", "verify8b", "microbatch8b", "decode70b", "verify70b", "compact8b", "head8b", "copycal")
+WORKLOADS = ("decode8b", "verify8b", "microbatch8b", "decode70b", "verify70b", "tree8b", "compact8b", "head8b", "copycal")
 
 
 def _line(metric, value, unit, args, steps, ms, config, bytes_per_step, roof, higher=True, **extra):
@@ -247,6 +251,49 @@ def other_workload(args) -> int:
                            query_tokens_per_s=round(S * n * 1e3 / ms, 1),
                            emitted_tokens_per_s=round(tot_em / tot_s, 1),
                            mean_tokens_kept_per_slot_step=round(tot_em / (steps * S), 4)))
+
+    elif args.workload == "tree8b":
+        P = 2048
+        parent = [-1] + [(i - 1) // 2 for i in range(1, 15)]       # binary tree: 1 + 2 + 4 + 8 nodes
+        n = len(parent)
+        anc = np.zeros((n, n), np.uint8)
+        for i in range(n):
+            k = i
+            while k >= 0:
+                anc[i, k] = 1
+                k = parent[k]
+        depth = anc.sum(axis=1) - 1
+        rows = np.ones((1, n, P + n), np.uint8)
+        rows[0, :, P:] = anc
+        state = stage.new_state(1, P + n + 8)
+        k, v = synth.make_kv(shape, 1, P, args.seed)
+        state.append(k, v)
+        del k, v
+        cases = [("tree", n, Request(state, (P + depth)[None].astype(np.int32), None, None, rows)),
+                 ("linear", 5, Request(state, (P + np.arange(5))[None].astype(np.int32), np.ones((1, P + 5), np.uint8)))]
+        for name, nn, req in cases:
+            xs = [synth.make_hidden(shape, nn, args.seed, 500 + i).cuda() for i in range(4)]
+            out = torch.empty_like(xs[0])
+            for i in range(args.warmup):
+                stage.forward([req], xs[i % 4], out)
+                state.truncate(P)
+            torch.cuda.synchronize()
+            stage.profile("gateup")
+            t = time.perf_counter()
+            for i in range(args.steps):
+                stage.forward([req], xs[i % 4], out)
+                state.truncate(P)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t) * 1e3 / args.steps
+            prof = stage.profile_read()
+            stage.profile(None)
+            desc = (f"{n}-node binary draft tree (depth 3), per-query-row mask" if name == "tree"
+                    else "5-token linear verify of one path")
+            cfg = {"workload": f"llama3.1-8b half stage spec verify, 1 slot, kv {P}, {desc}", **base_cfg,
+                   "kv_len": P, "tokens": nn}
+            lines.append(_line(f"spec-verify steps/s (8B half-stage, {name}, {nn} tokens)", 1e3 / ms, "steps/s", args,
+                               args.steps, ms, cfg, wbytes + (P + nn) * kvb, _gateup_roofline(shape, prof),
+                               query_tokens_per_s=round(nn * 1e3 / ms, 1)))
 
     elif args.workload == "decode70b":
         P = 8192

@@ -253,6 +253,15 @@ int kv_restore(KVState* state, const void* blob, int64_t blob_bytes, int blob_on
  *   attention_mask : host uint8 [S * mask_len], mask_len must equal P + n_tokens;
  *                    0 hides that key column from every query of the slot;
  *                    query i also never sees physical rows after P + i.
+ *   attention_mask_rows : optional host uint8 [S * n_tokens * mask_len], one
+ *                    key mask per query row (the 4-D form [slot][query][key] of
+ *                    "Continuous Batching on CPU, GPU, and NPU": block-diagonal
+ *                    packed sequences, a shared prefix region, tree-shaped
+ *                    drafts); NULL = none.  With it, query i of slot b sees
+ *                    key j iff attention_mask (if given) keeps j, row i keeps j,
+ *                    and j <= P + i (a query never sees a row appended after
+ *                    it; tree drafts are given in an order where every node
+ *                    follows its ancestors).  attention_mask may then be NULL.
  * Every query row must see at least one key (else STAGE_E_INVALID; a fully
  * masked softmax row has no value). */
 typedef struct StageRequest {
@@ -262,6 +271,7 @@ typedef struct StageRequest {
     const int32_t* beam_idx;
     const uint8_t* attention_mask;
     int32_t        mask_len;
+    const uint8_t* attention_mask_rows;
 } StageRequest;
 
 /* The forward of the stage ("Stateful KV-Cached Inference": hidden states,

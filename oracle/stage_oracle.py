@@ -158,20 +158,26 @@ def gemv_rows(h: np.ndarray, w: np.ndarray) -> np.ndarray:
 
 
 def attention_slot(q: np.ndarray, kc: np.ndarray, vc: np.ndarray, past: int,
-                   mask: np.ndarray) -> np.ndarray:
+                   mask: np.ndarray, mask_rows: Optional[np.ndarray] = None) -> np.ndarray:
     """Attention of one cache slot.
 
     q [n, Hq, D] (rotated), kc/vc [Hkv, >= past+n, D] (the slot's cache rows
-    after the new ones were appended), mask [past+n] (nonzero = visible).
-    Query i sees key j iff j <= past + i and mask[j] != 0; masked keys are
-    skipped, so they never enter the max or the sums.
+    after the new ones were appended), mask [past+n] (nonzero = visible) and
+    optionally mask_rows [n, past+n], one key mask per query (paper,
+    "Continuous Batching on CPU, GPU, and NPU": the per-query 4-D mask of a
+    packed window).  Query i sees key j iff j <= past + i, mask[j] != 0 and
+    (with mask_rows) mask_rows[i, j] != 0; hidden keys are skipped, so they
+    never enter the max or the sums.
     """
     n, hq, d = q.shape
     hkv = kc.shape[0]
     rep = hq // hkv
     out = np.empty_like(q)
     for i in range(n):
-        keep = np.flatnonzero(np.asarray(mask[: past + i + 1]) != 0)
+        vis = np.asarray(mask[: past + i + 1]) != 0
+        if mask_rows is not None:
+            vis = vis & (np.asarray(mask_rows[i, : past + i + 1]) != 0)
+        keep = np.flatnonzero(vis)
         if keep.size == 0:
             raise ValueError(f"query row {i} has no visible key")
         for h in range(hq):
@@ -319,12 +325,14 @@ def top1(logits) -> tuple:
     return idx, p, mx
 
 
-def forward(stage: OracleStage, state: OracleState, x, positions, beam_idx=None, mask=None) -> np.ndarray:
+def forward(stage: OracleStage, state: OracleState, x, positions, beam_idx=None, mask=None,
+            mask_rows=None) -> np.ndarray:
     """One stage forward for one request.
 
     x [S*n, H] (rows slot-major, token-minor; activation-dtype values),
     positions [S, n] integers, beam_idx [S] or None, mask [S, P+n] (None =
-    all visible).  Returns hidden_out [S*n, H] fp64 and advances ``state``.
+    all visible), mask_rows [S, n, P+n] (one key mask per query row) or None.
+    Returns hidden_out [S*n, H] fp64 and advances ``state``.
     """
     sh = stage.shape
     positions = np.asarray(positions, dtype=np.int64)
@@ -339,6 +347,10 @@ def forward(stage: OracleStage, state: OracleState, x, positions, beam_idx=None,
     mask = np.asarray(mask)
     if mask.shape != (S, P + n):
         raise ValueError(f"mask shape {mask.shape} != {(S, P + n)}")
+    if mask_rows is not None:
+        mask_rows = np.asarray(mask_rows)
+        if mask_rows.shape != (S, n, P + n):
+            raise ValueError(f"mask_rows shape {mask_rows.shape} != {(S, n, P + n)}")
     x = np.array(x, dtype=np.float64).reshape(S * n, sh.hidden)
 
     # Gather(ReadValue, beam_idx, axis=0): a physical reorder of every layer's cache.
@@ -365,7 +377,8 @@ def forward(stage: OracleStage, state: OracleState, x, positions, beam_idx=None,
         state.V[l][:, :, P:P + n] = v.transpose(0, 2, 1, 3)
         o = np.empty_like(q)
         for b in range(S):
-            o[b] = attention_slot(q[b], state.K[l][b], state.V[l][b], P, mask[b])
+            o[b] = attention_slot(q[b], state.K[l][b], state.V[l][b], P, mask[b],
+                                  None if mask_rows is None else mask_rows[b])
         x = x + gemv_rows(o.reshape(S * n, Hq * D), w["wo"])
         h2 = rmsnorm(x, w["ffn_norm"], sh.rms_eps)
         act = silu(gemv_rows(h2, w["wg"])) * gemv_rows(h2, w["wu"])
@@ -383,7 +396,8 @@ def forward_batch(stage: OracleStage, requests: List[dict], hidden) -> np.ndarra
     for req in requests:
         S, n = np.asarray(req["positions"]).shape
         rows = hidden[r0:r0 + S * n]
-        outs.append(forward(stage, req["state"], rows, req["positions"], req.get("beam_idx"), req.get("mask")))
+        outs.append(forward(stage, req["state"], rows, req["positions"], req.get("beam_idx"), req.get("mask"),
+                            req.get("mask_rows")))
         r0 += S * n
     if r0 != hidden.shape[0]:
         raise ValueError("hidden rows do not match the requests")

@@ -54,6 +54,7 @@ class StageRequest(ctypes.Structure):
     _fields_ = [
         ("state", ctypes.c_void_p), ("n_tokens", ctypes.c_int32), ("positions", ctypes.c_void_p),
         ("beam_idx", ctypes.c_void_p), ("attention_mask", ctypes.c_void_p), ("mask_len", ctypes.c_int32),
+        ("attention_mask_rows", ctypes.c_void_p),
     ]
 
 

@@ -35,6 +35,7 @@ struct PackedMat {
 // Per-request metadata on the device (one forward).
 struct ReqDev {
     int P, n, S, row0, cap, mask_off, mask_len, item0;
+    int rowmask_off;     // per-query-row masks [S][n][mask_len] in MetaDev::masks, or -1 (slot masks only)
     int splits;          // most attention splits per (slot, kv head): a function of the request alone
     uint16_t* kc;        // K cache, layer 0 base: [L][S][Hkv][cap][D]
     uint16_t* vc;        // V cache
@@ -51,7 +52,7 @@ struct MetaDev {
     const ItemDev* items;
     const int* positions;   // [M]: rotary position of each activation row
     const int* row_item;    // [M]: item (request slot) of each activation row
-    const uint8_t* masks;   // concatenated [S][P+n] per request
+    const uint8_t* masks;   // concatenated [S][P+n] per request, then the requests' per-row masks
     int n_items, M, n_req;
 };
 

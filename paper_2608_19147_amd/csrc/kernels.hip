@@ -911,6 +911,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     uint16_t* kl = rq.kc + (size_t)a.layer * lstride;
     uint16_t* vl = rq.vc + (size_t)a.layer * lstride;
     const uint8_t* mask = a.meta.masks + rq.mask_off + (size_t)b * rq.mask_len;
+    // per-query-row masks of the slot, [n][mask_len], when the request has them
+    const uint8_t* rmask = rq.rowmask_off >= 0 ? a.meta.masks + rq.rowmask_off + (size_t)b * n * rq.mask_len : nullptr;
     const int16_t* tab = rq.table + (size_t)b * rq.cap;
     const int rowbase = rq.row0 + b * n;
     const int d0 = li * EPL;
@@ -961,6 +963,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
                 for (int e = 0; e < EPL; ++e) sd += q[rr][e] * kf[e];
                 sd = sum16(sd);
                 if (j > P + qi[rr]) continue;                 // causal over the physical index
+                if (rmask && rmask[(size_t)qi[rr] * rq.mask_len + j] == 0) continue;   // hidden from this row
                 const float mn = fmaxf(mx[rr], sd);
                 const float corr = exp2f(mx[rr] - mn);
                 const float p = exp2f(sd - mn);
@@ -1218,6 +1221,8 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
     uint16_t* kl = rq.kc + (size_t)a.layer * lstride;
     uint16_t* vl = rq.vc + (size_t)a.layer * lstride;
     const uint8_t* mask = a.meta.masks + rq.mask_off + (size_t)b * rq.mask_len;
+    // per-query-row masks of the slot, [n][mask_len], when the request has them
+    const uint8_t* rmask = rq.rowmask_off >= 0 ? a.meta.masks + rq.rowmask_off + (size_t)b * n * rq.mask_len : nullptr;
     const int16_t* tab = rq.table + (size_t)b * rq.cap;
     const int rowbase = rq.row0 + b * n;
 
@@ -1437,6 +1442,14 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
                     const int ko = (e < 4) ? e : 12 + e;
                     const float x = e < 4 ? s0[e] : s1[e - 4];
                     sv[e] = (((vbits >> e) & 1u) && ko <= last) ? x : -INFINITY;
+                }
+                if (rmask) {                                 // this query row's own mask (uniform branch)
+                    const uint8_t* rrow = rmask + (size_t)min(qtok[u], n - 1) * rq.mask_len;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int j = min(kbase + ((e < 4) ? e : 12 + e), rq.mask_len - 1);
+                        if (rrow[j] == 0) sv[e] = -INFINITY;
+                    }
                 }
                 if constexpr (REC) {                             // test support: this tile's visible scores
                     const int r = 16 * (qg + wave + 4 * u) + ql;

@@ -1309,7 +1309,8 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             if (reqs[r2].state == q.state) return fail(STAGE_E_STATE_MISMATCH, who + "state used twice in one forward");
         const int S = q.state->S, n = q.n_tokens, P = q.state->P;
         if (n < 1) return fail(STAGE_E_INVALID, who + "n_tokens must be positive");
-        if (!q.positions || !q.attention_mask) return fail(STAGE_E_INVALID, who + "positions and attention_mask are required");
+        if (!q.positions || (!q.attention_mask && !q.attention_mask_rows))
+            return fail(STAGE_E_INVALID, who + "positions and a mask (attention_mask or attention_mask_rows) are required");
         if (q.mask_len != P + n)
             return fail(STAGE_E_SHAPE, who + "mask_len " + std::to_string(q.mask_len) + " != P + n = " + std::to_string(P + n));
         if (P + n > q.state->cap) return fail(STAGE_E_CAPACITY, who + "P + n exceeds the state's capacity");
@@ -1320,17 +1321,28 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             for (int b = 0; b < S; ++b)
                 if (q.beam_idx[b] < 0 || q.beam_idx[b] >= S) return fail(STAGE_E_INVALID, who + "beam_idx out of range");
         for (int b = 0; b < S; ++b) {
-            const uint8_t* mk = q.attention_mask + (size_t)b * q.mask_len;
-            int first = -1;
-            for (int j = 0; j < P + n; ++j)
-                if (mk[j]) { first = j; break; }
-            if (first < 0 || first > P)   // query 0 sees rows 0..P; later queries see more
-                return fail(STAGE_E_INVALID, who + "slot " + std::to_string(b) + " has a query row with no visible key");
+            const uint8_t* mk = q.attention_mask ? q.attention_mask + (size_t)b * q.mask_len : nullptr;
+            if (!q.attention_mask_rows) {
+                int first = -1;
+                for (int j = 0; j < P + n; ++j)
+                    if (mk[j]) { first = j; break; }
+                if (first < 0 || first > P)   // query 0 sees rows 0..P; later queries see more
+                    return fail(STAGE_E_INVALID, who + "slot " + std::to_string(b) + " has a query row with no visible key");
+                continue;
+            }
+            for (int i = 0; i < n; ++i) {     // each query row: some key j <= P + i kept by both masks
+                const uint8_t* rw = q.attention_mask_rows + ((size_t)b * n + i) * q.mask_len;
+                bool any = false;
+                for (int j = 0; j <= P + i && !any; ++j) any = rw[j] && (!mk || mk[j]);
+                if (!any)
+                    return fail(STAGE_E_INVALID, who + "slot " + std::to_string(b) + " query " + std::to_string(i) +
+                                                     " sees no key");
+            }
         }
         M += S * n;
         n_items += S;
         max_queries_item = std::max(max_queries_item, gs * n);
-        mask_bytes += (size_t)S * q.mask_len;
+        mask_bytes += (size_t)S * q.mask_len * (q.attention_mask_rows ? (size_t)(1 + n) : 1);
         if (q.beam_idx) beam_ints += S;
     }
     if (M > MAX_ROWS) return fail(STAGE_E_CAPACITY, "total rows " + std::to_string(M) + " exceed STAGE_MAX_ROWS");
@@ -1388,6 +1400,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             d.cap = kv->cap;
             d.mask_off = (int)moff;
             d.mask_len = q.mask_len;
+            d.rowmask_off = q.attention_mask_rows ? (int)(moff + (size_t)S * q.mask_len) : -1;   // rows follow the slot masks
             d.item0 = item;
             // attention splits: about two workgroups per CU over the request's own
             // slots and kv heads (never its batch-mates, so they cannot change its
@@ -1403,7 +1416,27 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
                 for (int i = 0; i < n; ++i) ritem[row + b * n + i] = item + b;
             }
             std::memcpy(pos + row, q.positions, sizeof(int) * S * n);
-            std::memcpy(masks + moff, q.attention_mask, (size_t)S * q.mask_len);
+            if (!q.attention_mask_rows) {
+                std::memcpy(masks + moff, q.attention_mask, (size_t)S * q.mask_len);
+            } else {
+                // slot mask: the keys some row of the slot keeps (and the 2-D mask keeps);
+                // the rows follow, each refined by the 2-D mask
+                const size_t ml = (size_t)q.mask_len;
+                uint8_t* sm = masks + moff;
+                uint8_t* rm = sm + (size_t)S * ml;
+                for (int b = 0; b < S; ++b)
+                    for (size_t j = 0; j < ml; ++j) {
+                        const bool keep2 = !q.attention_mask || q.attention_mask[b * ml + j];
+                        uint8_t any = 0;
+                        for (int i = 0; i < n; ++i) {
+                            const uint8_t v = (keep2 && q.attention_mask_rows[((size_t)b * n + i) * ml + j]) ? 1 : 0;
+                            rm[((size_t)b * n + i) * ml + j] = v;
+                            any |= v;
+                        }
+                        sm[b * ml + j] = any;
+                    }
+                moff += (size_t)S * n * ml;
+            }
             row += S * n;
             item += S;
             moff += (size_t)S * q.mask_len;

@@ -214,8 +214,9 @@ class Stage:
         keep = []
         for i, r in enumerate(requests):
             pos = np.ascontiguousarray(r.positions, dtype=np.int32)
-            mask = np.ascontiguousarray(r.mask, dtype=np.uint8)
-            keep += [pos, mask]
+            mask = None if r.mask is None else np.ascontiguousarray(r.mask, dtype=np.uint8)
+            rows = None if r.mask_rows is None else np.ascontiguousarray(r.mask_rows, dtype=np.uint8)
+            keep += [pos, mask, rows]
             beam = None
             if r.beam_idx is not None:
                 beam = np.ascontiguousarray(r.beam_idx, dtype=np.int32)
@@ -224,8 +225,10 @@ class Stage:
             arr[i].n_tokens = int(r.n_tokens)
             arr[i].positions = pos.ctypes.data
             arr[i].beam_idx = beam.ctypes.data if beam is not None else None
-            arr[i].attention_mask = mask.ctypes.data
-            arr[i].mask_len = int(mask.shape[-1]) if mask.ndim else 0
+            arr[i].attention_mask = mask.ctypes.data if mask is not None else None
+            arr[i].attention_mask_rows = rows.ctypes.data if rows is not None else None
+            src = mask if mask is not None else rows
+            arr[i].mask_len = int(src.shape[-1]) if src is not None and src.ndim else 0
         check(self.lib.stage_forward(self.handle, arr, len(requests), ctypes.c_void_p(hidden_in.data_ptr()),
                                      ctypes.c_void_p(hidden_out.data_ptr()), ctypes.c_void_p(_stream_ptr(stream))))
         return hidden_out
@@ -234,12 +237,14 @@ class Stage:
 @dataclass
 class Request:
     """One request of a forward: positions [S, n] int32, mask [S, P+n] uint8
-    (nonzero = visible), beam_idx [S] int32 or None."""
+    (nonzero = visible) or None, beam_idx [S] int32 or None, mask_rows
+    [S, n, P+n] uint8 (one key mask per query row) or None."""
 
     state: "KVState"
     positions: np.ndarray
-    mask: np.ndarray
+    mask: Optional[np.ndarray]
     beam_idx: Optional[np.ndarray] = None
+    mask_rows: Optional[np.ndarray] = None
 
     @property
     def n_tokens(self) -> int:

@@ -637,4 +637,86 @@ def pin_head_zero_weights():
     assert np.all(lg == 0) and np.all(idx == 0) and np.allclose(p, 1 / 64, rtol=0, atol=1e-16)
 
 
+# ------------------------------------------------------------------ per-row (4-D) masks
+
+def tree_case():
+    """A draft tree of 6 nodes after one root: parent of node i (-1 = the
+    cache), listed so that every node follows its parent, and the mask rows
+    that let node i see the cache and its ancestors only."""
+    parent = [-1, 0, 0, 1, 1, 2]
+    n = len(parent)
+    anc = np.zeros((n, n), np.uint8)
+    for i in range(n):
+        k = i
+        while k >= 0:
+            anc[i, k] = 1
+            k = parent[k]
+    depth = anc.sum(axis=1) - 1
+    return parent, anc, depth
+
+
+def pin_row_masks_equal_slot_mask():
+    """Rows that all repeat the 2-D mask give the 2-D forward, bitwise."""
+    shape = TINY2
+    st, _ = oracle_stage(shape, 91)
+    a = oracle_state(shape, 2, 30, 64, 91)
+    b = a.copy()
+    mask = np.ones((2, 34), np.uint8)
+    mask[0, [3, 17]] = 0
+    mask[1, 31] = 0
+    rows = np.repeat(mask[:, None, :], 4, axis=1)
+    x = f64(synth.make_hidden(shape, 8, 91))
+    pos = np.array([[28, 29, 30, 31], [29, 30, 30, 31]])
+    oa = oracle.forward(st, a, x, pos, None, mask)
+    ob = oracle.forward(st, b, x, pos, None, None, rows)
+    assert np.array_equal(oa, ob)
+
+
+def pin_tree_verify_equals_paths():
+    """A tree of drafts verified in one forward with per-row masks equals each
+    root-to-leaf path verified on its own (a linear verify on a copy of the
+    cache), bitwise, node by node (paper, "Negative Results": tree-shaped
+    speculation needs a per-query mask)."""
+    shape = TINY2
+    st, _ = oracle_stage(shape, 92)
+    past = 25
+    base = oracle_state(shape, 1, past, 64, 92)
+    parent, anc, depth = tree_case()
+    n = len(parent)
+    x = f64(synth.make_hidden(shape, n, 92))
+    rows = np.ones((1, n, past + n), np.uint8)
+    rows[0, :, past:] = anc
+    pos = (past + depth)[None]
+    tree = oracle.forward(st, base.copy(), x, pos, None, None, rows)
+    leaves = [i for i in range(n) if i not in parent]
+    for leaf in leaves:
+        path = [i for i in range(n) if anc[leaf, i]]           # ancestors in order, ending at the leaf
+        lin = oracle.forward(st, base.copy(), x[path], pos[:, path], None, None)
+        assert np.array_equal(lin, tree[path]), (leaf, np.max(np.abs(lin - tree[path])))
+
+
+def pin_packed_sequences_equal_separate():
+    """Two sequences packed into one slot behind a shared prefix, each seeing
+    the prefix and its own tokens (block-diagonal rows), equal the two run on
+    separate copies of the prefix, bitwise (paper, "Continuous Batching on CPU,
+    GPU, and NPU": packed slots share a read-only prefix region)."""
+    shape = TINY2
+    st, _ = oracle_stage(shape, 93)
+    past, na, nb = 20, 3, 2
+    base = oracle_state(shape, 1, past, 64, 93)
+    n = na + nb
+    x = f64(synth.make_hidden(shape, n, 93))
+    rows = np.zeros((1, n, past + n), np.uint8)
+    rows[0, :, :past] = 1
+    for i in range(na):
+        rows[0, i, past:past + i + 1] = 1
+    for i in range(nb):
+        rows[0, na + i, past + na:past + na + i + 1] = 1
+    pos = np.concatenate([past + np.arange(na), past + np.arange(nb)])[None]
+    packed = oracle.forward(st, base.copy(), x, pos, None, None, rows)
+    sa = oracle.forward(st, base.copy(), x[:na], pos[:, :na], None, None)
+    sb = oracle.forward(st, base.copy(), x[na:], pos[:, na:], None, None)
+    assert np.array_equal(packed[:na], sa) and np.array_equal(packed[na:], sb)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -56,14 +56,18 @@ def _silu_wrong(z):
 def _attn_factory(kind):
     orig = so.attention_slot
 
-    def attn(q, kc, vc, past, mask):
+    def attn(q, kc, vc, past, mask, mask_rows=None):
         n, hq, d = q.shape
         hkv = kc.shape[0]
         rep = hq // hkv
         out = np.empty_like(q)
         for i in range(n):
             lim = past + n if kind == "no_causal" else past + i + 1
-            keep = np.flatnonzero(np.asarray(mask[:lim]) != 0)
+            vis = np.asarray(mask[:lim]) != 0
+            if mask_rows is not None and kind != "rows_ignored":
+                ri = n - 1 - i if kind == "rows_reversed" else i
+                vis = vis & (np.asarray(mask_rows[ri, :lim]) != 0)
+            keep = np.flatnonzero(vis)
             if kind == "mask_ignored":
                 keep = np.arange(lim)
             if keep.size == 0:
@@ -93,7 +97,7 @@ def _round_trunc(x, fmt):
 def _forward_factory(kind):
     """A copy of the oracle's forward with one wiring mistake in the layer."""
 
-    def fwd(stage, state, x, positions, beam_idx=None, mask=None):
+    def fwd(stage, state, x, positions, beam_idx=None, mask=None, mask_rows=None):
         sh = stage.shape
         positions = np.asarray(positions, dtype=np.int64)
         S, n = positions.shape
@@ -128,7 +132,8 @@ def _forward_factory(kind):
             state.V[l][:, :, P:P + n] = v.transpose(0, 2, 1, 3)
             o = np.empty_like(q)
             for b in range(S):
-                o[b] = so.attention_slot(q[b], state.K[l][b], state.V[l][b], P, mask[b])
+                o[b] = so.attention_slot(q[b], state.K[l][b], state.V[l][b], P, mask[b],
+                                         None if mask_rows is None else mask_rows[b])
             h_attn = x
             x = x + so.gemv_rows(o.reshape(S * n, Hq * D), w["wo"])
             h2 = so.rmsnorm(h_attn if kind == "ffn_norm_on_h" else x, w[n_ffn], sh.rms_eps)
@@ -206,6 +211,8 @@ MUTANTS = {
     "attn_mask_ignored": ("attention_slot", _attn_factory("mask_ignored")),
     "attn_gqa_mod": ("attention_slot", _attn_factory("gqa_mod")),
     "attn_scale": ("attention_slot", _attn_factory("scale")),
+    "attn_rows_ignored": ("attention_slot", _attn_factory("rows_ignored")),
+    "attn_rows_reversed": ("attention_slot", _attn_factory("rows_reversed")),
     "round_truncates": ("round_rne", _round_trunc),
 }
 
