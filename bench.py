@@ -33,6 +33,9 @@ same fields, no CPU baseline):
                 Bernoulli(0.6) acceptance (about 7% masked holes per slot);
                 kv_compact in place (state re-installed from a full blob before
                 each timed call) and kv_capture of the kept rows to a device blob;
+  prefill8b     prompt prefill on the 8B half stage: 2048 prompt tokens from an empty
+                cache (and 512 after 1536 cached rows), stage_prefill (64-row chunks,
+                layer-major, matrix-core products and causal attention);
   tree8b        tree-shaped speculative verify on the 8B half stage: one slot at KV
                 2048, a 15-node binary draft tree (depth 3) in one forward with a
                 per-query-row mask (each node sees the cache and its ancestors);
@@ -128,7 +131,8 @@ def cpu_baseline(shape, kv_len: int, layers_sampled: int, seed: int, min_seconds
     }
 
 
-WORKLOADS = ("decode8b", "verify8b", "microbatch8b", "decode70b", "verify70b", "tree8b", "compact8b", "head8b", "copycal")
+WORKLOADS = ("decode8b", "verify8b", "microbatch8b", "decode70b", "verify70b", "prefill8b", "tree8b", "compact8b", "head8b",
+             "copycal")
 
 
 def _line(metric, value, unit, args, steps, ms, config, bytes_per_step, roof, higher=True, **extra):
@@ -251,6 +255,49 @@ def other_workload(args) -> int:
                            query_tokens_per_s=round(S * n * 1e3 / ms, 1),
                            emitted_tokens_per_s=round(tot_em / tot_s, 1),
                            mean_tokens_kept_per_slot_step=round(tot_em / (steps * S), 4)))
+
+    elif args.workload == "prefill8b":
+        MFMA_PEAK = 2500.0                                   # dense fp16 TFLOP/s
+        for P0, n in ((0, 2048), (1536, 512)):
+            state = stage.new_state(1, P0 + n + 8)
+            if P0:
+                k, v = synth.make_kv(shape, 1, P0, args.seed)
+                state.append(k, v)
+                del k, v
+            x = synth.make_hidden(shape, n, args.seed, 600).cuda()
+            out = torch.empty_like(x)
+            pos = P0 + np.arange(n, dtype=np.int32)
+            steps = max(1, args.steps // 20)
+            for i in range(max(1, args.warmup // 5)):
+                stage.prefill(state, pos, x, hidden_out=out)
+                state.truncate(P0)
+            torch.cuda.synchronize()
+            stage.profile("gateup")
+            t = time.perf_counter()
+            for i in range(steps):
+                stage.prefill(state, pos, x, hidden_out=out)
+                state.truncate(P0)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t) * 1e3 / steps
+            launches, gu_ms = stage.profile_read()
+            stage.profile(None)
+            # gate|up launches: one per layer and 64-row chunk
+            per = gu_ms / max(1, launches)
+            chunk_rows = [min(64, n - r0) for r0 in range(0, n, 64)]
+            gu_flop = 2.0 * 2 * shape.ffn * shape.hidden * (sum(chunk_rows) / len(chunk_rows))
+            tf = gu_flop / (per * 1e-3) / 1e12
+            roof = {"bound": "mfma", "kernel": "gemm_bp_kernel gate|up (one launch per layer and 64-row chunk)",
+                    "achieved": round(tf, 1), "peak": MFMA_PEAK, "unit": "TFLOP/s", "frac": round(tf / MFMA_PEAK, 4),
+                    "traffic": None, "flop_per_launch": gu_flop, "avg_launch_us": round(per * 1e3, 3),
+                    "launches_timed": launches}
+            lin_flop = 2.0 * n * shape.weight_bytes() * 2 / 1.03   # ~2 int4 weights per byte (scales ~3% of bytes)
+            cfg = {"workload": f"llama3.1-8b half stage prefill, {n} prompt tokens after {P0} cached rows", **base_cfg,
+                   "prompt_tokens": n, "kv_len_before": P0, "chunk_rows": 64}
+            lines.append(_line(f"prefill tokens/s (8B half-stage, {n} tokens after {P0})", n * 1e3 / ms, "tokens/s", args,
+                               steps, ms, cfg, wbytes + (P0 + n) * kvb, roof,
+                               linear_tflops=round(lin_flop / (ms * 1e-3) / 1e12, 1)))
+            state.free()
+            del x, out
 
     elif args.workload == "tree8b":
         P = 2048

@@ -289,6 +289,31 @@ int stage_forward(Stage* stage, const StageRequest* reqs, int n_req,
                   const void* hidden_in, void* hidden_out, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Prefill ("Stateful KV-Cached Inference": the prompt goes through the stage
+ * in one call that fills the cache before decoding; "NPU Stages: Static,
+ * Stateless Shards": a long prompt is processed in fixed-size chunks).
+ * ------------------------------------------------------------------------ */
+
+/* Most prompt rows of one stage_prefill call. */
+#define STAGE_MAX_PREFILL 8192
+
+/* n_tokens prompt rows of a one-slot state, appended after its P rows:
+ * hidden_in / hidden_out device [n][H] in act_dtype (must not overlap);
+ * positions host int32 [n] (rotary positions); past_mask host uint8 [P] or
+ * NULL (0 hides that past row from every prompt row).  Prompt row i sees the
+ * past rows the mask keeps and prompt rows 0..i.  The result equals
+ * stage_forward of the same rows with that mask (up to rounding: the prompt
+ * is processed in chunks of STAGE_MAX_ROWS rows, every chunk of a layer
+ * before the next layer, each chunk's RMSNorm input normalized in full).
+ * Afterwards P += n.  Allocates a workspace of 4 * n * H bytes on first use
+ * (kept, grown when a longer prompt comes).
+ * Errors: INVALID (NULL, overlap), SHAPE (state with more than one slot),
+ * CAPACITY (n outside [1, STAGE_MAX_PREFILL], P + n > capacity, position),
+ * STATE_MISMATCH, UNSUPPORTED (group size other than 128), OOM, HIP. */
+int stage_prefill(Stage* stage, KVState* state, int n_tokens, const int32_t* positions, const uint8_t* past_mask,
+                  const void* hidden_in, void* hidden_out, void* stream);
+
+/* ------------------------------------------------------------------------
  * Final-stage epilogue ("Top-1 Logits Compression": the last stage returns
  * the top-1 token and its probability instead of a full logits row; the last
  * stage of the pipeline owns the final norm and the LM head).

@@ -16,6 +16,7 @@ DTYPE_F16 = 1
 DTYPE_BF16 = 2
 MAX_ROWS = 64
 STATIC_SCRATCH_BYTES = 64 << 20   # STAGE_STATIC_SCRATCH_BYTES
+MAX_PREFILL = 8192                # STAGE_MAX_PREFILL
 
 # Every function that include/stage.h declares.
 EXPORTS = (
@@ -25,7 +26,7 @@ EXPORTS = (
     "stage_profile_enable", "stage_profile_read", "stage_debug_phase_trace", "stage_device_status",
     "stage_debug_attn_arm", "stage_debug_attn_read",
     "kv_compact", "kv_capture_size", "kv_capture", "kv_restore", "kv_capture_noalloc",
-    "stage_head_attach", "stage_head_top1",
+    "stage_head_attach", "stage_head_top1", "stage_prefill",
 )
 KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "persistent": 5}
 
@@ -98,6 +99,7 @@ def load() -> ctypes.CDLL:
         "kv_capture_noalloc": (I, [V, V, V, ctypes.c_int64, V]),
         "stage_head_attach": (I, [V, V, P(QuantMatrix), I, V]),
         "stage_head_top1": (I, [V, V, I, V, V, V, V, V]),
+        "stage_prefill": (I, [V, V, I, V, V, V, V, V]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

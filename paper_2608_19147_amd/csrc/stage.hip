@@ -121,6 +121,9 @@ struct Stage {
     DevMat head;
     uint16_t* final_norm = nullptr;
     float4* top1_part = nullptr;                       // [MAX_ROWS][head tiles]
+    // prefill: the residual stream of every prompt row, fp32 [pf_rows][H]
+    float* pf_x = nullptr;
+    size_t pf_rows = 0;
     // persistent-kernel weights (row layout) and barrier state
     bool ps_ok = false;
     int cpl_h = 0, cpl_q = 0, cpl_f = 0, kc_h = 0, kc_q = 0, kc_f = 0, ng_h = 0, ng_q = 0, ng_f = 0;
@@ -155,6 +158,11 @@ struct Stage {
 
     ~Stage() {
         for (hipEvent_t e : prof_ev) (void)hipEventDestroy(e);
+        if (pf_x) {
+            (void)hipSetDevice(device);
+            (void)hipDeviceSynchronize();
+            (void)hipFree(pf_x);
+        }
         if (done_ev) (void)hipEventDestroy(done_ev);
         (void)hipSetDevice(device);
         (void)hipDeviceSynchronize();
@@ -1228,6 +1236,235 @@ int stage_head_top1(Stage* st, const void* hidden, int M, int32_t* token_out, fl
     HIP_TRY(launch_gemm_bp(a, s));
     HIP_TRY(launch_top1_merge(st->top1_part, M, st->head.pm.ntiles, token_out, p_out, logit_out, s));
     HIP_TRY(mark_done(st, s));
+    return STAGE_OK;
+}
+
+int stage_prefill(Stage* st, KVState* kv, int n, const int32_t* positions, const uint8_t* past_mask, const void* hidden_in,
+                  void* hidden_out, void* stream) {
+    if (!st || !kv || !positions || !hidden_in || !hidden_out) return fail(STAGE_E_INVALID, "NULL argument");
+    if (kv->stage != st) return fail(STAGE_E_STATE_MISMATCH, "state belongs to another stage");
+    if (kv->S != 1) return fail(STAGE_E_SHAPE, "prefill takes a one-slot state");
+    if (n < 1 || n > STAGE_MAX_PREFILL) return fail(STAGE_E_CAPACITY, "n_tokens must be in [1, STAGE_MAX_PREFILL]");
+    if (!st->bp_ok) return fail(STAGE_E_UNSUPPORTED, "prefill needs 128-wide quantization groups");
+    const StageConfig& c = st->cfg;
+    const int H = c.hidden, D = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
+    const int P0 = kv->P;
+    if (P0 + n > kv->cap) return fail(STAGE_E_CAPACITY, "P + n_tokens exceeds the state's capacity");
+    for (int i = 0; i < n; ++i)
+        if (positions[i] < 0 || positions[i] >= c.max_positions)
+            return fail(STAGE_E_CAPACITY, "position " + std::to_string(positions[i]) + " outside the rotary table");
+    const int act_dt = dt_code(c.act_dtype), nqkv = Hq * D + 2 * Hkv * D;
+    const size_t row_bytes = (size_t)H * 2;
+    if ((const uint8_t*)hidden_in < (const uint8_t*)hidden_out + (size_t)n * row_bytes &&
+        (const uint8_t*)hidden_out < (const uint8_t*)hidden_in + (size_t)n * row_bytes)
+        return fail(STAGE_E_INVALID, "hidden_in and hidden_out overlap");
+    HIP_TRY(hipSetDevice(st->device));
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(order_on(st, s));
+    if (st->pf_rows < (size_t)n) {                        // the prompt's residual rows
+        HIP_TRY(hipDeviceSynchronize());
+        if (st->pf_x) HIP_TRY(hipFree(st->pf_x));
+        st->pf_x = nullptr;
+        st->pf_rows = 0;
+        if (hipMalloc(&st->pf_x, (size_t)n * H * sizeof(float)) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(STAGE_E_OOM, "prefill workspace allocation failed");
+        }
+        st->pf_rows = (size_t)n;
+    }
+
+    // ---------------- one request record per chunk of at most MAX_ROWS rows, in one upload:
+    // chunk q covers prompt rows [64 q, 64 q + m) and sees the past rows the mask
+    // keeps, the earlier chunks' rows and its own rows causally
+    const int nch = (n + MAX_ROWS - 1) / MAX_ROWS;
+    std::vector<size_t> off_req(nch), off_item(nch), off_pos(nch), off_ritem(nch), off_mask(nch);
+    size_t total = 0;
+    for (int q = 0; q < nch; ++q) {
+        const int r0 = q * MAX_ROWS, m = std::min(MAX_ROWS, n - r0);
+        off_req[q] = total;
+        off_item[q] = align16(off_req[q] + sizeof(ReqDev));
+        off_pos[q] = align16(off_item[q] + sizeof(ItemDev));
+        off_ritem[q] = align16(off_pos[q] + sizeof(int) * m);
+        off_mask[q] = align16(off_ritem[q] + sizeof(int) * m);
+        total = align16(off_mask[q] + (size_t)P0 + r0 + m);
+    }
+    int rc = ensure_meta(st, total);
+    if (rc) return rc;
+    const int slot_i = st->ring_i;
+    st->ring_i = (st->ring_i + 1) % META_RING;
+    if (st->meta_ev_used[slot_i]) HIP_TRY(hipEventSynchronize(st->meta_ev[slot_i]));
+    uint8_t* hb = st->meta_host[slot_i];
+    const int splits = std::max(1, std::min(ATTN_MAX_SPLITS, 2 * st->n_cus / Hkv));
+    for (int q = 0; q < nch; ++q) {
+        const int r0 = q * MAX_ROWS, m = std::min(MAX_ROWS, n - r0);
+        ReqDev d{};
+        d.P = P0 + r0;
+        d.n = m;
+        d.S = 1;
+        d.row0 = 0;
+        d.cap = kv->cap;
+        d.mask_off = 0;
+        d.mask_len = P0 + r0 + m;
+        d.rowmask_off = -1;
+        d.item0 = 0;
+        d.splits = splits;
+        d.kc = kv->kc;
+        d.vc = kv->vc;
+        d.table = kv->table[kv->cur];
+        std::memcpy(hb + off_req[q], &d, sizeof(d));
+        const ItemDev it{0, 0, d};
+        std::memcpy(hb + off_item[q], &it, sizeof(it));
+        std::memcpy(hb + off_pos[q], positions + r0, sizeof(int) * m);
+        std::memset(hb + off_ritem[q], 0, sizeof(int) * m);
+        uint8_t* mk = hb + off_mask[q];
+        for (int j = 0; j < P0; ++j) mk[j] = past_mask ? (past_mask[j] ? 1 : 0) : 1;
+        std::memset(mk + P0, 1, (size_t)r0 + m);
+    }
+    uint8_t* db = st->meta_dev;
+    HIP_TRY(hipMemcpyAsync(db, hb, total, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipEventRecord(st->meta_ev[slot_i], s));
+    st->meta_ev_used[slot_i] = true;
+
+    // ---------------- layer-major: every chunk of a layer before the next layer, so
+    // the later chunks read the layer's weights while they are still cached
+    for (int l = 0; l < c.n_layers; ++l) {
+        const LayerDev& Ld = st->layers[l];
+        const bool first = (l == 0), last = (l == c.n_layers - 1);
+        for (int q = 0; q < nch; ++q) {
+            const int r0 = q * MAX_ROWS, m = std::min(MAX_ROWS, n - r0);
+            float* xq = st->pf_x + (size_t)r0 * H;
+            const uint8_t* hin = (const uint8_t*)hidden_in + (size_t)r0 * row_bytes;
+            auto run_bp = [&](const DevMat& mat, GemvArgs a) -> hipError_t {
+                a.W = mat.pm;
+                a.M = m;
+                a.kp = st->kp;
+                a.partial = st->gpart;
+                a.counters = st->gcnt;
+                a.ksplit = mat.bp_split;
+                a.kg = mat.bp_kg;
+                return launch_gemm_bp(a, s);
+            };
+            // q|k|v = RMSNorm(x) W_qkv^T, the input normalized here for every layer
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_QKV, true, s));
+            HIP_TRY(launch_bprep(first ? (const void*)hin : (const void*)xq, first ? act_dt : DT_F32, H, Ld.attn_norm, act_dt,
+                                 H, c.rms_eps, m, st->bp[0], st->bc[0], st->kp, st->rsb, s));
+            {
+                GemvArgs a{};
+                a.bp_in = st->bp[0];
+                a.bc_in = st->bc[0];
+                a.cb_in = st->cbf[0];
+                a.norm = 2;
+                a.epi = EPI_STORE;
+                a.out = st->qkv;
+                a.out_ld = nqkv;
+                HIP_TRY(run_bp(Ld.qkv, a));
+            }
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_QKV, false, s));
+            // causal attention of the chunk: appends its rows to the cache
+            {
+                AttnArgs a{};
+                a.qkv = st->qkv;
+                a.qkv_ld = nqkv;
+                a.out = st->attn;
+                a.out_ld = Hq * D;
+                a.meta.reqs = (const ReqDev*)(db + off_req[q]);
+                a.meta.items = (const ItemDev*)(db + off_item[q]);
+                a.meta.positions = (const int*)(db + off_pos[q]);
+                a.meta.row_item = (const int*)(db + off_ritem[q]);
+                a.meta.masks = db + off_mask[q];
+                a.meta.n_items = 1;
+                a.meta.M = m;
+                a.meta.n_req = 1;
+                a.rope = st->rope;
+                a.layer = l;
+                a.Hq = Hq;
+                a.Hkv = Hkv;
+                a.kv_dt = dt_code(c.kv_dtype);
+                a.qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
+                a.part = st->apart;
+                a.counters = st->acnt;
+                a.nsplit_max = splits;
+                a.vector_path = st->attn_vector;
+                a.bp_out = st->bp[1];
+                a.bc_out = st->bc[1];
+                a.kp = st->kp;
+                HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, true, s));
+                HIP_TRY(launch_attention(a, D, (Hq / Hkv) * m, s));
+                HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, false, s));
+            }
+            // x = residual + o W_o^T; prepares RMSNorm_ffn's input
+            {
+                GemvArgs a{};
+                a.bp_in = st->bp[1];
+                a.bc_in = st->bc[1];
+                a.cb_in = st->cbf[1];
+                a.norm = 0;
+                a.epi = EPI_RESID;
+                a.out = xq;
+                a.out_ld = H;
+                a.resid = first ? (const void*)hin : (const void*)xq;
+                a.resid_dt = first ? act_dt : DT_F32;
+                a.resid_ld = H;
+                a.ssq_out = st->ssq;
+                a.bp_out = st->bp[0];
+                a.bc_out = st->bc[0];
+                a.cb_out = st->cbf[0];
+                a.gamma_next = Ld.ffn_norm;
+                a.gamma_next_dt = act_dt;
+                a.rs_in = st->rsb;
+                HIP_TRY(prof_mark(st, STAGE_KERNEL_OPROJ, true, s));
+                HIP_TRY(run_bp(Ld.o, a));
+                HIP_TRY(prof_mark(st, STAGE_KERNEL_OPROJ, false, s));
+            }
+            // act = silu(h2 W_g^T) * (h2 W_u^T); prepares the down product's input
+            {
+                GemvArgs a{};
+                a.bp_in = st->bp[0];
+                a.bc_in = st->bc[0];
+                a.cb_in = st->cbf[0];
+                a.norm = 1;
+                a.eps = c.rms_eps;
+                a.ssq_in = st->ssq;
+                a.ssq_tiles = st->ntiles_h;
+                a.rs_out = st->rsb;
+                a.epi = EPI_SWIGLU;
+                a.out = st->act;
+                a.out_ld = F;
+                a.n_valid = F;
+                a.bp_out = st->bp[1];
+                a.bc_out = st->bc[1];
+                a.cb_out = st->cbf[1];
+                HIP_TRY(prof_mark(st, STAGE_KERNEL_GATEUP, true, s));
+                HIP_TRY(run_bp(Ld.gu, a));
+                HIP_TRY(prof_mark(st, STAGE_KERNEL_GATEUP, false, s));
+            }
+            // x = x + act W_d^T; the last layer also writes hidden_out
+            {
+                GemvArgs a{};
+                a.bp_in = st->bp[1];
+                a.bc_in = st->bc[1];
+                a.cb_in = st->cbf[1];
+                a.norm = 0;
+                a.epi = EPI_RESID;
+                a.out = xq;
+                a.out_ld = H;
+                a.resid = xq;
+                a.resid_dt = DT_F32;
+                a.resid_ld = H;
+                a.ssq_out = st->ssq;
+                if (last) {
+                    a.out_act = (uint8_t*)hidden_out + (size_t)r0 * row_bytes;
+                    a.out_act_dt = act_dt;
+                    a.out_act_ld = H;
+                }
+                HIP_TRY(prof_mark(st, STAGE_KERNEL_DOWN, true, s));
+                HIP_TRY(run_bp(Ld.d, a));
+                HIP_TRY(prof_mark(st, STAGE_KERNEL_DOWN, false, s));
+            }
+        }
+    }
+    HIP_TRY(mark_done(st, s));
+    kv->P = P0 + n;
     return STAGE_OK;
 }
 

@@ -193,6 +193,20 @@ class Stage:
                                        ctypes.c_void_p(_stream_ptr(stream))))
         return tok, p, lg, full
 
+    def prefill(self, state: "KVState", positions, hidden_in: torch.Tensor, past_mask=None,
+                hidden_out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        """Prompt rows hidden_in [n, H] (device, act dtype) of a one-slot state;
+        positions [n]; past_mask [P] or None."""
+        if hidden_out is None:
+            hidden_out = torch.empty_like(hidden_in)
+        pos = np.ascontiguousarray(positions, dtype=np.int32).reshape(-1)
+        pm = None if past_mask is None else np.ascontiguousarray(past_mask, dtype=np.uint8).reshape(-1)
+        check(self.lib.stage_prefill(self.handle, state.handle, int(pos.size), ctypes.c_void_p(pos.ctypes.data),
+                                     ctypes.c_void_p(pm.ctypes.data if pm is not None else None),
+                                     ctypes.c_void_p(hidden_in.data_ptr()), ctypes.c_void_p(hidden_out.data_ptr()),
+                                     ctypes.c_void_p(_stream_ptr(stream))))
+        return hidden_out
+
     def new_state(self, n_slots: int, capacity: int) -> "KVState":
         return KVState(self, n_slots, capacity)
 
