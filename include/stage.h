@@ -302,11 +302,12 @@ int stage_forward(Stage* stage, const StageRequest* reqs, int n_req,
  * positions host int32 [n] (rotary positions); past_mask host uint8 [P] or
  * NULL (0 hides that past row from every prompt row).  Prompt row i sees the
  * past rows the mask keeps and prompt rows 0..i.  The result equals
- * stage_forward of the same rows with that mask (up to rounding: the prompt
- * is processed in chunks of STAGE_MAX_ROWS rows, every chunk of a layer
- * before the next layer, each chunk's RMSNorm input normalized in full).
- * Afterwards P += n.  Allocates a workspace of 4 * n * H bytes on first use
- * (kept, grown when a longer prompt comes).
+ * stage_forward of the same rows with that mask, up to rounding: the prompt
+ * goes through the layers in passes of at most 2048 rows (the products take a
+ * whole pass at once, the attention its 64-row chunks in one launch, every
+ * RMSNorm input is normalized in full).  Afterwards P += n.  Allocates a
+ * workspace for min(n, 2048) rows on first use (kept, grown when a longer
+ * prompt comes).
  * Errors: INVALID (NULL, overlap), SHAPE (state with more than one slot),
  * CAPACITY (n outside [1, STAGE_MAX_PREFILL], P + n > capacity, position),
  * STATE_MISMATCH, UNSUPPORTED (group size other than 128), OOM, HIP. */

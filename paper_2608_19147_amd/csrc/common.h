@@ -86,6 +86,21 @@ struct GemvArgs {
     float4* top1_part;                             // TOP1: [M][ntiles] (max, index bits, sum of exp(v - max), 0)
 };
 
+// Prefill product (gemm_pf_kernel): W [N][K] (tiled) times the prepared rows of
+// n tokens, kept as 64-row blocks of the prepared-operand layout (block b at
+// bp + b * bp_blk halves, its corrections at bc + b * bc_blk floats).
+struct PfArgs {
+    PackedMat W;
+    const uint16_t* bp; const float* bc; size_t bp_blk, bc_blk;
+    int n;                                         // tokens
+    int epi;                                       // EPI_STORE, EPI_RESID, EPI_SWIGLU
+    float* out; int out_ld;                        // STORE: out; RESID: new x; SWIGLU: act (fp32)
+    const void* resid; int resid_dt; int resid_ld; // RESID source (may be out itself)
+    void* out_act; int out_act_dt; int out_act_ld; // RESID: optional copy in the act dtype
+    int n_valid;                                   // SWIGLU: F
+    int nwt, ntb;                                  // groups of 4 weight tiles, 64-token blocks
+};
+
 struct AttnArgs {
     const float* qkv; int qkv_ld;
     float* out; int out_ld;
@@ -96,7 +111,8 @@ struct AttnArgs {
     float* part; unsigned* counters;
     int nsplit_max;
     int vector_path;         // 1: attn_kernel (vector units) instead of attn_mma_kernel
-    uint16_t* bp_out; float* bc_out; int kp;   // the attention output also in prepared form (o product input)
+    uint16_t* bp_out; float* bc_out; int kp;   // the attention output also in prepared form (o product input, 64-row blocks)
+    int no_append;           // the rows of this forward are already in the cache (prefill): do not write them
     // test support (null unless armed): the rotated queries [M][Hq][D] and the
     // scores q.k / sqrt(D) of every visible key [M][Hq][dbg_keys]
     float* dbg_q; float* dbg_logits; int dbg_keys;
@@ -237,6 +253,16 @@ hipError_t launch_kv_append(uint16_t* kc, uint16_t* vc, int16_t* table, const ui
 hipError_t launch_kv_read(const uint16_t* kc, const uint16_t* vc, const int16_t* table, int layer, int slot,
                           int start, int count, int S, int Hkv, int cap, int D, uint16_t* k_out, uint16_t* v_out,
                           hipStream_t st);
+hipError_t launch_gemm_pf(const PfArgs& a, hipStream_t st);
+// Cache rows P .. P + n - 1 of one layer of a one-slot state (kl, vl: that layer's
+// [Hkv][cap][D] base) from n q|k|v result rows: k rotated, both rounded; table
+// (layer 0 only, else nullptr) marks the rows as the slot's own.
+hipError_t launch_kv_rope_append(const float* qkv, int ld, const int* pos, const float2* rope, int n, int P, int Hq, int Hkv,
+                                 int D, uint16_t* kl, uint16_t* vl, int cap, int16_t* table, int kv_dt, hipStream_t st);
+// Rows [0, n) of `in` (fp32 or half, row stride in_ld) to 64-row prepared blocks:
+// gamma != nullptr: RMSNorm(row) * gamma (full normalization); nullptr: the row as it is.
+hipError_t launch_bprep_rows(const void* in, int in_dt, int in_ld, const uint16_t* gamma, int gamma_dt, int K, float eps,
+                             int n, uint16_t* bp, float* bc, int kp, hipStream_t st);
 hipError_t launch_dequant(const PackedMat& m, int row_off, int row_map, int n_rows, float* out, hipStream_t st);
 // Rows src[b][i] (< 0: zero padding) of every slot's logical view, read through
 // `table`, to dst [L][S][Hkv][dst_stride][D] rows i < Pn.

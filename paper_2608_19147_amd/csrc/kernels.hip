@@ -866,6 +866,230 @@ hipError_t launch_gemm_bp(const GemvArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ prefill product
+
+// Prepared rows of a prompt: row r of `in` goes to row r mod 64 of block r / 64
+// (blocks of 64 * kp codes and 2 * kp corrections).  With gamma, the row is
+// RMS-normalized first (its squares added in one fixed order by every slice);
+// without, it is taken as it is.  One workgroup per (row, slice of 1024 k).
+__global__ __launch_bounds__(256) void bprep_rows_kernel(const void* in, int in_dt, int in_ld, const uint16_t* gamma,
+                                                         int gamma_dt, int K, float eps, uint16_t* bp, float* bc, int kp) {
+    constexpr int SPT = BPREP_SLICE / 256;
+    __shared__ float red[4];
+    const int r = blockIdx.x, tid = threadIdx.x, k0 = BPREP_SLICE * blockIdx.y;
+    uint16_t* bpb = bp + (size_t)(r >> 6) * 64 * kp;
+    float* bcb = bc + (size_t)(r >> 6) * 2 * kp;
+    float rs = 1.f;
+    if (gamma) {
+        float ss = 0.f;
+        for (int k0b = 0; k0b < K; k0b += 256 * 8) {
+            float v[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int k = k0b + tid + 256 * i;
+                v[i] = load_val(in, in_dt, (size_t)r * in_ld + min(k, K - 1));
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) ss += (k0b + tid + 256 * i < K) ? v[i] * v[i] : 0.f;
+        }
+        ss = wave_sum_all(ss);
+        if ((tid & 63) == 0) red[tid >> 6] = ss;
+        __syncthreads();
+        rs = rsqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)K + eps);
+    }
+#pragma unroll
+    for (int i = 0; i < SPT; ++i) {
+        const int k = k0 + tid + 256 * i;
+        const int kc = min(k, K - 1);
+        const float x = load_val(in, in_dt, (size_t)r * in_ld + kc);
+        const float g = gamma ? half_bits_to_f32(gamma[kc], gamma_dt) : 1.f;
+        if (k0 + 256 * i < K) bp_put(bpb, bcb, kp, r & 63, k, x * rs * g, k < K);   // whole 32-lane groups
+    }
+}
+
+hipError_t launch_bprep_rows(const void* in, int in_dt, int in_ld, const uint16_t* gamma, int gamma_dt, int K, float eps,
+                             int n, uint16_t* bp, float* bc, int kp, hipStream_t st) {
+    if (K < 1 || n < 1 || kp < K || kp % 128) return hipErrorInvalidValue;
+    bprep_rows_kernel<<<dim3(n, (K + BPREP_SLICE - 1) / BPREP_SLICE), 256, 0, st>>>(in, in_dt, in_ld, gamma, gamma_dt, K,
+                                                                                   eps, bp, bc, kp);
+    return hipGetLastError();
+}
+
+// Product of a prompt's prepared rows with one matrix.  A workgroup takes four
+// 64-row weight tiles (one per wave) and one 64-token block, over all of K.
+// Per group of 128 k: the block's 16 operand fragments (16 KB) are copied into
+// LDS by direct loads (each wave four of them) and shared by the four waves;
+// each wave decodes its tile's codes into the A operands of
+// v_mfma_f32_16x16x32_f16 exactly as gemm_bp_kernel does, and adds
+// scale * (products - correction) per row and group.  The next group's
+// fragments and codes are loaded while a group computes (two LDS buffers, two
+// register sets).  Workgroups are numbered so that those sharing a weight tile
+// group run on the same XCD one after the other (its L2 keeps the tiles while
+// the token blocks sweep past).
+template <int DUMMY>
+__global__ __launch_bounds__(256, 1) void gemm_pf_kernel(PfArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t sb[2][16][64][8];
+    const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l16 = lane & 15, lg = lane >> 4;
+    const int total = a.nwt * a.ntb;
+    const int per_xcd = (total + 7) / 8;
+    const int q = (int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3);
+    if (q >= total) return;                                    // whole workgroup: no barrier is reached
+    const int wt = q / a.ntb, tb = q % a.ntb;
+    const PackedMat W = a.W;
+    const int t = 4 * wt + w;
+    const bool has = t < W.ntiles;
+    const int tt = has ? t : W.ntiles - 1;                     // loads stay in bounds; results are dropped
+    const int K = W.k;
+    const int ng = (K + 127) / 128;
+    const uint16_t* bpb = a.bp + (size_t)tb * a.bp_blk;
+    const float* bcb = a.bc + (size_t)tb * a.bc_blk;
+    uint32_t magic = 0x64006400u;
+    asm volatile("" : "+v"(magic));
+
+    // one group's operand fragments into LDS buffer `buf`: fragment 4 w + u by wave w
+    auto stage_b = [&](int g, int buf) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int f = 4 * w + u;
+            __builtin_amdgcn_global_load_lds(bpb + (((size_t)g * 16 + f) * 64 + lane) * 8,
+                                             (__attribute__((address_space(3))) void*)&sb[buf][f][0][0], 16, 0, 0);
+        }
+    };
+    // codes and scales of the wave's tile, and the corrections of the block's
+    // tokens (summed over the group's valid chunks), for group g
+    auto ld_w = [&](int g, u32x4 (&wv)[4], u32x2 (&sv)[4], float (&cs)[4]) {
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+            wv[rt] = __builtin_nontemporal_load((const u32x4*)(W.w + (((size_t)tt * W.nchunk + 4 * g + lg) * 64 + 16 * rt + l16) * 16));
+            sv[rt] = *(const u32x2*)(W.s + ((size_t)tt * W.ngroups + g) * 64 + 16 * rt + 4 * lg);
+        }
+        const int kb = 128 * g;
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+            const float4 c4 = *(const float4*)(bcb + ((size_t)g * 64 + 16 * cb + l16) * 4);
+            cs[cb] = ((kb < K ? c4.x : 0.f) + (kb + 32 < K ? c4.y : 0.f)) + ((kb + 64 < K ? c4.z : 0.f) + (kb + 96 < K ? c4.w : 0.f));
+        }
+    };
+
+    f32x4_t acc[4][4];
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) acc[rt][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+    u32x4 cw[4], nw[4];
+    u32x2 cs2[4], ns2[4];
+    float cc[4], nc[4];
+    stage_b(0, 0);
+    ld_w(0, cw, cs2, cc);
+    for (int g = 0; g < ng; ++g) {
+        const int buf = g & 1;
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");       // this wave's copies and loads of group g are done
+        __syncthreads();                                        // and every wave's; the other buffer is free
+        const bool more = g + 1 < ng;
+        if (more) {                                             // group g + 1 loads while group g computes
+            stage_b(g + 1, buf ^ 1);
+            ld_w(g + 1, nw, ns2, nc);
+        }
+        const int kb = 128 * g;
+        half8_t A[4][4];
+        float scl[4][4];
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t x = cw[rt][i], y = x >> 8;
+                u32x4 av;
+                av[0] = and_or_u32(0x000F000Fu, x, magic);
+                av[1] = and_or_u32(0x00F000F0u, x, magic);
+                av[2] = and_or_u32(0x000F000Fu, y, magic);
+                av[3] = and_or_u32(0x00F000F0u, y, magic);
+                A[rt][i] = __builtin_bit_cast(half8_t, av);
+            }
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+                const uint32_t h = cs2[rt][jj >> 1];
+                scl[rt][jj] = f16_to_f32((uint16_t)((jj & 1) ? (h >> 16) : (h & 0xFFFFu)));
+            }
+        }
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+            u32x4 B[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                B[i] = *(const u32x4*)&sb[buf][4 * cb + i][lane][0];
+                const bool in = kb + 32 * lg + 8 * i < K;          // past the end of a ragged last group: dropped
+#pragma unroll
+                for (int e = 0; e < 4; ++e) B[i][e] = in ? B[i][e] : 0u;
+            }
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt) {
+                f32x4_t c = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(A[rt][i], __builtin_bit_cast(half8_t, B[i]), c, 0, 0, 0);
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) acc[rt][cb][jj] = __builtin_fmaf(scl[rt][jj], c[jj] - cc[cb], acc[rt][cb][jj]);
+            }
+        }
+        if (more) {
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt) {
+                cw[rt] = nw[rt];
+                cs2[rt] = ns2[rt];
+            }
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) cc[cb] = nc[cb];
+        }
+    }
+    if (!has) return;
+
+    // ---- epilogue: lane holds rows 64 t + 16 rt + 4 lg + j of token 64 tb + 16 cb + l16
+    if (a.epi == EPI_SWIGLU) {                                 // rows 0..31 of a tile gate, 32..63 the matching up
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) {
+                const int tok = 64 * tb + 16 * cb + l16;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int f = 32 * t + 16 * rt + 4 * lg + j;
+                    if (tok < a.n && f < a.n_valid) {
+                        const float gt = acc[rt][cb][j], up = acc[rt + 2][cb][j];
+                        a.out[(size_t)tok * a.out_ld + f] = (gt / (1.0f + expf(-gt))) * up;
+                    }
+                }
+            }
+        return;
+    }
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) {
+            const int tok = 64 * tb + 16 * cb + l16;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int row = 64 * t + 16 * rt + 4 * lg + j;
+                if (tok >= a.n || row >= W.n) continue;
+                float v = acc[rt][cb][j];
+                if (a.epi == EPI_RESID) {
+                    v += load_val(a.resid, a.resid_dt, (size_t)tok * a.resid_ld + row);
+                    if (a.out_act) ((uint16_t*)a.out_act)[(size_t)tok * a.out_act_ld + row] = to_half_bits(v, a.out_act_dt);
+                }
+                a.out[(size_t)tok * a.out_ld + row] = v;
+            }
+        }
+}
+
+hipError_t launch_gemm_pf(const PfArgs& a, hipStream_t st) {
+    if (a.n < 1 || a.W.gchunks != 4 || a.nwt != (a.W.ntiles + 3) / 4 || a.ntb != (a.n + 63) / 64) return hipErrorInvalidValue;
+    const int total = a.nwt * a.ntb;
+    const unsigned grid = 8u * (unsigned)((total + 7) / 8);
+    gemm_pf_kernel<0><<<dim3(grid), dim3(256), 0, st>>>(a);
+    return hipGetLastError();
+}
+
 hipError_t launch_bprep(const void* in, int in_dt, int in_ld, const uint16_t* gamma, int gamma_dt, int K, float eps,
                         int M, uint16_t* bp, float* bc, int kp, float* rs_out, hipStream_t st) {
     if (K < 1 || K > 32 * 256) return hipErrorInvalidValue;
@@ -1041,7 +1265,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
             }
             consume(j, kf, vf);
         }
-        if (r0 == 0) {                                          // append: owner of row j writes it
+        if (r0 == 0 && !a.no_append) {                          // append: owner of row j writes it
             for (int j = max(j0, P) + kg; j < j1; j += KGROUPS) {
                 const int i = j - P;
                 const int m = rowbase + i;
@@ -1134,7 +1358,9 @@ __global__ __launch_bounds__(D) void attn_merge_kernel(AttnArgs a) {
     float O = 0.f;
     for (int s2 = 0; s2 < nsplit; ++s2) O += pp[(size_t)s2 * (D + 2) + 2 + d] * wgt[s2];
     a.out[(size_t)m * a.out_ld + (size_t)h * D + d] = O * inv_s;
-    if (a.bp_out) bp_put(a.bp_out, a.bc_out, a.kp, m, h * D + d, O * inv_s, true);   // the o product's input
+    if (a.bp_out)                                            // the o product's input (64-row blocks)
+        bp_put(a.bp_out + (size_t)(m >> 6) * 64 * a.kp, a.bc_out + (size_t)(m >> 6) * 2 * a.kp, a.kp, m & 63, h * D + d,
+               O * inv_s, true);
 }
 
 // ------------------------------------------------------------------ matrix-core attention
@@ -1321,7 +1547,7 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
         stab[tid + 256 * t2] = ptab[t2];
     }
     __syncthreads();
-    fetch(0, true);
+    fetch(0, !a.no_append);
     for (int qg = 0; qg < nqt; qg += 4 * QTW) {
         // ---- this wave's query tiles: rotated, scaled, split into rounded part and residual
         u32x4 qh[QTW][DB], qr[QTW][DB];
@@ -1392,14 +1618,14 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
                 stab[x] = j < P ? tab[j] : (int16_t)b;
             }
             __syncthreads();
-            fetch(0, qg == 0);
+            fetch(0, qg == 0 && !a.no_append);
         }
         const int nsteps = (c1 - c0 + AK - 1) / AK;
         stash(0);
         __syncthreads();
         for (int st = 0; st < nsteps; ++st) {
             const int buf = st & 1;
-            if (st + 1 < nsteps) fetch((st + 1) * AK, qg == 0);   // next step's loads fly during this one
+            if (st + 1 < nsteps) fetch((st + 1) * AK, qg == 0 && !a.no_append);   // next step's loads fly during this one
             // the lane's 8 keys: step key 4 lg + e (e < 4) or 16 + 4 lg + e - 4; visible ones as bits
             const int kbase = c0 + st * AK + 4 * lg;
             uint32_t vbits = 0u;
@@ -1855,6 +2081,42 @@ __global__ __launch_bounds__(256) void top1_merge_kernel(const float4* __restric
 hipError_t launch_top1_merge(const float4* part, int M, int ntiles, int32_t* token, float* p, float* logit, hipStream_t st) {
     if (M < 1 || ntiles < 1) return hipErrorInvalidValue;
     top1_merge_kernel<<<dim3((unsigned)M), dim3(256), 0, st>>>(part, ntiles, token, p, logit);
+    return hipGetLastError();
+}
+
+// The k and v rows of n prompt rows (q|k|v results [n][ld], fp32) of a one-slot
+// state to cache rows P .. P + n - 1 of one layer: k rotated at the row's
+// position (rotate-half pairing), both rounded to the cache dtype.  One thread
+// per (row, kv head, dimension).
+__global__ __launch_bounds__(256) void kv_rope_append_kernel(const float* __restrict__ qkv, int ld, const int* __restrict__ pos,
+                                                             const float2* __restrict__ rope, int n, int P, int Hq, int Hkv,
+                                                             int D, uint16_t* __restrict__ kl, uint16_t* __restrict__ vl,
+                                                             int cap, int16_t* __restrict__ table, int kv_dt) {
+    const size_t idx = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+    if (idx >= (size_t)n * Hkv * D) return;
+    const int d = (int)(idx % D);
+    const int g = (int)((idx / D) % Hkv);
+    const int i = (int)(idx / ((size_t)D * Hkv));
+    const int half = D / 2;
+    const float* krow = qkv + (size_t)i * ld + (size_t)(Hq + g) * D;
+    const float* vrow = qkv + (size_t)i * ld + (size_t)(Hq + Hkv + g) * D;
+    const bool lo_half = d < half;
+    const float xk = krow[d];
+    const float xp = lo_half ? krow[d + half] : krow[d - half];
+    const float2 cs = rope[(size_t)pos[i] * half + (lo_half ? d : d - half)];
+    const float y = lo_half ? (xk * cs.x - xp * cs.y) : (xk * cs.x + xp * cs.y);
+    const size_t off = ((size_t)g * cap + P + i) * D + d;
+    kl[off] = to_half_bits(y, kv_dt);
+    vl[off] = to_half_bits(vrow[d], kv_dt);
+    if (table && g == 0 && d == 0) table[P + i] = 0;
+}
+
+hipError_t launch_kv_rope_append(const float* qkv, int ld, const int* pos, const float2* rope, int n, int P, int Hq, int Hkv,
+                                 int D, uint16_t* kl, uint16_t* vl, int cap, int16_t* table, int kv_dt, hipStream_t st) {
+    const size_t t = (size_t)n * Hkv * D;
+    if (t == 0) return hipSuccess;
+    kv_rope_append_kernel<<<dim3((unsigned)((t + 255) / 256)), dim3(256), 0, st>>>(qkv, ld, pos, rope, n, P, Hq, Hkv, D, kl, vl,
+                                                                                    cap, table, kv_dt);
     return hipGetLastError();
 }
 

@@ -41,6 +41,7 @@ int fail(int code, const std::string& msg) {
     } while (0)
 
 constexpr int META_RING = 4;
+constexpr int PF_ROWS = 2048;            // prompt rows per prefill pass (all layers)
 
 // Looks up the address of `scratch` on the current device `dev` once.
 int scratch_init(int dev) {
@@ -121,8 +122,10 @@ struct Stage {
     DevMat head;
     uint16_t* final_norm = nullptr;
     float4* top1_part = nullptr;                       // [MAX_ROWS][head tiles]
-    // prefill: the residual stream of every prompt row, fp32 [pf_rows][H]
-    float* pf_x = nullptr;
+    // prefill workspace for pf_rows prompt rows: residual fp32 [rows][H], q|k|v fp32
+    // [rows][NQKV], SwiGLU output fp32 [rows][F], prepared inputs (64-row blocks)
+    float *pf_x = nullptr, *pf_qkv = nullptr, *pf_act = nullptr, *pf_bc = nullptr;
+    uint16_t* pf_bp = nullptr;
     size_t pf_rows = 0;
     // persistent-kernel weights (row layout) and barrier state
     bool ps_ok = false;
@@ -161,7 +164,7 @@ struct Stage {
         if (pf_x) {
             (void)hipSetDevice(device);
             (void)hipDeviceSynchronize();
-            (void)hipFree(pf_x);
+            for (void* p : {(void*)pf_x, (void*)pf_qkv, (void*)pf_act, (void*)pf_bc, (void*)pf_bp}) (void)hipFree(p);
         }
         if (done_ev) (void)hipEventDestroy(done_ev);
         (void)hipSetDevice(device);
@@ -1261,120 +1264,142 @@ int stage_prefill(Stage* st, KVState* kv, int n, const int32_t* positions, const
     HIP_TRY(hipSetDevice(st->device));
     hipStream_t s = (hipStream_t)stream;
     HIP_TRY(order_on(st, s));
-    if (st->pf_rows < (size_t)n) {                        // the prompt's residual rows
+    // workspace for one pass of at most PF_ROWS rows
+    const int pass_rows = std::min(n, PF_ROWS);
+    const size_t wrows = (size_t)(pass_rows + 63) / 64 * 64;
+    if (st->pf_rows < wrows) {
         HIP_TRY(hipDeviceSynchronize());
-        if (st->pf_x) HIP_TRY(hipFree(st->pf_x));
-        st->pf_x = nullptr;
+        for (void* p : {(void*)st->pf_x, (void*)st->pf_qkv, (void*)st->pf_act, (void*)st->pf_bc, (void*)st->pf_bp})
+            if (p) HIP_TRY(hipFree(p));
+        st->pf_x = st->pf_qkv = st->pf_act = st->pf_bc = nullptr;
+        st->pf_bp = nullptr;
         st->pf_rows = 0;
-        if (hipMalloc(&st->pf_x, (size_t)n * H * sizeof(float)) != hipSuccess) {
+        if (hipMalloc(&st->pf_x, wrows * H * 4) != hipSuccess || hipMalloc(&st->pf_qkv, wrows * nqkv * 4) != hipSuccess ||
+            hipMalloc(&st->pf_act, wrows * std::max(F, Hq * D) * 4) != hipSuccess ||
+            hipMalloc(&st->pf_bp, wrows * st->kp * 2) != hipSuccess ||
+            hipMalloc(&st->pf_bc, wrows / 64 * 2 * st->kp * 4) != hipSuccess) {
             (void)hipGetLastError();
             return fail(STAGE_E_OOM, "prefill workspace allocation failed");
         }
-        st->pf_rows = (size_t)n;
+        st->pf_rows = wrows;
     }
 
-    // ---------------- one request record per chunk of at most MAX_ROWS rows, in one upload:
-    // chunk q covers prompt rows [64 q, 64 q + m) and sees the past rows the mask
-    // keeps, the earlier chunks' rows and its own rows causally
+    // ---------------- one request record per chunk of at most MAX_ROWS rows (the
+    // attention's unit), in one upload: chunk q covers prompt rows [64 q, 64 q + m),
+    // sees the past rows the mask keeps, the earlier chunks' rows and its own rows
+    // causally.  Row numbers (row0, positions, row_item) count from the start of
+    // the chunk's pass.
     const int nch = (n + MAX_ROWS - 1) / MAX_ROWS;
-    std::vector<size_t> off_req(nch), off_item(nch), off_pos(nch), off_ritem(nch), off_mask(nch);
-    size_t total = 0;
-    for (int q = 0; q < nch; ++q) {
-        const int r0 = q * MAX_ROWS, m = std::min(MAX_ROWS, n - r0);
-        off_req[q] = total;
-        off_item[q] = align16(off_req[q] + sizeof(ReqDev));
-        off_pos[q] = align16(off_item[q] + sizeof(ItemDev));
-        off_ritem[q] = align16(off_pos[q] + sizeof(int) * m);
-        off_mask[q] = align16(off_ritem[q] + sizeof(int) * m);
-        total = align16(off_mask[q] + (size_t)P0 + r0 + m);
-    }
+    const int pass_chunks = PF_ROWS / MAX_ROWS;
+    size_t mask_total = 0;
+    for (int q = 0; q < nch; ++q) mask_total += (size_t)P0 + q * MAX_ROWS + std::min(MAX_ROWS, n - q * MAX_ROWS);
+    const size_t off_req = 0;
+    const size_t off_item = align16(off_req + sizeof(ReqDev) * nch);
+    const size_t off_pos = align16(off_item + sizeof(ItemDev) * nch);
+    const size_t off_ritem = align16(off_pos + sizeof(int) * n);
+    const size_t off_mask = align16(off_ritem + sizeof(int) * n);
+    const size_t total = align16(off_mask + mask_total);
     int rc = ensure_meta(st, total);
     if (rc) return rc;
     const int slot_i = st->ring_i;
     st->ring_i = (st->ring_i + 1) % META_RING;
     if (st->meta_ev_used[slot_i]) HIP_TRY(hipEventSynchronize(st->meta_ev[slot_i]));
     uint8_t* hb = st->meta_host[slot_i];
-    const int splits = std::max(1, std::min(ATTN_MAX_SPLITS, 2 * st->n_cus / Hkv));
-    for (int q = 0; q < nch; ++q) {
-        const int r0 = q * MAX_ROWS, m = std::min(MAX_ROWS, n - r0);
-        ReqDev d{};
-        d.P = P0 + r0;
-        d.n = m;
-        d.S = 1;
-        d.row0 = 0;
-        d.cap = kv->cap;
-        d.mask_off = 0;
-        d.mask_len = P0 + r0 + m;
-        d.rowmask_off = -1;
-        d.item0 = 0;
-        d.splits = splits;
-        d.kc = kv->kc;
-        d.vc = kv->vc;
-        d.table = kv->table[kv->cur];
-        std::memcpy(hb + off_req[q], &d, sizeof(d));
-        const ItemDev it{0, 0, d};
-        std::memcpy(hb + off_item[q], &it, sizeof(it));
-        std::memcpy(hb + off_pos[q], positions + r0, sizeof(int) * m);
-        std::memset(hb + off_ritem[q], 0, sizeof(int) * m);
-        uint8_t* mk = hb + off_mask[q];
-        for (int j = 0; j < P0; ++j) mk[j] = past_mask ? (past_mask[j] ? 1 : 0) : 1;
-        std::memset(mk + P0, 1, (size_t)r0 + m);
+    const int splits = 2;                              // per (chunk, kv head): the chunks fill the device
+    {
+        size_t moff = 0;
+        for (int q = 0; q < nch; ++q) {
+            const int r0 = q * MAX_ROWS, m = std::min(MAX_ROWS, n - r0);
+            const int qf = q / pass_chunks * pass_chunks;   // first chunk of the pass
+            ReqDev d{};
+            d.P = P0 + r0;
+            d.n = m;
+            d.S = 1;
+            d.row0 = (q - qf) * MAX_ROWS;
+            d.cap = kv->cap;
+            d.mask_off = (int)moff;
+            d.mask_len = P0 + r0 + m;
+            d.rowmask_off = -1;
+            d.item0 = q - qf;
+            d.splits = splits;
+            d.kc = kv->kc;
+            d.vc = kv->vc;
+            d.table = kv->table[kv->cur];
+            ((ReqDev*)(hb + off_req))[q] = d;
+            ((ItemDev*)(hb + off_item))[q] = ItemDev{q - qf, 0, d};
+            for (int i = 0; i < m; ++i) ((int*)(hb + off_ritem))[r0 + i] = q - qf;
+            uint8_t* mk = hb + off_mask + moff;
+            for (int jj = 0; jj < P0; ++jj) mk[jj] = past_mask ? (past_mask[jj] ? 1 : 0) : 1;
+            std::memset(mk + P0, 1, (size_t)r0 + m);
+            moff += (size_t)P0 + r0 + m;
+        }
+        std::memcpy(hb + off_pos, positions, sizeof(int) * n);
     }
     uint8_t* db = st->meta_dev;
     HIP_TRY(hipMemcpyAsync(db, hb, total, hipMemcpyHostToDevice, s));
     HIP_TRY(hipEventRecord(st->meta_ev[slot_i], s));
     st->meta_ev_used[slot_i] = true;
+    if ((size_t)PF_ROWS * Hq * splits * (D + 2) > (size_t)MAX_ROWS * Hq * ATTN_MAX_SPLITS * (D + 4))
+        return fail(STAGE_E_UNSUPPORTED, "attention partials of a prefill pass exceed the workspace");
 
-    // ---------------- layer-major: every chunk of a layer before the next layer, so
-    // the later chunks read the layer's weights while they are still cached
-    for (int l = 0; l < c.n_layers; ++l) {
-        const LayerDev& Ld = st->layers[l];
-        const bool first = (l == 0), last = (l == c.n_layers - 1);
-        for (int q = 0; q < nch; ++q) {
-            const int r0 = q * MAX_ROWS, m = std::min(MAX_ROWS, n - r0);
-            float* xq = st->pf_x + (size_t)r0 * H;
-            const uint8_t* hin = (const uint8_t*)hidden_in + (size_t)r0 * row_bytes;
-            auto run_bp = [&](const DevMat& mat, GemvArgs a) -> hipError_t {
-                a.W = mat.pm;
-                a.M = m;
-                a.kp = st->kp;
-                a.partial = st->gpart;
-                a.counters = st->gcnt;
-                a.ksplit = mat.bp_split;
-                a.kg = mat.bp_kg;
-                return launch_gemm_bp(a, s);
-            };
-            // q|k|v = RMSNorm(x) W_qkv^T, the input normalized here for every layer
+    // ---------------- passes of at most PF_ROWS rows, each through every layer: the
+    // products take all of a pass's rows at once (gemm_pf_kernel), the attention
+    // one 64-row chunk at a time (its keys include the earlier chunks' rows)
+    const int kp = st->kp;
+    const size_t bp_blk = (size_t)64 * kp, bc_blk = (size_t)2 * kp;
+    auto pf = [&](const DevMat& mat, int rows, int epi) {
+        PfArgs a{};
+        a.W = mat.pm;
+        a.bp = st->pf_bp;
+        a.bc = st->pf_bc;
+        a.bp_blk = bp_blk;
+        a.bc_blk = bc_blk;
+        a.n = rows;
+        a.epi = epi;
+        a.nwt = (mat.pm.ntiles + 3) / 4;
+        a.ntb = (rows + 63) / 64;
+        return a;
+    };
+    for (int p0 = 0; p0 < n; p0 += PF_ROWS) {
+        const int pr = std::min(PF_ROWS, n - p0);
+        const uint8_t* hin = (const uint8_t*)hidden_in + (size_t)p0 * row_bytes;
+        for (int l = 0; l < c.n_layers; ++l) {
+            const LayerDev& Ld = st->layers[l];
+            const bool first = (l == 0), last = (l == c.n_layers - 1);
+            // q|k|v = RMSNorm(x) W_qkv^T
             HIP_TRY(prof_mark(st, STAGE_KERNEL_QKV, true, s));
-            HIP_TRY(launch_bprep(first ? (const void*)hin : (const void*)xq, first ? act_dt : DT_F32, H, Ld.attn_norm, act_dt,
-                                 H, c.rms_eps, m, st->bp[0], st->bc[0], st->kp, st->rsb, s));
+            HIP_TRY(launch_bprep_rows(first ? (const void*)hin : (const void*)st->pf_x, first ? act_dt : DT_F32, H,
+                                      Ld.attn_norm, act_dt, H, c.rms_eps, pr, st->pf_bp, st->pf_bc, kp, s));
             {
-                GemvArgs a{};
-                a.bp_in = st->bp[0];
-                a.bc_in = st->bc[0];
-                a.cb_in = st->cbf[0];
-                a.norm = 2;
-                a.epi = EPI_STORE;
-                a.out = st->qkv;
+                PfArgs a = pf(Ld.qkv, pr, EPI_STORE);
+                a.out = st->pf_qkv;
                 a.out_ld = nqkv;
-                HIP_TRY(run_bp(Ld.qkv, a));
+                HIP_TRY(launch_gemm_pf(a, s));
             }
             HIP_TRY(prof_mark(st, STAGE_KERNEL_QKV, false, s));
-            // causal attention of the chunk: appends its rows to the cache
+            // the pass's k and v rows into the cache, then the causal attention of all its
+            // 64-row chunks in one launch (each a request whose past includes the
+            // earlier chunks' rows); the output goes to the o product as prepared blocks
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, true, s));
             {
+                const size_t lstride = (size_t)Hkv * kv->cap * D;   // one slot
+                HIP_TRY(launch_kv_rope_append(st->pf_qkv, nqkv, (const int*)(db + off_pos) + p0, st->rope, pr, P0 + p0, Hq, Hkv,
+                                              D, kv->kc + (size_t)l * lstride, kv->vc + (size_t)l * lstride, kv->cap,
+                                              first ? kv->table[kv->cur] : nullptr, dt_code(c.kv_dtype), s));
+                const int q0 = p0 / MAX_ROWS, nq = (pr + MAX_ROWS - 1) / MAX_ROWS;
                 AttnArgs a{};
-                a.qkv = st->qkv;
+                a.qkv = st->pf_qkv;
                 a.qkv_ld = nqkv;
-                a.out = st->attn;
+                a.out = st->pf_act;                                  // scratch: the gate|up product rewrites it
                 a.out_ld = Hq * D;
-                a.meta.reqs = (const ReqDev*)(db + off_req[q]);
-                a.meta.items = (const ItemDev*)(db + off_item[q]);
-                a.meta.positions = (const int*)(db + off_pos[q]);
-                a.meta.row_item = (const int*)(db + off_ritem[q]);
-                a.meta.masks = db + off_mask[q];
-                a.meta.n_items = 1;
-                a.meta.M = m;
-                a.meta.n_req = 1;
+                a.meta.reqs = (const ReqDev*)(db + off_req) + q0;
+                a.meta.items = (const ItemDev*)(db + off_item) + q0;
+                a.meta.positions = (const int*)(db + off_pos) + p0;
+                a.meta.row_item = (const int*)(db + off_ritem) + p0;
+                a.meta.masks = db + off_mask;
+                a.meta.n_items = nq;
+                a.meta.M = pr;
+                a.meta.n_req = nq;
                 a.rope = st->rope;
                 a.layer = l;
                 a.Hq = Hq;
@@ -1385,82 +1410,54 @@ int stage_prefill(Stage* st, KVState* kv, int n, const int32_t* positions, const
                 a.counters = st->acnt;
                 a.nsplit_max = splits;
                 a.vector_path = st->attn_vector;
-                a.bp_out = st->bp[1];
-                a.bc_out = st->bc[1];
-                a.kp = st->kp;
-                HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, true, s));
-                HIP_TRY(launch_attention(a, D, (Hq / Hkv) * m, s));
-                HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, false, s));
+                a.bp_out = st->pf_bp;
+                a.bc_out = st->pf_bc;
+                a.kp = kp;
+                a.no_append = 1;
+                HIP_TRY(launch_attention(a, D, (Hq / Hkv) * MAX_ROWS, s));
             }
-            // x = residual + o W_o^T; prepares RMSNorm_ffn's input
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, false, s));
+            // x = residual + o W_o^T
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_OPROJ, true, s));
             {
-                GemvArgs a{};
-                a.bp_in = st->bp[1];
-                a.bc_in = st->bc[1];
-                a.cb_in = st->cbf[1];
-                a.norm = 0;
-                a.epi = EPI_RESID;
-                a.out = xq;
+                PfArgs a = pf(Ld.o, pr, EPI_RESID);
+                a.out = st->pf_x;
                 a.out_ld = H;
-                a.resid = first ? (const void*)hin : (const void*)xq;
+                a.resid = first ? (const void*)hin : (const void*)st->pf_x;
                 a.resid_dt = first ? act_dt : DT_F32;
                 a.resid_ld = H;
-                a.ssq_out = st->ssq;
-                a.bp_out = st->bp[0];
-                a.bc_out = st->bc[0];
-                a.cb_out = st->cbf[0];
-                a.gamma_next = Ld.ffn_norm;
-                a.gamma_next_dt = act_dt;
-                a.rs_in = st->rsb;
-                HIP_TRY(prof_mark(st, STAGE_KERNEL_OPROJ, true, s));
-                HIP_TRY(run_bp(Ld.o, a));
-                HIP_TRY(prof_mark(st, STAGE_KERNEL_OPROJ, false, s));
+                HIP_TRY(launch_gemm_pf(a, s));
             }
-            // act = silu(h2 W_g^T) * (h2 W_u^T); prepares the down product's input
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_OPROJ, false, s));
+            // act = silu(h2 W_g^T) * (h2 W_u^T), h2 = RMSNorm(x)
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_GATEUP, true, s));
+            HIP_TRY(launch_bprep_rows(st->pf_x, DT_F32, H, Ld.ffn_norm, act_dt, H, c.rms_eps, pr, st->pf_bp, st->pf_bc, kp, s));
             {
-                GemvArgs a{};
-                a.bp_in = st->bp[0];
-                a.bc_in = st->bc[0];
-                a.cb_in = st->cbf[0];
-                a.norm = 1;
-                a.eps = c.rms_eps;
-                a.ssq_in = st->ssq;
-                a.ssq_tiles = st->ntiles_h;
-                a.rs_out = st->rsb;
-                a.epi = EPI_SWIGLU;
-                a.out = st->act;
+                PfArgs a = pf(Ld.gu, pr, EPI_SWIGLU);
+                a.out = st->pf_act;
                 a.out_ld = F;
                 a.n_valid = F;
-                a.bp_out = st->bp[1];
-                a.bc_out = st->bc[1];
-                a.cb_out = st->cbf[1];
-                HIP_TRY(prof_mark(st, STAGE_KERNEL_GATEUP, true, s));
-                HIP_TRY(run_bp(Ld.gu, a));
-                HIP_TRY(prof_mark(st, STAGE_KERNEL_GATEUP, false, s));
+                HIP_TRY(launch_gemm_pf(a, s));
             }
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_GATEUP, false, s));
             // x = x + act W_d^T; the last layer also writes hidden_out
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_DOWN, true, s));
+            HIP_TRY(launch_bprep_rows(st->pf_act, DT_F32, F, nullptr, act_dt, F, c.rms_eps, pr, st->pf_bp, st->pf_bc, kp, s));
             {
-                GemvArgs a{};
-                a.bp_in = st->bp[1];
-                a.bc_in = st->bc[1];
-                a.cb_in = st->cbf[1];
-                a.norm = 0;
-                a.epi = EPI_RESID;
-                a.out = xq;
+                PfArgs a = pf(Ld.d, pr, EPI_RESID);
+                a.out = st->pf_x;
                 a.out_ld = H;
-                a.resid = xq;
+                a.resid = st->pf_x;
                 a.resid_dt = DT_F32;
                 a.resid_ld = H;
-                a.ssq_out = st->ssq;
                 if (last) {
-                    a.out_act = (uint8_t*)hidden_out + (size_t)r0 * row_bytes;
+                    a.out_act = (uint8_t*)hidden_out + (size_t)p0 * row_bytes;
                     a.out_act_dt = act_dt;
                     a.out_act_ld = H;
                 }
-                HIP_TRY(prof_mark(st, STAGE_KERNEL_DOWN, true, s));
-                HIP_TRY(run_bp(Ld.d, a));
-                HIP_TRY(prof_mark(st, STAGE_KERNEL_DOWN, false, s));
+                HIP_TRY(launch_gemm_pf(a, s));
             }
+            HIP_TRY(prof_mark(st, STAGE_KERNEL_DOWN, false, s));
         }
     }
     HIP_TRY(mark_done(st, s));
