@@ -1185,6 +1185,14 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
             gam_f = half_bits_to_f32(Ly.ffn_norm[xr0 + lane], a.act_dt);
             if (!last) gam_a = half_bits_to_f32(a.layers[l + 1].attn_norm[xr0 + lane], a.act_dt);
         }
+        if (l > 0) {
+            // rs of the residual published after the previous layer's down product,
+            // polled while the compute waves run this layer's q|k|v rows.  No
+            // workgroup can rewrite these words before this one publishes q|k|v.
+            const float rs = stage_x_rs(a, a.ll_epoch + PS_LL_PER_LAYER * (l - 1) + 6, ok, l - 1, 5);
+            mq = rs / c;
+            c = rs;
+        }
         wg_barrier();                                         // q|k|v rows are in LDS
         stamp(a, l, 1);
         // ---- RMSNorm scale and rotary embedding of q and k (rows 2d, 2d + 1 of a head are d, d + D/2), as flag words
@@ -1319,14 +1327,17 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         if (lane < nxr) xrow += res[lane];
         publish_x(a, xr0, nxr, xrow, gam_f, c, f_xo);
         stamp(a, l, 6);
+        zero_pad(a.H, a.kc_h * 32, xs);                       // the compute waves stage the published x
+        wg_barrier();                                         // RMSNorm(x) staged
+        load_scales(Ly.d.s, xr0, nxr, a.ng_f, lb + a.l_sb1);   // o finished with this buffer
         {
-            const float rs = stage_x_rs(a, f_xo, ok, l, 3);      // the compute waves stage the published x
-            zero_pad(a.H, a.kc_h * 32, xs);
+            // rs of the published x, needed by the SwiGLU epilogue only: polled while
+            // the compute waves run gate|up.  No workgroup can rewrite these words
+            // before this one publishes its SwiGLU output, which comes later.
+            const float rs = stage_x_rs(a, f_xo, ok, l, 3);
             mg = rs / c;
             c = rs;
         }
-        wg_barrier();                                         // RMSNorm(x) staged
-        load_scales(Ly.d.s, xr0, nxr, a.ng_f, lb + a.l_sb1);   // o finished with this buffer
         wg_barrier();                                         // gate|up rows are in LDS
         stamp(a, l, 7);
         // ---- act = silu(gate) * up, two outputs per flag word
@@ -1373,11 +1384,9 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         }
         if (!last) {
             publish_x(a, xr0, nxr, xrow, gam_a, c, f_xd);
-            const float rs = stage_x_rs(a, f_xd, ok, l, 5);
             zero_pad(a.H, a.kc_h * 32, xs);
-            mq = rs / c;
-            c = rs;
             wg_barrier();                                     // next layer's q|k|v input staged
+            // its rs is polled at the start of the next layer (needed by the q|k|v epilogue)
         }
     }
 }
