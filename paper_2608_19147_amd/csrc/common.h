@@ -171,6 +171,9 @@ struct PsArgs {
     unsigned* err;                       // set when an exchange wait gives up
     unsigned spin_limit;                 // polling passes after which an exchange wait gives up
     unsigned long long* trace;           // optional [nwg][n_layers][PS_TRACE_PER_LAYER] real-time stamps
+    // test support (null unless armed): layer dbg_layer's rotated query [Hq][D]
+    // and the score q.k / sqrt(D) of every key the row sees, [Hq][dbg_keys]
+    float* dbg_q; float* dbg_logits; int dbg_keys, dbg_layer;
     // LDS byte offsets
     int l_xs, l_sb0, l_sb1, l_res, l_q, l_nkv, l_part, l_rope, l_dbg, l_end;
 };

@@ -627,8 +627,12 @@ __device__ __forceinline__ void kv_to_f32(const u32x4& w, float (&f)[8]) {
 // weights of its rows and one rescale of the running sums, instead of one
 // dependent update per row.  Each 16-lane row group keeps its own running
 // (max, sum, output); the groups are combined at the end.
-template <int GS, int D, int S, bool BF16, class Issue>
-__device__ __forceinline__ void att_seg_t(Issue& issue, Ring& rg, int T, uint32_t mbits, uint32_t qlds, uint32_t part) {
+// rec (test support, null unless the layer's record is armed): the scores of
+// the visible rows go to rec[h * keys + j], key j = j0 + t * RPS + lane / LPR of
+// slot pair t, in natural-log units (q.k / sqrt(D)).
+template <int GS, int D, int S, bool BF16, bool REC, class Issue>
+__device__ __forceinline__ void att_seg_t(Issue& issue, Ring& rg, int T, uint32_t mbits, uint32_t qlds, uint32_t part,
+                                          float* rec, int keys, int j0) {
     constexpr int LPR = AttGeo<D>::LPR;
     const int lane = threadIdx.x & 63;
     const int li = lane % LPR;
@@ -677,6 +681,10 @@ __device__ __forceinline__ void att_seg_t(Issue& issue, Ring& rg, int T, uint32_
                     for (int e = 0; e < 8; ++e) sd = __builtin_fmaf(qf[h][e], kf[e], sd);
                     sd = group_sum<LPR>(sd);
                     sc[t][h] = vis ? sd : -INFINITY;
+                    if constexpr (REC) {
+                        const int j = j0 + (t0 + t) * AttGeo<D>::RPS + lane / LPR;
+                        if (rec && vis && li == 0 && j < keys) rec[h * keys + j] = sd * 0.69314718055994531f;
+                    }
                 }
             }
             float vf[4][8];
@@ -744,7 +752,7 @@ __device__ __forceinline__ void att_seg_t(Issue& issue, Ring& rg, int T, uint32_
     }
 }
 
-template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S, bool KVB>
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S, bool KVB, bool REC>
 __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
     constexpr int LPR = AttGeo<D>::LPR, RPS = AttGeo<D>::RPS;
     const int lane = threadIdx.x & 63;
@@ -873,7 +881,10 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         wg_barrier();                                       // q|k|v rows are in LDS
         wg_barrier();                                       // q and the new row are staged
         cstamp(a, lb + a.l_dbg, 0);
-        att_seg_t<GS, D, S, KVB>(issue, rg, T, mbits, lb + a.l_q, lb + a.l_part);
+        float* rec = nullptr;
+        if constexpr (REC)
+            if (l == a.dbg_layer && has_att) rec = a.dbg_logits + (size_t)g * GS * a.dbg_keys;
+        att_seg_t<GS, D, S, KVB, REC>(issue, rg, T, mbits, lb + a.l_q, lb + a.l_part, rec, a.dbg_keys, j0);
         cstamp(a, lb + a.l_dbg, 1);
         wg_barrier();                                       // wave partials are in LDS
         wg_barrier();                                       // this workgroup's merge is done: polling starts now
@@ -1123,7 +1134,7 @@ __device__ __forceinline__ void merge_slices(const PsArgs& a, int g, int split, 
     }
 }
 
-template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S>
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S, bool REC>
 __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     const int lane = threadIdx.x & 63;
     const int w = blockIdx.x;
@@ -1286,7 +1297,13 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
                     sd = __shfl(sd, (lane & 32) + 31);
                 }
                 s_new = sd;
+                if constexpr (REC)
+                    if (l == a.dbg_layer && (lane % LPH) == 0 && P < a.dbg_keys)
+                        a.dbg_logits[(size_t)(g * GS + hq) * a.dbg_keys + P] = sd * 0.69314718055994531f;
             }
+            if constexpr (REC)
+                if (l == a.dbg_layer && split == 0)                   // this kv head's rotated queries
+                    for (int idx = lane; idx < GS * D; idx += 64) a.dbg_q[(size_t)g * GS * D + idx] = qs[idx] / a.qscale;
             float mx = s_new;
 #pragma unroll
             for (int c = 0; c < SK_CW; ++c) mx = fmaxf(mx, part[(c * GS + hq) * (D + 4)]);
@@ -1391,13 +1408,15 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     }
 }
 
-template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S, bool KVB>
+// REC: the variant that also writes the armed attention record (a.dbg_q,
+// a.dbg_logits); the plain variant carries none of that code.
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S, bool KVB, bool REC>
 __global__ __launch_bounds__(SK_THREADS) void stage_stream_kernel(PsArgs a) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     if ((threadIdx.x >> 6) < SK_CW)
-        compute_main<CPL_H, CPL_Q, CPL_F, D, GS, S, KVB>(a, lds_addr(smem));
+        compute_main<CPL_H, CPL_Q, CPL_F, D, GS, S, KVB, REC>(a, lds_addr(smem));
     else
-        control_main<CPL_H, CPL_Q, CPL_F, D, GS, S>(a, smem);
+        control_main<CPL_H, CPL_Q, CPL_F, D, GS, S, REC>(a, smem);
 }
 
 // ------------------------------------------------------------------ host side
@@ -1409,7 +1428,8 @@ __global__ __launch_bounds__(SK_THREADS) void stage_stream_kernel(PsArgs a) {
     X(1, 1, 1, 64, 2, 14, 0)    /* small test stages, fp16 cache */
 
 #define PS_KEY(H_, Q_, F_, D_, G_, K_) (cpl_h == H_ && cpl_q == Q_ && cpl_f == F_ && D == D_ && gs == G_ && kvb == K_)
-#define PS_KERNEL(H_, Q_, F_, D_, G_, S_, K_) stage_stream_kernel<H_, Q_, F_, D_, G_, S_, (K_ != 0)>
+#define PS_KERNEL(H_, Q_, F_, D_, G_, S_, K_) stage_stream_kernel<H_, Q_, F_, D_, G_, S_, (K_ != 0), false>
+#define PS_KERNEL_REC(H_, Q_, F_, D_, G_, S_, K_) stage_stream_kernel<H_, Q_, F_, D_, G_, S_, (K_ != 0), true>
 
 bool ps_supported(int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb) {
 #define PS_MATCH(H_, Q_, F_, D_, G_, S_, K_) \
@@ -1476,14 +1496,17 @@ static hipError_t launch_ps(const void* fn, const PsArgs& a, int nwg, size_t lds
 
 hipError_t launch_persistent(const PsArgs& a, int cpl_h, int cpl_q, int cpl_f, int D, int gs, int kvb, int nwg, size_t lds,
                              bool coop, hipStream_t st) {
-#define PS_MATCH(H_, Q_, F_, D_, G_, S_, K_) \
-    if (PS_KEY(H_, Q_, F_, D_, G_, K_)) return launch_ps((const void*)PS_KERNEL(H_, Q_, F_, D_, G_, S_, K_), a, nwg, lds, coop, st);
+#define PS_MATCH(H_, Q_, F_, D_, G_, S_, K_)                                                                      \
+    if (PS_KEY(H_, Q_, F_, D_, G_, K_))                                                                          \
+        return launch_ps(a.dbg_logits ? (const void*)PS_KERNEL_REC(H_, Q_, F_, D_, G_, S_, K_)                   \
+                                      : (const void*)PS_KERNEL(H_, Q_, F_, D_, G_, S_, K_), a, nwg, lds, coop, st);
     PS_SHAPES(PS_MATCH)
 #undef PS_MATCH
     return hipErrorInvalidValue;
 }
 #undef PS_KEY
 #undef PS_KERNEL
+#undef PS_KERNEL_REC
 
 // Destination row of source row r: row_off + r (map 0), 2r (map 1, gate),
 // 2r + 1 (map 2, up), or row_off + the rotary-pair order inside each head of

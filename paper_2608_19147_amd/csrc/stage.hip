@@ -1705,8 +1705,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     // ---------------- one launch for the whole stage: a single decode row
     const int RPS = 512 / D;                               // cache rows per 1 KB slot
     int nsplit = 0, split_len = 0, att_T = 0;
-    bool single = st->ps_ok && M == 1 && (st->prof_class < 0 || st->prof_class == STAGE_KERNEL_PERSISTENT) &&
-                  st->dbg_layer < 0;                        // an armed attention record takes the per-layer kernels
+    bool single = st->ps_ok && M == 1 && (st->prof_class < 0 || st->prof_class == STAGE_KERNEL_PERSISTENT);
     if (single) {
         const int P = reqs[0].state->P;
         // splits per kv head: a power of two; each split's merge slice is a multiple of 8 outputs
@@ -1751,6 +1750,15 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
         a.err = st->err;
         a.spin_limit = st->spin_limit;
         a.trace = st->trace;
+        a.dbg_layer = -1;
+        if (st->dbg_layer >= 0) {                         // test support: record one layer's queries and scores
+            HIP_TRY(launch_fill_u32((uint32_t*)st->dbg_logits, (size_t)Hq * st->dbg_keys, 0xFFFFFFFFu, s));   // NaN
+            a.dbg_q = st->dbg_q;
+            a.dbg_logits = st->dbg_logits;
+            a.dbg_keys = st->dbg_keys;
+            a.dbg_layer = st->dbg_layer;
+            st->dbg_rows = 1;
+        }
         const int kvb = c.kv_dtype == STAGE_DTYPE_BF16;
         const int lds = ps_layout(a, ps_slots(st->cpl_h, st->cpl_q, st->cpl_f, D, gs, kvb), D, gs);
         HIP_TRY(prof_mark(st, STAGE_KERNEL_PERSISTENT, true, s));

@@ -1,6 +1,6 @@
 """Attention logits within 1e-3 relative, fp32-accumulated.
 
-The matrix-core attention records, for one armed layer, the rotated query of
+The matrix-core attention and the single-launch stream kernel record, for one armed layer, the rotated query of
 every activation row and query head and the score q.k / sqrt(D) of every key
 that row sees (stage_debug_attn_arm / _read).  Each recorded row is compared
 with the score recomputed in fp64 from the GPU's own recorded query and the
@@ -36,13 +36,13 @@ def _per_layer_pair(shape, seed):
             os.environ["STAGE_PERSISTENT"] = old
 
 
-def _check_logits(shape, q, logits, rows):
+def _check_logits(shape, q, logits, rows, layer=0):
     """rows: list of (m, state, slot, P, i, mask_row) for every activation row."""
     D, gs = shape.head_dim, shape.n_q_heads // shape.n_kv_heads
     worst = 0.0
     for m, g, b, P, i, mrow in rows:
         L = P + 1 + i                                     # keys 0 .. P + i (physical causality)
-        k, _ = g.read(0, b, 0, L)
+        k, _ = g.read(layer, b, 0, L)
         K = k.double().cpu().numpy()                      # [Hkv, L, D] as the slot sees them
         vis = np.nonzero(mrow[:L] != 0)[0]
         for h in range(shape.n_q_heads):
@@ -159,3 +159,39 @@ def test_8b_layer_logits_64_tokens_kv2048():
     rows = [(i, g, 0, P, i, mask[0]) for i in range(n)]
     _check_logits(shape, q, logits, rows)
     assert rel_err(q, _oracle_q(p, p.layers[0], x, pos.reshape(-1))) <= TOL_STAGE
+
+
+def test_8b_stream_kernel_logits_decode_kv2048():
+    """The single-launch stream kernel (the benchmark's kernel): a two-layer
+    8B stage decoding one row from KV 2048 with 10% holes.  Layer 1's record
+    (its query depends on layer 0's output) and layer 0's (query also against
+    the oracle) within the bar; an armed forward's output is bitwise the
+    unarmed one's; the launch is the single launch."""
+    shape = synth.with_layers(synth.LLAMA8B_HALF, 2)
+    p = Pair(shape, 75)
+    P = 2048
+    holes = synth.hole_mask(P, 0.1, 75, 0)
+    holes[-1] = 1
+    mask = np.concatenate([holes, np.ones(1, np.uint8)])[None]
+    pos = np.array([[int(holes.sum())]])
+    x = synth.make_hidden(shape, 1, 75)
+    outs = []
+    for layer in (1, 0, -1):
+        g, _ = p.states(1, P, P + 4, seed=75, with_oracle=False)
+        p.gpu.profile("persistent")
+        if layer >= 0:
+            p.gpu.debug_attn_arm(layer, P + 1)
+        outs.append(run_gpu(p, [req(g, pos, mask)], x))
+        launches, _ = p.gpu.profile_read()
+        p.gpu.profile(None)
+        assert launches == 1                                  # one single-launch forward
+        if layer >= 0:
+            q, logits = p.gpu.debug_attn_read()
+            p.gpu.debug_attn_arm(-1, 1)
+            assert q.shape == (1, shape.n_q_heads, shape.head_dim)
+            _check_logits(shape, q, logits, [(0, g, 0, P, 0, mask[0])], layer=layer)
+            if layer == 0:
+                assert rel_err(q, _oracle_q(p, p.layers[0], x, pos.reshape(-1))) <= TOL_STAGE
+        g.free()
+    assert np.array_equal(outs[0], outs[2]) and np.array_equal(outs[1], outs[2])
+    p.close()
