@@ -315,46 +315,51 @@ struct Ring {
 // INT4 decode: a dword of codes holds k..k+7; masking with 0x000F000F /
 // 0x00F000F0 (of x and x >> 8) and or-ing 0x6400 gives fp16 pairs equal to
 // 1024 + u (pairs (k, k+1), (k+4, k+5)) or 1024 + 16u (pairs (k+2, k+3),
-// (k+6, k+7)) with u = q + 8.  Their dot products with the input are
-// corrected once per chunk: sum q x = lo + hi / 16 - (1032 S_lo + 72 S_hi),
-// where S_lo, S_hi are the chunk's input sums over the two kinds of position.
+// (k+6, k+7)) with u = q + 8.  The input slice is prepared once per segment:
+// the values that meet a 1024 + 16u code are divided by 16 (exact: a power of
+// two), so every product of a chunk adds into one sum, which starts from the
+// chunk's correction -(1032 S_lo + 72 S_hi) (S_lo, S_hi: the chunk's input
+// sums over the two kinds of position); then sum q x is the sum itself.
+//
+// Rows are consumed whole, four at a time (one wave-wide reduction per four
+// rows), from two register sets used alternately: while row r computes from
+// one set, the codes and scales of row r + 1 are read into the other.
 template <int CPL, int S, class Issue>
 __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg, int nrows, int rlocal, int ng,
                                          uint32_t sb, uint32_t xs, uint32_t res) {
     static_assert(S >= 2 * CPL, "the ring must hold two rows");
+    static_assert(CPL <= 4, "the input slice is kept in registers");
     if (nrows == 0) return;
-    // the input slice stays in registers for short rows; longer rows read it from LDS with each row
-    constexpr bool XR = CPL <= 4;
     const int lane = threadIdx.x & 63;
     const half2_t one2 = {(_Float16)1.0f, (_Float16)1.0f};
-    // chunk lane + 64 i of the input as 16 fp16 pairs, and its correction term
-    auto x_corr = [&](const u32x4 (&xc)[4]) {
+    const half2_t sixteenth2 = {(_Float16)0.0625f, (_Float16)0.0625f};
+    // chunk lane + 64 i of the input as 16 fp16 pairs (prepared), and its correction
+    const uint32_t xl = xs + 64 * lane;                      // chunk `lane`; chunk lane + 64 i is 4 KB i further
+    u32x4 xq[CPL][4];
+    float ncorr[CPL];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) xq[i][q4] = lds_rd16(xl + 4096 * i + 16 * q4);
+    lgkm_wait_all();
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
         float slo = 0.f, shi = 0.f;
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
-            const uint32_t e0 = xc[q4][0], e1 = xc[q4][1], e2 = xc[q4][2], e3 = xc[q4][3];
+            touch(xq[i][q4]);
+            // elements are taken into scalars before any bit cast
+            const uint32_t e0 = xq[i][q4][0], e1 = xq[i][q4][1], e2 = xq[i][q4][2], e3 = xq[i][q4][3];
             slo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e0), one2, slo, false);
             slo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e2), one2, slo, false);
             shi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e1), one2, shi, false);
             shi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e3), one2, shi, false);
+            const half2_t h1 = __builtin_bit_cast(half2_t, e1) * sixteenth2;
+            const half2_t h3 = __builtin_bit_cast(half2_t, e3) * sixteenth2;
+            xq[i][q4] = u32x4{e0, __builtin_bit_cast(uint32_t, h1), e2, __builtin_bit_cast(uint32_t, h3)};
         }
-        return 1032.0f * slo + 72.0f * shi;
-    };
-    const uint32_t xl = xs + 64 * lane;                      // chunk `lane`; chunk lane + 64 i is 4 KB i further
-    u32x4 xq[XR ? CPL : 1][4];
-    float corr[XR ? CPL : 1];
-    if constexpr (XR) {
-#pragma unroll
-        for (int i = 0; i < CPL; ++i)
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) xq[i][q4] = lds_rd16(xl + 4096 * i + 16 * q4);
-        lgkm_wait_all();
-#pragma unroll
-        for (int i = 0; i < CPL; ++i) {
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) touch(xq[i][q4]);
-            corr[i] = x_corr(xq[i]);
-        }
+        ncorr[i] = -(1032.0f * slo + 72.0f * shi);
+        asm volatile("" : "+v"(ncorr[i]));                  // computed here, not inside the row loop
     }
     const int gstep = 128 / a.gchunks;                      // scale bytes between chunk i and i + 1 of a row
     const uint32_t sl = sb + 2 * (uint32_t)(lane / a.gchunks) + 2 * rlocal * ng;
@@ -362,10 +367,8 @@ __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg
     uint32_t magic = 0x64006400u;
     asm volatile("" : "+v"(magic));                         // kept in a VGPR for v_bfi
 
-    // rows are consumed whole: codes and scales of row r are read (one wait) while
-    // row r - 1 computes; the row's slots are refilled as soon as they are in registers
-    u32x4 cw[CPL];
-    uint32_t cs[CPL];
+    u32x4 w0[CPL], w1[CPL];
+    uint32_t c0[CPL], c1[CPL];
     auto read_row = [&](int r, u32x4 (&w)[CPL], uint32_t (&sc)[CPL]) {
         int ri = rg.ri;
 #pragma unroll
@@ -375,50 +378,27 @@ __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg
             ri = Ring::next(ri, S);
         }
     };
-    if (rg.p <= rg.pmax) vm_wait<S - CPL>(); else vm_wait_all();   // S + p <= total: S - CPL younger loads
-    read_row(0, cw, cs);
-    lgkm_wait_all();
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-        touch(cw[i]);
-        touch(cs[i]);
-    }
-    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;          // per-lane partials of rows 4 (r / 4) + 0..3
-    for (int r = 0; r < nrows; ++r) {
-        // refill this row's slots, then start reading the next row
+    // Row r from (cw, cs): its slots are refilled (they are in registers), the
+    // next row is read into (nw, ns) (after the last row the reads fall on a
+    // ring slot and a scale of this segment, valid LDS addresses, and are not
+    // used), and the row's per-lane partial is returned once those reads are done.
+    auto row = [&](int r, const u32x4 (&cw)[CPL], const uint32_t (&cs)[CPL], u32x4 (&nw)[CPL],
+                   uint32_t (&ns)[CPL]) -> float {
 #pragma unroll
         for (int i = 0; i < CPL; ++i) {
             issue(rg.addr(rg.ri));
             rg.ri = Ring::next(rg.ri, S);
         }
         rg.p += CPL;
-        const bool more = r + 1 < nrows;
-        u32x4 nw[CPL];
-        uint32_t ns[CPL];
-        if (more) {
+        if (r + 1 < nrows) {
             // younger than the next row's last slot: S - CPL while the stream is not near its end
             if (rg.p <= rg.pmax) vm_wait<S - CPL>(); else vm_wait_all();
-            read_row(r + 1, nw, ns);
         }
+        read_row(min(r + 1, nrows - 1), nw, ns);
         float acc = 0.f;
-        constexpr int UNR = XR ? CPL : 1;
-#pragma unroll UNR
+#pragma unroll
         for (int i = 0; i < CPL; ++i) {
-            u32x4 xc[4];
-            float ci;
-            if constexpr (XR) {
-#pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) xc[q4] = xq[i][q4];
-                ci = corr[i];
-            } else {
-#pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) xc[q4] = lds_rd16(xl + 4096 * i + 16 * q4);
-                asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(acc)::"memory");
-#pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) touch(xc[q4]);
-                ci = x_corr(xc);
-            }
-            float lo0 = 0.f, lo1 = 0.f, hi0 = 0.f, hi1 = 0.f;
+            float t0 = ncorr[i], t1 = 0.f;
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
                 const uint32_t x = cw[i][q4];
@@ -427,37 +407,48 @@ __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg
                 const uint32_t p1 = bfi(0x00F000F0u, x, magic);
                 const uint32_t p2 = bfi(0x000F000Fu, y, magic);
                 const uint32_t p3 = bfi(0x00F000F0u, y, magic);
-                const uint32_t x0 = xc[q4][0], x1 = xc[q4][1], x2 = xc[q4][2], x3 = xc[q4][3];
-                float& lo = (q4 & 1) ? lo1 : lo0;
-                float& hi = (q4 & 1) ? hi1 : hi0;
-                lo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p0), __builtin_bit_cast(half2_t, x0), lo, false);
-                lo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p2), __builtin_bit_cast(half2_t, x2), lo, false);
-                hi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p1), __builtin_bit_cast(half2_t, x1), hi, false);
-                hi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p3), __builtin_bit_cast(half2_t, x3), hi, false);
+                const uint32_t x0 = xq[i][q4][0], x1 = xq[i][q4][1], x2 = xq[i][q4][2], x3 = xq[i][q4][3];
+                t0 = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p0), __builtin_bit_cast(half2_t, x0), t0, false);
+                t1 = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p1), __builtin_bit_cast(half2_t, x1), t1, false);
+                t0 = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p2), __builtin_bit_cast(half2_t, x2), t0, false);
+                t1 = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p3), __builtin_bit_cast(half2_t, x3), t1, false);
             }
-            const float dq = __builtin_fmaf(hi0 + hi1, 0.0625f, (lo0 + lo1) - ci);
-            acc = __builtin_fmaf(f16_to_f32((uint16_t)cs[i]), dq, acc);
+            acc = __builtin_fmaf(f16_to_f32((uint16_t)cs[i]), t0 + t1, acc);
         }
-        if (more) {
-            // the wait takes acc as an operand, so this row's arithmetic is issued before it
-            asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(acc)::"memory");
+        // the wait takes acc as an operand, so this row's arithmetic is issued before it
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(acc)::"memory");
 #pragma unroll
-            for (int i = 0; i < CPL; ++i) {
-                touch(nw[i]);
-                touch(ns[i]);
-                cw[i] = nw[i];
-                cs[i] = ns[i];
-            }
+        for (int i = 0; i < CPL; ++i) {
+            touch(nw[i]);
+            touch(ns[i]);
         }
-        const int q = r & 3;
-        a0 = q == 0 ? acc : a0;
-        a1 = q == 1 ? acc : a1;
-        a2 = q == 2 ? acc : a2;
-        a3 = q == 3 ? acc : a3;
-        if (q == 3 || !more) {                              // rows r - q .. r are complete (later ones hold stale sums)
-            const float rs = sum4_rows(a0, a1, a2, a3, lane);
-            if (lane <= q) lds_wr4(res + 4 * (rlocal + r - q + lane), rs);
-        }
+        return acc;
+    };
+    if (rg.p <= rg.pmax) vm_wait<S - CPL>(); else vm_wait_all();   // S + p <= total: S - CPL younger loads
+    read_row(0, w0, c0);
+    lgkm_wait_all();
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        touch(w0[i]);
+        touch(c0[i]);
+    }
+    int r = 0;
+    for (; r + 4 <= nrows; r += 4) {
+        const float a0 = row(r, w0, c0, w1, c1);
+        const float a1 = row(r + 1, w1, c1, w0, c0);
+        const float a2 = row(r + 2, w0, c0, w1, c1);
+        const float a3 = row(r + 3, w1, c1, w0, c0);
+        const float rs = sum4_rows(a0, a1, a2, a3, lane);
+        if (lane < 4) lds_wr4(res + 4 * (rlocal + r + lane), rs);
+    }
+    if (r < nrows) {                                        // one to three rows left
+        const int nt = nrows - r;
+        const float a0 = row(r, w0, c0, w1, c1);
+        float a1 = 0.f, a2 = 0.f;
+        if (nt > 1) a1 = row(r + 1, w1, c1, w0, c0);
+        if (nt > 2) a2 = row(r + 2, w0, c0, w1, c1);
+        const float rs = sum4_rows(a0, a1, a2, 0.f, lane);
+        if (lane < nt) lds_wr4(res + 4 * (rlocal + r + lane), rs);
     }
 }
 
