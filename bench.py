@@ -176,6 +176,20 @@ def _gateup_roofline(shape, prof):
             "bytes_per_launch": b, "avg_launch_us": round(per * 1e3, 3), "launches_timed": launches}
 
 
+def _profiled(stage, run):
+    """(launches, ms) of the gate|up product over one more pass of `run`, timed
+    with HIP events on the launch stream around each launch."""
+    import torch
+
+    torch.cuda.synchronize()
+    stage.profile("gateup")
+    run()
+    torch.cuda.synchronize()
+    prof = stage.profile_read()
+    stage.profile(None)
+    return prof
+
+
 def other_workload(args) -> int:
     """The measured configurations besides the headline decode (see --workload)."""
     import numpy as np
@@ -251,14 +265,14 @@ def other_workload(args) -> int:
 
         if args.warmup:
             episode(min(args.warmup, K), 10_000, False)
-        stage.profile("gateup")
         tot_s, tot_em, tot_b, done = 0.0, 0, 0, 0
         while done < steps:
             m = min(K, steps - done)
             el, em, nb = episode(m, done, True)
             tot_s, tot_em, tot_b, done = tot_s + el, tot_em + em, tot_b + nb, done + m
-        prof = stage.profile_read()
-        stage.profile(None)
+        # the gate|up launches are timed in a pass of their own: the events around
+        # each launch would otherwise add their own gaps to the timed steps
+        prof = _profiled(stage, lambda: episode(min(K, steps), 0, False))
         ms = tot_s * 1e3 / steps
         cfg = {"workload": (f"llama3.1-8b half stage speculative verify, {S} slots x {n} tokens, kv {P0} growing "
                             f"by up to {n} per step, drafts Bernoulli(0.6) truncated, beam identity/permutation "
@@ -287,15 +301,19 @@ def other_workload(args) -> int:
                 stage.prefill(state, pos, x, hidden_out=out)
                 state.truncate(P0)
             torch.cuda.synchronize()
-            stage.profile("gateup")
             t = time.perf_counter()
             for i in range(steps):
                 stage.prefill(state, pos, x, hidden_out=out)
                 state.truncate(P0)
             torch.cuda.synchronize()
             ms = (time.perf_counter() - t) * 1e3 / steps
-            launches, gu_ms = stage.profile_read()
-            stage.profile(None)
+
+            def again():
+                for i in range(steps):
+                    stage.prefill(state, pos, x, hidden_out=out)
+                    state.truncate(P0)
+
+            launches, gu_ms = _profiled(stage, again)
             # gate|up: one input preparation + one product per layer and pass of at most 2048 rows
             per = gu_ms / max(1, launches)
             pass_rows = [min(2048, n - r0) for r0 in range(0, n, 2048)]
@@ -340,15 +358,17 @@ def other_workload(args) -> int:
                 stage.forward([req], xs[i % 4], out)
                 state.truncate(P)
             torch.cuda.synchronize()
-            stage.profile("gateup")
+
+            def loop():
+                for i in range(args.steps):
+                    stage.forward([req], xs[i % 4], out)
+                    state.truncate(P)
+
             t = time.perf_counter()
-            for i in range(args.steps):
-                stage.forward([req], xs[i % 4], out)
-                state.truncate(P)
+            loop()
             torch.cuda.synchronize()
             ms = (time.perf_counter() - t) * 1e3 / args.steps
-            prof = stage.profile_read()
-            stage.profile(None)
+            prof = _profiled(stage, loop)
             desc = (f"{n}-node binary draft tree (depth 3), per-query-row mask" if name == "tree"
                     else "5-token linear verify of one path")
             cfg = {"workload": f"llama3.1-8b half stage spec verify, 1 slot, kv {P}, {desc}", **base_cfg,
@@ -371,15 +391,17 @@ def other_workload(args) -> int:
             stage.forward([req], xs[i % 8], out)
             state.truncate(P)
         torch.cuda.synchronize()
-        stage.profile("gateup")
+
+        def loop():
+            for i in range(steps):
+                stage.forward([req], xs[i % 8], out)
+                state.truncate(P)
+
         t = time.perf_counter()
-        for i in range(steps):
-            stage.forward([req], xs[i % 8], out)
-            state.truncate(P)
+        loop()
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t) * 1e3 / steps
-        prof = stage.profile_read()
-        stage.profile(None)
+        prof = _profiled(stage, loop)
         cfg = {"workload": f"llama3-70b quarter stage decode, bs=1, kv={P}", **base_cfg, "kv_len": P, "batch": 1}
         lines.append(_line("stage decode tokens/s (70B quarter-stage, bs=1)", 1e3 / ms, "tokens/s", args, steps, ms,
                            cfg, wbytes + (P + 1) * kvb, _gateup_roofline(shape, prof)))
@@ -414,14 +436,12 @@ def other_workload(args) -> int:
                 for i in range(args.warmup):
                     one(i)
                 torch.cuda.synchronize()
-                stage.profile("gateup")
                 t = time.perf_counter()
                 for i in range(args.steps):
                     one(i)
                 torch.cuda.synchronize()
                 ms = (time.perf_counter() - t) * 1e3 / args.steps
-                prof = stage.profile_read()
-                stage.profile(None)
+                prof = _profiled(stage, lambda: [one(i) for i in range(args.steps)])
                 cfg = {"workload": f"llama3.1-8b half stage micro-batch, {nr} requests, {mode} "
                                    f"(tokens per request {ns}), kv lengths {[int(x) for x in lens[nr]]}, 10% holes",
                        **base_cfg, "requests": nr, "mode": mode, "rows": rows}

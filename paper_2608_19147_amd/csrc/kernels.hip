@@ -620,33 +620,57 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
     u32x4 wr[2][4], br[2][NCB][4];
     u32x2 sr[2][4];
     float4 cr[2][NCB];
+    // The products of a group are issued k-slice by k-slice (i outer): the 4 NCB
+    // accumulators of the tile are independent, so no product waits for the one
+    // before it; each accumulator still adds its four slices in order.
     auto compute = [&](int gi, const u32x4 (&wv)[4], const u32x2 (&sv)[4], u32x4 (&bv)[NCB][4], const float4 (&cq)[NCB]) {
         const int kb = 128 * gi;
         float cv[NCB];
+        if (kb + 128 <= K) {                             // a whole group (uniform)
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {                // in place: the set is reloaded after this group
-                const bool in = kb + 32 * lg + 8 * i < K;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) bv[cb][i][e] = in ? bv[cb][i][e] : 0u;
+            for (int cb = 0; cb < NCB; ++cb) {
+                const float4 c4 = cq[cb];
+                cv[cb] = (c4.x + c4.y) + (c4.z + c4.w);
             }
-            const float4 c4 = cq[cb];
-            cv[cb] = ((kb < K ? c4.x : 0.f) + (kb + 32 < K ? c4.y : 0.f)) + ((kb + 64 < K ? c4.z : 0.f) + (kb + 96 < K ? c4.w : 0.f));
-        }
+        } else {
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt) {
+            for (int cb = 0; cb < NCB; ++cb) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {            // in place: the set is reloaded after this group
+                    const bool in = kb + 32 * lg + 8 * i < K;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) bv[cb][i][e] = in ? bv[cb][i][e] : 0u;
+                }
+                const float4 c4 = cq[cb];
+                cv[cb] = ((kb < K ? c4.x : 0.f) + (kb + 32 < K ? c4.y : 0.f)) + ((kb + 64 < K ? c4.z : 0.f) + (kb + 96 < K ? c4.w : 0.f));
+            }
+        }
+        f32x4_t c[4][NCB];
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) c[rt][cb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
             half8_t A[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int rt = 0; rt < 4; ++rt) {
                 const uint32_t x = wv[rt][i], y = x >> 8;
                 u32x4 av;
                 av[0] = and_or_u32(0x000F000Fu, x, magic);
                 av[1] = and_or_u32(0x00F000F0u, x, magic);
                 av[2] = and_or_u32(0x000F000Fu, y, magic);
                 av[3] = and_or_u32(0x00F000F0u, y, magic);
-                A[i] = __builtin_bit_cast(half8_t, av);
+                A[rt] = __builtin_bit_cast(half8_t, av);
             }
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb)
+                    c[rt][cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A[rt], __builtin_bit_cast(half8_t, bv[cb][i]), c[rt][cb], 0, 0, 0);
+        }
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
             float scl[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -654,14 +678,9 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
                 scl[j] = f16_to_f32((uint16_t)((j & 1) ? (h >> 16) : (h & 0xFFFFu)));
             }
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) {
-                f32x4_t c = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(A[i], __builtin_bit_cast(half8_t, bv[cb][i]), c, 0, 0, 0);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[rt][cb][j] = __builtin_fmaf(scl[j], c[j] - cv[cb], acc[rt][cb][j]);
-            }
+                for (int j = 0; j < 4; ++j) acc[rt][cb][j] = __builtin_fmaf(scl[j], c[rt][cb][j] - cv[cb], acc[rt][cb][j]);
         }
     };
     // each tile starts its range at its own group (rotation by the tile index): at
