@@ -43,6 +43,8 @@ same fields, no CPU baseline):
                 beside it the 5-token linear verify of one path;
   head8b        final-stage epilogue: final RMSNorm + INT4 LM head (128256 x 4096,
                 group 128) + on-device top-1 (token, probability), 1 and 20 rows;
+                and the first stage's embedding gather from the 128256 x 4096
+                bf16 table, 1, 20 and 2048 ids;
   copycal       1 GiB device copies (calibration of HBM byte counters).
 """
 from __future__ import annotations
@@ -497,6 +499,32 @@ def head_workload(args) -> int:
                "hidden": H, "group_size": G, "rows": M, "act": shape.act_dtype}
         lines.append(_line(f"final-stage top-1 rows/s (LM head {V} x {H}, {M} rows)", M * 1e3 / ms, "rows/s", args,
                            steps, ms, cfg, nbytes, roof))
+    del xs
+    table = synth.make_embedding(shape, V, args.seed)
+    stage.attach_embedding(table)
+    del table
+    for n in (1, 20, 2048):
+        ids = [torch.from_numpy(synth.make_token_ids(V, n, args.seed, 500 + i)).cuda() for i in range(4)]
+        out = torch.empty((n, H), dtype=stage.act_dtype, device="cuda")
+        for i in range(max(1, args.warmup)):
+            stage.embed(ids[i % 4], hidden_out=out)
+        torch.cuda.synchronize()
+        ev[0].record()
+        for i in range(steps):
+            stage.embed(ids[i % 4], hidden_out=out)
+        ev[1].record()
+        ev[1].synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / steps
+        nbytes = n * (2 * H * 2 + 4)                                # rows read + rows written + ids
+        gbps = nbytes / (ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "kernel": "embed_gather_kernel", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4), "traffic": None, "bytes_per_launch": nbytes,
+                "avg_launch_us": round(ms * 1e3, 3), "launches_timed": steps,
+                "timed": "HIP events around the call on its stream (one kernel)"}
+        cfg = {"workload": f"first-stage embedding gather: {n} ids from a {V} x {H} table", "vocab": V, "hidden": H,
+               "rows": n, "act": shape.act_dtype}
+        lines.append(_line(f"first-stage embedding rows/s ({V} x {H} table, {n} ids)", n * 1e3 / ms, "rows/s", args,
+                           steps, ms, cfg, nbytes, roof, dtype=shape.act_dtype))
     stage.device_status()
     stage.close()
     for ln in lines:

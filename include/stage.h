@@ -344,6 +344,31 @@ int stage_head_attach(Stage* stage, const uint16_t* final_norm, const QuantMatri
 int stage_head_top1(Stage* stage, const void* hidden, int M, int32_t* token_out, float* p_out, float* logit_out,
                     float* logits_out, void* stream);
 
+/* ------------------------------------------------------------------------
+ * First-stage role ("Per-Stage Export Pipeline": the first shard also holds
+ * the token embedding; in the "Overview" figure the stage-0 shard runs the
+ * embeddings before its layers).  The lookup is a plain row gather.
+ * ------------------------------------------------------------------------ */
+
+/* Attach the token embedding table: table [vocab][H] of act_dtype bit
+ * patterns (row t is token t's hidden vector), host memory if
+ * weights_on_device == 0, else device memory.  Copied into library-owned
+ * device memory as it is (no quantization).  Synchronizes the stream.  Once
+ * per stage.
+ * Errors: INVALID (NULL), SHAPE (vocab < 1), UNSUPPORTED (already attached),
+ * CAPACITY (vocab * H above 2^36), OOM, HIP. */
+int stage_embed_attach(Stage* stage, const uint16_t* table, int vocab, int weights_on_device, void* stream);
+
+/* hidden_out[m] = table[ids[m]] for m < n, bit for bit: ids device int32 [n]
+ * (e.g. the token_out of stage_head_top1 on the last stage), hidden_out device
+ * [n][H] in act_dtype, ready as the hidden_in of stage_forward or
+ * stage_prefill.  1 <= n <= STAGE_MAX_PREFILL.  Stream-ordered; the ids are
+ * read on the device, so an id outside [0, vocab) cannot fail the call: its
+ * row is written as zeros and the stage is flagged, and the next
+ * stage_device_status returns STAGE_E_DEVICE.
+ * Errors: INVALID (NULL, no table attached), CAPACITY (n), HIP. */
+int stage_embed(Stage* stage, const int32_t* ids, int n, void* hidden_out, void* stream);
+
 /* Test support: the dequantized weight matrix as the kernels decode it,
  * W[r][c] = code * scale exactly, written to out_host fp32 [n][k].
  * which: 0..6 = wq, wk, wv, wo, wg, wu, wd in the tiled layout of the
@@ -408,7 +433,8 @@ int stage_debug_attn_read(Stage* stage, float* q_host, float* logits_host, int* 
  * within a bounded number of polls (a workgroup held off the device) gives up,
  * lets the launch finish, and flags the stage.  Synchronizes the device, then
  * returns STAGE_OK, or STAGE_E_DEVICE once per flagged stage (the flag is
- * cleared).  Call it where the caller synchronizes anyway. */
+ * cleared; an id outside the table met by stage_embed flags the stage the
+ * same way).  Call it where the caller synchronizes anyway. */
 int stage_device_status(Stage* stage);
 
 /* Bytes of device memory the stage holds for weights (packed codes + scales +

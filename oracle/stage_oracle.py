@@ -46,7 +46,7 @@ __all__ = [
     "round_rne", "to_fp16", "to_bf16", "fp16_bits_to_f64", "unpack_int4", "dequant",
     "rmsnorm", "rope_inv_freq", "apply_rope", "silu", "attention_slot",
     "OracleStage", "OracleState", "forward", "forward_batch", "trimmed_twin", "compact", "head_logits", "top1",
-    "ORACLE_BLOCK_ROWS",
+    "embed", "ORACLE_BLOCK_ROWS",
 ]
 
 # (significand bits including the implicit one, minimum normal exponent)
@@ -323,6 +323,22 @@ def top1(logits) -> tuple:
     mx = logits[np.arange(logits.shape[0]), idx]
     p = 1.0 / np.exp(logits - mx[:, None]).sum(axis=1)
     return idx, p, mx
+
+
+def embed(table, ids) -> np.ndarray:
+    """The first stage's input: row ids[m] of the token embedding table
+    [vocab, H] for each m (paper, "Per-Stage Export Pipeline": the first
+    shard holds the embedding ahead of its layers).  A lookup, so the rows
+    come back unchanged (same dtype, same bits).  An id outside [0, vocab)
+    is an error."""
+    table = np.asarray(table)
+    ids = np.asarray(ids, dtype=np.int64).reshape(-1)
+    if ids.size and (ids.min() < 0 or ids.max() >= table.shape[0]):
+        raise IndexError("token id outside the embedding table")
+    out = np.empty((ids.size, table.shape[1]), dtype=table.dtype)
+    for m, t in enumerate(ids):
+        out[m] = table[t]
+    return out
 
 
 def forward(stage: OracleStage, state: OracleState, x, positions, beam_idx=None, mask=None,

@@ -26,7 +26,7 @@ EXPORTS = (
     "stage_profile_enable", "stage_profile_read", "stage_debug_phase_trace", "stage_device_status",
     "stage_debug_attn_arm", "stage_debug_attn_read",
     "kv_compact", "kv_capture_size", "kv_capture", "kv_restore", "kv_capture_noalloc",
-    "stage_head_attach", "stage_head_top1", "stage_prefill",
+    "stage_head_attach", "stage_head_top1", "stage_prefill", "stage_embed_attach", "stage_embed",
 )
 KERNEL_CLASSES = {"qkv": 0, "attn": 1, "oproj": 2, "gateup": 3, "down": 4, "persistent": 5}
 
@@ -100,6 +100,8 @@ def load() -> ctypes.CDLL:
         "stage_head_attach": (I, [V, V, P(QuantMatrix), I, V]),
         "stage_head_top1": (I, [V, V, I, V, V, V, V, V]),
         "stage_prefill": (I, [V, V, I, V, V, V, V, V]),
+        "stage_embed_attach": (I, [V, V, I, I, V]),
+        "stage_embed": (I, [V, V, I, V, V]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

@@ -282,4 +282,10 @@ hipError_t launch_table_identity(int16_t* table, int S, int cap, int n, hipStrea
 // 1 / sum over tiles of se * exp(max_t - max) (the softmax probability of it).
 hipError_t launch_top1_merge(const float4* part, int M, int ntiles, int32_t* token, float* p, float* logit, hipStream_t st);
 
+// Row m < n of out [n][H] = row ids[m] (device int32) of table [vocab][H]
+// (2-byte elements, copied bit for bit); an id outside [0, vocab) gives a zero
+// row and sets *err to 1.
+hipError_t launch_embed_gather(const uint16_t* table, const int32_t* ids, int n, int vocab, int H, uint16_t* out,
+                               unsigned* err, hipStream_t st);
+
 }  // namespace stg

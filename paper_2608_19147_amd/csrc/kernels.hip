@@ -2103,6 +2103,38 @@ hipError_t launch_top1_merge(const float4* part, int M, int ntiles, int32_t* tok
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------------ stage-0 embedding gather
+
+// Row m of out = row ids[m] of the token table [vocab][row_elems], copied
+// unchanged; an id outside [0, vocab) gives a zero row and sets *err.  One
+// workgroup per row; T is the copy width (16 bytes when both pointers allow).
+template <class T>
+__global__ __launch_bounds__(256) void embed_gather_kernel(const T* __restrict__ table, const int32_t* __restrict__ ids,
+                                                           int vocab, int row_elems, T* __restrict__ out,
+                                                           unsigned* __restrict__ err) {
+    const int m = blockIdx.x;
+    const int id = ids[m];
+    T* dst = out + (size_t)m * row_elems;
+    if (id < 0 || id >= vocab) {
+        for (int i = threadIdx.x; i < row_elems; i += 256) dst[i] = T(0);
+        if (threadIdx.x == 0) atomicOr(err, 1u);
+        return;
+    }
+    const T* src = table + (size_t)id * row_elems;
+    for (int i = threadIdx.x; i < row_elems; i += 256) dst[i] = src[i];
+}
+
+hipError_t launch_embed_gather(const uint16_t* table, const int32_t* ids, int n, int vocab, int H, uint16_t* out,
+                               unsigned* err, hipStream_t st) {
+    if (n < 1 || vocab < 1 || H < 1) return hipErrorInvalidValue;
+    if (H % 8 == 0 && ((uintptr_t)table & 15) == 0 && ((uintptr_t)out & 15) == 0)
+        embed_gather_kernel<u32x4><<<dim3((unsigned)n), dim3(256), 0, st>>>((const u32x4*)table, ids, vocab, H / 8,
+                                                                          (u32x4*)out, err);
+    else
+        embed_gather_kernel<uint16_t><<<dim3((unsigned)n), dim3(256), 0, st>>>(table, ids, vocab, H, out, err);
+    return hipGetLastError();
+}
+
 // The k and v rows of n prompt rows (q|k|v results [n][ld], fp32) of a one-slot
 // state to cache rows P .. P + n - 1 of one layer: k rotated at the row's
 // position (rotate-half pairing), both rounded to the cache dtype.  One thread

@@ -122,6 +122,10 @@ struct Stage {
     DevMat head;
     uint16_t* final_norm = nullptr;
     float4* top1_part = nullptr;                       // [MAX_ROWS][head tiles]
+    // first-stage role: token embedding table [embed_vocab][H] in act dtype (stage_embed_attach)
+    uint16_t* embed = nullptr;
+    int embed_vocab = 0;
+    unsigned* embed_err = nullptr;                     // set by a gather that met an id outside the table
     // prefill workspace for pf_rows prompt rows: residual fp32 [rows][H], q|k|v fp32
     // [rows][NQKV], SwiGLU output fp32 [rows][F], prepared inputs (64-row blocks)
     float *pf_x = nullptr, *pf_qkv = nullptr, *pf_act = nullptr, *pf_bc = nullptr;
@@ -775,15 +779,21 @@ int stage_debug_attn_read(Stage* st, float* q_host, float* logits_host, int* row
 
 int stage_device_status(Stage* st) {
     if (!st) return fail(STAGE_E_INVALID, "NULL argument");
-    if (!st->err) return STAGE_OK;                      // the stage has no single-launch forward
+    if (!st->err && !st->embed_err) return STAGE_OK;   // nothing on the device can flag this stage
     HIP_TRY(hipSetDevice(st->device));
     HIP_TRY(hipDeviceSynchronize());
-    unsigned flag = 0u;
-    HIP_TRY(hipMemcpy(&flag, st->err, sizeof(unsigned), hipMemcpyDeviceToHost));
-    if (flag == 0u) return STAGE_OK;
-    HIP_TRY(hipMemset(st->err, 0, sizeof(unsigned)));
-    return fail(STAGE_E_DEVICE, "a single-launch forward gave up waiting on another workgroup (was the device "
-                                "shared?); its outputs and appended cache rows are invalid");
+    unsigned flag = 0u, eflag = 0u;
+    if (st->err) HIP_TRY(hipMemcpy(&flag, st->err, sizeof(unsigned), hipMemcpyDeviceToHost));
+    if (st->embed_err) HIP_TRY(hipMemcpy(&eflag, st->embed_err, sizeof(unsigned), hipMemcpyDeviceToHost));
+    if (flag) HIP_TRY(hipMemset(st->err, 0, sizeof(unsigned)));
+    if (eflag) HIP_TRY(hipMemset(st->embed_err, 0, sizeof(unsigned)));
+    if (flag)
+        return fail(STAGE_E_DEVICE, "a single-launch forward gave up waiting on another workgroup (was the device "
+                                    "shared?); its outputs and appended cache rows are invalid");
+    if (eflag)
+        return fail(STAGE_E_DEVICE, "stage_embed met a token id outside [0, vocab); the rows of such ids were "
+                                    "written as zeros");
+    return STAGE_OK;
 }
 
 int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n, int* n_workgroups) {
@@ -1204,6 +1214,44 @@ int stage_head_attach(Stage* st, const uint16_t* final_norm, const QuantMatrix* 
     st->top1_part = part;
     st->vocab = V;
     st->head_ok = true;
+    HIP_TRY(mark_done(st, s));
+    return STAGE_OK;
+}
+
+int stage_embed_attach(Stage* st, const uint16_t* table, int vocab, int weights_on_device, void* stream) {
+    if (!st || !table) return fail(STAGE_E_INVALID, "NULL argument");
+    if (st->embed) return fail(STAGE_E_UNSUPPORTED, "the stage already has an embedding table");
+    if (vocab < 1) return fail(STAGE_E_SHAPE, "vocab must be >= 1");
+    const int H = st->cfg.hidden;
+    if ((int64_t)vocab * H > ((int64_t)1 << 36)) return fail(STAGE_E_CAPACITY, "embedding table too large");
+    HIP_TRY(hipSetDevice(st->device));
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(order_on(st, s));
+    uint16_t* t = nullptr;
+    unsigned* e = nullptr;
+    int rc;
+    if ((rc = st->alloc(&t, (size_t)vocab * H)) || (rc = st->alloc(&e, 1))) return rc;
+    HIP_TRY(hipMemsetAsync(e, 0, sizeof(unsigned), s));
+    HIP_TRY(hipMemcpyAsync(t, table, (size_t)vocab * H * 2, weights_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice,
+                           s));
+    HIP_TRY(hipStreamSynchronize(s));
+    st->weight_bytes += 2 * (int64_t)vocab * H;
+    st->embed = t;
+    st->embed_err = e;
+    st->embed_vocab = vocab;
+    HIP_TRY(mark_done(st, s));
+    return STAGE_OK;
+}
+
+int stage_embed(Stage* st, const int32_t* ids, int n, void* hidden_out, void* stream) {
+    if (!st || !ids || !hidden_out) return fail(STAGE_E_INVALID, "NULL argument");
+    if (!st->embed) return fail(STAGE_E_INVALID, "no embedding table attached (stage_embed_attach)");
+    if (n < 1 || n > STAGE_MAX_PREFILL) return fail(STAGE_E_CAPACITY, "n must be in [1, STAGE_MAX_PREFILL]");
+    HIP_TRY(hipSetDevice(st->device));
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(order_on(st, s));
+    HIP_TRY(launch_embed_gather(st->embed, ids, n, st->embed_vocab, st->cfg.hidden, (uint16_t*)hidden_out, st->embed_err,
+                                s));
     HIP_TRY(mark_done(st, s));
     return STAGE_OK;
 }

@@ -149,9 +149,9 @@ class Stage:
                 lg[: m * sh.n_q_heads * k].reshape(m, sh.n_q_heads, k))
 
     def device_status(self) -> None:
-        """Wait for the last single-launch forward; raise StageError
-        (STAGE_E_DEVICE) once if a forward of this stage gave up waiting on
-        another workgroup."""
+        """Wait for the device; raise StageError (STAGE_E_DEVICE) once if a
+        single-launch forward of this stage gave up waiting on another
+        workgroup or an embedding gather met an id outside its table."""
         check(self.lib.stage_device_status(self.handle))
 
     def phase_trace(self) -> np.ndarray:
@@ -192,6 +192,27 @@ class Stage:
                                        ctypes.c_void_p(full.data_ptr() if full is not None else None),
                                        ctypes.c_void_p(_stream_ptr(stream))))
         return tok, p, lg, full
+
+    def attach_embedding(self, table: torch.Tensor, on_device: bool = False, stream=None) -> None:
+        """Token embedding table [vocab, H] in the act dtype (first-stage role)."""
+        t = table.contiguous() if on_device else table.detach().cpu().contiguous()
+        if t.dim() != 2 or t.shape[1] != self.shape.hidden or t.element_size() != 2:
+            raise ValueError("embedding table must be [vocab, hidden] with 2-byte elements")
+        check(self.lib.stage_embed_attach(self.handle, ctypes.c_void_p(t.data_ptr()), int(t.shape[0]), int(on_device),
+                                          ctypes.c_void_p(_stream_ptr(stream))))
+        self.embed_vocab = int(t.shape[0])
+
+    def embed(self, ids: torch.Tensor, hidden_out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        """Hidden rows [n, H] (device, act dtype) = table[ids] for device int32 ids [n]."""
+        if ids.dtype != torch.int32 or not ids.is_cuda:
+            raise ValueError("ids must be a device int32 tensor")
+        ids = ids.contiguous()
+        n = int(ids.numel())
+        if hidden_out is None:
+            hidden_out = torch.empty((n, self.shape.hidden), dtype=self.act_dtype, device=ids.device)
+        check(self.lib.stage_embed(self.handle, ctypes.c_void_p(ids.data_ptr()), n, ctypes.c_void_p(hidden_out.data_ptr()),
+                                   ctypes.c_void_p(_stream_ptr(stream))))
+        return hidden_out
 
     def prefill(self, state: "KVState", positions, hidden_in: torch.Tensor, past_mask=None,
                 hidden_out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:

@@ -169,6 +169,25 @@ def make_head(shape: StageShape, vocab: int, seed: int = 0) -> Tuple[torch.Tenso
     return fn, make_quant_matrix(vocab, shape.hidden, shape.group_size, rng(seed, shape.config_id, 900_002))
 
 
+def make_embedding(shape: StageShape, vocab: int, seed: int = 0) -> torch.Tensor:
+    """The first stage's token embedding table [vocab, H] in the activation
+    dtype, ~N(0, 0.02^2) (the usual initialisation scale of Llama tables),
+    drawn in blocks of 8192 rows so a full vocabulary does not need one huge
+    float32 temporary."""
+    out = torch.empty((vocab, shape.hidden), dtype=_TORCH_DT[shape.act_dtype])
+    for b0 in range(0, vocab, 8192):
+        rows = min(8192, vocab - b0)
+        r = rng(seed, shape.config_id, 900_010, b0 // 8192)
+        out[b0:b0 + rows] = round_to(r.standard_normal((rows, shape.hidden), dtype=np.float32) * np.float32(0.02),
+                                     shape.act_dtype)
+    return out
+
+
+def make_token_ids(vocab: int, n: int, seed: int = 0, step: int = 0) -> np.ndarray:
+    """n token ids, uniform over [0, vocab), int32."""
+    return rng(seed, 4, 900_020, step).integers(0, vocab, n, dtype=np.int32)
+
+
 def make_kv(shape: StageShape, n_slots: int, n_tokens: int, seed: int = 0, stream: int = 0) -> Tuple[torch.Tensor, torch.Tensor]:
     """Already-stored cache rows ~N(0,1): K and V [L][S][Hkv][n][D] in the KV dtype."""
     dims = (shape.n_layers, n_slots, shape.n_kv_heads, n_tokens, shape.head_dim)

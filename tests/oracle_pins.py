@@ -637,6 +637,29 @@ def pin_head_zero_weights():
     assert np.all(lg == 0) and np.all(idx == 0) and np.allclose(p, 1 / 64, rtol=0, atol=1e-16)
 
 
+def pin_embed_against_torch_and_one_hot():
+    """The first stage's lookup: torch's embedding op, and a one-hot matrix
+    times the table (exact: one nonzero term per output), on ragged ids with
+    repeats and both ends of the vocabulary; an id outside the table is an
+    error."""
+    shape = TINY
+    V = 97
+    table = synth.make_embedding(shape, V, 84)
+    ids = np.concatenate([[0, V - 1, 5, 5], synth.make_token_ids(V, 9, 84)])
+    got = oracle.embed(table.numpy(), ids)
+    ref = F.embedding(torch.from_numpy(ids.astype(np.int64)), table).numpy()
+    assert got.dtype == ref.dtype and np.array_equal(got.view(np.uint16), ref.view(np.uint16))
+    one_hot = np.zeros((ids.size, V))
+    one_hot[np.arange(ids.size), ids] = 1.0
+    assert np.array_equal(one_hot @ f64(table), got.astype(np.float64))
+    for bad in ([V], [-1]):
+        try:
+            oracle.embed(table.numpy(), bad)
+        except IndexError:
+            continue
+        raise AssertionError(f"id {bad} accepted")
+
+
 # ------------------------------------------------------------------ per-row (4-D) masks
 
 def tree_case():

@@ -189,7 +189,19 @@ def _head_no_norm(x, final_norm, lm_q, lm_scales, vocab, group, eps):
     return so.gemv_rows(x * so._as_f64(final_norm), so.dequant(lm_q, lm_scales, x.shape[1], group))
 
 
+def _embed_off_by_one(table, ids):
+    table = np.asarray(table)
+    return table[np.clip(np.asarray(ids, dtype=np.int64) + 1, 0, table.shape[0] - 1)]
+
+
+def _embed_column(table, ids):
+    table = np.asarray(table)
+    return table[:, np.asarray(ids, dtype=np.int64) % table.shape[1]].T
+
+
 MUTANTS = {
+    "embed_off_by_one": ("embed", _embed_off_by_one),
+    "embed_column": ("embed", _embed_column),
     "top1_last_tie": ("top1", _top1_last_tie),
     "top1_prob_of_first": ("top1", _top1_prob_of_first),
     "head_no_norm": ("head_logits", _head_no_norm),
