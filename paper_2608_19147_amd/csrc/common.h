@@ -12,7 +12,7 @@ constexpr int MAX_ROWS = 64;         // activation rows per forward
 constexpr int GEMV_MAX_M = 8;        // rows one GEMV launch handles
 constexpr int GEMV_MAX_CPS = 64;     // chunks per workgroup: 4 waves x at most 16 chunks
 constexpr int ATTN_MAX_SPLITS = 64;  // KV splits per (slot, kv head)
-constexpr int ATTN_MIN_SPLIT = 128;  // fewest keys per split
+constexpr int ATTN_MIN_SPLIT = 256;  // fewest keys per split
 constexpr int KGROUPS = 16;          // 16-lane key groups per attention workgroup
 
 enum Dt : int { DT_F32 = 0, DT_F16 = 1, DT_BF16 = 2 };
@@ -113,6 +113,9 @@ struct AttnArgs {
     int vector_path;         // 1: attn_kernel (vector units) instead of attn_mma_kernel
     uint16_t* bp_out; float* bc_out; int kp;   // the attention output also in prepared form (o product input, 64-row blocks)
     int no_append;           // the rows of this forward are already in the cache (prefill): do not write them
+    int dma;                 // 1: cache rows by direct loads (attn_dma_kernel) where the launch allows it: every
+                             // split at most 1024 keys, per-row masks of at most 8 KB per split, at most 64
+                             // query vectors per kv head
     // test support (null unless armed): the rotated queries [M][Hq][D] and the
     // scores q.k / sqrt(D) of every visible key [M][Hq][dbg_keys]
     float* dbg_q; float* dbg_logits; int dbg_keys;

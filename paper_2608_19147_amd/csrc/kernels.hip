@@ -1411,6 +1411,19 @@ template <int KVDT>
 __device__ __forceinline__ uint16_t kv_round(float f) { return KVDT == DT_BF16 ? f32_to_bf16(f) : f32_to_f16(f); }
 template <int KVDT>
 __device__ __forceinline__ float kv_float(uint16_t b) { return KVDT == DT_BF16 ? bf16_to_f32(b) : f16_to_f32(b); }
+// Two floats rounded to the cache dtype (to nearest even) and packed, low half
+// first: one v_cvt_pk_bf16_f32 for bf16.  Equal to kv_round of each for every
+// finite input that is not an fp32 denormal (the probabilities it packs never are).
+template <int KVDT>
+__device__ __forceinline__ uint32_t kv_pack2(float lo, float hi) {
+    if constexpr (KVDT == DT_BF16) {
+        typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+        const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+        return __builtin_bit_cast(uint32_t, v);
+    } else {
+        return (uint32_t)kv_round<KVDT>(lo) | ((uint32_t)kv_round<KVDT>(hi) << 16);
+    }
+}
 
 // The values of v in this lane and in lane ^ sh (sh = 16 or 32): every lane of
 // the pair receives the lower lane's value in a and the upper lane's in b.
@@ -1580,30 +1593,45 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
             const bool ok = qt < nqt && r < R;
             const int i = ok ? r / gs : 0, h = g * gs + (ok ? r % gs : 0);
             const int m = rowbase + i;
-            const int pos = a.meta.positions[m];
             const float* qrow = a.qkv + (size_t)m * a.qkv_ld + (size_t)h * D;
             qtok[u] = ok ? i : n;
+            // every load of the tile at once (row 0 of the item stands in for a missing
+            // row): q and its rotary partners, then (cos, sin) at the row's position
+            float4 qa[DB][2], qp[DB][2], rc[DB][4];
 #pragma unroll
             for (int ib = 0; ib < DB; ++ib) {
-                // dims d0 .. d0 + 7 lie in one rotary half: 16-byte loads of q, its partner and (cos, sin)
+                const int d0 = 32 * ib + 8 * lg;
+                const bool lo_half = d0 < HALF;
+#pragma unroll
+                for (int h2 = 0; h2 < 2; ++h2) {
+                    qa[ib][h2] = ((const float4*)(qrow + d0))[h2];
+                    qp[ib][h2] = ((const float4*)(qrow + (lo_half ? d0 + HALF : d0 - HALF)))[h2];
+                }
+            }
+            const int pos = a.meta.positions[m];
+#pragma unroll
+            for (int ib = 0; ib < DB; ++ib) {
+                const int d0 = 32 * ib + 8 * lg;
+                const float4* r4 = (const float4*)(a.rope + (size_t)pos * HALF + (d0 < HALF ? d0 : d0 - HALF));
+#pragma unroll
+                for (int h4 = 0; h4 < 4; ++h4) rc[ib][h4] = r4[h4];
+            }
+#pragma unroll
+            for (int ib = 0; ib < DB; ++ib) {
+                // dims d0 .. d0 + 7 lie in one rotary half
                 const int d0 = 32 * ib + 8 * lg;
                 const bool lo_half = d0 < HALF;
                 float xv[8], xpv[8], cv[8], sv[8];
-                if (ok) {
-                    const float4* q4 = (const float4*)(qrow + d0);
-                    const float4* p4 = (const float4*)(qrow + (lo_half ? d0 + HALF : d0 - HALF));
-                    const float4* r4 = (const float4*)(a.rope + (size_t)pos * HALF + (lo_half ? d0 : d0 - HALF));
 #pragma unroll
-                    for (int h2 = 0; h2 < 2; ++h2) {
-                        const float4 x4 = q4[h2], y4 = p4[h2];
-                        xv[4 * h2] = x4.x; xv[4 * h2 + 1] = x4.y; xv[4 * h2 + 2] = x4.z; xv[4 * h2 + 3] = x4.w;
-                        xpv[4 * h2] = y4.x; xpv[4 * h2 + 1] = y4.y; xpv[4 * h2 + 2] = y4.z; xpv[4 * h2 + 3] = y4.w;
-                    }
+                for (int h2 = 0; h2 < 2; ++h2) {
+                    const float4 x4 = qa[ib][h2], y4 = qp[ib][h2];
+                    xv[4 * h2] = x4.x; xv[4 * h2 + 1] = x4.y; xv[4 * h2 + 2] = x4.z; xv[4 * h2 + 3] = x4.w;
+                    xpv[4 * h2] = y4.x; xpv[4 * h2 + 1] = y4.y; xpv[4 * h2 + 2] = y4.z; xpv[4 * h2 + 3] = y4.w;
+                }
 #pragma unroll
-                    for (int h4 = 0; h4 < 4; ++h4) {
-                        const float4 c4 = r4[h4];
-                        cv[2 * h4] = c4.x; sv[2 * h4] = c4.y; cv[2 * h4 + 1] = c4.z; sv[2 * h4 + 1] = c4.w;
-                    }
+                for (int h4 = 0; h4 < 4; ++h4) {
+                    const float4 c4 = rc[ib][h4];
+                    cv[2 * h4] = c4.x; sv[2 * h4] = c4.y; cv[2 * h4 + 1] = c4.z; sv[2 * h4 + 1] = c4.w;
                 }
                 uint16_t hb[8], rb[8];
 #pragma unroll
@@ -1716,15 +1744,12 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
                 lane_pair_k(mx, 32, x0, x1);
                 mx = fmaxf(x0, x1);
                 const float mn = fmaxf(mrun[u], mx);
-                float corr = 1.f, pv[8];
-                if (mn == -INFINITY) {
+                // no key seen yet (mn = -inf): base 0 makes every term and the correction 0
+                const float base = mn == -INFINITY ? 0.f : mn;
+                const float corr = __builtin_amdgcn_exp2f(mrun[u] - base);
+                float pv[8];
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) pv[e] = 0.f;
-                } else {
-                    corr = exp2f(mrun[u] - mn);
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) pv[e] = exp2f(sv[e] - mn);
-                }
+                for (int e = 0; e < 8; ++e) pv[e] = __builtin_amdgcn_exp2f(sv[e] - base);
                 float ps = 0.f;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) ps += pv[e];
@@ -1732,14 +1757,15 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
                 mrun[u] = mn;
                 u32x4 pb;
 #pragma unroll
-                for (int w2 = 0; w2 < 4; ++w2)
-                    pb[w2] = (uint32_t)kv_round<KVDT>(pv[2 * w2]) | ((uint32_t)kv_round<KVDT>(pv[2 * w2 + 1]) << 16);
+                for (int w2 = 0; w2 < 4; ++w2) pb[w2] = kv_pack2<KVDT>(pv[2 * w2], pv[2 * w2 + 1]);
+                if (__any(corr != 1.f)) {                        // the running maximum moved in some lane
 #pragma unroll
-                for (int mb = 0; mb < MB; ++mb) {
+                    for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-                    for (int jj = 0; jj < 4; ++jj) o[u][mb][jj] *= corr;
-                    o[u][mb] = mma_kv<KVDT>(vf[mb], pb, o[u][mb]);
+                        for (int jj = 0; jj < 4; ++jj) o[u][mb][jj] *= corr;
                 }
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) o[u][mb] = mma_kv<KVDT>(vf[mb], pb, o[u][mb]);
             }
             if (st + 1 < nsteps) stash(buf ^ 1);
             __syncthreads();
@@ -1773,15 +1799,432 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
     }
 }
 
+// ------------------------------------------------------------------ matrix-core attention, cache rows by direct loads
+//
+// attn_mma_kernel for items of at most 64 query vectors per kv head (one tile
+// per wave), with the same split, step order, arithmetic and partials (results
+// are bitwise equal), but with the cache rows of each 32-key step brought into
+// LDS by direct-to-LDS buffer loads issued ATTN_NB - 1 steps ahead instead of
+// through registers one step ahead.  A key the split does not keep (masked,
+// past the split, or a row of this forward, which is written in afterwards)
+// is read at an offset past the buffer's end, which the hardware answers with
+// zeros without a memory access.  K and V are stored as in memory, 16-byte
+// chunk c of key k at position c ^ (k mod chunks per row); the value fragments
+// of O^T += V^T P^T come from ds_read_b64_tr_b16, which hands lane i of each
+// 16-lane group element i mod 4 of the 8 bytes read by lane 4 e + i / 4 of the
+// group, as element e (e < 4): the four keys of a fragment half become one
+// lane's four k slots.  The whole split's table entries and mask bytes (at
+// most ATTN_SCH keys) and the rows of a per-query-row mask (at most ATTN_RSM
+// bytes) are staged first; LDS is read through inline assembly and the
+// workgroup synchronizes with a bare s_barrier, so no compiler-inserted wait
+// drains the loads in flight.
+constexpr int ATTN_NB = 4;                // step buffers (K and V of 32 keys each)
+constexpr int ATTN_SCH = 1024;            // most keys of one split on this path
+constexpr int ATTN_RSM = 8192;            // bytes of per-query-row mask staged per split (rows x split keys)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t attn_rsrc(const void* p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ void attn_dma(__amdgpu_buffer_rsrc_t r, uint32_t off, void* lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 2 /* nt */);
+}
+__device__ __forceinline__ u32x4 attn_lds16(uint32_t a) {
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
+    return v;
+}
+__device__ __forceinline__ u32x2 attn_lds_tr(uint32_t a) {
+    u32x2 v;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(a));
+    return v;
+}
+__device__ __forceinline__ uint32_t attn_lds4(uint32_t a) {
+    uint32_t v;
+    asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(a));
+    return v;
+}
+__device__ __forceinline__ uint32_t attn_lds_u16(uint32_t a) {
+    uint32_t v;
+    asm volatile("ds_read_u16 %0, %1" : "=v"(v) : "v"(a));
+    return v;
+}
+__device__ __forceinline__ uint32_t attn_lds_u8(uint32_t a) {
+    uint32_t v;
+    asm volatile("ds_read_u8 %0, %1" : "=v"(v) : "v"(a));
+    return v;
+}
+__device__ __forceinline__ void attn_lgkm() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// After attn_lgkm: makes v depend on the wait, so no use of a value read by
+// inline assembly moves above it (the compiler takes such values as ready).
+__device__ __forceinline__ void touch_v(u32x4& v) { asm volatile("" : "+v"(v)); }
+__device__ __forceinline__ void touch_u(uint32_t& v) { asm volatile("" : "+v"(v)); }
+template <int N>
+__device__ __forceinline__ void attn_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
+__device__ __forceinline__ void attn_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+template <int D, int KVDT, bool REC = false>
+__global__ __launch_bounds__(256, 2) void attn_dma_kernel(AttnArgs a) {
+    constexpr int HALF = D / 2;
+    constexpr int NCH = D / 8;               // 16-byte chunks per cache row
+    constexpr int DB = D / 32;               // k-blocks of the score products
+    constexpr int MB = D / 16;               // row blocks of O^T
+    constexpr int RB = 2 * D;                // bytes per cache row
+    constexpr int SB = AK * RB;              // bytes of one step's K (or V)
+    constexpr int KPI = 1024 / RB;           // keys per direct load (64 lanes x 16 bytes)
+    constexpr int NI = SB / 1024 / 4;        // direct loads per wave per step, K and V each
+    constexpr int VMN = 2 * NI * (ATTN_NB - 2);   // loads a lane may leave in flight at the top of a step
+    static_assert(NI >= 1 && VMN <= 63, "step geometry");
+    static_assert(AK * NCH % 256 == 0, "new-row staging");
+    __shared__ __attribute__((aligned(16))) uint8_t kvs[ATTN_NB][2][SB];
+    __shared__ int16_t stab[ATTN_SCH];
+    __shared__ __attribute__((aligned(16))) uint8_t smk[ATTN_SCH];
+    __shared__ __attribute__((aligned(16))) uint8_t srm[ATTN_RSM];   // [row][split key] when the request has row masks
+
+    const int item = blockIdx.x, g = blockIdx.y, split = blockIdx.z;
+    const ItemDev it = a.meta.items[item];
+    const ReqDev rq = it.rq;
+    const int b = it.slot;
+    const int P = rq.P, n = rq.n;
+    const int L = P + n;
+    int split_len = max(ATTN_MIN_SPLIT, (L + rq.splits - 1) / rq.splits);
+    split_len = (split_len + KGROUPS - 1) / KGROUPS * KGROUPS;
+    const int nsplit = (L + split_len - 1) / split_len;
+    if (split >= nsplit) return;
+    const int j0 = split * split_len, j1 = min(L, j0 + split_len);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int ql = lane & 15, lg = lane >> 4;
+    const int Hq = a.Hq, Hkv = a.Hkv;
+    const int gs = Hq / Hkv;
+    const int R = gs * n;
+    const int nqt = (R + 15) / 16;
+    const size_t lstride = (size_t)rq.S * Hkv * rq.cap * D;
+    uint16_t* kl = rq.kc + (size_t)a.layer * lstride;
+    uint16_t* vl = rq.vc + (size_t)a.layer * lstride;
+    const uint8_t* mask = a.meta.masks + rq.mask_off + (size_t)b * rq.mask_len;
+    const int16_t* tab = rq.table + (size_t)b * rq.cap;
+    const int rowbase = rq.row0 + b * n;
+
+    // ---- the split's table entries and mask bytes (and each query row's own mask)
+    for (int x = tid; x < j1 - j0; x += 256) {
+        const int j = j0 + x;
+        smk[x] = mask[j];
+        stab[x] = j < P ? tab[j] : (int16_t)b;
+    }
+    const uint8_t* rmask = rq.rowmask_off >= 0 ? a.meta.masks + rq.rowmask_off + (size_t)b * n * rq.mask_len : nullptr;
+    const int rspan = (j1 - j0 + 3) & ~3;                    // row stride of srm (the host checked n * rspan fits)
+    if (rmask)
+        for (int q = tid; q < n * rspan; q += 256) {
+            const int i = q / rspan, x = q - i * rspan;
+            srm[q] = x < j1 - j0 ? rmask[(size_t)i * rq.mask_len + j0 + x] : (uint8_t)0;
+        }
+    __syncthreads();
+
+    // ---- direct loads of step s into buffer s mod ATTN_NB: lane l of load h of
+    // this wave carries chunk position l mod NCH of key (NI wave + h) KPI + l / NCH
+    const int nsteps = (j1 - j0 + AK - 1) / AK;
+    const uint32_t lbytes = (uint32_t)(lstride * 2);
+    const __amdgpu_buffer_rsrc_t rk = attn_rsrc(kl, lbytes), rv = attn_rsrc(vl, lbytes);
+    const uint32_t smk_a = (uint32_t)(uintptr_t)smk, stab_a = (uint32_t)(uintptr_t)stab;
+    const uint32_t kvs_a = (uint32_t)(uintptr_t)&kvs[0][0][0];
+    const int cstop = min(j1, P);                            // keys below this come from the cache
+    auto issue = [&](int s) {
+        uint32_t off[NI];
+#pragma unroll
+        for (int h = 0; h < NI; ++h) {
+            const int key = (NI * wave + h) * KPI + lane / NCH;
+            const int x = min(s * AK + key, ATTN_SCH - 1), j = j0 + s * AK + key;
+            uint32_t mk = attn_lds_u8(smk_a + (uint32_t)x);
+            uint32_t tb = attn_lds_u16(stab_a + 2u * (uint32_t)x);
+            attn_lgkm();
+            touch_u(mk);
+            touch_u(tb);
+            const int slot = (int)(int16_t)tb;
+            const int c = (lane % NCH) ^ (key % NCH);
+            const bool kept = s < nsteps && j < cstop && mk != 0u;
+            off[h] = kept ? (uint32_t)(((((size_t)slot * Hkv + g) * rq.cap + j) * D + 8 * c) * 2) : 0xFFFFFFF0u;
+        }
+        uint8_t* kb = &kvs[s % ATTN_NB][0][0];
+#pragma unroll
+        for (int h = 0; h < NI; ++h) {
+            const int blk = (NI * wave + h) * 1024;
+            attn_dma(rk, off[h], kb + blk);
+            attn_dma(rv, off[h], kb + SB + blk);
+        }
+    };
+#pragma unroll
+    for (int s = 0; s < ATTN_NB - 1; ++s) issue(s);
+
+    // ---- this wave's query tile: rotated, scaled, split into rounded part and residual
+    const bool active = wave < nqt;
+    u32x4 qh[DB], qr[DB];
+    int qtok;
+    float mrun = -INFINITY, lsum = 0.f;
+    f32x4_t o[MB];
+    {
+        const int r = 16 * wave + ql;
+        const bool ok = active && r < R;
+        const int i = ok ? r / gs : 0, h = g * gs + (ok ? r % gs : 0);
+        const int m = rowbase + i;
+        const float* qrow = a.qkv + (size_t)m * a.qkv_ld + (size_t)h * D;
+        qtok = ok ? i : n;
+        // every load of the tile at once (row 0 of the item stands in for a missing
+        // row): q and its rotary partners, then (cos, sin) at the row's position
+        float4 qa[DB][2], qp[DB][2], rc[DB][4];
+#pragma unroll
+        for (int ib = 0; ib < DB; ++ib) {
+            const int d0 = 32 * ib + 8 * lg;
+            const bool lo_half = d0 < HALF;
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+                qa[ib][h2] = ((const float4*)(qrow + d0))[h2];
+                qp[ib][h2] = ((const float4*)(qrow + (lo_half ? d0 + HALF : d0 - HALF)))[h2];
+            }
+        }
+        const int pos = a.meta.positions[m];
+#pragma unroll
+        for (int ib = 0; ib < DB; ++ib) {
+            const int d0 = 32 * ib + 8 * lg;
+            const float4* r4 = (const float4*)(a.rope + (size_t)pos * HALF + (d0 < HALF ? d0 : d0 - HALF));
+#pragma unroll
+            for (int h4 = 0; h4 < 4; ++h4) rc[ib][h4] = r4[h4];
+        }
+#pragma unroll
+        for (int ib = 0; ib < DB; ++ib) {
+            // dims d0 .. d0 + 7 lie in one rotary half
+            const int d0 = 32 * ib + 8 * lg;
+            const bool lo_half = d0 < HALF;
+            float xv[8], xpv[8], cv[8], sv[8];
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+                const float4 x4 = qa[ib][h2], y4 = qp[ib][h2];
+                xv[4 * h2] = x4.x; xv[4 * h2 + 1] = x4.y; xv[4 * h2 + 2] = x4.z; xv[4 * h2 + 3] = x4.w;
+                xpv[4 * h2] = y4.x; xpv[4 * h2 + 1] = y4.y; xpv[4 * h2 + 2] = y4.z; xpv[4 * h2 + 3] = y4.w;
+            }
+#pragma unroll
+            for (int h4 = 0; h4 < 4; ++h4) {
+                const float4 c4 = rc[ib][h4];
+                cv[2 * h4] = c4.x; sv[2 * h4] = c4.y; cv[2 * h4 + 1] = c4.z; sv[2 * h4 + 1] = c4.w;
+            }
+            uint16_t hb[8], rb[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                float y = 0.f;
+                if (ok) y = lo_half ? (xv[e] * cv[e] - xpv[e] * sv[e]) : (xv[e] * cv[e] + xpv[e] * sv[e]);
+                if constexpr (REC) if (ok) a.dbg_q[((size_t)m * Hq + h) * D + d0 + e] = y;
+                y *= a.qscale;
+                hb[e] = kv_round<KVDT>(y);
+                rb[e] = kv_round<KVDT>(y - kv_float<KVDT>(hb[e]));
+            }
+#pragma unroll
+            for (int w2 = 0; w2 < 4; ++w2) {
+                qh[ib][w2] = (uint32_t)hb[2 * w2] | ((uint32_t)hb[2 * w2 + 1] << 16);
+                qr[ib][w2] = (uint32_t)rb[2 * w2] | ((uint32_t)rb[2 * w2 + 1] << 16);
+            }
+        }
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) o[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+
+    for (int st = 0; st < nsteps; ++st) {
+        const int buf = st % ATTN_NB;
+        if constexpr (REC) attn_vm<0>();                     // the record's stores share the load counter
+        else attn_vm<VMN>();                                 // this step's loads (later steps may stay in flight)
+        attn_barrier();                                      // every lane's loads of this step are in LDS
+        issue(st + ATTN_NB - 1);                             // into the buffer every wave finished with
+        const int x0 = st * AK;
+        if (j0 + x0 + AK > P && j0 + x0 < j1) {              // the step holds rows of this forward (uniform)
+            uint8_t* kb = &kvs[buf][0][0];
+#pragma unroll
+            for (int u = 0; u < AK * NCH / 256; ++u) {
+                const int q = tid + 256 * u, k = q / NCH, c = q % NCH;
+                const int j = j0 + x0 + k;
+                if (j < P || j >= j1) continue;
+                const int i = j - P;
+                const int m = rowbase + i;
+                const int pos = a.meta.positions[m];
+                const float* krow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + g) * D;
+                const float* vrow = a.qkv + (size_t)m * a.qkv_ld + (size_t)(Hq + Hkv + g) * D;
+                uint16_t kb8[8], vb8[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int d = 8 * c + e;
+                    const bool lo_half = d < HALF;
+                    const float xk = krow[d];
+                    const float xp = lo_half ? krow[d + HALF] : krow[d - HALF];
+                    const float2 cs = a.rope[(size_t)pos * HALF + (lo_half ? d : d - HALF)];
+                    const float y = lo_half ? (xk * cs.x - xp * cs.y) : (xk * cs.x + xp * cs.y);
+                    kb8[e] = kv_round<KVDT>(y);
+                    vb8[e] = kv_round<KVDT>(vrow[d]);
+                }
+                u32x4 kk, vv;
+#pragma unroll
+                for (int w2 = 0; w2 < 4; ++w2) {
+                    kk[w2] = (uint32_t)kb8[2 * w2] | ((uint32_t)kb8[2 * w2 + 1] << 16);
+                    vv[w2] = (uint32_t)vb8[2 * w2] | ((uint32_t)vb8[2 * w2 + 1] << 16);
+                }
+                if (!a.no_append) {                          // append: owner of row j writes it
+                    const size_t off = (((size_t)b * Hkv + g) * rq.cap + j) * D + 8 * c;
+                    *(u32x4*)(kl + off) = kk;
+                    *(u32x4*)(vl + off) = vv;
+                    if (a.layer == 0 && g == 0 && c == 0) rq.table[(size_t)b * rq.cap + j] = (int16_t)b;
+                }
+                if (smk[x0 + k] != 0) {                      // a kept row enters; a dropped one stays zero
+                    const int pos16 = 16 * (c ^ (k % NCH));
+                    *(u32x4*)(kb + k * RB + pos16) = kk;
+                    *(u32x4*)(kb + SB + k * RB + pos16) = vv;
+                }
+            }
+            attn_barrier();
+        }
+        if (active) {
+            const uint32_t kb_a = kvs_a + (uint32_t)(buf * 2 * SB), vb_a = kb_a + SB;
+            const int kbase = j0 + x0 + 4 * lg;
+            u32x4 kf0[DB], kf1[DB], vf[MB];
+#pragma unroll
+            for (int ib = 0; ib < DB; ++ib) {
+                const int c = 4 * ib + lg;
+                kf0[ib] = attn_lds16(kb_a + (uint32_t)(ql * RB + 16 * (c ^ (ql % NCH))));
+                kf1[ib] = attn_lds16(kb_a + (uint32_t)((16 + ql) * RB + 16 * (c ^ ((16 + ql) % NCH))));
+            }
+            // value fragments: read h gives keys 16 h + 4 lg + e; this lane supplies
+            // key 16 h + 4 lg + ql / 4, dims 16 mb + 4 (ql mod 4) .. + 3
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                u32x2 p0, p1;
+#pragma unroll
+                for (int hh = 0; hh < 2; ++hh) {
+                    const int key = 16 * hh + 4 * lg + (ql >> 2);
+                    const int d = 16 * mb + 4 * (ql & 3);
+                    const uint32_t ad = vb_a + (uint32_t)(key * RB + 16 * ((d >> 3) ^ (key % NCH)) + 2 * (d & 7));
+                    if (hh == 0) p0 = attn_lds_tr(ad);
+                    else p1 = attn_lds_tr(ad);
+                }
+                vf[mb] = u32x4{p0[0], p0[1], p1[0], p1[1]};
+            }
+            uint32_t w0 = attn_lds4(smk_a + (uint32_t)(x0 + 4 * lg));
+            uint32_t w1 = attn_lds4(smk_a + (uint32_t)(x0 + 16 + 4 * lg));
+            uint32_t r0 = ~0u, r1 = ~0u;                     // this query row's own mask bytes (all kept without)
+            if (rmask) {                                     // uniform branch
+                const uint32_t ra = (uint32_t)(uintptr_t)srm + (uint32_t)(min(qtok, n - 1) * rspan + x0 + 4 * lg);
+                r0 = attn_lds4(ra);
+                r1 = attn_lds4(ra + 16);
+            }
+            attn_lgkm();
+            touch_u(w0);
+            touch_u(w1);
+            touch_u(r0);
+            touch_u(r1);
+#pragma unroll
+            for (int ib = 0; ib < DB; ++ib) { touch_v(kf0[ib]); touch_v(kf1[ib]); }
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) touch_v(vf[mb]);
+            uint32_t vbits = 0u;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int ko = (e < 4) ? e : 12 + e;
+                const int sh = 8 * (e & 3);
+                const uint32_t byte = ((e < 4 ? w0 : w1) >> sh) & 0xFFu, rbyte = ((e < 4 ? r0 : r1) >> sh) & 0xFFu;
+                vbits |= ((kbase + ko < j1 && byte != 0u && rbyte != 0u) ? 1u : 0u) << e;
+            }
+            f32x4_t s0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+#pragma unroll
+            for (int ib = 0; ib < DB; ++ib) {
+                s0 = mma_kv<KVDT>(kf0[ib], qh[ib], s0);
+                s1 = mma_kv<KVDT>(kf1[ib], qh[ib], s1);
+                s0 = mma_kv<KVDT>(kf0[ib], qr[ib], s0);
+                s1 = mma_kv<KVDT>(kf1[ib], qr[ib], s1);
+            }
+            const int last = P + qtok - kbase;               // keys up to kbase + last are causal
+            float sv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int ko = (e < 4) ? e : 12 + e;
+                const float x = e < 4 ? s0[e] : s1[e - 4];
+                sv[e] = (((vbits >> e) & 1u) && ko <= last) ? x : -INFINITY;
+            }
+            if constexpr (REC) {                             // test support: this tile's visible scores
+                const int r = 16 * wave + ql;
+                if (r < R) {
+                    const size_t row = ((size_t)(rowbase + r / gs) * Hq + g * gs + r % gs) * a.dbg_keys;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int j = kbase + ((e < 4) ? e : 12 + e);
+                        if (sv[e] != -INFINITY && j < a.dbg_keys) a.dbg_logits[row + j] = sv[e] * 0.69314718055994531f;
+                    }
+                }
+            }
+            float mx = sv[0];
+#pragma unroll
+            for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
+            float x0f, x1f;
+            lane_pair_k(mx, 16, x0f, x1f);
+            mx = fmaxf(x0f, x1f);
+            lane_pair_k(mx, 32, x0f, x1f);
+            mx = fmaxf(x0f, x1f);
+            const float mn = fmaxf(mrun, mx);
+            // no key seen yet (mn = -inf): base 0 makes every term and the correction 0
+            const float base = mn == -INFINITY ? 0.f : mn;
+            const float corr = __builtin_amdgcn_exp2f(mrun - base);
+            float pv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pv[e] = __builtin_amdgcn_exp2f(sv[e] - base);
+            float ps = 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) ps += pv[e];
+            lsum = lsum * corr + ps;
+            mrun = mn;
+            u32x4 pb;
+#pragma unroll
+            for (int w2 = 0; w2 < 4; ++w2) pb[w2] = kv_pack2<KVDT>(pv[2 * w2], pv[2 * w2 + 1]);
+            if (__any(corr != 1.f)) {                        // the running maximum moved in some lane
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj) o[mb][jj] *= corr;
+            }
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) o[mb] = mma_kv<KVDT>(vf[mb], pb, o[mb]);
+        }
+    }
+    attn_vm<0>();                                            // no direct load may land after the workgroup ends
+
+    // ---- this split's partial of each query vector: (max, sum, unnormalized output)
+    if (active) {
+        float x0f, x1f, lt = lsum;
+        lane_pair_k(lt, 16, x0f, x1f);
+        lt = x0f + x1f;
+        lane_pair_k(lt, 32, x0f, x1f);
+        lt = x0f + x1f;
+        const int r = 16 * wave + ql;
+        if (r < R) {
+            const int i = r / gs, h = g * gs + (r % gs);
+            const int m = rowbase + i;
+            float* pp = a.part + (((size_t)m * Hq + h) * a.nsplit_max + split) * (D + 2);
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int jj = 0; jj < 4; ++jj) pp[2 + 16 * mb + 4 * lg + jj] = o[mb][jj];
+            if (lg == 0) {
+                pp[0] = mrun;
+                pp[1] = lt;
+            }
+        }
+    }
+}
+
 hipError_t launch_attention(const AttnArgs& a, int head_dim, int queries_per_item_max, hipStream_t st) {
     const dim3 grid(a.meta.n_items, a.Hkv, a.nsplit_max), block(256);
     const dim3 mgrid(a.meta.M, a.Hq);
     const bool wide = queries_per_item_max > 4;
     const bool bf = a.kv_dt == DT_BF16;
     const bool one = queries_per_item_max <= 64;                // every item's query tiles: one per wave
+    const bool dma = one && a.dma;
 #define ATTN_MMA_R(D_, R_)                                                                        \
     do {                                                                                          \
-        if (bf && one) attn_mma_kernel<D_, DT_BF16, 1, R_><<<grid, block, 0, st>>>(a);            \
+        if (bf && dma) attn_dma_kernel<D_, DT_BF16, R_><<<grid, block, 0, st>>>(a);               \
+        else if (!bf && dma) attn_dma_kernel<D_, DT_F16, R_><<<grid, block, 0, st>>>(a);          \
+        else if (bf && one) attn_mma_kernel<D_, DT_BF16, 1, R_><<<grid, block, 0, st>>>(a);       \
         else if (bf) attn_mma_kernel<D_, DT_BF16, 2, R_><<<grid, block, 0, st>>>(a);              \
         else if (one) attn_mma_kernel<D_, DT_F16, 1, R_><<<grid, block, 0, st>>>(a);              \
         else attn_mma_kernel<D_, DT_F16, 2, R_><<<grid, block, 0, st>>>(a);                       \

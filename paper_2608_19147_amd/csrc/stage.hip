@@ -151,6 +151,7 @@ struct Stage {
     unsigned ll_epoch = 0;                              // flag numbers used so far
     bool ps_coop = false;                               // cooperative launch (STAGE_COOP=1), else a plain launch
     int attn_vector = 0;                                // attention on the vector units (STAGE_ATTN_VECTOR=1)
+    bool attn_dma = true;                               // cache rows by direct loads where allowed (STAGE_ATTN_DMA=0: off)
     int gemm_min_rows = 1;                              // rows from which products use the matrix cores (STAGE_GEMM_MIN_ROWS)
     unsigned long long* trace = nullptr;   // phase stamps of the last persistent forward (STAGE_PS_TRACE=1)
     int prof_class = -1;
@@ -530,6 +531,7 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
     }
     if (const char* e = std::getenv("STAGE_GEMM_MIN_ROWS")) st->gemm_min_rows = std::max(1, atoi(e));
     if (const char* e = std::getenv("STAGE_ATTN_VECTOR")) st->attn_vector = atoi(e) != 0;
+    if (const char* e = std::getenv("STAGE_ATTN_DMA")) st->attn_dma = atoi(e) != 0;
     for (int l = 0; l < c.n_layers; ++l) {
         LayerDev& L = st->layers[l];
         const LayerWeights& w = layers[l];
@@ -1658,6 +1660,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
     uint8_t* masks = hb + off_mask;
     std::vector<int> beam_off(n_req, -1);
     std::vector<bool> do_gather(n_req, false);
+    bool attn_dma_ok = st->attn_dma;
     {
         int row = 0, item = 0;
         size_t moff = 0, boff = 0;
@@ -1690,6 +1693,16 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             d.splits = std::max(1, std::min(ATTN_MAX_SPLITS, 2 * st->n_cus / (S * Hkv)));
             if (const char* e = std::getenv("STAGE_ATTN_SPLITS")) d.splits = std::max(1, std::min(ATTN_MAX_SPLITS, atoi(e)));
             max_splits = std::max(max_splits, d.splits);
+            {                                            // the direct-load attention stages a whole split's table
+                const int Lr = d.P + n;
+                int sl = std::max(ATTN_MIN_SPLIT, (Lr + d.splits - 1) / d.splits);
+                sl = (sl + KGROUPS - 1) / KGROUPS * KGROUPS;
+                // and addresses one layer of the cache through a buffer resource (32-bit offsets)
+                const size_t layer_bytes = (size_t)S * Hkv * kv->cap * c.head_dim * 2;
+                // and the split's rows of a per-query-row mask (n rows x split keys, at most 8 KB)
+                const bool rows_fit = !q.attention_mask_rows || (size_t)n * ((sl + 3) / 4 * 4) <= 8192;
+                if (sl > 1024 || !rows_fit || layer_bytes > 0xFFFFFFF0ull) attn_dma_ok = false;
+            }
             d.kc = kv->kc;
             d.vc = kv->vc;
             d.table = kv->table[do_gather[r] ? 1 - kv->cur : kv->cur];
@@ -1932,6 +1945,7 @@ int stage_forward(Stage* st, const StageRequest* reqs, int n_req, const void* hi
             // and is the stride of the partials
             a.nsplit_max = max_splits;
             a.vector_path = st->attn_vector;
+            a.dma = attn_dma_ok ? 1 : 0;
             if (l == st->dbg_layer && !st->attn_vector) {    // test support: record this layer's queries and scores
                 HIP_TRY(launch_fill_u32((uint32_t*)st->dbg_logits, (size_t)M * Hq * st->dbg_keys, 0xFFFFFFFFu, s));   // NaN
                 a.dbg_q = st->dbg_q;

@@ -1,8 +1,9 @@
 """The forms of the per-layer kernels that the default configuration does not
 pick, against the fp64 oracle: the VALU attention (STAGE_ATTN_VECTOR=1), the
-one-row product for several rows (STAGE_GEMM_MIN_ROWS above the row count),
-and a stage with 64-wide quantization groups, whose products all take the
-one-row form.  Each runs a micro-batch of verify and decode requests with
+matrix-core attention with cache rows staged through registers
+(STAGE_ATTN_DMA=0), the one-row product for several rows (STAGE_GEMM_MIN_ROWS
+above the row count), and a stage with 64-wide quantization groups, whose
+products all take the one-row form.  Each runs a micro-batch of verify and decode requests with
 holes and a 5-token verify whose last drafts are masked."""
 import dataclasses
 import os
@@ -69,7 +70,8 @@ def _masked_verify(p, seed):
     (TINY2, {"STAGE_ATTN_VECTOR": "1"}),
     (TINY2, {"STAGE_GEMM_MIN_ROWS": "65"}),
     (TINY_G64, {}),
-], ids=["vector-attention", "one-row-products", "group-64"])
+    (TINY2, {"STAGE_ATTN_DMA": "0"}),
+], ids=["vector-attention", "one-row-products", "group-64", "register-staged-attention"])
 def test_alternate_forms_vs_oracle(shape, env):
     p = _pair(shape, 61, env)
     _microbatch(p, 61)
