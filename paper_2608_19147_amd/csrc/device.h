@@ -30,6 +30,25 @@ __device__ __forceinline__ float load_val(const void* p, int dt, size_t i) {
     return dt == DT_BF16 ? bf16_to_f32(b) : f16_to_f32(b);
 }
 
+// N values at element offsets off[i] of p (dtype dt, the same in every lane),
+// every load issued before any is converted: the dtype branch sits outside the
+// loads (a branch per value makes each load wait for the one before).
+template <int N>
+__device__ __forceinline__ void load_vals(const void* p, int dt, const size_t (&off)[N], float (&out)[N]) {
+    if (dt == DT_F32) {
+        const float* f = (const float*)p;
+#pragma unroll
+        for (int i = 0; i < N; ++i) out[i] = f[off[i]];
+    } else {
+        const uint16_t* h = (const uint16_t*)p;
+        uint16_t bits[N];
+#pragma unroll
+        for (int i = 0; i < N; ++i) bits[i] = h[off[i]];
+#pragma unroll
+        for (int i = 0; i < N; ++i) out[i] = dt == DT_BF16 ? bf16_to_f32(bits[i]) : f16_to_f32(bits[i]);
+    }
+}
+
 __device__ __forceinline__ uint16_t to_half_bits(float f, int dt) { return dt == DT_BF16 ? f32_to_bf16(f) : f32_to_f16(f); }
 __device__ __forceinline__ float half_bits_to_f32(uint16_t b, int dt) { return dt == DT_BF16 ? bf16_to_f32(b) : f16_to_f32(b); }
 

@@ -494,21 +494,18 @@ __global__ __launch_bounds__(256) void bprep_kernel(const void* in, int in_dt, i
     __shared__ float red[4];
     const int m = blockIdx.x, tid = threadIdx.x, k0 = BPREP_SLICE * blockIdx.y;
     float v[NPT], xs[SPT], gs[SPT];
+    size_t off[NPT], offs[SPT];                          // every load issued before any is used (clamped, then dropped)
 #pragma unroll
-    for (int i = 0; i < NPT; ++i) {                      // every load issued before any is used (clamped, then dropped)
-        const int k = tid + 256 * i;
-        const float x = load_val(in, in_dt, (size_t)m * in_ld + min(k, K - 1));
-        v[i] = k < K ? x : 0.f;
-    }
+    for (int i = 0; i < NPT; ++i) off[i] = (size_t)m * in_ld + min(tid + 256 * i, K - 1);
 #pragma unroll
-    for (int i = 0; i < SPT; ++i) {
-        const int k = min(k0 + tid + 256 * i, K - 1);
-        xs[i] = load_val(in, in_dt, (size_t)m * in_ld + k);
-        gs[i] = half_bits_to_f32(gamma[k], gamma_dt);
-    }
+    for (int i = 0; i < SPT; ++i) offs[i] = (size_t)m * in_ld + min(k0 + tid + 256 * i, K - 1);
+    load_vals(in, in_dt, off, v);
+    load_vals(in, in_dt, offs, xs);
+#pragma unroll
+    for (int i = 0; i < SPT; ++i) gs[i] = half_bits_to_f32(gamma[min(k0 + tid + 256 * i, K - 1)], gamma_dt);
     float ss = 0.f;
 #pragma unroll
-    for (int i = 0; i < NPT; ++i) ss += v[i] * v[i];
+    for (int i = 0; i < NPT; ++i) ss += tid + 256 * i < K ? v[i] * v[i] : 0.f;
     ss = wave_sum_all(ss);
     if ((tid & 63) == 0) red[tid >> 6] = ss;
     __syncthreads();
@@ -521,27 +518,50 @@ __global__ __launch_bounds__(256) void bprep_kernel(const void* in, int in_dt, i
     if (blockIdx.y == 0 && tid == 0) rs_out[m] = rs;
 }
 
+// Inputs of the row factors: the first 32 of this thread's quarter of row m's
+// sums of squares (4 threads per row; loads clamped, then dropped past cnt),
+// issued early so that they fly with the first group's loads.
+struct RowFactorLoads {
+    float v[32];
+    float cb;
+    int cnt;
+    const float* src;
+};
+__device__ __forceinline__ void row_factor_loads(const GemvArgs& a, RowFactorLoads& r) {
+    const int tid = threadIdx.x, m = tid >> 2, part = tid & 3;
+    r.cb = 1.f;
+    r.cnt = 0;
+    r.src = a.ssq_in;
+    if (a.norm == 1 && m < a.M) {
+        r.cb = a.cb_in[m];
+        const int per = (a.ssq_tiles + 3) / 4;
+        r.src = a.ssq_in + (size_t)m * a.ssq_tiles + part * per;
+        r.cnt = max(0, min(per, a.ssq_tiles - part * per));
+        if (r.cnt > 0) {
+#pragma unroll
+            for (int e = 0; e < 32; ++e) r.v[e] = r.src[min(e, r.cnt - 1)];
+        }
+    }
+}
+
 // Factor of every row m < 64 of a product's results into fs (1 unless the
 // input is a deferred RMSNorm: then rs / c, rs from the row's sums of squares,
-// which 4 threads per row add (each a quarter of the partials, all loads in
-// flight) and combine in a fixed order); with write_rs, rs also goes to
-// a.rs_out.  Ends with a workgroup barrier.
-__device__ __forceinline__ void row_factors(const GemvArgs& a, int K, bool write_rs, float* fs) {
+// added by 4 threads per row in index order and combined in a fixed order);
+// with write_rs, rs also goes to a.rs_out.  No barrier: fs is read after the
+// workgroup's next one.
+__device__ __forceinline__ void row_factors_finish(const GemvArgs& a, int K, bool write_rs, const RowFactorLoads& r,
+                                                   float* fs) {
     const int tid = threadIdx.x, m = tid >> 2, part = tid & 3;
-    float ss = 0.f, cb = 1.f;
+    float ss = 0.f;
     if (a.norm == 1 && m < a.M) {
-        cb = a.cb_in[m];
-        const int per = (a.ssq_tiles + 3) / 4;
-        const float* src = a.ssq_in + (size_t)m * a.ssq_tiles + part * per;
-        const int cnt = max(0, min(per, a.ssq_tiles - part * per));
-        // 32 partials per pass, all loads issued before any is added (clamped, then
-        // dropped past cnt), added in index order
-        for (int tt = 0; tt < cnt; tt += 32) {
+#pragma unroll
+        for (int e = 0; e < 32; ++e) ss += (e < r.cnt) ? r.v[e] : 0.f;
+        for (int tt = 32; tt < r.cnt; tt += 32) {             // more than 128 partials per row
             float v[32];
 #pragma unroll
-            for (int e = 0; e < 32; ++e) v[e] = src[min(tt + e, cnt - 1)];
+            for (int e = 0; e < 32; ++e) v[e] = r.src[min(tt + e, r.cnt - 1)];
 #pragma unroll
-            for (int e = 0; e < 32; ++e) ss += (tt + e < cnt) ? v[e] : 0.f;
+            for (int e = 0; e < 32; ++e) ss += (tt + e < r.cnt) ? v[e] : 0.f;
         }
     }
     ss += dpp_f<0xB1>(ss);                                    // lane ^ 1
@@ -550,12 +570,11 @@ __device__ __forceinline__ void row_factors(const GemvArgs& a, int K, bool write
         float f = 1.f;
         if (a.norm == 1 && m < a.M) {
             const float rs = rsqrtf(ss / (float)K + a.eps);
-            f = rs / cb;
+            f = rs / r.cb;
             if (write_rs && a.rs_out) a.rs_out[m] = rs;
         }
         fs[m] = f;
     }
-    __syncthreads();
 }
 
 // Product of the prepared input with one matrix: a workgroup's 4 waves take
@@ -690,10 +709,6 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
         q = min(q, n - 1) + rot;
         return g0 + (q >= n ? q - n : q);
     };
-    if (n > 0) {
-        ldw(G(0), wr[0], sr[0]);
-        ldb(G(0), br[0], cr[0]);
-    }
     // With 17 or more rows the residual epilogue's inputs (the tile's residual
     // rows, the next norm's weights and the rows' rs) are read now by every split
     // of the tile, off the last split's tail; the residual is rewritten only by
@@ -701,19 +716,33 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
     // added start latency outweighs the shorter tail: measured.)
     constexpr bool PRE = NCB >= 2;
     const bool resid_epi = PRE && a.epi == EPI_RESID;
-    float pres[NV], pgam = 0.f, prs = 0.f;
+    float pres[NV], prs = 0.f;
+    uint16_t pgam_bits = 0;
     if (resid_epi) {
+        size_t off[NV];                                  // clamped to a valid element; outside rows are never used
 #pragma unroll
         for (int q = 0; q < NV; ++q) {
-            const int idx = tid + 256 * q, m = idx >> 6, n = t * 64 + (idx & 63);
-            pres[q] = (m < M && n < W.n) ? load_val(a.resid, a.resid_dt, (size_t)m * a.resid_ld + n) : 0.f;
+            const int idx = tid + 256 * q, m = min(idx >> 6, M - 1), n = min(t * 64 + (idx & 63), W.n - 1);
+            off[q] = (size_t)m * a.resid_ld + n;
         }
-        if (a.bp_out && tid < 64 && t * 64 + tid < W.n) pgam = half_bits_to_f32(a.gamma_next[t * 64 + tid], a.gamma_next_dt);
-        if (a.bp_out && tid < M) prs = a.rs_in[tid];
+        load_vals(a.resid, a.resid_dt, off, pres);
+        if (a.bp_out) {                                  // raw now, converted once every load is out
+            pgam_bits = a.gamma_next[min(t * 64 + (tid & 63), W.n - 1)];
+            prs = a.rs_in[min(tid, M - 1)];
+        }
     }
-    // factor of each row (rs / c for a deferred RMSNorm input, else 1): its inputs
-    // come from the kernel before, so its loads fly with the first group's
-    row_factors(a, K, t == 0 && s == 0, fs);
+    // factor of each row (rs / c for a deferred RMSNorm input, else 1): its
+    // inputs come from the kernel before; they and the epilogue's inputs are
+    // issued before the first group's loads, so nothing below waits for those
+    RowFactorLoads rfl;
+    row_factor_loads(a, rfl);
+    __builtin_amdgcn_sched_barrier(0);
+    if (n > 0) {
+        ldw(G(0), wr[0], sr[0]);
+        ldb(G(0), br[0], cr[0]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    row_factors_finish(a, K, t == 0 && s == 0, rfl, fs);
     if constexpr (PRE) {
         if (resid_epi) {
 #pragma unroll
@@ -721,7 +750,7 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
                 const int idx = tid + 256 * q;
                 sres[idx >> 6][idx & 63] = pres[q];
             }
-            if (tid < 64) sgam[tid] = pgam;
+            if (tid < 64) sgam[tid] = half_bits_to_f32(pgam_bits, a.gamma_next_dt);
             if (tid < MP) srs[tid] = prs;
         }
     }
@@ -802,6 +831,23 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
             }
         }
     } else if (a.epi == EPI_RESID) {
+        // the residual rows, the next norm's weights and the rows' rs (read at the
+        // start with 17 or more rows), every load issued before any is used
+        float xres[NV], egam[NV], ers[NV];
+        if constexpr (!PRE) {
+            size_t off[NV];
+            uint16_t gbits[NV];
+#pragma unroll
+            for (int q = 0; q < NV; ++q) {
+                const int idx = tid + 256 * q, m = min(idx >> 6, M - 1), n = min(t * 64 + (idx & 63), W.n - 1);
+                off[q] = (size_t)m * a.resid_ld + n;
+                gbits[q] = a.bp_out ? a.gamma_next[n] : (uint16_t)0;
+                ers[q] = a.bp_out ? a.rs_in[m] : 0.f;
+            }
+            load_vals(a.resid, a.resid_dt, off, xres);
+#pragma unroll
+            for (int q = 0; q < NV; ++q) egam[q] = half_bits_to_f32(gbits[q], a.gamma_next_dt);
+        }
 #pragma unroll
         for (int q = 0; q < NV; ++q) {
             const int idx = tid + 256 * q;
@@ -812,7 +858,7 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
             if (ok) {
                 float xr;
                 if constexpr (PRE) xr = sres[m][r];
-                else xr = load_val(a.resid, a.resid_dt, (size_t)m * a.resid_ld + n);
+                else xr = xres[q];
                 xn = xr + vals[q] * fs[m];
                 a.out[(size_t)m * a.out_ld + n] = xn;
                 if (a.out_act) ((uint16_t*)a.out_act)[(size_t)m * a.out_act_ld + n] = to_half_bits(xn, a.out_act_dt);
@@ -826,8 +872,8 @@ __global__ __launch_bounds__(256, NCB <= 2 ? 2 : 1) void gemm_bp_kernel(GemvArgs
                     c = srs[m];
                     gm = sgam[r];
                 } else {
-                    c = a.rs_in[m];
-                    gm = half_bits_to_f32(a.gamma_next[n], a.gamma_next_dt);
+                    c = ers[q];
+                    gm = egam[q];
                 }
                 const float h = ok ? xn * gm * c : 0.f;
                 bp_put(a.bp_out, a.bc_out, a.kp, m, n, h, ok);
