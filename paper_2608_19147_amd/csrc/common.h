@@ -114,7 +114,7 @@ struct AttnArgs {
     uint16_t* bp_out; float* bc_out; int kp;   // the attention output also in prepared form (o product input, 64-row blocks)
     int no_append;           // the rows of this forward are already in the cache (prefill): do not write them
     int dma;                 // 1: cache rows by direct loads (attn_dma_kernel) where the launch allows it: every
-                             // split at most 1024 keys, per-row masks of at most 8 KB per split, at most 64
+                             // split at most 1024 keys, per-row masks of at most 8 KB per split, at most 256
                              // query vectors per kv head
     // test support (null unless armed): the rotated queries [M][Hq][D] and the
     // scores q.k / sqrt(D) of every visible key [M][Hq][dbg_keys]

@@ -1847,11 +1847,11 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_mma_kernel(AttnArg
 
 // ------------------------------------------------------------------ matrix-core attention, cache rows by direct loads
 //
-// attn_mma_kernel for items of at most 64 query vectors per kv head (one tile
-// per wave), with the same split, step order, arithmetic and partials (results
-// are bitwise equal), but with the cache rows of each 32-key step brought into
-// LDS by direct-to-LDS buffer loads issued ATTN_NB - 1 steps ahead instead of
-// through registers one step ahead.  A key the split does not keep (masked,
+// attn_mma_kernel for items of at most 256 query vectors per kv head (up to four
+// tiles per wave), with the same split, step order, arithmetic and partials
+// (results are bitwise equal), but with the cache rows of each 32-key step
+// brought into LDS by direct-to-LDS buffer loads issued ATTN_NB - 1 steps ahead
+// instead of through registers one step ahead.  A key the split does not keep (masked,
 // past the split, or a row of this forward, which is written in afterwards)
 // is read at an offset past the buffer's end, which the hardware answers with
 // zeros without a memory access.  K and V are stored as in memory, 16-byte
@@ -1908,8 +1908,10 @@ template <int N>
 __device__ __forceinline__ void attn_vm() { asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory"); }
 __device__ __forceinline__ void attn_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-template <int D, int KVDT, bool REC = false>
-__global__ __launch_bounds__(256, 2) void attn_dma_kernel(AttnArgs a) {
+// QTW: query tiles of 16 vectors per wave (1, 2 or 4; tile wave + 4 u); with
+// more than one, one workgroup per CU holds their registers.
+template <int D, int KVDT, int QTW, bool REC = false>
+__global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_dma_kernel(AttnArgs a) {
     constexpr int HALF = D / 2;
     constexpr int NCH = D / 8;               // 16-byte chunks per cache row
     constexpr int DB = D / 32;               // k-blocks of the score products
@@ -2001,19 +2003,22 @@ __global__ __launch_bounds__(256, 2) void attn_dma_kernel(AttnArgs a) {
 #pragma unroll
     for (int s = 0; s < ATTN_NB - 1; ++s) issue(s);
 
-    // ---- this wave's query tile: rotated, scaled, split into rounded part and residual
+    // ---- this wave's query tiles: rotated, scaled, split into rounded part and residual
     const bool active = wave < nqt;
-    u32x4 qh[DB], qr[DB];
-    int qtok;
-    float mrun = -INFINITY, lsum = 0.f;
-    f32x4_t o[MB];
-    {
-        const int r = 16 * wave + ql;
-        const bool ok = active && r < R;
+    u32x4 qh[QTW][DB], qr[QTW][DB];
+    int qtok[QTW];
+    float mrun[QTW], lsum[QTW];
+    f32x4_t o[QTW][MB];
+#pragma unroll
+    for (int u = 0; u < QTW; ++u) {
+        const int r = 16 * (wave + 4 * u) + ql;
+        const bool ok = wave + 4 * u < nqt && r < R;
         const int i = ok ? r / gs : 0, h = g * gs + (ok ? r % gs : 0);
         const int m = rowbase + i;
         const float* qrow = a.qkv + (size_t)m * a.qkv_ld + (size_t)h * D;
-        qtok = ok ? i : n;
+        qtok[u] = ok ? i : n;
+        mrun[u] = -INFINITY;
+        lsum[u] = 0.f;
         // every load of the tile at once (row 0 of the item stands in for a missing
         // row): q and its rotary partners, then (cos, sin) at the row's position
         float4 qa[DB][2], qp[DB][2], rc[DB][4];
@@ -2064,12 +2069,12 @@ __global__ __launch_bounds__(256, 2) void attn_dma_kernel(AttnArgs a) {
             }
 #pragma unroll
             for (int w2 = 0; w2 < 4; ++w2) {
-                qh[ib][w2] = (uint32_t)hb[2 * w2] | ((uint32_t)hb[2 * w2 + 1] << 16);
-                qr[ib][w2] = (uint32_t)rb[2 * w2] | ((uint32_t)rb[2 * w2 + 1] << 16);
+                qh[u][ib][w2] = (uint32_t)hb[2 * w2] | ((uint32_t)hb[2 * w2 + 1] << 16);
+                qr[u][ib][w2] = (uint32_t)rb[2 * w2] | ((uint32_t)rb[2 * w2 + 1] << 16);
             }
         }
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) o[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int mb = 0; mb < MB; ++mb) o[u][mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
 
     for (int st = 0; st < nsteps; ++st) {
@@ -2150,99 +2155,107 @@ __global__ __launch_bounds__(256, 2) void attn_dma_kernel(AttnArgs a) {
             }
             uint32_t w0 = attn_lds4(smk_a + (uint32_t)(x0 + 4 * lg));
             uint32_t w1 = attn_lds4(smk_a + (uint32_t)(x0 + 16 + 4 * lg));
-            uint32_t r0 = ~0u, r1 = ~0u;                     // this query row's own mask bytes (all kept without)
-            if (rmask) {                                     // uniform branch
-                const uint32_t ra = (uint32_t)(uintptr_t)srm + (uint32_t)(min(qtok, n - 1) * rspan + x0 + 4 * lg);
-                r0 = attn_lds4(ra);
-                r1 = attn_lds4(ra + 16);
-            }
             attn_lgkm();
             touch_u(w0);
             touch_u(w1);
-            touch_u(r0);
-            touch_u(r1);
 #pragma unroll
             for (int ib = 0; ib < DB; ++ib) { touch_v(kf0[ib]); touch_v(kf1[ib]); }
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) touch_v(vf[mb]);
-            uint32_t vbits = 0u;
+            uint32_t vb0 = 0u;                               // keys of the step this split keeps
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int ko = (e < 4) ? e : 12 + e;
-                const int sh = 8 * (e & 3);
-                const uint32_t byte = ((e < 4 ? w0 : w1) >> sh) & 0xFFu, rbyte = ((e < 4 ? r0 : r1) >> sh) & 0xFFu;
-                vbits |= ((kbase + ko < j1 && byte != 0u && rbyte != 0u) ? 1u : 0u) << e;
+                const uint32_t byte = ((e < 4 ? w0 : w1) >> (8 * (e & 3))) & 0xFFu;
+                vb0 |= ((kbase + ko < j1 && byte != 0u) ? 1u : 0u) << e;
             }
-            f32x4_t s0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, s1 = s0;
 #pragma unroll
-            for (int ib = 0; ib < DB; ++ib) {
-                s0 = mma_kv<KVDT>(kf0[ib], qh[ib], s0);
-                s1 = mma_kv<KVDT>(kf1[ib], qh[ib], s1);
-                s0 = mma_kv<KVDT>(kf0[ib], qr[ib], s0);
-                s1 = mma_kv<KVDT>(kf1[ib], qr[ib], s1);
-            }
-            const int last = P + qtok - kbase;               // keys up to kbase + last are causal
-            float sv[8];
+            for (int u = 0; u < QTW; ++u) {
+                if (wave + 4 * u >= nqt) continue;           // wave-uniform
+                uint32_t vbits = vb0;
+                if (rmask) {                                 // this query row's own mask bytes (uniform branch)
+                    const uint32_t ra = (uint32_t)(uintptr_t)srm + (uint32_t)(min(qtok[u], n - 1) * rspan + x0 + 4 * lg);
+                    uint32_t r0 = attn_lds4(ra), r1 = attn_lds4(ra + 16);
+                    attn_lgkm();
+                    touch_u(r0);
+                    touch_u(r1);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int ko = (e < 4) ? e : 12 + e;
-                const float x = e < 4 ? s0[e] : s1[e - 4];
-                sv[e] = (((vbits >> e) & 1u) && ko <= last) ? x : -INFINITY;
-            }
-            if constexpr (REC) {                             // test support: this tile's visible scores
-                const int r = 16 * wave + ql;
-                if (r < R) {
-                    const size_t row = ((size_t)(rowbase + r / gs) * Hq + g * gs + r % gs) * a.dbg_keys;
+                    for (int e = 0; e < 8; ++e)
+                        if ((((e < 4 ? r0 : r1) >> (8 * (e & 3))) & 0xFFu) == 0u) vbits &= ~(1u << e);
+                }
+                f32x4_t s0 = f32x4_t{0.f, 0.f, 0.f, 0.f}, s1 = s0;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int j = kbase + ((e < 4) ? e : 12 + e);
-                        if (sv[e] != -INFINITY && j < a.dbg_keys) a.dbg_logits[row + j] = sv[e] * 0.69314718055994531f;
+                for (int ib = 0; ib < DB; ++ib) {
+                    s0 = mma_kv<KVDT>(kf0[ib], qh[u][ib], s0);
+                    s1 = mma_kv<KVDT>(kf1[ib], qh[u][ib], s1);
+                    s0 = mma_kv<KVDT>(kf0[ib], qr[u][ib], s0);
+                    s1 = mma_kv<KVDT>(kf1[ib], qr[u][ib], s1);
+                }
+                const int last = P + qtok[u] - kbase;        // keys up to kbase + last are causal
+                float sv[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int ko = (e < 4) ? e : 12 + e;
+                    const float x = e < 4 ? s0[e] : s1[e - 4];
+                    sv[e] = (((vbits >> e) & 1u) && ko <= last) ? x : -INFINITY;
+                }
+                if constexpr (REC) {                         // test support: this tile's visible scores
+                    const int r = 16 * (wave + 4 * u) + ql;
+                    if (r < R) {
+                        const size_t row = ((size_t)(rowbase + r / gs) * Hq + g * gs + r % gs) * a.dbg_keys;
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const int j = kbase + ((e < 4) ? e : 12 + e);
+                            if (sv[e] != -INFINITY && j < a.dbg_keys) a.dbg_logits[row + j] = sv[e] * 0.69314718055994531f;
+                        }
                     }
                 }
+                float mx = sv[0];
+#pragma unroll
+                for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
+                float x0f, x1f;
+                lane_pair_k(mx, 16, x0f, x1f);
+                mx = fmaxf(x0f, x1f);
+                lane_pair_k(mx, 32, x0f, x1f);
+                mx = fmaxf(x0f, x1f);
+                const float mn = fmaxf(mrun[u], mx);
+                // no key seen yet (mn = -inf): base 0 makes every term and the correction 0
+                const float base = mn == -INFINITY ? 0.f : mn;
+                const float corr = __builtin_amdgcn_exp2f(mrun[u] - base);
+                float pv[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) pv[e] = __builtin_amdgcn_exp2f(sv[e] - base);
+                float ps = 0.f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) ps += pv[e];
+                lsum[u] = lsum[u] * corr + ps;
+                mrun[u] = mn;
+                u32x4 pb;
+#pragma unroll
+                for (int w2 = 0; w2 < 4; ++w2) pb[w2] = kv_pack2<KVDT>(pv[2 * w2], pv[2 * w2 + 1]);
+                if (__any(corr != 1.f)) {                    // the running maximum moved in some lane
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                        for (int jj = 0; jj < 4; ++jj) o[u][mb][jj] *= corr;
+                }
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) o[u][mb] = mma_kv<KVDT>(vf[mb], pb, o[u][mb]);
             }
-            float mx = sv[0];
-#pragma unroll
-            for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
-            float x0f, x1f;
-            lane_pair_k(mx, 16, x0f, x1f);
-            mx = fmaxf(x0f, x1f);
-            lane_pair_k(mx, 32, x0f, x1f);
-            mx = fmaxf(x0f, x1f);
-            const float mn = fmaxf(mrun, mx);
-            // no key seen yet (mn = -inf): base 0 makes every term and the correction 0
-            const float base = mn == -INFINITY ? 0.f : mn;
-            const float corr = __builtin_amdgcn_exp2f(mrun - base);
-            float pv[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) pv[e] = __builtin_amdgcn_exp2f(sv[e] - base);
-            float ps = 0.f;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) ps += pv[e];
-            lsum = lsum * corr + ps;
-            mrun = mn;
-            u32x4 pb;
-#pragma unroll
-            for (int w2 = 0; w2 < 4; ++w2) pb[w2] = kv_pack2<KVDT>(pv[2 * w2], pv[2 * w2 + 1]);
-            if (__any(corr != 1.f)) {                        // the running maximum moved in some lane
-#pragma unroll
-                for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-                    for (int jj = 0; jj < 4; ++jj) o[mb][jj] *= corr;
-            }
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) o[mb] = mma_kv<KVDT>(vf[mb], pb, o[mb]);
         }
     }
     attn_vm<0>();                                            // no direct load may land after the workgroup ends
 
     // ---- this split's partial of each query vector: (max, sum, unnormalized output)
-    if (active) {
-        float x0f, x1f, lt = lsum;
+#pragma unroll
+    for (int u = 0; u < QTW; ++u) {
+        if (wave + 4 * u >= nqt) continue;
+        float x0f, x1f, lt = lsum[u];
         lane_pair_k(lt, 16, x0f, x1f);
         lt = x0f + x1f;
         lane_pair_k(lt, 32, x0f, x1f);
         lt = x0f + x1f;
-        const int r = 16 * wave + ql;
+        const int r = 16 * (wave + 4 * u) + ql;
         if (r < R) {
             const int i = r / gs, h = g * gs + (r % gs);
             const int m = rowbase + i;
@@ -2250,9 +2263,9 @@ __global__ __launch_bounds__(256, 2) void attn_dma_kernel(AttnArgs a) {
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-                for (int jj = 0; jj < 4; ++jj) pp[2 + 16 * mb + 4 * lg + jj] = o[mb][jj];
+                for (int jj = 0; jj < 4; ++jj) pp[2 + 16 * mb + 4 * lg + jj] = o[u][mb][jj];
             if (lg == 0) {
-                pp[0] = mrun;
+                pp[0] = mrun[u];
                 pp[1] = lt;
             }
         }
@@ -2265,11 +2278,18 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int queries_per_ite
     const bool wide = queries_per_item_max > 4;
     const bool bf = a.kv_dt == DT_BF16;
     const bool one = queries_per_item_max <= 64;                // every item's query tiles: one per wave
-    const bool dma = one && a.dma;
+    // the direct-load form takes up to four tiles per wave (256 query vectors per kv head)
+    const int dq = !a.dma || queries_per_item_max > 256 ? 0 : one ? 1 : queries_per_item_max <= 128 ? 2 : 4;
+#define ATTN_DMA_Q(D_, T_, R_)                                                                    \
+    do {                                                                                          \
+        if (bf) attn_dma_kernel<D_, DT_BF16, T_, R_><<<grid, block, 0, st>>>(a);                  \
+        else attn_dma_kernel<D_, DT_F16, T_, R_><<<grid, block, 0, st>>>(a);                      \
+    } while (0)
 #define ATTN_MMA_R(D_, R_)                                                                        \
     do {                                                                                          \
-        if (bf && dma) attn_dma_kernel<D_, DT_BF16, R_><<<grid, block, 0, st>>>(a);               \
-        else if (!bf && dma) attn_dma_kernel<D_, DT_F16, R_><<<grid, block, 0, st>>>(a);          \
+        if (dq == 1) ATTN_DMA_Q(D_, 1, R_);                                                       \
+        else if (dq == 2) ATTN_DMA_Q(D_, 2, R_);                                                  \
+        else if (dq == 4) ATTN_DMA_Q(D_, 4, R_);                                                  \
         else if (bf && one) attn_mma_kernel<D_, DT_BF16, 1, R_><<<grid, block, 0, st>>>(a);       \
         else if (bf) attn_mma_kernel<D_, DT_BF16, 2, R_><<<grid, block, 0, st>>>(a);              \
         else if (one) attn_mma_kernel<D_, DT_F16, 1, R_><<<grid, block, 0, st>>>(a);              \
@@ -2295,6 +2315,7 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int queries_per_ite
     }
 #undef ATTN_MMA
 #undef ATTN_MMA_R
+#undef ATTN_DMA_Q
     return hipGetLastError();
 }
 

@@ -1334,15 +1334,20 @@ int stage_prefill(Stage* st, KVState* kv, int n, const int32_t* positions, const
         st->pf_rows = wrows;
     }
 
-    // ---------------- one request record per chunk of at most MAX_ROWS rows (the
-    // attention's unit), in one upload: chunk q covers prompt rows [64 q, 64 q + m),
+    // ---------------- one request record per chunk of at most PF_ATT_ROWS rows (the
+    // attention's unit), in one upload: chunk q covers prompt rows [16 q, 16 q + m),
     // sees the past rows the mask keeps, the earlier chunks' rows and its own rows
     // causally.  Row numbers (row0, positions, row_item) count from the start of
-    // the chunk's pass.
-    const int nch = (n + MAX_ROWS - 1) / MAX_ROWS;
-    const int pass_chunks = PF_ROWS / MAX_ROWS;
+    // the chunk's pass.  16-row chunks keep a chunk's query vectors (16 x query
+    // heads per kv head) within one or two tiles per wave, so the attention runs
+    // two workgroups per CU without spilling; the chunks of one context read the
+    // same cache rows, mostly from the caches.
+    constexpr int PF_ATT_ROWS = 16;
+    const int nch = (n + PF_ATT_ROWS - 1) / PF_ATT_ROWS;
+    const int pass_chunks = PF_ROWS / PF_ATT_ROWS;
     size_t mask_total = 0;
-    for (int q = 0; q < nch; ++q) mask_total += (size_t)P0 + q * MAX_ROWS + std::min(MAX_ROWS, n - q * MAX_ROWS);
+    for (int q = 0; q < nch; ++q)
+        mask_total += (size_t)P0 + q * PF_ATT_ROWS + std::min(PF_ATT_ROWS, n - q * PF_ATT_ROWS);
     const size_t off_req = 0;
     const size_t off_item = align16(off_req + sizeof(ReqDev) * nch);
     const size_t off_pos = align16(off_item + sizeof(ItemDev) * nch);
@@ -1359,13 +1364,13 @@ int stage_prefill(Stage* st, KVState* kv, int n, const int32_t* positions, const
     {
         size_t moff = 0;
         for (int q = 0; q < nch; ++q) {
-            const int r0 = q * MAX_ROWS, m = std::min(MAX_ROWS, n - r0);
+            const int r0 = q * PF_ATT_ROWS, m = std::min(PF_ATT_ROWS, n - r0);
             const int qf = q / pass_chunks * pass_chunks;   // first chunk of the pass
             ReqDev d{};
             d.P = P0 + r0;
             d.n = m;
             d.S = 1;
-            d.row0 = (q - qf) * MAX_ROWS;
+            d.row0 = (q - qf) * PF_ATT_ROWS;
             d.cap = kv->cap;
             d.mask_off = (int)moff;
             d.mask_len = P0 + r0 + m;
@@ -1428,7 +1433,7 @@ int stage_prefill(Stage* st, KVState* kv, int n, const int32_t* positions, const
             }
             HIP_TRY(prof_mark(st, STAGE_KERNEL_QKV, false, s));
             // the pass's k and v rows into the cache, then the causal attention of all its
-            // 64-row chunks in one launch (each a request whose past includes the
+            // 16-row chunks in one launch (each a request whose past includes the
             // earlier chunks' rows); the output goes to the o product as prepared blocks
             HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, true, s));
             {
@@ -1436,7 +1441,7 @@ int stage_prefill(Stage* st, KVState* kv, int n, const int32_t* positions, const
                 HIP_TRY(launch_kv_rope_append(st->pf_qkv, nqkv, (const int*)(db + off_pos) + p0, st->rope, pr, P0 + p0, Hq, Hkv,
                                               D, kv->kc + (size_t)l * lstride, kv->vc + (size_t)l * lstride, kv->cap,
                                               first ? kv->table[kv->cur] : nullptr, dt_code(c.kv_dtype), s));
-                const int q0 = p0 / MAX_ROWS, nq = (pr + MAX_ROWS - 1) / MAX_ROWS;
+                const int q0 = p0 / PF_ATT_ROWS, nq = (pr + PF_ATT_ROWS - 1) / PF_ATT_ROWS;
                 AttnArgs a{};
                 a.qkv = st->pf_qkv;
                 a.qkv_ld = nqkv;
@@ -1460,11 +1465,17 @@ int stage_prefill(Stage* st, KVState* kv, int n, const int32_t* positions, const
                 a.counters = st->acnt;
                 a.nsplit_max = splits;
                 a.vector_path = st->attn_vector;
+                {                                            // the direct-load form: the longest chunk's split fits
+                    const int Lmax = P0 + p0 + pr;
+                    int sl = std::max(ATTN_MIN_SPLIT, (Lmax + splits - 1) / splits);
+                    sl = (sl + KGROUPS - 1) / KGROUPS * KGROUPS;
+                    a.dma = st->attn_dma && sl <= 1024 && lstride * 2 <= 0xFFFFFFF0ull ? 1 : 0;
+                }
                 a.bp_out = st->pf_bp;
                 a.bc_out = st->pf_bc;
                 a.kp = kp;
                 a.no_append = 1;
-                HIP_TRY(launch_attention(a, D, (Hq / Hkv) * MAX_ROWS, s));
+                HIP_TRY(launch_attention(a, D, (Hq / Hkv) * PF_ATT_ROWS, s));
             }
             HIP_TRY(prof_mark(st, STAGE_KERNEL_ATTN, false, s));
             // x = residual + o W_o^T

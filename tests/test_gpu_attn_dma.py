@@ -5,8 +5,9 @@ the appended cache rows must be bitwise equal.  Cases: speculative verify on
 4 slots x 5 tokens from KV 2048 with 10% masked holes, a masked last draft and
 a beam permutation, then a decode step (two 8B layers); a micro-batch of
 decode and verify requests of several lengths; a 15-node draft tree with one
-key mask per query row; a 70B-shaped layer verifying 5 tokens (40 query
-vectors per kv head: three tiles); and the tiny shape (head_dim 64).  The oracle checks of the default path run in the other GPU
+key mask per query row; 24 and 64 rows of one slot (two and four query tiles
+per wave); a 70B-shaped layer verifying 5 tokens (40 query vectors per kv
+head: three tiles); and the tiny shape (head_dim 64).  The oracle checks of the default path run in the other GPU
 tests."""
 import os
 
@@ -139,6 +140,22 @@ def test_8b_tree_row_masks():
         return [(0, (P + depth)[None], slot_mask, None, rows)], n
 
     _run_both(shape, 75, {"states": [(1, P, P + 32)], "forwards": [fwd]})
+
+
+@pytest.mark.parametrize("n", [24, 64])
+def test_8b_many_query_rows(n):
+    """24 rows (96 query vectors per kv head: two tiles per wave) and 64 rows
+    (256: four tiles per wave, the prefill chunk's shape), one slot from KV 700
+    with holes."""
+    shape = synth.with_layers(synth.LLAMA8B_HALF, 1)
+    P = 700
+    mask = np.ones((1, P + n), np.uint8)
+    mask[0, :P] = synth.hole_mask(P, 0.1, 76, n)
+
+    def fwd(st):
+        return [(0, np.arange(P, P + n, dtype=np.int32)[None], mask, None)], n
+
+    _run_both(shape, 76, {"states": [(1, P, P + 80)], "forwards": [fwd]})
 
 
 def test_70b_layer_verify():
