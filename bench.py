@@ -668,8 +668,9 @@ def main() -> int:
         t_end = time.perf_counter()
         prof = None
         if profile:
-            prof = stage.profile_read()
+            each = stage.profile_read_each()
             stage.profile(None)
+            prof = (len(each), float(each.astype(np.float64).sum()), each)
         ms = (t_end - t_start) * 1e3 / args.steps
         return ms, prof
 
@@ -686,8 +687,9 @@ def main() -> int:
 
     b = algorithmic_bytes(shape, args.kv)
     gbps = b["total"] / (ms_main * 1e-3) / 1e9
-    launches, prof_ms = prof
+    launches, prof_ms, each = prof
     per_launch_ms = prof_ms / max(1, launches)
+    pct = np.percentile(each, [10, 50, 90]) * 1e3 if len(each) else [0.0, 0.0, 0.0]
     if dominant == "persistent":
         k_bytes, k_name = b["total"], "stage_stream_kernel (whole stage forward, one launch per step)"
     else:
@@ -721,6 +723,7 @@ def main() -> int:
             "frac": round(k_gbps / HBM_PEAK_GBPS, 4),
             "traffic": MEASURED_TRAFFIC.get((kernel_digest(), args.kv)) if dominant == "persistent" else None,
             "bytes_per_launch": k_bytes, "avg_launch_us": round(per_launch_ms * 1e3, 3), "launches_timed": launches,
+            "launch_us_p10_median_p90": [round(float(x), 3) for x in pct],
         },
     }
     if ms_also:

@@ -386,7 +386,9 @@ int stage_debug_dequant(Stage* stage, int layer, int which, float* out_host);
  * to stop.
  * stage_profile_read synchronizes on the last recorded event, returns the number
  * of recorded launches and the sum of their durations in milliseconds, and
- * clears the record. */
+ * clears the record.  stage_profile_read_each does the same but writes each
+ * launch's duration in milliseconds, in launch order, to ms_out host [capacity]
+ * (launches beyond capacity are counted in *launches, not written). */
 #define STAGE_KERNEL_QKV    0
 #define STAGE_KERNEL_ATTN   1
 #define STAGE_KERNEL_OPROJ  2
@@ -395,6 +397,7 @@ int stage_debug_dequant(Stage* stage, int layer, int which, float* out_host);
 #define STAGE_KERNEL_PERSISTENT 5
 int stage_profile_enable(Stage* stage, int kernel_class);
 int stage_profile_read(Stage* stage, int* launches, double* total_ms);
+int stage_profile_read_each(Stage* stage, float* ms_out, int capacity, int* launches);
 
 /* Test and measurement support: phase-boundary timestamps of the last
  * single-launch forward, recorded only when STAGE_PS_TRACE=1 was set in the

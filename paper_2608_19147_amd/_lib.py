@@ -23,7 +23,7 @@ EXPORTS = (
     "stage_create", "stage_destroy", "kv_state_alloc", "kv_state_free", "kv_state_reset",
     "kv_append", "kv_length", "kv_read", "kv_truncate", "stage_forward",
     "stage_debug_dequant", "stage_weight_bytes", "stage_last_error",
-    "stage_profile_enable", "stage_profile_read", "stage_debug_phase_trace", "stage_device_status",
+    "stage_profile_enable", "stage_profile_read", "stage_profile_read_each", "stage_debug_phase_trace", "stage_device_status",
     "stage_debug_attn_arm", "stage_debug_attn_read",
     "kv_compact", "kv_capture_size", "kv_capture", "kv_restore", "kv_capture_noalloc",
     "stage_head_attach", "stage_head_top1", "stage_prefill", "stage_embed_attach", "stage_embed",
@@ -88,6 +88,7 @@ def load() -> ctypes.CDLL:
         "stage_last_error": (ctypes.c_char_p, []),
         "stage_profile_enable": (I, [V, I]),
         "stage_profile_read": (I, [V, P(I), P(ctypes.c_double)]),
+        "stage_profile_read_each": (I, [V, V, I, P(I)]),
         "stage_debug_phase_trace": (I, [V, V, I, V]),
         "stage_device_status": (I, [V]),
         "stage_debug_attn_arm": (I, [V, I, I]),

@@ -838,6 +838,21 @@ int stage_profile_read(Stage* stage, int* launches, double* total_ms) {
     return STAGE_OK;
 }
 
+int stage_profile_read_each(Stage* stage, float* ms_out, int capacity, int* launches) {
+    if (!stage || !launches || (!ms_out && capacity > 0)) return fail(STAGE_E_INVALID, "NULL argument");
+    *launches = 0;
+    const size_t pairs = stage->prof_used / 2;
+    if (pairs) {
+        HIP_TRY(hipSetDevice(stage->device));
+        HIP_TRY(hipEventSynchronize(stage->prof_ev[2 * pairs - 1]));
+        for (size_t i = 0; i < pairs && (long long)i < capacity; ++i)
+            HIP_TRY(hipEventElapsedTime(&ms_out[i], stage->prof_ev[2 * i], stage->prof_ev[2 * i + 1]));
+        *launches = (int)pairs;
+    }
+    stage->prof_used = 0;
+    return STAGE_OK;
+}
+
 int kv_state_alloc(Stage* stage, int n_slots, int capacity, KVState** out) {
     if (!stage || !out) return fail(STAGE_E_INVALID, "NULL argument");
     *out = nullptr;

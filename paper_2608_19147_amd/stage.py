@@ -129,6 +129,14 @@ class Stage:
         check(self.lib.stage_profile_read(self.handle, ctypes.byref(n), ctypes.byref(ms)))
         return n.value, ms.value
 
+    def profile_read_each(self, capacity: int = 65536) -> np.ndarray:
+        """Each recorded launch's duration in ms (launch order) since profile()
+        or the last read."""
+        out = np.zeros(capacity, np.float32)
+        n = ctypes.c_int()
+        check(self.lib.stage_profile_read_each(self.handle, ctypes.c_void_p(out.ctypes.data), capacity, ctypes.byref(n)))
+        return out[: min(n.value, capacity)].copy()
+
     def debug_attn_arm(self, layer: int, max_keys: int) -> None:
         """Record `layer`'s rotated queries and visible scores in later forwards
         (per-layer kernels); layer = -1 disarms."""
