@@ -178,12 +178,16 @@ struct PsArgs {
     // and the score q.k / sqrt(D) of every key the row sees, [Hq][dbg_keys]
     float* dbg_q; float* dbg_logits; int dbg_keys, dbg_layer;
     // LDS byte offsets
-    int l_xs, l_sb0, l_sb1, l_res, l_q, l_nkv, l_part, l_rope, l_dbg, l_end;
+    int l_xs, l_sb0, l_sb1, l_res, l_q, l_qb, l_nkv, l_part, l_rope, l_dbg, l_end;
 };
 constexpr int PS_LL_PER_LAYER = 6;      // flag-word exchanges per layer: q|k|v, split partials, attention
                                         // output, residual after o, SwiGLU output, residual after down
 constexpr int PS_TRACE_PER_LAYER = 32;   // 10 control-wave boundaries, 6 from compute wave 0, 6 exchange pass
-                                         // counts, 6 exchange end times, 3 first-pass times, 1 spare
+                                         // counts, 6 exchange end times, 3 first-pass times, partial published
+
+// The stream kernel's attention runs on the matrix cores for head_dim 128 and
+// at most four query heads per kv head.
+constexpr bool ps_att_mma(int D, int gs) { return D == 128 && gs <= 4; }
 
 // LDS layout of the stream kernel with `slots` ring slots per compute wave;
 // returns the total bytes.
@@ -205,14 +209,18 @@ inline int ps_layout(PsArgs& a, int slots, int D, int gs) {
     a.l_res = off;  off += up(rows * 4, 16);
     a.l_q = off;    off += gs * D * 4;
     a.l_nkv = off;  off += 2 * D * 4;
-    // the compute waves' attention partials live only between the q|k|v product
-    // (the last reader of the staged input) and the staging of the o input, so
-    // they share the staged-input region when they fit
-    const int part_b = SK_CW * gs * (D + 4) * 4;
-    if (part_b <= kcmax * 64) {
+    // the compute waves' attention partials and the queries as two cache-dtype
+    // terms live only between the q|k|v product (the last reader of the staged
+    // input) and the staging of the o input, so they share the staged-input
+    // region when they fit
+    const int part_b = up(SK_CW * gs * (D + 4) * 4, 16);
+    const int qb_b = ps_att_mma(D, gs) ? 2 * gs * D * 2 : 0;
+    if (part_b + qb_b <= kcmax * 64) {
         a.l_part = a.l_xs;
+        a.l_qb = a.l_xs + part_b;
     } else {
-        a.l_part = off; off += up(part_b, 16);
+        a.l_part = off; off += part_b;
+        a.l_qb = off;   off += up(qb_b, 16);
     }
     a.l_rope = off; off += (D / 2) * 8;
     a.l_dbg = off;  off += 64;                                        // compute-wave trace stamps

@@ -63,6 +63,11 @@ __device__ __forceinline__ u32x4 lds_rd16(uint32_t a) {
     asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
     return v;
 }
+__device__ __forceinline__ u32x2 lds_rd8(uint32_t a) {
+    u32x2 v;
+    asm volatile("ds_read_b64 %0, %1" : "=v"(v) : "v"(a));
+    return v;
+}
 __device__ __forceinline__ uint32_t lds_rdu16(uint32_t a) {
     uint32_t v;
     asm volatile("ds_read_u16 %0, %1" : "=v"(v) : "v"(a));
@@ -77,6 +82,7 @@ __device__ __forceinline__ void lds_wr16(uint32_t a, f32x4 v) {
 // After lgkm_wait_all: makes `v` depend on the wait, so no use moves above it.
 __device__ __forceinline__ void touch(u32x4& v) { asm volatile("" : "+v"(v)); }
 __device__ __forceinline__ void touch(uint32_t& v) { asm volatile("" : "+v"(v)); }
+__device__ __forceinline__ void touch(u32x2& v) { asm volatile("" : "+v"(v)); }
 
 // (x & m) | c for c free of m's bits, in one instruction (mask from an SGPR,
 // constant from a VGPR: a VOP3 encoding takes no literal operands).
@@ -871,6 +877,205 @@ __device__ __forceinline__ void att_seg_h(Issue& issue, Ring& rg, int T, uint64_
     if (li == 0) lds_wr16(base, f32x4{m, l, 0.f, 0.f});
 }
 
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+
+// 8 bytes per lane through the LDS transpose unit: in each 16-lane block, lane
+// i receives element i % 4 of the reads of lanes i / 4, 4 + i / 4, 8 + i / 4
+// and 12 + i / 4, in that order.
+__device__ __forceinline__ u32x2 lds_rd8_tr(uint32_t a) {
+    u32x2 v;
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(a));
+    return v;
+}
+
+// 16x16x32 and 16x16x16 products in the cache dtype, fp32 accumulation.
+template <bool BF16>
+__device__ __forceinline__ f32x4 mma_k32(const u32x4& A, const u32x4& B, f32x4 c) {
+    if constexpr (BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, A), __builtin_bit_cast(bf16x8_t, B), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, A), __builtin_bit_cast(f16x8_t, B), c, 0, 0, 0);
+}
+template <bool BF16>
+__device__ __forceinline__ f32x4 mma_k16(const u32x2& A, const u32x2& B, f32x4 c) {
+    if constexpr (BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, A), __builtin_bit_cast(i16x4_t, B), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4_t, A), __builtin_bit_cast(f16x4_t, B), c, 0, 0, 0);
+}
+template <bool BF16>
+__device__ __forceinline__ float kv_value(uint16_t b) { return BF16 ? bf16_to_f32(b) : f16_to_f32(b); }
+// Two floats rounded to the cache dtype (to nearest even), low half first.
+template <bool BF16>
+__device__ __forceinline__ uint32_t kv_pair(float lo, float hi) {
+    if constexpr (BF16) {
+        typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+        const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+        return __builtin_bit_cast(uint32_t, v);
+    } else {
+        return (uint32_t)f32_to_f16(lo) | ((uint32_t)f32_to_f16(hi) << 16);
+    }
+}
+
+// The matrix-core form of the wave's attention (head_dim 128, at most four
+// query heads per kv head): the rows go sixteen at a time (four slot pairs).
+// The scores are computed transposed, S^T = K Q^T, with the 16 rows as the
+// product's M rows and the heads as its N columns, each query entering as two
+// cache-dtype terms (q = qh + qr, qr the rounding residual of qh), as in the
+// per-layer attention.  Lane l then holds the scores of head l % 16 for rows
+// 4 (l / 16) + j, j < 4, which is the A-operand layout of the 16x16x16 product
+// P V: the weights are rounded to the cache dtype and used where they are.
+// The V operand of 16-lane block b is slot pair b's V slot, transposed by the
+// LDS read.  Running (max, sum) per head are kept per lane and combined over
+// the four blocks at the end; the output accumulators hold head 4 (l / 16) + j
+// in register j, so heads < 4 sit in lanes 0..15.
+// qlds: the queries' two terms as written by the control wave (GS D values qh,
+// then GS D values qr, head-major).  mall: bit 4 t + r set when row r of slot
+// pair t is visible.
+template <int GS, int D, int S, bool BF16, bool REC, class Issue>
+__device__ __forceinline__ void att_seg_m(Issue& issue, Ring& rg, int T, uint64_t mall, uint32_t qlds, uint32_t part,
+                                          float* rec, int keys, int j0) {
+    static_assert(D == 128 && GS >= 1 && GS <= 4 && S >= 8, "head_dim 128, up to four heads, two chunks of ring");
+    constexpr int KB = D / 32;                 // 32-dim blocks of the score product
+    constexpr int DB = D / 16;                 // 16-dim blocks of the output
+    constexpr uint32_t RB = 2 * D;             // bytes per cache row
+    const int lane = threadIdx.x & 63;
+    const int i16 = lane & 15, b4 = lane >> 4;
+    float m = -INFINITY, lsum = 0.f;
+    f32x4 o[DB];
+#pragma unroll
+    for (int d = 0; d < DB; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (T > 0) {
+        // query operand: head i16 (zero for heads >= GS), dims 8 b4 + 32 kb .. + 7
+        u32x4 qh[KB], qr[KB];
+        {
+            const uint32_t qa = qlds + 2u * (uint32_t)((i16 < GS ? i16 : 0) * D + 8 * b4);
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) {
+                qh[kb] = lds_rd16(qa + 64u * kb);
+                qr[kb] = lds_rd16(qa + (uint32_t)(GS * D * 2) + 64u * kb);
+            }
+            lgkm_wait_all();
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) {
+                touch(qh[kb]);
+                touch(qr[kb]);
+                if (i16 >= GS) {
+                    qh[kb] = u32x4{0u, 0u, 0u, 0u};
+                    qr[kb] = u32x4{0u, 0u, 0u, 0u};
+                }
+            }
+        }
+        for (int t0 = 0; t0 < T; t0 += 4) {
+            const int tc = min(4, T - t0);
+            if (rg.p > rg.pmax) vm_wait_all();
+            else if (tc == 4) vm_wait<S - 8>();
+            else if (tc == 3) vm_wait<S - 6>();
+            else if (tc == 2) vm_wait<S - 4>();
+            else vm_wait<S - 2>();
+            // K operand: row i16 of the chunk (pair i16 / 4, row i16 % 4), dims 8 b4 + 32 kb;
+            // V operand of block b4: pair b4's V slot.  Pairs past the chunk read the
+            // chunk's last pair and are zeroed below (ring slots of other data may hold
+            // any bits, and a zero weight times a NaN is a NaN).
+            const int tk = i16 >> 2;
+            int rk = rg.ri + 2 * min(tk, tc - 1);
+            int rv = rg.ri + 2 * min(b4, tc - 1) + 1;
+            rk -= rk >= S ? S : 0;
+            rv -= rv >= S ? S : 0;
+            const uint32_t ka = rg.addr(rk) + (uint32_t)(i16 & 3) * RB + 16u * (uint32_t)b4;
+            const uint32_t va = rg.addr(rv) + (uint32_t)(i16 >> 2) * RB + 8u * (uint32_t)(i16 & 3);
+            u32x4 kw[KB];
+            u32x2 vf[DB];
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) kw[kb] = lds_rd16(ka + 64u * kb);
+#pragma unroll
+            for (int d = 0; d < DB; ++d) vf[d] = lds_rd8_tr(va + 32u * d);
+            lgkm_wait_all();
+            const bool kval = tk < tc, vval = b4 < tc;
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) {
+                touch(kw[kb]);
+                if (!kval) kw[kb] = u32x4{0u, 0u, 0u, 0u};
+            }
+#pragma unroll
+            for (int d = 0; d < DB; ++d) {
+                touch(vf[d]);
+                if (!vval) vf[d] = u32x2{0u, 0u};
+            }
+#pragma nounroll
+            for (int t = 0; t < 2 * tc; ++t) {
+                issue(rg.addr(rg.ri));
+                rg.ri = Ring::next(rg.ri, S);
+            }
+            rg.p += 2 * tc;
+            // scores of rows 4 b4 + j for head i16
+            f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) {
+                sc = mma_k32<BF16>(kw[kb], qh[kb], sc);
+                sc = mma_k32<BF16>(kw[kb], qr[kb], sc);
+            }
+            const int sh = 4 * (t0 + b4);
+            const uint32_t vis4 = sh < 64 ? (uint32_t)(mall >> sh) & 0xFu : 0u;
+            float sv[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const bool vis = i16 < GS && ((vis4 >> j) & 1u);
+                sv[j] = vis ? sc[j] : -INFINITY;
+                if constexpr (REC) {
+                    const int key = j0 + sh + j;
+                    if (rec && vis && key < keys) rec[i16 * keys + key] = sc[j] * 0.69314718055994531f;
+                }
+            }
+            float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+            float xa, xb;
+            lane_pair(mx, 16, xa, xb);
+            mx = fmaxf(xa, xb);
+            lane_pair(mx, 32, xa, xb);
+            mx = fmaxf(xa, xb);
+            const float mn = fmaxf(m, mx);
+            const float mref = (mn == -INFINITY) ? 0.f : mn;    // no visible row yet: nothing changes
+            const float corr = exp2_raw(m - mref);
+            float p[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) p[j] = exp2_raw(sv[j] - mref);
+            lsum = __builtin_fmaf(lsum, corr, (p[0] + p[1]) + (p[2] + p[3]));
+            m = mn;
+            const u32x2 pa = u32x2{kv_pair<BF16>(p[0], p[1]), kv_pair<BF16>(p[2], p[3])};
+            if (t0 > 0 && __any(i16 < GS && corr != 1.f)) {     // some head's maximum moved (first chunk: o = 0)
+                float cj[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    cj[j] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, corr), j));
+#pragma unroll
+                for (int d = 0; d < DB; ++d)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) o[d][j] *= cj[j];
+            }
+#pragma unroll
+            for (int d = 0; d < DB; ++d) o[d] = mma_k16<BF16>(pa, vf[d], o[d]);
+        }
+        float la, lb2;
+        lane_pair(lsum, 16, la, lb2);
+        lsum = la + lb2;
+        lane_pair(lsum, 32, la, lb2);
+        lsum = la + lb2;
+    }
+    const int cw = threadIdx.x >> 6;
+    if (b4 == 0) {
+#pragma unroll
+        for (int j = 0; j < GS; ++j) {
+            const uint32_t base = part + 4 * ((cw * GS + j) * (D + 4));
+#pragma unroll
+            for (int d = 0; d < DB; ++d) lds_wr4(base + 16 + 4 * (16 * d + i16), o[d][j]);
+        }
+        if (i16 < GS) lds_wr16(part + 4 * ((cw * GS + i16) * (D + 4)), f32x4{m, lsum, 0.f, 0.f});
+    }
+}
+
 template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S, bool KVB, bool REC>
 __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
     constexpr int LPR = AttGeo<D>::LPR, RPS = AttGeo<D>::RPS;
@@ -896,7 +1101,8 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
     const uint8_t* kbase = (const uint8_t*)rq.kc;
     const uint8_t* vbase = (const uint8_t*)rq.vc;
     uint32_t mbits = 0u;
-    uint64_t mall = 0u;           // head-per-group form: every row r of slot pair t, at bit RPS t + r
+    constexpr bool ATT_MMA = ps_att_mma(D, GS) && RPS * SK_TMAX <= 64;
+    uint64_t mall = 0u;           // head-per-group and matrix-core forms: every row r of slot pair t, at bit RPS t + r
     uint32_t aoff[SK_TMAX];       // per-lane byte offset of cache-row slot pair t within one layer
     {
         const uint8_t* mask = a.meta.masks + rq.mask_off + (size_t)b * rq.mask_len;
@@ -909,7 +1115,7 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
             const int phys = valid ? (int)tab[jj] : b;
             if (valid && mask[jj] != 0) mbits |= 1u << t;
             aoff[t] = (uint32_t)(((((u64)phys * a.Hkv + g) * rq.cap + jj) * D + 8 * (lane % LPR)) * 2);
-            if constexpr (GS == RPS && RPS * SK_TMAX <= 64) {
+            if constexpr (ATT_MMA || (GS == RPS && RPS * SK_TMAX <= 64)) {
 #pragma unroll
                 for (int r = 0; r < RPS; ++r) {
                     const int jr = j0 + t * RPS + r;
@@ -1011,7 +1217,9 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
         float* rec = nullptr;
         if constexpr (REC)
             if (l == a.dbg_layer && has_att) rec = a.dbg_logits + (size_t)g * GS * a.dbg_keys;
-        if constexpr (GS == RPS && RPS * SK_TMAX <= 64)
+        if constexpr (ATT_MMA)
+            att_seg_m<GS, D, S, KVB, REC>(issue, rg, T, mall, lb + a.l_qb, lb + a.l_part, rec, a.dbg_keys, j0);
+        else if constexpr (GS == RPS && RPS * SK_TMAX <= 64)
             att_seg_h<GS, D, S, KVB, REC>(issue, rg, T, mall, lb + a.l_q, lb + a.l_part, rec, a.dbg_keys, j0);
         else
             att_seg_t<GS, D, S, KVB, REC>(issue, rg, T, mbits, lb + a.l_q, lb + a.l_part, rec, a.dbg_keys, j0);
@@ -1216,7 +1424,7 @@ __device__ __forceinline__ bool stage_pairs(const PsArgs& a, const u64* buf, int
 // for its own 1/nsplit slice of the group's outputs, combines them in a fixed
 // butterfly order and publishes that slice of the attention output.
 template <int GS, int D>
-__device__ __forceinline__ void merge_slices(const PsArgs& a, int g, int split, uint32_t f_part, uint32_t f_o) {
+__device__ __forceinline__ void merge_slices(const PsArgs& a, int g, int split, uint32_t f_part, uint32_t f_o, int l) {
     const int SL = GS * D / a.nsplit;                 // outputs per slice (multiple of 8)
     const int CH = SL / 8;                            // 8-output chunks per slice
     const int ml = fresh_lane();
@@ -1229,7 +1437,7 @@ __device__ __forceinline__ void merge_slices(const PsArgs& a, int g, int split, 
     const int off[5] = {base, base + 8 * (2 + dd), base + 8 * (2 + dd) + 16, base + 8 * (2 + dd) + 32,
                         base + 8 * (2 + dd) + 48};
     u32x4 pv[5];
-    ll_wait<5>(a, r, off, act ? 0x1Fu : 0u, f_part, [&](int i, const u32x4& pc) { pv[i] = pc; }, true);
+    ll_wait<5>(a, r, off, act ? 0x1Fu : 0u, f_part, [&](int i, const u32x4& pc) { pv[i] = pc; }, true, l, 1);
     float ms = -INFINITY, ls = 0.f, ov[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) ov[e] = 0.f;
@@ -1264,7 +1472,7 @@ __device__ __forceinline__ void merge_slices(const PsArgs& a, int g, int split, 
     }
 }
 
-template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S, bool REC>
+template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S, bool KVB, bool REC>
 __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     const int lane = threadIdx.x & 63;
     const int w = blockIdx.x;
@@ -1272,6 +1480,7 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     uint8_t* xs = smem + a.l_xs;
     const float* res = (const float*)(smem + a.l_res);
     float* qs = (float*)(smem + a.l_q);
+    uint32_t* qhb = (uint32_t*)(smem + a.l_qb);   // query pairs as two cache-dtype terms: qh, then qr
     float* nkv = (float*)(smem + a.l_nkv);
     const float* part = (const float*)(smem + a.l_part);
     const float2* rope = (const float2*)(smem + a.l_rope);
@@ -1289,6 +1498,7 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     const int g = has_att ? w / a.nsplit : 0;
     const int split = has_att ? w % a.nsplit : 0;
     const bool owns_new = has_att && split == a.nsplit - 1;
+    const bool new_vis = owns_new && mask[P] != 0;           // this forward's row is visible to its own query
     const int KVD = a.Hkv * D;
     const size_t lstride = (size_t)rq.S * a.Hkv * rq.cap * D;
     const int hq = lane / LPH, d0 = (lane % LPH) * OPL;     // merge lane layout
@@ -1383,10 +1593,19 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
             u32x4 kv[2 * NKP];                                 // new k, v pieces
             ok = ll_wait<NP>(a, r, off, use, f_qkv, [&](int i, const u32x4& pc) {
                 const uint32_t p0 = pc[0], p1 = pc[2];
-                if (i < NQP)
-                    *(float2*)(qs + 2 * (lane + 64 * i)) = float2{__uint_as_float(p0) * a.qscale, __uint_as_float(p1) * a.qscale};
-                else
+                if (i < NQP) {
+                    const float y0 = __uint_as_float(p0) * a.qscale, y1 = __uint_as_float(p1) * a.qscale;
+                    *(float2*)(qs + 2 * (lane + 64 * i)) = float2{y0, y1};
+                    if constexpr (ps_att_mma(D, GS)) {              // the matrix-core attention's query terms
+                        const uint32_t hi = kv_pair<KVB>(y0, y1);
+                        const float r0 = y0 - kv_value<KVB>((uint16_t)(hi & 0xFFFFu));
+                        const float r1 = y1 - kv_value<KVB>((uint16_t)(hi >> 16));
+                        qhb[lane + 64 * i] = hi;
+                        qhb[GS * D / 2 + lane + 64 * i] = kv_pair<KVB>(r0, r1);
+                    }
+                } else {
                     kv[i - NQP] = pc;
+                }
             }, ok, l, 0);
             if (owns_new) {
                 uint16_t* kl = rq.kc + (size_t)l * lstride + (((size_t)b * a.Hkv + g) * rq.cap + P) * D;
@@ -1415,11 +1634,95 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         stamp(a, l, 3);
         // ---- merge the waves (and the new row) into this split's partial; the last split merges the splits
         if (has_att) {
+            // every wave's (max, sum) of head hq and this lane's OPL outputs of it, and
+            // the new row's query and cache values, read with one wait
+            constexpr int NR = OPL >= 4 ? OPL / 4 : 1;         // 16-byte reads per OPL values (OPL = 2: one 8-byte read)
+            u32x4 pml[SK_CW], po[SK_CW][NR], qn[NR], kn[NR], vn[NR];
+            u32x2 po2[SK_CW], qn2 = u32x2{0u, 0u}, kn2 = qn2, vn2 = qn2;
+#pragma unroll
+            for (int r = 0; r < NR; ++r) qn[r] = kn[r] = vn[r] = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int c = 0; c < SK_CW; ++c) {
+                const uint32_t pa = lb + a.l_part + 4u * (uint32_t)((c * GS + hq) * (D + 4));
+                pml[c] = lds_rd16(pa);
+                if constexpr (OPL >= 4) {
+#pragma unroll
+                    for (int r = 0; r < NR; ++r) po[c][r] = lds_rd16(pa + 16u + 4u * d0 + 16u * r);
+                } else {
+                    po2[c] = lds_rd8(pa + 16u + 4u * d0);
+                }
+            }
+            if (new_vis) {
+                const uint32_t qa = lb + a.l_q + 4u * (uint32_t)(hq * D + d0), na = lb + a.l_nkv + 4u * d0;
+                if constexpr (OPL >= 4) {
+#pragma unroll
+                    for (int r = 0; r < NR; ++r) {
+                        qn[r] = lds_rd16(qa + 16u * r);
+                        kn[r] = lds_rd16(na + 16u * r);
+                        vn[r] = lds_rd16(na + 4u * D + 16u * r);
+                    }
+                } else {
+                    qn2 = lds_rd8(qa);
+                    kn2 = lds_rd8(na);
+                    vn2 = lds_rd8(na + 4u * D);
+                }
+            }
+            lgkm_wait_all();
+            float pm[SK_CW], pl[SK_CW], pov[SK_CW][OPL], qv[OPL], kv_[OPL], vv[OPL];
+#pragma unroll
+            for (int c = 0; c < SK_CW; ++c) {
+                touch(pml[c]);
+                const uint32_t m0 = pml[c][0], l0 = pml[c][1];
+                pm[c] = __uint_as_float(m0);
+                pl[c] = __uint_as_float(l0);
+                if constexpr (OPL >= 4) {
+#pragma unroll
+                    for (int r = 0; r < NR; ++r) {
+                        touch(po[c][r]);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const uint32_t x = po[c][r][e];
+                            pov[c][4 * r + e] = __uint_as_float(x);
+                        }
+                    }
+                } else {
+                    touch(po2[c]);
+                    const uint32_t x0 = po2[c][0], x1 = po2[c][1];
+                    pov[c][0] = __uint_as_float(x0);
+                    pov[c][1] = __uint_as_float(x1);
+                }
+            }
+            if constexpr (OPL >= 4) {
+#pragma unroll
+                for (int r = 0; r < NR; ++r) {
+                    touch(qn[r]);
+                    touch(kn[r]);
+                    touch(vn[r]);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t xq = qn[r][e], xk = kn[r][e], xv = vn[r][e];
+                        qv[4 * r + e] = __uint_as_float(xq);
+                        kv_[4 * r + e] = __uint_as_float(xk);
+                        vv[4 * r + e] = __uint_as_float(xv);
+                    }
+                }
+            } else {
+                touch(qn2);
+                touch(kn2);
+                touch(vn2);
+#pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    const uint32_t xq = qn2[e], xk = kn2[e], xv = vn2[e];
+                    qv[e] = __uint_as_float(xq);
+                    kv_[e] = __uint_as_float(xk);
+                    vv[e] = __uint_as_float(xv);
+                }
+            }
             float s_new = -INFINITY;
-            if (owns_new && mask[P] != 0) {
+            if (new_vis) {
                 float sd = 0.f;
 #pragma unroll
-                for (int e = 0; e < OPL; ++e) sd += qs[hq * D + d0 + e] * nkv[d0 + e];
+                for (int e = 0; e < OPL; ++e) sd += qv[e] * kv_[e];
                 sd = (LPH == 16) ? group_sum<16>(sd) : (LPH == 8) ? group_sum<8>(sd) : sd;
                 if constexpr (LPH == 32) {
                     sd = group_sum<16>(sd);
@@ -1436,7 +1739,7 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
                     for (int idx = lane; idx < GS * D; idx += 64) a.dbg_q[(size_t)g * GS * D + idx] = qs[idx] / a.qscale;
             float mx = s_new;
 #pragma unroll
-            for (int c = 0; c < SK_CW; ++c) mx = fmaxf(mx, part[(c * GS + hq) * (D + 4)]);
+            for (int c = 0; c < SK_CW; ++c) mx = fmaxf(mx, pm[c]);
             float L = 0.f, O[OPL];
 #pragma unroll
             for (int e = 0; e < OPL; ++e) O[e] = 0.f;
@@ -1444,16 +1747,14 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
                 const float wn = exp2f(s_new - mx);
                 L = wn;
 #pragma unroll
-                for (int e = 0; e < OPL; ++e) O[e] = wn * nkv[D + d0 + e];
+                for (int e = 0; e < OPL; ++e) O[e] = wn * vv[e];
             }
 #pragma unroll
             for (int c = 0; c < SK_CW; ++c) {
-                const float* pc = part + (c * GS + hq) * (D + 4);
-                const float mc = pc[0];
-                const float wc = (mc == -INFINITY) ? 0.f : exp2f(mc - mx);
-                L += wc * pc[1];
+                const float wc = (pm[c] == -INFINITY) ? 0.f : exp2f(pm[c] - mx);
+                L += wc * pl[c];
 #pragma unroll
-                for (int e = 0; e < OPL; ++e) O[e] += wc * pc[4 + d0 + e];
+                for (int e = 0; e < OPL; ++e) O[e] += wc * pov[c][e];
             }
             u64* pp = a.ll_part + (((size_t)g * a.nsplit + split) * GS + hq) * (D + 2);
 #pragma unroll
@@ -1462,7 +1763,9 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
                 ll_store(pp, __float_as_uint(mx), f_part);
                 ll_store(pp + 1, __float_as_uint(L), f_part);
             }
-            merge_slices<GS, D>(a, g, split, f_part, f_o);
+            if (a.trace && lane == 0)
+                a.trace[((size_t)w * a.n_layers + l) * PS_TRACE_PER_LAYER + 31] = wall_clock64();
+            merge_slices<GS, D>(a, g, split, f_part, f_o, l);
         }
         stamp(a, l, 4);
         wg_barrier();                                         // merge done: the compute waves poll the attention output
@@ -1546,7 +1849,7 @@ __global__ __launch_bounds__(SK_THREADS) void stage_stream_kernel(PsArgs a) {
     if ((threadIdx.x >> 6) < SK_CW)
         compute_main<CPL_H, CPL_Q, CPL_F, D, GS, S, KVB, REC>(a, lds_addr(smem));
     else
-        control_main<CPL_H, CPL_Q, CPL_F, D, GS, S, REC>(a, smem);
+        control_main<CPL_H, CPL_Q, CPL_F, D, GS, S, KVB, REC>(a, smem);
 }
 
 // ------------------------------------------------------------------ host side
