@@ -1419,6 +1419,40 @@ __device__ __forceinline__ bool stage_pairs(const PsArgs& a, const u64* buf, int
     }, ok);
 }
 
+// v combined (op: commutative, exact for max) over the lanes congruent to this
+// one modulo ch (a power of two, 1..64): lane exchanges within 4 lanes, DPP
+// rotations within a 16-lane row, then the swaps of 16- and 32-lane halves.
+// N values at once: one uniform branch per step.
+template <int N, class Op>
+__device__ __forceinline__ void split_combine(float (&v)[N], int ch, Op op) {
+    if (ch <= 1)
+#pragma unroll
+        for (int i = 0; i < N; ++i) v[i] = op(v[i], dpp_f<0xB1>(v[i]));   // quad_perm [1,0,3,2]: lane ^ 1
+    if (ch <= 2)
+#pragma unroll
+        for (int i = 0; i < N; ++i) v[i] = op(v[i], dpp_f<0x4E>(v[i]));   // quad_perm [2,3,0,1]: lane ^ 2
+    if (ch <= 4)
+#pragma unroll
+        for (int i = 0; i < N; ++i) v[i] = op(v[i], dpp_f<0x124>(v[i]));  // row_ror:4
+    if (ch <= 8)
+#pragma unroll
+        for (int i = 0; i < N; ++i) v[i] = op(v[i], dpp_f<0x128>(v[i]));  // row_ror:8: the class within the row
+    if (ch <= 16)
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            float a, b;
+            lane_pair(v[i], 16, a, b);
+            v[i] = op(a, b);
+        }
+    if (ch <= 32)
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            float a, b;
+            lane_pair(v[i], 32, a, b);
+            v[i] = op(a, b);
+        }
+}
+
 // Split merge (control wave of each attention workgroup): every split of a
 // kv head reads the partials (max, sum, outputs) of all the head group's splits
 // for its own 1/nsplit slice of the group's outputs, combines them in a fixed
@@ -1452,18 +1486,20 @@ __device__ __forceinline__ void merge_slices(const PsArgs& a, int g, int split, 
             ov[2 * j + 1] = __uint_as_float(x1);
         }
     }
-    // combine the splits: lanes c, c + CH, c + 2 CH, ... (fixed butterfly order)
-    float Mx = ms;
-    for (int sh = CH; sh < 64; sh <<= 1) Mx = fmaxf(Mx, __shfl_xor(Mx, sh));
-    const float wgt = (ms == -INFINITY) ? 0.f : exp2f(ms - Mx);
-    float Ls = wgt * ls;
+    // combine the splits: lanes c, c + CH, c + 2 CH, ... (CH a power of two), by
+    // lane exchanges that stay in registers; every lane of a class gets the same
+    // maximum, and lanes 0..CH-1 sums taken in a fixed order
+    float mv[1] = {ms};
+    split_combine(mv, CH, [](float x, float y) { return fmaxf(x, y); });
+    const float wgt = (ms == -INFINITY) ? 0.f : exp2f(ms - mv[0]);
+    float sv[9];
+    sv[8] = wgt * ls;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) ov[e] *= wgt;
-    for (int sh = CH; sh < 64; sh <<= 1) {
-        Ls += __shfl_xor(Ls, sh);
+    for (int e = 0; e < 8; ++e) sv[e] = ov[e] * wgt;
+    split_combine(sv, CH, [](float x, float y) { return x + y; });
+    const float Ls = sv[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) ov[e] += __shfl_xor(ov[e], sh);
-    }
+    for (int e = 0; e < 8; ++e) ov[e] = sv[e];
     if (act && s2 == 0) {
         const float inv = 1.0f / Ls;
         u64* dst = a.ll_o + ((size_t)(g * GS + hh) * D + dd) / 2;
@@ -1628,8 +1664,6 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
             }
         }
         wg_barrier();                                         // q and the new row are staged
-        // gate|up scales (q|k|v finished with this buffer) load while the compute waves run the attention
-        load_scales(Ly.gu.s, w * a.rpw_gu, max(0, min(2 * a.F, (w + 1) * a.rpw_gu) - w * a.rpw_gu), a.ng_h, lb + a.l_sb0);
         wg_barrier();                                         // wave partials are in LDS
         stamp(a, l, 3);
         // ---- merge the waves (and the new row) into this split's partial; the last split merges the splits
@@ -1769,7 +1803,12 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         }
         stamp(a, l, 4);
         wg_barrier();                                         // merge done: the compute waves poll the attention output
+        // gate|up scales (q|k|v finished with this buffer), loaded after the exchange
+        // waits of the attention, which they would hold up, and awaited while the
+        // compute waves stage the attention output
+        load_scales(Ly.gu.s, w * a.rpw_gu, max(0, min(2 * a.F, (w + 1) * a.rpw_gu) - w * a.rpw_gu), a.ng_h, lb + a.l_sb0);
         zero_pad(a.QD, a.kc_q * 32, xs);                      // (they stage it)
+        vm_wait_all();
         wg_barrier();                                         // attention output staged
         wg_barrier();                                         // o rows are in LDS
         stamp(a, l, 5);
