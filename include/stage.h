@@ -415,7 +415,8 @@ int stage_profile_read_each(Stage* stage, float* ms_out, int capacity, int* laun
  * entries 22-27 are the times those waits ended, entries 28-30 the times the
  * first pass of the residual-after-o, residual-after-down and remaining waits
  * returned, entry 31 the time an attention workgroup published its split's
- * partial.  n = capacity of out_host in entries.  Synchronizes the device. */
+ * partial, entries 32-37 the times the first polling pass of each of the six
+ * waits was issued (38, 39 unused).  n = capacity of out_host in entries.  Synchronizes the device. */
 int stage_debug_phase_trace(Stage* stage, uint64_t* out_host, int n, int* n_workgroups);
 
 /* Test support: attention record of one layer.  stage_debug_attn_arm(stage,

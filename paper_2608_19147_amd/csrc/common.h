@@ -182,8 +182,9 @@ struct PsArgs {
 };
 constexpr int PS_LL_PER_LAYER = 6;      // flag-word exchanges per layer: q|k|v, split partials, attention
                                         // output, residual after o, SwiGLU output, residual after down
-constexpr int PS_TRACE_PER_LAYER = 32;   // 10 control-wave boundaries, 6 from compute wave 0, 6 exchange pass
-                                         // counts, 6 exchange end times, 3 first-pass times, partial published
+constexpr int PS_TRACE_PER_LAYER = 40;   // 10 control-wave boundaries, 6 from compute wave 0, 6 exchange pass
+                                         // counts, 6 exchange end times, 3 first-pass times, partial published,
+                                         // 6 first-pass issue times, 2 spare
 
 // The stream kernel's attention runs on the matrix cores for head_dim 128 and
 // at most four query heads per kv head.

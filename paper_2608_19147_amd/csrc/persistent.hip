@@ -191,6 +191,13 @@ __device__ __forceinline__ float sum4_rows(float v0, float v1, float v2, float v
 __device__ __forceinline__ void ll_store(u64* p, uint32_t v, uint32_t flag) {
     __hip_atomic_store(p, ((u64)flag << 32) | (u64)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// Two adjacent flag words (16-byte aligned, byte offset off in the buffer
+// behind r) in one device-coherent 16-byte store: each 8-byte half carries the
+// write number, and readers check both halves.  Fewer store instructions before
+// a wave's next poll: its loads wait for its stores' acknowledgement.
+__device__ __forceinline__ void ll_store2(__amdgpu_buffer_rsrc_t r, int off, uint32_t v0, uint32_t v1, uint32_t flag) {
+    __builtin_amdgcn_raw_buffer_store_b128(u32x4{v0, flag, v1, flag}, r, off, 0, 16);
+}
 // A 16-bit value with the low 16 bits of the write number in one 4-byte word.
 // Every buffer is rewritten at each use, so a stale word carries a number at
 // most a few hundred writes old, never equal to the expected one modulo 2^16.
@@ -224,7 +231,8 @@ __device__ __forceinline__ bool ll_wait(const PsArgs& a, __amdgpu_buffer_rsrc_t 
     const int lane = threadIdx.x & 63;
     uint32_t pend = use;
     unsigned spins = 0;
-    while (true) {
+    const u64 t_issue = (a.trace && tw >= 0) ? wall_clock64() : 0ull;   // stored at the end: a store now would
+    while (true) {                                                      // join this wave's load count
         u32x4 v[NP];
 #pragma unroll
         for (int i = 0; i < NP; ++i)
@@ -254,6 +262,7 @@ __device__ __forceinline__ bool ll_wait(const PsArgs& a, __amdgpu_buffer_rsrc_t 
                 u64* tr = a.trace + ((size_t)blockIdx.x * a.n_layers + tl) * PS_TRACE_PER_LAYER;
                 tr[16 + tw] = spins + 1;
                 tr[22 + tw] = wall_clock64();
+                tr[32 + tw] = t_issue;
             }
             return ok;
         }
@@ -1502,9 +1511,12 @@ __device__ __forceinline__ void merge_slices(const PsArgs& a, int g, int split, 
     for (int e = 0; e < 8; ++e) ov[e] = sv[e];
     if (act && s2 == 0) {
         const float inv = 1.0f / Ls;
-        u64* dst = a.ll_o + ((size_t)(g * GS + hh) * D + dd) / 2;
+        const __amdgpu_buffer_rsrc_t orr = make_rsrc(a.ll_o, (size_t)a.QD * 4);
+        const int ob = ((g * GS + hh) * D + dd) * 4;      // byte offset of output dd's word (dd: a multiple of 8)
 #pragma unroll
-        for (int e = 0; e < 8; e += 2) ll_store(dst + e / 2, pack_f16x2(ov[e] * inv, ov[e + 1] * inv), f_o);
+        for (int e = 0; e < 8; e += 4)
+            ll_store2(orr, ob + 4 * e, pack_f16x2(ov[e] * inv, ov[e + 1] * inv),
+                      pack_f16x2(ov[e + 2] * inv, ov[e + 3] * inv), f_o);
     }
 }
 
@@ -1790,16 +1802,17 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
 #pragma unroll
                 for (int e = 0; e < OPL; ++e) O[e] += wc * pov[c][e];
             }
-            u64* pp = a.ll_part + (((size_t)g * a.nsplit + split) * GS + hq) * (D + 2);
+            {                                                 // (max, sum) and the outputs as pairs of flag words
+                const __amdgpu_buffer_rsrc_t pr = make_rsrc(a.ll_part, (size_t)a.Hkv * a.nsplit * GS * (D + 2) * 8);
+                const int pb = (((g * a.nsplit + split) * GS + hq) * (D + 2)) * 8;
 #pragma unroll
-            for (int e = 0; e < OPL; ++e) ll_store(pp + 2 + d0 + e, __float_as_uint(O[e]), f_part);
-            if (d0 == 0) {
-                ll_store(pp, __float_as_uint(mx), f_part);
-                ll_store(pp + 1, __float_as_uint(L), f_part);
+                for (int e = 0; e < OPL; e += 2)
+                    ll_store2(pr, pb + 8 * (2 + d0 + e), __float_as_uint(O[e]), __float_as_uint(O[e + 1]), f_part);
+                if (d0 == 0) ll_store2(pr, pb, __float_as_uint(mx), __float_as_uint(L), f_part);
             }
-            if (a.trace && lane == 0)
-                a.trace[((size_t)w * a.n_layers + l) * PS_TRACE_PER_LAYER + 31] = wall_clock64();
+            const u64 t_pub = a.trace ? wall_clock64() : 0ull;
             merge_slices<GS, D>(a, g, split, f_part, f_o, l);
+            if (a.trace && lane == 0) a.trace[((size_t)w * a.n_layers + l) * PS_TRACE_PER_LAYER + 31] = t_pub;
         }
         stamp(a, l, 4);
         wg_barrier();                                         // merge done: the compute waves poll the attention output

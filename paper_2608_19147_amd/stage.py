@@ -163,14 +163,15 @@ class Stage:
         check(self.lib.stage_device_status(self.handle))
 
     def phase_trace(self) -> np.ndarray:
-        """[workgroups, layers, 32] device real-time stamps (100 MHz) and exchange
+        """[workgroups, layers, 40] device real-time stamps (100 MHz) and exchange
         pass counts of the last single-launch forward (needs STAGE_PS_TRACE=1 at
         creation)."""
-        n = torch.cuda.get_device_properties(0).multi_processor_count * self.shape.n_layers * 32
+        per = 40                                   # entries per workgroup and layer
+        n = torch.cuda.get_device_properties(0).multi_processor_count * self.shape.n_layers * per
         out = np.empty(n, dtype=np.uint64)
         nwg = ctypes.c_int()
         check(self.lib.stage_debug_phase_trace(self.handle, out.ctypes.data, n, ctypes.byref(nwg)))
-        return out[: nwg.value * self.shape.n_layers * 32].reshape(nwg.value, self.shape.n_layers, 32)
+        return out[: nwg.value * self.shape.n_layers * per].reshape(nwg.value, self.shape.n_layers, per)
 
     def attach_head(self, final_norm: torch.Tensor, lm_head, on_device: bool = False, stream=None) -> None:
         """Final RMSNorm weight [H] (act dtype) and INT4 LM head (``q`` uint8
