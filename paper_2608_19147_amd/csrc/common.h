@@ -169,7 +169,8 @@ struct PsArgs {
     const float2* rope;
     float qscale;                        // log2(e) / sqrt(D)
     int nsplit, split_len, att_T;        // splits per kv head (power of two), cache rows per split, slot pairs per wave
-    unsigned long long* ll_part;         // [Hkv][nsplit][Hq/Hkv][D + 2] flag words (fp32): max, sum, D outputs
+    unsigned long long* ll_part;         // [Hkv][nsplit][Hq/Hkv][ps_part_words(D)] flag words: max, sum (fp32),
+                                         // then the outputs / sum as fp16 pairs
     unsigned ll_epoch;                   // flag numbers used by earlier launches (PS_LL_PER_LAYER per layer)
     unsigned* err;                       // set when an exchange wait gives up
     unsigned spin_limit;                 // polling passes after which an exchange wait gives up
@@ -185,6 +186,9 @@ constexpr int PS_LL_PER_LAYER = 6;      // flag-word exchanges per layer: q|k|v,
 constexpr int PS_TRACE_PER_LAYER = 40;   // 10 control-wave boundaries, 6 from compute wave 0, 6 exchange pass
                                          // counts, 6 exchange end times, 3 first-pass times, partial published,
                                          // 6 first-pass issue times, 2 spare
+
+// Flag words of one split's partial of one query head: max, sum, D / 2 pairs.
+constexpr int ps_part_words(int D) { return 2 + D / 2; }
 
 // The stream kernel's attention runs on the matrix cores for head_dim 128 and
 // at most four query heads per kv head.

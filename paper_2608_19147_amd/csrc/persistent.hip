@@ -1475,12 +1475,12 @@ __device__ __forceinline__ void merge_slices(const PsArgs& a, int g, int split, 
     const bool act = s2 < a.nsplit;
     const int o0 = split * SL + 8 * c;                // first output of the chunk within the head group
     const int hh = o0 / D, dd = o0 % D;
-    const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_part, (size_t)a.Hkv * a.nsplit * GS * (D + 2) * 8);
-    const int base = act ? (int)((((size_t)g * a.nsplit + s2) * GS + hh) * (D + 2)) * 8 : 0;
-    const int off[5] = {base, base + 8 * (2 + dd), base + 8 * (2 + dd) + 16, base + 8 * (2 + dd) + 32,
-                        base + 8 * (2 + dd) + 48};
-    u32x4 pv[5];
-    ll_wait<5>(a, r, off, act ? 0x1Fu : 0u, f_part, [&](int i, const u32x4& pc) { pv[i] = pc; }, true, l, 1);
+    constexpr int PREC = ps_part_words(D);
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(a.ll_part, (size_t)a.Hkv * a.nsplit * GS * PREC * 8);
+    const int base = act ? (int)((((size_t)g * a.nsplit + s2) * GS + hh) * PREC) * 8 : 0;
+    const int off[3] = {base, base + 8 * (2 + dd / 2), base + 8 * (2 + dd / 2) + 16};
+    u32x4 pv[3];
+    ll_wait<3>(a, r, off, act ? 0x7u : 0u, f_part, [&](int i, const u32x4& pc) { pv[i] = pc; }, true, l, 1);
     float ms = -INFINITY, ls = 0.f, ov[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) ov[e] = 0.f;
@@ -1490,19 +1490,20 @@ __device__ __forceinline__ void merge_slices(const PsArgs& a, int g, int split, 
         ls = __uint_as_float(l0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const uint32_t x0 = pv[1 + j][0], x1 = pv[1 + j][2];
-            ov[2 * j] = __uint_as_float(x0);
-            ov[2 * j + 1] = __uint_as_float(x1);
+            const uint32_t x = pv[1 + j / 2][2 * (j % 2)];      // fp16 pair of outputs 2j, 2j + 1
+            ov[2 * j] = f16_to_f32((uint16_t)(x & 0xFFFFu));
+            ov[2 * j + 1] = f16_to_f32((uint16_t)(x >> 16));
         }
     }
     // combine the splits: lanes c, c + CH, c + 2 CH, ... (CH a power of two), by
     // lane exchanges that stay in registers; every lane of a class gets the same
-    // maximum, and lanes 0..CH-1 sums taken in a fixed order
+    // maximum, and lanes 0..CH-1 sums taken in a fixed order.  A split's weight is
+    // 2^(m - M) times its sum (its outputs are normalized by that sum).
     float mv[1] = {ms};
     split_combine(mv, CH, [](float x, float y) { return fmaxf(x, y); });
-    const float wgt = (ms == -INFINITY) ? 0.f : exp2f(ms - mv[0]);
+    const float wgt = (ms == -INFINITY) ? 0.f : exp2f(ms - mv[0]) * ls;
     float sv[9];
-    sv[8] = wgt * ls;
+    sv[8] = wgt;
 #pragma unroll
     for (int e = 0; e < 8; ++e) sv[e] = ov[e] * wgt;
     split_combine(sv, CH, [](float x, float y) { return x + y; });
@@ -1802,12 +1803,20 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
 #pragma unroll
                 for (int e = 0; e < OPL; ++e) O[e] += wc * pov[c][e];
             }
-            {                                                 // (max, sum) and the outputs as pairs of flag words
-                const __amdgpu_buffer_rsrc_t pr = make_rsrc(a.ll_part, (size_t)a.Hkv * a.nsplit * GS * (D + 2) * 8);
-                const int pb = (((g * a.nsplit + split) * GS + hq) * (D + 2)) * 8;
+            {   // (max, sum), and the outputs divided by the sum and rounded to fp16 (the
+                // precision the merged output is published in), as pairs of flag words
+                constexpr int PREC = ps_part_words(D);
+                const __amdgpu_buffer_rsrc_t pr = make_rsrc(a.ll_part, (size_t)a.Hkv * a.nsplit * GS * PREC * 8);
+                const int pb = (((g * a.nsplit + split) * GS + hq) * PREC) * 8;
+                const float inv = L > 0.f ? 1.0f / L : 0.f;
+                if constexpr (OPL >= 4) {
 #pragma unroll
-                for (int e = 0; e < OPL; e += 2)
-                    ll_store2(pr, pb + 8 * (2 + d0 + e), __float_as_uint(O[e]), __float_as_uint(O[e + 1]), f_part);
+                    for (int e = 0; e < OPL; e += 4)
+                        ll_store2(pr, pb + 8 * (2 + (d0 + e) / 2), pack_f16x2(O[e] * inv, O[e + 1] * inv),
+                                  pack_f16x2(O[e + 2] * inv, O[e + 3] * inv), f_part);
+                } else {
+                    ll_store(a.ll_part + pb / 8 + 2 + d0 / 2, pack_f16x2(O[0] * inv, O[1] * inv), f_part);
+                }
                 if (d0 == 0) ll_store2(pr, pb, __float_as_uint(mx), __float_as_uint(L), f_part);
             }
             const u64 t_pub = a.trace ? wall_clock64() : 0ull;

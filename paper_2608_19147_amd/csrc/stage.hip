@@ -686,7 +686,7 @@ int stage_create(const StageConfig* cfg, const LayerWeights* layers, int weights
         if (slots <= 0 || ps_layout(probe, slots, D, Hq / Hkv) > 160 * 1024) st->ps_ok = false;
         // flag-word buffers start with flag number 0, which no exchange uses
         const size_t max_split = (size_t)std::max(1, std::min(nwg / Hkv, (Hq / Hkv) * D / 8));
-        const size_t n_part = (size_t)Hkv * max_split * (Hq / Hkv) * (D + 2);
+        const size_t n_part = (size_t)Hkv * max_split * (Hq / Hkv) * ps_part_words(D);
         const size_t x_words = (size_t)H + 2 * (size_t)((nwg + 1) & ~1);   // 4-byte words
         if ((rc = st->alloc(&st->ll_qkv, nqkv)) || (rc = st->alloc(&st->ll_o, (size_t)Hq * D / 2)) ||
             (rc = st->alloc(&st->ll_part, n_part)) || (rc = st->alloc(&st->ll_x, x_words)) ||
