@@ -339,11 +339,19 @@ struct Ring {
 // Rows are consumed whole, four at a time (one wave-wide reduction per four
 // rows), from two register sets used alternately: while row r computes from
 // one set, the codes and scales of row r + 1 are read into the other.
+template <int S, class Issue>
+__device__ __forceinline__ void gemv_seg1(const PsArgs& a, Issue& issue, Ring& rg, int nrows, int rlocal, int ng,
+                                          uint32_t sb, uint32_t xs, uint32_t res);
+
 template <int CPL, int S, class Issue>
 __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg, int nrows, int rlocal, int ng,
                                          uint32_t sb, uint32_t xs, uint32_t res) {
     static_assert(S >= 2 * CPL, "the ring must hold two rows");
     static_assert(CPL <= 4, "the input slice is kept in registers");
+    if constexpr (CPL == 1) {
+        gemv_seg1<S>(a, issue, rg, nrows, rlocal, ng, sb, xs, res);
+        return;
+    }
     if (nrows == 0) return;
     const int lane = threadIdx.x & 63;
     const half2_t one2 = {(_Float16)1.0f, (_Float16)1.0f};
@@ -463,6 +471,125 @@ __device__ __forceinline__ void gemv_seg(const PsArgs& a, Issue& issue, Ring& rg
         if (nt > 1) a1 = row(r + 1, w1, c1, w0, c0);
         if (nt > 2) a2 = row(r + 2, w0, c0, w1, c1);
         const float rs = sum4_rows(a0, a1, a2, 0.f, lane);
+        if (lane < nt) lds_wr4(res + 4 * (rlocal + r + lane), rs);
+    }
+}
+
+// The one-chunk form of gemv_seg (rows of K = 2048, one slot each): every row
+// multiplies the same input chunk, so rows go two at a time; a step holds the
+// arithmetic of two slots, which covers the LDS reads of the next step's two
+// slots and scales (one slot of arithmetic does not).
+template <int S, class Issue>
+__device__ __forceinline__ void gemv_seg1(const PsArgs& a, Issue& issue, Ring& rg, int nrows, int rlocal, int ng,
+                                          uint32_t sb, uint32_t xs, uint32_t res) {
+    static_assert(S >= 4, "the ring must hold two steps");
+    if (nrows == 0) return;
+    const int lane = threadIdx.x & 63;
+    const half2_t one2 = {(_Float16)1.0f, (_Float16)1.0f};
+    const half2_t sixteenth2 = {(_Float16)0.0625f, (_Float16)0.0625f};
+    u32x4 xq[4];
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) xq[q4] = lds_rd16(xs + 64 * lane + 16 * q4);
+    lgkm_wait_all();
+    float ncorr;
+    {
+        float slo = 0.f, shi = 0.f;
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+            touch(xq[q4]);
+            const uint32_t e0 = xq[q4][0], e1 = xq[q4][1], e2 = xq[q4][2], e3 = xq[q4][3];
+            slo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e0), one2, slo, false);
+            slo = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e2), one2, slo, false);
+            shi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e1), one2, shi, false);
+            shi = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, e3), one2, shi, false);
+            const half2_t h1 = __builtin_bit_cast(half2_t, e1) * sixteenth2;
+            const half2_t h3 = __builtin_bit_cast(half2_t, e3) * sixteenth2;
+            xq[q4] = u32x4{e0, __builtin_bit_cast(uint32_t, h1), e2, __builtin_bit_cast(uint32_t, h3)};
+        }
+        ncorr = -(1032.0f * slo + 72.0f * shi);
+        asm volatile("" : "+v"(ncorr));
+    }
+    const uint32_t sl = sb + 2 * (uint32_t)(lane / a.gchunks) + 2 * rlocal * ng;
+    const uint32_t lane16 = 16 * lane;
+    uint32_t magic = 0x64006400u;
+    asm volatile("" : "+v"(magic));
+
+    u32x4 w0[2], w1[2];
+    uint32_t c0[2], c1[2];
+    // rows r, r + 1 (a row past the segment reads the next ring slot and the
+    // segment's last scale: valid LDS addresses, not used)
+    auto read_pair = [&](int r, u32x4 (&w)[2], uint32_t (&sc)[2]) {
+        const int r1 = Ring::next(rg.ri, S);
+        w[0] = lds_rd16(rg.addr(rg.ri) + lane16);
+        w[1] = lds_rd16(rg.addr(r1) + lane16);
+        sc[0] = lds_rdu16(sl + 2 * min(r, nrows - 1) * ng);
+        sc[1] = lds_rdu16(sl + 2 * min(r + 1, nrows - 1) * ng);
+    };
+    auto dot = [&](const u32x4& cw, uint32_t cs) -> float {
+        float t0 = ncorr, t1 = 0.f;
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+            const uint32_t x = cw[q4];
+            const uint32_t y = x >> 8;
+            const uint32_t p0 = bfi(0x000F000Fu, x, magic);
+            const uint32_t p1 = bfi(0x00F000F0u, x, magic);
+            const uint32_t p2 = bfi(0x000F000Fu, y, magic);
+            const uint32_t p3 = bfi(0x00F000F0u, y, magic);
+            const uint32_t x0 = xq[q4][0], x1 = xq[q4][1], x2 = xq[q4][2], x3 = xq[q4][3];
+            t0 = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p0), __builtin_bit_cast(half2_t, x0), t0, false);
+            t1 = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p1), __builtin_bit_cast(half2_t, x1), t1, false);
+            t0 = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p2), __builtin_bit_cast(half2_t, x2), t0, false);
+            t1 = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, p3), __builtin_bit_cast(half2_t, x3), t1, false);
+        }
+        return f16_to_f32((uint16_t)cs) * (t0 + t1);
+    };
+    // Rows r, r + 1 (only r when it is the last) from (cw, cs): their slots are
+    // refilled, the next step is read into (nw, ns), and the rows' per-lane
+    // partials are returned once those reads are done.
+    auto step = [&](int r, const u32x4 (&cw)[2], const uint32_t (&cs)[2], u32x4 (&nw)[2], uint32_t (&ns)[2],
+                    float& p0, float& p1) {
+        const bool two = r + 1 < nrows;                     // wave-uniform
+        issue(rg.addr(rg.ri));
+        rg.ri = Ring::next(rg.ri, S);
+        if (two) {
+            issue(rg.addr(rg.ri));
+            rg.ri = Ring::next(rg.ri, S);
+        }
+        rg.p += two ? 2 : 1;
+        if (r + 2 < nrows) {
+            // the next step's two positions: S - 2 younger loads while the stream is not near its end
+            if (rg.p + 1 <= rg.pmax) vm_wait<S - 2>(); else vm_wait_all();
+        }
+        read_pair(r + 2, nw, ns);
+        p0 = dot(cw[0], cs[0]);
+        p1 = two ? dot(cw[1], cs[1]) : 0.f;
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(p0), "+v"(p1)::"memory");
+        touch(nw[0]);
+        touch(nw[1]);
+        touch(ns[0]);
+        touch(ns[1]);
+    };
+    if (rg.p + 1 <= rg.pmax) vm_wait<S - 2>(); else vm_wait_all();
+    read_pair(0, w0, c0);
+    lgkm_wait_all();
+    touch(w0[0]);
+    touch(w0[1]);
+    touch(c0[0]);
+    touch(c0[1]);
+    int r = 0;
+    for (; r + 4 <= nrows; r += 4) {
+        float a0, a1, a2, a3;
+        step(r, w0, c0, w1, c1, a0, a1);
+        step(r + 2, w1, c1, w0, c0, a2, a3);
+        const float rs = sum4_rows(a0, a1, a2, a3, lane);
+        if (lane < 4) lds_wr4(res + 4 * (rlocal + r + lane), rs);
+    }
+    if (r < nrows) {                                        // one to three rows left
+        const int nt = nrows - r;
+        float a0, a1, a2 = 0.f, a3 = 0.f;
+        step(r, w0, c0, w1, c1, a0, a1);
+        if (nt > 2) step(r + 2, w1, c1, w0, c0, a2, a3);
+        const float rs = sum4_rows(a0, a1, a2, a3, lane);
         if (lane < nt) lds_wr4(res + 4 * (rlocal + r + lane), rs);
     }
 }
