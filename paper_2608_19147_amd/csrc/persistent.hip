@@ -1648,9 +1648,15 @@ __device__ __forceinline__ void merge_slices(const PsArgs& a, int g, int split, 
     }
 }
 
+// The layer table, read through the constant address space: it is not written
+// during the launch, so its (uniform) reads are scalar loads, which do not wait
+// behind this wave's outstanding global stores and direct-to-LDS loads.
+typedef const __attribute__((address_space(4))) PsLayer CPsLayer;
+
 template <int CPL_H, int CPL_Q, int CPL_F, int D, int GS, int S, bool KVB, bool REC>
 __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     const int lane = threadIdx.x & 63;
+    CPsLayer* lays = (CPsLayer*)a.layers;
     const int w = blockIdx.x;
     const uint32_t lb = lds_addr(smem);
     uint8_t* xs = smem + a.l_xs;
@@ -1685,13 +1691,13 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     float xrow = 0.f;
     if (lane < nxr) xrow = half_bits_to_f32(((const uint16_t*)a.hidden_in)[xr0 + lane], a.act_dt);
     if (lane < D / 2) ((float2*)rope)[lane] = a.rope[(size_t)pos * (D / 2) + lane];
-    load_scales(a.layers[0].qkv.s, w * a.rpw_qkv, max(0, min(a.NQKV, (w + 1) * a.rpw_qkv) - w * a.rpw_qkv), a.ng_h,
+    load_scales(lays[0].qkv.s, w * a.rpw_qkv, max(0, min(a.NQKV, (w + 1) * a.rpw_qkv) - w * a.rpw_qkv), a.ng_h,
                 lb + a.l_sb0);
     vm_wait_all();
     // c: scale of the last published residual (the last RMSNorm scale); mq, mg: the
     // factors rs / c applied to the q|k|v and gate|up results.  The first
     // normalization reads the stage input and its RMSNorm weights from memory.
-    float c = stage_norm<NT_H>(a.hidden_in, a.act_dt, a.H, a.kc_h * 32, (const uint8_t*)a.layers[0].attn_norm, a.act_dt,
+    float c = stage_norm<NT_H>(a.hidden_in, a.act_dt, a.H, a.kc_h * 32, (const uint8_t*)lays[0].attn_norm, a.act_dt,
                                a.eps, xs);
     float mq = 1.f, mg = 1.f;
     bool ok = true;
@@ -1699,7 +1705,7 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
     wg_barrier();                                             // q|k|v input staged
 
     for (int l = 0; l < a.n_layers; ++l) {
-        const PsLayer& Ly = a.layers[l];
+        const CPsLayer& Ly = lays[l];
         const bool last = (l == a.n_layers - 1);
         // flag numbers of this layer's exchanges
         const uint32_t f_qkv = a.ll_epoch + PS_LL_PER_LAYER * l + 1, f_part = f_qkv + 1, f_o = f_qkv + 2,
@@ -1710,7 +1716,7 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         float gam_f = 0.f, gam_a = 0.f;
         if (lane < nxr) {
             gam_f = half_bits_to_f32(Ly.ffn_norm[xr0 + lane], a.act_dt);
-            if (!last) gam_a = half_bits_to_f32(a.layers[l + 1].attn_norm[xr0 + lane], a.act_dt);
+            if (!last) gam_a = half_bits_to_f32(lays[l + 1].attn_norm[xr0 + lane], a.act_dt);
         }
         if (l > 0) {
             // rs of the residual published after the previous layer's down product,
@@ -1996,7 +2002,7 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
         zero_pad(a.F, a.kc_f * 32, xs);                       // the compute waves stage the SwiGLU output
         wg_barrier();                                         // SwiGLU output staged
         if (!last) {
-            const PsLayer& Ln = a.layers[l + 1];
+            const CPsLayer& Ln = lays[l + 1];
             load_scales(Ln.qkv.s, w * a.rpw_qkv, max(0, min(a.NQKV, (w + 1) * a.rpw_qkv) - w * a.rpw_qkv), a.ng_h,
                         lb + a.l_sb0);
         }
