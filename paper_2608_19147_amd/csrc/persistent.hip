@@ -1116,19 +1116,22 @@ __device__ __forceinline__ void att_seg_m(Issue& issue, Ring& rg, int T, uint64_
             // V operand of block b4: pair b4's V slot.  Pairs past the chunk read the
             // chunk's last pair and are zeroed below (ring slots of other data may hold
             // any bits, and a zero weight times a NaN is a NaN).
+            // (chunk c of key j sits at chunk c ^ (j mod 16) of its row)
             const int tk = i16 >> 2;
             int rk = rg.ri + 2 * min(tk, tc - 1);
             int rv = rg.ri + 2 * min(b4, tc - 1) + 1;
             rk -= rk >= S ? S : 0;
             rv -= rv >= S ? S : 0;
-            const uint32_t ka = rg.addr(rk) + (uint32_t)(i16 & 3) * RB + 16u * (uint32_t)b4;
-            const uint32_t va = rg.addr(rv) + (uint32_t)(i16 >> 2) * RB + 8u * (uint32_t)(i16 & 3);
+            const int swk = (j0 + 4 * (t0 + tk) + (i16 & 3)) & 15;   // key of this lane's K row
+            const int swv = (j0 + 4 * (t0 + b4) + (i16 >> 2)) & 15;  // key of this lane's V read row
+            const uint32_t ka = rg.addr(rk) + (uint32_t)(i16 & 3) * RB;
+            const uint32_t va = rg.addr(rv) + (uint32_t)(i16 >> 2) * RB + 8u * (uint32_t)(i16 & 1);
             u32x4 kw[KB];
             u32x2 vf[DB];
 #pragma unroll
-            for (int kb = 0; kb < KB; ++kb) kw[kb] = lds_rd16(ka + 64u * kb);
+            for (int kb = 0; kb < KB; ++kb) kw[kb] = lds_rd16(ka + 16u * (uint32_t)((b4 + 4 * kb) ^ swk));
 #pragma unroll
-            for (int d = 0; d < DB; ++d) vf[d] = lds_rd8_tr(va + 32u * d);
+            for (int d = 0; d < DB; ++d) vf[d] = lds_rd8_tr(va + 16u * (uint32_t)((2 * d + ((i16 & 3) >> 1)) ^ swv));
             lgkm_wait_all();
             const bool kval = tk < tc, vval = b4 < tc;
 #pragma unroll
@@ -1148,12 +1151,13 @@ __device__ __forceinline__ void att_seg_m(Issue& issue, Ring& rg, int T, uint64_
             }
             rg.p += 2 * tc;
             // scores of rows 4 b4 + j for head i16
-            f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+            f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f}, sr = sc;       // two independent chains: qh and qr terms
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb) {
                 sc = mma_k32<BF16>(kw[kb], qh[kb], sc);
-                sc = mma_k32<BF16>(kw[kb], qr[kb], sc);
+                sr = mma_k32<BF16>(kw[kb], qr[kb], sr);
             }
+            sc += sr;
             const int sh = 4 * (t0 + b4);
             const uint32_t vis4 = sh < 64 ? (uint32_t)(mall >> sh) & 0xFu : 0u;
             float sv[4];
@@ -1250,7 +1254,11 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
             const int jj = valid ? j : 0;
             const int phys = valid ? (int)tab[jj] : b;
             if (valid && mask[jj] != 0) mbits |= 1u << t;
-            aoff[t] = (uint32_t)(((((u64)phys * a.Hkv + g) * rq.cap + jj) * D + 8 * (lane % LPR)) * 2);
+            // the matrix-core attention keeps row j's 16-byte chunk c at chunk c ^ (j mod 16)
+            // of its LDS row (no two of a chunk's 16 rows on the same banks): this lane
+            // loads the chunk that lands at its position
+            const int ck = ATT_MMA ? ((lane % LPR) ^ (j & 15)) : lane % LPR;
+            aoff[t] = (uint32_t)(((((u64)phys * a.Hkv + g) * rq.cap + jj) * D + 8 * ck) * 2);
             if constexpr (ATT_MMA || (GS == RPS && RPS * SK_TMAX <= 64)) {
 #pragma unroll
                 for (int r = 0; r < RPS; ++r) {
