@@ -885,134 +885,6 @@ __device__ __forceinline__ void att_seg_t(Issue& issue, Ring& rg, int T, uint32_
     }
 }
 
-// Up to two cache-row slot pairs for the head-per-group form: every lane reads,
-// for each of the RPS rows of a slot, the 16 bytes of its own dimensions (one
-// wait for the ring, one for LDS), then the pairs' refills are issued.  While
-// the stream is not near its end, S - 2 tc younger ring positions stay in flight.
-template <int S, int D>
-__device__ __forceinline__ void att_read_rows(Ring& rg, int tc, u32x4 (&kw)[2][AttGeo<D>::RPS],
-                                              u32x4 (&vw)[2][AttGeo<D>::RPS]) {
-    constexpr int LPR = AttGeo<D>::LPR, RPS = AttGeo<D>::RPS;
-    static_assert(S >= 4, "two pairs must fit the ring");
-    const uint32_t lo = 16u * (uint32_t)((threadIdx.x & 63) % LPR);   // this lane's dimensions within a row
-    if (rg.p > rg.pmax) vm_wait_all();
-    else if (tc == 2) vm_wait<S - 4>();
-    else vm_wait<S - 2>();
-    int ri = rg.ri;
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        const int rk = ri, rv = Ring::next(ri, S);
-#pragma unroll
-        for (int r = 0; r < RPS; ++r) {
-            kw[t][r] = t < tc ? lds_rd16(rg.addr(rk) + (uint32_t)(r * 2 * D) + lo) : u32x4{0u, 0u, 0u, 0u};
-            vw[t][r] = t < tc ? lds_rd16(rg.addr(rv) + (uint32_t)(r * 2 * D) + lo) : u32x4{0u, 0u, 0u, 0u};
-        }
-        ri = Ring::next(rv, S);
-    }
-    lgkm_wait_all();
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int r = 0; r < RPS; ++r) {
-            touch(kw[t][r]);
-            touch(vw[t][r]);
-        }
-}
-
-// The head-per-group form of att_seg_t, for GS == RPS: row group h of the wave
-// (LPR lanes) takes query head h over every row of the wave's slot pairs, each
-// lane its 8 dimensions; the scores of a pair's RPS rows are lane reductions
-// within the group.  A head's running (max, sum, output) never leaves its
-// group, so no merge across the wave's groups is needed at the end.
-// mall: bit RPS t + r set when row r of slot pair t is visible.
-template <int GS, int D, int S, bool BF16, bool REC, class Issue>
-__device__ __forceinline__ void att_seg_h(Issue& issue, Ring& rg, int T, uint64_t mall, uint32_t qlds, uint32_t part,
-                                          float* rec, int keys, int j0) {
-    constexpr int LPR = AttGeo<D>::LPR, RPS = AttGeo<D>::RPS;
-    static_assert(GS == RPS && RPS * SK_TMAX <= 64, "one query head per row group, one mask bit per row");
-    const int lane = threadIdx.x & 63;
-    const int li = lane % LPR, h = lane / LPR;
-    float m = -INFINITY, l = 0.f, o[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = 0.f;
-    if (T > 0) {
-        u32x4 qv[2];
-#pragma unroll
-        for (int k = 0; k < 2; ++k) qv[k] = lds_rd16(qlds + 4 * (h * D + 8 * li + 4 * k));
-        lgkm_wait_all();
-        float qf[8];
-#pragma unroll
-        for (int k = 0; k < 2; ++k) {
-            touch(qv[k]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t qe = qv[k][e];            // a scalar copy: bit_cast of a vector element reads element 0
-                qf[4 * k + e] = __builtin_bit_cast(float, qe);
-            }
-        }
-        for (int t0 = 0; t0 < T; t0 += 2) {
-            const int tc = min(2, T - t0);
-            u32x4 kw[2][RPS], vw[2][RPS];
-            att_read_rows<S, D>(rg, tc, kw, vw);
-#pragma unroll
-            for (int t = 0; t < 2 * tc; ++t) {
-                issue(rg.addr(rg.ri));
-                rg.ri = Ring::next(rg.ri, S);
-            }
-            rg.p += 2 * tc;
-            float sc[2][RPS];
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int r = 0; r < RPS; ++r) {
-                    float kf[8];
-                    kv_to_f32<BF16>(kw[t][r], kf);
-                    float sd = 0.f;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) sd = __builtin_fmaf(qf[e], kf[e], sd);
-                    sd = group_sum<LPR>(sd);
-                    const bool vis = t < tc && ((mall >> (RPS * (t0 + t) + r)) & 1ull);
-                    sc[t][r] = vis ? sd : -INFINITY;
-                    if constexpr (REC) {
-                        const int j = j0 + (t0 + t) * RPS + r;
-                        if (rec && vis && li == 0 && j < keys) rec[h * keys + j] = sd * 0.69314718055994531f;
-                    }
-                }
-            float mn = m;
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int r = 0; r < RPS; ++r) mn = fmaxf(mn, sc[t][r]);
-            const float mref = (mn == -INFINITY) ? 0.f : mn;    // no visible row yet: nothing changes
-            const float corr = exp2_raw(m - mref);
-            float p[2][RPS], ls = 0.f;
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int r = 0; r < RPS; ++r) {
-                    p[t][r] = exp2_raw(sc[t][r] - mref);
-                    ls += p[t][r];
-                }
-            l = __builtin_fmaf(l, corr, ls);
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int r = 0; r < RPS; ++r) {
-                    float vf[8];
-                    kv_to_f32<BF16>(vw[t][r], vf);
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) o[e] = __builtin_fmaf(p[t][r], vf[e], (t == 0 && r == 0) ? o[e] * corr : o[e]);
-                }
-            m = mn;
-        }
-    }
-    const int cw = threadIdx.x >> 6;
-    const uint32_t base = part + 4 * ((cw * GS + h) * (D + 4));
-    lds_wr16(base + 16 + 32 * li, f32x4{o[0], o[1], o[2], o[3]});
-    lds_wr16(base + 32 + 32 * li, f32x4{o[4], o[5], o[6], o[7]});
-    if (li == 0) lds_wr16(base, f32x4{m, l, 0.f, 0.f});
-}
-
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
@@ -1242,7 +1114,7 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
     const uint8_t* vbase = (const uint8_t*)rq.vc;
     uint32_t mbits = 0u;
     constexpr bool ATT_MMA = ps_att_mma(D, GS) && RPS * SK_TMAX <= 64;
-    uint64_t mall = 0u;           // head-per-group and matrix-core forms: every row r of slot pair t, at bit RPS t + r
+    uint64_t mall = 0u;           // matrix-core form: every row r of slot pair t, at bit RPS t + r
     uint32_t aoff[SK_TMAX];       // per-lane byte offset of cache-row slot pair t within one layer
     {
         const uint8_t* mask = a.meta.masks + rq.mask_off + (size_t)b * rq.mask_len;
@@ -1259,7 +1131,7 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
             // loads the chunk that lands at its position
             const int ck = ATT_MMA ? ((lane % LPR) ^ (j & 15)) : lane % LPR;
             aoff[t] = (uint32_t)(((((u64)phys * a.Hkv + g) * rq.cap + jj) * D + 8 * ck) * 2);
-            if constexpr (ATT_MMA || (GS == RPS && RPS * SK_TMAX <= 64)) {
+            if constexpr (ATT_MMA) {
 #pragma unroll
                 for (int r = 0; r < RPS; ++r) {
                     const int jr = j0 + t * RPS + r;
@@ -1363,8 +1235,6 @@ __device__ __forceinline__ void compute_main(const PsArgs& a, uint32_t lb) {
             if (l == a.dbg_layer && has_att) rec = a.dbg_logits + (size_t)g * GS * a.dbg_keys;
         if constexpr (ATT_MMA)
             att_seg_m<GS, D, S, KVB, REC>(issue, rg, T, mall, lb + a.l_qb, lb + a.l_part, rec, a.dbg_keys, j0);
-        else if constexpr (GS == RPS && RPS * SK_TMAX <= 64)
-            att_seg_h<GS, D, S, KVB, REC>(issue, rg, T, mall, lb + a.l_q, lb + a.l_part, rec, a.dbg_keys, j0);
         else
             att_seg_t<GS, D, S, KVB, REC>(issue, rg, T, mbits, lb + a.l_q, lb + a.l_part, rec, a.dbg_keys, j0);
         cstamp(a, lb + a.l_dbg, 1);
