@@ -46,6 +46,30 @@ def test_8b_two_layer_decode_kv2048_persistent():
     assert rel_err(out, ref) <= TOL_STAGE
 
 
+def test_8b_decode_long_kv_persistent():
+    """Single launch from KV 12000 with 10% masked holes (splits of 375 rows:
+    four 16-row chunks per wave in the matrix-core attention, the last one
+    partial) vs the oracle; the forward is one stream-kernel launch."""
+    shape = synth.with_layers(synth.LLAMA8B_HALF, 2)
+    p = _pair(shape, 52, cache_weights=False)
+    P = 12000
+    g, o = p.states(1, P, P + 4, seed=52)
+    holes = synth.hole_mask(P, 0.1, 52, 0)
+    holes[-1] = 1
+    mask = np.concatenate([holes, np.ones(1, np.uint8)])[None]
+    pos = np.array([[int(holes.sum())]])
+    x = synth.make_hidden(shape, 1, 52)
+    p.gpu.profile("persistent")
+    out = run_gpu(p, [req(g, pos, mask, [0])], x)
+    launches, _ = p.gpu.profile_read()
+    p.gpu.profile(None)
+    assert launches == 1
+    ref = oracle.forward(p.orc, o, host(x), pos, np.array([0]), mask)
+    err = rel_err(out, ref)
+    print(f"8B 2 layers, KV {P} with holes, single launch vs oracle: {err:.2e}")
+    assert err <= TOL_STAGE
+
+
 def _layer0_new_kv(shape, layer, x, position):
     """Oracle k and v rows (stored form: k rotated, both rounded to the KV dtype)
     that layer 0 appends for one input row."""

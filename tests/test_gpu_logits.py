@@ -167,17 +167,27 @@ def test_8b_stream_kernel_logits_decode_kv2048():
     (its query depends on layer 0's output) and layer 0's (query also against
     the oracle) within the bar; an armed forward's output is bitwise the
     unarmed one's; the launch is the single launch."""
+    _stream_logits(2048, 75)
+
+
+def test_8b_stream_kernel_logits_decode_kv12000():
+    """As above from KV 12000: splits of 375 rows, so each wave's matrix-core
+    attention takes four 16-row chunks (the last one partial) and rescales its
+    running maximum between them."""
+    _stream_logits(12000, 76)
+
+
+def _stream_logits(P, seed):
     shape = synth.with_layers(synth.LLAMA8B_HALF, 2)
-    p = Pair(shape, 75)
-    P = 2048
-    holes = synth.hole_mask(P, 0.1, 75, 0)
+    p = Pair(shape, seed)
+    holes = synth.hole_mask(P, 0.1, seed, 0)
     holes[-1] = 1
     mask = np.concatenate([holes, np.ones(1, np.uint8)])[None]
     pos = np.array([[int(holes.sum())]])
-    x = synth.make_hidden(shape, 1, 75)
+    x = synth.make_hidden(shape, 1, seed)
     outs = []
     for layer in (1, 0, -1):
-        g, _ = p.states(1, P, P + 4, seed=75, with_oracle=False)
+        g, _ = p.states(1, P, P + 4, seed=seed, with_oracle=False)
         p.gpu.profile("persistent")
         if layer >= 0:
             p.gpu.debug_attn_arm(layer, P + 1)
