@@ -2260,13 +2260,13 @@ __global__ __launch_bounds__(256, QTW == 1 ? 2 : 1) void attn_dma_kernel(AttnArg
             const int i = r / gs, h = g * gs + (r % gs);
             const int m = rowbase + i;
             float* pp = a.part + (((size_t)m * Hq + h) * a.nsplit_max + split) * (D + 2);
+            // 16-byte stores (the record is only 8-byte aligned; the hardware takes
+            // 4-byte aligned wide stores): a store per value lengthens the launch's drain
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-                for (int jj = 0; jj < 4; ++jj) pp[2 + 16 * mb + 4 * lg + jj] = o[u][mb][jj];
+            for (int mb = 0; mb < MB; ++mb) __builtin_memcpy(pp + 2 + 16 * mb + 4 * lg, &o[u][mb], 16);
             if (lg == 0) {
-                pp[0] = mrun[u];
-                pp[1] = lt;
+                const float2 ml = {mrun[u], lt};
+                __builtin_memcpy(pp, &ml, 8);
             }
         }
     }
