@@ -187,6 +187,11 @@ constexpr int PS_TRACE_PER_LAYER = 40;   // 10 control-wave boundaries, 6 from c
                                          // counts, 6 exchange end times, 3 first-pass times, partial published,
                                          // 6 first-pass issue times, 2 spare
 
+// Values per head in the stream kernel's LDS copy of the query terms: D plus
+// 32 of padding, so the four heads a 16-byte read meets start 64 bytes apart
+// in the LDS banks.
+constexpr int ps_qb_stride(int D) { return D + 32; }
+
 // Flag words of one split's partial of one query head: max, sum, D / 2 pairs.
 constexpr int ps_part_words(int D) { return 2 + D / 2; }
 
@@ -219,7 +224,7 @@ inline int ps_layout(PsArgs& a, int slots, int D, int gs) {
     // input) and the staging of the o input, so they share the staged-input
     // region when they fit
     const int part_b = up(SK_CW * gs * (D + 4) * 4, 16);
-    const int qb_b = ps_att_mma(D, gs) ? 2 * gs * D * 2 : 0;
+    const int qb_b = ps_att_mma(D, gs) ? 2 * gs * ps_qb_stride(D) * 2 : 0;
     if (part_b + qb_b <= kcmax * 64) {
         a.l_part = a.l_xs;
         a.l_qb = a.l_xs + part_b;

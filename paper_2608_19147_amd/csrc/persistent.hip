@@ -940,8 +940,8 @@ __device__ __forceinline__ uint32_t kv_pair(float lo, float hi) {
 // LDS read.  Running (max, sum) per head are kept per lane and combined over
 // the four blocks at the end; the output accumulators hold head 4 (l / 16) + j
 // in register j, so heads < 4 sit in lanes 0..15.
-// qlds: the queries' two terms as written by the control wave (GS D values qh,
-// then GS D values qr, head-major).  mall: bit 4 t + r set when row r of slot
+// qlds: the queries' two terms as written by the control wave (GS heads of qh,
+// then GS heads of qr, each head ps_qb_stride(D) values).  mall: bit 4 t + r set when row r of slot
 // pair t is visible.
 template <int GS, int D, int S, bool BF16, bool REC, class Issue>
 __device__ __forceinline__ void att_seg_m(Issue& issue, Ring& rg, int T, uint64_t mall, uint32_t qlds, uint32_t part,
@@ -960,11 +960,12 @@ __device__ __forceinline__ void att_seg_m(Issue& issue, Ring& rg, int T, uint64_
         // query operand: head i16 (zero for heads >= GS), dims 8 b4 + 32 kb .. + 7
         u32x4 qh[KB], qr[KB];
         {
-            const uint32_t qa = qlds + 2u * (uint32_t)((i16 < GS ? i16 : 0) * D + 8 * b4);
+            constexpr int QS = ps_qb_stride(D);
+            const uint32_t qa = qlds + 2u * (uint32_t)((i16 < GS ? i16 : 0) * QS + 8 * b4);
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb) {
                 qh[kb] = lds_rd16(qa + 64u * kb);
-                qr[kb] = lds_rd16(qa + (uint32_t)(GS * D * 2) + 64u * kb);
+                qr[kb] = lds_rd16(qa + (uint32_t)(GS * QS * 2) + 64u * kb);
             }
             lgkm_wait_all();
 #pragma unroll
@@ -1660,8 +1661,11 @@ __device__ __forceinline__ void control_main(const PsArgs& a, uint8_t* smem) {
                         const uint32_t hi = kv_pair<KVB>(y0, y1);
                         const float r0 = y0 - kv_value<KVB>((uint16_t)(hi & 0xFFFFu));
                         const float r1 = y1 - kv_value<KVB>((uint16_t)(hi >> 16));
-                        qhb[lane + 64 * i] = hi;
-                        qhb[GS * D / 2 + lane + 64 * i] = kv_pair<KVB>(r0, r1);
+                        constexpr int QS = ps_qb_stride(D);          // values per head in LDS
+                        const int vi = 2 * (lane + 64 * i);          // first value of the pair
+                        const int wo = (vi / D) * (QS / 2) + (vi % D) / 2;
+                        qhb[wo] = hi;
+                        qhb[GS * QS / 2 + wo] = kv_pair<KVB>(r0, r1);
                     }
                 } else {
                     kv[i - NQP] = pc;
