@@ -63,18 +63,19 @@ HBM_PEAK_GBPS = 8000.0
 # HBM bytes per launch of the single-launch forward at the headline workload
 # (KV 2048), from one FETCH_SIZE and one WRITE_SIZE counter run scaled by what
 # the same counters read for a plain 1 GiB device copy (x2.0 and x1.0).  Keyed
-# by a digest of the sources that define the kernel and its launch: after any
-# change to them the figure no longer applies and ``traffic`` is null.
+# by a digest of the sources and build flags that define the kernel and its
+# launch: after any change to them the figure no longer applies and ``traffic``
+# is null.
 MEASURED_TRAFFIC = {("862573a4e3b21f36", 2048): 2_026_655_886}
-KERNEL_SOURCES = ("persistent.hip", "common.h", "device.h", "stage.hip")
+KERNEL_SOURCES = ("csrc/persistent.hip", "csrc/common.h", "csrc/device.h", "csrc/stage.hip", "build.py")
 
 
 def kernel_digest() -> str:
     import hashlib
 
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2608_19147_amd", "csrc", name), "rb") as f:
+    for name in KERNEL_SOURCES:                          # the sources and the compiler flags
+        with open(os.path.join(ROOT, "paper_2608_19147_amd", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
