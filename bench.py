@@ -66,7 +66,7 @@ HBM_PEAK_GBPS = 8000.0
 # by a digest of the sources and build flags that define the kernel and its
 # launch: after any change to them the figure no longer applies and ``traffic``
 # is null.
-MEASURED_TRAFFIC = {("862573a4e3b21f36", 2048): 2_026_655_886}
+MEASURED_TRAFFIC = {("d5ac1b9e5a58db0e", 2048): 2_027_096_834}
 KERNEL_SOURCES = ("csrc/persistent.hip", "csrc/common.h", "csrc/device.h", "csrc/stage.hip", "build.py")
 
 
